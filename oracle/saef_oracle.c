@@ -1,0 +1,267 @@
+/*
+ * CPU oracle for the SAEF round -- TEST INFRASTRUCTURE ONLY (see saef_oracle.h).
+ *
+ * What it follows:
+ *   - Eq. (2): C(v) = (||v||_1 / d) sign(v), applied layer-wise, i.e. one
+ *     scale per parameter tensor (Experiments: "all compression are performed
+ *     in a layer-wise way"), so d becomes the tensor size n_l.
+ *   - Algorithm 1, SAEF branch, with momentum constant mu = 0 (SAEF-SGD):
+ *       every p iterations the local errors are replaced by their mean,
+ *       x_{t+1/2} = x_t - e_t            (step ahead)
+ *       m = grad                         (mu = 0)
+ *       Delta^(k) = e^(k) + x_{t+1/2} - (x_{t+1/2} - eta m) = e^(k) + eta m
+ *       e^(k) <- Delta^(k) - C(Delta^(k))
+ *       server: Delta = e + (1/K) sum_k C(Delta^(k));  e <- Delta - C(Delta)
+ *       re-update: x <- x - C(Delta)
+ *   - Single-way compression (Experiments, method notation): the server sends
+ *     its average back uncompressed and keeps no error.
+ *
+ * Readings where the paper is silent (each one is a fixed rule here):
+ *   - sign(0) = +1 for +0 and -0, so ||C(v)||_1 = ||v||_1 always holds.
+ *   - ||v||_1 is summed exactly as the integer S = sum floor(|v_i| 2^80)
+ *     (requires |v_i| < 2^19 and n <= 2^28); the scale is
+ *     fp32( fp64( fp64(S) / n ) * 2^-80 ).
+ *   - eta * m + e is formed with one rounding (fused multiply-add).
+ *   - Means over the K workers are binary64 sums taken in worker order
+ *     0..K-1, divided by K in binary64, then rounded once to fp32.
+ *   - Delta = fp32(e_server + fp32(average)); every other fp32 result is the
+ *     correctly rounded fp32 operation of its two fp32 operands.
+ *
+ * Built with -O1 -ffp-contract=off and no fast-math so that every float
+ * expression below is exactly one IEEE operation.
+ */
+#include "saef_oracle.h"
+
+#include <math.h>
+#include <stddef.h>
+#include <string.h>
+
+typedef unsigned __int128 u128;
+
+/* |v| must stay below 2^19 for the 128-bit exact sum of up to 2^28 terms. */
+static const float kMaxAbs = 524288.0f; /* 2^19 */
+static const int64_t kMaxN = (int64_t)1 << 28;
+
+/* ---- layout checks ------------------------------------------------------ */
+
+static int check_layout(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad)
+{
+    if (L < 1 || off == NULL || n == NULL || d_pad < 1) return ORACLE_EINVAL;
+    for (int32_t l = 0; l < L; ++l) {
+        if (off[l] < 0 || off[l] % 64 != 0) return ORACLE_EINVAL;
+        if (n[l] < 1 || n[l] > kMaxN) return ORACLE_EINVAL;
+        if (off[l] + n[l] > d_pad) return ORACLE_EINVAL;
+    }
+    /* no two tensors may share an element (quadratic, fine for an oracle) */
+    for (int32_t a = 0; a < L; ++a)
+        for (int32_t b = a + 1; b < L; ++b)
+            if (off[a] < off[b] + n[b] && off[b] < off[a] + n[a]) return ORACLE_EINVAL;
+    return ORACLE_OK;
+}
+
+static int value_in_range(float v)
+{
+    /* NaN fails every comparison, so it is out of range too */
+    return fabsf(v) < kMaxAbs;
+}
+
+/* ---- Eq. (2): the scaled sign compressor on one tensor -------------------- */
+
+int oracle_l1_fixed(const float* v, int64_t n, uint64_t* s_hi, uint64_t* s_lo)
+{
+    u128 S = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        if (!value_in_range(v[i])) return ORACLE_ERANGE;
+        /* |v| * 2^80 is exact in binary64 (only the exponent changes); the
+         * conversion to an integer truncates, i.e. takes the floor. */
+        double scaled = ldexp((double)fabsf(v[i]), 80);
+        S += (u128)scaled;
+    }
+    *s_hi = (uint64_t)(S >> 64);
+    *s_lo = (uint64_t)S;
+    return ORACLE_OK;
+}
+
+float oracle_scale_from_sum(uint64_t s_hi, uint64_t s_lo, int64_t n)
+{
+    u128 S = ((u128)s_hi << 64) | (u128)s_lo;
+    double S64 = (double)S;             /* round to nearest even */
+    double mean = S64 / (double)n;       /* binary64 division */
+    return (float)ldexp(mean, -80);      /* exact scaling, then round to fp32 */
+}
+
+/* sign(v) as a bit: 1 for v >= 0 (both zeros included), 0 for v < 0. */
+static int sign_bit(float v)
+{
+    return v >= 0.0f ? 1 : 0;
+}
+
+/* One element of C(v) from the message (scale, sign bit). */
+static float message_value(float scale, int bit)
+{
+    return bit ? scale : -scale;
+}
+
+static int get_bit(const uint64_t* words, int64_t off, int64_t i)
+{
+    return (int)((words[off / 64 + i / 64] >> (i % 64)) & 1u);
+}
+
+/* Compress the n values v of one tensor: writes the message (scale and the
+ * ceil(n/64) sign words starting at words[off/64]) and the residual
+ * err = v - C(v) (Algorithm 1, local/server error update).  err may alias v. */
+static int compress_tensor(const float* v, int64_t n, int64_t off,
+                           float* scale_out, uint64_t* words, float* err)
+{
+    uint64_t hi, lo;
+    int rc = oracle_l1_fixed(v, n, &hi, &lo);
+    if (rc != ORACLE_OK) return rc;
+    float scale = oracle_scale_from_sum(hi, lo, n);
+
+    int64_t nwords = (n + 63) / 64;
+    for (int64_t j = 0; j < nwords; ++j) words[off / 64 + j] = 0;
+    for (int64_t i = 0; i < n; ++i)
+        if (sign_bit(v[i])) words[off / 64 + i / 64] |= (uint64_t)1 << (i % 64);
+
+    for (int64_t i = 0; i < n; ++i) {
+        int bit = get_bit(words, off, i);
+        err[i] = v[i] - message_value(scale, bit);
+    }
+    *scale_out = scale;
+    return ORACLE_OK;
+}
+
+/* ---- Algorithm 1: worker compression ------------------------------------ */
+
+int oracle_compress(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                    int32_t K, float lr, const float* g, float* e,
+                    uint64_t* signs, float* scales)
+{
+    int rc = check_layout(L, off, n, d_pad);
+    if (rc != ORACLE_OK) return rc;
+    if (K < 1 || g == NULL || e == NULL || signs == NULL || scales == NULL) return ORACLE_EINVAL;
+    int status = ORACLE_OK;
+    for (int32_t k = 0; k < K; ++k) {
+        const float* gk = g + (int64_t)k * d_pad;
+        float* ek = e + (int64_t)k * d_pad;
+        uint64_t* wk = signs + (int64_t)k * (d_pad / 64);
+        for (int32_t l = 0; l < L; ++l) {
+            /* Delta^(k) = e^(k) + eta * m^(k), m = grad (mu = 0) */
+            for (int64_t i = 0; i < n[l]; ++i) {
+                int64_t j = off[l] + i;
+                ek[j] = fmaf(lr, gk[j], ek[j]);
+            }
+            /* e^(k) <- Delta^(k) - C(Delta^(k)); message goes to the server */
+            rc = compress_tensor(ek + off[l], n[l], off[l], &scales[(int64_t)k * L + l],
+                                 wk, ek + off[l]);
+            if (rc != ORACLE_OK) status = rc;
+        }
+    }
+    return status;
+}
+
+/* ---- Algorithm 1: server aggregation and worker re-update --------------- */
+
+int oracle_aggregate(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                     int32_t K, int32_t mode, const uint64_t* signs, const float* scales,
+                     float* avg, float* e_srv, uint64_t* srv_signs, float* srv_scales,
+                     float* x)
+{
+    int rc = check_layout(L, off, n, d_pad);
+    if (rc != ORACLE_OK) return rc;
+    if (K < 1 || (mode != 0 && mode != 1) || signs == NULL || scales == NULL || x == NULL)
+        return ORACLE_EINVAL;
+    if (mode == 1 && (e_srv == NULL || srv_signs == NULL || srv_scales == NULL))
+        return ORACLE_EINVAL;
+    int status = ORACLE_OK;
+    for (int32_t l = 0; l < L; ++l) {
+        int64_t nl = n[l];
+        /* (1/K) sum_k C(Delta^(k)), decoded from the K messages */
+        for (int64_t i = 0; i < nl; ++i) {
+            double acc = 0.0;
+            for (int32_t k = 0; k < K; ++k) {
+                const uint64_t* wk = signs + (int64_t)k * (d_pad / 64);
+                acc += (double)message_value(scales[(int64_t)k * L + l], get_bit(wk, off[l], i));
+            }
+            float a = (float)(acc / (double)K);
+            if (avg != NULL) avg[off[l] + i] = a;
+            if (mode == 1) {
+                /* Delta = e + (1/K) sum_k C(Delta^(k)), held in e_srv until compressed */
+                e_srv[off[l] + i] = e_srv[off[l] + i] + a;
+            } else {
+                /* single-way: x <- x - (1/K) sum_k C(Delta^(k)) */
+                x[off[l] + i] = x[off[l] + i] - a;
+            }
+        }
+        if (mode == 1) {
+            /* e <- Delta - C(Delta); broadcast C(Delta); x <- x - C(Delta) */
+            rc = compress_tensor(e_srv + off[l], nl, off[l], &srv_scales[l], srv_signs,
+                                 e_srv + off[l]);
+            if (rc != ORACLE_OK) { status = rc; continue; }
+            for (int64_t i = 0; i < nl; ++i) {
+                int bit = get_bit(srv_signs, off[l], i);
+                x[off[l] + i] = x[off[l] + i] - message_value(srv_scales[l], bit);
+            }
+        }
+    }
+    return status;
+}
+
+/* ---- Algorithm 1: step ahead and error averaging ------------------------ */
+
+int oracle_step_ahead(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                      int32_t K, const float* x, const float* e, float* xh)
+{
+    int rc = check_layout(L, off, n, d_pad);
+    if (rc != ORACLE_OK) return rc;
+    if (K < 1 || x == NULL || e == NULL || xh == NULL) return ORACLE_EINVAL;
+    for (int32_t k = 0; k < K; ++k)
+        for (int32_t l = 0; l < L; ++l)
+            for (int64_t i = 0; i < n[l]; ++i) {
+                int64_t j = off[l] + i;
+                /* x^(k)_{t+1/2} = x^(k)_t - e^(k)_t */
+                xh[(int64_t)k * d_pad + j] = x[j] - e[(int64_t)k * d_pad + j];
+            }
+    return ORACLE_OK;
+}
+
+int oracle_error_average(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                         int32_t K, float* e)
+{
+    int rc = check_layout(L, off, n, d_pad);
+    if (rc != ORACLE_OK) return rc;
+    if (K < 1 || e == NULL) return ORACLE_EINVAL;
+    for (int32_t l = 0; l < L; ++l)
+        for (int64_t i = 0; i < n[l]; ++i) {
+            int64_t j = off[l] + i;
+            double acc = 0.0;
+            for (int32_t k = 0; k < K; ++k) acc += (double)e[(int64_t)k * d_pad + j];
+            float mean = (float)(acc / (double)K);
+            for (int32_t k = 0; k < K; ++k) e[(int64_t)k * d_pad + j] = mean;
+        }
+    return ORACLE_OK;
+}
+
+/* ---- one iteration of Algorithm 1 (SAEF branch, mu = 0) ----------------- */
+
+int oracle_round(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                 int64_t t, int64_t period, int32_t K, float lr, int32_t mode,
+                 const float* g, float* e, float* e_srv, float* x, float* xh,
+                 uint64_t* signs, float* scales, uint64_t* srv_signs, float* srv_scales)
+{
+    if (t < 0 || period < 0) return ORACLE_EINVAL;
+    int rc;
+    if (period > 0 && (t + 1) % period == 0) {
+        rc = oracle_error_average(L, off, n, d_pad, K, e);
+        if (rc != ORACLE_OK) return rc;
+    }
+    rc = oracle_step_ahead(L, off, n, d_pad, K, x, e, xh);
+    if (rc != ORACLE_OK) return rc;
+    /* the gradient at xh is the caller's input g */
+    int status = oracle_compress(L, off, n, d_pad, K, lr, g, e, signs, scales);
+    if (status == ORACLE_EINVAL) return status;
+    rc = oracle_aggregate(L, off, n, d_pad, K, mode, signs, scales, NULL, e_srv,
+                          srv_signs, srv_scales, x);
+    if (rc != ORACLE_OK) status = rc;
+    return status;
+}

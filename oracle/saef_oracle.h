@@ -1,0 +1,73 @@
+/*
+ * CPU oracle for the Step-Ahead Error Feedback (SAEF) round with the scaled
+ * sign compressor.  TEST INFRASTRUCTURE ONLY: the tests, the smoke check and
+ * the benchmark's CPU baseline may load it; the product library never does.
+ *
+ * Plain, slow, single-threaded C.  It shares no code, header, table or helper
+ * with the HIP library.  Every buffer is a host pointer.  Layout convention:
+ * L tensors, tensor l occupies elements [off[l], off[l] + n[l]) of a flat
+ * vector of d_pad floats; off[l] is a multiple of 64; worker k's vector sits at
+ * base + k * d_pad.  Sign words: bit b of word off[l]/64 + j is the sign of
+ * element 64*j + b of tensor l (1 means the value >= 0, i.e. the message
+ * carries +scale); bits past n[l] are 0.  Elements outside every tensor are
+ * never read or written.
+ *
+ * Return codes: 0 ok, -1 invalid arguments, -2 value out of the exact-sum
+ * range (|value| >= 2^19 or not finite) -- outputs are then unspecified.
+ */
+#ifndef SAEF_ORACLE_H
+#define SAEF_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ORACLE_OK 0
+#define ORACLE_EINVAL (-1)
+#define ORACLE_ERANGE (-2)
+
+/* Exact fixed-point L1 norm: S = sum_i floor(|v_i| * 2^80), returned as two
+ * 64-bit halves.  Eq. (2) numerator. */
+int oracle_l1_fixed(const float* v, int64_t n, uint64_t* s_hi, uint64_t* s_lo);
+
+/* The scale of Eq. (2) from the exact sum: fp32(fp64(fp64(S) / n) * 2^-80). */
+float oracle_scale_from_sum(uint64_t s_hi, uint64_t s_lo, int64_t n);
+
+/* Worker side of Algorithm 1 with mu = 0: Delta = e + lr * g (one rounding),
+ * message C(Delta) = (scale, sign words), e <- Delta - C(Delta). */
+int oracle_compress(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                    int32_t K, float lr, const float* g, float* e,
+                    uint64_t* signs, float* scales);
+
+/* Server side of Algorithm 1 and the re-update.  mode 1 = double-way
+ * compression (server error and server message), mode 0 = single-way (the
+ * average goes back uncompressed).  avg may be NULL.  In mode 0 e_srv,
+ * srv_signs and srv_scales may be NULL. */
+int oracle_aggregate(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                     int32_t K, int32_t mode, const uint64_t* signs, const float* scales,
+                     float* avg, float* e_srv, uint64_t* srv_signs, float* srv_scales,
+                     float* x);
+
+/* Step ahead: xh[k] = x - e[k]. */
+int oracle_step_ahead(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                      int32_t K, const float* x, const float* e, float* xh);
+
+/* Error averaging: every e[k] <- (1/K) sum_k e[k]. */
+int oracle_error_average(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                         int32_t K, float* e);
+
+/* One full iteration t of Algorithm 1 (SAEF branch, mu = 0) in the paper's
+ * order: error averaging when (t+1) mod period == 0 (period 0 = never),
+ * step ahead, [gradient g supplied], worker compression, server, re-update. */
+int oracle_round(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                 int64_t t, int64_t period, int32_t K, float lr, int32_t mode,
+                 const float* g, float* e, float* e_srv, float* x, float* xh,
+                 uint64_t* signs, float* scales, uint64_t* srv_signs, float* srv_scales);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif
