@@ -1,0 +1,157 @@
+/*
+ * saef.h -- C ABI of the MI355X (gfx950) library for the per-iteration hot
+ * path of Step-Ahead Error Feedback (SAEF) with the scaled sign compressor.
+ *
+ * The method (Xu, Huo, Huang, "Step-Ahead Error Feedback for Distributed
+ * Training with Compressed Gradient", AAAI 2021):
+ *   C(v) = (||v||_1 / d) sign(v)                                   Eq. (2)
+ * applied layer-wise (one scale per parameter tensor, d = tensor size n_l),
+ * inside Algorithm 1 (SAEF branch) with momentum constant 0:
+ *   if (t+1) mod p == 0:  e^(k) <- (1/K) sum_k e^(k)          error averaging
+ *   x^(k)_{t+1/2} = x_t - e^(k)                                step ahead
+ *   [gradient g^(k) computed at x^(k)_{t+1/2} by the caller]
+ *   Delta^(k) = e^(k) + lr g^(k);  e^(k) <- Delta^(k) - C(Delta^(k))   worker
+ *   Delta = e + (1/K) sum_k C(Delta^(k));  e <- Delta - C(Delta)       server
+ *   x <- x - C(Delta)                                          re-update
+ * The K workers are simulated on one GPU: worker k's vectors are rows of
+ * (K, d_pad) device arrays and "send"/"broadcast" are device buffers.
+ *
+ * ---------------------------------------------------------------- numbers
+ * Every fp32 result is defined exactly, so results do not depend on the
+ * launch geometry and runs are bit-reproducible:
+ *   Delta^(k)   = fma(lr, g, e)                (one rounding)
+ *   sign bit    = (v >= 0)  -- +0 and -0 give +1 (the paper leaves sign(0) open)
+ *   ||v||_1     = S = sum floor(|v_i| 2^80) as an exact integer
+ *                 (needs |v_i| < 2^19; n_l <= 2^28)
+ *   scale       = fp32( fp64( fp64(S) / n_l ) * 2^-80 )
+ *   error       = fp32(v - (bit ? scale : -scale))
+ *   worker mean = fp32( (sum_{k=0..K-1} in binary64, in k order) / K )
+ *   server Delta = fp32(e_srv + fp32(mean));   x, xh: one fp32 subtraction
+ *
+ * ---------------------------------------------------------------- layout
+ * A layout describes L parameter tensors inside a flat vector of d_pad
+ * floats: tensor l is elements [off[l], off[l] + n[l]).  off[l] must be a
+ * multiple of 64, tensors must not overlap, 1 <= n[l] <= 2^28 and
+ * off[l] + n[l] <= d_pad.  Elements outside every tensor (padding) are never
+ * read or written.  Sign words: worker k's message is the uint64 row
+ * signs[k][d_pad/64]; bit b of word off[l]/64 + j is the sign bit of element
+ * 64 j + b of tensor l (1 = the message carries +scale); bits past n[l] are
+ * written as 0.  Scales: scales[k][L] (fp32).  The server message uses
+ * srv_signs[d_pad/64] and srv_scales[L].
+ *
+ * ---------------------------------------------------------------- conventions
+ * All pointers other than the layout arrays are DEVICE pointers owned by the
+ * caller (16-byte aligned; PyTorch gives 256).  Every call is asynchronous
+ * and ordered on `stream`; nothing allocates or frees device memory except
+ * saef_layout_create / saef_layout_destroy.  Calls that use the same layout
+ * must not run concurrently (the layout holds the reduction scratch).
+ * Return codes: SAEF_OK, SAEF_EINVAL (argument check, nothing enqueued),
+ * SAEF_EHIP (a HIP call failed).  Values outside the exact-sum range (|v| >=
+ * 2^19, Inf or NaN) set a sticky device flag that saef_status reports as
+ * SAEF_ERANGE; the outputs of that call are then unspecified.
+ */
+#ifndef SAEF_H
+#define SAEF_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SAEF_OK 0
+#define SAEF_EINVAL (-1)
+#define SAEF_ERANGE (-2)
+#define SAEF_EHIP (-3)
+
+#define SAEF_MODE_SC 0 /* single-way: the server returns the mean uncompressed */
+#define SAEF_MODE_DC 1 /* double-way: Algorithm 1 (server error + server message) */
+
+typedef struct saef_layout saef_layout;
+
+/* Layer-wise compression needs one scale per tensor (Experiments: all
+ * compression is layer-wise).  Copies the host arrays off[L], n[L], builds
+ * the tile tables on the current HIP device and allocates the reduction
+ * scratch for up to k_max workers.  Synchronous.  *out receives the handle,
+ * owned by the caller until saef_layout_destroy. */
+int saef_layout_create(const int64_t* off, const int64_t* n, int32_t L, int64_t d_pad,
+                       int32_t k_max, saef_layout** out);
+int saef_layout_destroy(saef_layout* layout);
+
+/* Worker side of Algorithm 1 (local update, Delta^(k), error update, send):
+ * for every worker k < K and tensor l, Delta = fma(lr, g[k], e[k]);
+ * scales[k][l] and signs[k] receive C(Delta); e[k] <- Delta - C(Delta).
+ * g: (K, d_pad) read only.  e: (K, d_pad) in/out.  signs: (K, d_pad/64) out.
+ * scales: (K, L) out.  1 <= K <= k_max. */
+int saef_compress(const saef_layout* layout, int32_t K, float lr, const float* g, float* e,
+                  uint64_t* signs, float* scales, hipStream_t stream);
+
+/* Server side of Algorithm 1 plus the re-update.  mean = (1/K) sum_k C_k
+ * decoded from signs/scales.  mode SAEF_MODE_DC: Delta = e_srv + mean,
+ * srv_signs/srv_scales <- C(Delta), e_srv <- Delta - C(Delta),
+ * x <- x - C(Delta).  mode SAEF_MODE_SC (method notation "SC"):
+ * x <- x - mean; e_srv, srv_signs, srv_scales are unused (may be NULL).
+ * avg (d_pad) receives the mean when not NULL.  x, e_srv: (d_pad) in/out. */
+int saef_aggregate(const saef_layout* layout, int32_t K, int32_t mode, const uint64_t* signs,
+                   const float* scales, float* avg, float* e_srv, uint64_t* srv_signs,
+                   float* srv_scales, float* x, hipStream_t stream);
+
+/* Step ahead (Algorithm 1, SAEF branch): xh[k] = x - e[k] for k < K.
+ * x: (d_pad), e: (K, d_pad) read only; xh: (K, d_pad) out, must not overlap
+ * x or e. */
+int saef_step_ahead(const saef_layout* layout, int32_t K, const float* x, const float* e,
+                    float* xh, hipStream_t stream);
+
+/* Error averaging (Algorithm 1 and the "Error Averaging" section): every
+ * e[k] <- (1/K) sum_k e[k], in place.  The caller decides when it is due
+ * ((t+1) mod p == 0). */
+int saef_error_average(const saef_layout* layout, int32_t K, float* e, hipStream_t stream);
+
+/* One whole iteration t of Algorithm 1 in the paper's order: error averaging
+ * when period > 0 and (t+1) mod period == 0 (period 0 = never, p = infinity),
+ * step ahead into xh, [the caller's gradient g, already in place], worker
+ * compression, server aggregation and re-update.
+ *
+ * State form: to make each kernel a single streaming pass, saef_round keeps
+ * the state with its last compression correction pending.  After a call,
+ *   e_true[k]  = e[k]  - (bit_k ? scales[k][l] : -scales[k][l])
+ *   e_srv_true = e_srv - (bit ? srv_scales[l] : -srv_scales[l])     (DC)
+ *   x_true     = x     - (bit ? srv_scales[l] : -srv_scales[l])     (DC)
+ * (SC: x and e_srv hold plain values).  The next saef_round applies the
+ * pending corrections as it reads them; saef_materialize produces the plain
+ * values.  At t == 0 the buffers are taken as plain (Algorithm 1 starts from
+ * e = 0 and x_0) and signs/scales need no initial value; for t > 0 they must
+ * hold what the previous call left (a plain state can be entered at t > 0 by
+ * setting every scale to 0 and every sign bit to 1).
+ * xh holds the plain step-ahead weights x_t - e^(k)_t of iteration t. */
+int saef_round(const saef_layout* layout, int64_t t, int64_t period, int32_t K, float lr,
+               int32_t mode, const float* g, float* e, float* e_srv, float* x, float* xh,
+               uint64_t* signs, float* scales, uint64_t* srv_signs, float* srv_scales,
+               hipStream_t stream);
+
+/* Plain values of a saef_round state: writes e_true to e_out (K, d_pad),
+ * e_srv_true to e_srv_out and x_true to x_out (each may be NULL to skip, and
+ * may equal its input to convert in place -- the state is then plain and a
+ * later saef_round must be told so as described above). */
+int saef_materialize(const saef_layout* layout, int32_t K, int32_t mode, const float* e,
+                     const float* e_srv, const float* x, const uint64_t* signs,
+                     const float* scales, const uint64_t* srv_signs, const float* srv_scales,
+                     float* e_out, float* e_srv_out, float* x_out, hipStream_t stream);
+
+/* Synchronises `stream`, then returns and clears the layout's sticky device
+ * flag: SAEF_ERANGE if any call since the last saef_status met a value with
+ * |v| >= 2^19, Inf or NaN, SAEF_OK otherwise (SAEF_EHIP on a HIP error). */
+int saef_status(const saef_layout* layout, hipStream_t stream);
+
+/* Host-side query of a layout: tensor count, padded length, worker limit and
+ * the number of work tiles the kernels split the tensors into.  Any output
+ * pointer may be NULL.  No device work. */
+int saef_layout_info(const saef_layout* layout, int32_t* L, int64_t* d_pad, int32_t* k_max,
+                     int64_t* n_tiles);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

@@ -1,0 +1,296 @@
+// C ABI of the SAEF library: argument checks, the layout object and the
+// order in which the kernels of one SAEF iteration are enqueued.
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "saef.h"
+#include "saef_internal.h"
+
+using saef::DevLayout;
+using saef::TensorInfo;
+using saef::Tile;
+
+struct saef_layout {
+  int device = 0;
+  int32_t L = 0;
+  int32_t k_max = 0;
+  int64_t d_pad = 0;
+  std::vector<int64_t> off, n;
+  DevLayout dev{};
+  void* mem_tiles = nullptr;
+  void* mem_tensors = nullptr;
+  void* mem_acc = nullptr;
+  void* mem_cnt = nullptr;
+  void* mem_status = nullptr;
+};
+
+namespace {
+
+// Elements per work tile of a tensor of n elements: 4096, or more for very
+// large tensors so that no tensor has more than kMaxTilesPerTensor tiles
+// (bounds the arrivals on one accumulator).
+int64_t tile_elems(int64_t n) {
+  int64_t t = saef::kTileElems;
+  if (n > t * saef::kMaxTilesPerTensor) {
+    t = (n + saef::kMaxTilesPerTensor - 1) / saef::kMaxTilesPerTensor;
+    t = (t + 63) / 64 * 64;
+  }
+  return t;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// [p, p + bytes) and [q, q + qbytes) overlap?
+bool overlap(const void* p, size_t bytes, const void* q, size_t qbytes) {
+  const uintptr_t a = reinterpret_cast<uintptr_t>(p), b = reinterpret_cast<uintptr_t>(q);
+  return a < b + qbytes && b < a + bytes;
+}
+
+int check_common(const saef_layout* lay, int32_t K) {
+  if (lay == nullptr) return SAEF_EINVAL;
+  if (K < 1 || K > lay->k_max) return SAEF_EINVAL;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return SAEF_EHIP;
+  if (dev != lay->device) return SAEF_EINVAL;
+  return SAEF_OK;
+}
+
+bool f32_ok(const float* p) { return p != nullptr && aligned(p, 4); }
+bool u64_ok(const uint64_t* p) { return p != nullptr && aligned(p, 8); }
+
+int hip_rc(hipError_t e) { return e == hipSuccess ? SAEF_OK : SAEF_EHIP; }
+
+void free_layout(saef_layout* l) {
+  if (l == nullptr) return;
+  (void)hipFree(l->mem_tiles);
+  (void)hipFree(l->mem_tensors);
+  (void)hipFree(l->mem_acc);
+  (void)hipFree(l->mem_cnt);
+  (void)hipFree(l->mem_status);
+  delete l;
+}
+
+}  // namespace
+
+extern "C" {
+
+int saef_layout_create(const int64_t* off, const int64_t* n, int32_t L, int64_t d_pad,
+                       int32_t k_max, saef_layout** out) {
+  if (out == nullptr) return SAEF_EINVAL;
+  *out = nullptr;
+  if (off == nullptr || n == nullptr || L < 1 || d_pad < 64 || d_pad % 64 != 0) return SAEF_EINVAL;
+  if (k_max < 1 || k_max > 4096) return SAEF_EINVAL;
+  // tensors: 64-aligned, non-empty, in range, non-overlapping
+  std::vector<int32_t> order(L);
+  for (int32_t l = 0; l < L; ++l) {
+    if (off[l] < 0 || off[l] % 64 != 0) return SAEF_EINVAL;
+    if (n[l] < 1 || n[l] > saef::kMaxTensor) return SAEF_EINVAL;
+    if (off[l] > d_pad - n[l]) return SAEF_EINVAL;
+    order[l] = l;
+  }
+  std::sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return off[a] < off[b]; });
+  for (int32_t i = 1; i < L; ++i)
+    if (off[order[i - 1]] + n[order[i - 1]] > off[order[i]]) return SAEF_EINVAL;
+
+  saef_layout* lay = new (std::nothrow) saef_layout();
+  if (lay == nullptr) return SAEF_EHIP;
+  if (hipGetDevice(&lay->device) != hipSuccess) {
+    delete lay;
+    return SAEF_EHIP;
+  }
+  lay->L = L;
+  lay->k_max = k_max;
+  lay->d_pad = d_pad;
+  lay->off.assign(off, off + L);
+  lay->n.assign(n, n + L);
+
+  std::vector<Tile> tiles;
+  std::vector<TensorInfo> tensors(L);
+  for (int32_t l = 0; l < L; ++l) {
+    const int64_t te = tile_elems(n[l]);
+    const int64_t nt = (n[l] + te - 1) / te;
+    tensors[l] = TensorInfo{off[l], n[l], (int32_t)nt, 0};
+    for (int64_t j = 0; j < nt; ++j) {
+      const int64_t c = std::min(te, n[l] - j * te);
+      tiles.push_back(Tile{off[l] + j * te, l, (int32_t)c});
+    }
+  }
+  const size_t n_rows = (size_t)k_max + 1;
+  const size_t acc_bytes = n_rows * L * saef::kSlots * 2 * sizeof(unsigned long long);
+  const size_t cnt_bytes = n_rows * L * sizeof(unsigned int);
+  hipError_t err = hipSuccess;
+  err = hipMalloc(&lay->mem_tiles, tiles.size() * sizeof(Tile));
+  if (err == hipSuccess) err = hipMalloc(&lay->mem_tensors, tensors.size() * sizeof(TensorInfo));
+  if (err == hipSuccess) err = hipMalloc(&lay->mem_acc, acc_bytes);
+  if (err == hipSuccess) err = hipMalloc(&lay->mem_cnt, cnt_bytes);
+  if (err == hipSuccess) err = hipMalloc(&lay->mem_status, sizeof(int));
+  if (err == hipSuccess)
+    err = hipMemcpy(lay->mem_tiles, tiles.data(), tiles.size() * sizeof(Tile),
+                    hipMemcpyHostToDevice);
+  if (err == hipSuccess)
+    err = hipMemcpy(lay->mem_tensors, tensors.data(), tensors.size() * sizeof(TensorInfo),
+                    hipMemcpyHostToDevice);
+  if (err == hipSuccess) err = hipMemset(lay->mem_acc, 0, acc_bytes);
+  if (err == hipSuccess) err = hipMemset(lay->mem_cnt, 0, cnt_bytes);
+  if (err == hipSuccess) err = hipMemset(lay->mem_status, 0, sizeof(int));
+  if (err == hipSuccess) err = hipDeviceSynchronize();
+  if (err != hipSuccess) {
+    free_layout(lay);
+    return SAEF_EHIP;
+  }
+  DevLayout& d = lay->dev;
+  d.tiles = static_cast<const Tile*>(lay->mem_tiles);
+  d.tensors = static_cast<const TensorInfo*>(lay->mem_tensors);
+  d.acc = static_cast<unsigned long long*>(lay->mem_acc);
+  d.cnt = static_cast<unsigned int*>(lay->mem_cnt);
+  d.status = static_cast<int*>(lay->mem_status);
+  d.n_tiles = (int64_t)tiles.size();
+  d.d_pad = d_pad;
+  d.L = L;
+  d.k_max = k_max;
+  *out = lay;
+  return SAEF_OK;
+}
+
+int saef_layout_destroy(saef_layout* layout) {
+  if (layout == nullptr) return SAEF_EINVAL;
+  free_layout(layout);
+  return SAEF_OK;
+}
+
+int saef_layout_info(const saef_layout* layout, int32_t* L, int64_t* d_pad, int32_t* k_max,
+                     int64_t* n_tiles) {
+  if (layout == nullptr) return SAEF_EINVAL;
+  if (L) *L = layout->L;
+  if (d_pad) *d_pad = layout->d_pad;
+  if (k_max) *k_max = layout->k_max;
+  if (n_tiles) *n_tiles = layout->dev.n_tiles;
+  return SAEF_OK;
+}
+
+int saef_compress(const saef_layout* layout, int32_t K, float lr, const float* g, float* e,
+                  uint64_t* signs, float* scales, hipStream_t stream) {
+  int rc = check_common(layout, K);
+  if (rc != SAEF_OK) return rc;
+  if (!f32_ok(g) || !f32_ok(e) || !u64_ok(signs) || !f32_ok(scales) || !std::isfinite(lr))
+    return SAEF_EINVAL;
+  const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
+  if (overlap(g, vb, e, vb)) return SAEF_EINVAL;
+  rc = hip_rc(saef::launch_compress(layout->dev, K, lr, g, e, signs, scales, false, stream));
+  if (rc != SAEF_OK) return rc;
+  return hip_rc(saef::launch_materialize(layout->dev, K, SAEF_MODE_SC, e, signs, scales, e,
+                                         nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                         stream));
+}
+
+int saef_aggregate(const saef_layout* layout, int32_t K, int32_t mode, const uint64_t* signs,
+                   const float* scales, float* avg, float* e_srv, uint64_t* srv_signs,
+                   float* srv_scales, float* x, hipStream_t stream) {
+  int rc = check_common(layout, K);
+  if (rc != SAEF_OK) return rc;
+  if (mode != SAEF_MODE_SC && mode != SAEF_MODE_DC) return SAEF_EINVAL;
+  if (!u64_ok(signs) || !f32_ok(scales) || !f32_ok(x)) return SAEF_EINVAL;
+  if (avg != nullptr && !aligned(avg, 4)) return SAEF_EINVAL;
+  if (mode == SAEF_MODE_DC && (!f32_ok(e_srv) || !u64_ok(srv_signs) || !f32_ok(srv_scales)))
+    return SAEF_EINVAL;
+  rc = hip_rc(saef::launch_aggregate(layout->dev, K, mode, signs, scales, avg, e_srv, srv_signs,
+                                     srv_scales, x, false, stream));
+  if (rc != SAEF_OK || mode == SAEF_MODE_SC) return rc;
+  // e_srv <- Delta - C(Delta), x <- x - C(Delta)
+  return hip_rc(saef::launch_materialize(layout->dev, 0, SAEF_MODE_DC, nullptr, nullptr,
+                                         nullptr, nullptr, e_srv, x, srv_signs, srv_scales,
+                                         e_srv, x, stream));
+}
+
+int saef_step_ahead(const saef_layout* layout, int32_t K, const float* x, const float* e,
+                    float* xh, hipStream_t stream) {
+  int rc = check_common(layout, K);
+  if (rc != SAEF_OK) return rc;
+  if (!f32_ok(x) || !f32_ok(e) || !f32_ok(xh)) return SAEF_EINVAL;
+  const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
+  if (overlap(xh, vb, x, layout->d_pad * sizeof(float)) || overlap(xh, vb, e, vb))
+    return SAEF_EINVAL;
+  return hip_rc(saef::launch_step_ahead(layout->dev, K, const_cast<float*>(x), nullptr, nullptr,
+                                        false, const_cast<float*>(e), nullptr, nullptr, false,
+                                        false, xh, stream));
+}
+
+int saef_error_average(const saef_layout* layout, int32_t K, float* e, hipStream_t stream) {
+  int rc = check_common(layout, K);
+  if (rc != SAEF_OK) return rc;
+  if (!f32_ok(e)) return SAEF_EINVAL;
+  return hip_rc(saef::launch_step_ahead(layout->dev, K, nullptr, nullptr, nullptr, false, e,
+                                        nullptr, nullptr, false, true, nullptr, stream));
+}
+
+int saef_round(const saef_layout* layout, int64_t t, int64_t period, int32_t K, float lr,
+               int32_t mode, const float* g, float* e, float* e_srv, float* x, float* xh,
+               uint64_t* signs, float* scales, uint64_t* srv_signs, float* srv_scales,
+               hipStream_t stream) {
+  int rc = check_common(layout, K);
+  if (rc != SAEF_OK) return rc;
+  if (t < 0 || period < 0 || !std::isfinite(lr)) return SAEF_EINVAL;
+  if (mode != SAEF_MODE_SC && mode != SAEF_MODE_DC) return SAEF_EINVAL;
+  if (!f32_ok(g) || !f32_ok(e) || !f32_ok(x) || !f32_ok(xh) || !u64_ok(signs) || !f32_ok(scales))
+    return SAEF_EINVAL;
+  if (mode == SAEF_MODE_DC && (!f32_ok(e_srv) || !u64_ok(srv_signs) || !f32_ok(srv_scales)))
+    return SAEF_EINVAL;
+  const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
+  const size_t xb = layout->d_pad * sizeof(float);
+  if (overlap(xh, vb, x, xb) || overlap(xh, vb, e, vb) || overlap(xh, vb, g, vb) ||
+      overlap(g, vb, e, vb))
+    return SAEF_EINVAL;
+
+  const bool pending = t > 0;  // at t == 0 the state is plain (Algorithm 1 initialisation)
+  const bool averaging = period > 0 && (t + 1) % period == 0;
+  const bool dc = mode == SAEF_MODE_DC;
+  // error averaging (when due) and step ahead, applying last iteration's
+  // pending corrections to e and (double-way) x
+  rc = hip_rc(saef::launch_step_ahead(layout->dev, K, x, srv_signs, srv_scales, pending && dc, e,
+                                      signs, scales, pending, averaging, xh, stream));
+  if (rc != SAEF_OK) return rc;
+  // [gradient slot: g was computed at xh by the caller]
+  // worker compression; e is plain after an averaging step
+  rc = hip_rc(saef::launch_compress(layout->dev, K, lr, g, e, signs, scales,
+                                    pending && !averaging, stream));
+  if (rc != SAEF_OK) return rc;
+  // server aggregation, server compression; x keeps its correction pending
+  return hip_rc(saef::launch_aggregate(layout->dev, K, mode, signs, scales, nullptr, e_srv,
+                                       srv_signs, srv_scales, x, pending && dc, stream));
+}
+
+int saef_materialize(const saef_layout* layout, int32_t K, int32_t mode, const float* e,
+                     const float* e_srv, const float* x, const uint64_t* signs,
+                     const float* scales, const uint64_t* srv_signs, const float* srv_scales,
+                     float* e_out, float* e_srv_out, float* x_out, hipStream_t stream) {
+  int rc = check_common(layout, K);
+  if (rc != SAEF_OK) return rc;
+  if (mode != SAEF_MODE_SC && mode != SAEF_MODE_DC) return SAEF_EINVAL;
+  if (e_out != nullptr && (!f32_ok(e_out) || !f32_ok(e) || !u64_ok(signs) || !f32_ok(scales)))
+    return SAEF_EINVAL;
+  if (x_out != nullptr && (!f32_ok(x_out) || !f32_ok(x))) return SAEF_EINVAL;
+  if (e_srv_out != nullptr && !f32_ok(e_srv_out)) return SAEF_EINVAL;
+  if (mode == SAEF_MODE_DC && (e_srv_out != nullptr || x_out != nullptr) &&
+      (!u64_ok(srv_signs) || !f32_ok(srv_scales)))
+    return SAEF_EINVAL;
+  if (mode == SAEF_MODE_DC && e_srv_out != nullptr && !f32_ok(e_srv)) return SAEF_EINVAL;
+  return hip_rc(saef::launch_materialize(layout->dev, K, mode, e, signs, scales,
+                                         e_out, e_srv, x, srv_signs, srv_scales, e_srv_out,
+                                         x_out, stream));
+}
+
+int saef_status(const saef_layout* layout, hipStream_t stream) {
+  if (layout == nullptr) return SAEF_EINVAL;
+  if (hipStreamSynchronize(stream) != hipSuccess) return SAEF_EHIP;
+  int flag = 0;
+  if (hipMemcpy(&flag, layout->dev.status, sizeof(int), hipMemcpyDeviceToHost) != hipSuccess)
+    return SAEF_EHIP;
+  if (flag != 0 && hipMemset(layout->dev.status, 0, sizeof(int)) != hipSuccess) return SAEF_EHIP;
+  return (flag & saef::kStatusRange) ? SAEF_ERANGE : SAEF_OK;
+}
+
+}  // extern "C"

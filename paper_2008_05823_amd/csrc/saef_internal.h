@@ -1,0 +1,85 @@
+// Internal declarations shared by the kernel and host translation units of
+// the SAEF library (not part of the public C ABI in include/saef.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace saef {
+
+constexpr int kWave = 64;             // CDNA wavefront width
+constexpr int kBlock = 256;           // threads per workgroup (4 waves)
+constexpr int kWaves = kBlock / kWave;
+constexpr int kSlots = 8;             // spread of the per-tensor sum over addresses
+constexpr int kTileElems = 4096;      // default work tile (elements, multiple of 64)
+constexpr int kMaxTilesPerTensor = 2048;
+constexpr int64_t kMaxTensor = int64_t(1) << 28;
+
+// One unit of work: `count` consecutive elements of tensor `l` starting at
+// absolute element index `start` (a multiple of 64).
+struct Tile {
+  int64_t start;
+  int32_t l;
+  int32_t count;
+};
+
+struct TensorInfo {
+  int64_t off;
+  int64_t n;
+  int32_t ntiles;
+  int32_t pad_;
+};
+
+// Device-side view of a layout, passed by value to every kernel.
+struct DevLayout {
+  const Tile* tiles;
+  const TensorInfo* tensors;
+  unsigned long long* acc;  // [(k_max + 1) * L * kSlots * 2] partial exact sums (lo, hi)
+  unsigned int* cnt;        // [(k_max + 1) * L] arrival tickets
+  int* status;              // sticky error flag
+  int64_t n_tiles;
+  int64_t d_pad;
+  int32_t L;
+  int32_t k_max;
+};
+
+// status flag bits
+constexpr int kStatusRange = 1;
+
+// ---- kernel launchers (defined in saef_kernels.hip) ----------------------
+// All return hipSuccess or the launch error.  Arguments are validated by the
+// caller.
+
+// Worker compression.  decode: e holds values with a pending correction
+// (signs/scales of the previous compression) that is applied on read.
+// Always writes Delta (before correction) into e, the new sign words and the
+// new scales.
+hipError_t launch_compress(const DevLayout& lay, int K, float lr, const float* g, float* e,
+                           uint64_t* signs, float* scales, bool decode, hipStream_t s);
+
+// Server aggregation.  mode 1: reads/writes e_srv (Delta before correction),
+// writes srv_signs/srv_scales; decode applies the pending server correction
+// to e_srv on read.  mode 0: x <- x - mean.  avg written when non-null.
+hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_t* signs,
+                            const float* scales, float* avg, float* e_srv, uint64_t* srv_signs,
+                            float* srv_scales, float* x, bool decode, hipStream_t s);
+
+// Step ahead / error averaging.  decode_x: apply the pending server
+// correction to x and write x back plain.  decode_e: apply the pending worker
+// corrections to e on read.  average: replace every e[k] by the mean and
+// write it back (plain).  xh written when non-null.
+hipError_t launch_step_ahead(const DevLayout& lay, int K, float* x, const uint64_t* srv_signs,
+                             const float* srv_scales, bool decode_x, float* e,
+                             const uint64_t* signs, const float* scales, bool decode_e,
+                             bool average, float* xh, hipStream_t s);
+
+// Apply pending corrections: e_out[k] = e[k] - c_k for k < K (when e_out),
+// and, when e_srv_out or x_out is given, e_srv_out = e_srv - c and
+// x_out = x - c (mode 1) or plain copies (mode 0; e_srv_out then receives 0).
+hipError_t launch_materialize(const DevLayout& lay, int K, int mode, const float* e,
+                              const uint64_t* signs, const float* scales, float* e_out,
+                              const float* e_srv, const float* x, const uint64_t* srv_signs,
+                              const float* srv_scales, float* e_srv_out, float* x_out,
+                              hipStream_t s);
+
+}  // namespace saef

@@ -1,0 +1,158 @@
+"""Helpers of the GPU parity tests: device buffers for a workload, the same
+iteration run by the HIP library and by the CPU oracle, and comparisons.
+
+The oracle and the HIP path share nothing but the inputs drawn by
+paper_2008_05823_amd.workloads; expected values always come from the oracle.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from oracle import oracle as O
+from paper_2008_05823_amd import workloads as W
+
+REL_TOL, ABS_TOL = 1e-6, 1e-7   # acceptance bound for fp32 state
+
+
+def dev(a: np.ndarray) -> torch.Tensor:
+    if a.dtype == np.uint64:
+        a = a.view(np.int64)
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t: torch.Tensor, like=np.float32) -> np.ndarray:
+    a = t.detach().cpu().numpy()
+    if like == np.uint64:
+        a = a.view(np.uint64)
+    return a
+
+
+def tensor_word_mask(off, n, d_pad) -> np.ndarray:
+    m = np.zeros(d_pad // 64, bool)
+    for o, nl in zip(off, n):
+        m[o // 64:o // 64 + (nl + 63) // 64] = True
+    return m
+
+
+def assert_f32_equal(got: np.ndarray, want: np.ndarray, mask: np.ndarray, what: str):
+    """Bit-exact equality on the masked elements (the design gives identical
+    IEEE operations on both sides); the report also shows the spec tolerance."""
+    g = got[..., mask]
+    w = want[..., mask]
+    same = g.view(np.uint32) == w.view(np.uint32)
+    if same.all():
+        return
+    tol_ok = np.abs(g.astype(np.float64) - w) <= ABS_TOL + REL_TOL * np.abs(w.astype(np.float64))
+    bad = np.argwhere(~same)
+    first = tuple(bad[0])
+    raise AssertionError(
+        f"{what}: {int((~same).sum())} of {same.size} values differ from the oracle "
+        f"({int((~tol_ok).sum())} beyond 1e-6 rel/1e-7 abs); first at {first}: "
+        f"got {g[first]!r} want {w[first]!r}")
+
+
+def assert_words_equal(got: np.ndarray, want: np.ndarray, wmask: np.ndarray, what: str):
+    g = got[..., wmask]
+    w = want[..., wmask]
+    if not np.array_equal(g, w):
+        bad = np.argwhere(g != w)
+        first = tuple(bad[0])
+        raise AssertionError(f"{what}: {len(bad)} sign words differ; first at {first}: "
+                             f"got {int(g[first]):#x} want {int(w[first]):#x}")
+
+
+class OracleState:
+    """Host state of Algorithm 1 advanced by the C oracle."""
+
+    def __init__(self, w: W.Workload, x0: np.ndarray | None = None, K: int | None = None):
+        self.w = w
+        self.K = w.K if K is None else K
+        off, n, d_pad = w.layout()
+        self.orc = O.Oracle(off, n, d_pad)
+        self.x = (W.initial_x(w) if x0 is None else x0).copy()
+        self.e = np.zeros((self.K, d_pad), np.float32)
+        self.e_srv = np.zeros(d_pad, np.float32)
+        self.xh = np.zeros((self.K, d_pad), np.float32)
+        self.signs = np.zeros((self.K, d_pad // 64), np.uint64)
+        self.scales = np.zeros((self.K, w.L), np.float32)
+        self.srv_signs = np.zeros(d_pad // 64, np.uint64)
+        self.srv_scales = np.zeros(w.L, np.float32)
+
+    def round(self, t: int, g: np.ndarray, period=None, mode=None):
+        w = self.w
+        rc = self.orc.round(t, w.period if period is None else period, self.K, np.float32(w.lr),
+                            w.mode if mode is None else mode, g, self.e, self.e_srv, self.x,
+                            self.xh, self.signs, self.scales, self.srv_signs, self.srv_scales)
+        assert rc == O.OK, rc
+
+
+class GpuState:
+    """Device buffers of one workload driven through the HIP library."""
+
+    def __init__(self, w: W.Workload, x0: np.ndarray | None = None, K: int | None = None,
+                 k_max: int | None = None):
+        from paper_2008_05823_amd import saef
+        self.saef = saef
+        self.w = w
+        self.K = w.K if K is None else K
+        off, n, d_pad = w.layout()
+        self.off, self.n, self.d_pad = off, n, d_pad
+        self.layout = saef.Layout(off, n, d_pad, k_max or self.K)
+        f32 = dict(dtype=torch.float32, device="cuda")
+        i64 = dict(dtype=torch.int64, device="cuda")
+        self.x = dev(W.initial_x(w) if x0 is None else x0)
+        self.e = torch.zeros((self.K, d_pad), **f32)
+        self.e_srv = torch.zeros(d_pad, **f32)
+        self.xh = torch.zeros((self.K, d_pad), **f32)
+        self.signs = torch.zeros((self.K, d_pad // 64), **i64)
+        self.scales = torch.zeros((self.K, w.L), **f32)
+        self.srv_signs = torch.zeros(d_pad // 64, **i64)
+        self.srv_scales = torch.zeros(w.L, **f32)
+        self.g = torch.zeros((self.K, d_pad), **f32)
+
+    def round(self, t: int, g: np.ndarray | torch.Tensor, period=None, mode=None):
+        w = self.w
+        if isinstance(g, np.ndarray):
+            self.g.copy_(torch.from_numpy(g))
+        else:
+            self.g.copy_(g)
+        self.saef.saef_round(self.layout, t, w.period if period is None else period, self.K,
+                             w.lr, w.mode if mode is None else mode, self.g, self.e,
+                             self.e_srv, self.x, self.xh, self.signs, self.scales,
+                             self.srv_signs, self.srv_scales)
+
+    def plain(self, mode=None) -> dict:
+        """Materialized (plain) state, downloaded to the host."""
+        mode = self.w.mode if mode is None else mode
+        e_out = torch.zeros_like(self.e)
+        es_out = torch.zeros_like(self.e_srv)
+        x_out = torch.zeros_like(self.x)
+        self.saef.saef_materialize(self.layout, self.K, mode, self.e, self.e_srv, self.x,
+                                   self.signs, self.scales, self.srv_signs, self.srv_scales,
+                                   e_out, es_out, x_out)
+        torch.cuda.synchronize()
+        return dict(e=host(e_out), e_srv=host(es_out), x=host(x_out), xh=host(self.xh),
+                    signs=host(self.signs, np.uint64), scales=host(self.scales),
+                    srv_signs=host(self.srv_signs, np.uint64), srv_scales=host(self.srv_scales))
+
+    def status(self) -> int:
+        return self.saef.saef_status(self.layout)
+
+
+def compare_state(gpu: dict, orc: OracleState, t: int, what: str = ""):
+    w = orc.w
+    off, n, d_pad = w.layout()
+    m = W.tensor_mask(w)
+    wm = tensor_word_mask(off, n, d_pad)
+    tag = f"{what} t={t}"
+    assert_words_equal(gpu["signs"], orc.signs, wm, f"{tag} worker sign words")
+    assert_f32_equal(gpu["scales"], orc.scales, np.ones(w.L, bool), f"{tag} worker scales")
+    assert_f32_equal(gpu["e"], orc.e, m, f"{tag} worker errors")
+    assert_f32_equal(gpu["xh"], orc.xh, m, f"{tag} step-ahead weights")
+    assert_f32_equal(gpu["x"], orc.x, m, f"{tag} weights")
+    if w.mode == 1:
+        assert_words_equal(gpu["srv_signs"], orc.srv_signs, wm, f"{tag} server sign words")
+        assert_f32_equal(gpu["srv_scales"], orc.srv_scales, np.ones(w.L, bool),
+                         f"{tag} server scales")
+        assert_f32_equal(gpu["e_srv"], orc.e_srv, m, f"{tag} server error")

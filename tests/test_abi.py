@@ -1,0 +1,63 @@
+"""The C ABI library loads and exports every entry point of include/saef.h,
+and its host-side argument checks work without a GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "saef.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^int\s+(saef_\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def saef():
+    from paper_2008_05823_amd import saef as mod
+    return mod
+
+
+def test_header_declares_the_entry_points():
+    names = header_functions()
+    for required in ("saef_compress", "saef_aggregate", "saef_step_ahead",
+                     "saef_error_average", "saef_round", "saef_layout_create",
+                     "saef_layout_destroy", "saef_status", "saef_materialize"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol(saef):
+    lib = ctypes.CDLL(saef.LIB_PATH)
+    for name in header_functions():
+        assert hasattr(lib, name), f"{name} declared in saef.h but not exported"
+    assert sorted(saef.EXPORTS) == header_functions()
+
+
+def test_layout_create_rejects_bad_layouts_on_host(saef):
+    lib = saef.raw_library()
+    h = ctypes.c_void_p()
+
+    def create(off, n, d_pad, k_max=2):
+        o = (ctypes.c_int64 * len(off))(*off)
+        s = (ctypes.c_int64 * len(n))(*n)
+        return lib.saef_layout_create(o, s, len(off), d_pad, k_max, ctypes.byref(h))
+
+    assert create([32], [10], 64) == saef.EINVAL            # offset not 64-aligned
+    assert create([0, 64], [100, 10], 192) == saef.EINVAL   # overlap
+    assert create([0], [0], 64) == saef.EINVAL              # empty tensor
+    assert create([0], [65], 64) == saef.EINVAL             # past d_pad
+    assert create([0], [10], 64, k_max=0) == saef.EINVAL    # no workers
+    assert create([0], [1 << 29], 1 << 29) == saef.EINVAL   # above 2^28 elements
+    assert h.value is None
+
+
+def test_null_layout_is_rejected(saef):
+    lib = saef.raw_library()
+    assert lib.saef_layout_destroy(None) == saef.EINVAL
+    assert lib.saef_status(None, None) == saef.EINVAL
+    assert lib.saef_compress(None, 1, ctypes.c_float(0.1), None, None, None, None,
+                             None) == saef.EINVAL
+    assert lib.saef_round(None, 0, 0, 1, ctypes.c_float(0.1), 1, *([None] * 10)) == saef.EINVAL
