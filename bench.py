@@ -1,0 +1,224 @@
+"""Benchmark of the SAEF iteration on one MI355X.
+
+One step = one whole iteration of Algorithm 1 (SAEF branch, double-way
+compression) through the C ABI entry point saef_round: error averaging when
+due, step ahead, worker compression of all K workers, server aggregation and
+re-update.  The synthetic gradients of the iteration are already resident in
+HBM when the timed region starts (two seeded gradient sets alternate).
+
+Default workload: ResNet-50 shaped tensor list (161 tensors, d = 25,557,032),
+K = 8 workers, lr 0.1, error averaging period 20.
+
+Prints one JSON line (metric, value = parameters per second per K-worker
+iteration, roofline of the dominant kernel, CPU oracle baseline).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0      # MI355X HBM3E
+METRIC = "params/s per K-worker SAEF round + achieved HBM GB/s vs MI355X peak"
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2008_05823_amd", "csrc", "saef_kernels.hip")
+
+
+def kernel_hash() -> str:
+    with open(KERNEL_SOURCE, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
+def traffic_from_profile(workload: str):
+    """HBM bytes per compress launch from the committed rocprofv3 counter
+    summary, when it was taken on the current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", f"compress_{workload}_counters.txt")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    if fields.get("kernel_source_sha256_16") != kernel_hash():
+        return None
+    try:
+        return float(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, grads_host, x0, rounds: int) -> dict:
+    """The CPU oracle (single thread) on the first `rounds` iterations of the
+    same workload and inputs."""
+    import numpy as np
+    from oracle import oracle as O
+    off, n, d_pad = w.layout()
+    orc = O.Oracle(off, n, d_pad)
+    K, L = w.K, w.L
+    x = x0.copy()
+    e = np.zeros((K, d_pad), np.float32)
+    e_srv = np.zeros(d_pad, np.float32)
+    xh = np.zeros((K, d_pad), np.float32)
+    signs = np.zeros((K, d_pad // 64), np.uint64)
+    scales = np.zeros((K, L), np.float32)
+    ss = np.zeros(d_pad // 64, np.uint64)
+    sscales = np.zeros(L, np.float32)
+    total = 0.0
+    for t in range(rounds):
+        g = grads_host[t % len(grads_host)]
+        t0 = time.perf_counter()
+        rc = orc.round(t, w.period, K, np.float32(w.lr), w.mode, g, e, e_srv, x, xh, signs,
+                       scales, ss, sscales)
+        total += time.perf_counter() - t0
+        if rc != 0:
+            raise RuntimeError(f"oracle returned {rc}")
+    per_round = total / rounds
+    return {"value": w.d / per_round, "unit": "params/s", "cores": 1, "kind": "oracle",
+            "sample": f"{rounds} full iterations (t=0..{rounds - 1}) of the {w.name} workload, "
+                      f"K={K}, single-threaded C oracle, {per_round:.2f} s per iteration"}
+
+
+def copy_probe_gbps(nbytes: int = 2 << 30) -> float:
+    """Read+write GB/s of a plain device-to-device copy (context for the roofline)."""
+    import torch
+    a = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1.0)
+    for _ in range(2):
+        b.copy_(a)
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 10
+    s.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / reps
+    del a, b
+    return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="resnet50",
+                    help="flat64k | resnet56 | resnet50 | bert_base | flat256m")
+    ap.add_argument("--cpu-rounds", type=int, default=1,
+                    help="iterations of the CPU oracle baseline (0 = skip)")
+    ap.add_argument("--no-probe", action="store_true", help="skip the copy-bandwidth probe")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (got --gpus {args.gpus}); the "
+              "K workers are simulated on that GPU", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+    from paper_2008_05823_amd import saef
+    from paper_2008_05823_amd import workloads as W
+
+    w = W.get(args.workload)
+    off, n, d_pad = w.layout()
+    K, L, d = w.K, w.L, w.d
+    torch.cuda.set_device(0)
+
+    # synthetic inputs, resident in HBM before timing
+    n_grad = 2
+    grads_host = [W.gradients(w, t) for t in range(n_grad)]
+    x0 = W.initial_x(w)
+    f32 = dict(dtype=torch.float32, device="cuda")
+    g_dev = [torch.from_numpy(g).cuda() for g in grads_host]
+    x = torch.from_numpy(x0).cuda()
+    e = torch.zeros((K, d_pad), **f32)
+    e_srv = torch.zeros(d_pad, **f32)
+    xh = torch.zeros((K, d_pad), **f32)
+    signs = torch.zeros((K, d_pad // 64), dtype=torch.int64, device="cuda")
+    scales = torch.zeros((K, L), **f32)
+    srv_signs = torch.zeros(d_pad // 64, dtype=torch.int64, device="cuda")
+    srv_scales = torch.zeros(L, **f32)
+    layout = saef.Layout(off, n, d_pad, K)
+
+    def step(t):
+        saef.saef_round(layout, t, w.period, K, w.lr, w.mode, g_dev[t % n_grad], e, e_srv, x, xh,
+                        signs, scales, srv_signs, srv_scales)
+
+    for t in range(args.warmup):
+        step(t)
+    torch.cuda.synchronize()
+    saef.saef_profile_enable(layout, 5 * args.steps)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        step(args.warmup + i)
+    stop.record()
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    prof = saef.saef_profile_read(layout)
+    saef.saef_profile_enable(layout, 0)
+    if saef.saef_status(layout) != saef.OK:
+        print("bench.py: a value left the exact-sum range", file=sys.stderr)
+        return 1
+    ms_per_step = ms_total / args.steps
+
+    timed_ts = range(args.warmup, args.warmup + args.steps)
+    n_avg = sum(1 for t in timed_ts if w.period and (t + 1) % w.period == 0)
+    bytes_round = np.mean([W.algorithmic_bytes_per_param(
+        K, w.mode, averaging=bool(w.period and (t + 1) % w.period == 0)) for t in timed_ts]) * d
+
+    # dominant kernel: worker compression (12 K + K/8 bytes per parameter)
+    c_count, c_ms = prof["compress"]
+    c_avg_ms = c_ms / max(c_count, 1)
+    c_bytes = (12 * K + K / 8) * d
+    c_gbps = c_bytes / (c_avg_ms * 1e-3) / 1e9
+    traffic = traffic_from_profile(args.workload)
+
+    kernels = {k: {"launches": c, "avg_us": (ms / c * 1e3) if c else None}
+               for k, (c, ms) in prof.items()}
+    probe = None if args.no_probe else round(copy_probe_gbps(), 1)
+
+    out = {
+        "metric": METRIC,
+        "value": d / (ms_per_step * 1e-3),
+        "unit": "params/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: {L} tensors, d={d}, K={K} simulated workers, "
+                               f"double-way, lr={w.lr}, error averaging period {w.period}",
+                   "K": K, "d": d, "L": L, "period": w.period, "mode": "DC"},
+        "worker_params_per_s": K * d / (ms_per_step * 1e-3),
+        "round_hbm_gbps": bytes_round / (ms_per_step * 1e-3) / 1e9,
+        "round_frac_of_peak": bytes_round / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "averaging_steps_timed": n_avg,
+        "kernels": kernels,
+        "copy_probe_gbps": probe,
+        "roofline": {"bound": "hbm", "kernel": "compress", "achieved": c_gbps,
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": c_gbps / HBM_PEAK_GBPS,
+                     "traffic": traffic, "algorithmic_bytes_per_launch": c_bytes},
+    }
+    if args.cpu_rounds > 0:
+        out["cpu_baseline"] = cpu_baseline(w, grads_host, x0, args.cpu_rounds)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

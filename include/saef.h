@@ -144,6 +144,18 @@ int saef_materialize(const saef_layout* layout, int32_t K, int32_t mode, const f
  * |v| >= 2^19, Inf or NaN, SAEF_OK otherwise (SAEF_EHIP on a HIP error). */
 int saef_status(const saef_layout* layout, hipStream_t stream);
 
+/* Per-kernel timing of saef_round, for measurement.  saef_profile_enable
+ * with capacity > 0 creates that many HIP event pairs; every later
+ * saef_round on this layout then records one pair around each kernel it
+ * enqueues (kind 0 = step ahead and error averaging, 1 = worker compression,
+ * 2 = worker scales from the tile sums, 3 = server aggregation, 4 = server
+ * scales) until the pairs run out.  saef_profile_read waits for the recorded
+ * events and returns, per kind, the number of launches timed (counts[5]) and
+ * their summed durations in milliseconds (total_ms[5]), then starts over with
+ * all pairs free.  capacity 0 releases the events and stops recording. */
+int saef_profile_enable(saef_layout* layout, int32_t capacity);
+int saef_profile_read(saef_layout* layout, int32_t* counts, double* total_ms);
+
 /* Host-side query of a layout: tensor count, padded length, worker limit and
  * the number of work tiles the kernels split the tensors into.  Any output
  * pointer may be NULL.  No device work. */

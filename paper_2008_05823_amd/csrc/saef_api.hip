@@ -23,9 +23,12 @@ struct saef_layout {
   DevLayout dev{};
   void* mem_tiles = nullptr;
   void* mem_tensors = nullptr;
-  void* mem_acc = nullptr;
-  void* mem_cnt = nullptr;
+  void* mem_part = nullptr;
   void* mem_status = nullptr;
+  // measurement: event pairs recorded around the kernels of saef_round
+  std::vector<hipEvent_t> ev_start, ev_stop;
+  std::vector<int> ev_kind;
+  size_t ev_used = 0;
 };
 
 namespace {
@@ -41,6 +44,8 @@ int64_t tile_elems(int64_t n) {
   }
   return t;
 }
+
+constexpr int kProfileKinds = 5;
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -64,12 +69,38 @@ bool u64_ok(const uint64_t* p) { return p != nullptr && aligned(p, 8); }
 
 int hip_rc(hipError_t e) { return e == hipSuccess ? SAEF_OK : SAEF_EHIP; }
 
+void release_events(saef_layout* l) {
+  for (hipEvent_t e : l->ev_start) (void)hipEventDestroy(e);
+  for (hipEvent_t e : l->ev_stop) (void)hipEventDestroy(e);
+  l->ev_start.clear();
+  l->ev_stop.clear();
+  l->ev_kind.clear();
+  l->ev_used = 0;
+}
+
+// Launches one kernel of saef_round, bracketed by an event pair when the
+// layout is being profiled and a pair is free.
+template <typename F>
+hipError_t timed(const saef_layout* cl, int kind, hipStream_t s, F&& launch) {
+  saef_layout* l = const_cast<saef_layout*>(cl);
+  const bool rec = l->ev_used < l->ev_start.size();
+  if (rec && hipEventRecord(l->ev_start[l->ev_used], s) != hipSuccess) return hipErrorUnknown;
+  hipError_t err = launch();
+  if (err != hipSuccess) return err;
+  if (rec) {
+    if (hipEventRecord(l->ev_stop[l->ev_used], s) != hipSuccess) return hipErrorUnknown;
+    l->ev_kind[l->ev_used] = kind;
+    ++l->ev_used;
+  }
+  return hipSuccess;
+}
+
 void free_layout(saef_layout* l) {
   if (l == nullptr) return;
+  release_events(l);
   (void)hipFree(l->mem_tiles);
   (void)hipFree(l->mem_tensors);
-  (void)hipFree(l->mem_acc);
-  (void)hipFree(l->mem_cnt);
+  (void)hipFree(l->mem_part);
   (void)hipFree(l->mem_status);
   delete l;
 }
@@ -113,20 +144,18 @@ int saef_layout_create(const int64_t* off, const int64_t* n, int32_t L, int64_t 
   for (int32_t l = 0; l < L; ++l) {
     const int64_t te = tile_elems(n[l]);
     const int64_t nt = (n[l] + te - 1) / te;
-    tensors[l] = TensorInfo{off[l], n[l], (int32_t)nt, 0};
+    tensors[l] = TensorInfo{off[l], n[l], (int32_t)tiles.size(), (int32_t)nt};
     for (int64_t j = 0; j < nt; ++j) {
       const int64_t c = std::min(te, n[l] - j * te);
       tiles.push_back(Tile{off[l] + j * te, l, (int32_t)c});
     }
   }
   const size_t n_rows = (size_t)k_max + 1;
-  const size_t acc_bytes = n_rows * L * saef::kSlots * 2 * sizeof(unsigned long long);
-  const size_t cnt_bytes = n_rows * L * sizeof(unsigned int);
+  const size_t part_bytes = n_rows * tiles.size() * 2 * sizeof(unsigned long long);
   hipError_t err = hipSuccess;
   err = hipMalloc(&lay->mem_tiles, tiles.size() * sizeof(Tile));
   if (err == hipSuccess) err = hipMalloc(&lay->mem_tensors, tensors.size() * sizeof(TensorInfo));
-  if (err == hipSuccess) err = hipMalloc(&lay->mem_acc, acc_bytes);
-  if (err == hipSuccess) err = hipMalloc(&lay->mem_cnt, cnt_bytes);
+  if (err == hipSuccess) err = hipMalloc(&lay->mem_part, part_bytes);
   if (err == hipSuccess) err = hipMalloc(&lay->mem_status, sizeof(int));
   if (err == hipSuccess)
     err = hipMemcpy(lay->mem_tiles, tiles.data(), tiles.size() * sizeof(Tile),
@@ -134,8 +163,7 @@ int saef_layout_create(const int64_t* off, const int64_t* n, int32_t L, int64_t 
   if (err == hipSuccess)
     err = hipMemcpy(lay->mem_tensors, tensors.data(), tensors.size() * sizeof(TensorInfo),
                     hipMemcpyHostToDevice);
-  if (err == hipSuccess) err = hipMemset(lay->mem_acc, 0, acc_bytes);
-  if (err == hipSuccess) err = hipMemset(lay->mem_cnt, 0, cnt_bytes);
+  if (err == hipSuccess) err = hipMemset(lay->mem_part, 0, part_bytes);
   if (err == hipSuccess) err = hipMemset(lay->mem_status, 0, sizeof(int));
   if (err == hipSuccess) err = hipDeviceSynchronize();
   if (err != hipSuccess) {
@@ -145,8 +173,7 @@ int saef_layout_create(const int64_t* off, const int64_t* n, int32_t L, int64_t 
   DevLayout& d = lay->dev;
   d.tiles = static_cast<const Tile*>(lay->mem_tiles);
   d.tensors = static_cast<const TensorInfo*>(lay->mem_tensors);
-  d.acc = static_cast<unsigned long long*>(lay->mem_acc);
-  d.cnt = static_cast<unsigned int*>(lay->mem_cnt);
+  d.part = static_cast<unsigned long long*>(lay->mem_part);
   d.status = static_cast<int*>(lay->mem_status);
   d.n_tiles = (int64_t)tiles.size();
   d.d_pad = d_pad;
@@ -182,6 +209,8 @@ int saef_compress(const saef_layout* layout, int32_t K, float lr, const float* g
   if (overlap(g, vb, e, vb)) return SAEF_EINVAL;
   rc = hip_rc(saef::launch_compress(layout->dev, K, lr, g, e, signs, scales, false, stream));
   if (rc != SAEF_OK) return rc;
+  rc = hip_rc(saef::launch_finalize(layout->dev, K, false, scales, stream));
+  if (rc != SAEF_OK) return rc;
   return hip_rc(saef::launch_materialize(layout->dev, K, SAEF_MODE_SC, e, signs, scales, e,
                                          nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
                                          stream));
@@ -200,6 +229,8 @@ int saef_aggregate(const saef_layout* layout, int32_t K, int32_t mode, const uin
   rc = hip_rc(saef::launch_aggregate(layout->dev, K, mode, signs, scales, avg, e_srv, srv_signs,
                                      srv_scales, x, false, stream));
   if (rc != SAEF_OK || mode == SAEF_MODE_SC) return rc;
+  rc = hip_rc(saef::launch_finalize(layout->dev, K, true, srv_scales, stream));
+  if (rc != SAEF_OK) return rc;
   // e_srv <- Delta - C(Delta), x <- x - C(Delta)
   return hip_rc(saef::launch_materialize(layout->dev, 0, SAEF_MODE_DC, nullptr, nullptr,
                                          nullptr, nullptr, e_srv, x, srv_signs, srv_scales,
@@ -250,17 +281,29 @@ int saef_round(const saef_layout* layout, int64_t t, int64_t period, int32_t K, 
   const bool dc = mode == SAEF_MODE_DC;
   // error averaging (when due) and step ahead, applying last iteration's
   // pending corrections to e and (double-way) x
-  rc = hip_rc(saef::launch_step_ahead(layout->dev, K, x, srv_signs, srv_scales, pending && dc, e,
-                                      signs, scales, pending, averaging, xh, stream));
+  const DevLayout& d = layout->dev;
+  rc = hip_rc(timed(layout, 0, stream, [&] {
+    return saef::launch_step_ahead(d, K, x, srv_signs, srv_scales, pending && dc, e, signs,
+                                   scales, pending, averaging, xh, stream);
+  }));
   if (rc != SAEF_OK) return rc;
   // [gradient slot: g was computed at xh by the caller]
   // worker compression; e is plain after an averaging step
-  rc = hip_rc(saef::launch_compress(layout->dev, K, lr, g, e, signs, scales,
-                                    pending && !averaging, stream));
+  rc = hip_rc(timed(layout, 1, stream, [&] {
+    return saef::launch_compress(d, K, lr, g, e, signs, scales, pending && !averaging, stream);
+  }));
+  if (rc != SAEF_OK) return rc;
+  rc = hip_rc(timed(layout, 2, stream,
+                    [&] { return saef::launch_finalize(d, K, false, scales, stream); }));
   if (rc != SAEF_OK) return rc;
   // server aggregation, server compression; x keeps its correction pending
-  return hip_rc(saef::launch_aggregate(layout->dev, K, mode, signs, scales, nullptr, e_srv,
-                                       srv_signs, srv_scales, x, pending && dc, stream));
+  rc = hip_rc(timed(layout, 3, stream, [&] {
+    return saef::launch_aggregate(d, K, mode, signs, scales, nullptr, e_srv, srv_signs,
+                                  srv_scales, x, pending && dc, stream);
+  }));
+  if (rc != SAEF_OK || !dc) return rc;
+  return hip_rc(timed(layout, 4, stream,
+                      [&] { return saef::launch_finalize(d, K, true, srv_scales, stream); }));
 }
 
 int saef_materialize(const saef_layout* layout, int32_t K, int32_t mode, const float* e,
@@ -281,6 +324,45 @@ int saef_materialize(const saef_layout* layout, int32_t K, int32_t mode, const f
   return hip_rc(saef::launch_materialize(layout->dev, K, mode, e, signs, scales,
                                          e_out, e_srv, x, srv_signs, srv_scales, e_srv_out,
                                          x_out, stream));
+}
+
+int saef_profile_enable(saef_layout* layout, int32_t capacity) {
+  if (layout == nullptr || capacity < 0 || capacity > (1 << 20)) return SAEF_EINVAL;
+  release_events(layout);
+  for (int32_t i = 0; i < capacity; ++i) {
+    hipEvent_t a = nullptr, b = nullptr;
+    if (hipEventCreate(&a) != hipSuccess) return SAEF_EHIP;
+    if (hipEventCreate(&b) != hipSuccess) {
+      (void)hipEventDestroy(a);
+      return SAEF_EHIP;
+    }
+    layout->ev_start.push_back(a);
+    layout->ev_stop.push_back(b);
+    layout->ev_kind.push_back(-1);
+  }
+  layout->ev_used = 0;
+  return SAEF_OK;
+}
+
+int saef_profile_read(saef_layout* layout, int32_t* counts, double* total_ms) {
+  if (layout == nullptr || counts == nullptr || total_ms == nullptr) return SAEF_EINVAL;
+  for (int i = 0; i < kProfileKinds; ++i) {
+    counts[i] = 0;
+    total_ms[i] = 0.0;
+  }
+  for (size_t i = 0; i < layout->ev_used; ++i) {
+    if (hipEventSynchronize(layout->ev_stop[i]) != hipSuccess) return SAEF_EHIP;
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, layout->ev_start[i], layout->ev_stop[i]) != hipSuccess)
+      return SAEF_EHIP;
+    const int k = layout->ev_kind[i];
+    if (k >= 0 && k < kProfileKinds) {
+      counts[k] += 1;
+      total_ms[k] += ms;
+    }
+  }
+  layout->ev_used = 0;
+  return SAEF_OK;
 }
 
 int saef_status(const saef_layout* layout, hipStream_t stream) {

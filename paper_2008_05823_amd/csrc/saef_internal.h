@@ -10,7 +10,6 @@ namespace saef {
 constexpr int kWave = 64;             // CDNA wavefront width
 constexpr int kBlock = 256;           // threads per workgroup (4 waves)
 constexpr int kWaves = kBlock / kWave;
-constexpr int kSlots = 8;             // spread of the per-tensor sum over addresses
 constexpr int kTileElems = 4096;      // default work tile (elements, multiple of 64)
 constexpr int kMaxTilesPerTensor = 2048;
 constexpr int64_t kMaxTensor = int64_t(1) << 28;
@@ -26,17 +25,17 @@ struct Tile {
 struct TensorInfo {
   int64_t off;
   int64_t n;
+  int32_t first_tile;
   int32_t ntiles;
-  int32_t pad_;
 };
 
 // Device-side view of a layout, passed by value to every kernel.
 struct DevLayout {
   const Tile* tiles;
   const TensorInfo* tensors;
-  unsigned long long* acc;  // [(k_max + 1) * L * kSlots * 2] partial exact sums (lo, hi)
-  unsigned int* cnt;        // [(k_max + 1) * L] arrival tickets
-  int* status;              // sticky error flag
+  unsigned long long* part;  // [(k_max + 1) * n_tiles * 2] exact partial sums (lo, hi) of
+                             // each tile; row k_max belongs to the server
+  int* status;               // sticky error flag
   int64_t n_tiles;
   int64_t d_pad;
   int32_t L;
@@ -53,16 +52,23 @@ constexpr int kStatusRange = 1;
 // Worker compression.  decode: e holds values with a pending correction
 // (signs/scales of the previous compression) that is applied on read.
 // Always writes Delta (before correction) into e, the new sign words and the
-// new scales.
+// tile partial sums; launch_finalize then writes the new scales.
 hipError_t launch_compress(const DevLayout& lay, int K, float lr, const float* g, float* e,
-                           uint64_t* signs, float* scales, bool decode, hipStream_t s);
+                           uint64_t* signs, const float* scales, bool decode, hipStream_t s);
+
+// Scales from the tile partial sums: worker rows 0..K-1 into scales[k][l]
+// (server == false) or the server row into scales[l] (server == true).
+hipError_t launch_finalize(const DevLayout& lay, int K, bool server, float* scales,
+                           hipStream_t s);
 
 // Server aggregation.  mode 1: reads/writes e_srv (Delta before correction),
-// writes srv_signs/srv_scales; decode applies the pending server correction
-// to e_srv on read.  mode 0: x <- x - mean.  avg written when non-null.
+// writes srv_signs and the server tile partial sums (launch_finalize then
+// writes srv_scales); decode applies the pending server correction (old
+// srv_signs/srv_scales) to e_srv on read.  mode 0: x <- x - mean.  avg
+// written when non-null.
 hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_t* signs,
                             const float* scales, float* avg, float* e_srv, uint64_t* srv_signs,
-                            float* srv_scales, float* x, bool decode, hipStream_t s);
+                            const float* srv_scales, float* x, bool decode, hipStream_t s);
 
 // Step ahead / error averaging.  decode_x: apply the pending server
 // correction to x and write x back plain.  decode_e: apply the pending worker

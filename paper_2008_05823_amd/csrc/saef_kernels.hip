@@ -6,15 +6,16 @@
 // words w*U .. w*U+U-1, then strides by 4*U words; lane i of a wave owns
 // element 64*word + i, so every global load/store of a wave is one contiguous
 // 256-byte segment and the sign word of those 64 elements is a single
-// wave-wide ballot.
+// wave-wide ballot.  Value buffers are streamed with non-temporal loads and
+// stores: nothing is re-read soon enough to profit from the caches.
 //
-// Layer-wise scale (Eq. (2), one scale per tensor): every workgroup adds the
-// exact integer sum of floor(|v| 2^80) over its tile to a 128-bit accumulator
-// of (worker, tensor) with two 64-bit atomics, then takes an arrival ticket;
-// the workgroup that arrives last converts the total into the fp32 scale and
-// clears the accumulator for the next launch.  Integer addition is
-// associative, so the scale does not depend on the tiling or on the order in
-// which workgroups arrive.
+// Layer-wise scale (Eq. (2), one scale per tensor): every workgroup reduces
+// the exact integer sum of floor(|v| 2^80) over its tile and stores it as a
+// 128-bit partial (plain stores, no cross-workgroup atomics: on a multi-XCD
+// part those go to memory-side atomics and serialise).  A small finalize
+// kernel then adds the partials of each tensor and converts the total into
+// the fp32 scale.  Integer addition is associative, so the scale does not
+// depend on the tiling or on the order of anything.
 //
 // Single pass: the error update e = Delta - C(Delta) needs the scale of the
 // whole tensor, which is known only after every tile was read.  The kernels
@@ -30,35 +31,34 @@ namespace {
 typedef unsigned long long u64;
 
 constexpr uint32_t kAbsLimitBits = 0x49000000u;  // bit pattern of 2^19
+constexpr int kWPW = 16;  // words per wave held in registers by the K-worker kernels
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+__device__ __forceinline__ float ld_nt(const float* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ void st_nt(float* p, float v) { __builtin_nontemporal_store(v, p); }
 
 // Adds floor(|v| * 2^80) to the 128-bit integer (hi, lo); `a` is the bit
 // pattern of |v| and must be below that of 2^19.
 __device__ __forceinline__ void add_fixed(uint32_t a, u64& lo, u64& hi) {
   uint32_t ex = a >> 23;
   uint32_t m = a & 0x7FFFFFu;
-  if (ex != 0) {
-    m |= 0x800000u;
-  } else {
-    ex = 1;  // subnormal: m * 2^-149
-  }
-  // |v| = m * 2^(ex - 150), so |v| * 2^80 = m * 2^(ex - 70)
+  m |= (ex != 0) ? 0x800000u : 0u;
+  ex = (ex != 0) ? ex : 1u;  // subnormal: m * 2^-149
+  // |v| = m * 2^(ex - 150), so |v| * 2^80 = m * 2^(ex - 70), ex - 70 in [-69, 75]
   const int sh = (int)ex - 70;
-  u64 vlo, vhi;
-  if (sh >= 64) {
-    vlo = 0;
-    vhi = (u64)m << (sh - 64);
-  } else if (sh > 0) {
-    vlo = (u64)m << sh;
-    vhi = (u64)m >> (64 - sh);
-  } else if (sh == 0) {
-    vlo = m;
-    vhi = 0;
+  // split as t * 2^(32 q) with t = m * 2^(sh mod 32) < 2^55, q in {0, 1, 2}
+  u64 t;
+  int q;
+  if (sh >= 0) {
+    q = sh >> 5;
+    t = (u64)m << (sh & 31);
   } else {
-    vlo = (sh > -32) ? (u64)(m >> (-sh)) : 0ull;
-    vhi = 0;
+    q = 0;
+    t = (sh > -32) ? (u64)(m >> (-sh)) : 0ull;
   }
+  const u64 vlo = (q == 0) ? t : ((q == 1) ? (t << 32) : 0ull);
+  const u64 vhi = (q == 0) ? 0ull : ((q == 1) ? (t >> 32) : t);
   lo += vlo;
   hi += vhi + (lo < vlo ? 1ull : 0ull);
 }
@@ -106,15 +106,20 @@ __device__ float scale_from_sum(u64 hi, u64 lo, int64_t n) {
 
 __device__ __forceinline__ float corr(bool bit, float s) { return bit ? s : -s; }
 
-__device__ __forceinline__ bool bit_of(u64 word, int lane) {
-  return ((word >> lane) & 1ull) != 0;
+// The 32-bit half of the sign word at p that holds bit `lane` (a per-lane
+// load: one VGPR per word instead of a scalar register pair).
+__device__ __forceinline__ uint32_t half_word(const uint64_t* p, int lane) {
+  return reinterpret_cast<const uint32_t*>(p)[lane >> 5];
+}
+__device__ __forceinline__ bool half_bit(uint32_t h, int lane) {
+  return ((h >> (lane & 31)) & 1u) != 0;
 }
 
-// Reduce the per-lane exact sums of the workgroup, add them to the
-// accumulator of (row, l) and, in the last workgroup to arrive, write the
-// tensor's scale to *scale_out.
-__device__ void block_finish(const DevLayout& lay, int row, int l, u64 lo, u64 hi, bool bad,
-                             float* scale_out) {
+// Adds up the per-lane exact sums of the workgroup and stores the total as
+// the partial of (row, tile); raises the range flag if any lane saw a value
+// outside the exact-sum range.
+__device__ void block_partial(const DevLayout& lay, int row, int64_t tile, u64 lo, u64 hi,
+                              bool bad) {
   __shared__ u64 s_lo[kWaves];
   __shared__ u64 s_hi[kWaves];
   wave_sum128(lo, hi);
@@ -127,28 +132,10 @@ __device__ void block_finish(const DevLayout& lay, int row, int l, u64 lo, u64 h
   if (threadIdx.x != 0) return;
   u64 tlo = 0, thi = 0;
   for (int i = 0; i < kWaves; ++i) add128(tlo, thi, s_lo[i], s_hi[i]);
+  u64* p = lay.part + ((int64_t)row * lay.n_tiles + tile) * 2;
+  p[0] = tlo;
+  p[1] = thi;
   if (any_bad) atomicOr(lay.status, kStatusRange);
-
-  const size_t idx = (size_t)row * lay.L + l;
-  u64* a = lay.acc + (idx * kSlots + (blockIdx.x & (kSlots - 1))) * 2;
-  const u64 old = atomicAdd(a, tlo);
-  const u64 carry = (old + tlo < old) ? 1ull : 0ull;
-  atomicAdd(a + 1, thi + carry);
-  __threadfence();
-  const unsigned ticket = atomicAdd(lay.cnt + idx, 1u);
-  if (ticket != (unsigned)lay.tensors[l].ntiles - 1) return;
-
-  // last arrival: every other tile of (row, l) has added its part
-  __threadfence();
-  u64 slo = 0, shi = 0;
-  for (int sl = 0; sl < kSlots; ++sl) {
-    u64* as = lay.acc + (idx * kSlots + sl) * 2;
-    const u64 plo = atomicExch(as, 0ull);
-    const u64 phi = atomicExch(as + 1, 0ull);
-    add128(slo, shi, plo, phi);
-  }
-  atomicExch(lay.cnt + idx, 0u);
-  *scale_out = scale_from_sum(shi, slo, lay.tensors[l].n);
 }
 
 // ------------------------------------------------------------------ compress
@@ -158,11 +145,12 @@ __global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float
                                                      const float* __restrict__ g,
                                                      float* __restrict__ e,
                                                      uint64_t* __restrict__ signs,
-                                                     float* __restrict__ scales) {
+                                                     const float* __restrict__ scales) {
   constexpr int U = 4;
   const int64_t b = blockIdx.x;
   const int k = (int)(b % K);
-  const Tile tile = lay.tiles[b / K];
+  const int64_t ti = b / K;
+  const Tile tile = lay.tiles[ti];
   const int l = tile.l;
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
@@ -177,14 +165,14 @@ __global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float
   bool bad = false;
   for (int w0 = wave * U; w0 < nw; w0 += kWaves * U) {
     float gv[U], ev[U];
-    u64 ow[U];
+    uint32_t ow[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int j = (w0 + u) * 64 + lane;
       const bool ok = (w0 + u < nw) && j < tile.count;
-      gv[u] = ok ? gk[j] : 0.0f;
-      ev[u] = ok ? ek[j] : 0.0f;
-      ow[u] = (kDecode && w0 + u < nw) ? sk[w0 + u] : 0ull;
+      gv[u] = ok ? ld_nt(gk + j) : 0.0f;
+      ev[u] = ok ? ld_nt(ek + j) : 0.0f;
+      ow[u] = (kDecode && w0 + u < nw) ? half_word(sk + w0 + u, lane) : 0u;
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -193,7 +181,7 @@ __global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float
       const int j = w * 64 + lane;
       const bool ok = j < tile.count;
       float ev2 = ev[u];
-      if (kDecode) ev2 = ev2 - corr(bit_of(ow[u], lane), s_old);
+      if (kDecode) ev2 = ev2 - corr(half_bit(ow[u], lane), s_old);
       // Delta^(k) = e^(k) + lr * g^(k), one rounding
       const float p = __builtin_fmaf(lr, gv[u], ev2);
       const u64 word = __ballot(ok && p >= 0.0f);
@@ -205,15 +193,98 @@ __global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float
         } else {
           bad = true;
         }
-        ek[j] = p;
+        st_nt(ek + j, p);
       }
     }
   }
-  block_finish(lay, k, l, lo, hi, bad, scales + (int64_t)k * lay.L + l);
+  block_partial(lay, k, ti, lo, hi, bad);
+}
+
+// ------------------------------------------------------------------ finalize
+// Grid: rows * L single-wave workgroups; workgroup b adds the tile partials
+// of tensor b % L for row b / L (or the server row) and writes the scale.
+__global__ __launch_bounds__(kWave) void k_finalize(DevLayout lay, int server,
+                                                    float* __restrict__ scales) {
+  const int64_t b = blockIdx.x;
+  const int l = (int)(b % lay.L);
+  const int r = (int)(b / lay.L);
+  const int row = server ? lay.k_max : r;
+  const TensorInfo t = lay.tensors[l];
+  const u64* p = lay.part + ((int64_t)row * lay.n_tiles + t.first_tile) * 2;
+  u64 lo = 0, hi = 0;
+  for (int i = threadIdx.x; i < t.ntiles; i += kWave) add128(lo, hi, p[2 * i], p[2 * i + 1]);
+  wave_sum128(lo, hi);
+  if (threadIdx.x == 0) scales[server ? l : (int64_t)r * lay.L + l] = scale_from_sum(hi, lo, t.n);
 }
 
 // ------------------------------------------------------------------ aggregate
-// Grid: n_tiles workgroups.  mean = (sum_k +-scale_k in binary64, k order)/K.
+// One pass of a wave over kWPW words (elements base + 64 u, u < kWPW) of a
+// tile: the wave holds the words in registers and walks the K worker
+// messages in order, mean = (sum_k +-scale_k in binary64, k order) / K.
+// kFull: all kWPW words lie inside the tile (no per-lane guards); otherwise
+// only the first nv words are present and element base + 64 u exists iff
+// 64 u < lim.
+template <int kMode, bool kDecode, bool kAvg, bool kFull, int kN>
+__device__ __forceinline__ void aggregate_pass(const DevLayout& lay, int K, double inv_k, int l,
+                                               int64_t base, int64_t gw, int nv, int lim,
+                                               const uint64_t* __restrict__ signs,
+                                               const float* __restrict__ scales,
+                                               float* __restrict__ avg, float* __restrict__ es,
+                                               uint64_t* __restrict__ ss, float s_srv_old,
+                                               float* __restrict__ x, u64& lo, u64& hi,
+                                               bool& bad) {
+  const int lane = lane_id();
+  const int64_t W = lay.d_pad >> 6;
+  float v[kN];
+#pragma unroll
+  for (int u = 0; u < kN; ++u) {
+    v[u] = 0.0f;
+    if (kFull || (u < nv && u * 64 < lim))
+      v[u] = (kMode == 1) ? ld_nt(es + base + u * 64) : ld_nt(x + base + u * 64);
+  }
+  double acc[kN];
+#pragma unroll
+  for (int u = 0; u < kN; ++u) acc[u] = 0.0;
+  for (int k = 0; k < K; ++k) {
+    const double sd = (double)scales[(int64_t)k * lay.L + l];
+    const uint64_t* sk = signs + (int64_t)k * W + gw;
+    uint32_t hw[kN];
+#pragma unroll
+    for (int u = 0; u < kN; ++u) hw[u] = (kFull || u < nv) ? half_word(sk + u, lane) : 0u;
+#pragma unroll
+    for (int u = 0; u < kN; ++u) acc[u] += half_bit(hw[u], lane) ? sd : -sd;
+  }
+#pragma unroll
+  for (int u = 0; u < kN; ++u) {
+    if (!kFull && u >= nv) continue;
+    const bool ok = kFull || u * 64 < lim;
+    const float mean = (inv_k != 0.0) ? (float)(acc[u] * inv_k) : (float)(acc[u] / (double)K);
+    const int64_t i = base + u * 64;
+    if (kAvg && ok) avg[i] = mean;
+    if (kMode == 1) {
+      float ev = v[u];
+      if (kDecode) ev = ev - corr(half_bit(half_word(ss + gw + u, lane), lane), s_srv_old);
+      // Delta = e + (1/K) sum_k C(Delta^(k))
+      const float D = ev + mean;
+      const u64 word = __ballot(ok && D >= 0.0f);
+      if (lane == 0) ss[gw + u] = word;
+      if (ok) {
+        const uint32_t a = __float_as_uint(D) & 0x7FFFFFFFu;
+        if (a < kAbsLimitBits) {
+          add_fixed(a, lo, hi);
+        } else {
+          bad = true;
+        }
+        st_nt(es + i, D);
+      }
+    } else if (ok) {
+      st_nt(x + i, v[u] - mean);  // single-way: the mean itself comes back
+    }
+  }
+}
+
+// Grid: n_tiles workgroups; wave w takes passes of kWPW words starting at
+// word w*kWPW, striding by 4*kWPW words.
 template <int kMode, bool kDecode, bool kAvg>
 __global__ __launch_bounds__(kBlock) void k_aggregate(DevLayout lay, int K, double inv_k,
                                                       const uint64_t* __restrict__ signs,
@@ -221,61 +292,128 @@ __global__ __launch_bounds__(kBlock) void k_aggregate(DevLayout lay, int K, doub
                                                       float* __restrict__ avg,
                                                       float* __restrict__ es,
                                                       uint64_t* __restrict__ ss,
-                                                      float* __restrict__ sscales,
+                                                      const float* __restrict__ sscales,
                                                       float* __restrict__ x) {
-  constexpr int U = 2;
-  const Tile tile = lay.tiles[blockIdx.x];
+  const int64_t ti = blockIdx.x;
+  const Tile tile = lay.tiles[ti];
   const int l = tile.l;
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
-  const int64_t W = lay.d_pad >> 6;
-  const int64_t gw0 = tile.start >> 6;
   const int nw = (tile.count + 63) >> 6;
   const float s_srv_old = (kMode == 1 && kDecode) ? sscales[l] : 0.0f;
-
   u64 lo = 0, hi = 0;
   bool bad = false;
-  for (int w0 = wave * U; w0 < nw; w0 += kWaves * U) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int w = w0 + u;
-      if (w >= nw) break;
-      const int j = w * 64 + lane;
-      const bool ok = j < tile.count;
-      const int64_t i = tile.start + j;
-      double acc = 0.0;
-      for (int k = 0; k < K; ++k) {
-        const u64 word = signs[(int64_t)k * W + gw0 + w];
-        const float s = scales[(int64_t)k * lay.L + l];
-        acc += (double)corr(bit_of(word, lane), s);
-      }
-      const float mean = (inv_k != 0.0) ? (float)(acc * inv_k) : (float)(acc / (double)K);
-      if (kAvg && ok) avg[i] = mean;
-      if (kMode == 1) {
-        float ev = ok ? es[i] : 0.0f;
-        if (kDecode) ev = ev - corr(bit_of(ss[gw0 + w], lane), s_srv_old);
-        // Delta = e + (1/K) sum_k C(Delta^(k))
-        const float D = ev + mean;
-        const u64 word = __ballot(ok && D >= 0.0f);
-        if (lane == 0) ss[gw0 + w] = word;
-        if (ok) {
-          const uint32_t a = __float_as_uint(D) & 0x7FFFFFFFu;
-          if (a < kAbsLimitBits) {
-            add_fixed(a, lo, hi);
-          } else {
-            bad = true;
-          }
-          es[i] = D;
-        }
-      } else if (ok) {
-        x[i] = x[i] - mean;  // single-way: the mean itself comes back
+  for (int wb = wave * kWPW; wb < nw; wb += kWaves * kWPW) {
+    const int64_t base = tile.start + wb * 64 + lane;
+    const int64_t gw = (tile.start >> 6) + wb;
+    if ((wb + kWPW) * 64 <= tile.count) {
+      aggregate_pass<kMode, kDecode, kAvg, true, kWPW>(lay, K, inv_k, l, base, gw, kWPW, 0, signs,
+                                                       scales, avg, es, ss, s_srv_old, x, lo, hi,
+                                                       bad);
+    } else {
+      // tail of the tile: one word at a time, guarded per lane
+      const int nv = min(kWPW, nw - wb);
+      for (int u = 0; u < nv; ++u) {
+        aggregate_pass<kMode, kDecode, kAvg, false, 1>(
+            lay, K, inv_k, l, base + u * 64, gw + u, 1, tile.count - (wb + u) * 64 - lane,
+            signs, scales, avg, es, ss, s_srv_old, x, lo, hi, bad);
       }
     }
   }
-  if (kMode == 1) block_finish(lay, lay.k_max, l, lo, hi, bad, sscales + l);
+  if (kMode == 1) block_partial(lay, lay.k_max, ti, lo, hi, bad);
 }
 
 // ------------------------------------------------------------------ step ahead
+// One pass over kWPW words of a tile (same conventions as aggregate_pass):
+// x is read once into registers, then the K workers are walked in order.
+template <bool kDecX, bool kDecE, bool kAverage, bool kXh, bool kFull, int kN>
+__device__ __forceinline__ void step_pass(const DevLayout& lay, int K, double inv_k, int l,
+                                          int64_t base, int64_t gw, int nv, int lim,
+                                          float* __restrict__ x, const uint64_t* __restrict__ ss,
+                                          float s_srv, float* __restrict__ e,
+                                          const uint64_t* __restrict__ signs,
+                                          const float* __restrict__ scales,
+                                          float* __restrict__ xh) {
+  const int lane = lane_id();
+  const int64_t d_pad = lay.d_pad;
+  const int64_t W = d_pad >> 6;
+  float xv[kN];
+#pragma unroll
+  for (int u = 0; u < kN; ++u) {
+    xv[u] = 0.0f;
+    if ((kXh || kDecX) && (kFull || (u < nv && u * 64 < lim))) xv[u] = ld_nt(x + base + u * 64);
+  }
+  if (kDecX) {
+#pragma unroll
+    for (int u = 0; u < kN; ++u) {
+      if (!kFull && u >= nv) continue;
+      // pending re-update x <- x - C(Delta) of the previous iteration
+      xv[u] = xv[u] - corr(half_bit(half_word(ss + gw + u, lane), lane), s_srv);
+      if (kFull || u * 64 < lim) st_nt(x + base + u * 64, xv[u]);
+    }
+  }
+  if (kAverage) {
+    // e^(k) <- (1/K) sum_k e^(k), binary64 sum in worker order
+    double acc[kN];
+#pragma unroll
+    for (int u = 0; u < kN; ++u) acc[u] = 0.0;
+    for (int k = 0; k < K; ++k) {
+      const float* ek = e + (int64_t)k * d_pad + base;
+      const uint64_t* sk = signs + (int64_t)k * W + gw;
+      const float s = kDecE ? scales[(int64_t)k * lay.L + l] : 0.0f;
+      float ev[kN];
+      uint32_t hw[kN];
+#pragma unroll
+      for (int u = 0; u < kN; ++u) {
+        ev[u] = 0.0f;
+        if (kFull || (u < nv && u * 64 < lim)) ev[u] = ld_nt(ek + u * 64);
+        hw[u] = (kDecE && (kFull || u < nv)) ? half_word(sk + u, lane) : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < kN; ++u) {
+        if (kDecE) ev[u] = ev[u] - corr(half_bit(hw[u], lane), s);
+        acc[u] += (double)ev[u];
+      }
+    }
+    float m[kN];
+#pragma unroll
+    for (int u = 0; u < kN; ++u)
+      m[u] = (inv_k != 0.0) ? (float)(acc[u] * inv_k) : (float)(acc[u] / (double)K);
+    for (int k = 0; k < K; ++k) {
+      float* ek = e + (int64_t)k * d_pad + base;
+      float* hk = xh + (int64_t)k * d_pad + base;
+#pragma unroll
+      for (int u = 0; u < kN; ++u) {
+        if (kFull || (u < nv && u * 64 < lim)) {
+          st_nt(ek + u * 64, m[u]);
+          if (kXh) st_nt(hk + u * 64, xv[u] - m[u]);
+        }
+      }
+    }
+  } else if (kXh) {
+    // x^(k)_{t+1/2} = x_t - e^(k)_t
+    for (int k = 0; k < K; ++k) {
+      const float* ek = e + (int64_t)k * d_pad + base;
+      float* hk = xh + (int64_t)k * d_pad + base;
+      const uint64_t* sk = signs + (int64_t)k * W + gw;
+      const float s = kDecE ? scales[(int64_t)k * lay.L + l] : 0.0f;
+      float ev[kN];
+      uint32_t hw[kN];
+#pragma unroll
+      for (int u = 0; u < kN; ++u) {
+        ev[u] = 0.0f;
+        if (kFull || (u < nv && u * 64 < lim)) ev[u] = ld_nt(ek + u * 64);
+        hw[u] = (kDecE && (kFull || u < nv)) ? half_word(sk + u, lane) : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < kN; ++u) {
+        if (kDecE) ev[u] = ev[u] - corr(half_bit(hw[u], lane), s);
+        if (kFull || (u < nv && u * 64 < lim)) st_nt(hk + u * 64, xv[u] - ev[u]);
+      }
+    }
+  }
+}
+
 // Grid: n_tiles workgroups, each handles all K workers of its tile so x is
 // read once.
 template <bool kDecX, bool kDecE, bool kAverage, bool kXh>
@@ -287,59 +425,25 @@ __global__ __launch_bounds__(kBlock) void k_step_ahead(DevLayout lay, int K, dou
                                                        const uint64_t* __restrict__ signs,
                                                        const float* __restrict__ scales,
                                                        float* __restrict__ xh) {
-  constexpr int U = 2;
   const Tile tile = lay.tiles[blockIdx.x];
   const int l = tile.l;
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
-  const int64_t d_pad = lay.d_pad;
-  const int64_t W = d_pad >> 6;
-  const int64_t gw0 = tile.start >> 6;
   const int nw = (tile.count + 63) >> 6;
   const float s_srv = kDecX ? sscales[l] : 0.0f;
-
-  for (int w0 = wave * U; w0 < nw; w0 += kWaves * U) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int w = w0 + u;
-      if (w >= nw) break;
-      const int j = w * 64 + lane;
-      const bool ok = j < tile.count;
-      const int64_t i = tile.start + j;
-      float xv = 0.0f;
-      if ((kXh || kDecX) && ok) xv = x[i];
-      if (kDecX) {
-        xv = xv - corr(bit_of(ss[gw0 + w], lane), s_srv);  // pending re-update
-        if (ok) x[i] = xv;
-      }
-      if (kAverage) {
-        // e^(k) <- (1/K) sum_k e^(k)
-        double acc = 0.0;
-        for (int k = 0; k < K; ++k) {
-          float ev = ok ? e[(int64_t)k * d_pad + i] : 0.0f;
-          if (kDecE) {
-            ev = ev - corr(bit_of(signs[(int64_t)k * W + gw0 + w], lane),
-                           scales[(int64_t)k * lay.L + l]);
-          }
-          acc += (double)ev;
-        }
-        const float m = (inv_k != 0.0) ? (float)(acc * inv_k) : (float)(acc / (double)K);
-        if (ok) {
-          for (int k = 0; k < K; ++k) {
-            e[(int64_t)k * d_pad + i] = m;
-            if (kXh) xh[(int64_t)k * d_pad + i] = xv - m;
-          }
-        }
-      } else if (kXh) {
-        // x^(k)_{t+1/2} = x_t - e^(k)_t
-        for (int k = 0; k < K; ++k) {
-          float ev = ok ? e[(int64_t)k * d_pad + i] : 0.0f;
-          if (kDecE) {
-            ev = ev - corr(bit_of(signs[(int64_t)k * W + gw0 + w], lane),
-                           scales[(int64_t)k * lay.L + l]);
-          }
-          if (ok) xh[(int64_t)k * d_pad + i] = xv - ev;
-        }
+  for (int wb = wave * kWPW; wb < nw; wb += kWaves * kWPW) {
+    const int64_t base = tile.start + wb * 64 + lane;
+    const int64_t gw = (tile.start >> 6) + wb;
+    if ((wb + kWPW) * 64 <= tile.count) {
+      step_pass<kDecX, kDecE, kAverage, kXh, true, kWPW>(lay, K, inv_k, l, base, gw, kWPW, 0, x,
+                                                         ss, s_srv, e, signs, scales, xh);
+    } else {
+      // tail of the tile: one word at a time, guarded per lane
+      const int nv = min(kWPW, nw - wb);
+      for (int u = 0; u < nv; ++u) {
+        step_pass<kDecX, kDecE, kAverage, kXh, false, 1>(
+            lay, K, inv_k, l, base + u * 64, gw + u, 1, tile.count - (wb + u) * 64 - lane, x, ss,
+            s_srv, e, signs, scales, xh);
       }
     }
   }
@@ -364,14 +468,13 @@ __global__ __launch_bounds__(kBlock) void k_materialize(
   const int64_t gw0 = tile.start >> 6;
   const int nw = (tile.count + 63) >> 6;
   if (row < K) {
-    if (e_out == nullptr) return;
     const float s = scales[(int64_t)row * lay.L + l];
     const uint64_t* sk = signs + (int64_t)row * (d_pad >> 6) + gw0;
     for (int w = wave; w < nw; w += kWaves) {
       const int j = w * 64 + lane;
       if (j < tile.count) {
         const int64_t i = (int64_t)row * d_pad + tile.start + j;
-        e_out[i] = e[i] - corr(bit_of(sk[w], lane), s);
+        e_out[i] = e[i] - corr(half_bit(half_word(sk + w, lane), lane), s);
       }
     }
     return;
@@ -382,7 +485,7 @@ __global__ __launch_bounds__(kBlock) void k_materialize(
     if (j >= tile.count) continue;
     const int64_t i = tile.start + j;
     if (mode == 1) {
-      const float c = corr(bit_of(ss[gw0 + w], lane), s);
+      const float c = corr(half_bit(half_word(ss + gw0 + w, lane), lane), s);
       if (es_out) es_out[i] = es[i] - c;
       if (x_out) x_out[i] = x[i] - c;
     } else {
@@ -397,7 +500,7 @@ double inv_pow2(int K) { return (K & (K - 1)) == 0 ? 1.0 / (double)K : 0.0; }
 }  // namespace
 
 hipError_t launch_compress(const DevLayout& lay, int K, float lr, const float* g, float* e,
-                           uint64_t* signs, float* scales, bool decode, hipStream_t s) {
+                           uint64_t* signs, const float* scales, bool decode, hipStream_t s) {
   const dim3 grid((unsigned)(lay.n_tiles * K));
   if (decode) {
     hipLaunchKernelGGL(k_compress<true>, grid, dim3(kBlock), 0, s, lay, K, lr, g, e, signs,
@@ -409,9 +512,16 @@ hipError_t launch_compress(const DevLayout& lay, int K, float lr, const float* g
   return hipGetLastError();
 }
 
+hipError_t launch_finalize(const DevLayout& lay, int K, bool server, float* scales,
+                           hipStream_t s) {
+  const dim3 grid((unsigned)((server ? 1 : K) * lay.L));
+  hipLaunchKernelGGL(k_finalize, grid, dim3(kWave), 0, s, lay, server ? 1 : 0, scales);
+  return hipGetLastError();
+}
+
 hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_t* signs,
                             const float* scales, float* avg, float* e_srv, uint64_t* srv_signs,
-                            float* srv_scales, float* x, bool decode, hipStream_t s) {
+                            const float* srv_scales, float* x, bool decode, hipStream_t s) {
   const dim3 grid((unsigned)lay.n_tiles);
   const double ik = inv_pow2(K);
 #define SAEF_AGG(M, D, A)                                                                  \

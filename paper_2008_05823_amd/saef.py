@@ -41,6 +41,8 @@ _SIGS = {
     "saef_round": [_P, _i64, _i64, _i32, _f32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P],
     "saef_materialize": [_P, _i32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P],
     "saef_status": [_P, _P],
+    "saef_profile_enable": [_P, _i32],
+    "saef_profile_read": [_P, _P, _P],
 }
 for _name, _args in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -184,6 +186,21 @@ def saef_status(layout: Layout, stream=None) -> int:
     if rc not in (OK, ERANGE):
         raise SaefError("saef_status", rc)
     return rc
+
+
+PROFILE_KINDS = ("step_ahead", "compress", "worker_scales", "aggregate", "server_scales")
+
+
+def saef_profile_enable(layout: Layout, capacity: int) -> None:
+    _check("saef_profile_enable", _lib.saef_profile_enable(layout.handle, int(capacity)))
+
+
+def saef_profile_read(layout: Layout) -> dict:
+    """{kind: (launches timed, summed milliseconds)} since the last read."""
+    counts = (ctypes.c_int32 * len(PROFILE_KINDS))()
+    ms = (ctypes.c_double * len(PROFILE_KINDS))()
+    _check("saef_profile_read", _lib.saef_profile_read(layout.handle, counts, ms))
+    return {k: (counts[i], ms[i]) for i, k in enumerate(PROFILE_KINDS)}
 
 
 def raw_library() -> ctypes.CDLL:
