@@ -29,9 +29,11 @@ def hipcc() -> str:
     return path if os.path.exists(path) else "hipcc"
 
 
-def build(out: str = LIB, verbose: bool = False) -> str:
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"),
-           "-o", out + ".tmp", *SOURCES]
+def build(out: str = LIB, verbose: bool = False, defines=()) -> str:
+    """Compile the library to `out`; `defines` are extra -D options (tuning
+    variants, e.g. SAEF_TILE_ELEMS=2048)."""
+    cmd = [hipcc(), *HIPCC_FLAGS, *[f"-D{d}" for d in defines],
+           "-I", os.path.join(ROOT, "include"), "-o", out + ".tmp", *SOURCES]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

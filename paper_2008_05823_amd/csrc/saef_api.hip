@@ -45,7 +45,7 @@ int64_t tile_elems(int64_t n) {
   return t;
 }
 
-constexpr int kProfileKinds = 5;
+constexpr int kProfileKinds = 6;
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -245,9 +245,9 @@ int saef_step_ahead(const saef_layout* layout, int32_t K, const float* x, const 
   const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
   if (overlap(xh, vb, x, layout->d_pad * sizeof(float)) || overlap(xh, vb, e, vb))
     return SAEF_EINVAL;
-  return hip_rc(saef::launch_step_ahead(layout->dev, K, const_cast<float*>(x), nullptr, nullptr,
-                                        false, const_cast<float*>(e), nullptr, nullptr, false,
-                                        false, xh, stream));
+  return hip_rc(saef::launch_step_ahead(layout->dev, K, x, nullptr, nullptr, false,
+                                        const_cast<float*>(e), nullptr, nullptr, false, false, xh,
+                                        stream));
 }
 
 int saef_error_average(const saef_layout* layout, int32_t K, float* e, hipStream_t stream) {
@@ -282,7 +282,7 @@ int saef_round(const saef_layout* layout, int64_t t, int64_t period, int32_t K, 
   // error averaging (when due) and step ahead, applying last iteration's
   // pending corrections to e and (double-way) x
   const DevLayout& d = layout->dev;
-  rc = hip_rc(timed(layout, 0, stream, [&] {
+  rc = hip_rc(timed(layout, averaging ? 5 : 0, stream, [&] {
     return saef::launch_step_ahead(d, K, x, srv_signs, srv_scales, pending && dc, e, signs,
                                    scales, pending, averaging, xh, stream);
   }));

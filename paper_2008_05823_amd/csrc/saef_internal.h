@@ -10,8 +10,11 @@ namespace saef {
 constexpr int kWave = 64;             // CDNA wavefront width
 constexpr int kBlock = 256;           // threads per workgroup (4 waves)
 constexpr int kWaves = kBlock / kWave;
-constexpr int kTileElems = 4096;      // default work tile (elements, multiple of 64)
-constexpr int kMaxTilesPerTensor = 2048;
+#ifndef SAEF_TILE_ELEMS
+#define SAEF_TILE_ELEMS 2048
+#endif
+constexpr int kTileElems = SAEF_TILE_ELEMS;  // default work tile (elements, multiple of 64)
+constexpr int kMaxTilesPerTensor = 8192;
 constexpr int64_t kMaxTensor = int64_t(1) << 28;
 
 // One unit of work: `count` consecutive elements of tensor `l` starting at
@@ -64,19 +67,20 @@ hipError_t launch_finalize(const DevLayout& lay, int K, bool server, float* scal
 // Server aggregation.  mode 1: reads/writes e_srv (Delta before correction),
 // writes srv_signs and the server tile partial sums (launch_finalize then
 // writes srv_scales); decode applies the pending server correction (old
-// srv_signs/srv_scales) to e_srv on read.  mode 0: x <- x - mean.  avg
-// written when non-null.
+// srv_signs/srv_scales) to e_srv on read and materializes it into x.
+// mode 0: x <- x - mean.  avg written when non-null.
 hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_t* signs,
                             const float* scales, float* avg, float* e_srv, uint64_t* srv_signs,
                             const float* srv_scales, float* x, bool decode, hipStream_t s);
 
 // Step ahead / error averaging.  decode_x: apply the pending server
-// correction to x and write x back plain.  decode_e: apply the pending worker
-// corrections to e on read.  average: replace every e[k] by the mean and
-// write it back (plain).  xh written when non-null.
-hipError_t launch_step_ahead(const DevLayout& lay, int K, float* x, const uint64_t* srv_signs,
-                             const float* srv_scales, bool decode_x, float* e,
-                             const uint64_t* signs, const float* scales, bool decode_e,
+// correction to x on read (x is never written here; the aggregate kernel
+// materializes it).  decode_e: apply the pending worker corrections to e on
+// read.  average: replace every e[k] by the mean and write it back (plain).
+// xh written when non-null (required unless average).
+hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
+                             const uint64_t* srv_signs, const float* srv_scales, bool decode_x,
+                             float* e, const uint64_t* signs, const float* scales, bool decode_e,
                              bool average, float* xh, hipStream_t s);
 
 // Apply pending corrections: e_out[k] = e[k] - c_k for k < K (when e_out),

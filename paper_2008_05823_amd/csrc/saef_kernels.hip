@@ -1,28 +1,29 @@
 // HIP kernels for the SAEF round on gfx950 (CDNA4, wave64).
 //
-// Work decomposition: a layout is cut into tiles of at most a few thousand
-// elements of one tensor (tile starts are multiples of 64, so one 64-bit sign
-// word never spans two tiles).  Inside a tile, wave w handles 64-element
-// words w*U .. w*U+U-1, then strides by 4*U words; lane i of a wave owns
-// element 64*word + i, so every global load/store of a wave is one contiguous
-// 256-byte segment and the sign word of those 64 elements is a single
-// wave-wide ballot.  Value buffers are streamed with non-temporal loads and
-// stores: nothing is re-read soon enough to profit from the caches.
+// Work decomposition: a layout is cut into tiles of 1024 elements of one
+// tensor (more for very large tensors; tile starts are multiples of 64, so a
+// 64-bit sign word never spans two tiles).  Lane i of a wave owns element
+// 64*word + i of the 64-element words it processes, so every global load or
+// store of a wave is one contiguous 256-byte segment and the sign word of
+// those 64 elements is a single wave-wide ballot.  Value buffers are
+// streamed with non-temporal loads and stores (nothing is re-read soon
+// enough to profit from the caches), except x, which the K workers of a
+// tile read through the L2 of one XCD.
 //
-// Layer-wise scale (Eq. (2), one scale per tensor): every workgroup reduces
-// the exact integer sum of floor(|v| 2^80) over its tile and stores it as a
-// 128-bit partial (plain stores, no cross-workgroup atomics: on a multi-XCD
-// part those go to memory-side atomics and serialise).  A small finalize
-// kernel then adds the partials of each tensor and converts the total into
-// the fp32 scale.  Integer addition is associative, so the scale does not
-// depend on the tiling or on the order of anything.
+// Layer-wise scale (Eq. (2), one scale per tensor): the workgroup (or wave)
+// that owns a tile reduces the exact integer sum of floor(|v| 2^80) over it
+// and stores it as a 128-bit partial with plain stores -- no cross-workgroup
+// atomics, which on a multi-XCD part go to memory-side atomics and
+// serialise.  A small finalize kernel adds the partials of each tensor and
+// converts the total into the fp32 scale.  Integer addition is associative,
+// so the scale does not depend on the tiling or on the order of anything.
 //
 // Single pass: the error update e = Delta - C(Delta) needs the scale of the
 // whole tensor, which is known only after every tile was read.  The kernels
 // therefore store Delta (before its correction) and leave the correction
 // pending: the next kernel that reads the buffer subtracts
 // (bit ? scale : -scale) on the fly.  The materialize kernel applies the
-// pending correction for callers that want plain values.
+// pending corrections for callers that want plain values.
 #include "saef_internal.h"
 
 namespace saef {
@@ -31,12 +32,36 @@ namespace {
 typedef unsigned long long u64;
 
 constexpr uint32_t kAbsLimitBits = 0x49000000u;  // bit pattern of 2^19
-constexpr int kWPW = 16;  // words per wave held in registers by the K-worker kernels
+constexpr int kU = 4;     // words per wave per pass in the per-(tile, worker) kernels
+constexpr int kWPW = 16;  // words per wave per pass in the one-wave-per-tile kernels
+constexpr int kXcds = 8;  // MI355X: 8 XCDs, workgroups dealt round-robin
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+}
 
 __device__ __forceinline__ float ld_nt(const float* p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ void st_nt(float* p, float v) { __builtin_nontemporal_store(v, p); }
+
+// Per lane: bit `lane` of the 64-bit mask ? if1 : if0, in one VALU op
+// (v_cndmask with the mask as its lane condition).  The mask must be the
+// same in every lane (a sign word read at a wave-uniform address); it is
+// moved to scalar registers explicitly, which costs nothing when it already
+// is in one.
+__device__ __forceinline__ uint32_t sel_by_bit(u64 mask, uint32_t if1, uint32_t if0) {
+  const uint32_t mlo = __builtin_amdgcn_readfirstlane((uint32_t)mask);
+  const uint32_t mhi = __builtin_amdgcn_readfirstlane((uint32_t)(mask >> 32));
+  const u64 m = ((u64)mhi << 32) | mlo;
+  uint32_t r;
+  asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(if0), "v"(if1), "s"(m));
+  return r;
+}
+__device__ __forceinline__ float sel_by_bit(u64 mask, float if1, float if0) {
+  return __uint_as_float(sel_by_bit(mask, __float_as_uint(if1), __float_as_uint(if0)));
+}
+// The compression correction C(v)_i = bit ? scale : -scale.
+__device__ __forceinline__ float corr(u64 word, float s) { return sel_by_bit(word, s, -s); }
 
 // Adds floor(|v| * 2^80) to the 128-bit integer (hi, lo); `a` is the bit
 // pattern of |v| and must be below that of 2^19.
@@ -61,6 +86,16 @@ __device__ __forceinline__ void add_fixed(uint32_t a, u64& lo, u64& hi) {
   const u64 vhi = (q == 0) ? 0ull : ((q == 1) ? (t >> 32) : t);
   lo += vlo;
   hi += vhi + (lo < vlo ? 1ull : 0ull);
+}
+
+// Exact-sum term of one value: adds it when |v| < 2^19, else flags it.
+__device__ __forceinline__ void sum_abs(float v, u64& lo, u64& hi, bool& bad) {
+  const uint32_t a = __float_as_uint(v) & 0x7FFFFFFFu;
+  if (a < kAbsLimitBits) {
+    add_fixed(a, lo, hi);
+  } else {
+    bad = true;  // |v| >= 2^19, Inf or NaN
+  }
 }
 
 __device__ __forceinline__ void add128(u64& lo, u64& hi, u64 olo, u64 ohi) {
@@ -104,20 +139,25 @@ __device__ float scale_from_sum(u64 hi, u64 lo, int64_t n) {
   return (float)(mean * 0x1p-80);
 }
 
-__device__ __forceinline__ float corr(bool bit, float s) { return bit ? s : -s; }
-
-// The 32-bit half of the sign word at p that holds bit `lane` (a per-lane
-// load: one VGPR per word instead of a scalar register pair).
-__device__ __forceinline__ uint32_t half_word(const uint64_t* p, int lane) {
-  return reinterpret_cast<const uint32_t*>(p)[lane >> 5];
-}
-__device__ __forceinline__ bool half_bit(uint32_t h, int lane) {
-  return ((h >> (lane & 31)) & 1u) != 0;
+// (1/K) * acc, binary64; inv_k is 1/K when K is a power of two (exact), else 0.
+__device__ __forceinline__ double mean_of(double acc, double inv_k, int K) {
+  return (inv_k != 0.0) ? acc * inv_k : acc / (double)K;
 }
 
-// Adds up the per-lane exact sums of the workgroup and stores the total as
-// the partial of (row, tile); raises the range flag if any lane saw a value
-// outside the exact-sum range.
+// Stores the exact partial of (row, tile) summed over one wave.
+__device__ __forceinline__ void wave_partial(const DevLayout& lay, int row, int64_t tile, u64 lo,
+                                             u64 hi, bool bad) {
+  wave_sum128(lo, hi);
+  const bool any_bad = __ballot(bad) != 0;
+  if (lane_id() == 0) {
+    u64* p = lay.part + ((int64_t)row * lay.n_tiles + tile) * 2;
+    p[0] = lo;
+    p[1] = hi;
+    if (any_bad) atomicOr(lay.status, kStatusRange);
+  }
+}
+
+// Stores the exact partial of (row, tile) summed over the workgroup.
 __device__ void block_partial(const DevLayout& lay, int row, int64_t tile, u64 lo, u64 hi,
                               bool bad) {
   __shared__ u64 s_lo[kWaves];
@@ -139,72 +179,85 @@ __device__ void block_partial(const DevLayout& lay, int row, int64_t tile, u64 l
 }
 
 // ------------------------------------------------------------------ compress
-// Grid: n_tiles * K workgroups, workgroup b handles worker b % K of tile b / K.
+// kU words of one worker's tile starting at word w0: Delta = fma(lr, g, e)
+// (e decoded when kDecode), sign words by ballot, exact-sum terms, Delta
+// stored.  kFull: all kU words are whole words of the tile (no guards).
+template <bool kDecode, bool kFull>
+__device__ __forceinline__ void compress_words(int w0, int nw, int count, float lr,
+                                               const float* __restrict__ gk,
+                                               float* __restrict__ ek,
+                                               uint64_t* __restrict__ sk, float s_old, u64& lo,
+                                               u64& hi, bool& bad) {
+  const int lane = lane_id();
+  float gv[kU], ev[kU];
+  u64 ow[kU];
+#pragma unroll
+  for (int u = 0; u < kU; ++u) {
+    const int j = (w0 + u) * 64 + lane;
+    const bool ok = kFull || ((w0 + u < nw) && j < count);
+    gv[u] = ok ? ld_nt(gk + j) : 0.0f;
+    ev[u] = ok ? ld_nt(ek + j) : 0.0f;
+    ow[u] = (kDecode && (kFull || w0 + u < nw)) ? sk[w0 + u] : 0ull;
+  }
+#pragma unroll
+  for (int u = 0; u < kU; ++u) {
+    const int w = w0 + u;
+    if (!kFull && w >= nw) continue;
+    const int j = w * 64 + lane;
+    const bool ok = kFull || j < count;
+    float ev2 = ev[u];
+    if (kDecode) ev2 = ev2 - corr(ow[u], s_old);
+    // Delta^(k) = e^(k) + lr * g^(k), one rounding
+    const float p = __builtin_fmaf(lr, gv[u], ev2);
+    const u64 word = __ballot(ok && p >= 0.0f);
+    if (lane == 0) sk[w] = word;
+    if (ok) {
+      sum_abs(p, lo, hi, bad);
+      st_nt(ek + j, p);
+    }
+  }
+}
+
+// Grid: n_tiles * K workgroups; workgroup b handles worker b % K of tile
+// b / K.  Wave w takes words w*kU .. w*kU+kU-1 of the tile, then strides by
+// 4*kU words.
 template <bool kDecode>
 __global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float lr,
                                                      const float* __restrict__ g,
                                                      float* __restrict__ e,
                                                      uint64_t* __restrict__ signs,
                                                      const float* __restrict__ scales) {
-  constexpr int U = 4;
-  const int64_t b = blockIdx.x;
-  const int k = (int)(b % K);
-  const int64_t ti = b / K;
+  const unsigned b = blockIdx.x;
+  const int k = (int)(b % (unsigned)K);
+  const int64_t ti = b / (unsigned)K;
   const Tile tile = lay.tiles[ti];
-  const int l = tile.l;
-  const int lane = lane_id();
-  const int wave = threadIdx.x / kWave;
+  const int wave = wave_id();
   const int64_t row = (int64_t)k * lay.d_pad + tile.start;
   const float* gk = g + row;
   float* ek = e + row;
   uint64_t* sk = signs + (int64_t)k * (lay.d_pad >> 6) + (tile.start >> 6);
-  const float s_old = kDecode ? scales[(int64_t)k * lay.L + l] : 0.0f;
+  const float s_old = kDecode ? scales[(int64_t)k * lay.L + tile.l] : 0.0f;
   const int nw = (tile.count + 63) >> 6;
 
   u64 lo = 0, hi = 0;
   bool bad = false;
-  for (int w0 = wave * U; w0 < nw; w0 += kWaves * U) {
-    float gv[U], ev[U];
-    uint32_t ow[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int j = (w0 + u) * 64 + lane;
-      const bool ok = (w0 + u < nw) && j < tile.count;
-      gv[u] = ok ? ld_nt(gk + j) : 0.0f;
-      ev[u] = ok ? ld_nt(ek + j) : 0.0f;
-      ow[u] = (kDecode && w0 + u < nw) ? half_word(sk + w0 + u, lane) : 0u;
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int w = w0 + u;
-      if (w >= nw) break;
-      const int j = w * 64 + lane;
-      const bool ok = j < tile.count;
-      float ev2 = ev[u];
-      if (kDecode) ev2 = ev2 - corr(half_bit(ow[u], lane), s_old);
-      // Delta^(k) = e^(k) + lr * g^(k), one rounding
-      const float p = __builtin_fmaf(lr, gv[u], ev2);
-      const u64 word = __ballot(ok && p >= 0.0f);
-      if (lane == 0) sk[w] = word;
-      if (ok) {
-        const uint32_t a = __float_as_uint(p) & 0x7FFFFFFFu;
-        if (a < kAbsLimitBits) {
-          add_fixed(a, lo, hi);
-        } else {
-          bad = true;
-        }
-        st_nt(ek + j, p);
-      }
+  for (int w0 = wave * kU; w0 < nw; w0 += kWaves * kU) {
+    if ((w0 + kU) * 64 <= tile.count) {
+      compress_words<kDecode, true>(w0, nw, tile.count, lr, gk, ek, sk, s_old, lo, hi, bad);
+    } else {
+      compress_words<kDecode, false>(w0, nw, tile.count, lr, gk, ek, sk, s_old, lo, hi, bad);
     }
   }
   block_partial(lay, k, ti, lo, hi, bad);
 }
 
 // ------------------------------------------------------------------ finalize
-// Grid: rows * L single-wave workgroups; workgroup b adds the tile partials
-// of tensor b % L for row b / L (or the server row) and writes the scale.
-__global__ __launch_bounds__(kWave) void k_finalize(DevLayout lay, int server,
-                                                    float* __restrict__ scales) {
+// Grid: rows * L workgroups; workgroup b adds the tile partials of tensor
+// b % L for row b / L (or the server row) and writes the scale.
+__global__ __launch_bounds__(kBlock) void k_finalize(DevLayout lay, int server,
+                                                     float* __restrict__ scales) {
+  __shared__ u64 s_lo[kWaves];
+  __shared__ u64 s_hi[kWaves];
   const int64_t b = blockIdx.x;
   const int l = (int)(b % lay.L);
   const int r = (int)(b / lay.L);
@@ -212,79 +265,258 @@ __global__ __launch_bounds__(kWave) void k_finalize(DevLayout lay, int server,
   const TensorInfo t = lay.tensors[l];
   const u64* p = lay.part + ((int64_t)row * lay.n_tiles + t.first_tile) * 2;
   u64 lo = 0, hi = 0;
-  for (int i = threadIdx.x; i < t.ntiles; i += kWave) add128(lo, hi, p[2 * i], p[2 * i + 1]);
+  for (int i = threadIdx.x; i < t.ntiles; i += kBlock) add128(lo, hi, p[2 * i], p[2 * i + 1]);
   wave_sum128(lo, hi);
-  if (threadIdx.x == 0) scales[server ? l : (int64_t)r * lay.L + l] = scale_from_sum(hi, lo, t.n);
+  const int w = threadIdx.x / kWave;
+  if (lane_id() == 0) {
+    s_lo[w] = lo;
+    s_hi[w] = hi;
+  }
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  u64 tlo = 0, thi = 0;
+  for (int i = 0; i < kWaves; ++i) add128(tlo, thi, s_lo[i], s_hi[i]);
+  scales[server ? l : (int64_t)r * lay.L + l] = scale_from_sum(thi, tlo, t.n);
+}
+
+// ------------------------------------------------------------------ step ahead
+// kU words of one worker's tile starting at word w0: x^(k)_{t+1/2} = x_t -
+// e^(k)_t with the pending corrections of x and e applied on the fly.
+// kFull: all kU words are whole words of the tile (no guards).
+template <bool kDecX, bool kDecE, bool kFull>
+__device__ __forceinline__ void step_words(int w0, int nw, int count,
+                                           const float* __restrict__ xt,
+                                           const float* __restrict__ ek, float* __restrict__ hk,
+                                           const uint64_t* __restrict__ sx,
+                                           const uint64_t* __restrict__ sk, float s_x,
+                                           float s_e) {
+  const int lane = lane_id();
+  float xv[kU], ev[kU];
+  u64 mx[kU], me[kU];
+#pragma unroll
+  for (int u = 0; u < kU; ++u) {
+    const int j = (w0 + u) * 64 + lane;
+    const bool ok = kFull || ((w0 + u < nw) && j < count);
+    xv[u] = ok ? xt[j] : 0.0f;
+    ev[u] = ok ? ld_nt(ek + j) : 0.0f;
+    mx[u] = (kDecX && (kFull || w0 + u < nw)) ? sx[w0 + u] : 0ull;
+    me[u] = (kDecE && (kFull || w0 + u < nw)) ? sk[w0 + u] : 0ull;
+  }
+#pragma unroll
+  for (int u = 0; u < kU; ++u) {
+    const int j = (w0 + u) * 64 + lane;
+    if (!kFull && w0 + u >= nw) continue;
+    float xc = xv[u], ec = ev[u];
+    if (kDecX) xc = xc - corr(mx[u], s_x);  // x_t = x_{t-1} - C(Delta_t)
+    if (kDecE) ec = ec - corr(me[u], s_e);  // e_t = Delta - C(Delta)
+    if (kFull || j < count) st_nt(hk + j, xc - ec);  // x^(k)_{t+1/2} = x_t - e^(k)_t
+  }
+}
+
+// Grid: ceil(n_tiles / 8) * 8 * K workgroups, one per (tile, worker).  The K
+// workgroups of a tile are consecutive in dispatch order on one XCD
+// (workgroups go to the XCDs round-robin), so x is fetched from HBM once and
+// re-read from that XCD's L2.  x itself is not written: the pending
+// re-update of x is applied here on the fly and materialized by the
+// aggregate kernel.
+template <bool kDecX, bool kDecE>
+__global__ __launch_bounds__(kBlock) void k_step(DevLayout lay, int K, const float* __restrict__ x,
+                                                 const uint64_t* __restrict__ ss,
+                                                 const float* __restrict__ sscales,
+                                                 const float* __restrict__ e,
+                                                 const uint64_t* __restrict__ signs,
+                                                 const float* __restrict__ scales,
+                                                 float* __restrict__ xh) {
+  const unsigned b = blockIdx.x;
+  const unsigned r = b / kXcds;
+  const int k = (int)(r % (unsigned)K);
+  const int64_t ti = (int64_t)(r / (unsigned)K) * kXcds + (b % kXcds);
+  if (ti >= lay.n_tiles) return;
+  const Tile tile = lay.tiles[ti];
+  const int wave = wave_id();
+  const int64_t d_pad = lay.d_pad;
+  const int64_t gw0 = tile.start >> 6;
+  const float* ek = e + (int64_t)k * d_pad + tile.start;
+  float* hk = xh + (int64_t)k * d_pad + tile.start;
+  const float* xt = x + tile.start;
+  const uint64_t* sk = signs + (int64_t)k * (d_pad >> 6) + gw0;
+  const uint64_t* sx = ss + gw0;
+  const float s_e = kDecE ? scales[(int64_t)k * lay.L + tile.l] : 0.0f;
+  const float s_x = kDecX ? sscales[tile.l] : 0.0f;
+  const int nw = (tile.count + 63) >> 6;
+  for (int w0 = wave * kU; w0 < nw; w0 += kWaves * kU) {
+    if ((w0 + kU) * 64 <= tile.count) {
+      step_words<kDecX, kDecE, true>(w0, nw, tile.count, xt, ek, hk, sx, sk, s_x, s_e);
+    } else {
+      step_words<kDecX, kDecE, false>(w0, nw, tile.count, xt, ek, hk, sx, sk, s_x, s_e);
+    }
+  }
+}
+
+// ------------------------------------------------------------------ step ahead with averaging
+// One pass of a wave over kN words (elements base + 64 u) of a tile: the
+// local errors of all K workers are read in order and replaced by their
+// mean (binary64 sum in worker order), then x^(k)_{t+1/2} = x_t - mean.
+// kFull: all kN words lie inside the tile; otherwise element base + 64 u
+// exists iff 64 u < lim (kN is then 1).
+template <bool kDecX, bool kDecE, bool kXh, bool kFull, int kN>
+__device__ __forceinline__ void average_pass(const DevLayout& lay, int K, double inv_k, int l,
+                                             int64_t base, int64_t gw, int lim,
+                                             const float* __restrict__ x,
+                                             const uint64_t* __restrict__ ss, float s_x,
+                                             float* __restrict__ e,
+                                             const uint64_t* __restrict__ signs,
+                                             const float* __restrict__ scales,
+                                             float* __restrict__ xh) {
+  const int64_t d_pad = lay.d_pad;
+  const int64_t W = d_pad >> 6;
+  double acc[kN];
+#pragma unroll
+  for (int u = 0; u < kN; ++u) acc[u] = 0.0;
+  for (int k = 0; k < K; ++k) {
+    const float* ek = e + (int64_t)k * d_pad + base;
+    const uint64_t* sk = signs + (int64_t)k * W + gw;
+    const float s = kDecE ? scales[(int64_t)k * lay.L + l] : 0.0f;
+    float ev[kN];
+    u64 m[kN];
+#pragma unroll
+    for (int u = 0; u < kN; ++u) {
+      ev[u] = (kFull || u * 64 < lim) ? ld_nt(ek + u * 64) : 0.0f;
+      m[u] = kDecE ? sk[u] : 0ull;
+    }
+#pragma unroll
+    for (int u = 0; u < kN; ++u) {
+      if (kDecE) ev[u] = ev[u] - corr(m[u], s);
+      acc[u] += (double)ev[u];
+    }
+  }
+  float mean[kN], xv[kN];
+#pragma unroll
+  for (int u = 0; u < kN; ++u) {
+    mean[u] = (float)mean_of(acc[u], inv_k, K);
+    xv[u] = 0.0f;
+    if (kXh) {
+      const u64 m = kDecX ? ss[gw + u] : 0ull;
+      if (kFull || u * 64 < lim) xv[u] = x[base + u * 64];
+      if (kDecX) xv[u] = xv[u] - corr(m, s_x);
+    }
+  }
+  for (int k = 0; k < K; ++k) {
+    float* ek = e + (int64_t)k * d_pad + base;
+    float* hk = xh + (int64_t)k * d_pad + base;
+#pragma unroll
+    for (int u = 0; u < kN; ++u) {
+      if (kFull || u * 64 < lim) {
+        st_nt(ek + u * 64, mean[u]);
+        if (kXh) st_nt(hk + u * 64, xv[u] - mean[u]);
+      }
+    }
+  }
+}
+
+// Grid: ceil(n_tiles / 4) workgroups; wave w of workgroup b owns tile 4b + w.
+template <bool kDecX, bool kDecE, bool kXh>
+__global__ __launch_bounds__(kBlock) void k_step_average(DevLayout lay, int K, double inv_k,
+                                                         const float* __restrict__ x,
+                                                         const uint64_t* __restrict__ ss,
+                                                         const float* __restrict__ sscales,
+                                                         float* __restrict__ e,
+                                                         const uint64_t* __restrict__ signs,
+                                                         const float* __restrict__ scales,
+                                                         float* __restrict__ xh) {
+  const int64_t ti = (int64_t)blockIdx.x * kWaves + wave_id();
+  if (ti >= lay.n_tiles) return;
+  const Tile tile = lay.tiles[ti];
+  const int lane = lane_id();
+  const int nw = (tile.count + 63) >> 6;
+  const float s_x = kDecX ? sscales[tile.l] : 0.0f;
+  for (int wb = 0; wb < nw; wb += kWPW) {
+    const int64_t base = tile.start + wb * 64 + lane;
+    const int64_t gw = (tile.start >> 6) + wb;
+    if ((wb + kWPW) * 64 <= tile.count) {
+      average_pass<kDecX, kDecE, kXh, true, kWPW>(lay, K, inv_k, tile.l, base, gw, 0, x, ss,
+                                                  s_x, e, signs, scales, xh);
+    } else {
+      // tail of the tile: one word at a time, guarded per lane
+      for (int u = 0; u < min(kWPW, nw - wb); ++u) {
+        average_pass<kDecX, kDecE, kXh, false, 1>(lay, K, inv_k, tile.l, base + u * 64, gw + u,
+                                                  tile.count - (wb + u) * 64 - lane, x, ss, s_x,
+                                                  e, signs, scales, xh);
+      }
+    }
+  }
 }
 
 // ------------------------------------------------------------------ aggregate
-// One pass of a wave over kWPW words (elements base + 64 u, u < kWPW) of a
-// tile: the wave holds the words in registers and walks the K worker
-// messages in order, mean = (sum_k +-scale_k in binary64, k order) / K.
-// kFull: all kWPW words lie inside the tile (no per-lane guards); otherwise
-// only the first nv words are present and element base + 64 u exists iff
-// 64 u < lim.
+// One pass of a wave over kN words of a tile: the K worker messages are
+// decoded in order, mean = (sum_k +-scale_k in binary64, k order) / K.
+// Same kFull / lim conventions as average_pass.
 template <int kMode, bool kDecode, bool kAvg, bool kFull, int kN>
 __device__ __forceinline__ void aggregate_pass(const DevLayout& lay, int K, double inv_k, int l,
-                                               int64_t base, int64_t gw, int nv, int lim,
+                                               int64_t base, int64_t gw, int lim,
                                                const uint64_t* __restrict__ signs,
                                                const float* __restrict__ scales,
                                                float* __restrict__ avg, float* __restrict__ es,
-                                               uint64_t* __restrict__ ss, float s_srv_old,
+                                               uint64_t* __restrict__ ss, float s_old,
                                                float* __restrict__ x, u64& lo, u64& hi,
                                                bool& bad) {
   const int lane = lane_id();
   const int64_t W = lay.d_pad >> 6;
-  float v[kN];
+  constexpr bool kUpdX = kMode == 0 || kDecode;  // x is read and written
+  float ev[kN], xv[kN];
+  u64 mo[kN];
 #pragma unroll
   for (int u = 0; u < kN; ++u) {
-    v[u] = 0.0f;
-    if (kFull || (u < nv && u * 64 < lim))
-      v[u] = (kMode == 1) ? ld_nt(es + base + u * 64) : ld_nt(x + base + u * 64);
+    const bool ok = kFull || u * 64 < lim;
+    ev[u] = (kMode == 1 && ok) ? ld_nt(es + base + u * 64) : 0.0f;
+    xv[u] = (kUpdX && ok) ? ld_nt(x + base + u * 64) : 0.0f;
+    mo[u] = (kMode == 1 && kDecode) ? ss[gw + u] : 0ull;
   }
   double acc[kN];
 #pragma unroll
   for (int u = 0; u < kN; ++u) acc[u] = 0.0;
   for (int k = 0; k < K; ++k) {
+    // +-scale_k in binary64: the two values differ only in the sign bit
     const double sd = (double)scales[(int64_t)k * lay.L + l];
+    const uint32_t pos_hi = (uint32_t)__double2hiint(sd);
+    const uint32_t lo_bits = (uint32_t)__double2loint(sd);
+    const uint32_t neg_hi = pos_hi ^ 0x80000000u;
     const uint64_t* sk = signs + (int64_t)k * W + gw;
-    uint32_t hw[kN];
+    u64 m[kN];
 #pragma unroll
-    for (int u = 0; u < kN; ++u) hw[u] = (kFull || u < nv) ? half_word(sk + u, lane) : 0u;
+    for (int u = 0; u < kN; ++u) m[u] = sk[u];
 #pragma unroll
-    for (int u = 0; u < kN; ++u) acc[u] += half_bit(hw[u], lane) ? sd : -sd;
+    for (int u = 0; u < kN; ++u)
+      acc[u] += __hiloint2double((int)sel_by_bit(m[u], pos_hi, neg_hi), (int)lo_bits);
   }
 #pragma unroll
   for (int u = 0; u < kN; ++u) {
-    if (!kFull && u >= nv) continue;
     const bool ok = kFull || u * 64 < lim;
-    const float mean = (inv_k != 0.0) ? (float)(acc[u] * inv_k) : (float)(acc[u] / (double)K);
+    const float mean = (float)mean_of(acc[u], inv_k, K);
     const int64_t i = base + u * 64;
     if (kAvg && ok) avg[i] = mean;
     if (kMode == 1) {
-      float ev = v[u];
-      if (kDecode) ev = ev - corr(half_bit(half_word(ss + gw + u, lane), lane), s_srv_old);
-      // Delta = e + (1/K) sum_k C(Delta^(k))
-      const float D = ev + mean;
+      float evc = ev[u];
+      if (kDecode) {
+        const float c = corr(mo[u], s_old);
+        evc = evc - c;                    // e_t = Delta_t - C(Delta_t)
+        if (ok) st_nt(x + i, xv[u] - c);  // re-update x_t = x_{t-1} - C(Delta_t)
+      }
+      // Delta_{t+1} = e_t + (1/K) sum_k C(Delta^(k))
+      const float D = evc + mean;
       const u64 word = __ballot(ok && D >= 0.0f);
       if (lane == 0) ss[gw + u] = word;
       if (ok) {
-        const uint32_t a = __float_as_uint(D) & 0x7FFFFFFFu;
-        if (a < kAbsLimitBits) {
-          add_fixed(a, lo, hi);
-        } else {
-          bad = true;
-        }
+        sum_abs(D, lo, hi, bad);
         st_nt(es + i, D);
       }
     } else if (ok) {
-      st_nt(x + i, v[u] - mean);  // single-way: the mean itself comes back
+      st_nt(x + i, xv[u] - mean);  // single-way: the mean itself comes back
     }
   }
 }
 
-// Grid: n_tiles workgroups; wave w takes passes of kWPW words starting at
-// word w*kWPW, striding by 4*kWPW words.
+// Grid: ceil(n_tiles / 4) workgroups; wave w of workgroup b owns tile 4b + w.
 template <int kMode, bool kDecode, bool kAvg>
 __global__ __launch_bounds__(kBlock) void k_aggregate(DevLayout lay, int K, double inv_k,
                                                       const uint64_t* __restrict__ signs,
@@ -294,159 +526,31 @@ __global__ __launch_bounds__(kBlock) void k_aggregate(DevLayout lay, int K, doub
                                                       uint64_t* __restrict__ ss,
                                                       const float* __restrict__ sscales,
                                                       float* __restrict__ x) {
-  const int64_t ti = blockIdx.x;
+  const int64_t ti = (int64_t)blockIdx.x * kWaves + wave_id();
+  if (ti >= lay.n_tiles) return;
   const Tile tile = lay.tiles[ti];
-  const int l = tile.l;
   const int lane = lane_id();
-  const int wave = threadIdx.x / kWave;
   const int nw = (tile.count + 63) >> 6;
-  const float s_srv_old = (kMode == 1 && kDecode) ? sscales[l] : 0.0f;
+  const float s_old = (kMode == 1 && kDecode) ? sscales[tile.l] : 0.0f;
   u64 lo = 0, hi = 0;
   bool bad = false;
-  for (int wb = wave * kWPW; wb < nw; wb += kWaves * kWPW) {
+  for (int wb = 0; wb < nw; wb += kWPW) {
     const int64_t base = tile.start + wb * 64 + lane;
     const int64_t gw = (tile.start >> 6) + wb;
     if ((wb + kWPW) * 64 <= tile.count) {
-      aggregate_pass<kMode, kDecode, kAvg, true, kWPW>(lay, K, inv_k, l, base, gw, kWPW, 0, signs,
-                                                       scales, avg, es, ss, s_srv_old, x, lo, hi,
+      aggregate_pass<kMode, kDecode, kAvg, true, kWPW>(lay, K, inv_k, tile.l, base, gw, 0, signs,
+                                                       scales, avg, es, ss, s_old, x, lo, hi,
                                                        bad);
     } else {
       // tail of the tile: one word at a time, guarded per lane
-      const int nv = min(kWPW, nw - wb);
-      for (int u = 0; u < nv; ++u) {
+      for (int u = 0; u < min(kWPW, nw - wb); ++u) {
         aggregate_pass<kMode, kDecode, kAvg, false, 1>(
-            lay, K, inv_k, l, base + u * 64, gw + u, 1, tile.count - (wb + u) * 64 - lane,
-            signs, scales, avg, es, ss, s_srv_old, x, lo, hi, bad);
+            lay, K, inv_k, tile.l, base + u * 64, gw + u, tile.count - (wb + u) * 64 - lane,
+            signs, scales, avg, es, ss, s_old, x, lo, hi, bad);
       }
     }
   }
-  if (kMode == 1) block_partial(lay, lay.k_max, ti, lo, hi, bad);
-}
-
-// ------------------------------------------------------------------ step ahead
-// One pass over kWPW words of a tile (same conventions as aggregate_pass):
-// x is read once into registers, then the K workers are walked in order.
-template <bool kDecX, bool kDecE, bool kAverage, bool kXh, bool kFull, int kN>
-__device__ __forceinline__ void step_pass(const DevLayout& lay, int K, double inv_k, int l,
-                                          int64_t base, int64_t gw, int nv, int lim,
-                                          float* __restrict__ x, const uint64_t* __restrict__ ss,
-                                          float s_srv, float* __restrict__ e,
-                                          const uint64_t* __restrict__ signs,
-                                          const float* __restrict__ scales,
-                                          float* __restrict__ xh) {
-  const int lane = lane_id();
-  const int64_t d_pad = lay.d_pad;
-  const int64_t W = d_pad >> 6;
-  float xv[kN];
-#pragma unroll
-  for (int u = 0; u < kN; ++u) {
-    xv[u] = 0.0f;
-    if ((kXh || kDecX) && (kFull || (u < nv && u * 64 < lim))) xv[u] = ld_nt(x + base + u * 64);
-  }
-  if (kDecX) {
-#pragma unroll
-    for (int u = 0; u < kN; ++u) {
-      if (!kFull && u >= nv) continue;
-      // pending re-update x <- x - C(Delta) of the previous iteration
-      xv[u] = xv[u] - corr(half_bit(half_word(ss + gw + u, lane), lane), s_srv);
-      if (kFull || u * 64 < lim) st_nt(x + base + u * 64, xv[u]);
-    }
-  }
-  if (kAverage) {
-    // e^(k) <- (1/K) sum_k e^(k), binary64 sum in worker order
-    double acc[kN];
-#pragma unroll
-    for (int u = 0; u < kN; ++u) acc[u] = 0.0;
-    for (int k = 0; k < K; ++k) {
-      const float* ek = e + (int64_t)k * d_pad + base;
-      const uint64_t* sk = signs + (int64_t)k * W + gw;
-      const float s = kDecE ? scales[(int64_t)k * lay.L + l] : 0.0f;
-      float ev[kN];
-      uint32_t hw[kN];
-#pragma unroll
-      for (int u = 0; u < kN; ++u) {
-        ev[u] = 0.0f;
-        if (kFull || (u < nv && u * 64 < lim)) ev[u] = ld_nt(ek + u * 64);
-        hw[u] = (kDecE && (kFull || u < nv)) ? half_word(sk + u, lane) : 0u;
-      }
-#pragma unroll
-      for (int u = 0; u < kN; ++u) {
-        if (kDecE) ev[u] = ev[u] - corr(half_bit(hw[u], lane), s);
-        acc[u] += (double)ev[u];
-      }
-    }
-    float m[kN];
-#pragma unroll
-    for (int u = 0; u < kN; ++u)
-      m[u] = (inv_k != 0.0) ? (float)(acc[u] * inv_k) : (float)(acc[u] / (double)K);
-    for (int k = 0; k < K; ++k) {
-      float* ek = e + (int64_t)k * d_pad + base;
-      float* hk = xh + (int64_t)k * d_pad + base;
-#pragma unroll
-      for (int u = 0; u < kN; ++u) {
-        if (kFull || (u < nv && u * 64 < lim)) {
-          st_nt(ek + u * 64, m[u]);
-          if (kXh) st_nt(hk + u * 64, xv[u] - m[u]);
-        }
-      }
-    }
-  } else if (kXh) {
-    // x^(k)_{t+1/2} = x_t - e^(k)_t
-    for (int k = 0; k < K; ++k) {
-      const float* ek = e + (int64_t)k * d_pad + base;
-      float* hk = xh + (int64_t)k * d_pad + base;
-      const uint64_t* sk = signs + (int64_t)k * W + gw;
-      const float s = kDecE ? scales[(int64_t)k * lay.L + l] : 0.0f;
-      float ev[kN];
-      uint32_t hw[kN];
-#pragma unroll
-      for (int u = 0; u < kN; ++u) {
-        ev[u] = 0.0f;
-        if (kFull || (u < nv && u * 64 < lim)) ev[u] = ld_nt(ek + u * 64);
-        hw[u] = (kDecE && (kFull || u < nv)) ? half_word(sk + u, lane) : 0u;
-      }
-#pragma unroll
-      for (int u = 0; u < kN; ++u) {
-        if (kDecE) ev[u] = ev[u] - corr(half_bit(hw[u], lane), s);
-        if (kFull || (u < nv && u * 64 < lim)) st_nt(hk + u * 64, xv[u] - ev[u]);
-      }
-    }
-  }
-}
-
-// Grid: n_tiles workgroups, each handles all K workers of its tile so x is
-// read once.
-template <bool kDecX, bool kDecE, bool kAverage, bool kXh>
-__global__ __launch_bounds__(kBlock) void k_step_ahead(DevLayout lay, int K, double inv_k,
-                                                       float* __restrict__ x,
-                                                       const uint64_t* __restrict__ ss,
-                                                       const float* __restrict__ sscales,
-                                                       float* __restrict__ e,
-                                                       const uint64_t* __restrict__ signs,
-                                                       const float* __restrict__ scales,
-                                                       float* __restrict__ xh) {
-  const Tile tile = lay.tiles[blockIdx.x];
-  const int l = tile.l;
-  const int lane = lane_id();
-  const int wave = threadIdx.x / kWave;
-  const int nw = (tile.count + 63) >> 6;
-  const float s_srv = kDecX ? sscales[l] : 0.0f;
-  for (int wb = wave * kWPW; wb < nw; wb += kWaves * kWPW) {
-    const int64_t base = tile.start + wb * 64 + lane;
-    const int64_t gw = (tile.start >> 6) + wb;
-    if ((wb + kWPW) * 64 <= tile.count) {
-      step_pass<kDecX, kDecE, kAverage, kXh, true, kWPW>(lay, K, inv_k, l, base, gw, kWPW, 0, x,
-                                                         ss, s_srv, e, signs, scales, xh);
-    } else {
-      // tail of the tile: one word at a time, guarded per lane
-      const int nv = min(kWPW, nw - wb);
-      for (int u = 0; u < nv; ++u) {
-        step_pass<kDecX, kDecE, kAverage, kXh, false, 1>(
-            lay, K, inv_k, l, base + u * 64, gw + u, 1, tile.count - (wb + u) * 64 - lane, x, ss,
-            s_srv, e, signs, scales, xh);
-      }
-    }
-  }
+  if (kMode == 1) wave_partial(lay, lay.k_max, ti, lo, hi, bad);
 }
 
 // ------------------------------------------------------------------ materialize
@@ -463,7 +567,7 @@ __global__ __launch_bounds__(kBlock) void k_materialize(
   const Tile tile = lay.tiles[b / rows];
   const int l = tile.l;
   const int lane = lane_id();
-  const int wave = threadIdx.x / kWave;
+  const int wave = wave_id();
   const int64_t d_pad = lay.d_pad;
   const int64_t gw0 = tile.start >> 6;
   const int nw = (tile.count + 63) >> 6;
@@ -471,21 +575,23 @@ __global__ __launch_bounds__(kBlock) void k_materialize(
     const float s = scales[(int64_t)row * lay.L + l];
     const uint64_t* sk = signs + (int64_t)row * (d_pad >> 6) + gw0;
     for (int w = wave; w < nw; w += kWaves) {
+      const u64 m = sk[w];
       const int j = w * 64 + lane;
       if (j < tile.count) {
         const int64_t i = (int64_t)row * d_pad + tile.start + j;
-        e_out[i] = e[i] - corr(half_bit(half_word(sk + w, lane), lane), s);
+        e_out[i] = e[i] - corr(m, s);
       }
     }
     return;
   }
   const float s = (mode == 1) ? sscales[l] : 0.0f;
   for (int w = wave; w < nw; w += kWaves) {
+    const u64 m = (mode == 1) ? ss[gw0 + w] : 0ull;
     const int j = w * 64 + lane;
     if (j >= tile.count) continue;
     const int64_t i = tile.start + j;
     if (mode == 1) {
-      const float c = corr(half_bit(half_word(ss + gw0 + w, lane), lane), s);
+      const float c = corr(m, s);
       if (es_out) es_out[i] = es[i] - c;
       if (x_out) x_out[i] = x[i] - c;
     } else {
@@ -496,6 +602,10 @@ __global__ __launch_bounds__(kBlock) void k_materialize(
 }
 
 double inv_pow2(int K) { return (K & (K - 1)) == 0 ? 1.0 / (double)K : 0.0; }
+
+unsigned per_wave_grid(const DevLayout& lay) {
+  return (unsigned)((lay.n_tiles + kWaves - 1) / kWaves);
+}
 
 }  // namespace
 
@@ -515,14 +625,14 @@ hipError_t launch_compress(const DevLayout& lay, int K, float lr, const float* g
 hipError_t launch_finalize(const DevLayout& lay, int K, bool server, float* scales,
                            hipStream_t s) {
   const dim3 grid((unsigned)((server ? 1 : K) * lay.L));
-  hipLaunchKernelGGL(k_finalize, grid, dim3(kWave), 0, s, lay, server ? 1 : 0, scales);
+  hipLaunchKernelGGL(k_finalize, grid, dim3(kBlock), 0, s, lay, server ? 1 : 0, scales);
   return hipGetLastError();
 }
 
 hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_t* signs,
                             const float* scales, float* avg, float* e_srv, uint64_t* srv_signs,
                             const float* srv_scales, float* x, bool decode, hipStream_t s) {
-  const dim3 grid((unsigned)lay.n_tiles);
+  const dim3 grid(per_wave_grid(lay));
   const double ik = inv_pow2(K);
 #define SAEF_AGG(M, D, A)                                                                  \
   hipLaunchKernelGGL((k_aggregate<M, D, A>), grid, dim3(kBlock), 0, s, lay, K, ik, signs, \
@@ -541,30 +651,43 @@ hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_
   return hipGetLastError();
 }
 
-hipError_t launch_step_ahead(const DevLayout& lay, int K, float* x, const uint64_t* srv_signs,
-                             const float* srv_scales, bool decode_x, float* e,
-                             const uint64_t* signs, const float* scales, bool decode_e,
+hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
+                             const uint64_t* srv_signs, const float* srv_scales, bool decode_x,
+                             float* e, const uint64_t* signs, const float* scales, bool decode_e,
                              bool average, float* xh, hipStream_t s) {
-  const dim3 grid((unsigned)lay.n_tiles);
-  const double ik = inv_pow2(K);
-#define SAEF_SA(DX, DE, AV, XH)                                                             \
-  hipLaunchKernelGGL((k_step_ahead<DX, DE, AV, XH>), grid, dim3(kBlock), 0, s, lay, K, ik, \
-                     x, srv_signs, srv_scales, e, signs, scales, xh)
-  const bool h = xh != nullptr;
-  if (!decode_x && !decode_e) {
-    if (average) {
-      if (h) SAEF_SA(false, false, true, true); else SAEF_SA(false, false, true, false);
+  if (decode_x && !decode_e) return hipErrorInvalidValue;  // never requested
+  if (average) {
+    const dim3 grid(per_wave_grid(lay));
+    const double ik = inv_pow2(K);
+#define SAEF_AV(DX, DE, XH)                                                                  \
+  hipLaunchKernelGGL((k_step_average<DX, DE, XH>), grid, dim3(kBlock), 0, s, lay, K, ik, x, \
+                     srv_signs, srv_scales, e, signs, scales, xh)
+    if (xh == nullptr) {
+      if (decode_e) return hipErrorInvalidValue;  // plain averaging only
+      SAEF_AV(false, false, false);
+    } else if (decode_x) {
+      SAEF_AV(true, true, true);
+    } else if (decode_e) {
+      SAEF_AV(false, true, true);
     } else {
-      SAEF_SA(false, false, false, true);
+      SAEF_AV(false, false, true);
     }
-  } else if (decode_x && decode_e) {
-    if (average) SAEF_SA(true, true, true, true); else SAEF_SA(true, true, false, true);
-  } else if (!decode_x && decode_e) {
-    if (average) SAEF_SA(false, true, true, true); else SAEF_SA(false, true, false, true);
+#undef SAEF_AV
   } else {
-    return hipErrorInvalidValue;  // decode_x without decode_e is never requested
+    if (xh == nullptr) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((lay.n_tiles + kXcds - 1) / kXcds * kXcds * K));
+#define SAEF_ST(DX, DE)                                                                \
+  hipLaunchKernelGGL((k_step<DX, DE>), grid, dim3(kBlock), 0, s, lay, K, x, srv_signs, \
+                     srv_scales, e, signs, scales, xh)
+    if (decode_x) {
+      SAEF_ST(true, true);
+    } else if (decode_e) {
+      SAEF_ST(false, true);
+    } else {
+      SAEF_ST(false, false);
+    }
+#undef SAEF_ST
   }
-#undef SAEF_SA
   return hipGetLastError();
 }
 

@@ -16,7 +16,8 @@ import os
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libsaef.so")
+# SAEF_LIBRARY may name another build of the library (e.g. a tuning variant)
+LIB_PATH = os.environ.get("SAEF_LIBRARY") or os.path.join(HERE, "libsaef.so")
 
 OK, EINVAL, ERANGE, EHIP = 0, -1, -2, -3
 MODE_SC, MODE_DC = 0, 1
@@ -188,7 +189,8 @@ def saef_status(layout: Layout, stream=None) -> int:
     return rc
 
 
-PROFILE_KINDS = ("step_ahead", "compress", "worker_scales", "aggregate", "server_scales")
+PROFILE_KINDS = ("step_ahead", "compress", "worker_scales", "aggregate", "server_scales",
+                 "step_ahead_averaging")
 
 
 def saef_profile_enable(layout: Layout, capacity: int) -> None:
