@@ -26,12 +26,17 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0      # MI355X HBM3E
 METRIC = "params/s per K-worker SAEF round + achieved HBM GB/s vs MI355X peak"
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2008_05823_amd", "csrc", "saef_kernels.hip")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2008_05823_amd", "csrc", f)
+                  for f in ("saef_kernels.hip", "saef_internal.h")]
 
 
 def kernel_hash() -> str:
-    with open(KERNEL_SOURCE, "rb") as fh:
-        return hashlib.sha256(fh.read()).hexdigest()[:16]
+    """Hash of the kernel sources (the counters in profiles/ apply to it only)."""
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def traffic_from_profile(workload: str):

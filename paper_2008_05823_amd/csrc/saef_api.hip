@@ -33,9 +33,9 @@ struct saef_layout {
 
 namespace {
 
-// Elements per work tile of a tensor of n elements: 4096, or more for very
-// large tensors so that no tensor has more than kMaxTilesPerTensor tiles
-// (bounds the arrivals on one accumulator).
+// Elements per work tile of a tensor of n elements: kTileElems, or more for
+// very large tensors so that no tensor has more than kMaxTilesPerTensor tiles
+// (bounds the number of partial sums the finalize kernel adds per tensor).
 int64_t tile_elems(int64_t n) {
   int64_t t = saef::kTileElems;
   if (n > t * saef::kMaxTilesPerTensor) {
