@@ -146,15 +146,17 @@ int saef_status(const saef_layout* layout, hipStream_t stream);
 
 /* Per-kernel timing of saef_round, for measurement.  saef_profile_enable
  * with capacity > 0 creates that many HIP event pairs; every later
- * saef_round on this layout then records one pair around each kernel it
- * enqueues (kind 0 = step ahead, 1 = worker compression, 2 = worker scales
- * from the tile sums, 3 = server aggregation, 4 = server scales, 5 = step
- * ahead of an error-averaging iteration) until the pairs run out.
- * saef_profile_read waits for the recorded events and returns, per kind, the
- * number of launches timed (counts[6]) and their summed durations in
- * milliseconds (total_ms[6]), then starts over with all pairs free.
- * capacity 0 releases the events and stops recording. */
-int saef_profile_enable(saef_layout* layout, int32_t capacity);
+ * saef_round on this layout then has the dispatch of each kernel whose kind
+ * bit is set in kind_mask stamp its start and end into a free pair (kind 0 =
+ * step ahead, 1 = worker compression, 2 = worker scales from the tile sums,
+ * 3 = server aggregation, 4 = server scales, 5 = step ahead of an
+ * error-averaging iteration), until the pairs run out.  saef_profile_read
+ * waits for the recorded events and returns, per kind, the number of
+ * launches timed (counts[6]) and their summed durations in milliseconds
+ * (total_ms[6]), then starts over with all pairs free.  capacity 0 releases
+ * the events and stops recording.  Timed dispatches cost a few microseconds
+ * each, so time only the kernels of interest. */
+int saef_profile_enable(saef_layout* layout, int32_t capacity, uint32_t kind_mask);
 int saef_profile_read(saef_layout* layout, int32_t* counts, double* total_ms);
 
 /* Host-side query of a layout: tensor count, padded length, worker limit and

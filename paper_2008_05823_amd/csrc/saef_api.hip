@@ -29,6 +29,7 @@ struct saef_layout {
   std::vector<hipEvent_t> ev_start, ev_stop;
   std::vector<int> ev_kind;
   size_t ev_used = 0;
+  uint32_t ev_mask = 0;  // kinds being timed
 };
 
 namespace {
@@ -78,17 +79,20 @@ void release_events(saef_layout* l) {
   l->ev_used = 0;
 }
 
-// Launches one kernel of saef_round, bracketed by an event pair when the
-// layout is being profiled and a pair is free.
+// Launches one kernel of saef_round; while the layout is being profiled and
+// an event pair is free, the dispatch stamps its start and end into the pair.
 template <typename F>
-hipError_t timed(const saef_layout* cl, int kind, hipStream_t s, F&& launch) {
+hipError_t timed(const saef_layout* cl, int kind, F&& launch) {
   saef_layout* l = const_cast<saef_layout*>(cl);
-  const bool rec = l->ev_used < l->ev_start.size();
-  if (rec && hipEventRecord(l->ev_start[l->ev_used], s) != hipSuccess) return hipErrorUnknown;
-  hipError_t err = launch();
+  saef::LaunchEvents ev;
+  const bool rec = l->ev_used < l->ev_start.size() && ((l->ev_mask >> kind) & 1u) != 0;
+  if (rec) {
+    ev.start = l->ev_start[l->ev_used];
+    ev.stop = l->ev_stop[l->ev_used];
+  }
+  hipError_t err = launch(ev);
   if (err != hipSuccess) return err;
   if (rec) {
-    if (hipEventRecord(l->ev_stop[l->ev_used], s) != hipSuccess) return hipErrorUnknown;
     l->ev_kind[l->ev_used] = kind;
     ++l->ev_used;
   }
@@ -282,28 +286,31 @@ int saef_round(const saef_layout* layout, int64_t t, int64_t period, int32_t K, 
   // error averaging (when due) and step ahead, applying last iteration's
   // pending corrections to e and (double-way) x
   const DevLayout& d = layout->dev;
-  rc = hip_rc(timed(layout, averaging ? 5 : 0, stream, [&] {
+  rc = hip_rc(timed(layout, averaging ? 5 : 0, [&](const saef::LaunchEvents& ev) {
     return saef::launch_step_ahead(d, K, x, srv_signs, srv_scales, pending && dc, e, signs,
-                                   scales, pending, averaging, xh, stream);
+                                   scales, pending, averaging, xh, stream, ev);
   }));
   if (rc != SAEF_OK) return rc;
   // [gradient slot: g was computed at xh by the caller]
   // worker compression; e is plain after an averaging step
-  rc = hip_rc(timed(layout, 1, stream, [&] {
-    return saef::launch_compress(d, K, lr, g, e, signs, scales, pending && !averaging, stream);
+  rc = hip_rc(timed(layout, 1, [&](const saef::LaunchEvents& ev) {
+    return saef::launch_compress(d, K, lr, g, e, signs, scales, pending && !averaging, stream,
+                                 ev);
   }));
   if (rc != SAEF_OK) return rc;
-  rc = hip_rc(timed(layout, 2, stream,
-                    [&] { return saef::launch_finalize(d, K, false, scales, stream); }));
+  rc = hip_rc(timed(layout, 2, [&](const saef::LaunchEvents& ev) {
+    return saef::launch_finalize(d, K, false, scales, stream, ev);
+  }));
   if (rc != SAEF_OK) return rc;
   // server aggregation, server compression; x keeps its correction pending
-  rc = hip_rc(timed(layout, 3, stream, [&] {
+  rc = hip_rc(timed(layout, 3, [&](const saef::LaunchEvents& ev) {
     return saef::launch_aggregate(d, K, mode, signs, scales, nullptr, e_srv, srv_signs,
-                                  srv_scales, x, pending && dc, stream);
+                                  srv_scales, x, pending && dc, stream, ev);
   }));
   if (rc != SAEF_OK || !dc) return rc;
-  return hip_rc(timed(layout, 4, stream,
-                      [&] { return saef::launch_finalize(d, K, true, srv_scales, stream); }));
+  return hip_rc(timed(layout, 4, [&](const saef::LaunchEvents& ev) {
+    return saef::launch_finalize(d, K, true, srv_scales, stream, ev);
+  }));
 }
 
 int saef_materialize(const saef_layout* layout, int32_t K, int32_t mode, const float* e,
@@ -326,9 +333,10 @@ int saef_materialize(const saef_layout* layout, int32_t K, int32_t mode, const f
                                          x_out, stream));
 }
 
-int saef_profile_enable(saef_layout* layout, int32_t capacity) {
+int saef_profile_enable(saef_layout* layout, int32_t capacity, uint32_t kind_mask) {
   if (layout == nullptr || capacity < 0 || capacity > (1 << 20)) return SAEF_EINVAL;
   release_events(layout);
+  layout->ev_mask = kind_mask;
   for (int32_t i = 0; i < capacity; ++i) {
     hipEvent_t a = nullptr, b = nullptr;
     if (hipEventCreate(&a) != hipSuccess) return SAEF_EHIP;

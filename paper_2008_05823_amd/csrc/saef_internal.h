@@ -48,21 +48,30 @@ struct DevLayout {
 // status flag bits
 constexpr int kStatusRange = 1;
 
+// Optional timing of one launch: when set, the kernel's dispatch packet
+// records its start and end in these events (no extra queue packets).
+struct LaunchEvents {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+
 // ---- kernel launchers (defined in saef_kernels.hip) ----------------------
 // All return hipSuccess or the launch error.  Arguments are validated by the
-// caller.
+// caller.  Each launcher enqueues exactly one kernel.
 
 // Worker compression.  decode: e holds values with a pending correction
 // (signs/scales of the previous compression) that is applied on read.
 // Always writes Delta (before correction) into e, the new sign words and the
 // tile partial sums; launch_finalize then writes the new scales.
 hipError_t launch_compress(const DevLayout& lay, int K, float lr, const float* g, float* e,
-                           uint64_t* signs, const float* scales, bool decode, hipStream_t s);
+                           uint64_t* signs, const float* scales, bool decode, hipStream_t s,
+                           const LaunchEvents& ev = LaunchEvents());
 
 // Scales from the tile partial sums: worker rows 0..K-1 into scales[k][l]
 // (server == false) or the server row into scales[l] (server == true).
 hipError_t launch_finalize(const DevLayout& lay, int K, bool server, float* scales,
-                           hipStream_t s);
+                           hipStream_t s,
+                           const LaunchEvents& ev = LaunchEvents());
 
 // Server aggregation.  mode 1: reads/writes e_srv (Delta before correction),
 // writes srv_signs and the server tile partial sums (launch_finalize then
@@ -71,7 +80,8 @@ hipError_t launch_finalize(const DevLayout& lay, int K, bool server, float* scal
 // mode 0: x <- x - mean.  avg written when non-null.
 hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_t* signs,
                             const float* scales, float* avg, float* e_srv, uint64_t* srv_signs,
-                            const float* srv_scales, float* x, bool decode, hipStream_t s);
+                            const float* srv_scales, float* x, bool decode, hipStream_t s,
+                           const LaunchEvents& ev = LaunchEvents());
 
 // Step ahead / error averaging.  decode_x: apply the pending server
 // correction to x on read (x is never written here; the aggregate kernel
@@ -81,7 +91,8 @@ hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_
 hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
                              const uint64_t* srv_signs, const float* srv_scales, bool decode_x,
                              float* e, const uint64_t* signs, const float* scales, bool decode_e,
-                             bool average, float* xh, hipStream_t s);
+                             bool average, float* xh, hipStream_t s,
+                           const LaunchEvents& ev = LaunchEvents());
 
 // Apply pending corrections: e_out[k] = e[k] - c_k for k < K (when e_out),
 // and, when e_srv_out or x_out is given, e_srv_out = e_srv - c and
@@ -90,6 +101,7 @@ hipError_t launch_materialize(const DevLayout& lay, int K, int mode, const float
                               const uint64_t* signs, const float* scales, float* e_out,
                               const float* e_srv, const float* x, const uint64_t* srv_signs,
                               const float* srv_scales, float* e_srv_out, float* x_out,
-                              hipStream_t s);
+                              hipStream_t s,
+                           const LaunchEvents& ev = LaunchEvents());
 
 }  // namespace saef

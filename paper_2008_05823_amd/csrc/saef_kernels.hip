@@ -24,6 +24,8 @@
 // pending: the next kernel that reads the buffer subtracts
 // (bit ? scale : -scale) on the fly.  The materialize kernel applies the
 // pending corrections for callers that want plain values.
+#include <hip/hip_ext.h>
+
 #include "saef_internal.h"
 
 namespace saef {
@@ -62,6 +64,16 @@ __device__ __forceinline__ float sel_by_bit(u64 mask, float if1, float if0) {
 }
 // The compression correction C(v)_i = bit ? scale : -scale.
 __device__ __forceinline__ float corr(u64 word, float s) { return sel_by_bit(word, s, -s); }
+
+// The 32-bit half of the sign word at p that holds bit `lane`, read per lane
+// (a vector register instead of a scalar pair, for kernels that keep many
+// words live), and the lane's bit in it.
+__device__ __forceinline__ uint32_t half_word(const uint64_t* p, int lane) {
+  return reinterpret_cast<const uint32_t*>(p)[lane >> 5];
+}
+__device__ __forceinline__ bool half_bit(uint32_t h, int lane) {
+  return ((h >> (lane & 31)) & 1u) != 0;
+}
 
 // Adds floor(|v| * 2^80) to the 128-bit integer (hi, lo); `a` is the bit
 // pattern of |v| and must be below that of 2^19.
@@ -354,40 +366,58 @@ __global__ __launch_bounds__(kBlock) void k_step(DevLayout lay, int K, const flo
 }
 
 // ------------------------------------------------------------------ step ahead with averaging
-// One pass of a wave over kN words (elements base + 64 u) of a tile: the
-// local errors of all K workers are read in order and replaced by their
-// mean (binary64 sum in worker order), then x^(k)_{t+1/2} = x_t - mean.
-// kFull: all kN words lie inside the tile; otherwise element base + 64 u
-// exists iff 64 u < lim (kN is then 1).
+constexpr int kAvgChunk = 4;  // workers whose loads are issued together
+
+// kN words of one tile starting at word w0, all K workers: the local errors
+// are read in worker order (pending corrections applied when kDecE) and
+// replaced by their mean (binary64 sum in worker order, /K, fp32); then
+// x^(k)_{t+1/2} = x_t - mean for every worker when kXh.  kFull: the kN
+// words are whole words of the tile; otherwise kN is 1 and the lane's
+// element exists iff `valid`.
 template <bool kDecX, bool kDecE, bool kXh, bool kFull, int kN>
-__device__ __forceinline__ void average_pass(const DevLayout& lay, int K, double inv_k, int l,
-                                             int64_t base, int64_t gw, int lim,
-                                             const float* __restrict__ x,
-                                             const uint64_t* __restrict__ ss, float s_x,
-                                             float* __restrict__ e,
-                                             const uint64_t* __restrict__ signs,
-                                             const float* __restrict__ scales,
-                                             float* __restrict__ xh) {
+__device__ __forceinline__ void average_words(const DevLayout& lay, int K, double inv_k, int l,
+                                              int w0, bool valid, int64_t start,
+                                              const float* __restrict__ x,
+                                              const uint64_t* __restrict__ ss, float s_x,
+                                              float* __restrict__ e,
+                                              const uint64_t* __restrict__ signs,
+                                              const float* __restrict__ scales,
+                                              float* __restrict__ xh) {
+  const int lane = lane_id();
   const int64_t d_pad = lay.d_pad;
   const int64_t W = d_pad >> 6;
+  const int64_t gw0 = (start >> 6) + w0;
+  const int64_t base = start + w0 * 64 + lane;
+  const bool ok = kFull || valid;
   double acc[kN];
 #pragma unroll
   for (int u = 0; u < kN; ++u) acc[u] = 0.0;
-  for (int k = 0; k < K; ++k) {
-    const float* ek = e + (int64_t)k * d_pad + base;
-    const uint64_t* sk = signs + (int64_t)k * W + gw;
-    const float s = kDecE ? scales[(int64_t)k * lay.L + l] : 0.0f;
-    float ev[kN];
-    u64 m[kN];
+  for (int k0 = 0; k0 < K; k0 += kAvgChunk) {
+    // sign words are fetched per lane as the 32-bit half holding the lane's
+    // bit (vector registers: this kernel keeps kAvgChunk * kN words live)
+    float ev[kAvgChunk][kN];
+    uint32_t hw[kAvgChunk][kN];
 #pragma unroll
-    for (int u = 0; u < kN; ++u) {
-      ev[u] = (kFull || u * 64 < lim) ? ld_nt(ek + u * 64) : 0.0f;
-      m[u] = kDecE ? sk[u] : 0ull;
+    for (int c = 0; c < kAvgChunk; ++c) {
+      const bool kin = k0 + c < K;
+      const float* ek = e + (int64_t)(k0 + c) * d_pad + base;
+      const uint64_t* sk = signs + (int64_t)(k0 + c) * W + gw0;
+#pragma unroll
+      for (int u = 0; u < kN; ++u) {
+        ev[c][u] = (kin && ok) ? ld_nt(ek + u * 64) : 0.0f;
+        hw[c][u] = (kDecE && kin) ? half_word(sk + u, lane) : 0u;
+      }
     }
 #pragma unroll
-    for (int u = 0; u < kN; ++u) {
-      if (kDecE) ev[u] = ev[u] - corr(m[u], s);
-      acc[u] += (double)ev[u];
+    for (int c = 0; c < kAvgChunk; ++c) {
+      if (k0 + c >= K) continue;
+      const float s = kDecE ? scales[(int64_t)(k0 + c) * lay.L + l] : 0.0f;
+#pragma unroll
+      for (int u = 0; u < kN; ++u) {
+        float v = ev[c][u];
+        if (kDecE) v = v - (half_bit(hw[c][u], lane) ? s : -s);
+        acc[u] += (double)v;
+      }
     }
   }
   float mean[kN], xv[kN];
@@ -396,25 +426,25 @@ __device__ __forceinline__ void average_pass(const DevLayout& lay, int K, double
     mean[u] = (float)mean_of(acc[u], inv_k, K);
     xv[u] = 0.0f;
     if (kXh) {
-      const u64 m = kDecX ? ss[gw + u] : 0ull;
-      if (kFull || u * 64 < lim) xv[u] = x[base + u * 64];
-      if (kDecX) xv[u] = xv[u] - corr(m, s_x);
+      const uint32_t hx = kDecX ? half_word(ss + gw0 + u, lane) : 0u;
+      if (ok) xv[u] = x[base + u * 64];
+      if (kDecX) xv[u] = xv[u] - (half_bit(hx, lane) ? s_x : -s_x);
     }
   }
+  if (!ok) return;
   for (int k = 0; k < K; ++k) {
     float* ek = e + (int64_t)k * d_pad + base;
     float* hk = xh + (int64_t)k * d_pad + base;
 #pragma unroll
     for (int u = 0; u < kN; ++u) {
-      if (kFull || u * 64 < lim) {
-        st_nt(ek + u * 64, mean[u]);
-        if (kXh) st_nt(hk + u * 64, xv[u] - mean[u]);
-      }
+      st_nt(ek + u * 64, mean[u]);
+      if (kXh) st_nt(hk + u * 64, xv[u] - mean[u]);
     }
   }
 }
 
-// Grid: ceil(n_tiles / 4) workgroups; wave w of workgroup b owns tile 4b + w.
+// Grid: n_tiles workgroups; wave w takes words w*kU .. w*kU+kU-1 of the tile,
+// then strides by 4*kU words.
 template <bool kDecX, bool kDecE, bool kXh>
 __global__ __launch_bounds__(kBlock) void k_step_average(DevLayout lay, int K, double inv_k,
                                                          const float* __restrict__ x,
@@ -424,24 +454,20 @@ __global__ __launch_bounds__(kBlock) void k_step_average(DevLayout lay, int K, d
                                                          const uint64_t* __restrict__ signs,
                                                          const float* __restrict__ scales,
                                                          float* __restrict__ xh) {
-  const int64_t ti = (int64_t)blockIdx.x * kWaves + wave_id();
-  if (ti >= lay.n_tiles) return;
-  const Tile tile = lay.tiles[ti];
-  const int lane = lane_id();
+  const Tile tile = lay.tiles[blockIdx.x];
+  const int wave = wave_id();
   const int nw = (tile.count + 63) >> 6;
   const float s_x = kDecX ? sscales[tile.l] : 0.0f;
-  for (int wb = 0; wb < nw; wb += kWPW) {
-    const int64_t base = tile.start + wb * 64 + lane;
-    const int64_t gw = (tile.start >> 6) + wb;
-    if ((wb + kWPW) * 64 <= tile.count) {
-      average_pass<kDecX, kDecE, kXh, true, kWPW>(lay, K, inv_k, tile.l, base, gw, 0, x, ss,
-                                                  s_x, e, signs, scales, xh);
+  for (int w0 = wave * kU; w0 < nw; w0 += kWaves * kU) {
+    if ((w0 + kU) * 64 <= tile.count) {
+      average_words<kDecX, kDecE, kXh, true, kU>(lay, K, inv_k, tile.l, w0, true, tile.start, x,
+                                                 ss, s_x, e, signs, scales, xh);
     } else {
       // tail of the tile: one word at a time, guarded per lane
-      for (int u = 0; u < min(kWPW, nw - wb); ++u) {
-        average_pass<kDecX, kDecE, kXh, false, 1>(lay, K, inv_k, tile.l, base + u * 64, gw + u,
-                                                  tile.count - (wb + u) * 64 - lane, x, ss, s_x,
-                                                  e, signs, scales, xh);
+      for (int w = w0; w < min(w0 + kU, nw); ++w) {
+        average_words<kDecX, kDecE, kXh, false, 1>(lay, K, inv_k, tile.l, w,
+                                                   w * 64 + lane_id() < tile.count, tile.start, x,
+                                                   ss, s_x, e, signs, scales, xh);
       }
     }
   }
@@ -450,7 +476,8 @@ __global__ __launch_bounds__(kBlock) void k_step_average(DevLayout lay, int K, d
 // ------------------------------------------------------------------ aggregate
 // One pass of a wave over kN words of a tile: the K worker messages are
 // decoded in order, mean = (sum_k +-scale_k in binary64, k order) / K.
-// Same kFull / lim conventions as average_pass.
+// kFull: all kN words lie inside the tile; otherwise element base + 64 u
+// exists iff 64 u < lim (kN is then 1).
 template <int kMode, bool kDecode, bool kAvg, bool kFull, int kN>
 __device__ __forceinline__ void aggregate_pass(const DevLayout& lay, int K, double inv_k, int l,
                                                int64_t base, int64_t gw, int lim,
@@ -603,6 +630,11 @@ __global__ __launch_bounds__(kBlock) void k_materialize(
 
 double inv_pow2(int K) { return (K & (K - 1)) == 0 ? 1.0 / (double)K : 0.0; }
 
+// All launches go through hipExtLaunchKernelGGL so that an optional event
+// pair is stamped by the dispatch itself.
+#define SAEF_LAUNCH(kernel, grid, block, shmem, stream, ...) \
+  hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ev.start, ev.stop, 0, __VA_ARGS__)
+
 unsigned per_wave_grid(const DevLayout& lay) {
   return (unsigned)((lay.n_tiles + kWaves - 1) / kWaves);
 }
@@ -610,32 +642,32 @@ unsigned per_wave_grid(const DevLayout& lay) {
 }  // namespace
 
 hipError_t launch_compress(const DevLayout& lay, int K, float lr, const float* g, float* e,
-                           uint64_t* signs, const float* scales, bool decode, hipStream_t s) {
+                           uint64_t* signs, const float* scales, bool decode, hipStream_t s, const LaunchEvents& ev) {
   const dim3 grid((unsigned)(lay.n_tiles * K));
   if (decode) {
-    hipLaunchKernelGGL(k_compress<true>, grid, dim3(kBlock), 0, s, lay, K, lr, g, e, signs,
+    SAEF_LAUNCH(k_compress<true>, grid, dim3(kBlock), 0, s, lay, K, lr, g, e, signs,
                        scales);
   } else {
-    hipLaunchKernelGGL(k_compress<false>, grid, dim3(kBlock), 0, s, lay, K, lr, g, e, signs,
+    SAEF_LAUNCH(k_compress<false>, grid, dim3(kBlock), 0, s, lay, K, lr, g, e, signs,
                        scales);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_finalize(const DevLayout& lay, int K, bool server, float* scales,
-                           hipStream_t s) {
+                           hipStream_t s, const LaunchEvents& ev) {
   const dim3 grid((unsigned)((server ? 1 : K) * lay.L));
-  hipLaunchKernelGGL(k_finalize, grid, dim3(kBlock), 0, s, lay, server ? 1 : 0, scales);
+  SAEF_LAUNCH(k_finalize, grid, dim3(kBlock), 0, s, lay, server ? 1 : 0, scales);
   return hipGetLastError();
 }
 
 hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_t* signs,
                             const float* scales, float* avg, float* e_srv, uint64_t* srv_signs,
-                            const float* srv_scales, float* x, bool decode, hipStream_t s) {
+                            const float* srv_scales, float* x, bool decode, hipStream_t s, const LaunchEvents& ev) {
   const dim3 grid(per_wave_grid(lay));
   const double ik = inv_pow2(K);
 #define SAEF_AGG(M, D, A)                                                                  \
-  hipLaunchKernelGGL((k_aggregate<M, D, A>), grid, dim3(kBlock), 0, s, lay, K, ik, signs, \
+  SAEF_LAUNCH((k_aggregate<M, D, A>), grid, dim3(kBlock), 0, s, lay, K, ik, signs, \
                      scales, avg, e_srv, srv_signs, srv_scales, x)
   const bool a = avg != nullptr;
   if (mode == 1) {
@@ -654,13 +686,13 @@ hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_
 hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
                              const uint64_t* srv_signs, const float* srv_scales, bool decode_x,
                              float* e, const uint64_t* signs, const float* scales, bool decode_e,
-                             bool average, float* xh, hipStream_t s) {
+                             bool average, float* xh, hipStream_t s, const LaunchEvents& ev) {
   if (decode_x && !decode_e) return hipErrorInvalidValue;  // never requested
   if (average) {
-    const dim3 grid(per_wave_grid(lay));
+    const dim3 grid((unsigned)lay.n_tiles);
     const double ik = inv_pow2(K);
 #define SAEF_AV(DX, DE, XH)                                                                  \
-  hipLaunchKernelGGL((k_step_average<DX, DE, XH>), grid, dim3(kBlock), 0, s, lay, K, ik, x, \
+  SAEF_LAUNCH((k_step_average<DX, DE, XH>), grid, dim3(kBlock), 0, s, lay, K, ik, x, \
                      srv_signs, srv_scales, e, signs, scales, xh)
     if (xh == nullptr) {
       if (decode_e) return hipErrorInvalidValue;  // plain averaging only
@@ -677,7 +709,7 @@ hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
     if (xh == nullptr) return hipErrorInvalidValue;
     const dim3 grid((unsigned)((lay.n_tiles + kXcds - 1) / kXcds * kXcds * K));
 #define SAEF_ST(DX, DE)                                                                \
-  hipLaunchKernelGGL((k_step<DX, DE>), grid, dim3(kBlock), 0, s, lay, K, x, srv_signs, \
+  SAEF_LAUNCH((k_step<DX, DE>), grid, dim3(kBlock), 0, s, lay, K, x, srv_signs, \
                      srv_scales, e, signs, scales, xh)
     if (decode_x) {
       SAEF_ST(true, true);
@@ -695,12 +727,12 @@ hipError_t launch_materialize(const DevLayout& lay, int K, int mode, const float
                               const uint64_t* signs, const float* scales, float* e_out,
                               const float* e_srv, const float* x, const uint64_t* srv_signs,
                               const float* srv_scales, float* e_srv_out, float* x_out,
-                              hipStream_t s) {
+                              hipStream_t s, const LaunchEvents& ev) {
   const int k_rows = e_out != nullptr ? K : 0;
   const int rows = k_rows + ((e_srv_out != nullptr || x_out != nullptr) ? 1 : 0);
   if (rows == 0) return hipSuccess;
   const dim3 grid((unsigned)(lay.n_tiles * rows));
-  hipLaunchKernelGGL(k_materialize, grid, dim3(kBlock), 0, s, lay, k_rows, rows, mode, e, signs,
+  SAEF_LAUNCH(k_materialize, grid, dim3(kBlock), 0, s, lay, k_rows, rows, mode, e, signs,
                      scales, e_out, e_srv, x, srv_signs, srv_scales, e_srv_out, x_out);
   return hipGetLastError();
 }

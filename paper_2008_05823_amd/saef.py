@@ -42,7 +42,7 @@ _SIGS = {
     "saef_round": [_P, _i64, _i64, _i32, _f32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P],
     "saef_materialize": [_P, _i32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P],
     "saef_status": [_P, _P],
-    "saef_profile_enable": [_P, _i32],
+    "saef_profile_enable": [_P, _i32, ctypes.c_uint32],
     "saef_profile_read": [_P, _P, _P],
 }
 for _name, _args in _SIGS.items():
@@ -51,6 +51,10 @@ for _name, _args in _SIGS.items():
     _fn.restype = ctypes.c_int
 
 EXPORTS = tuple(_SIGS)
+
+# kernel kinds of saef_profile_enable / saef_profile_read, in bit order
+PROFILE_KINDS = ("step_ahead", "compress", "worker_scales", "aggregate", "server_scales",
+                 "step_ahead_averaging")
 
 
 class SaefError(RuntimeError):
@@ -189,12 +193,13 @@ def saef_status(layout: Layout, stream=None) -> int:
     return rc
 
 
-PROFILE_KINDS = ("step_ahead", "compress", "worker_scales", "aggregate", "server_scales",
-                 "step_ahead_averaging")
-
-
-def saef_profile_enable(layout: Layout, capacity: int) -> None:
-    _check("saef_profile_enable", _lib.saef_profile_enable(layout.handle, int(capacity)))
+def saef_profile_enable(layout: Layout, capacity: int, kinds=PROFILE_KINDS) -> None:
+    """Time the kernels of the given kinds (names from PROFILE_KINDS) in the
+    next saef_round calls, up to `capacity` launches."""
+    mask = 0
+    for k in kinds:
+        mask |= 1 << PROFILE_KINDS.index(k)
+    _check("saef_profile_enable", _lib.saef_profile_enable(layout.handle, int(capacity), mask))
 
 
 def saef_profile_read(layout: Layout) -> dict:
