@@ -24,6 +24,7 @@ struct saef_layout {
   void* mem_tiles = nullptr;
   void* mem_tensors = nullptr;
   void* mem_part = nullptr;
+  void* mem_part2 = nullptr;
   void* mem_status = nullptr;
   // measurement: event pairs recorded around the kernels of saef_round
   std::vector<hipEvent_t> ev_start, ev_stop;
@@ -105,6 +106,7 @@ void free_layout(saef_layout* l) {
   (void)hipFree(l->mem_tiles);
   (void)hipFree(l->mem_tensors);
   (void)hipFree(l->mem_part);
+  (void)hipFree(l->mem_part2);
   (void)hipFree(l->mem_status);
   delete l;
 }
@@ -156,10 +158,15 @@ int saef_layout_create(const int64_t* off, const int64_t* n, int32_t L, int64_t 
   }
   const size_t n_rows = (size_t)k_max + 1;
   const size_t part_bytes = n_rows * tiles.size() * 2 * sizeof(unsigned long long);
+  int32_t max_tiles = 1;
+  for (int32_t l = 0; l < L; ++l) max_tiles = std::max(max_tiles, tensors[l].ntiles);
+  const int32_t fin_split = (max_tiles + saef::kFinChunk - 1) / saef::kFinChunk;
+  const size_t part2_bytes = n_rows * L * fin_split * 2 * sizeof(unsigned long long);
   hipError_t err = hipSuccess;
   err = hipMalloc(&lay->mem_tiles, tiles.size() * sizeof(Tile));
   if (err == hipSuccess) err = hipMalloc(&lay->mem_tensors, tensors.size() * sizeof(TensorInfo));
   if (err == hipSuccess) err = hipMalloc(&lay->mem_part, part_bytes);
+  if (err == hipSuccess) err = hipMalloc(&lay->mem_part2, part2_bytes);
   if (err == hipSuccess) err = hipMalloc(&lay->mem_status, sizeof(int));
   if (err == hipSuccess)
     err = hipMemcpy(lay->mem_tiles, tiles.data(), tiles.size() * sizeof(Tile),
@@ -178,6 +185,8 @@ int saef_layout_create(const int64_t* off, const int64_t* n, int32_t L, int64_t 
   d.tiles = static_cast<const Tile*>(lay->mem_tiles);
   d.tensors = static_cast<const TensorInfo*>(lay->mem_tensors);
   d.part = static_cast<unsigned long long*>(lay->mem_part);
+  d.part2 = static_cast<unsigned long long*>(lay->mem_part2);
+  d.fin_split = fin_split;
   d.status = static_cast<int*>(lay->mem_status);
   d.n_tiles = (int64_t)tiles.size();
   d.d_pad = d_pad;

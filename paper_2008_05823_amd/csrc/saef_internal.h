@@ -14,7 +14,8 @@ constexpr int kWaves = kBlock / kWave;
 #define SAEF_TILE_ELEMS 2048
 #endif
 constexpr int kTileElems = SAEF_TILE_ELEMS;  // default work tile (elements, multiple of 64)
-constexpr int kMaxTilesPerTensor = 8192;
+constexpr int kMaxTilesPerTensor = 1 << 17;  // 2048-element tiles up to 2^28 elements
+constexpr int kFinChunk = 4096;              // tile partials per finalize workgroup
 constexpr int64_t kMaxTensor = int64_t(1) << 28;
 
 // One unit of work: `count` consecutive elements of tensor `l` starting at
@@ -38,6 +39,8 @@ struct DevLayout {
   const TensorInfo* tensors;
   unsigned long long* part;  // [(k_max + 1) * n_tiles * 2] exact partial sums (lo, hi) of
                              // each tile; row k_max belongs to the server
+  unsigned long long* part2; // [(k_max + 1) * L * fin_split * 2] second-level sums
+  int32_t fin_split;         // finalize workgroups per (row, tensor): ceil(max tiles / kFinChunk)
   int* status;               // sticky error flag
   int64_t n_tiles;
   int64_t d_pad;
@@ -57,7 +60,7 @@ struct LaunchEvents {
 
 // ---- kernel launchers (defined in saef_kernels.hip) ----------------------
 // All return hipSuccess or the launch error.  Arguments are validated by the
-// caller.  Each launcher enqueues exactly one kernel.
+// caller.  Each launcher enqueues one kernel (launch_finalize: one or two).
 
 // Worker compression.  decode: e holds values with a pending correction
 // (signs/scales of the previous compression) that is applied on read.
@@ -68,7 +71,8 @@ hipError_t launch_compress(const DevLayout& lay, int K, float lr, const float* g
                            const LaunchEvents& ev = LaunchEvents());
 
 // Scales from the tile partial sums: worker rows 0..K-1 into scales[k][l]
-// (server == false) or the server row into scales[l] (server == true).
+// (server == false) or the server row into scales[l] (server == true).  One
+// kernel, or two when a tensor has more than kFinChunk tiles (fin_split > 1).
 hipError_t launch_finalize(const DevLayout& lay, int K, bool server, float* scales,
                            hipStream_t s,
                            const LaunchEvents& ev = LaunchEvents());

@@ -264,20 +264,12 @@ __global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float
 }
 
 // ------------------------------------------------------------------ finalize
-// Grid: rows * L workgroups; workgroup b adds the tile partials of tensor
-// b % L for row b / L (or the server row) and writes the scale.
-__global__ __launch_bounds__(kBlock) void k_finalize(DevLayout lay, int server,
-                                                     float* __restrict__ scales) {
+// Adds the 128-bit values v[0..n) over the workgroup (thread 0 gets the sum).
+__device__ void block_sum128(const u64* __restrict__ v, int64_t n, u64& tlo, u64& thi) {
   __shared__ u64 s_lo[kWaves];
   __shared__ u64 s_hi[kWaves];
-  const int64_t b = blockIdx.x;
-  const int l = (int)(b % lay.L);
-  const int r = (int)(b / lay.L);
-  const int row = server ? lay.k_max : r;
-  const TensorInfo t = lay.tensors[l];
-  const u64* p = lay.part + ((int64_t)row * lay.n_tiles + t.first_tile) * 2;
   u64 lo = 0, hi = 0;
-  for (int i = threadIdx.x; i < t.ntiles; i += kBlock) add128(lo, hi, p[2 * i], p[2 * i + 1]);
+  for (int64_t i = threadIdx.x; i < n; i += kBlock) add128(lo, hi, v[2 * i], v[2 * i + 1]);
   wave_sum128(lo, hi);
   const int w = threadIdx.x / kWave;
   if (lane_id() == 0) {
@@ -285,10 +277,52 @@ __global__ __launch_bounds__(kBlock) void k_finalize(DevLayout lay, int server,
     s_hi[w] = hi;
   }
   __syncthreads();
+  tlo = 0;
+  thi = 0;
+  if (threadIdx.x == 0)
+    for (int i = 0; i < kWaves; ++i) add128(tlo, thi, s_lo[i], s_hi[i]);
+}
+
+// Grid: rows * L * S workgroups (S = lay.fin_split); workgroup b adds the
+// tile partials of part s = b % S of tensor (b / S) % L for row b / (S L)
+// (or the server row).  With S = 1 it writes the tensor's scale; otherwise
+// it stores a second-level partial that k_finalize2 adds up.
+__global__ __launch_bounds__(kBlock) void k_finalize(DevLayout lay, int server,
+                                                     float* __restrict__ scales) {
+  const int S = lay.fin_split;
+  const int64_t b = blockIdx.x;
+  const int s = (int)(b % S);
+  const int l = (int)((b / S) % lay.L);
+  const int r = (int)(b / ((int64_t)S * lay.L));
+  const int row = server ? lay.k_max : r;
+  const TensorInfo t = lay.tensors[l];
+  const int per = (t.ntiles + S - 1) / S;
+  const int i0 = min(t.ntiles, s * per), i1 = min(t.ntiles, i0 + per);
+  u64 tlo, thi;
+  block_sum128(lay.part + ((int64_t)row * lay.n_tiles + t.first_tile + i0) * 2, i1 - i0, tlo,
+               thi);
   if (threadIdx.x != 0) return;
-  u64 tlo = 0, thi = 0;
-  for (int i = 0; i < kWaves; ++i) add128(tlo, thi, s_lo[i], s_hi[i]);
-  scales[server ? l : (int64_t)r * lay.L + l] = scale_from_sum(thi, tlo, t.n);
+  if (S == 1) {
+    scales[server ? l : (int64_t)r * lay.L + l] = scale_from_sum(thi, tlo, t.n);
+  } else {
+    u64* q = lay.part2 + (((int64_t)row * lay.L + l) * S + s) * 2;
+    q[0] = tlo;
+    q[1] = thi;
+  }
+}
+
+// Grid: rows * L workgroups: the S second-level partials of (row, tensor).
+__global__ __launch_bounds__(kBlock) void k_finalize2(DevLayout lay, int server,
+                                                      float* __restrict__ scales) {
+  const int S = lay.fin_split;
+  const int64_t b = blockIdx.x;
+  const int l = (int)(b % lay.L);
+  const int r = (int)(b / lay.L);
+  const int row = server ? lay.k_max : r;
+  u64 tlo, thi;
+  block_sum128(lay.part2 + ((int64_t)row * lay.L + l) * S * 2, S, tlo, thi);
+  if (threadIdx.x != 0) return;
+  scales[server ? l : (int64_t)r * lay.L + l] = scale_from_sum(thi, tlo, lay.tensors[l].n);
 }
 
 // ------------------------------------------------------------------ step ahead
@@ -656,8 +690,19 @@ hipError_t launch_compress(const DevLayout& lay, int K, float lr, const float* g
 
 hipError_t launch_finalize(const DevLayout& lay, int K, bool server, float* scales,
                            hipStream_t s, const LaunchEvents& ev) {
-  const dim3 grid((unsigned)((server ? 1 : K) * lay.L));
-  SAEF_LAUNCH(k_finalize, grid, dim3(kBlock), 0, s, lay, server ? 1 : 0, scales);
+  const int rows = server ? 1 : K;
+  const dim3 grid1((unsigned)((int64_t)rows * lay.L * lay.fin_split));
+  if (lay.fin_split == 1) {
+    SAEF_LAUNCH(k_finalize, grid1, dim3(kBlock), 0, s, lay, server ? 1 : 0, scales);
+    return hipGetLastError();
+  }
+  // two kernels: the event pair brackets both
+  hipExtLaunchKernelGGL(k_finalize, grid1, dim3(kBlock), 0, s, ev.start, nullptr, 0, lay,
+                        server ? 1 : 0, scales);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  hipExtLaunchKernelGGL(k_finalize2, dim3((unsigned)(rows * lay.L)), dim3(kBlock), 0, s, nullptr,
+                        ev.stop, 0, lay, server ? 1 : 0, scales);
   return hipGetLastError();
 }
 

@@ -37,6 +37,7 @@ def _rand_err(rng, K, w, scale=0.01):
     (3, ADVERSARIAL),
     (8, [4096 * 3 + 17, 64, 1, 70000]),
     (4, [(1 << 20) + 3]),
+    (2, [9_000_001, 64]),   # > 4096 tiles in one tensor: two-level scale reduction
 ])
 def test_compress_parity(K, sizes):
     _case(f"compress K={K} sizes={sizes}")
