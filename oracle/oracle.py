@@ -51,6 +51,9 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "oracle_step_ahead": lay + [i32, _P, _P, _P],
         "oracle_error_average": lay + [i32, _P],
         "oracle_round": lay + [i64, i64, i32, f32, i32, _P, _P, _P, _P, _P, _P, _P, _P, _P],
+        "oracle_compress_momentum": lay + [i32, f32, f32, _P, _P, _P, _P, _P],
+        "oracle_round_momentum": lay + [i64, i64, i32, f32, f32, i32, _P, _P, _P, _P, _P, _P,
+                                        _P, _P, _P, _P],
     }
     for name, args in sigs.items():
         fn = getattr(lib, name)
@@ -108,6 +111,17 @@ class Oracle:
         return self.lib.oracle_aggregate(*self._lay(), K, mode, _ptr(signs), _ptr(scales),
                                          _ptr(avg), _ptr(e_srv), _ptr(srv_signs),
                                          _ptr(srv_scales), _ptr(x))
+
+    def compress_momentum(self, K, lr, mu, g, m, e, signs, scales):
+        return self.lib.oracle_compress_momentum(*self._lay(), K, lr, mu, _ptr(g), _ptr(m),
+                                                 _ptr(e), _ptr(signs), _ptr(scales))
+
+    def round_momentum(self, t, period, K, lr, mu, mode, g, m, e, e_srv, x, xh, signs, scales,
+                       srv_signs, srv_scales):
+        return self.lib.oracle_round_momentum(*self._lay(), t, period, K, lr, mu, mode, _ptr(g),
+                                              _ptr(m), _ptr(e), _ptr(e_srv), _ptr(x), _ptr(xh),
+                                              _ptr(signs), _ptr(scales), _ptr(srv_signs),
+                                              _ptr(srv_scales))
 
     def step_ahead(self, K, x, e, xh):
         return self.lib.oracle_step_ahead(*self._lay(), K, _ptr(x), _ptr(e), _ptr(xh))

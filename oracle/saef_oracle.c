@@ -5,7 +5,9 @@
  *   - Eq. (2): C(v) = (||v||_1 / d) sign(v), applied layer-wise, i.e. one
  *     scale per parameter tensor (Experiments: "all compression are performed
  *     in a layer-wise way"), so d becomes the tensor size n_l.
- *   - Algorithm 1, SAEF branch, with momentum constant mu = 0 (SAEF-SGD):
+ *   - Algorithm 1, SAEF branch, with momentum constant mu = 0 (SAEF-SGD), and
+ *     with mu > 0 through the *_momentum entry points (m <- mu m + grad,
+ *     Delta^(k) = e^(k) + eta m):
  *       every p iterations the local errors are replaced by their mean,
  *       x_{t+1/2} = x_t - e_t            (step ahead)
  *       m = grad                         (mu = 0)
@@ -21,7 +23,8 @@
  *   - ||v||_1 is summed exactly as the integer S = sum floor(|v_i| 2^80)
  *     (requires |v_i| < 2^19 and n <= 2^28); the scale is
  *     fp32( fp64( fp64(S) / n ) * 2^-80 ).
- *   - eta * m + e is formed with one rounding (fused multiply-add).
+ *   - eta * m + e is formed with one rounding (fused multiply-add), and so
+ *     is the momentum update mu * m + grad.
  *   - Means over the K workers are binary64 sums taken in worker order
  *     0..K-1, divided by K in binary64, then rounded once to fp32.
  *   - Delta = fp32(e_server + fp32(average)); every other fp32 result is the
@@ -160,6 +163,38 @@ int oracle_compress(int32_t L, const int64_t* off, const int64_t* n, int64_t d_p
     return status;
 }
 
+int oracle_compress_momentum(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                             int32_t K, float lr, float mu, const float* g, float* m, float* e,
+                             uint64_t* signs, float* scales)
+{
+    int rc = check_layout(L, off, n, d_pad);
+    if (rc != ORACLE_OK) return rc;
+    if (K < 1 || g == NULL || m == NULL || e == NULL || signs == NULL || scales == NULL)
+        return ORACLE_EINVAL;
+    if (!(mu >= 0.0f && mu < 1.0f)) return ORACLE_EINVAL;
+    int status = ORACLE_OK;
+    for (int32_t k = 0; k < K; ++k) {
+        const float* gk = g + (int64_t)k * d_pad;
+        float* mk = m + (int64_t)k * d_pad;
+        float* ek = e + (int64_t)k * d_pad;
+        uint64_t* wk = signs + (int64_t)k * (d_pad / 64);
+        for (int32_t l = 0; l < L; ++l) {
+            for (int64_t i = 0; i < n[l]; ++i) {
+                int64_t j = off[l] + i;
+                /* m^(k)_{t+1} = mu m^(k)_t + grad */
+                mk[j] = fmaf(mu, mk[j], gk[j]);
+                /* Delta^(k) = e^(k) + eta * m^(k)_{t+1} */
+                ek[j] = fmaf(lr, mk[j], ek[j]);
+            }
+            /* e^(k) <- Delta^(k) - C(Delta^(k)); message goes to the server */
+            rc = compress_tensor(ek + off[l], n[l], off[l], &scales[(int64_t)k * L + l],
+                                 wk, ek + off[l]);
+            if (rc != ORACLE_OK) status = rc;
+        }
+    }
+    return status;
+}
+
 /* ---- Algorithm 1: server aggregation and worker re-update --------------- */
 
 int oracle_aggregate(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
@@ -259,6 +294,29 @@ int oracle_round(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
     if (rc != ORACLE_OK) return rc;
     /* the gradient at xh is the caller's input g */
     int status = oracle_compress(L, off, n, d_pad, K, lr, g, e, signs, scales);
+    if (status == ORACLE_EINVAL) return status;
+    rc = oracle_aggregate(L, off, n, d_pad, K, mode, signs, scales, NULL, e_srv,
+                          srv_signs, srv_scales, x);
+    if (rc != ORACLE_OK) status = rc;
+    return status;
+}
+
+int oracle_round_momentum(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                          int64_t t, int64_t period, int32_t K, float lr, float mu, int32_t mode,
+                          const float* g, float* m, float* e, float* e_srv, float* x, float* xh,
+                          uint64_t* signs, float* scales, uint64_t* srv_signs,
+                          float* srv_scales)
+{
+    if (t < 0 || period < 0) return ORACLE_EINVAL;
+    int rc;
+    if (period > 0 && (t + 1) % period == 0) {
+        rc = oracle_error_average(L, off, n, d_pad, K, e);
+        if (rc != ORACLE_OK) return rc;
+    }
+    rc = oracle_step_ahead(L, off, n, d_pad, K, x, e, xh);
+    if (rc != ORACLE_OK) return rc;
+    /* the gradient at xh is the caller's input g */
+    int status = oracle_compress_momentum(L, off, n, d_pad, K, lr, mu, g, m, e, signs, scales);
     if (status == ORACLE_EINVAL) return status;
     rc = oracle_aggregate(L, off, n, d_pad, K, mode, signs, scales, NULL, e_srv,
                           srv_signs, srv_scales, x);

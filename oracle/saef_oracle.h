@@ -41,6 +41,13 @@ int oracle_compress(int32_t L, const int64_t* off, const int64_t* n, int64_t d_p
                     int32_t K, float lr, const float* g, float* e,
                     uint64_t* signs, float* scales);
 
+/* Worker side of Algorithm 1 with momentum constant mu (0 <= mu < 1):
+ * m <- mu m + g (one rounding), Delta = e + lr m (one rounding), then the
+ * message and error update as in oracle_compress.  m: (K, d_pad) in/out. */
+int oracle_compress_momentum(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                             int32_t K, float lr, float mu, const float* g, float* m, float* e,
+                             uint64_t* signs, float* scales);
+
 /* Server side of Algorithm 1 and the re-update.  mode 1 = double-way
  * compression (server error and server message), mode 0 = single-way (the
  * average goes back uncompressed).  avg may be NULL.  In mode 0 e_srv,
@@ -65,6 +72,13 @@ int oracle_round(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
                  int64_t t, int64_t period, int32_t K, float lr, int32_t mode,
                  const float* g, float* e, float* e_srv, float* x, float* xh,
                  uint64_t* signs, float* scales, uint64_t* srv_signs, float* srv_scales);
+
+/* oracle_round with momentum: the worker step uses oracle_compress_momentum. */
+int oracle_round_momentum(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                          int64_t t, int64_t period, int32_t K, float lr, float mu, int32_t mode,
+                          const float* g, float* m, float* e, float* e_srv, float* x, float* xh,
+                          uint64_t* signs, float* scales, uint64_t* srv_signs,
+                          float* srv_scales);
 
 #ifdef __cplusplus
 }

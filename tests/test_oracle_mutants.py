@@ -1,8 +1,8 @@
 """Planted mistakes in the oracle must be caught by its pins.
 
 Each mutant is a copy of the oracle source with one plausible slip (a dropped
-term, a flipped sign, a wrong index or condition), compiled on the CPU into a
-temporary library.  The pins of tests/oracle_pins.py are run against it and at
+term, a flipped sign, a wrong index or condition -- at every place the
+mutated line occurs), compiled on the CPU into a temporary library.  The pins of tests/oracle_pins.py are run against it and at
 least one must fail; otherwise the pins would not be strong enough to trust
 the oracle as the parity reference.
 """
@@ -33,6 +33,9 @@ MUTANTS = {
     "l1_rounds_not_floors": ("S += (u128)scaled;", "S += (u128)(scaled + 0.5);"),
     "decode_swapped": ("return bit ? scale : -scale;", "return bit ? -scale : scale;"),
     "worker_stride": ("float* ek = e + (int64_t)k * d_pad;", "float* ek = e + (int64_t)(K - 1 - k) * d_pad;"),
+    "momentum_dropped": ("mk[j] = fmaf(mu, mk[j], gk[j]);", "mk[j] = gk[j];"),
+    "momentum_swapped": ("mk[j] = fmaf(mu, mk[j], gk[j]);", "mk[j] = fmaf(mu, gk[j], mk[j]);"),
+    "momentum_lr_dropped": ("ek[j] = fmaf(lr, mk[j], ek[j]);", "ek[j] = mk[j] + ek[j];"),
     "step_ahead_skips_worker": ("for (int32_t k = 0; k < K; ++k)\n        for (int32_t l = 0; l < L; ++l)\n            for (int64_t i = 0; i < n[l]; ++i) {\n                int64_t j = off[l] + i;\n                /* x^(k)",
                                 "for (int32_t k = 0; k < K - (K > 1); ++k)\n        for (int32_t l = 0; l < L; ++l)\n            for (int64_t i = 0; i < n[l]; ++i) {\n                int64_t j = off[l] + i;\n                /* x^(k)"),
 }
@@ -42,7 +45,7 @@ MUTANTS = {
 def test_mutant_is_caught(tmp_path, name):
     old, new = MUTANTS[name]
     src = open(O.SRC).read()
-    assert src.count(old) == 1, f"mutation site for {name} not found exactly once"
+    assert src.count(old) >= 1, f"mutation site for {name} not found"
     msrc = tmp_path / "saef_oracle.c"
     msrc.write_text(src.replace(old, new))
     (tmp_path / "saef_oracle.h").write_text(open(os.path.join(O.HERE, "saef_oracle.h")).read())
