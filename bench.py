@@ -7,7 +7,8 @@ re-update.  The synthetic gradients of the iteration are already resident in
 HBM when the timed region starts (two seeded gradient sets alternate).
 
 Default workload: ResNet-50 shaped tensor list (161 tensors, d = 25,557,032),
-K = 8 workers, lr 0.1, error averaging period 20.
+K = 8 workers, lr 0.1, error averaging period 20.  --momentum MU runs the
+momentum variant of the worker step (saef_round_momentum) instead.
 
 Prints one JSON line (metric, value = parameters per second per K-worker
 iteration, roofline of the dominant kernel, CPU oracle baseline).
@@ -119,6 +120,8 @@ def main() -> int:
     ap.add_argument("--cpu-rounds", type=int, default=1,
                     help="iterations of the CPU oracle baseline (0 = skip)")
     ap.add_argument("--no-probe", action="store_true", help="skip the copy-bandwidth probe")
+    ap.add_argument("--momentum", type=float, default=None,
+                    help="momentum constant mu in [0, 1): time saef_round_momentum")
     ap.add_argument("--kernel-events", choices=("on", "off"), default="on",
                     help="HIP events around each kernel in the timed region (roofline); "
                          "'off' times the iterations alone")
@@ -154,10 +157,16 @@ def main() -> int:
     srv_signs = torch.zeros(d_pad // 64, dtype=torch.int64, device="cuda")
     srv_scales = torch.zeros(L, **f32)
     layout = saef.Layout(off, n, d_pad, K)
+    mu = args.momentum
+    m = torch.zeros((K, d_pad), **f32) if mu is not None else None
 
     def step(t):
-        saef.saef_round(layout, t, w.period, K, w.lr, w.mode, g_dev[t % n_grad], e, e_srv, x, xh,
-                        signs, scales, srv_signs, srv_scales)
+        if mu is None:
+            saef.saef_round(layout, t, w.period, K, w.lr, w.mode, g_dev[t % n_grad], e, e_srv, x,
+                            xh, signs, scales, srv_signs, srv_scales)
+        else:
+            saef.saef_round_momentum(layout, t, w.period, K, w.lr, mu, w.mode, g_dev[t % n_grad],
+                                     m, e, e_srv, x, xh, signs, scales, srv_signs, srv_scales)
 
     for t in range(args.warmup):
         step(t)
@@ -184,13 +193,15 @@ def main() -> int:
     timed_ts = range(args.warmup, args.warmup + args.steps)
     n_avg = sum(1 for t in timed_ts if w.period and (t + 1) % w.period == 0)
     bytes_round = np.mean([W.algorithmic_bytes_per_param(
-        K, w.mode, averaging=bool(w.period and (t + 1) % w.period == 0)) for t in timed_ts]) * d
+        K, w.mode, averaging=bool(w.period and (t + 1) % w.period == 0),
+        momentum=mu is not None) for t in timed_ts]) * d
 
-    # dominant kernel: worker compression (12 K + K/8 bytes per parameter)
+    # dominant kernel: worker compression (12 K + K/8 bytes per parameter,
+    # 20 K + K/8 with momentum)
     c_count, c_ms = prof["compress"]
-    c_bytes = (12 * K + K / 8) * d
+    c_bytes = ((20 if mu is not None else 12) * K + K / 8) * d
     c_gbps = c_bytes / (c_ms / c_count * 1e-3) / 1e9 if c_count else None
-    traffic = traffic_from_profile(args.workload)
+    traffic = traffic_from_profile(args.workload) if mu is None else None
 
     # breakdown of every kernel, from a separate pass of the same length (each
     # timed dispatch costs a few microseconds, so it is kept out of the value)
@@ -220,8 +231,10 @@ def main() -> int:
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": f"{w.name}: {L} tensors, d={d}, K={K} simulated workers, "
-                               f"double-way, lr={w.lr}, error averaging period {w.period}",
-                   "K": K, "d": d, "L": L, "period": w.period, "mode": "DC"},
+                               f"double-way, lr={w.lr}, error averaging period {w.period}"
+                               + (f", momentum {mu}" if mu is not None else ""),
+                   "K": K, "d": d, "L": L, "period": w.period, "mode": "DC",
+                   **({"momentum": mu} if mu is not None else {})},
         "worker_params_per_s": K * d / (ms_per_step * 1e-3),
         "round_hbm_gbps": bytes_round / (ms_per_step * 1e-3) / 1e9,
         "round_frac_of_peak": bytes_round / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,

@@ -20,6 +20,7 @@
  * Every fp32 result is defined exactly, so results do not depend on the
  * launch geometry and runs are bit-reproducible:
  *   Delta^(k)   = fma(lr, g, e)                (one rounding)
+ *   momentum    m = fma(mu, m, g), Delta^(k) = fma(lr, m, e)  (*_momentum)
  *   sign bit    = (v >= 0)  -- +0 and -0 give +1 (the paper leaves sign(0) open)
  *   ||v||_1     = S = sum floor(|v_i| 2^80) as an exact integer
  *                 (needs |v_i| < 2^19; n_l <= 2^28)
@@ -87,6 +88,16 @@ int saef_layout_destroy(saef_layout* layout);
 int saef_compress(const saef_layout* layout, int32_t K, float lr, const float* g, float* e,
                   uint64_t* signs, float* scales, hipStream_t stream);
 
+/* Worker side of Algorithm 1 with momentum constant mu (0 <= mu < 1, the
+ * momentum SGD update of the SAEF branch): m[k] <- fma(mu, m[k], g[k]) (one
+ * rounding), then Delta = fma(lr, m[k], e[k]) and everything else as in
+ * saef_compress.  m: (K, d_pad) in/out momentum buffers, zero at the start
+ * of training (Algorithm 1 initialisation).  SAEF_EINVAL for mu outside
+ * [0, 1) or m NULL. */
+int saef_compress_momentum(const saef_layout* layout, int32_t K, float lr, float mu,
+                           const float* g, float* m, float* e, uint64_t* signs, float* scales,
+                           hipStream_t stream);
+
 /* Server side of Algorithm 1 plus the re-update.  mean = (1/K) sum_k C_k
  * decoded from signs/scales.  mode SAEF_MODE_DC: Delta = e_srv + mean,
  * srv_signs/srv_scales <- C(Delta), e_srv <- Delta - C(Delta),
@@ -129,6 +140,14 @@ int saef_round(const saef_layout* layout, int64_t t, int64_t period, int32_t K, 
                int32_t mode, const float* g, float* e, float* e_srv, float* x, float* xh,
                uint64_t* signs, float* scales, uint64_t* srv_signs, float* srv_scales,
                hipStream_t stream);
+
+/* saef_round with momentum: the worker compression step is the one of
+ * saef_compress_momentum (m in/out, plain values).  Same state form and t
+ * conventions as saef_round. */
+int saef_round_momentum(const saef_layout* layout, int64_t t, int64_t period, int32_t K,
+                        float lr, float mu, int32_t mode, const float* g, float* m, float* e,
+                        float* e_srv, float* x, float* xh, uint64_t* signs, float* scales,
+                        uint64_t* srv_signs, float* srv_scales, hipStream_t stream);
 
 /* Plain values of a saef_round state: writes e_true to e_out (K, d_pad),
  * e_srv_true to e_srv_out and x_true to x_out (each may be NULL to skip, and

@@ -212,21 +212,47 @@ int saef_layout_info(const saef_layout* layout, int32_t* L, int64_t* d_pad, int3
   return SAEF_OK;
 }
 
-int saef_compress(const saef_layout* layout, int32_t K, float lr, const float* g, float* e,
-                  uint64_t* signs, float* scales, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// saef_compress / saef_compress_momentum (m == nullptr: no momentum).
+int compress_impl(const saef_layout* layout, int32_t K, float lr, float mu, const float* g,
+                  float* m, float* e, uint64_t* signs, float* scales, hipStream_t stream) {
   int rc = check_common(layout, K);
   if (rc != SAEF_OK) return rc;
   if (!f32_ok(g) || !f32_ok(e) || !u64_ok(signs) || !f32_ok(scales) || !std::isfinite(lr))
     return SAEF_EINVAL;
   const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
   if (overlap(g, vb, e, vb)) return SAEF_EINVAL;
-  rc = hip_rc(saef::launch_compress(layout->dev, K, lr, g, e, signs, scales, false, stream));
+  if (m != nullptr && (!f32_ok(m) || overlap(m, vb, g, vb) || overlap(m, vb, e, vb)))
+    return SAEF_EINVAL;
+  rc = hip_rc(
+      saef::launch_compress(layout->dev, K, lr, mu, g, m, e, signs, scales, false, stream));
   if (rc != SAEF_OK) return rc;
   rc = hip_rc(saef::launch_finalize(layout->dev, K, false, scales, stream));
   if (rc != SAEF_OK) return rc;
   return hip_rc(saef::launch_materialize(layout->dev, K, SAEF_MODE_SC, e, signs, scales, e,
                                          nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
                                          stream));
+}
+
+bool mu_ok(float mu) { return mu >= 0.0f && mu < 1.0f; }
+
+}  // namespace
+
+extern "C" {
+
+int saef_compress(const saef_layout* layout, int32_t K, float lr, const float* g, float* e,
+                  uint64_t* signs, float* scales, hipStream_t stream) {
+  return compress_impl(layout, K, lr, 0.0f, g, nullptr, e, signs, scales, stream);
+}
+
+int saef_compress_momentum(const saef_layout* layout, int32_t K, float lr, float mu,
+                           const float* g, float* m, float* e, uint64_t* signs, float* scales,
+                           hipStream_t stream) {
+  if (!mu_ok(mu) || m == nullptr) return SAEF_EINVAL;
+  return compress_impl(layout, K, lr, mu, g, m, e, signs, scales, stream);
 }
 
 int saef_aggregate(const saef_layout* layout, int32_t K, int32_t mode, const uint64_t* signs,
@@ -271,10 +297,15 @@ int saef_error_average(const saef_layout* layout, int32_t K, float* e, hipStream
                                         nullptr, nullptr, false, true, nullptr, stream));
 }
 
-int saef_round(const saef_layout* layout, int64_t t, int64_t period, int32_t K, float lr,
-               int32_t mode, const float* g, float* e, float* e_srv, float* x, float* xh,
-               uint64_t* signs, float* scales, uint64_t* srv_signs, float* srv_scales,
-               hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// saef_round / saef_round_momentum (m == nullptr: no momentum).
+int round_impl(const saef_layout* layout, int64_t t, int64_t period, int32_t K, float lr,
+               float mu, int32_t mode, const float* g, float* m, float* e, float* e_srv,
+               float* x, float* xh, uint64_t* signs, float* scales, uint64_t* srv_signs,
+               float* srv_scales, hipStream_t stream) {
   int rc = check_common(layout, K);
   if (rc != SAEF_OK) return rc;
   if (t < 0 || period < 0 || !std::isfinite(lr)) return SAEF_EINVAL;
@@ -287,6 +318,9 @@ int saef_round(const saef_layout* layout, int64_t t, int64_t period, int32_t K, 
   const size_t xb = layout->d_pad * sizeof(float);
   if (overlap(xh, vb, x, xb) || overlap(xh, vb, e, vb) || overlap(xh, vb, g, vb) ||
       overlap(g, vb, e, vb))
+    return SAEF_EINVAL;
+  if (m != nullptr && (!f32_ok(m) || overlap(m, vb, g, vb) || overlap(m, vb, e, vb) ||
+                       overlap(m, vb, xh, vb) || overlap(m, vb, x, xb)))
     return SAEF_EINVAL;
 
   const bool pending = t > 0;  // at t == 0 the state is plain (Algorithm 1 initialisation)
@@ -301,10 +335,11 @@ int saef_round(const saef_layout* layout, int64_t t, int64_t period, int32_t K, 
   }));
   if (rc != SAEF_OK) return rc;
   // [gradient slot: g was computed at xh by the caller]
-  // worker compression; e is plain after an averaging step
+  // worker compression (momentum update first when m is given); e is plain
+  // after an averaging step
   rc = hip_rc(timed(layout, 1, [&](const saef::LaunchEvents& ev) {
-    return saef::launch_compress(d, K, lr, g, e, signs, scales, pending && !averaging, stream,
-                                 ev);
+    return saef::launch_compress(d, K, lr, mu, g, m, e, signs, scales, pending && !averaging,
+                                 stream, ev);
   }));
   if (rc != SAEF_OK) return rc;
   rc = hip_rc(timed(layout, 2, [&](const saef::LaunchEvents& ev) {
@@ -320,6 +355,27 @@ int saef_round(const saef_layout* layout, int64_t t, int64_t period, int32_t K, 
   return hip_rc(timed(layout, 4, [&](const saef::LaunchEvents& ev) {
     return saef::launch_finalize(d, K, true, srv_scales, stream, ev);
   }));
+}
+
+}  // namespace
+
+extern "C" {
+
+int saef_round(const saef_layout* layout, int64_t t, int64_t period, int32_t K, float lr,
+               int32_t mode, const float* g, float* e, float* e_srv, float* x, float* xh,
+               uint64_t* signs, float* scales, uint64_t* srv_signs, float* srv_scales,
+               hipStream_t stream) {
+  return round_impl(layout, t, period, K, lr, 0.0f, mode, g, nullptr, e, e_srv, x, xh, signs,
+                    scales, srv_signs, srv_scales, stream);
+}
+
+int saef_round_momentum(const saef_layout* layout, int64_t t, int64_t period, int32_t K,
+                        float lr, float mu, int32_t mode, const float* g, float* m, float* e,
+                        float* e_srv, float* x, float* xh, uint64_t* signs, float* scales,
+                        uint64_t* srv_signs, float* srv_scales, hipStream_t stream) {
+  if (!mu_ok(mu) || m == nullptr) return SAEF_EINVAL;
+  return round_impl(layout, t, period, K, lr, mu, mode, g, m, e, e_srv, x, xh, signs, scales,
+                    srv_signs, srv_scales, stream);
 }
 
 int saef_materialize(const saef_layout* layout, int32_t K, int32_t mode, const float* e,

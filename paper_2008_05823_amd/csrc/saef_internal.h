@@ -63,12 +63,14 @@ struct LaunchEvents {
 // caller.  Each launcher enqueues one kernel (launch_finalize: one or two).
 
 // Worker compression.  decode: e holds values with a pending correction
-// (signs/scales of the previous compression) that is applied on read.
-// Always writes Delta (before correction) into e, the new sign words and the
-// tile partial sums; launch_finalize then writes the new scales.
-hipError_t launch_compress(const DevLayout& lay, int K, float lr, const float* g, float* e,
-                           uint64_t* signs, const float* scales, bool decode, hipStream_t s,
-                           const LaunchEvents& ev = LaunchEvents());
+// (signs/scales of the previous compression) that is applied on read.  m
+// non-null: momentum, m <- fma(mu, m, g) and Delta = fma(lr, m, e); else
+// Delta = fma(lr, g, e).  Always writes Delta (before correction) into e,
+// the new sign words and the tile partial sums; launch_finalize then writes
+// the new scales.
+hipError_t launch_compress(const DevLayout& lay, int K, float lr, float mu, const float* g,
+                           float* m, float* e, uint64_t* signs, const float* scales, bool decode,
+                           hipStream_t s, const LaunchEvents& ev = LaunchEvents());
 
 // Scales from the tile partial sums: worker rows 0..K-1 into scales[k][l]
 // (server == false) or the server row into scales[l] (server == true).  One

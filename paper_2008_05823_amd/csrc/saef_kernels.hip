@@ -191,17 +191,19 @@ __device__ void block_partial(const DevLayout& lay, int row, int64_t tile, u64 l
 }
 
 // ------------------------------------------------------------------ compress
-// kU words of one worker's tile starting at word w0: Delta = fma(lr, g, e)
+// kU words of one worker's tile starting at word w0: with kMom, the momentum
+// buffer m <- fma(mu, m, g) first (one rounding); Delta = fma(lr, m or g, e)
 // (e decoded when kDecode), sign words by ballot, exact-sum terms, Delta
 // stored.  kFull: all kU words are whole words of the tile (no guards).
-template <bool kDecode, bool kFull>
-__device__ __forceinline__ void compress_words(int w0, int nw, int count, float lr,
+template <bool kDecode, bool kMom, bool kFull>
+__device__ __forceinline__ void compress_words(int w0, int nw, int count, float lr, float mu,
                                                const float* __restrict__ gk,
+                                               float* __restrict__ mk,
                                                float* __restrict__ ek,
                                                uint64_t* __restrict__ sk, float s_old, u64& lo,
                                                u64& hi, bool& bad) {
   const int lane = lane_id();
-  float gv[kU], ev[kU];
+  float gv[kU], ev[kU], mv[kU];
   u64 ow[kU];
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
@@ -209,6 +211,7 @@ __device__ __forceinline__ void compress_words(int w0, int nw, int count, float 
     const bool ok = kFull || ((w0 + u < nw) && j < count);
     gv[u] = ok ? ld_nt(gk + j) : 0.0f;
     ev[u] = ok ? ld_nt(ek + j) : 0.0f;
+    mv[u] = (kMom && ok) ? ld_nt(mk + j) : 0.0f;
     ow[u] = (kDecode && (kFull || w0 + u < nw)) ? sk[w0 + u] : 0ull;
   }
 #pragma unroll
@@ -219,8 +222,13 @@ __device__ __forceinline__ void compress_words(int w0, int nw, int count, float 
     const bool ok = kFull || j < count;
     float ev2 = ev[u];
     if (kDecode) ev2 = ev2 - corr(ow[u], s_old);
-    // Delta^(k) = e^(k) + lr * g^(k), one rounding
-    const float p = __builtin_fmaf(lr, gv[u], ev2);
+    float step = gv[u];
+    if (kMom) {
+      step = __builtin_fmaf(mu, mv[u], gv[u]);  // m^(k)_{t+1} = mu m^(k)_t + grad
+      if (ok) st_nt(mk + j, step);
+    }
+    // Delta^(k) = e^(k) + lr * m^(k)_{t+1}, one rounding (m = grad when mu = 0)
+    const float p = __builtin_fmaf(lr, step, ev2);
     const u64 word = __ballot(ok && p >= 0.0f);
     if (lane == 0) sk[w] = word;
     if (ok) {
@@ -233,9 +241,10 @@ __device__ __forceinline__ void compress_words(int w0, int nw, int count, float 
 // Grid: n_tiles * K workgroups; workgroup b handles worker b % K of tile
 // b / K.  Wave w takes words w*kU .. w*kU+kU-1 of the tile, then strides by
 // 4*kU words.
-template <bool kDecode>
-__global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float lr,
+template <bool kDecode, bool kMom>
+__global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float lr, float mu,
                                                      const float* __restrict__ g,
+                                                     float* __restrict__ m,
                                                      float* __restrict__ e,
                                                      uint64_t* __restrict__ signs,
                                                      const float* __restrict__ scales) {
@@ -246,6 +255,7 @@ __global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float
   const int wave = wave_id();
   const int64_t row = (int64_t)k * lay.d_pad + tile.start;
   const float* gk = g + row;
+  float* mk = kMom ? m + row : nullptr;
   float* ek = e + row;
   uint64_t* sk = signs + (int64_t)k * (lay.d_pad >> 6) + (tile.start >> 6);
   const float s_old = kDecode ? scales[(int64_t)k * lay.L + tile.l] : 0.0f;
@@ -255,9 +265,11 @@ __global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float
   bool bad = false;
   for (int w0 = wave * kU; w0 < nw; w0 += kWaves * kU) {
     if ((w0 + kU) * 64 <= tile.count) {
-      compress_words<kDecode, true>(w0, nw, tile.count, lr, gk, ek, sk, s_old, lo, hi, bad);
+      compress_words<kDecode, kMom, true>(w0, nw, tile.count, lr, mu, gk, mk, ek, sk, s_old,
+                                          lo, hi, bad);
     } else {
-      compress_words<kDecode, false>(w0, nw, tile.count, lr, gk, ek, sk, s_old, lo, hi, bad);
+      compress_words<kDecode, kMom, false>(w0, nw, tile.count, lr, mu, gk, mk, ek, sk, s_old,
+                                           lo, hi, bad);
     }
   }
   block_partial(lay, k, ti, lo, hi, bad);
@@ -675,16 +687,18 @@ unsigned per_wave_grid(const DevLayout& lay) {
 
 }  // namespace
 
-hipError_t launch_compress(const DevLayout& lay, int K, float lr, const float* g, float* e,
-                           uint64_t* signs, const float* scales, bool decode, hipStream_t s, const LaunchEvents& ev) {
+hipError_t launch_compress(const DevLayout& lay, int K, float lr, float mu, const float* g,
+                           float* m, float* e, uint64_t* signs, const float* scales, bool decode,
+                           hipStream_t s, const LaunchEvents& ev) {
   const dim3 grid((unsigned)(lay.n_tiles * K));
-  if (decode) {
-    SAEF_LAUNCH(k_compress<true>, grid, dim3(kBlock), 0, s, lay, K, lr, g, e, signs,
-                       scales);
+#define SAEF_CMP(D, M) \
+  SAEF_LAUNCH((k_compress<D, M>), grid, dim3(kBlock), 0, s, lay, K, lr, mu, g, m, e, signs, scales)
+  if (m != nullptr) {
+    if (decode) SAEF_CMP(true, true); else SAEF_CMP(false, true);
   } else {
-    SAEF_LAUNCH(k_compress<false>, grid, dim3(kBlock), 0, s, lay, K, lr, g, e, signs,
-                       scales);
+    if (decode) SAEF_CMP(true, false); else SAEF_CMP(false, false);
   }
+#undef SAEF_CMP
   return hipGetLastError();
 }
 

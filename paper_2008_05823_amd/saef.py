@@ -36,10 +36,13 @@ _SIGS = {
     "saef_layout_destroy": [_P],
     "saef_layout_info": [_P, _P, _P, _P, _P],
     "saef_compress": [_P, _i32, _f32, _P, _P, _P, _P, _P],
+    "saef_compress_momentum": [_P, _i32, _f32, _f32, _P, _P, _P, _P, _P, _P],
     "saef_aggregate": [_P, _i32, _i32, _P, _P, _P, _P, _P, _P, _P, _P],
     "saef_step_ahead": [_P, _i32, _P, _P, _P, _P],
     "saef_error_average": [_P, _i32, _P, _P],
     "saef_round": [_P, _i64, _i64, _i32, _f32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P],
+    "saef_round_momentum": [_P, _i64, _i64, _i32, _f32, _f32, _i32, _P, _P, _P, _P, _P, _P, _P,
+                            _P, _P, _P, _P],
     "saef_materialize": [_P, _i32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P],
     "saef_status": [_P, _P],
     "saef_profile_enable": [_P, _i32, ctypes.c_uint32],
@@ -152,6 +155,13 @@ def saef_compress(layout: Layout, K: int, lr: float, g, e, signs, scales, stream
                                                _f(scales), _stream(stream)))
 
 
+def saef_compress_momentum(layout: Layout, K: int, lr: float, mu: float, g, m, e, signs, scales,
+                           stream=None):
+    _check("saef_compress_momentum",
+           _lib.saef_compress_momentum(layout.handle, K, lr, mu, _f(g), _f(m), _f(e), _w(signs),
+                                       _f(scales), _stream(stream)))
+
+
 def saef_aggregate(layout: Layout, K: int, mode: int, signs, scales, x, e_srv=None,
                    srv_signs=None, srv_scales=None, avg=None, stream=None):
     _check("saef_aggregate", _lib.saef_aggregate(layout.handle, K, mode, _w(signs), _f(scales),
@@ -174,6 +184,15 @@ def saef_round(layout: Layout, t: int, period: int, K: int, lr: float, mode: int
     _check("saef_round", _lib.saef_round(layout.handle, t, period, K, lr, mode, _f(g), _f(e),
                                          _f(e_srv), _f(x), _f(xh), _w(signs), _f(scales),
                                          _w(srv_signs), _f(srv_scales), _stream(stream)))
+
+
+def saef_round_momentum(layout: Layout, t: int, period: int, K: int, lr: float, mu: float,
+                        mode: int, g, m, e, e_srv, x, xh, signs, scales, srv_signs=None,
+                        srv_scales=None, stream=None):
+    _check("saef_round_momentum",
+           _lib.saef_round_momentum(layout.handle, t, period, K, lr, mu, mode, _f(g), _f(m),
+                                    _f(e), _f(e_srv), _f(x), _f(xh), _w(signs), _f(scales),
+                                    _w(srv_signs), _f(srv_scales), _stream(stream)))
 
 
 def saef_materialize(layout: Layout, K: int, mode: int, e, e_srv, x, signs, scales,

@@ -262,7 +262,8 @@ def gradients(w: Workload, t: int, K: int | None = None) -> np.ndarray:
     return np.stack([gradient(w, t, k, se) for k in range(K)])
 
 
-def algorithmic_bytes_per_param(K: int, mode: int = 1, averaging: bool = False) -> float:
+def algorithmic_bytes_per_param(K: int, mode: int = 1, averaging: bool = False,
+                                momentum: bool = False) -> float:
     """Bytes the method itself moves per parameter per round.
 
     step ahead: read x and e[k], write xh[k]            4 + 8K
@@ -271,8 +272,9 @@ def algorithmic_bytes_per_param(K: int, mode: int = 1, averaging: bool = False) 
       the server sign bits                                    16 + 1/8 + K/8
     server, single-way: read the K sign streams, read/write x    8 + K/8
     an error-averaging round also writes e[k] once more          + 4K
+    momentum: the worker step also reads and writes m[k]        + 8K
     """
     step = 4 + 8 * K
-    comp = 12 * K + K / 8
+    comp = (20 if momentum else 12) * K + K / 8
     server = (16 + 1 / 8 + K / 8) if mode == 1 else (8 + K / 8)
     return step + comp + server + (4 * K if averaging else 0)

@@ -63,10 +63,13 @@ def assert_words_equal(got: np.ndarray, want: np.ndarray, wmask: np.ndarray, wha
 
 
 class OracleState:
-    """Host state of Algorithm 1 advanced by the C oracle."""
+    """Host state of Algorithm 1 advanced by the C oracle (with momentum
+    constant mu when given)."""
 
-    def __init__(self, w: W.Workload, x0: np.ndarray | None = None, K: int | None = None):
+    def __init__(self, w: W.Workload, x0: np.ndarray | None = None, K: int | None = None,
+                 mu: float | None = None):
         self.w = w
+        self.mu = mu
         self.K = w.K if K is None else K
         off, n, d_pad = w.layout()
         self.orc = O.Oracle(off, n, d_pad)
@@ -78,23 +81,34 @@ class OracleState:
         self.scales = np.zeros((self.K, w.L), np.float32)
         self.srv_signs = np.zeros(d_pad // 64, np.uint64)
         self.srv_scales = np.zeros(w.L, np.float32)
+        self.m = np.zeros((self.K, d_pad), np.float32) if mu is not None else None
 
     def round(self, t: int, g: np.ndarray, period=None, mode=None):
         w = self.w
-        rc = self.orc.round(t, w.period if period is None else period, self.K, np.float32(w.lr),
-                            w.mode if mode is None else mode, g, self.e, self.e_srv, self.x,
-                            self.xh, self.signs, self.scales, self.srv_signs, self.srv_scales)
+        period = w.period if period is None else period
+        mode = w.mode if mode is None else mode
+        if self.mu is None:
+            rc = self.orc.round(t, period, self.K, np.float32(w.lr), mode, g, self.e, self.e_srv,
+                                self.x, self.xh, self.signs, self.scales, self.srv_signs,
+                                self.srv_scales)
+        else:
+            rc = self.orc.round_momentum(t, period, self.K, np.float32(w.lr),
+                                         np.float32(self.mu), mode, g, self.m, self.e,
+                                         self.e_srv, self.x, self.xh, self.signs, self.scales,
+                                         self.srv_signs, self.srv_scales)
         assert rc == O.OK, rc
 
 
 class GpuState:
-    """Device buffers of one workload driven through the HIP library."""
+    """Device buffers of one workload driven through the HIP library (with
+    momentum constant mu when given)."""
 
     def __init__(self, w: W.Workload, x0: np.ndarray | None = None, K: int | None = None,
-                 k_max: int | None = None):
+                 k_max: int | None = None, mu: float | None = None):
         from paper_2008_05823_amd import saef
         self.saef = saef
         self.w = w
+        self.mu = mu
         self.K = w.K if K is None else K
         off, n, d_pad = w.layout()
         self.off, self.n, self.d_pad = off, n, d_pad
@@ -110,6 +124,7 @@ class GpuState:
         self.srv_signs = torch.zeros(d_pad // 64, **i64)
         self.srv_scales = torch.zeros(w.L, **f32)
         self.g = torch.zeros((self.K, d_pad), **f32)
+        self.m = torch.zeros((self.K, d_pad), **f32) if mu is not None else None
 
     def round(self, t: int, g: np.ndarray | torch.Tensor, period=None, mode=None):
         w = self.w
@@ -117,10 +132,17 @@ class GpuState:
             self.g.copy_(torch.from_numpy(g))
         else:
             self.g.copy_(g)
-        self.saef.saef_round(self.layout, t, w.period if period is None else period, self.K,
-                             w.lr, w.mode if mode is None else mode, self.g, self.e,
-                             self.e_srv, self.x, self.xh, self.signs, self.scales,
-                             self.srv_signs, self.srv_scales)
+        period = w.period if period is None else period
+        mode = w.mode if mode is None else mode
+        if self.mu is None:
+            self.saef.saef_round(self.layout, t, period, self.K, w.lr, mode, self.g, self.e,
+                                 self.e_srv, self.x, self.xh, self.signs, self.scales,
+                                 self.srv_signs, self.srv_scales)
+        else:
+            self.saef.saef_round_momentum(self.layout, t, period, self.K, w.lr, self.mu, mode,
+                                          self.g, self.m, self.e, self.e_srv, self.x, self.xh,
+                                          self.signs, self.scales, self.srv_signs,
+                                          self.srv_scales)
 
     def plain(self, mode=None) -> dict:
         """Materialized (plain) state, downloaded to the host."""
@@ -132,9 +154,12 @@ class GpuState:
                                    self.signs, self.scales, self.srv_signs, self.srv_scales,
                                    e_out, es_out, x_out)
         torch.cuda.synchronize()
-        return dict(e=host(e_out), e_srv=host(es_out), x=host(x_out), xh=host(self.xh),
-                    signs=host(self.signs, np.uint64), scales=host(self.scales),
-                    srv_signs=host(self.srv_signs, np.uint64), srv_scales=host(self.srv_scales))
+        out = dict(e=host(e_out), e_srv=host(es_out), x=host(x_out), xh=host(self.xh),
+                   signs=host(self.signs, np.uint64), scales=host(self.scales),
+                   srv_signs=host(self.srv_signs, np.uint64), srv_scales=host(self.srv_scales))
+        if self.m is not None:
+            out["m"] = host(self.m)
+        return out
 
     def status(self) -> int:
         return self.saef.saef_status(self.layout)
@@ -151,6 +176,8 @@ def compare_state(gpu: dict, orc: OracleState, t: int, what: str = ""):
     assert_f32_equal(gpu["e"], orc.e, m, f"{tag} worker errors")
     assert_f32_equal(gpu["xh"], orc.xh, m, f"{tag} step-ahead weights")
     assert_f32_equal(gpu["x"], orc.x, m, f"{tag} weights")
+    if orc.m is not None:
+        assert_f32_equal(gpu["m"], orc.m, m, f"{tag} momentum buffers")
     if w.mode == 1:
         assert_words_equal(gpu["srv_signs"], orc.srv_signs, wm, f"{tag} server sign words")
         assert_f32_equal(gpu["srv_scales"], orc.srv_scales, np.ones(w.L, bool),

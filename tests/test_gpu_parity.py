@@ -151,6 +151,73 @@ def test_round_parity(name):
     assert gs.status() == 0
 
 
+@pytest.mark.parametrize("K,sizes", [(3, ADVERSARIAL), (8, [4096 * 3 + 17, 64, 1, 70000])])
+def test_compress_momentum_parity(K, sizes):
+    _case(f"compress with momentum K={K} sizes={sizes}")
+    rng = np.random.default_rng(K + 17)
+    w = W.custom(sizes, K=K, scale_range=(1e-3, 1.0), seed=K + 77)
+    off, n, d_pad = w.layout()
+    msk = W.tensor_mask(w)
+    g = W.gradients(w, 0)
+    e = _rand_err(rng, K, w)
+    m0 = _rand_err(rng, K, w, 0.5)
+    mu = np.float32(0.9)
+    orc = H.OracleState(w, mu=0.9)
+    orc.e[:] = e
+    orc.m[:] = m0
+    assert orc.orc.compress_momentum(K, LR, mu, g, orc.m, orc.e, orc.signs, orc.scales) == 0
+    gs = H.GpuState(w, mu=0.9)
+    gs.e.copy_(torch.from_numpy(e))
+    gs.m.copy_(torch.from_numpy(m0))
+    gs.saef.saef_compress_momentum(gs.layout, K, float(LR), float(mu), H.dev(g), gs.m, gs.e,
+                                   gs.signs, gs.scales)
+    assert gs.status() == 0
+    H.assert_words_equal(H.host(gs.signs, np.uint64), orc.signs,
+                         H.tensor_word_mask(off, n, d_pad), "signs")
+    H.assert_f32_equal(H.host(gs.scales), orc.scales, np.ones(w.L, bool), "scales")
+    H.assert_f32_equal(H.host(gs.e), orc.e, msk, "errors")
+    H.assert_f32_equal(H.host(gs.m), orc.m, msk, "momentum buffers")
+
+
+MOMENTUM_CASES = {
+    "flat64k": W.get("flat64k"),
+    "resnet56": W.get("resnet56").with_(rounds=12),
+    "ragged_sc": W.custom(ADVERSARIAL + [70001], K=3, period=3, rounds=7, mode=0,
+                          scale_range=(1e-4, 1e-1), dist="laplace_zeros", seed=998),
+}
+
+
+@pytest.mark.parametrize("name", list(MOMENTUM_CASES))
+def test_round_momentum_parity(name):
+    """saef_round_momentum (mu = 0.9, the paper's momentum constant) over
+    every iteration, state and momentum buffers compared with the oracle."""
+    w = MOMENTUM_CASES[name]
+    _case(f"momentum round parity {name} K={w.K} L={w.L} rounds={w.rounds}")
+    orc = H.OracleState(w, mu=0.9)
+    gs = H.GpuState(w, mu=0.9)
+    for t in range(w.rounds):
+        g = W.gradients(w, t)
+        orc.round(t, g)
+        gs.round(t, g)
+        H.compare_state(gs.plain(), orc, t, name)
+    assert gs.status() == 0
+
+
+def test_round_momentum_zero_equals_round():
+    """mu = 0 with zero momentum buffers is the plain iteration, bit for bit."""
+    w = W.get("resnet56").with_(period=3, rounds=5)
+    _case("momentum 0 vs plain round")
+    a = H.GpuState(w)
+    b = H.GpuState(w, mu=0.0)
+    for t in range(w.rounds):
+        g = W.gradients(w, t)
+        a.round(t, g)
+        b.round(t, g)
+    pa, pb = a.plain(), b.plain()
+    for key in pa:
+        assert pa[key].tobytes() == pb[key].tobytes(), key
+
+
 def test_round_equals_eager_ops():
     """The fused iteration and the four separate entry points called in
     Algorithm 1 order give identical states."""
