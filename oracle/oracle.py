@@ -54,6 +54,9 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "oracle_compress_momentum": lay + [i32, f32, f32, _P, _P, _P, _P, _P],
         "oracle_round_momentum": lay + [i64, i64, i32, f32, f32, i32, _P, _P, _P, _P, _P, _P,
                                         _P, _P, _P, _P],
+        "oracle_mismatch": lay + [i32, _P, _P, _P, _P],
+        "oracle_round_begin": lay + [i64, i64, i32, i32, i32, _P, _P, _P, _P, _P],
+        "oracle_round_end": lay + [i32, f32, f32, i32, _P, _P, _P, _P, _P, _P, _P, _P, _P],
     }
     for name, args in sigs.items():
         fn = getattr(lib, name)
@@ -122,6 +125,25 @@ class Oracle:
                                               _ptr(m), _ptr(e), _ptr(e_srv), _ptr(x), _ptr(xh),
                                               _ptr(signs), _ptr(scales), _ptr(srv_signs),
                                               _ptr(srv_scales))
+
+    def mismatch(self, K, e, e_srv=None):
+        """(ef, saef): per-tensor gradient-mismatch bounds (binary64)."""
+        ef = np.zeros(self.L, np.float64)
+        saef = np.zeros(self.L, np.float64)
+        rc = self.lib.oracle_mismatch(*self._lay(), K, _ptr(e), _ptr(e_srv), _ptr(ef),
+                                      _ptr(saef))
+        assert rc == 0, rc
+        return ef, saef
+
+    def round_begin(self, t, period, K, mode, variant, e, e_srv, x, xh, mismatch=None):
+        return self.lib.oracle_round_begin(*self._lay(), t, period, K, mode, variant, _ptr(e),
+                                           _ptr(e_srv), _ptr(x), _ptr(xh), _ptr(mismatch))
+
+    def round_end(self, K, lr, mu, mode, g, m, e, e_srv, x, signs, scales, srv_signs,
+                  srv_scales):
+        return self.lib.oracle_round_end(*self._lay(), K, lr, mu, mode, _ptr(g), _ptr(m),
+                                         _ptr(e), _ptr(e_srv), _ptr(x), _ptr(signs),
+                                         _ptr(scales), _ptr(srv_signs), _ptr(srv_scales))
 
     def step_ahead(self, K, x, e, xh):
         return self.lib.oracle_step_ahead(*self._lay(), K, _ptr(x), _ptr(e), _ptr(xh))

@@ -277,28 +277,97 @@ int oracle_error_average(int32_t L, const int64_t* off, const int64_t* n, int64_
     return ORACLE_OK;
 }
 
-/* ---- one iteration of Algorithm 1 (SAEF branch, mu = 0) ----------------- */
+/* ---- gradient-mismatch bounds ("Gradient Mismatch", "Step Ahead" and
+ * "Error Averaging" sections, with the Lipschitz constant and the variance
+ * term left out) ------------------------------------------------------------
+ *
+ * With the server error e_t and the mean of the local errors ebar, local
+ * error feedback evaluates worker k's gradient at x_t while the auxiliary
+ * variable sits at x_t - (e_t + ebar); step ahead evaluates it at x_t - e^(k)_t.
+ * The squared distances, summed over the elements of tensor l:
+ *   ef[l]   = || e_t + ebar ||^2
+ *   saef[l] = (1/K) sum_k || e_t + ebar - e^(k)_t ||^2
+ * all in binary64: ebar_i = (sum_k e^(k)_i, worker order) / K. */
+int oracle_mismatch(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                    int32_t K, const float* e, const float* e_srv, double* ef, double* saef)
+{
+    int rc = check_layout(L, off, n, d_pad);
+    if (rc != ORACLE_OK) return rc;
+    if (K < 1 || e == NULL || ef == NULL || saef == NULL) return ORACLE_EINVAL;
+    for (int32_t l = 0; l < L; ++l) {
+        double a = 0.0, b = 0.0;
+        for (int64_t i = 0; i < n[l]; ++i) {
+            int64_t j = off[l] + i;
+            double sum = 0.0;
+            for (int32_t k = 0; k < K; ++k) sum += (double)e[(int64_t)k * d_pad + j];
+            double ebar = sum / (double)K;
+            /* single-way compression has no server error (e_srv == NULL) */
+            double u = (e_srv != NULL ? (double)e_srv[j] : 0.0) + ebar;
+            a += u * u;
+            for (int32_t k = 0; k < K; ++k) {
+                double dk = u - (double)e[(int64_t)k * d_pad + j];
+                b += dk * dk;
+            }
+        }
+        ef[l] = a;
+        saef[l] = b / (double)K;
+    }
+    return ORACLE_OK;
+}
+
+/* ---- one iteration of Algorithm 1, in two halves around the gradient ----- */
+
+int oracle_round_begin(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                       int64_t t, int64_t period, int32_t K, int32_t mode, int32_t variant,
+                       float* e, const float* e_srv, const float* x, float* xh, double* mismatch)
+{
+    if (t < 0 || period < 0) return ORACLE_EINVAL;
+    if (variant != 0 && variant != 1) return ORACLE_EINVAL;
+    int rc = check_layout(L, off, n, d_pad);
+    if (rc != ORACLE_OK) return rc;
+    if (x == NULL || xh == NULL) return ORACLE_EINVAL;
+    if (period > 0 && (t + 1) % period == 0) {
+        rc = oracle_error_average(L, off, n, d_pad, K, e);
+        if (rc != ORACLE_OK) return rc;
+    }
+    if (mismatch != NULL) {
+        rc = oracle_mismatch(L, off, n, d_pad, K, e, mode == 1 ? e_srv : NULL, mismatch,
+                             mismatch + L);
+        if (rc != ORACLE_OK) return rc;
+    }
+    if (variant == 1) /* SAEF: one step ahead */
+        return oracle_step_ahead(L, off, n, d_pad, K, x, e, xh);
+    /* local error feedback: the gradient is taken at the weights themselves */
+    for (int32_t l = 0; l < L; ++l)
+        for (int64_t i = 0; i < n[l]; ++i) xh[off[l] + i] = x[off[l] + i];
+    return ORACLE_OK;
+}
+
+int oracle_round_end(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                     int32_t K, float lr, float mu, int32_t mode, const float* g, float* m,
+                     float* e, float* e_srv, float* x, uint64_t* signs, float* scales,
+                     uint64_t* srv_signs, float* srv_scales)
+{
+    /* the gradient at xh is the caller's input g */
+    int status = (m != NULL)
+        ? oracle_compress_momentum(L, off, n, d_pad, K, lr, mu, g, m, e, signs, scales)
+        : oracle_compress(L, off, n, d_pad, K, lr, g, e, signs, scales);
+    if (status == ORACLE_EINVAL) return status;
+    int rc = oracle_aggregate(L, off, n, d_pad, K, mode, signs, scales, NULL, e_srv,
+                              srv_signs, srv_scales, x);
+    if (rc != ORACLE_OK) status = rc;
+    return status;
+}
 
 int oracle_round(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
                  int64_t t, int64_t period, int32_t K, float lr, int32_t mode,
                  const float* g, float* e, float* e_srv, float* x, float* xh,
                  uint64_t* signs, float* scales, uint64_t* srv_signs, float* srv_scales)
 {
-    if (t < 0 || period < 0) return ORACLE_EINVAL;
-    int rc;
-    if (period > 0 && (t + 1) % period == 0) {
-        rc = oracle_error_average(L, off, n, d_pad, K, e);
-        if (rc != ORACLE_OK) return rc;
-    }
-    rc = oracle_step_ahead(L, off, n, d_pad, K, x, e, xh);
+    int rc = oracle_round_begin(L, off, n, d_pad, t, period, K, mode, 1, e, e_srv, x, xh, NULL);
     if (rc != ORACLE_OK) return rc;
-    /* the gradient at xh is the caller's input g */
-    int status = oracle_compress(L, off, n, d_pad, K, lr, g, e, signs, scales);
-    if (status == ORACLE_EINVAL) return status;
-    rc = oracle_aggregate(L, off, n, d_pad, K, mode, signs, scales, NULL, e_srv,
-                          srv_signs, srv_scales, x);
-    if (rc != ORACLE_OK) status = rc;
-    return status;
+    return oracle_round_end(L, off, n, d_pad, K, lr, 0.0f, mode, g, NULL, e, e_srv, x, signs,
+                            scales, srv_signs, srv_scales);
 }
 
 int oracle_round_momentum(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
@@ -307,19 +376,9 @@ int oracle_round_momentum(int32_t L, const int64_t* off, const int64_t* n, int64
                           uint64_t* signs, float* scales, uint64_t* srv_signs,
                           float* srv_scales)
 {
-    if (t < 0 || period < 0) return ORACLE_EINVAL;
-    int rc;
-    if (period > 0 && (t + 1) % period == 0) {
-        rc = oracle_error_average(L, off, n, d_pad, K, e);
-        if (rc != ORACLE_OK) return rc;
-    }
-    rc = oracle_step_ahead(L, off, n, d_pad, K, x, e, xh);
+    if (m == NULL) return ORACLE_EINVAL;
+    int rc = oracle_round_begin(L, off, n, d_pad, t, period, K, mode, 1, e, e_srv, x, xh, NULL);
     if (rc != ORACLE_OK) return rc;
-    /* the gradient at xh is the caller's input g */
-    int status = oracle_compress_momentum(L, off, n, d_pad, K, lr, mu, g, m, e, signs, scales);
-    if (status == ORACLE_EINVAL) return status;
-    rc = oracle_aggregate(L, off, n, d_pad, K, mode, signs, scales, NULL, e_srv,
-                          srv_signs, srv_scales, x);
-    if (rc != ORACLE_OK) status = rc;
-    return status;
+    return oracle_round_end(L, off, n, d_pad, K, lr, mu, mode, g, m, e, e_srv, x, signs, scales,
+                            srv_signs, srv_scales);
 }

@@ -65,6 +65,32 @@ int oracle_step_ahead(int32_t L, const int64_t* off, const int64_t* n, int64_t d
 int oracle_error_average(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
                          int32_t K, float* e);
 
+/* Gradient-mismatch bounds of the "Step Ahead" and "Error Averaging"
+ * sections (Lipschitz constant and variance term left out), per tensor l:
+ *   ef[l]   = sum_i (e_srv_i + ebar_i)^2                      local error feedback
+ *   saef[l] = (1/K) sum_k sum_i (e_srv_i + ebar_i - e[k]_i)^2     step ahead
+ * in binary64, ebar_i = (sum_k e[k]_i in worker order) / K.  e_srv NULL
+ * means no server error (single-way compression). */
+int oracle_mismatch(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                    int32_t K, const float* e, const float* e_srv, double* ef, double* saef);
+
+/* First half of iteration t of Algorithm 1, up to the gradient: error
+ * averaging when (t+1) mod period == 0 (period 0 = never), then the point
+ * where the gradient is taken: variant 1 (SAEF) xh[k] = x - e[k] for every
+ * worker; variant 0 (local error feedback, the EF branch) xh[0..d_pad) = x.
+ * mismatch (may be NULL): 2 L doubles, oracle_mismatch of the state after
+ * averaging (ef in [0, L), saef in [L, 2 L)); mode 0 ignores e_srv. */
+int oracle_round_begin(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                       int64_t t, int64_t period, int32_t K, int32_t mode, int32_t variant,
+                       float* e, const float* e_srv, const float* x, float* xh, double* mismatch);
+
+/* Second half: worker compression (oracle_compress_momentum when m is not
+ * NULL, else oracle_compress), then oracle_aggregate. */
+int oracle_round_end(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                     int32_t K, float lr, float mu, int32_t mode, const float* g, float* m,
+                     float* e, float* e_srv, float* x, uint64_t* signs, float* scales,
+                     uint64_t* srv_signs, float* srv_scales);
+
 /* One full iteration t of Algorithm 1 (SAEF branch, mu = 0) in the paper's
  * order: error averaging when (t+1) mod period == 0 (period 0 = never),
  * step ahead, [gradient g supplied], worker compression, server, re-update. */

@@ -82,15 +82,27 @@ def _run_golden(libpath, name):
         xh = np.zeros((K, d_pad), np.float32)
         srv_signs = np.zeros(W, np.uint64)
         srv_scales = np.zeros(L, np.float32)
+        variant = int(gd["variant"][0]) if "variant" in gd else None
+        mism = np.zeros(2 * L, np.float64)
         for t in range(rounds):
             g = np.stack([vec(gd[f"g.{t}.{k}"]) for k in range(K)])
-            if mu is None:
+            if variant is not None:
+                # the two halves of the iteration, with the mismatch bounds
+                rc = orc.round_begin(t, period, K, mode, variant, e, e_srv, x, xh, mism)
+                assert rc == O.OK, name
+                rc = orc.round_end(K, lr, 0.0, mode, g, None, e, e_srv, x, signs, scales,
+                                   srv_signs, srv_scales)
+            elif mu is None:
                 rc = orc.round(t, period, K, lr, mode, g, e, e_srv, x, xh, signs, scales,
                                srv_signs, srv_scales)
             else:
                 rc = orc.round_momentum(t, period, K, lr, mu, mode, g, m, e, e_srv, x, xh, signs,
                                         scales, srv_signs, srv_scales)
             assert rc == O.OK, name
+        if "expect.mismatch_ef" in gd:
+            assert np.array_equal(mism[:L], golden_io.floats(gd["expect.mismatch_ef"])), (name, mism)
+            assert np.array_equal(mism[L:], golden_io.floats(gd["expect.mismatch_saef"])), (name,
+                                                                                             mism)
     n0 = sizes[0]
     exp_scales = golden_io.floats(gd["expect.scales"])
     assert np.array_equal(scales.reshape(-1), exp_scales), (name, scales, exp_scales)
@@ -472,7 +484,120 @@ def pin_auxiliary_identity_momentum(libpath):
         assert (err <= 8 * 2.0 ** -24 * mag[msk] + 1e-30).all(), (mode, period, float(err.max()))
 
 
-QUICK_PINS = [pin_goldens, pin_momentum_exact, pin_auxiliary_identity_momentum, pin_l1_fixed_exact, pin_compress_exact, pin_aggregate_exact,
+def run_split_rounds(libpath, w, rounds, variant, gens=None):
+    """Run the two halves of each iteration (round_begin with the mismatch
+    bounds, round_end) over `rounds` iterations of workload w; records the
+    state seen by the bounds (after averaging) and the end state."""
+    from paper_2008_05823_amd import workloads as W
+    off, n, d_pad = w.layout()
+    orc = O.Oracle(off, n, d_pad, libpath)
+    K, L = w.K, w.L
+    x = W.initial_x(w)
+    e = np.zeros((K, d_pad), np.float32)
+    e_srv = np.zeros(d_pad, np.float32)
+    xh = np.zeros((K, d_pad), np.float32)
+    signs = np.zeros((K, d_pad // 64), np.uint64)
+    scales = np.zeros((K, L), np.float32)
+    srv_signs = np.zeros(d_pad // 64, np.uint64)
+    srv_scales = np.zeros(L, np.float32)
+    hist = []
+    for t in range(rounds):
+        g = W.gradients(w, t) if gens is None else gens(t)
+        mism = np.full(2 * L, np.nan)
+        x_start = x.copy()
+        assert orc.round_begin(t, w.period, K, w.mode, variant, e, e_srv, x, xh, mism) == O.OK
+        seen = dict(e=e.copy(), e_srv=e_srv.copy(), x=x_start)
+        assert orc.round_end(K, np.float32(w.lr), 0.0, w.mode, g, None, e, e_srv, x, signs,
+                             scales, srv_signs, srv_scales) == O.OK
+        hist.append(dict(g=g, mism=mism, seen=seen, xh=xh.copy(), x=x.copy(), e=e.copy(),
+                         e_srv=e_srv.copy(), signs=signs.copy(), scales=scales.copy(),
+                         srv_signs=srv_signs.copy(), srv_scales=srv_scales.copy()))
+    return hist
+
+
+def _per_tensor(v, off, n):
+    return np.array([v[..., o:o + m].sum() for o, m in zip(off, n)])
+
+
+def pin_mismatch_identities(libpath):
+    """The two bounds against identities that hold in exact arithmetic:
+    (1/K) sum_k ||u - e^(k)||^2 = ||e_srv||^2 + (1/K) sum_k ||ebar - e^(k)||^2
+    (the cross term vanishes because sum_k (ebar - e^(k)) = 0), and
+    ||u||^2 = SAEF bound + 2 <u, ebar> - (1/K) sum_k ||e^(k)||^2; at an
+    averaging iteration the step-ahead bound is the server error alone,
+    ||e_t||^2 (zero in single-way compression) -- the "Error Averaging" bound."""
+    from paper_2008_05823_amd import workloads as W
+    cases = [W.custom([300, 64, 1, 129], K=3, period=3, rounds=6, scale_range=(1e-3, 1.0),
+                      seed=31),
+             W.custom([1000, 17], K=4, period=2, rounds=4, mode=0, scale_range=(0.01, 1.0),
+                      seed=32, dist="laplace_zeros")]
+    for w in cases:
+        off, n, _ = w.layout()
+        for t, h in enumerate(run_split_rounds(libpath, w, w.rounds, variant=1)):
+            e = h["seen"]["e"].astype(np.float64)
+            es = h["seen"]["e_srv"].astype(np.float64) if w.mode == 1 else 0.0 * e[0]
+            ebar = e.mean(axis=0)
+            u = es + ebar
+            ef, sa = h["mism"][:w.L], h["mism"][w.L:]
+            srv2 = _per_tensor(es * es, off, n)
+            var = _per_tensor(((ebar - e) ** 2).mean(axis=0), off, n)
+            np.testing.assert_allclose(sa, srv2 + var, rtol=1e-12, atol=1e-300)
+            cross = _per_tensor(u * ebar, off, n)
+            ek2 = _per_tensor((e * e).mean(axis=0), off, n)
+            scale = ef + sa + 2 * np.abs(cross) + ek2
+            assert np.all(np.abs(ef - (sa + 2 * cross - ek2)) <= 1e-12 * scale), (t, ef)
+            if (t + 1) % w.period == 0:
+                if w.mode == 0:
+                    assert np.all(sa == 0.0), (t, sa)
+                else:
+                    np.testing.assert_allclose(sa, srv2, rtol=1e-12)
+
+
+def pin_mismatch_proposition(libpath):
+    """Proposition of the "Step Ahead" section, single-way (no server error):
+    for the same local errors the step-ahead bound is the smaller one exactly
+    when the spread of the errors across workers is at most the squared norm
+    of their mean."""
+    rng = np.random.default_rng(33)
+    off, n, d_pad = _one_tensor_layout([500])
+    orc = O.Oracle(off, n, d_pad, libpath)
+    K = 5
+    seen = set()
+    for trial in range(40):
+        c = rng.standard_normal(500).astype(np.float32)
+        spread = np.float32(10.0 ** rng.uniform(-2, 1))
+        e = np.zeros((K, d_pad), np.float32)
+        e[:, :500] = c + spread * rng.standard_normal((K, 500)).astype(np.float32)
+        ef, sa = orc.mismatch(K, e)
+        e64 = e[:, :500].astype(np.float64)
+        var = ((e64 - e64.mean(axis=0)) ** 2).sum() / K
+        mean2 = (e64.mean(axis=0) ** 2).sum()
+        assert (sa[0] <= ef[0]) == (var <= mean2), (trial, sa, ef, var, mean2)
+        seen.add(bool(var <= mean2))
+    assert seen == {True, False}
+
+
+def pin_ef_variant(libpath):
+    """Local error feedback (the EF branch) takes the gradient at x_t itself;
+    both branches form Delta^(k) = e^(k) + eta m^(k) (Algorithm 1), so with
+    gradients that do not depend on the evaluation point the two branches
+    produce the same state, bit for bit, and only the evaluation points
+    differ: x_t for EF, x_t - e^(k)_t for SAEF."""
+    from paper_2008_05823_amd import workloads as W
+    w = W.custom([200, 64, 3], K=3, period=3, rounds=5, scale_range=(0.01, 1.0), seed=34)
+    ef = run_split_rounds(libpath, w, w.rounds, variant=0)
+    sa = run_split_rounds(libpath, w, w.rounds, variant=1)
+    for a, b in zip(ef, sa):
+        for key in ("x", "e", "e_srv", "signs", "scales", "srv_signs", "srv_scales"):
+            assert np.array_equal(a[key], b[key]), key
+        np.testing.assert_array_equal(a["mism"], b["mism"])
+        assert np.array_equal(a["xh"][0], a["seen"]["x"])
+        for k in range(w.K):
+            exp = (b["seen"]["x"] - b["seen"]["e"][k]).astype(np.float32)
+            assert np.array_equal(b["xh"][k], exp)
+
+
+QUICK_PINS = [pin_goldens, pin_mismatch_identities, pin_mismatch_proposition, pin_ef_variant, pin_momentum_exact, pin_auxiliary_identity_momentum, pin_l1_fixed_exact, pin_compress_exact, pin_aggregate_exact,
               pin_step_ahead_and_average_exact, pin_auxiliary_identity,
               pin_delta_compressor_equality, pin_zero_error_is_scaled_signsgd,
               pin_identical_workers, pin_period_one]

@@ -33,6 +33,14 @@ MUTANTS = {
     "l1_rounds_not_floors": ("S += (u128)scaled;", "S += (u128)(scaled + 0.5);"),
     "decode_swapped": ("return bit ? scale : -scale;", "return bit ? -scale : scale;"),
     "worker_stride": ("float* ek = e + (int64_t)k * d_pad;", "float* ek = e + (int64_t)(K - 1 - k) * d_pad;"),
+    "mismatch_drops_server_error": ("double u = (e_srv != NULL ? (double)e_srv[j] : 0.0) + ebar;",
+                                    "double u = ebar;"),
+    "mismatch_mean_not_divided": ("double ebar = sum / (double)K;", "double ebar = sum;"),
+    "mismatch_saef_not_divided": ("saef[l] = b / (double)K;", "saef[l] = b;"),
+    "mismatch_sign": ("double dk = u - (double)e[", "double dk = u + (double)e["),
+    "mismatch_ef_not_squared": ("a += u * u;", "a += fabs(u);"),
+    "ef_variant_steps_ahead": ("if (variant == 1) /* SAEF: one step ahead */",
+                               "if (variant >= 0) /* SAEF: one step ahead */"),
     "momentum_dropped": ("mk[j] = fmaf(mu, mk[j], gk[j]);", "mk[j] = gk[j];"),
     "momentum_swapped": ("mk[j] = fmaf(mu, mk[j], gk[j]);", "mk[j] = fmaf(mu, gk[j], mk[j]);"),
     "momentum_lr_dropped": ("ek[j] = fmaf(lr, mk[j], ek[j]);", "ek[j] = mk[j] + ek[j];"),
