@@ -122,6 +122,11 @@ def main() -> int:
     ap.add_argument("--no-probe", action="store_true", help="skip the copy-bandwidth probe")
     ap.add_argument("--momentum", type=float, default=None,
                     help="momentum constant mu in [0, 1): time saef_round_momentum")
+    ap.add_argument("--variant", choices=("saef", "ef"), default="saef",
+                    help="saef: step ahead (default); ef: local error feedback, the gradient "
+                         "is taken at x_t (saef_round_begin / saef_round_end)")
+    ap.add_argument("--mismatch", action="store_true",
+                    help="compute the gradient-mismatch bounds in every iteration")
     ap.add_argument("--kernel-events", choices=("on", "off"), default="on",
                     help="HIP events around each kernel in the timed region (roofline); "
                          "'off' times the iterations alone")
@@ -159,9 +164,19 @@ def main() -> int:
     layout = saef.Layout(off, n, d_pad, K)
     mu = args.momentum
     m = torch.zeros((K, d_pad), **f32) if mu is not None else None
+    split = args.variant == "ef" or args.mismatch
+    variant = saef.VARIANT_EF if args.variant == "ef" else saef.VARIANT_SAEF
+    mism = torch.zeros(2 * L, dtype=torch.float64, device="cuda") if args.mismatch else None
+    xh_arg = xh if variant == saef.VARIANT_SAEF else xh[0]
 
     def step(t):
-        if mu is None:
+        if split:
+            saef.saef_round_begin(layout, t, w.period, K, w.mode, variant, e, e_srv, x, xh_arg,
+                                  signs, scales, srv_signs, srv_scales, mism)
+            saef.saef_round_end(layout, t, w.period, K, w.lr, 0.0 if mu is None else mu, w.mode,
+                                g_dev[t % n_grad], m, e, e_srv, x, signs, scales, srv_signs,
+                                srv_scales)
+        elif mu is None:
             saef.saef_round(layout, t, w.period, K, w.lr, w.mode, g_dev[t % n_grad], e, e_srv, x,
                             xh, signs, scales, srv_signs, srv_scales)
         else:
@@ -194,14 +209,15 @@ def main() -> int:
     n_avg = sum(1 for t in timed_ts if w.period and (t + 1) % w.period == 0)
     bytes_round = np.mean([W.algorithmic_bytes_per_param(
         K, w.mode, averaging=bool(w.period and (t + 1) % w.period == 0),
-        momentum=mu is not None) for t in timed_ts]) * d
+        momentum=mu is not None, step_ahead=variant == saef.VARIANT_SAEF,
+        mismatch=args.mismatch) for t in timed_ts]) * d
 
     # dominant kernel: worker compression (12 K + K/8 bytes per parameter,
     # 20 K + K/8 with momentum)
     c_count, c_ms = prof["compress"]
     c_bytes = ((20 if mu is not None else 12) * K + K / 8) * d
     c_gbps = c_bytes / (c_ms / c_count * 1e-3) / 1e9 if c_count else None
-    traffic = traffic_from_profile(args.workload) if mu is None else None
+    traffic = traffic_from_profile(args.workload) if (mu is None and not split) else None
 
     # breakdown of every kernel, from a separate pass of the same length (each
     # timed dispatch costs a few microseconds, so it is kept out of the value)
@@ -232,9 +248,14 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": f"{w.name}: {L} tensors, d={d}, K={K} simulated workers, "
                                f"double-way, lr={w.lr}, error averaging period {w.period}"
-                               + (f", momentum {mu}" if mu is not None else ""),
-                   "K": K, "d": d, "L": L, "period": w.period, "mode": "DC",
-                   **({"momentum": mu} if mu is not None else {})},
+                               + (f", momentum {mu}" if mu is not None else "")
+                               + (", local error feedback" if args.variant == "ef" else "")
+                               + (", mismatch bounds" if args.mismatch else ""),
+                   "K": K, "d": d, "L": L, "period": w.period,
+                   "mode": "DC" if w.mode == 1 else "SC",
+                   **({"momentum": mu} if mu is not None else {}),
+                   **({"variant": "ef"} if args.variant == "ef" else {}),
+                   **({"mismatch": True} if args.mismatch else {})},
         "worker_params_per_s": K * d / (ms_per_step * 1e-3),
         "round_hbm_gbps": bytes_round / (ms_per_step * 1e-3) / 1e9,
         "round_frac_of_peak": bytes_round / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,

@@ -69,6 +69,9 @@ extern "C" {
 #define SAEF_MODE_SC 0 /* single-way: the server returns the mean uncompressed */
 #define SAEF_MODE_DC 1 /* double-way: Algorithm 1 (server error + server message) */
 
+#define SAEF_VARIANT_EF 0   /* local error feedback: gradient taken at x_t (EF branch) */
+#define SAEF_VARIANT_SAEF 1 /* step ahead: gradient taken at x_t - e^(k)_t (SAEF branch) */
+
 typedef struct saef_layout saef_layout;
 
 /* Layer-wise compression needs one scale per tensor (Experiments: all
@@ -149,6 +152,43 @@ int saef_round_momentum(const saef_layout* layout, int64_t t, int64_t period, in
                         float* e_srv, float* x, float* xh, uint64_t* signs, float* scales,
                         uint64_t* srv_signs, float* srv_scales, hipStream_t stream);
 
+/* saef_round in two halves around the gradient, for callers that compute
+ * the gradient at the evaluation point the first half writes (Algorithm 1,
+ * both branches).  Same state form, t conventions and arguments as
+ * saef_round; calling saef_round_begin(t, variant SAEF_VARIANT_SAEF) and then
+ * saef_round_end(t) with the same t and period gives exactly saef_round(t).
+ *
+ * saef_round_begin: error averaging when (t+1) mod period == 0 (period 0 =
+ * never; both variants, e is then left plain), then the evaluation point:
+ *   SAEF_VARIANT_SAEF  xh[k] = x_t - e^(k)_t, xh is (K, d_pad)    step ahead
+ *   SAEF_VARIANT_EF    xh    = x_t,          xh is (d_pad)        local EF
+ * x and e_srv are read only.  mismatch (device, 2 L doubles, may be NULL):
+ * the gradient-mismatch bounds of the "Gradient Mismatch", "Step Ahead" and
+ * "Error Averaging" sections without the Lipschitz constant and the
+ * variance term, per tensor l, from the state after averaging:
+ *   mismatch[l]     = sum_i (e_srv_i + ebar_i)^2          (local error feedback)
+ *   mismatch[L + l] = (1/K) sum_k sum_i (e_srv_i + ebar_i - e^(k)_i)^2   (step ahead)
+ * in binary64 with ebar_i = (sum_k e^(k)_i, worker order) / K and e_srv = 0
+ * in SAEF_MODE_SC (e_srv may then be NULL).  Each element's terms are exact
+ * functions of the state; the sums over a tensor are taken in a fixed order
+ * of the library's own (deterministic run to run, not the sequential order),
+ * so they agree with a sequential binary64 sum to within 2 n_l K 2^-53
+ * relative.  Signs/scales (and srv_* in DC) are read only when t > 0.
+ *
+ * saef_round_end: worker compression (with momentum m, 0 <= mu < 1, when m
+ * is not NULL; m == NULL requires mu == 0), server aggregation and
+ * compression, re-update.  g holds the gradients the caller computed at the
+ * evaluation points of saef_round_begin(t). */
+int saef_round_begin(const saef_layout* layout, int64_t t, int64_t period, int32_t K,
+                     int32_t mode, int32_t variant, float* e, const float* e_srv, const float* x,
+                     float* xh, const uint64_t* signs, const float* scales,
+                     const uint64_t* srv_signs, const float* srv_scales, double* mismatch,
+                     hipStream_t stream);
+int saef_round_end(const saef_layout* layout, int64_t t, int64_t period, int32_t K, float lr,
+                   float mu, int32_t mode, const float* g, float* m, float* e, float* e_srv,
+                   float* x, uint64_t* signs, float* scales, uint64_t* srv_signs,
+                   float* srv_scales, hipStream_t stream);
+
 /* Plain values of a saef_round state: writes e_true to e_out (K, d_pad),
  * e_srv_true to e_srv_out and x_true to x_out (each may be NULL to skip, and
  * may equal its input to convert in place -- the state is then plain and a
@@ -163,16 +203,18 @@ int saef_materialize(const saef_layout* layout, int32_t K, int32_t mode, const f
  * |v| >= 2^19, Inf or NaN, SAEF_OK otherwise (SAEF_EHIP on a HIP error). */
 int saef_status(const saef_layout* layout, hipStream_t stream);
 
-/* Per-kernel timing of saef_round, for measurement.  saef_profile_enable
- * with capacity > 0 creates that many HIP event pairs; every later
- * saef_round on this layout then has the dispatch of each kernel whose kind
- * bit is set in kind_mask stamp its start and end into a free pair (kind 0 =
- * step ahead, 1 = worker compression, 2 = worker scales from the tile sums,
- * 3 = server aggregation, 4 = server scales, 5 = step ahead of an
- * error-averaging iteration), until the pairs run out.  saef_profile_read
- * waits for the recorded events and returns, per kind, the number of
- * launches timed (counts[6]) and their summed durations in milliseconds
- * (total_ms[6]), then starts over with all pairs free.  capacity 0 releases
+/* Per-kernel timing of saef_round (and its halves), for measurement.
+ * saef_profile_enable with capacity > 0 creates that many HIP event pairs;
+ * every later saef_round / saef_round_begin / saef_round_end on this layout
+ * then has the dispatch of each kernel whose kind bit is set in kind_mask
+ * stamp its start and end into a free pair (kind 0 = step ahead, or the
+ * copy of x_t for local error feedback, 1 = worker compression, 2 = worker
+ * scales from the tile sums, 3 = server aggregation, 4 = server scales, 5 =
+ * error averaging (with step ahead in the SAEF variant), 6 = mismatch
+ * bounds), until the pairs run out.  saef_profile_read waits for the
+ * recorded events and returns, per kind, the number of launches timed
+ * (counts[7]) and their summed durations in milliseconds (total_ms[7]), then
+ * starts over with all pairs free.  capacity 0 releases
  * the events and stops recording.  Timed dispatches cost a few microseconds
  * each, so time only the kernels of interest. */
 int saef_profile_enable(saef_layout* layout, int32_t capacity, uint32_t kind_mask);

@@ -47,7 +47,7 @@ int64_t tile_elems(int64_t n) {
   return t;
 }
 
-constexpr int kProfileKinds = 6;
+constexpr int kProfileKinds = 7;
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -302,41 +302,101 @@ int saef_error_average(const saef_layout* layout, int32_t K, float* e, hipStream
 namespace {
 
 // saef_round / saef_round_momentum (m == nullptr: no momentum).
-int round_impl(const saef_layout* layout, int64_t t, int64_t period, int32_t K, float lr,
-               float mu, int32_t mode, const float* g, float* m, float* e, float* e_srv,
-               float* x, float* xh, uint64_t* signs, float* scales, uint64_t* srv_signs,
-               float* srv_scales, hipStream_t stream) {
+// The first half of iteration t (Algorithm 1 up to the gradient): error
+// averaging when due, the mismatch bounds when requested, then the point
+// where the gradient is taken (step ahead, or the weights themselves for
+// local error feedback).  The state is in saef_round's pending form.
+int round_begin_impl(const saef_layout* layout, int64_t t, int64_t period, int32_t K,
+                     int32_t mode, int32_t variant, float* e, const float* e_srv, const float* x,
+                     float* xh, const uint64_t* signs, const float* scales,
+                     const uint64_t* srv_signs, const float* srv_scales, double* mismatch,
+                     hipStream_t stream) {
+  int rc = check_common(layout, K);
+  if (rc != SAEF_OK) return rc;
+  if (t < 0 || period < 0) return SAEF_EINVAL;
+  if (mode != SAEF_MODE_SC && mode != SAEF_MODE_DC) return SAEF_EINVAL;
+  if (variant != SAEF_VARIANT_EF && variant != SAEF_VARIANT_SAEF) return SAEF_EINVAL;
+  const bool pending = t > 0;  // at t == 0 the state is plain (Algorithm 1 initialisation)
+  const bool averaging = period > 0 && (t + 1) % period == 0;
+  const bool dc = mode == SAEF_MODE_DC;
+  if (!f32_ok(e) || !f32_ok(x) || !f32_ok(xh)) return SAEF_EINVAL;
+  if (pending && (!u64_ok(signs) || !f32_ok(scales))) return SAEF_EINVAL;
+  if (pending && dc && (!u64_ok(srv_signs) || !f32_ok(srv_scales))) return SAEF_EINVAL;
+  if (mismatch != nullptr && (!aligned(mismatch, 8) || (dc && !f32_ok(e_srv))))
+    return SAEF_EINVAL;
+  const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
+  const size_t xb = layout->d_pad * sizeof(float);
+  const size_t hb = variant == SAEF_VARIANT_SAEF ? vb : xb;
+  if (overlap(xh, hb, x, xb) || overlap(xh, hb, e, vb) ||
+      (e_srv != nullptr && overlap(xh, hb, e_srv, xb)))
+    return SAEF_EINVAL;
+  if (mismatch != nullptr) {
+    const size_t mb = 2 * (size_t)layout->L * sizeof(double);
+    if (overlap(mismatch, mb, e, vb) || overlap(mismatch, mb, xh, hb) ||
+        overlap(mismatch, mb, x, xb) || (e_srv != nullptr && overlap(mismatch, mb, e_srv, xb)))
+      return SAEF_EINVAL;
+  }
+  const DevLayout& d = layout->dev;
+  if (variant == SAEF_VARIANT_SAEF) {
+    // error averaging (when due) and step ahead, applying last iteration's
+    // pending corrections to e and (double-way) x
+    rc = hip_rc(timed(layout, averaging ? 5 : 0, [&](const saef::LaunchEvents& ev) {
+      return saef::launch_step_ahead(d, K, x, srv_signs, srv_scales, pending && dc, e, signs,
+                                     scales, pending, averaging, xh, stream, ev);
+    }));
+    if (rc != SAEF_OK) return rc;
+  } else if (averaging) {
+    // local error feedback with error averaging: average only
+    rc = hip_rc(timed(layout, 5, [&](const saef::LaunchEvents& ev) {
+      return saef::launch_step_ahead(d, K, x, srv_signs, srv_scales, false, e, signs, scales,
+                                     pending, true, nullptr, stream, ev);
+    }));
+    if (rc != SAEF_OK) return rc;
+  }
+  if (mismatch != nullptr) {
+    // the errors are plain after an averaging step
+    rc = hip_rc(timed(layout, 6, [&](const saef::LaunchEvents& ev) {
+      return saef::launch_mismatch(d, K, mode, e, signs, scales, pending && !averaging, e_srv,
+                                   srv_signs, srv_scales, pending && dc, mismatch, stream, ev);
+    }));
+    if (rc != SAEF_OK) return rc;
+  }
+  if (variant == SAEF_VARIANT_SAEF) return SAEF_OK;
+  // local error feedback: the gradient is taken at x_t itself (one row)
+  return hip_rc(timed(layout, 0, [&](const saef::LaunchEvents& ev) {
+    return saef::launch_materialize(d, K, (pending && dc) ? SAEF_MODE_DC : SAEF_MODE_SC, nullptr,
+                                    nullptr, nullptr, nullptr, nullptr, x, srv_signs, srv_scales,
+                                    nullptr, xh, stream, ev);
+  }));
+}
+
+// The second half of iteration t: worker compression (momentum update first
+// when m is given), worker scales, server aggregation and compression,
+// server scales.  e is plain when the first half averaged it.
+int round_end_impl(const saef_layout* layout, int64_t t, int64_t period, int32_t K, float lr,
+                   float mu, int32_t mode, const float* g, float* m, float* e, float* e_srv,
+                   float* x, uint64_t* signs, float* scales, uint64_t* srv_signs,
+                   float* srv_scales, hipStream_t stream) {
   int rc = check_common(layout, K);
   if (rc != SAEF_OK) return rc;
   if (t < 0 || period < 0 || !std::isfinite(lr)) return SAEF_EINVAL;
   if (mode != SAEF_MODE_SC && mode != SAEF_MODE_DC) return SAEF_EINVAL;
-  if (!f32_ok(g) || !f32_ok(e) || !f32_ok(x) || !f32_ok(xh) || !u64_ok(signs) || !f32_ok(scales))
+  if (!f32_ok(g) || !f32_ok(e) || !f32_ok(x) || !u64_ok(signs) || !f32_ok(scales))
     return SAEF_EINVAL;
   if (mode == SAEF_MODE_DC && (!f32_ok(e_srv) || !u64_ok(srv_signs) || !f32_ok(srv_scales)))
     return SAEF_EINVAL;
   const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
   const size_t xb = layout->d_pad * sizeof(float);
-  if (overlap(xh, vb, x, xb) || overlap(xh, vb, e, vb) || overlap(xh, vb, g, vb) ||
-      overlap(g, vb, e, vb))
-    return SAEF_EINVAL;
+  if (overlap(g, vb, e, vb) || overlap(g, vb, x, xb) || overlap(e, vb, x, xb)) return SAEF_EINVAL;
   if (m != nullptr && (!f32_ok(m) || overlap(m, vb, g, vb) || overlap(m, vb, e, vb) ||
-                       overlap(m, vb, xh, vb) || overlap(m, vb, x, xb)))
+                       overlap(m, vb, x, xb)))
     return SAEF_EINVAL;
 
-  const bool pending = t > 0;  // at t == 0 the state is plain (Algorithm 1 initialisation)
+  const bool pending = t > 0;
   const bool averaging = period > 0 && (t + 1) % period == 0;
   const bool dc = mode == SAEF_MODE_DC;
-  // error averaging (when due) and step ahead, applying last iteration's
-  // pending corrections to e and (double-way) x
   const DevLayout& d = layout->dev;
-  rc = hip_rc(timed(layout, averaging ? 5 : 0, [&](const saef::LaunchEvents& ev) {
-    return saef::launch_step_ahead(d, K, x, srv_signs, srv_scales, pending && dc, e, signs,
-                                   scales, pending, averaging, xh, stream, ev);
-  }));
-  if (rc != SAEF_OK) return rc;
-  // [gradient slot: g was computed at xh by the caller]
-  // worker compression (momentum update first when m is given); e is plain
-  // after an averaging step
+  // [gradient slot: g was computed by the caller at the first half's xh]
   rc = hip_rc(timed(layout, 1, [&](const saef::LaunchEvents& ev) {
     return saef::launch_compress(d, K, lr, mu, g, m, e, signs, scales, pending && !averaging,
                                  stream, ev);
@@ -355,6 +415,34 @@ int round_impl(const saef_layout* layout, int64_t t, int64_t period, int32_t K, 
   return hip_rc(timed(layout, 4, [&](const saef::LaunchEvents& ev) {
     return saef::launch_finalize(d, K, true, srv_scales, stream, ev);
   }));
+}
+
+int round_impl(const saef_layout* layout, int64_t t, int64_t period, int32_t K, float lr,
+               float mu, int32_t mode, const float* g, float* m, float* e, float* e_srv,
+               float* x, float* xh, uint64_t* signs, float* scales, uint64_t* srv_signs,
+               float* srv_scales, hipStream_t stream) {
+  // check both halves' arguments before anything is enqueued
+  int rc = check_common(layout, K);
+  if (rc != SAEF_OK) return rc;
+  if (t < 0 || period < 0 || !std::isfinite(lr)) return SAEF_EINVAL;
+  if (mode != SAEF_MODE_SC && mode != SAEF_MODE_DC) return SAEF_EINVAL;
+  if (!f32_ok(g) || !f32_ok(e) || !f32_ok(x) || !f32_ok(xh) || !u64_ok(signs) || !f32_ok(scales))
+    return SAEF_EINVAL;
+  if (mode == SAEF_MODE_DC && (!f32_ok(e_srv) || !u64_ok(srv_signs) || !f32_ok(srv_scales)))
+    return SAEF_EINVAL;
+  const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
+  const size_t xb = layout->d_pad * sizeof(float);
+  if (overlap(xh, vb, x, xb) || overlap(xh, vb, e, vb) || overlap(xh, vb, g, vb) ||
+      overlap(g, vb, e, vb) || overlap(g, vb, x, xb) || overlap(e, vb, x, xb))
+    return SAEF_EINVAL;
+  if (m != nullptr && (!f32_ok(m) || overlap(m, vb, g, vb) || overlap(m, vb, e, vb) ||
+                       overlap(m, vb, xh, vb) || overlap(m, vb, x, xb)))
+    return SAEF_EINVAL;
+  rc = round_begin_impl(layout, t, period, K, mode, SAEF_VARIANT_SAEF, e, e_srv, x, xh, signs,
+                        scales, srv_signs, srv_scales, nullptr, stream);
+  if (rc != SAEF_OK) return rc;
+  return round_end_impl(layout, t, period, K, lr, mu, mode, g, m, e, e_srv, x, signs, scales,
+                        srv_signs, srv_scales, stream);
 }
 
 }  // namespace
@@ -376,6 +464,24 @@ int saef_round_momentum(const saef_layout* layout, int64_t t, int64_t period, in
   if (!mu_ok(mu) || m == nullptr) return SAEF_EINVAL;
   return round_impl(layout, t, period, K, lr, mu, mode, g, m, e, e_srv, x, xh, signs, scales,
                     srv_signs, srv_scales, stream);
+}
+
+int saef_round_begin(const saef_layout* layout, int64_t t, int64_t period, int32_t K,
+                     int32_t mode, int32_t variant, float* e, const float* e_srv, const float* x,
+                     float* xh, const uint64_t* signs, const float* scales,
+                     const uint64_t* srv_signs, const float* srv_scales, double* mismatch,
+                     hipStream_t stream) {
+  return round_begin_impl(layout, t, period, K, mode, variant, e, e_srv, x, xh, signs, scales,
+                          srv_signs, srv_scales, mismatch, stream);
+}
+
+int saef_round_end(const saef_layout* layout, int64_t t, int64_t period, int32_t K, float lr,
+                   float mu, int32_t mode, const float* g, float* m, float* e, float* e_srv,
+                   float* x, uint64_t* signs, float* scales, uint64_t* srv_signs,
+                   float* srv_scales, hipStream_t stream) {
+  if (m == nullptr ? mu != 0.0f : !mu_ok(mu)) return SAEF_EINVAL;
+  return round_end_impl(layout, t, period, K, lr, mu, mode, g, m, e, e_srv, x, signs, scales,
+                        srv_signs, srv_scales, stream);
 }
 
 int saef_materialize(const saef_layout* layout, int32_t K, int32_t mode, const float* e,

@@ -93,7 +93,8 @@ hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_
 // correction to x on read (x is never written here; the aggregate kernel
 // materializes it).  decode_e: apply the pending worker corrections to e on
 // read.  average: replace every e[k] by the mean and write it back (plain).
-// xh written when non-null (required unless average).
+// xh written when non-null (required unless average; without xh, x is not
+// read and decode_x must be false).
 hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
                              const uint64_t* srv_signs, const float* srv_scales, bool decode_x,
                              float* e, const uint64_t* signs, const float* scales, bool decode_e,
@@ -108,6 +109,17 @@ hipError_t launch_materialize(const DevLayout& lay, int K, int mode, const float
                               const float* e_srv, const float* x, const uint64_t* srv_signs,
                               const float* srv_scales, float* e_srv_out, float* x_out,
                               hipStream_t s,
+                           const LaunchEvents& ev = LaunchEvents());
+
+// Gradient-mismatch bounds of the state (a diagnostic): out[l] = sum over
+// tensor l of (e_srv + ebar)^2 and out[L + l] = (1/K) sum_k sum (e_srv + ebar
+// - e^(k))^2, binary64 (mode 0: no server error).  decode_e / decode_s apply
+// the pending worker / server corrections on read.  Uses the tile
+// partial-sum scratch of row 0 (and the second-level scratch).
+hipError_t launch_mismatch(const DevLayout& lay, int K, int mode, const float* e,
+                           const uint64_t* signs, const float* scales, bool decode_e,
+                           const float* e_srv, const uint64_t* srv_signs,
+                           const float* srv_scales, bool decode_s, double* out, hipStream_t s,
                            const LaunchEvents& ev = LaunchEvents());
 
 }  // namespace saef

@@ -1,6 +1,6 @@
 // HIP kernels for the SAEF round on gfx950 (CDNA4, wave64).
 //
-// Work decomposition: a layout is cut into tiles of 1024 elements of one
+// Work decomposition: a layout is cut into tiles of 2048 elements of one
 // tensor (more for very large tensors; tile starts are multiples of 64, so a
 // 64-bit sign word never spans two tiles).  Lane i of a wave owns element
 // 64*word + i of the 64-element words it processes, so every global load or
@@ -674,6 +674,183 @@ __global__ __launch_bounds__(kBlock) void k_materialize(
   }
 }
 
+// ------------------------------------------------------------------ mismatch
+// Gradient-mismatch bounds (a diagnostic, "Step Ahead" and "Error Averaging"
+// sections with the Lipschitz constant and the variance term left out), per
+// element in binary64:
+//   ebar = (sum_k e^(k), worker order) / K,   u = e_srv + ebar,
+//   a = u^2 (local error feedback),   b = sum_k (u - e^(k))^2 (step ahead).
+// Each wave sums a and b over one tile and stores the two doubles in the
+// tile's slot of the partial-sum scratch (row 0); k_mfinalize adds them per
+// tensor.  The K errors are read twice: the second read finds them in the
+// caches (kMisWords words per wave keep the working set small).
+constexpr int kMisWords = 4;
+
+template <bool kDC, bool kDecE, bool kDecS, bool kFull, int kN>
+__device__ __forceinline__ void mismatch_pass(const DevLayout& lay, int K, double inv_k, int l,
+                                              int64_t base, int64_t gw, int lim,
+                                              const float* __restrict__ e,
+                                              const uint64_t* __restrict__ signs,
+                                              const float* __restrict__ scales,
+                                              const float* __restrict__ es,
+                                              const uint64_t* __restrict__ ss, float s_srv,
+                                              double& a, double& b) {
+  const int64_t W = lay.d_pad >> 6;
+  const int64_t d_pad = lay.d_pad;
+  double acc[kN];
+#pragma unroll
+  for (int u = 0; u < kN; ++u) acc[u] = 0.0;
+  for (int k = 0; k < K; ++k) {
+    const float s = kDecE ? scales[(int64_t)k * lay.L + l] : 0.0f;
+    const float* ek = e + (int64_t)k * d_pad + base;
+    const uint64_t* sk = signs + (int64_t)k * W + gw;
+#pragma unroll
+    for (int u = 0; u < kN; ++u) {
+      const bool ok = kFull || u * 64 < lim;
+      float v = ok ? ek[u * 64] : 0.0f;
+      if (kDecE) v = v - corr(sk[u], s);
+      acc[u] += (double)v;
+    }
+  }
+  double uu[kN], bs[kN];
+#pragma unroll
+  for (int u = 0; u < kN; ++u) {
+    const bool ok = kFull || u * 64 < lim;
+    const double ebar = mean_of(acc[u], inv_k, K);
+    float esv = 0.0f;
+    if (kDC) {
+      esv = ok ? es[base + u * 64] : 0.0f;
+      if (kDecS) esv = esv - corr(ss[gw + u], s_srv);
+    }
+    uu[u] = (double)esv + ebar;
+    if (ok) a += uu[u] * uu[u];
+    bs[u] = 0.0;
+  }
+  for (int k = 0; k < K; ++k) {
+    const float s = kDecE ? scales[(int64_t)k * lay.L + l] : 0.0f;
+    const float* ek = e + (int64_t)k * d_pad + base;
+    const uint64_t* sk = signs + (int64_t)k * W + gw;
+#pragma unroll
+    for (int u = 0; u < kN; ++u) {
+      const bool ok = kFull || u * 64 < lim;
+      float v = ok ? ek[u * 64] : 0.0f;
+      if (kDecE) v = v - corr(sk[u], s);
+      const double dk = uu[u] - (double)v;
+      bs[u] += dk * dk;
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kN; ++u)
+    if (kFull || u * 64 < lim) b += bs[u];
+}
+
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+// Grid: ceil(n_tiles / 4) workgroups; wave w of workgroup b owns tile 4b + w.
+template <bool kDC, bool kDecE, bool kDecS>
+__global__ __launch_bounds__(kBlock) void k_mismatch(DevLayout lay, int K, double inv_k,
+                                                     const float* __restrict__ e,
+                                                     const uint64_t* __restrict__ signs,
+                                                     const float* __restrict__ scales,
+                                                     const float* __restrict__ es,
+                                                     const uint64_t* __restrict__ ss,
+                                                     const float* __restrict__ sscales) {
+  const int64_t ti = (int64_t)blockIdx.x * kWaves + wave_id();
+  if (ti >= lay.n_tiles) return;
+  const Tile tile = lay.tiles[ti];
+  const int lane = lane_id();
+  const int nw = (tile.count + 63) >> 6;
+  const float s_srv = kDecS ? sscales[tile.l] : 0.0f;
+  double a = 0.0, b = 0.0;
+  for (int wb = 0; wb < nw; wb += kMisWords) {
+    const int64_t base = tile.start + wb * 64 + lane;
+    const int64_t gw = (tile.start >> 6) + wb;
+    if ((wb + kMisWords) * 64 <= tile.count) {
+      mismatch_pass<kDC, kDecE, kDecS, true, kMisWords>(lay, K, inv_k, tile.l, base, gw, 0, e,
+                                                        signs, scales, es, ss, s_srv, a, b);
+    } else {
+      for (int u = 0; u < min(kMisWords, nw - wb); ++u) {
+        mismatch_pass<kDC, kDecE, kDecS, false, 1>(lay, K, inv_k, tile.l, base + u * 64, gw + u,
+                                                   tile.count - (wb + u) * 64 - lane, e, signs,
+                                                   scales, es, ss, s_srv, a, b);
+      }
+    }
+  }
+  a = wave_sum_f64(a);
+  b = wave_sum_f64(b);
+  if (lane == 0) {
+    u64* p = lay.part + ti * 2;
+    p[0] = (u64)__double_as_longlong(a);
+    p[1] = (u64)__double_as_longlong(b);
+  }
+}
+
+// Adds the (a, b) double pairs v[0..n) over the workgroup in a fixed order
+// (thread 0 gets the sums).
+__device__ void block_sum_pairs(const u64* __restrict__ v, int64_t n, double& ta, double& tb) {
+  __shared__ double s_a[kWaves];
+  __shared__ double s_b[kWaves];
+  double a = 0.0, b = 0.0;
+  for (int64_t i = threadIdx.x; i < n; i += kBlock) {
+    a += __longlong_as_double((long long)v[2 * i]);
+    b += __longlong_as_double((long long)v[2 * i + 1]);
+  }
+  a = wave_sum_f64(a);
+  b = wave_sum_f64(b);
+  const int w = threadIdx.x / kWave;
+  if (lane_id() == 0) {
+    s_a[w] = a;
+    s_b[w] = b;
+  }
+  __syncthreads();
+  ta = 0.0;
+  tb = 0.0;
+  if (threadIdx.x == 0)
+    for (int i = 0; i < kWaves; ++i) {
+      ta += s_a[i];
+      tb += s_b[i];
+    }
+}
+
+// Grid: L * S workgroups (S = lay.fin_split): part s of tensor l's tile sums.
+// With S = 1 it writes out[l] = sum a and out[L + l] = (sum b) / K, else a
+// second-level pair that k_mfinalize2 adds.
+__global__ __launch_bounds__(kBlock) void k_mfinalize(DevLayout lay, int K,
+                                                      double* __restrict__ out) {
+  const int S = lay.fin_split;
+  const int s = (int)(blockIdx.x % S);
+  const int l = (int)(blockIdx.x / S);
+  const TensorInfo t = lay.tensors[l];
+  const int per = (t.ntiles + S - 1) / S;
+  const int i0 = min(t.ntiles, s * per), i1 = min(t.ntiles, i0 + per);
+  double a, b;
+  block_sum_pairs(lay.part + (int64_t)(t.first_tile + i0) * 2, i1 - i0, a, b);
+  if (threadIdx.x != 0) return;
+  if (S == 1) {
+    out[l] = a;
+    out[lay.L + l] = b / (double)K;
+  } else {
+    u64* q = lay.part2 + ((int64_t)l * S + s) * 2;
+    q[0] = (u64)__double_as_longlong(a);
+    q[1] = (u64)__double_as_longlong(b);
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_mfinalize2(DevLayout lay, int K,
+                                                       double* __restrict__ out) {
+  const int S = lay.fin_split;
+  const int l = blockIdx.x;
+  double a, b;
+  block_sum_pairs(lay.part2 + (int64_t)l * S * 2, S, a, b);
+  if (threadIdx.x != 0) return;
+  out[l] = a;
+  out[lay.L + l] = b / (double)K;
+}
+
 double inv_pow2(int K) { return (K & (K - 1)) == 0 ? 1.0 / (double)K : 0.0; }
 
 // All launches go through hipExtLaunchKernelGGL so that an optional event
@@ -754,8 +931,8 @@ hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
   SAEF_LAUNCH((k_step_average<DX, DE, XH>), grid, dim3(kBlock), 0, s, lay, K, ik, x, \
                      srv_signs, srv_scales, e, signs, scales, xh)
     if (xh == nullptr) {
-      if (decode_e) return hipErrorInvalidValue;  // plain averaging only
-      SAEF_AV(false, false, false);
+      if (decode_x) return hipErrorInvalidValue;  // x is not read without xh
+      if (decode_e) SAEF_AV(false, true, false); else SAEF_AV(false, false, false);
     } else if (decode_x) {
       SAEF_AV(true, true, true);
     } else if (decode_e) {
@@ -793,6 +970,39 @@ hipError_t launch_materialize(const DevLayout& lay, int K, int mode, const float
   const dim3 grid((unsigned)(lay.n_tiles * rows));
   SAEF_LAUNCH(k_materialize, grid, dim3(kBlock), 0, s, lay, k_rows, rows, mode, e, signs,
                      scales, e_out, e_srv, x, srv_signs, srv_scales, e_srv_out, x_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_mismatch(const DevLayout& lay, int K, int mode, const float* e,
+                           const uint64_t* signs, const float* scales, bool decode_e,
+                           const float* e_srv, const uint64_t* srv_signs,
+                           const float* srv_scales, bool decode_s, double* out, hipStream_t s,
+                           const LaunchEvents& ev) {
+  const dim3 grid(per_wave_grid(lay));
+  const double ik = inv_pow2(K);
+#define SAEF_MIS(DC, DE, DS)                                                                  \
+  hipExtLaunchKernelGGL((k_mismatch<DC, DE, DS>), grid, dim3(kBlock), 0, s, ev.start, nullptr, \
+                        0, lay, K, ik, e, signs, scales, e_srv, srv_signs, srv_scales)
+  if (mode == 1) {
+    if (decode_e) {
+      if (decode_s) SAEF_MIS(true, true, true); else SAEF_MIS(true, true, false);
+    } else {
+      if (decode_s) SAEF_MIS(true, false, true); else SAEF_MIS(true, false, false);
+    }
+  } else {
+    if (decode_e) SAEF_MIS(false, true, false); else SAEF_MIS(false, false, false);
+  }
+#undef SAEF_MIS
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  const int S = lay.fin_split;
+  // the event pair brackets the element kernel and the one or two sums
+  hipExtLaunchKernelGGL(k_mfinalize, dim3((unsigned)(lay.L * S)), dim3(kBlock), 0, s, nullptr,
+                        S == 1 ? ev.stop : nullptr, 0, lay, K, out);
+  err = hipGetLastError();
+  if (err != hipSuccess || S == 1) return err;
+  hipExtLaunchKernelGGL(k_mfinalize2, dim3((unsigned)lay.L), dim3(kBlock), 0, s, nullptr, ev.stop,
+                        0, lay, K, out);
   return hipGetLastError();
 }
 

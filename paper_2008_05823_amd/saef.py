@@ -21,6 +21,7 @@ LIB_PATH = os.environ.get("SAEF_LIBRARY") or os.path.join(HERE, "libsaef.so")
 
 OK, EINVAL, ERANGE, EHIP = 0, -1, -2, -3
 MODE_SC, MODE_DC = 0, 1
+VARIANT_EF, VARIANT_SAEF = 0, 1
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build the HIP library first "
@@ -43,6 +44,10 @@ _SIGS = {
     "saef_round": [_P, _i64, _i64, _i32, _f32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P],
     "saef_round_momentum": [_P, _i64, _i64, _i32, _f32, _f32, _i32, _P, _P, _P, _P, _P, _P, _P,
                             _P, _P, _P, _P],
+    "saef_round_begin": [_P, _i64, _i64, _i32, _i32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                         _P],
+    "saef_round_end": [_P, _i64, _i64, _i32, _f32, _f32, _i32, _P, _P, _P, _P, _P, _P, _P, _P,
+                       _P, _P],
     "saef_materialize": [_P, _i32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P],
     "saef_status": [_P, _P],
     "saef_profile_enable": [_P, _i32, ctypes.c_uint32],
@@ -57,7 +62,7 @@ EXPORTS = tuple(_SIGS)
 
 # kernel kinds of saef_profile_enable / saef_profile_read, in bit order
 PROFILE_KINDS = ("step_ahead", "compress", "worker_scales", "aggregate", "server_scales",
-                 "step_ahead_averaging")
+                 "step_ahead_averaging", "mismatch")
 
 
 class SaefError(RuntimeError):
@@ -193,6 +198,27 @@ def saef_round_momentum(layout: Layout, t: int, period: int, K: int, lr: float, 
            _lib.saef_round_momentum(layout.handle, t, period, K, lr, mu, mode, _f(g), _f(m),
                                     _f(e), _f(e_srv), _f(x), _f(xh), _w(signs), _f(scales),
                                     _w(srv_signs), _f(srv_scales), _stream(stream)))
+
+
+def saef_round_begin(layout: Layout, t: int, period: int, K: int, mode: int, variant: int, e,
+                     e_srv, x, xh, signs, scales, srv_signs=None, srv_scales=None,
+                     mismatch=None, stream=None):
+    """First half of iteration t; mismatch: float64 device tensor of 2 L or None."""
+    _check("saef_round_begin",
+           _lib.saef_round_begin(layout.handle, t, period, K, mode, variant, _f(e), _f(e_srv),
+                                 _f(x), _f(xh), _w(signs), _f(scales), _w(srv_signs),
+                                 _f(srv_scales), _dev(mismatch, torch.float64),
+                                 _stream(stream)))
+
+
+def saef_round_end(layout: Layout, t: int, period: int, K: int, lr: float, mu: float, mode: int,
+                   g, m, e, e_srv, x, signs, scales, srv_signs=None, srv_scales=None,
+                   stream=None):
+    """Second half of iteration t (m None: no momentum, mu must be 0)."""
+    _check("saef_round_end",
+           _lib.saef_round_end(layout.handle, t, period, K, lr, mu, mode, _f(g), _f(m), _f(e),
+                               _f(e_srv), _f(x), _w(signs), _f(scales), _w(srv_signs),
+                               _f(srv_scales), _stream(stream)))
 
 
 def saef_materialize(layout: Layout, K: int, mode: int, e, e_srv, x, signs, scales,

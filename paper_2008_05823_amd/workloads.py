@@ -263,7 +263,8 @@ def gradients(w: Workload, t: int, K: int | None = None) -> np.ndarray:
 
 
 def algorithmic_bytes_per_param(K: int, mode: int = 1, averaging: bool = False,
-                                momentum: bool = False) -> float:
+                                momentum: bool = False, step_ahead: bool = True,
+                                mismatch: bool = False) -> float:
     """Bytes the method itself moves per parameter per round.
 
     step ahead: read x and e[k], write xh[k]            4 + 8K
@@ -273,8 +274,11 @@ def algorithmic_bytes_per_param(K: int, mode: int = 1, averaging: bool = False,
     server, single-way: read the K sign streams, read/write x    8 + K/8
     an error-averaging round also writes e[k] once more          + 4K
     momentum: the worker step also reads and writes m[k]        + 8K
+    local error feedback instead of step ahead: read x, write one copy   8
+    mismatch bounds: read e[k] and (double-way) e_srv           4K (+ 4)
     """
-    step = 4 + 8 * K
+    step = (4 + 8 * K) if step_ahead else 8
     comp = (20 if momentum else 12) * K + K / 8
     server = (16 + 1 / 8 + K / 8) if mode == 1 else (8 + K / 8)
-    return step + comp + server + (4 * K if averaging else 0)
+    mis = (4 * K + (4 if mode == 1 else 0)) if mismatch else 0
+    return step + comp + server + (4 * K if averaging else 0) + mis

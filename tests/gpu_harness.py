@@ -98,6 +98,26 @@ class OracleState:
                                          self.srv_signs, self.srv_scales)
         assert rc == O.OK, rc
 
+    def begin(self, t: int, variant: int, period=None, mode=None, mismatch=True):
+        """First half of iteration t; returns the 2 L mismatch bounds (or None)."""
+        w = self.w
+        period = w.period if period is None else period
+        mode = w.mode if mode is None else mode
+        mism = np.full(2 * w.L, np.nan) if mismatch else None
+        rc = self.orc.round_begin(t, period, self.K, mode, variant, self.e, self.e_srv, self.x,
+                                  self.xh, mism)
+        assert rc == O.OK, rc
+        return mism
+
+    def end(self, t: int, g: np.ndarray, mode=None):
+        w = self.w
+        mode = w.mode if mode is None else mode
+        mu = 0.0 if self.mu is None else np.float32(self.mu)
+        rc = self.orc.round_end(self.K, np.float32(w.lr), mu, mode, g, self.m, self.e,
+                                self.e_srv, self.x, self.signs, self.scales, self.srv_signs,
+                                self.srv_scales)
+        assert rc == O.OK, rc
+
 
 class GpuState:
     """Device buffers of one workload driven through the HIP library (with
@@ -144,6 +164,33 @@ class GpuState:
                                           self.signs, self.scales, self.srv_signs,
                                           self.srv_scales)
 
+    def begin(self, t: int, variant: int, period=None, mode=None, mismatch=True):
+        """First half of iteration t (EF writes row 0 of xh); returns the 2 L
+        mismatch bounds downloaded to the host (or None)."""
+        w = self.w
+        period = w.period if period is None else period
+        mode = w.mode if mode is None else mode
+        mism = torch.full((2 * w.L,), float("nan"), dtype=torch.float64,
+                          device="cuda") if mismatch else None
+        xh = self.xh if variant == self.saef.VARIANT_SAEF else self.xh[0]
+        self.saef.saef_round_begin(self.layout, t, period, self.K, mode, variant, self.e,
+                                   self.e_srv, self.x, xh, self.signs, self.scales,
+                                   self.srv_signs, self.srv_scales, mism)
+        return None if mism is None else mism.cpu().numpy()
+
+    def end(self, t: int, g, period=None, mode=None):
+        w = self.w
+        if isinstance(g, np.ndarray):
+            self.g.copy_(torch.from_numpy(g))
+        else:
+            self.g.copy_(g)
+        period = w.period if period is None else period
+        mode = w.mode if mode is None else mode
+        self.saef.saef_round_end(self.layout, t, period, self.K, w.lr,
+                                 0.0 if self.mu is None else self.mu, mode, self.g, self.m,
+                                 self.e, self.e_srv, self.x, self.signs, self.scales,
+                                 self.srv_signs, self.srv_scales)
+
     def plain(self, mode=None) -> dict:
         """Materialized (plain) state, downloaded to the host."""
         mode = self.w.mode if mode is None else mode
@@ -183,3 +230,23 @@ def compare_state(gpu: dict, orc: OracleState, t: int, what: str = ""):
         assert_f32_equal(gpu["srv_scales"], orc.srv_scales, np.ones(w.L, bool),
                          f"{tag} server scales")
         assert_f32_equal(gpu["e_srv"], orc.e_srv, m, f"{tag} server error")
+
+
+def mismatch_tol(w: W.Workload, K: int) -> np.ndarray:
+    """Per-entry bound on |gpu - oracle| / value for the 2 L mismatch sums:
+    every term is the same binary64 value on both sides and non-negative, so
+    two summation orders of N terms differ by at most 2 (N - 1) 2^-53 of the
+    sum (N = n_l for the EF bound, n_l K for the step-ahead bound)."""
+    n = w.sizes.astype(np.float64)
+    return np.concatenate([2 * n, 2 * n * K]) * 2.0 ** -53 + 4 * 2.0 ** -53
+
+
+def assert_mismatch_close(got: np.ndarray, want: np.ndarray, w: W.Workload, K: int, what: str):
+    rel = mismatch_tol(w, K)
+    err = np.abs(got - want)
+    ok = err <= rel * np.abs(want) + 1e-300
+    if not ok.all():
+        i = int(np.argwhere(~ok)[0][0])
+        raise AssertionError(f"{what}: mismatch bound {i} got {got[i]!r} want {want[i]!r} "
+                             f"(rel err {err[i] / max(abs(want[i]), 1e-300):.3g}, "
+                             f"bound {rel[i]:.3g})")

@@ -292,3 +292,100 @@ def test_invalid_arguments_are_rejected():
         S.saef_aggregate(gs.layout, 2, 1, gs.signs, gs.scales, gs.x)
     with pytest.raises(S.SaefError):             # g and e overlap
         S.saef_compress(gs.layout, 2, 0.1, gs.e, gs.e, gs.signs, gs.scales)
+
+
+# ---------------------------------------------------------------- two halves, EF, mismatch
+
+SPLIT_CASES = {
+    "resnet56_dc": W.get("resnet56").with_(period=4, rounds=9),
+    "ragged_sc": W.custom(ADVERSARIAL + [70001], K=3, period=3, rounds=7, mode=0,
+                          scale_range=(1e-4, 1e-1), dist="laplace_zeros", seed=998),
+    "flat64k_no_avg": W.get("flat64k").with_(period=0, rounds=6),
+}
+
+
+@pytest.mark.parametrize("variant", [0, 1], ids=["ef", "saef"])
+@pytest.mark.parametrize("name", list(SPLIT_CASES))
+def test_round_halves_parity(name, variant):
+    """saef_round_begin (with the mismatch bounds) + saef_round_end against
+    the oracle's two halves, every iteration; EF writes one row of xh."""
+    w = SPLIT_CASES[name]
+    _case(f"round halves {name} variant={variant} K={w.K} L={w.L} rounds={w.rounds}")
+    orc = H.OracleState(w)
+    gs = H.GpuState(w)
+    for t in range(w.rounds):
+        g = W.gradients(w, t)
+        want = orc.begin(t, variant)
+        got = gs.begin(t, variant)
+        H.assert_mismatch_close(got, want, w, w.K, f"{name} t={t}")
+        orc.end(t, g)
+        gs.end(t, g)
+        H.compare_state(gs.plain(), orc, t, name)
+    assert gs.status() == 0
+
+
+def test_round_halves_equal_round():
+    """begin(SAEF) + end is saef_round, bit for bit (pending form included)."""
+    w = W.get("resnet56").with_(period=3, rounds=6)
+    _case("round halves vs saef_round")
+    a = H.GpuState(w)
+    b = H.GpuState(w)
+    for t in range(w.rounds):
+        g = W.gradients(w, t)
+        a.round(t, g)
+        b.begin(t, 1, mismatch=(t % 2 == 0))
+        b.end(t, g)
+    torch.cuda.synchronize()
+    for key in ("e", "e_srv", "x", "xh", "signs", "scales", "srv_signs", "srv_scales"):
+        assert torch.equal(getattr(a, key), getattr(b, key)), key
+
+
+@pytest.mark.parametrize("variant", [0, 1], ids=["ef", "saef"])
+def test_closed_loop_quadratic(variant):
+    """Gradients that depend on the evaluation point: a noisy quadratic,
+    g^(k) = (xh - x*) / 2 + noise^(k), computed with fp32 elementwise torch
+    ops between the two halves on the GPU and with numpy on the host (the
+    same correctly rounded operations).  The two branches now follow
+    different trajectories, and each matches the oracle bit for bit."""
+    w = W.get("resnet56").with_(period=0, rounds=8)
+    _case(f"closed-loop quadratic variant={variant}")
+    off, n, d_pad = w.layout()
+    rng = np.random.default_rng(2024)
+    xstar = (rng.standard_normal(d_pad) * 0.05).astype(np.float32)
+    orc = H.OracleState(w)
+    gs = H.GpuState(w)
+    xstar_d = torch.from_numpy(xstar).cuda()
+    for t in range(w.rounds):
+        noise = (rng.standard_normal((w.K, d_pad)) * 0.01).astype(np.float32)
+        want = orc.begin(t, variant)
+        got = gs.begin(t, variant)
+        H.assert_mismatch_close(got, want, w, w.K, f"closed loop t={t}")
+        rows = orc.xh if variant == 1 else np.repeat(orc.xh[:1], w.K, axis=0)
+        g_host = (np.float32(0.5) * (rows - xstar)).astype(np.float32) + noise
+        xh_d = gs.xh if variant == 1 else gs.xh[:1].expand(w.K, d_pad)
+        g_dev = (0.5 * (xh_d - xstar_d)) + torch.from_numpy(noise).cuda()
+        orc.end(t, g_host)
+        gs.end(t, g_dev.contiguous())
+        H.compare_state(gs.plain(), orc, t, f"closed loop v{variant}")
+    assert gs.status() == 0
+
+
+def test_round_halves_invalid():
+    w = W.custom([100], K=2)
+    gs = H.GpuState(w)
+    s = gs.saef
+    with pytest.raises(s.SaefError):  # unknown variant
+        s.saef_round_begin(gs.layout, 0, 0, 2, 1, 2, gs.e, gs.e_srv, gs.x, gs.xh, gs.signs,
+                           gs.scales, gs.srv_signs, gs.srv_scales)
+    with pytest.raises(s.SaefError):  # EF evaluation point aliases the weights
+        s.saef_round_begin(gs.layout, 0, 0, 2, 1, 0, gs.e, gs.e_srv, gs.x, gs.x, gs.signs,
+                           gs.scales, gs.srv_signs, gs.srv_scales)
+    with pytest.raises(s.SaefError):  # mu without a momentum buffer
+        s.saef_round_end(gs.layout, 0, 0, 2, 0.1, 0.9, 1, gs.g, None, gs.e, gs.e_srv, gs.x,
+                         gs.signs, gs.scales, gs.srv_signs, gs.srv_scales)
+    with pytest.raises(s.SaefError):  # mismatch bounds need the server error in DC
+        s.saef_round_begin(gs.layout, 0, 0, 2, 1, 1, gs.e, None, gs.x, gs.xh, gs.signs,
+                           gs.scales, gs.srv_signs, gs.srv_scales,
+                           torch.zeros(2, dtype=torch.float64, device="cuda"))
+    torch.cuda.synchronize()
+    assert gs.status() == 0
