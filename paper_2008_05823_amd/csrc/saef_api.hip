@@ -364,9 +364,7 @@ int round_begin_impl(const saef_layout* layout, int64_t t, int64_t period, int32
   if (variant == SAEF_VARIANT_SAEF) return SAEF_OK;
   // local error feedback: the gradient is taken at x_t itself (one row)
   return hip_rc(timed(layout, 0, [&](const saef::LaunchEvents& ev) {
-    return saef::launch_materialize(d, K, (pending && dc) ? SAEF_MODE_DC : SAEF_MODE_SC, nullptr,
-                                    nullptr, nullptr, nullptr, nullptr, x, srv_signs, srv_scales,
-                                    nullptr, xh, stream, ev);
+    return saef::launch_weights(d, x, srv_signs, srv_scales, pending && dc, xh, stream, ev);
   }));
 }
 

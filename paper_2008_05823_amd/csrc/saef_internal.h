@@ -101,6 +101,12 @@ hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
                              bool average, float* xh, hipStream_t s,
                            const LaunchEvents& ev = LaunchEvents());
 
+// The weights x_t into xh (one row): the evaluation point of local error
+// feedback.  decode_x applies the pending server correction on read.
+hipError_t launch_weights(const DevLayout& lay, const float* x, const uint64_t* srv_signs,
+                          const float* srv_scales, bool decode_x, float* xh, hipStream_t s,
+                          const LaunchEvents& ev = LaunchEvents());
+
 // Apply pending corrections: e_out[k] = e[k] - c_k for k < K (when e_out),
 // and, when e_srv_out or x_out is given, e_srv_out = e_srv - c and
 // x_out = x - c (mode 1) or plain copies (mode 0; e_srv_out then receives 0).

@@ -339,9 +339,10 @@ __global__ __launch_bounds__(kBlock) void k_finalize2(DevLayout lay, int server,
 
 // ------------------------------------------------------------------ step ahead
 // kU words of one worker's tile starting at word w0: x^(k)_{t+1/2} = x_t -
-// e^(k)_t with the pending corrections of x and e applied on the fly.
+// e^(k)_t with the pending corrections of x and e applied on the fly
+// (kHasE false: x_t itself, the evaluation point of local error feedback).
 // kFull: all kU words are whole words of the tile (no guards).
-template <bool kDecX, bool kDecE, bool kFull>
+template <bool kDecX, bool kDecE, bool kHasE, bool kFull>
 __device__ __forceinline__ void step_words(int w0, int nw, int count,
                                            const float* __restrict__ xt,
                                            const float* __restrict__ ek, float* __restrict__ hk,
@@ -355,8 +356,8 @@ __device__ __forceinline__ void step_words(int w0, int nw, int count,
   for (int u = 0; u < kU; ++u) {
     const int j = (w0 + u) * 64 + lane;
     const bool ok = kFull || ((w0 + u < nw) && j < count);
-    xv[u] = ok ? xt[j] : 0.0f;
-    ev[u] = ok ? ld_nt(ek + j) : 0.0f;
+    xv[u] = ok ? (kHasE ? xt[j] : ld_nt(xt + j)) : 0.0f;
+    ev[u] = (kHasE && ok) ? ld_nt(ek + j) : 0.0f;
     mx[u] = (kDecX && (kFull || w0 + u < nw)) ? sx[w0 + u] : 0ull;
     me[u] = (kDecE && (kFull || w0 + u < nw)) ? sk[w0 + u] : 0ull;
   }
@@ -367,7 +368,7 @@ __device__ __forceinline__ void step_words(int w0, int nw, int count,
     float xc = xv[u], ec = ev[u];
     if (kDecX) xc = xc - corr(mx[u], s_x);  // x_t = x_{t-1} - C(Delta_t)
     if (kDecE) ec = ec - corr(me[u], s_e);  // e_t = Delta - C(Delta)
-    if (kFull || j < count) st_nt(hk + j, xc - ec);  // x^(k)_{t+1/2} = x_t - e^(k)_t
+    if (kFull || j < count) st_nt(hk + j, kHasE ? xc - ec : xc);  // x^(k)_{t+1/2} = x_t - e^(k)_t
   }
 }
 
@@ -376,8 +377,8 @@ __device__ __forceinline__ void step_words(int w0, int nw, int count,
 // (workgroups go to the XCDs round-robin), so x is fetched from HBM once and
 // re-read from that XCD's L2.  x itself is not written: the pending
 // re-update of x is applied here on the fly and materialized by the
-// aggregate kernel.
-template <bool kDecX, bool kDecE>
+// aggregate kernel.  kHasE false (K = 1, e unused): xh = x_t.
+template <bool kDecX, bool kDecE, bool kHasE>
 __global__ __launch_bounds__(kBlock) void k_step(DevLayout lay, int K, const float* __restrict__ x,
                                                  const uint64_t* __restrict__ ss,
                                                  const float* __restrict__ sscales,
@@ -394,7 +395,7 @@ __global__ __launch_bounds__(kBlock) void k_step(DevLayout lay, int K, const flo
   const int wave = wave_id();
   const int64_t d_pad = lay.d_pad;
   const int64_t gw0 = tile.start >> 6;
-  const float* ek = e + (int64_t)k * d_pad + tile.start;
+  const float* ek = kHasE ? e + (int64_t)k * d_pad + tile.start : nullptr;
   float* hk = xh + (int64_t)k * d_pad + tile.start;
   const float* xt = x + tile.start;
   const uint64_t* sk = signs + (int64_t)k * (d_pad >> 6) + gw0;
@@ -404,9 +405,9 @@ __global__ __launch_bounds__(kBlock) void k_step(DevLayout lay, int K, const flo
   const int nw = (tile.count + 63) >> 6;
   for (int w0 = wave * kU; w0 < nw; w0 += kWaves * kU) {
     if ((w0 + kU) * 64 <= tile.count) {
-      step_words<kDecX, kDecE, true>(w0, nw, tile.count, xt, ek, hk, sx, sk, s_x, s_e);
+      step_words<kDecX, kDecE, kHasE, true>(w0, nw, tile.count, xt, ek, hk, sx, sk, s_x, s_e);
     } else {
-      step_words<kDecX, kDecE, false>(w0, nw, tile.count, xt, ek, hk, sx, sk, s_x, s_e);
+      step_words<kDecX, kDecE, kHasE, false>(w0, nw, tile.count, xt, ek, hk, sx, sk, s_x, s_e);
     }
   }
 }
@@ -684,8 +685,12 @@ __global__ __launch_bounds__(kBlock) void k_materialize(
 // tile's slot of the partial-sum scratch (row 0); k_mfinalize adds them per
 // tensor.  The K errors are read twice: the second read finds them in the
 // caches (kMisWords words per wave keep the working set small).
-constexpr int kMisWords = 4;
+constexpr int kMisWords = 4;   // words per pass, two-read path
+constexpr int kMisRegK = 16;   // at most this many workers: one read, values kept in registers
+constexpr int kMisRegWords = 2;
 
+// Two-read path (any K): the errors are read once for the mean and again
+// for the distances.
 template <bool kDC, bool kDecE, bool kDecS, bool kFull, int kN>
 __device__ __forceinline__ void mismatch_pass(const DevLayout& lay, int K, double inv_k, int l,
                                               int64_t base, int64_t gw, int lim,
@@ -744,6 +749,85 @@ __device__ __forceinline__ void mismatch_pass(const DevLayout& lay, int K, doubl
     if (kFull || u * 64 < lim) b += bs[u];
 }
 
+// One-read path (K <= kMisRegK): the decoded errors stay in registers; the
+// loads of kAvgChunk workers are issued together, sign words are read per
+// lane as the 32-bit half that holds the lane's bit.  Same arithmetic as
+// mismatch_pass.
+template <bool kDC, bool kDecE, bool kDecS, bool kFull, int kN>
+__device__ __forceinline__ void mismatch_pass_reg(const DevLayout& lay, int K, double inv_k,
+                                                  int l, int64_t base, int64_t gw, int lim,
+                                                  const float* __restrict__ e,
+                                                  const uint64_t* __restrict__ signs,
+                                                  const float* __restrict__ scales,
+                                                  const float* __restrict__ es,
+                                                  const uint64_t* __restrict__ ss, float s_srv,
+                                                  double& a, double& b) {
+  const int lane = lane_id();
+  const int64_t W = lay.d_pad >> 6;
+  const int64_t d_pad = lay.d_pad;
+  float v[kMisRegK][kN];
+  double acc[kN];
+#pragma unroll
+  for (int u = 0; u < kN; ++u) acc[u] = 0.0;
+  float esv[kN];
+  uint32_t hs[kN];
+#pragma unroll
+  for (int u = 0; u < kN; ++u) {
+    const bool ok = kFull || u * 64 < lim;
+    esv[u] = (kDC && ok) ? ld_nt(es + base + u * 64) : 0.0f;
+    hs[u] = kDecS ? half_word(ss + gw + u, lane) : 0u;
+  }
+#pragma unroll
+  for (int k0 = 0; k0 < kMisRegK; k0 += kAvgChunk) {
+    if (k0 >= K) break;
+    uint32_t hw[kAvgChunk][kN];
+#pragma unroll
+    for (int c = 0; c < kAvgChunk; ++c) {
+      const int k = k0 + c;
+      const bool kin = k < K;
+      const float* ek = e + (int64_t)k * d_pad + base;
+      const uint64_t* sk = signs + (int64_t)k * W + gw;
+#pragma unroll
+      for (int u = 0; u < kN; ++u) {
+        const bool ok = kFull || u * 64 < lim;
+        v[k][u] = (kin && ok) ? ld_nt(ek + u * 64) : 0.0f;
+        hw[c][u] = (kDecE && kin) ? half_word(sk + u, lane) : 0u;
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < kAvgChunk; ++c) {
+      const int k = k0 + c;
+      if (k >= K) continue;
+      const float s = kDecE ? scales[(int64_t)k * lay.L + l] : 0.0f;
+#pragma unroll
+      for (int u = 0; u < kN; ++u) {
+        if (kDecE) v[k][u] = v[k][u] - (half_bit(hw[c][u], lane) ? s : -s);
+        acc[u] += (double)v[k][u];
+      }
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kN; ++u) {
+    const bool ok = kFull || u * 64 < lim;
+    const double ebar = mean_of(acc[u], inv_k, K);
+    float ev = esv[u];
+    if (kDecS) ev = ev - (half_bit(hs[u], lane) ? s_srv : -s_srv);
+    const double uu = (double)ev + ebar;
+    double bs = 0.0;
+#pragma unroll
+    for (int k = 0; k < kMisRegK; ++k) {
+      if (k < K) {
+        const double dk = uu - (double)v[k][u];
+        bs += dk * dk;
+      }
+    }
+    if (ok) {
+      a += uu * uu;
+      b += bs;
+    }
+  }
+}
+
 __device__ __forceinline__ double wave_sum_f64(double v) {
 #pragma unroll
   for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
@@ -751,7 +835,7 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
 }
 
 // Grid: ceil(n_tiles / 4) workgroups; wave w of workgroup b owns tile 4b + w.
-template <bool kDC, bool kDecE, bool kDecS>
+template <bool kDC, bool kDecE, bool kDecS, bool kReg>
 __global__ __launch_bounds__(kBlock) void k_mismatch(DevLayout lay, int K, double inv_k,
                                                      const float* __restrict__ e,
                                                      const uint64_t* __restrict__ signs,
@@ -765,18 +849,29 @@ __global__ __launch_bounds__(kBlock) void k_mismatch(DevLayout lay, int K, doubl
   const int lane = lane_id();
   const int nw = (tile.count + 63) >> 6;
   const float s_srv = kDecS ? sscales[tile.l] : 0.0f;
+  constexpr int kW = kReg ? kMisRegWords : kMisWords;
   double a = 0.0, b = 0.0;
-  for (int wb = 0; wb < nw; wb += kMisWords) {
+  for (int wb = 0; wb < nw; wb += kW) {
     const int64_t base = tile.start + wb * 64 + lane;
     const int64_t gw = (tile.start >> 6) + wb;
-    if ((wb + kMisWords) * 64 <= tile.count) {
-      mismatch_pass<kDC, kDecE, kDecS, true, kMisWords>(lay, K, inv_k, tile.l, base, gw, 0, e,
-                                                        signs, scales, es, ss, s_srv, a, b);
-    } else {
-      for (int u = 0; u < min(kMisWords, nw - wb); ++u) {
-        mismatch_pass<kDC, kDecE, kDecS, false, 1>(lay, K, inv_k, tile.l, base + u * 64, gw + u,
-                                                   tile.count - (wb + u) * 64 - lane, e, signs,
+    if ((wb + kW) * 64 <= tile.count) {
+      if (kReg)
+        mismatch_pass_reg<kDC, kDecE, kDecS, true, kW>(lay, K, inv_k, tile.l, base, gw, 0, e,
+                                                       signs, scales, es, ss, s_srv, a, b);
+      else
+        mismatch_pass<kDC, kDecE, kDecS, true, kW>(lay, K, inv_k, tile.l, base, gw, 0, e, signs,
                                                    scales, es, ss, s_srv, a, b);
+    } else {
+      for (int u = 0; u < min(kW, nw - wb); ++u) {
+        const int lim = tile.count - (wb + u) * 64 - lane;
+        if (kReg)
+          mismatch_pass_reg<kDC, kDecE, kDecS, false, 1>(lay, K, inv_k, tile.l, base + u * 64,
+                                                         gw + u, lim, e, signs, scales, es, ss,
+                                                         s_srv, a, b);
+        else
+          mismatch_pass<kDC, kDecE, kDecS, false, 1>(lay, K, inv_k, tile.l, base + u * 64,
+                                                     gw + u, lim, e, signs, scales, es, ss,
+                                                     s_srv, a, b);
       }
     }
   }
@@ -945,7 +1040,7 @@ hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
     if (xh == nullptr) return hipErrorInvalidValue;
     const dim3 grid((unsigned)((lay.n_tiles + kXcds - 1) / kXcds * kXcds * K));
 #define SAEF_ST(DX, DE)                                                                \
-  SAEF_LAUNCH((k_step<DX, DE>), grid, dim3(kBlock), 0, s, lay, K, x, srv_signs, \
+  SAEF_LAUNCH((k_step<DX, DE, true>), grid, dim3(kBlock), 0, s, lay, K, x, srv_signs, \
                      srv_scales, e, signs, scales, xh)
     if (decode_x) {
       SAEF_ST(true, true);
@@ -955,6 +1050,20 @@ hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
       SAEF_ST(false, false);
     }
 #undef SAEF_ST
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_weights(const DevLayout& lay, const float* x, const uint64_t* srv_signs,
+                          const float* srv_scales, bool decode_x, float* xh, hipStream_t s,
+                          const LaunchEvents& ev) {
+  const dim3 grid((unsigned)((lay.n_tiles + kXcds - 1) / kXcds * kXcds));
+  if (decode_x) {
+    SAEF_LAUNCH((k_step<true, false, false>), grid, dim3(kBlock), 0, s, lay, 1, x, srv_signs,
+                srv_scales, nullptr, nullptr, nullptr, xh);
+  } else {
+    SAEF_LAUNCH((k_step<false, false, false>), grid, dim3(kBlock), 0, s, lay, 1, x, srv_signs,
+                srv_scales, nullptr, nullptr, nullptr, xh);
   }
   return hipGetLastError();
 }
@@ -980,9 +1089,14 @@ hipError_t launch_mismatch(const DevLayout& lay, int K, int mode, const float* e
                            const LaunchEvents& ev) {
   const dim3 grid(per_wave_grid(lay));
   const double ik = inv_pow2(K);
-#define SAEF_MIS(DC, DE, DS)                                                                  \
-  hipExtLaunchKernelGGL((k_mismatch<DC, DE, DS>), grid, dim3(kBlock), 0, s, ev.start, nullptr, \
-                        0, lay, K, ik, e, signs, scales, e_srv, srv_signs, srv_scales)
+#define SAEF_MIS2(DC, DE, DS, R)                                                               \
+  hipExtLaunchKernelGGL((k_mismatch<DC, DE, DS, R>), grid, dim3(kBlock), 0, s, ev.start,        \
+                        nullptr, 0, lay, K, ik, e, signs, scales, e_srv, srv_signs, srv_scales)
+#define SAEF_MIS(DC, DE, DS)                                  \
+  do {                                                        \
+    if (K <= kMisRegK) SAEF_MIS2(DC, DE, DS, true);           \
+    else SAEF_MIS2(DC, DE, DS, false);                        \
+  } while (0)
   if (mode == 1) {
     if (decode_e) {
       if (decode_s) SAEF_MIS(true, true, true); else SAEF_MIS(true, true, false);
@@ -993,6 +1107,7 @@ hipError_t launch_mismatch(const DevLayout& lay, int K, int mode, const float* e
     if (decode_e) SAEF_MIS(false, true, false); else SAEF_MIS(false, false, false);
   }
 #undef SAEF_MIS
+#undef SAEF_MIS2
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const int S = lay.fin_split;
