@@ -57,6 +57,10 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "oracle_mismatch": lay + [i32, _P, _P, _P, _P],
         "oracle_round_begin": lay + [i64, i64, i32, i32, i32, _P, _P, _P, _P, _P],
         "oracle_round_end": lay + [i32, f32, f32, i32, _P, _P, _P, _P, _P, _P, _P, _P, _P],
+        "oracle_topk_compress": lay + [i32, f32, f32, _P, _P, _P, _P, _P, _P, _P],
+        "oracle_topk_aggregate": lay + [i32, i32, _P, _P, _P, _P, _P, _P, _P, _P, _P],
+        "oracle_topk_round": lay + [i64, i64, i32, f32, f32, i32, _P, _P, _P, _P, _P, _P, _P, _P,
+                                    _P, _P, _P, _P, _P],
     }
     for name, args in sigs.items():
         fn = getattr(lib, name)
@@ -144,6 +148,27 @@ class Oracle:
         return self.lib.oracle_round_end(*self._lay(), K, lr, mu, mode, _ptr(g), _ptr(m),
                                          _ptr(e), _ptr(e_srv), _ptr(x), _ptr(signs),
                                          _ptr(scales), _ptr(srv_signs), _ptr(srv_scales))
+
+    def topk_compress(self, K, lr, mu, keep, g, m, e, sel, rank, vals):
+        keep = np.ascontiguousarray(keep, dtype=np.int64)
+        return self.lib.oracle_topk_compress(*self._lay(), K, lr, mu, _ptr(keep), _ptr(g),
+                                             _ptr(m), _ptr(e), _ptr(sel), _ptr(rank),
+                                             _ptr(vals))
+
+    def topk_aggregate(self, K, mode, keep, sel, vals, x, e_srv=None, srv_sel=None,
+                       srv_rank=None, srv_vals=None, avg=None):
+        keep = np.ascontiguousarray(keep, dtype=np.int64)
+        return self.lib.oracle_topk_aggregate(*self._lay(), K, mode, _ptr(keep), _ptr(sel),
+                                              _ptr(vals), _ptr(avg), _ptr(e_srv), _ptr(srv_sel),
+                                              _ptr(srv_rank), _ptr(srv_vals), _ptr(x))
+
+    def topk_round(self, t, period, K, lr, mu, mode, keep, g, m, e, e_srv, x, xh, sel, rank,
+                   vals, srv_sel, srv_rank, srv_vals):
+        keep = np.ascontiguousarray(keep, dtype=np.int64)
+        return self.lib.oracle_topk_round(*self._lay(), t, period, K, lr, mu, mode, _ptr(keep),
+                                          _ptr(g), _ptr(m), _ptr(e), _ptr(e_srv), _ptr(x),
+                                          _ptr(xh), _ptr(sel), _ptr(rank), _ptr(vals),
+                                          _ptr(srv_sel), _ptr(srv_rank), _ptr(srv_vals))
 
     def step_ahead(self, K, x, e, xh):
         return self.lib.oracle_step_ahead(*self._lay(), K, _ptr(x), _ptr(e), _ptr(xh))

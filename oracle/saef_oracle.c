@@ -37,6 +37,7 @@
 
 #include <math.h>
 #include <stddef.h>
+#include <stdlib.h>
 #include <string.h>
 
 typedef unsigned __int128 u128;
@@ -381,4 +382,221 @@ int oracle_round_momentum(int32_t L, const int64_t* off, const int64_t* n, int64
     if (rc != ORACLE_OK) return rc;
     return oracle_round_end(L, off, n, d_pad, K, lr, mu, mode, g, m, e, e_srv, x, signs, scales,
                             srv_signs, srv_scales);
+}
+
+/* ---- layer-wise Top-K sparsification -------------------------------------
+ * The paper's second compressor (Experiments: "Top-K" with the sparsity in
+ * percent, layer-wise; "How related to compression?"): C(v) keeps the k_l
+ * components of largest magnitude of each tensor and sets the others to 0.
+ * Equal magnitudes are ordered by index (the lower index is kept), so the
+ * kept set is unique.
+ *
+ * Message of one sender: sel words (the sign-word layout: bit b of word
+ * off[l]/64 + j set when element 64 j + b of tensor l is kept), rank words
+ * (rank[w] = kept elements of the tensor in its words before w) and the kept
+ * values of tensor l, in index order, at vals[voff_l .. voff_l + k_l) with
+ * voff_l = k_0 + ... + k_{l-1}. */
+
+static const float* g_topk_values; /* qsort passes no context */
+
+static int topk_order(const void* pa, const void* pb)
+{
+    int64_t a = *(const int64_t*)pa, b = *(const int64_t*)pb;
+    float ma = fabsf(g_topk_values[a]), mb = fabsf(g_topk_values[b]);
+    if (ma > mb) return -1;
+    if (ma < mb) return 1;
+    return (a < b) ? -1 : (a > b) ? 1 : 0;
+}
+
+static int check_keep(int32_t L, const int64_t* n, const int64_t* keep)
+{
+    if (keep == NULL) return ORACLE_EINVAL;
+    for (int32_t l = 0; l < L; ++l)
+        if (keep[l] < 1 || keep[l] > n[l]) return ORACLE_EINVAL;
+    return ORACLE_OK;
+}
+
+/* Keeps the top k of v[0..n) (flags in kept[]), all values finite. */
+static int topk_select(const float* v, int64_t n, int64_t k, unsigned char* kept)
+{
+    int64_t* order = (int64_t*)malloc((size_t)n * sizeof(int64_t));
+    if (order == NULL) return ORACLE_EINVAL;
+    for (int64_t i = 0; i < n; ++i) order[i] = i;
+    g_topk_values = v;
+    qsort(order, (size_t)n, sizeof(int64_t), topk_order);
+    for (int64_t i = 0; i < n; ++i) kept[i] = 0;
+    for (int64_t r = 0; r < k; ++r) kept[order[r]] = 1;
+    free(order);
+    return ORACLE_OK;
+}
+
+/* C(v) of one tensor v[0..n) (v = a vector at base + off): the message, and
+ * err[i] = v[i] - C(v)_i.  Returns ERANGE when a value is not finite. */
+static int topk_tensor(const float* v, int64_t n, int64_t k, int64_t off, uint64_t* sel,
+                       uint32_t* rank, float* vals, float* err, float* applied_to)
+{
+    for (int64_t i = 0; i < n; ++i)
+        if (!isfinite(v[i])) return ORACLE_ERANGE;
+    unsigned char* kept = (unsigned char*)malloc((size_t)n);
+    if (kept == NULL) return ORACLE_EINVAL;
+    int rc = topk_select(v, n, k, kept);
+    if (rc != ORACLE_OK) {
+        free(kept);
+        return rc;
+    }
+    int64_t nw = (n + 63) / 64, count = 0;
+    for (int64_t w = 0; w < nw; ++w) {
+        sel[off / 64 + w] = 0;
+        rank[off / 64 + w] = (uint32_t)count;
+        for (int64_t b = 0; b < 64 && 64 * w + b < n; ++b) {
+            int64_t i = 64 * w + b;
+            if (kept[i]) {
+                sel[off / 64 + w] |= (uint64_t)1 << b;
+                vals[count++] = v[i];
+            }
+        }
+    }
+    for (int64_t i = 0; i < n; ++i) {
+        float c = kept[i] ? v[i] : 0.0f; /* C(v)_i */
+        if (applied_to != NULL) applied_to[i] = applied_to[i] - c;
+        err[i] = v[i] - c;
+    }
+    free(kept);
+    return ORACLE_OK;
+}
+
+int oracle_topk_compress(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                         int32_t K, float lr, float mu, const int64_t* keep, const float* g,
+                         float* m, float* e, uint64_t* sel, uint32_t* rank, float* vals)
+{
+    int rc = check_layout(L, off, n, d_pad);
+    if (rc != ORACLE_OK) return rc;
+    if (check_keep(L, n, keep) != ORACLE_OK) return ORACLE_EINVAL;
+    if (K < 1 || g == NULL || e == NULL || sel == NULL || rank == NULL || vals == NULL)
+        return ORACLE_EINVAL;
+    if (m == NULL ? mu != 0.0f : !(mu >= 0.0f && mu < 1.0f)) return ORACLE_EINVAL;
+    int64_t total = 0;
+    for (int32_t l = 0; l < L; ++l) total += keep[l];
+    int status = ORACLE_OK;
+    float* delta = (float*)malloc((size_t)d_pad * sizeof(float));
+    if (delta == NULL) return ORACLE_EINVAL;
+    for (int32_t k = 0; k < K; ++k) {
+        const float* gk = g + (int64_t)k * d_pad;
+        float* ek = e + (int64_t)k * d_pad;
+        float* mk = m != NULL ? m + (int64_t)k * d_pad : NULL;
+        int64_t voff = 0;
+        for (int32_t l = 0; l < L; ++l) {
+            for (int64_t i = 0; i < n[l]; ++i) {
+                int64_t j = off[l] + i;
+                /* Delta^(k) = e^(k) + eta m^(k), m = mu m + grad (m = grad when mu = 0) */
+                if (mk != NULL) {
+                    mk[j] = fmaf(mu, mk[j], gk[j]);
+                    delta[j] = fmaf(lr, mk[j], ek[j]);
+                } else {
+                    delta[j] = fmaf(lr, gk[j], ek[j]);
+                }
+            }
+            rc = topk_tensor(delta + off[l], n[l], keep[l], off[l],
+                             sel + (int64_t)k * (d_pad / 64), rank + (int64_t)k * (d_pad / 64),
+                             vals + (int64_t)k * total + voff, ek + off[l], NULL);
+            if (rc == ORACLE_EINVAL) {
+                free(delta);
+                return rc;
+            }
+            if (rc != ORACLE_OK) status = rc;
+            voff += keep[l];
+        }
+    }
+    free(delta);
+    return status;
+}
+
+/* C(Delta^(k)) of one message, decoded into dense[] (tensor elements only):
+ * the kept elements, in index order, take the values in order. */
+static void topk_decode(int32_t L, const int64_t* off, const int64_t* n, const int64_t* keep,
+                        const uint64_t* sel, const float* vals, float* dense)
+{
+    int64_t voff = 0;
+    for (int32_t l = 0; l < L; ++l) {
+        int64_t next = voff;
+        for (int64_t i = 0; i < n[l]; ++i)
+            dense[off[l] + i] = get_bit(sel, off[l], i) ? vals[next++] : 0.0f;
+        voff += keep[l];
+    }
+}
+
+int oracle_topk_aggregate(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                          int32_t K, int32_t mode, const int64_t* keep, const uint64_t* sel,
+                          const float* vals, float* avg, float* e_srv, uint64_t* srv_sel,
+                          uint32_t* srv_rank, float* srv_vals, float* x)
+{
+    int rc = check_layout(L, off, n, d_pad);
+    if (rc != ORACLE_OK) return rc;
+    if (check_keep(L, n, keep) != ORACLE_OK) return ORACLE_EINVAL;
+    if (K < 1 || sel == NULL || vals == NULL || x == NULL) return ORACLE_EINVAL;
+    if (mode != 0 && mode != 1) return ORACLE_EINVAL;
+    if (mode == 1 && (e_srv == NULL || srv_sel == NULL || srv_rank == NULL || srv_vals == NULL))
+        return ORACLE_EINVAL;
+    int64_t total = 0;
+    for (int32_t l = 0; l < L; ++l) total += keep[l];
+    double* acc = (double*)calloc((size_t)d_pad, sizeof(double));
+    float* dense = (float*)calloc((size_t)d_pad, sizeof(float));
+    float* mean = (float*)calloc((size_t)d_pad, sizeof(float));
+    if (acc == NULL || dense == NULL || mean == NULL) {
+        free(acc); free(dense); free(mean);
+        return ORACLE_EINVAL;
+    }
+    /* (1/K) sum_k C(Delta^(k)): binary64 sum in worker order, then /K, then fp32 */
+    for (int32_t k = 0; k < K; ++k) {
+        topk_decode(L, off, n, keep, sel + (int64_t)k * (d_pad / 64), vals + (int64_t)k * total,
+                    dense);
+        for (int32_t l = 0; l < L; ++l)
+            for (int64_t i = 0; i < n[l]; ++i) acc[off[l] + i] += (double)dense[off[l] + i];
+    }
+    int status = ORACLE_OK;
+    for (int32_t l = 0; l < L; ++l)
+        for (int64_t i = 0; i < n[l]; ++i) {
+            int64_t j = off[l] + i;
+            mean[j] = (float)(acc[j] / (double)K);
+            if (avg != NULL) avg[j] = mean[j];
+        }
+    if (mode == 0) {
+        /* single-way: the mean comes back uncompressed */
+        for (int32_t l = 0; l < L; ++l)
+            for (int64_t i = 0; i < n[l]; ++i) x[off[l] + i] = x[off[l] + i] - mean[off[l] + i];
+    } else {
+        int64_t voff = 0;
+        for (int32_t l = 0; l < L; ++l) {
+            /* server: Delta = e + mean; e <- Delta - C(Delta); x <- x - C(Delta) */
+            for (int64_t i = 0; i < n[l]; ++i)
+                e_srv[off[l] + i] = e_srv[off[l] + i] + mean[off[l] + i];
+            rc = topk_tensor(e_srv + off[l], n[l], keep[l], off[l], srv_sel, srv_rank,
+                             srv_vals + voff, e_srv + off[l], x + off[l]);
+            if (rc == ORACLE_EINVAL) status = rc;
+            else if (rc != ORACLE_OK && status == ORACLE_OK) status = rc;
+            voff += keep[l];
+        }
+    }
+    free(acc);
+    free(dense);
+    free(mean);
+    return status;
+}
+
+int oracle_topk_round(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                      int64_t t, int64_t period, int32_t K, float lr, float mu, int32_t mode,
+                      const int64_t* keep, const float* g, float* m, float* e, float* e_srv,
+                      float* x, float* xh, uint64_t* sel, uint32_t* rank, float* vals,
+                      uint64_t* srv_sel, uint32_t* srv_rank, float* srv_vals)
+{
+    int rc = oracle_round_begin(L, off, n, d_pad, t, period, K, mode, 1, e, e_srv, x, xh, NULL);
+    if (rc != ORACLE_OK) return rc;
+    /* the gradient at xh is the caller's input g */
+    int status = oracle_topk_compress(L, off, n, d_pad, K, lr, mu, keep, g, m, e, sel, rank,
+                                      vals);
+    if (status == ORACLE_EINVAL) return status;
+    rc = oracle_topk_aggregate(L, off, n, d_pad, K, mode, keep, sel, vals, NULL, e_srv, srv_sel,
+                               srv_rank, srv_vals, x);
+    if (rc != ORACLE_OK) status = rc;
+    return status;
 }

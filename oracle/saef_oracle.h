@@ -106,6 +106,39 @@ int oracle_round_momentum(int32_t L, const int64_t* off, const int64_t* n, int64
                           uint64_t* signs, float* scales, uint64_t* srv_signs,
                           float* srv_scales);
 
+/* Layer-wise Top-K sparsification (the paper's second compressor, kept
+ * count keep[l] per tensor, 1 <= keep[l] <= n[l]): C(v) keeps the keep[l]
+ * elements of largest |v| of each tensor (equal magnitudes: lower index
+ * first) and zeroes the rest.  Message of a sender: sel words (sign-word
+ * layout, bit set = element kept), rank words (uint32 per 64-bit word: kept
+ * elements of the tensor in the words before it) and the kept values of
+ * tensor l in index order at vals[voff_l ..), voff_l = keep[0] + ... +
+ * keep[l-1]; total = sum keep.  Values must be finite (else -2).
+ *
+ * Worker side: Delta = fma(lr, g, e) (with m: m = fma(mu, m, g), Delta =
+ * fma(lr, m, e); m NULL requires mu == 0), message of C(Delta), e <- Delta -
+ * C(Delta).  sel, rank: (K, d_pad/64); vals: (K, total). */
+int oracle_topk_compress(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                         int32_t K, float lr, float mu, const int64_t* keep, const float* g,
+                         float* m, float* e, uint64_t* sel, uint32_t* rank, float* vals);
+
+/* Server side: mean = fp32((sum_k C(Delta^(k)), binary64, worker order) / K),
+ * decoded from the messages (sel, vals; rank is not needed to decode).  mode
+ * 1: Delta = fp32(e_srv + mean), server message of C(Delta), e_srv <- Delta -
+ * C(Delta), x <- x - C(Delta); mode 0: x <- x - mean.  avg may be NULL. */
+int oracle_topk_aggregate(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                          int32_t K, int32_t mode, const int64_t* keep, const uint64_t* sel,
+                          const float* vals, float* avg, float* e_srv, uint64_t* srv_sel,
+                          uint32_t* srv_rank, float* srv_vals, float* x);
+
+/* One iteration of Algorithm 1 (SAEF branch) with the Top-K compressor:
+ * oracle_round_begin (SAEF), oracle_topk_compress, oracle_topk_aggregate. */
+int oracle_topk_round(int32_t L, const int64_t* off, const int64_t* n, int64_t d_pad,
+                      int64_t t, int64_t period, int32_t K, float lr, float mu, int32_t mode,
+                      const int64_t* keep, const float* g, float* m, float* e, float* e_srv,
+                      float* x, float* xh, uint64_t* sel, uint32_t* rank, float* vals,
+                      uint64_t* srv_sel, uint32_t* srv_rank, float* srv_vals);
+
 #ifdef __cplusplus
 }
 #endif

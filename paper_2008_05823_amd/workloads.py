@@ -262,6 +262,16 @@ def gradients(w: Workload, t: int, K: int | None = None) -> np.ndarray:
     return np.stack([gradient(w, t, k, se) for k in range(K)])
 
 
+def topk_keep(w: Workload, percent: float) -> np.ndarray:
+    """Kept elements per tensor for Top-K sparsification at `percent` (the
+    paper's Top-1%, 5%, 10%): k_l = ceil(n_l * percent / 100), at least 1.
+    Computed in integers (percent in hundredths) so no rounding can move it."""
+    hundredths = int(round(percent * 100))
+    n = w.sizes
+    k = (n * hundredths + 9999) // 10000
+    return np.maximum(k, 1).astype(np.int64)
+
+
 def algorithmic_bytes_per_param(K: int, mode: int = 1, averaging: bool = False,
                                 momentum: bool = False, step_ahead: bool = True,
                                 mismatch: bool = False) -> float:

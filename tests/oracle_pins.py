@@ -50,8 +50,60 @@ def pin_goldens(libpath):
         _run_golden(libpath, name)
 
 
+def _run_topk_golden(libpath, name, gd):
+    K = int(gd["K"][0])
+    lr = np.float32(float(gd["lr"][0]))
+    sizes = [int(s) for s in gd["sizes"]]
+    keep = np.array([int(k) for k in gd["keep"]], np.int64)
+    off, n, d_pad = _one_tensor_layout(sizes)
+    orc = O.Oracle(off, n, d_pad, libpath)
+    W = d_pad // 64
+    total = int(keep.sum())
+    n0 = sizes[0]
+    sel = np.zeros((K, W), np.uint64)
+    rank = np.zeros((K, W), np.uint32)
+    vals = np.zeros((K, total), np.float32)
+
+    def vec(v):
+        out = np.zeros(d_pad, np.float32)
+        out[:len(v)] = golden_io.floats(v)
+        return out
+
+    if gd["op"][0] == "topk_compress":
+        g = np.stack([vec(gd[f"g.{k}"]) for k in range(K)])
+        e = np.stack([vec(gd[f"e.{k}"]) for k in range(K)])
+        assert orc.topk_compress(K, lr, 0.0, keep, g, None, e, sel, rank, vals) == O.OK, name
+    else:
+        mode, period, rounds = int(gd["mode"][0]), int(gd["period"][0]), int(gd["rounds"][0])
+        x = vec(gd["x0"])
+        e = np.zeros((K, d_pad), np.float32)
+        e_srv = np.zeros(d_pad, np.float32)
+        xh = np.zeros((K, d_pad), np.float32)
+        srv_sel = np.zeros(W, np.uint64)
+        srv_rank = np.zeros(W, np.uint32)
+        srv_vals = np.zeros(total, np.float32)
+        for t in range(rounds):
+            g = np.stack([vec(gd[f"g.{t}.{k}"]) for k in range(K)])
+            rc = orc.topk_round(t, period, K, lr, 0.0, mode, keep, g, None, e, e_srv, x, xh, sel,
+                                rank, vals, srv_sel, srv_rank, srv_vals)
+            assert rc == O.OK, name
+        assert np.array_equal(x[:n0], golden_io.floats(gd["expect.x"])), (name, x[:n0])
+        if mode == 1:
+            assert np.array_equal(srv_sel, golden_io.words(gd["expect.srv_words"])), name
+            assert np.array_equal(srv_vals, golden_io.floats(gd["expect.srv_vals"])), name
+            assert np.array_equal(e_srv[:n0], golden_io.floats(gd["expect.e_srv"])), name
+    for k in range(K):
+        assert np.array_equal(sel[k], golden_io.words(gd[f"expect.words.{k}"])), (name, k)
+        assert np.array_equal(vals[k], golden_io.floats(gd[f"expect.vals.{k}"])), (name, k)
+        assert np.array_equal(e[k, :n0], golden_io.floats(gd[f"expect.e.{k}"])), (name, k, e[k])
+        if f"expect.xh.{k}" in gd:
+            assert np.array_equal(xh[k, :n0], golden_io.floats(gd[f"expect.xh.{k}"])), (name, k)
+
+
 def _run_golden(libpath, name):
     gd = golden_io.load(name)
+    if gd["op"][0].startswith("topk"):
+        return _run_topk_golden(libpath, name, gd)
     K = int(gd["K"][0])
     lr = np.float32(float(gd["lr"][0]))
     sizes = [int(s) for s in gd["sizes"]]
@@ -597,7 +649,255 @@ def pin_ef_variant(libpath):
             assert np.array_equal(b["xh"][k], exp)
 
 
-QUICK_PINS = [pin_goldens, pin_mismatch_identities, pin_mismatch_proposition, pin_ef_variant, pin_momentum_exact, pin_auxiliary_identity_momentum, pin_l1_fixed_exact, pin_compress_exact, pin_aggregate_exact,
+# ---------------------------------------------------------------- Top-K
+
+def _topk_message_dense(sel_row, rank_row, vals_row, off, n, keep):
+    """C(v) of every tensor decoded through the rank words (the oracle itself
+    decodes by walking the bits in order)."""
+    out = {}
+    voff = 0
+    for l in range(len(n)):
+        o, nl = int(off[l]), int(n[l])
+        c = np.zeros(nl, np.float32)
+        kept = np.zeros(nl, bool)
+        for i in range(nl):
+            w = o // 64 + i // 64
+            word = int(sel_row[w])
+            if (word >> (i % 64)) & 1:
+                below = bin(word & ((1 << (i % 64)) - 1)).count("1")
+                c[i] = vals_row[voff + int(rank_row[w]) + below]
+                kept[i] = True
+        out[l] = (c, kept)
+        voff += int(keep[l])
+    return out
+
+
+def _topk_values(rng, n):
+    """Values with repeated magnitudes (ties), zeros of both signs and spread."""
+    v = _rand_values(rng, n)
+    dup = rng.random(n) < 0.2
+    v[dup] = np.float32(0.375) * np.where(rng.random(int(dup.sum())) < 0.5, 1, -1)
+    return v
+
+
+def pin_topk_compress_exact(libpath, seed=41):
+    """Top-K worker step against the definition's properties: exactly k_l
+    kept, every kept magnitude >= every dropped one, equal magnitudes at the
+    cut kept in index order, Delta = fma(lr, g, e) rounded once (checked in
+    exact arithmetic), e = Delta - C(Delta) exactly, the rank words count the
+    kept elements before each word, padding untouched."""
+    rng = np.random.default_rng(seed)
+    sizes = [1, 3, 64, 65, 130, 200]
+    off, n, d_pad = _one_tensor_layout(sizes)
+    orc = O.Oracle(off, n, d_pad, libpath)
+    K, L = 3, len(sizes)
+    for keep in ([1, 1, 1, 1, 1, 1], [1, 2, 7, 64, 13, 100], [1, 3, 64, 65, 130, 200]):
+        keep = np.array(keep, np.int64)
+        g = np.full((K, d_pad), np.nan, np.float32)
+        e = np.full((K, d_pad), np.nan, np.float32)
+        for l in range(L):
+            g[:, off[l]:off[l] + n[l]] = _topk_values(rng, K * n[l]).reshape(K, n[l])
+            e[:, off[l]:off[l] + n[l]] = _topk_values(rng, K * n[l]).reshape(K, n[l]) * 0.01
+        e0 = e.copy()
+        sel = np.full((K, d_pad // 64), 0xFFFF, np.uint64)
+        rank = np.zeros((K, d_pad // 64), np.uint32)
+        vals = np.zeros((K, int(keep.sum())), np.float32)
+        assert orc.topk_compress(K, LR, 0.0, keep, g, None, e, sel, rank, vals) == O.OK
+        for k in range(K):
+            dec = _topk_message_dense(sel[k], rank[k], vals[k], off, n, keep)
+            for l in range(L):
+                o, nl = int(off[l]), int(n[l])
+                p = np.array([exact.rn32(Fraction(float(LR)) * exact.frac(g[k, o + i])
+                                         + exact.frac(e0[k, o + i])) for i in range(nl)],
+                             np.float32)
+                c, kept = dec[l]
+                assert kept.sum() == keep[l], (k, l)
+                mag = np.abs(p.astype(np.float64))
+                if kept.sum() < nl:
+                    lo_kept = mag[kept].min()
+                    assert mag[~kept].max() <= lo_kept, (k, l)
+                    ties_dropped = np.where(~kept & (mag == lo_kept))[0]
+                    ties_kept = np.where(kept & (mag == lo_kept))[0]
+                    if len(ties_dropped):
+                        assert ties_kept.max() < ties_dropped.min(), (k, l)
+                assert np.array_equal(c[kept], p[kept]), (k, l)
+                err = e[k, o:o + nl]
+                assert np.array_equal(err[kept], np.zeros(int(kept.sum()), np.float32))
+                # (values: the exact reference does not carry the sign of a zero)
+                assert np.array_equal(err[~kept], p[~kept])
+                nw = (nl + 63) // 64
+                if nl % 64:
+                    assert int(sel[k, o // 64 + nw - 1]) >> (nl % 64) == 0
+            pad = ~_tensor_mask(off, n, d_pad)
+            assert np.isnan(e[k, pad]).all(), "padding must not be written"
+
+
+def pin_topk_momentum_exact(libpath, seed=45):
+    """Top-K worker step with momentum (Algorithm 1): m <- mu m + g and Delta =
+    e + eta m, each rounded once (exact arithmetic); the message carries the
+    kept Delta values."""
+    rng = np.random.default_rng(seed)
+    sizes = [100, 3]
+    off, n, d_pad = _one_tensor_layout(sizes)
+    orc = O.Oracle(off, n, d_pad, libpath)
+    K = 2
+    keep = np.array([10, 2], np.int64)
+    mu = np.float32(0.9)
+    g = np.zeros((K, d_pad), np.float32)
+    m = np.zeros((K, d_pad), np.float32)
+    e = np.zeros((K, d_pad), np.float32)
+    for l in range(2):
+        sl = slice(int(off[l]), int(off[l] + n[l]))
+        g[:, sl] = _topk_values(rng, K * int(n[l])).reshape(K, -1)
+        m[:, sl] = _topk_values(rng, K * int(n[l])).reshape(K, -1)
+        e[:, sl] = _topk_values(rng, K * int(n[l])).reshape(K, -1) * 0.01
+    m0, e0 = m.copy(), e.copy()
+    sel = np.zeros((K, d_pad // 64), np.uint64)
+    rank = np.zeros((K, d_pad // 64), np.uint32)
+    vals = np.zeros((K, int(keep.sum())), np.float32)
+    assert orc.topk_compress(K, LR, mu, keep, g, m, e, sel, rank, vals) == O.OK
+    for k in range(K):
+        dec = _topk_message_dense(sel[k], rank[k], vals[k], off, n, keep)
+        for l in range(2):
+            o, nl = int(off[l]), int(n[l])
+            mm = np.array([exact.rn32(exact.frac(mu) * exact.frac(m0[k, o + i])
+                                      + exact.frac(g[k, o + i])) for i in range(nl)], np.float32)
+            assert np.array_equal(m[k, o:o + nl], mm), (k, l)
+            p = np.array([exact.rn32(exact.frac(LR) * exact.frac(mm[i])
+                                     + exact.frac(e0[k, o + i])) for i in range(nl)], np.float32)
+            c, kept = dec[l]
+            assert np.array_equal(c[kept], p[kept]) and np.array_equal(e[k, o:o + nl][~kept],
+                                                                       p[~kept]), (k, l)
+
+
+def pin_topk_delta_compressor(libpath, seed=42):
+    """Top-K is a delta-approximate compressor (the paper's compressor
+    assumption) with delta = k_l / n_l per tensor:
+    ||C(v) - v||^2 <= (1 - k_l/n_l) ||v||^2, in exact arithmetic."""
+    rng = np.random.default_rng(seed)
+    sizes = [5, 100, 257]
+    off, n, d_pad = _one_tensor_layout(sizes)
+    orc = O.Oracle(off, n, d_pad, libpath)
+    for trial in range(6):
+        keep = np.array([int(rng.integers(1, m + 1)) for m in sizes], np.int64)
+        g = np.zeros((1, d_pad), np.float32)
+        for l in range(len(sizes)):
+            g[0, off[l]:off[l] + n[l]] = _topk_values(rng, int(n[l]))
+        e = np.zeros_like(g)
+        sel = np.zeros((1, d_pad // 64), np.uint64)
+        rank = np.zeros((1, d_pad // 64), np.uint32)
+        vals = np.zeros((1, int(keep.sum())), np.float32)
+        assert orc.topk_compress(1, np.float32(1.0), 0.0, keep, g, None, e, sel, rank, vals) == 0
+        for l in range(len(sizes)):
+            o, nl = int(off[l]), int(n[l])
+            v = [exact.frac(x) for x in g[0, o:o + nl]]
+            r = [exact.frac(x) for x in e[0, o:o + nl]]   # v - C(v)
+            lhs = sum(x * x for x in r)
+            rhs = (1 - Fraction(int(keep[l]), nl)) * sum(x * x for x in v)
+            assert lhs <= rhs, (trial, l)
+
+
+def pin_topk_aggregate_exact(libpath, seed=43):
+    """Top-K server step: the mean of the decoded messages is the correctly
+    rounded binary64 worker-order sum / K (checked exactly when no binary64
+    rounding can occur: K = 4 and values of a few bits), Delta = fp32(e_srv +
+    mean), and the server message/error/x follow the Top-K definition; x
+    changes only at kept elements (x - Delta there)."""
+    rng = np.random.default_rng(seed)
+    sizes = [70, 129]
+    off, n, d_pad = _one_tensor_layout(sizes)
+    orc = O.Oracle(off, n, d_pad, libpath)
+    K, L = 4, 2
+    keep = np.array([9, 40], np.int64)
+    total = int(keep.sum())
+    g = np.zeros((K, d_pad), np.float32)
+    for l in range(L):
+        g[:, off[l]:off[l] + n[l]] = (rng.integers(-64, 65, (K, int(n[l]))) / 16.0)
+    e = np.zeros_like(g)
+    sel = np.zeros((K, d_pad // 64), np.uint64)
+    rank = np.zeros((K, d_pad // 64), np.uint32)
+    vals = np.zeros((K, total), np.float32)
+    assert orc.topk_compress(K, np.float32(1.0), 0.0, keep, g, None, e, sel, rank, vals) == 0
+    for mode in (0, 1):
+        x = (rng.integers(-100, 101, d_pad) / 8.0).astype(np.float32)
+        x0 = x.copy()
+        e_srv = (rng.integers(-8, 9, d_pad) / 32.0).astype(np.float32)
+        es0 = e_srv.copy()
+        avg = np.zeros(d_pad, np.float32)
+        ss = np.zeros(d_pad // 64, np.uint64)
+        sr = np.zeros(d_pad // 64, np.uint32)
+        sv = np.zeros(total, np.float32)
+        assert orc.topk_aggregate(K, mode, keep, sel, vals, x, e_srv, ss, sr, sv, avg) == 0
+        decs = [_topk_message_dense(sel[k], rank[k], vals[k], off, n, keep) for k in range(K)]
+        for l in range(L):
+            o, nl = int(off[l]), int(n[l])
+            mean = [exact.rn32(sum((exact.frac(decs[k][l][0][i]) for k in range(K)), Fraction(0))
+                               / K) for i in range(nl)]
+            assert np.array_equal(avg[o:o + nl], np.array(mean, np.float32)), (mode, l)
+            if mode == 0:
+                want = [exact.rn32(exact.frac(x0[o + i]) - exact.frac(mean[i])) for i in range(nl)]
+                assert np.array_equal(x[o:o + nl], np.array(want, np.float32))
+                continue
+            D = np.array([exact.rn32(exact.frac(es0[o + i]) + exact.frac(mean[i]))
+                          for i in range(nl)], np.float32)
+            c, kept = _topk_message_dense(ss, sr, sv, off, n, keep)[l]
+            assert kept.sum() == keep[l]
+            mag = np.abs(D.astype(np.float64))
+            if kept.sum() < nl:
+                assert mag[~kept].max() <= mag[kept].min()
+            assert np.array_equal(c[kept], D[kept])
+            assert np.array_equal(e_srv[o:o + nl][kept], np.zeros(int(kept.sum()), np.float32))
+            assert np.array_equal(e_srv[o:o + nl][~kept], D[~kept])
+            want_x = np.where(kept, [exact.rn32(exact.frac(x0[o + i]) - exact.frac(D[i]))
+                                     for i in range(nl)], x0[o:o + nl]).astype(np.float32)
+            assert np.array_equal(x[o:o + nl], want_x)
+
+
+def pin_topk_auxiliary_identity(libpath):
+    """Eq. (3) for any compressor: x~_T = x_T - (e_srv + mean_k e^(k)) =
+    x_0 - eta sum_t mean_k g_t (binary64 with a rounding allowance), with
+    Top-K in both modes and with averaging; keep = n gives plain SGD (no
+    error at all)."""
+    from paper_2008_05823_amd import workloads as W
+    for mode, period, pct in ((1, 0, 10), (0, 3, 5), (1, 2, 1), (1, 0, 100)):
+        w = W.custom([300, 64, 1, 129], K=3, period=period, rounds=5, mode=mode,
+                     scale_range=(1e-3, 1.0), seed=44 + pct)
+        off, n, d_pad = w.layout()
+        keep = W.topk_keep(w, pct)
+        orc = O.Oracle(off, n, d_pad, libpath)
+        K, L = w.K, w.L
+        x = W.initial_x(w)
+        x0 = x.astype(np.float64)
+        e = np.zeros((K, d_pad), np.float32)
+        e_srv = np.zeros(d_pad, np.float32)
+        xh = np.zeros((K, d_pad), np.float32)
+        sel = np.zeros((K, d_pad // 64), np.uint64)
+        rank = np.zeros((K, d_pad // 64), np.uint32)
+        vals = np.zeros((K, int(keep.sum())), np.float32)
+        ss = np.zeros(d_pad // 64, np.uint64)
+        sr = np.zeros(d_pad // 64, np.uint32)
+        sv = np.zeros(int(keep.sum()), np.float32)
+        gsum = np.zeros(d_pad)
+        mag = np.zeros(d_pad)
+        for t in range(w.rounds):
+            g = W.gradients(w, t)
+            assert orc.topk_round(t, period, K, np.float32(w.lr), 0.0, mode, keep, g, None, e,
+                                  e_srv, x, xh, sel, rank, vals, ss, sr, sv) == O.OK
+            gsum += g.astype(np.float64).mean(axis=0)
+            mag += np.abs(g.astype(np.float64)).mean(axis=0) * w.lr
+        m = W.tensor_mask(w)
+        xt = x.astype(np.float64) - (e_srv.astype(np.float64) * (mode == 1)
+                                     + e.astype(np.float64).mean(axis=0))
+        want = x0 - np.float64(np.float32(w.lr)) * gsum
+        tol = 16 * w.rounds * 2.0 ** -24 * (np.abs(x0) + mag + np.abs(xt)) + 1e-30
+        assert np.all(np.abs(xt - want)[m] <= tol[m]), (mode, period, pct)
+        if pct == 100:
+            assert not e[:, m].any() and not e_srv[m].any()
+
+
+QUICK_PINS = [pin_goldens, pin_topk_compress_exact, pin_topk_momentum_exact,
+              pin_topk_delta_compressor,
+              pin_topk_aggregate_exact, pin_topk_auxiliary_identity, pin_mismatch_identities, pin_mismatch_proposition, pin_ef_variant, pin_momentum_exact, pin_auxiliary_identity_momentum, pin_l1_fixed_exact, pin_compress_exact, pin_aggregate_exact,
               pin_step_ahead_and_average_exact, pin_auxiliary_identity,
               pin_delta_compressor_equality, pin_zero_error_is_scaled_signsgd,
               pin_identical_workers, pin_period_one]

@@ -41,6 +41,19 @@ MUTANTS = {
     "mismatch_ef_not_squared": ("a += u * u;", "a += fabs(u);"),
     "ef_variant_steps_ahead": ("if (variant == 1) /* SAEF: one step ahead */",
                                "if (variant >= 0) /* SAEF: one step ahead */"),
+    "topk_keeps_smallest": ("if (ma > mb) return -1;\n    if (ma < mb) return 1;",
+                            "if (ma < mb) return -1;\n    if (ma > mb) return 1;"),
+    "topk_tie_high_index": ("return (a < b) ? -1 : (a > b) ? 1 : 0;",
+                            "return (a < b) ? 1 : (a > b) ? -1 : 0;"),
+    "topk_error_keeps_value": ("err[i] = v[i] - c;", "err[i] = v[i];"),
+    "topk_rank_shifted": ("rank[off / 64 + w] = (uint32_t)count;",
+                          "rank[off / 64 + w] = (uint32_t)(count > 0 ? count - 1 : 0);"),
+    "topk_reupdate_plus": ("applied_to[i] = applied_to[i] - c;", "applied_to[i] = applied_to[i] + c;"),
+    "topk_mean_wrong_k": ("mean[j] = (float)(acc[j] / (double)K);",
+                          "mean[j] = (float)(acc[j] / (double)(K + 1));"),
+    "topk_value_magnitude": ("vals[count++] = v[i];", "vals[count++] = fabsf(v[i]);"),
+    "topk_momentum_dropped": ("mk[j] = fmaf(mu, mk[j], gk[j]);\n                    delta[j]",
+                              "mk[j] = gk[j];\n                    delta[j]"),
     "momentum_dropped": ("mk[j] = fmaf(mu, mk[j], gk[j]);", "mk[j] = gk[j];"),
     "momentum_swapped": ("mk[j] = fmaf(mu, mk[j], gk[j]);", "mk[j] = fmaf(mu, gk[j], mk[j]);"),
     "momentum_lr_dropped": ("ek[j] = fmaf(lr, mk[j], ek[j]);", "ek[j] = mk[j] + ek[j];"),
