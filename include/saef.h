@@ -198,6 +198,63 @@ int saef_materialize(const saef_layout* layout, int32_t K, int32_t mode, const f
                      const float* scales, const uint64_t* srv_signs, const float* srv_scales,
                      float* e_out, float* e_srv_out, float* x_out, hipStream_t stream);
 
+/* ---------------------------------------------------------------- Top-K
+ * The paper's second compressor (Experiments: Top-K sparsification with the
+ * sparsity in percent, layer-wise; "How related to compression?"): C(v)
+ * keeps the keep[l] elements of largest |v| of each tensor and sets the
+ * others to 0.  Equal magnitudes are kept in index order (lower index
+ * first), so the kept set is unique.  Values must be finite (Inf or NaN
+ * sets the SAEF_ERANGE flag); no other range limit applies.
+ *
+ * Message of one sender (worker k: row k of each array; server: one row):
+ *   sel[d_pad/64]    uint64 words in the sign-word layout, bit set = kept
+ *                    (bits past a tensor's end are 0);
+ *   rank[d_pad/64]   uint32 per word: kept elements of the tensor in its
+ *                    words before this one;
+ *   vals[total]      the kept values of tensor l, in index order, at
+ *                    voff_l = keep[0] + ... + keep[l-1]; total = sum keep.
+ * The Top-K state is always plain (no pending corrections): e = Delta -
+ * C(Delta) is Delta with the kept elements set to 0, and x is updated in
+ * place.  The tie rule, encoding and plain state are the library's own
+ * choices; the paper gives none. */
+typedef struct saef_topk saef_topk;
+
+/* Top-K plan on a layout: keep[L] (host, 1 <= keep[l] <= n[l]) is copied;
+ * the plan owns the selection scratch (per-chunk histograms, selection
+ * state, tile counts).  Calls using one plan must not run concurrently.
+ * Synchronises the device; the layout must outlive the plan. */
+int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk** out);
+int saef_topk_destroy(saef_topk* plan);
+/* total = sum keep, the length of one message's value array. */
+int saef_topk_info(const saef_topk* plan, int64_t* total);
+
+/* Worker side with Top-K: Delta = fma(lr, g, e) (with m != NULL: m =
+ * fma(mu, m, g), Delta = fma(lr, m, e), 0 <= mu < 1; m == NULL requires mu
+ * == 0); writes the message (sel, rank: (K, d_pad/64); vals: (K, total))
+ * and e <- Delta - C(Delta) in place. */
+int saef_topk_compress(const saef_topk* plan, int32_t K, float lr, float mu, const float* g,
+                       float* m, float* e, uint64_t* sel, uint32_t* rank, float* vals,
+                       hipStream_t stream);
+
+/* Server side with Top-K: mean = fp32((sum_k C(Delta^(k)), binary64, worker
+ * order) / K) decoded from the K messages.  SAEF_MODE_DC: Delta = fp32(e_srv
+ * + mean), server message (srv_sel, srv_rank, srv_vals) of C(Delta), e_srv
+ * <- Delta - C(Delta), x <- x - C(Delta).  SAEF_MODE_SC: x <- x - mean
+ * (e_srv and srv_* may be NULL).  avg (may be NULL) receives the mean. */
+int saef_topk_aggregate(const saef_topk* plan, int32_t K, int32_t mode, const uint64_t* sel,
+                        const uint32_t* rank, const float* vals, float* avg, float* e_srv,
+                        uint64_t* srv_sel, uint32_t* srv_rank, float* srv_vals, float* x,
+                        hipStream_t stream);
+
+/* One iteration t of Algorithm 1 (SAEF branch) with Top-K: error averaging
+ * when (t+1) mod period == 0 (period 0 = never), step ahead xh[k] = x -
+ * e[k], [gradient g computed at xh by the caller], saef_topk_compress (m
+ * may be NULL, then mu must be 0), saef_topk_aggregate. */
+int saef_topk_round(const saef_topk* plan, int64_t t, int64_t period, int32_t K, float lr,
+                    float mu, int32_t mode, const float* g, float* m, float* e, float* e_srv,
+                    float* x, float* xh, uint64_t* sel, uint32_t* rank, float* vals,
+                    uint64_t* srv_sel, uint32_t* srv_rank, float* srv_vals, hipStream_t stream);
+
 /* Synchronises `stream`, then returns and clears the layout's sticky device
  * flag: SAEF_ERANGE if any call since the last saef_status met a value with
  * |v| >= 2^19, Inf or NaN, SAEF_OK otherwise (SAEF_EHIP on a HIP error). */

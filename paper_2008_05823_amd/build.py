@@ -11,7 +11,8 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SOURCES = [os.path.join(HERE, "csrc", f) for f in ("saef_kernels.hip", "saef_api.hip")]
+SOURCES = [os.path.join(HERE, "csrc", f) for f in ("saef_kernels.hip", "saef_topk.hip",
+                                                          "saef_api.hip")]
 LIB = os.path.join(HERE, "libsaef.so")
 ARCH = "gfx950"
 

@@ -33,6 +33,20 @@ struct saef_layout {
   uint32_t ev_mask = 0;  // kinds being timed
 };
 
+// A Top-K plan: the kept count of every tensor and the selection scratch.
+struct saef_topk {
+  const saef_layout* layout = nullptr;
+  std::vector<int64_t> keep;
+  int64_t total_keep = 0;
+  saef::TkDev dev{};
+  void* mem_chunks = nullptr;
+  void* mem_tens = nullptr;
+  void* mem_hist = nullptr;
+  void* mem_hist2 = nullptr;
+  void* mem_sel = nullptr;
+  void* mem_tile_cnt = nullptr;
+};
+
 namespace {
 
 // Elements per work tile of a tensor of n elements: kTileElems, or more for
@@ -109,6 +123,17 @@ void free_layout(saef_layout* l) {
   (void)hipFree(l->mem_part2);
   (void)hipFree(l->mem_status);
   delete l;
+}
+
+void free_topk(saef_topk* p) {
+  if (p == nullptr) return;
+  (void)hipFree(p->mem_chunks);
+  (void)hipFree(p->mem_tens);
+  (void)hipFree(p->mem_hist);
+  (void)hipFree(p->mem_hist2);
+  (void)hipFree(p->mem_sel);
+  (void)hipFree(p->mem_tile_cnt);
+  delete p;
 }
 
 }  // namespace
@@ -540,6 +565,178 @@ int saef_profile_read(saef_layout* layout, int32_t* counts, double* total_ms) {
   }
   layout->ev_used = 0;
   return SAEF_OK;
+}
+
+int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk** out) {
+  if (out == nullptr) return SAEF_EINVAL;
+  *out = nullptr;
+  if (layout == nullptr || keep == nullptr) return SAEF_EINVAL;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return SAEF_EHIP;
+  if (dev != layout->device) return SAEF_EINVAL;
+  const int32_t L = layout->L;
+  for (int32_t l = 0; l < L; ++l)
+    if (keep[l] < 1 || keep[l] > layout->n[l]) return SAEF_EINVAL;
+  saef_topk* p = new (std::nothrow) saef_topk();
+  if (p == nullptr) return SAEF_EHIP;
+  p->layout = layout;
+  p->keep.assign(keep, keep + L);
+  std::vector<saef::TkChunk> chunks;
+  std::vector<saef::TkTensor> tens(L);
+  int32_t max_chunks = 1;
+  for (int32_t l = 0; l < L; ++l) {
+    const int64_t n = layout->n[l];
+    const int64_t nc = (n + saef::kTkChunk - 1) / saef::kTkChunk;
+    tens[l] = saef::TkTensor{p->total_keep, keep[l], (int32_t)chunks.size(), (int32_t)nc};
+    p->total_keep += keep[l];
+    max_chunks = std::max(max_chunks, (int32_t)nc);
+    for (int64_t c = 0; c < nc; ++c)
+      chunks.push_back(saef::TkChunk{layout->off[l] + c * saef::kTkChunk, l,
+                                     (int32_t)std::min<int64_t>(saef::kTkChunk,
+                                                                n - c * saef::kTkChunk)});
+  }
+  const int32_t red_split = max_chunks > saef::kTkRedChunks
+                                ? (max_chunks + saef::kTkRedChunks - 1) / saef::kTkRedChunks
+                                : 1;
+  const size_t rows = (size_t)layout->k_max + 1;
+  const size_t hist_bytes = rows * chunks.size() * saef::kTkBins * sizeof(uint32_t);
+  const size_t hist2_bytes =
+      red_split > 1 ? rows * L * red_split * saef::kTkBins * sizeof(uint32_t) : 0;
+  const size_t sel_bytes = rows * L * sizeof(saef::TkSel);
+  const size_t cnt_bytes = rows * layout->dev.n_tiles * sizeof(uint32_t);
+  hipError_t err = hipMalloc(&p->mem_chunks, chunks.size() * sizeof(saef::TkChunk));
+  if (err == hipSuccess) err = hipMalloc(&p->mem_tens, tens.size() * sizeof(saef::TkTensor));
+  if (err == hipSuccess) err = hipMalloc(&p->mem_hist, hist_bytes);
+  if (err == hipSuccess && hist2_bytes) err = hipMalloc(&p->mem_hist2, hist2_bytes);
+  if (err == hipSuccess) err = hipMalloc(&p->mem_sel, sel_bytes);
+  if (err == hipSuccess) err = hipMalloc(&p->mem_tile_cnt, cnt_bytes);
+  if (err == hipSuccess)
+    err = hipMemcpy(p->mem_chunks, chunks.data(), chunks.size() * sizeof(saef::TkChunk),
+                    hipMemcpyHostToDevice);
+  if (err == hipSuccess)
+    err = hipMemcpy(p->mem_tens, tens.data(), tens.size() * sizeof(saef::TkTensor),
+                    hipMemcpyHostToDevice);
+  if (err == hipSuccess) err = hipMemset(p->mem_sel, 0, sel_bytes);
+  if (err == hipSuccess) err = hipDeviceSynchronize();
+  if (err != hipSuccess) {
+    free_topk(p);
+    return SAEF_EHIP;
+  }
+  saef::TkDev& d = p->dev;
+  d.chunks = static_cast<const saef::TkChunk*>(p->mem_chunks);
+  d.tens = static_cast<const saef::TkTensor*>(p->mem_tens);
+  d.hist = static_cast<uint32_t*>(p->mem_hist);
+  d.hist2 = static_cast<uint32_t*>(p->mem_hist2);
+  d.sel = static_cast<saef::TkSel*>(p->mem_sel);
+  d.tile_cnt = static_cast<uint32_t*>(p->mem_tile_cnt);
+  d.n_chunks = (int64_t)chunks.size();
+  d.total_keep = p->total_keep;
+  d.red_split = red_split;
+  *out = p;
+  return SAEF_OK;
+}
+
+int saef_topk_destroy(saef_topk* plan) {
+  if (plan == nullptr) return SAEF_EINVAL;
+  free_topk(plan);
+  return SAEF_OK;
+}
+
+int saef_topk_info(const saef_topk* plan, int64_t* total_keep) {
+  if (plan == nullptr) return SAEF_EINVAL;
+  if (total_keep) *total_keep = plan->total_keep;
+  return SAEF_OK;
+}
+
+int saef_topk_compress(const saef_topk* plan, int32_t K, float lr, float mu, const float* g,
+                       float* m, float* e, uint64_t* sel, uint32_t* rank, float* vals,
+                       hipStream_t stream) {
+  if (plan == nullptr) return SAEF_EINVAL;
+  const saef_layout* layout = plan->layout;
+  int rc = check_common(layout, K);
+  if (rc != SAEF_OK) return rc;
+  if (!std::isfinite(lr) || (m == nullptr ? mu != 0.0f : !mu_ok(mu))) return SAEF_EINVAL;
+  if (!f32_ok(g) || !f32_ok(e) || !u64_ok(sel) || rank == nullptr || !aligned(rank, 4) ||
+      !f32_ok(vals))
+    return SAEF_EINVAL;
+  const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
+  const size_t wb = (size_t)K * (layout->d_pad / 64) * sizeof(uint64_t);
+  const size_t rb = (size_t)K * (layout->d_pad / 64) * sizeof(uint32_t);
+  const size_t mb = (size_t)K * plan->total_keep * sizeof(float);
+  if (overlap(g, vb, e, vb) || overlap(vals, mb, e, vb) || overlap(vals, mb, g, vb) ||
+      overlap(sel, wb, e, vb) || overlap(rank, rb, e, vb) || overlap(rank, rb, vals, mb) ||
+      overlap(sel, wb, vals, mb) || overlap(sel, wb, rank, rb))
+    return SAEF_EINVAL;
+  if (m != nullptr && (!f32_ok(m) || overlap(m, vb, g, vb) || overlap(m, vb, e, vb) ||
+                       overlap(m, vb, vals, mb)))
+    return SAEF_EINVAL;
+  return hip_rc(timed(layout, 1, [&](const saef::LaunchEvents& ev) {
+    return saef::launch_topk_compress(layout->dev, plan->dev, K, lr, mu, g, m, e, sel, rank,
+                                      vals, stream, ev);
+  }));
+}
+
+int saef_topk_aggregate(const saef_topk* plan, int32_t K, int32_t mode, const uint64_t* sel,
+                        const uint32_t* rank, const float* vals, float* avg, float* e_srv,
+                        uint64_t* srv_sel, uint32_t* srv_rank, float* srv_vals, float* x,
+                        hipStream_t stream) {
+  if (plan == nullptr) return SAEF_EINVAL;
+  const saef_layout* layout = plan->layout;
+  int rc = check_common(layout, K);
+  if (rc != SAEF_OK) return rc;
+  if (mode != SAEF_MODE_SC && mode != SAEF_MODE_DC) return SAEF_EINVAL;
+  if (!u64_ok(sel) || rank == nullptr || !aligned(rank, 4) || !f32_ok(vals) || !f32_ok(x))
+    return SAEF_EINVAL;
+  if (avg != nullptr && !f32_ok(avg)) return SAEF_EINVAL;
+  const size_t xb = layout->d_pad * sizeof(float);
+  const size_t wb1 = (layout->d_pad / 64) * sizeof(uint64_t);
+  const size_t rb1 = (layout->d_pad / 64) * sizeof(uint32_t);
+  const size_t mb1 = plan->total_keep * sizeof(float);
+  if (mode == SAEF_MODE_DC) {
+    if (!f32_ok(e_srv) || !u64_ok(srv_sel) || srv_rank == nullptr || !aligned(srv_rank, 4) ||
+        !f32_ok(srv_vals))
+      return SAEF_EINVAL;
+    if (overlap(e_srv, xb, x, xb) || overlap(srv_vals, mb1, x, xb) ||
+        overlap(srv_vals, mb1, e_srv, xb) || overlap(srv_sel, wb1, x, xb) ||
+        overlap(srv_sel, wb1, e_srv, xb) || overlap(srv_rank, rb1, x, xb) ||
+        overlap(srv_rank, rb1, e_srv, xb) || overlap(srv_rank, rb1, srv_vals, mb1))
+      return SAEF_EINVAL;
+  }
+  if (avg != nullptr && (overlap(avg, xb, x, xb) || (e_srv && overlap(avg, xb, e_srv, xb))))
+    return SAEF_EINVAL;
+  return hip_rc(timed(layout, 3, [&](const saef::LaunchEvents& ev) {
+    return saef::launch_topk_aggregate(layout->dev, plan->dev, K, mode, sel, rank, vals, avg,
+                                       e_srv, srv_sel, srv_rank, srv_vals, x, stream, ev);
+  }));
+}
+
+int saef_topk_round(const saef_topk* plan, int64_t t, int64_t period, int32_t K, float lr,
+                    float mu, int32_t mode, const float* g, float* m, float* e, float* e_srv,
+                    float* x, float* xh, uint64_t* sel, uint32_t* rank, float* vals,
+                    uint64_t* srv_sel, uint32_t* srv_rank, float* srv_vals, hipStream_t stream) {
+  if (plan == nullptr) return SAEF_EINVAL;
+  const saef_layout* layout = plan->layout;
+  int rc = check_common(layout, K);
+  if (rc != SAEF_OK) return rc;
+  if (t < 0 || period < 0) return SAEF_EINVAL;
+  if (!f32_ok(x) || !f32_ok(xh) || !f32_ok(e)) return SAEF_EINVAL;
+  const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
+  const size_t xb = layout->d_pad * sizeof(float);
+  if (overlap(xh, vb, x, xb) || overlap(xh, vb, e, vb) || overlap(e, vb, x, xb) ||
+      (g != nullptr && overlap(xh, vb, g, vb)))
+    return SAEF_EINVAL;
+  // the Top-K state is always plain: step ahead (after averaging when due)
+  const bool averaging = period > 0 && (t + 1) % period == 0;
+  rc = hip_rc(timed(layout, averaging ? 5 : 0, [&](const saef::LaunchEvents& ev) {
+    return saef::launch_step_ahead(layout->dev, K, x, nullptr, nullptr, false, e, nullptr,
+                                   nullptr, false, averaging, xh, stream, ev);
+  }));
+  if (rc != SAEF_OK) return rc;
+  // [gradient slot: g was computed by the caller at xh]
+  rc = saef_topk_compress(plan, K, lr, mu, g, m, e, sel, rank, vals, stream);
+  if (rc != SAEF_OK) return rc;
+  return saef_topk_aggregate(plan, K, mode, sel, rank, vals, nullptr, e_srv, srv_sel, srv_rank,
+                             srv_vals, x, stream);
 }
 
 int saef_status(const saef_layout* layout, hipStream_t stream) {

@@ -1,0 +1,43 @@
+// Device helpers shared by the kernel translation units of the SAEF library.
+#pragma once
+
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "saef_internal.h"
+
+namespace saef {
+
+typedef unsigned long long u64;
+
+constexpr int kXcds = 8;  // MI355X: 8 XCDs, workgroups dealt round-robin
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+}
+
+// Streaming accesses: nothing is re-read soon enough to profit from the caches.
+__device__ __forceinline__ float ld_nt(const float* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ void st_nt(float* p, float v) { __builtin_nontemporal_store(v, p); }
+
+// (1/K) * acc, binary64; inv_k is 1/K when K is a power of two (exact), else 0.
+__device__ __forceinline__ double mean_of(double acc, double inv_k, int K) {
+  return (inv_k != 0.0) ? acc * inv_k : acc / (double)K;
+}
+
+// Host: 1/K when K is a power of two (then acc * inv_k == acc / K exactly), else 0.
+inline double inv_pow2(int K) { return (K & (K - 1)) == 0 ? 1.0 / (double)K : 0.0; }
+
+// Workgroups of 4 waves, one wave per tile.
+inline unsigned per_wave_grid(const DevLayout& lay) {
+  return (unsigned)((lay.n_tiles + kWaves - 1) / kWaves);
+}
+
+}  // namespace saef
+
+// All launches go through hipExtLaunchKernelGGL so that an optional event
+// pair (a LaunchEvents `ev` in scope) is stamped by the dispatch itself.
+#define SAEF_LAUNCH(kernel, grid, block, shmem, stream, ...) \
+  hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ev.start, ev.stop, 0, __VA_ARGS__)

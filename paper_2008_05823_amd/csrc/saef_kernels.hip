@@ -26,25 +26,15 @@
 // pending corrections for callers that want plain values.
 #include <hip/hip_ext.h>
 
+#include "saef_device.h"
 #include "saef_internal.h"
 
 namespace saef {
 namespace {
 
-typedef unsigned long long u64;
-
 constexpr uint32_t kAbsLimitBits = 0x49000000u;  // bit pattern of 2^19
 constexpr int kU = 4;     // words per wave per pass in the per-(tile, worker) kernels
 constexpr int kWPW = 16;  // words per wave per pass in the one-wave-per-tile kernels
-constexpr int kXcds = 8;  // MI355X: 8 XCDs, workgroups dealt round-robin
-
-__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
-__device__ __forceinline__ int wave_id() {
-  return __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-}
-
-__device__ __forceinline__ float ld_nt(const float* p) { return __builtin_nontemporal_load(p); }
-__device__ __forceinline__ void st_nt(float* p, float v) { __builtin_nontemporal_store(v, p); }
 
 // Per lane: bit `lane` of the 64-bit mask ? if1 : if0, in one VALU op
 // (v_cndmask with the mask as its lane condition).  The mask must be the
@@ -151,10 +141,6 @@ __device__ float scale_from_sum(u64 hi, u64 lo, int64_t n) {
   return (float)(mean * 0x1p-80);
 }
 
-// (1/K) * acc, binary64; inv_k is 1/K when K is a power of two (exact), else 0.
-__device__ __forceinline__ double mean_of(double acc, double inv_k, int K) {
-  return (inv_k != 0.0) ? acc * inv_k : acc / (double)K;
-}
 
 // Stores the exact partial of (row, tile) summed over one wave.
 __device__ __forceinline__ void wave_partial(const DevLayout& lay, int row, int64_t tile, u64 lo,
@@ -946,16 +932,6 @@ __global__ __launch_bounds__(kBlock) void k_mfinalize2(DevLayout lay, int K,
   out[lay.L + l] = b / (double)K;
 }
 
-double inv_pow2(int K) { return (K & (K - 1)) == 0 ? 1.0 / (double)K : 0.0; }
-
-// All launches go through hipExtLaunchKernelGGL so that an optional event
-// pair is stamped by the dispatch itself.
-#define SAEF_LAUNCH(kernel, grid, block, shmem, stream, ...) \
-  hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ev.start, ev.stop, 0, __VA_ARGS__)
-
-unsigned per_wave_grid(const DevLayout& lay) {
-  return (unsigned)((lay.n_tiles + kWaves - 1) / kWaves);
-}
 
 }  // namespace
 

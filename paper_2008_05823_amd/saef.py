@@ -48,6 +48,13 @@ _SIGS = {
                          _P],
     "saef_round_end": [_P, _i64, _i64, _i32, _f32, _f32, _i32, _P, _P, _P, _P, _P, _P, _P, _P,
                        _P, _P],
+    "saef_topk_create": [_P, _P, ctypes.POINTER(_P)],
+    "saef_topk_destroy": [_P],
+    "saef_topk_info": [_P, _P],
+    "saef_topk_compress": [_P, _i32, _f32, _f32, _P, _P, _P, _P, _P, _P, _P],
+    "saef_topk_aggregate": [_P, _i32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P],
+    "saef_topk_round": [_P, _i64, _i64, _i32, _f32, _f32, _i32, _P, _P, _P, _P, _P, _P, _P, _P,
+                        _P, _P, _P, _P, _P],
     "saef_materialize": [_P, _i32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P],
     "saef_status": [_P, _P],
     "saef_profile_enable": [_P, _i32, ctypes.c_uint32],
@@ -198,6 +205,72 @@ def saef_round_momentum(layout: Layout, t: int, period: int, K: int, lr: float, 
            _lib.saef_round_momentum(layout.handle, t, period, K, lr, mu, mode, _f(g), _f(m),
                                     _f(e), _f(e_srv), _f(x), _f(xh), _w(signs), _f(scales),
                                     _w(srv_signs), _f(srv_scales), _stream(stream)))
+
+
+def _u32(t):
+    """Rank words: int32 or uint32 device tensors (the same bits)."""
+    if t is None:
+        return None
+    if t.dtype not in (torch.int32, torch.uint32):
+        raise TypeError(f"rank words must be int32/uint32, got {t.dtype}")
+    return _dev(t, t.dtype)
+
+
+class TopK:
+    """A Top-K plan on a layout (see saef_topk_create); keep[l] per tensor."""
+
+    def __init__(self, layout: "Layout", keep):
+        k = (ctypes.c_int64 * len(keep))(*[int(v) for v in keep])
+        if len(k) != layout.L:
+            raise ValueError("one kept count per tensor")
+        handle = _P()
+        _check("saef_topk_create", _lib.saef_topk_create(layout.handle, k, ctypes.byref(handle)))
+        self._h = handle
+        self.layout = layout  # the layout must outlive the plan
+        total = _i64()
+        _check("saef_topk_info", _lib.saef_topk_info(self._h, ctypes.byref(total)))
+        self.total = int(total.value)
+
+    @property
+    def handle(self):
+        if self._h is None:
+            raise ValueError("plan destroyed")
+        return self._h
+
+    def destroy(self):
+        if self._h is not None:
+            _check("saef_topk_destroy", _lib.saef_topk_destroy(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
+def saef_topk_compress(plan: TopK, K: int, lr: float, mu: float, g, m, e, sel, rank, vals,
+                       stream=None):
+    _check("saef_topk_compress",
+           _lib.saef_topk_compress(plan.handle, K, lr, mu, _f(g), _f(m), _f(e), _w(sel),
+                                   _u32(rank), _f(vals), _stream(stream)))
+
+
+def saef_topk_aggregate(plan: TopK, K: int, mode: int, sel, rank, vals, x, e_srv=None,
+                        srv_sel=None, srv_rank=None, srv_vals=None, avg=None, stream=None):
+    _check("saef_topk_aggregate",
+           _lib.saef_topk_aggregate(plan.handle, K, mode, _w(sel), _u32(rank), _f(vals), _f(avg),
+                                    _f(e_srv), _w(srv_sel), _u32(srv_rank), _f(srv_vals), _f(x),
+                                    _stream(stream)))
+
+
+def saef_topk_round(plan: TopK, t: int, period: int, K: int, lr: float, mu: float, mode: int,
+                    g, m, e, e_srv, x, xh, sel, rank, vals, srv_sel=None, srv_rank=None,
+                    srv_vals=None, stream=None):
+    _check("saef_topk_round",
+           _lib.saef_topk_round(plan.handle, t, period, K, lr, mu, mode, _f(g), _f(m), _f(e),
+                                _f(e_srv), _f(x), _f(xh), _w(sel), _u32(rank), _f(vals),
+                                _w(srv_sel), _u32(srv_rank), _f(srv_vals), _stream(stream)))
 
 
 def saef_round_begin(layout: Layout, t: int, period: int, K: int, mode: int, variant: int, e,

@@ -1,0 +1,290 @@
+"""Parity of the layer-wise Top-K path of the HIP library with the CPU oracle
+(needs an MI355X).
+
+The kept set is a discrete decision taken on exact keys on both sides, so
+everything is compared bit for bit: selection words, rank words, kept
+values, errors, weights.  Inputs include heavy ties (few distinct
+magnitudes), exact zeros of both signs, tensors spanning many histogram
+chunks (a second reduction level above 64 chunks) and ragged sizes.
+"""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2008_05823_amd import workloads as W
+from tests import gpu_harness as H
+
+pytestmark = pytest.mark.gpu
+
+LR = np.float32(0.1)
+ADVERSARIAL = [1, 3, 4, 10, 63, 64, 65, 255, 256, 257, 4095, 4096, 4097, 8193, 12345]
+
+
+def _case(msg):
+    print(f"[case] {msg}", flush=True)
+
+
+def _tie_values(rng, shape, levels=4):
+    """Values with few distinct magnitudes (long runs of equal keys), signed
+    zeros included."""
+    mag = rng.integers(0, levels, shape).astype(np.float32) * np.float32(0.25)
+    sign = np.where(rng.random(shape) < 0.5, -1.0, 1.0).astype(np.float32)
+    return (mag * sign).astype(np.float32)
+
+
+class TopkOracle:
+    def __init__(self, w, keep, K=None, x0=None, mu=None):
+        from oracle import oracle as O
+        self.O = O
+        self.w, self.K = w, (w.K if K is None else K)
+        off, n, d_pad = w.layout()
+        self.orc = O.Oracle(off, n, d_pad)
+        self.keep = np.asarray(keep, np.int64)
+        total = int(self.keep.sum())
+        Wd = d_pad // 64
+        self.x = (W.initial_x(w) if x0 is None else x0).copy()
+        self.e = np.zeros((self.K, d_pad), np.float32)
+        self.m = np.zeros((self.K, d_pad), np.float32) if mu is not None else None
+        self.mu = mu
+        self.e_srv = np.zeros(d_pad, np.float32)
+        self.xh = np.zeros((self.K, d_pad), np.float32)
+        self.sel = np.zeros((self.K, Wd), np.uint64)
+        self.rank = np.zeros((self.K, Wd), np.uint32)
+        self.vals = np.zeros((self.K, total), np.float32)
+        self.srv_sel = np.zeros(Wd, np.uint64)
+        self.srv_rank = np.zeros(Wd, np.uint32)
+        self.srv_vals = np.zeros(total, np.float32)
+
+    def round(self, t, g, period=None, mode=None):
+        w = self.w
+        mu = np.float32(0.0 if self.mu is None else self.mu)
+        rc = self.orc.topk_round(t, w.period if period is None else period, self.K,
+                                 np.float32(w.lr), mu, w.mode if mode is None else mode,
+                                 self.keep, g, self.m, self.e, self.e_srv, self.x, self.xh,
+                                 self.sel, self.rank, self.vals, self.srv_sel, self.srv_rank,
+                                 self.srv_vals)
+        assert rc == self.O.OK, rc
+
+
+class TopkGpu:
+    def __init__(self, w, keep, K=None, x0=None, mu=None):
+        from paper_2008_05823_amd import saef
+        self.saef = saef
+        self.w, self.K, self.mu = w, (w.K if K is None else K), mu
+        off, n, d_pad = w.layout()
+        self.layout = saef.Layout(off, n, d_pad, self.K)
+        self.plan = saef.TopK(self.layout, keep)
+        total = self.plan.total
+        f32 = dict(dtype=torch.float32, device="cuda")
+        Wd = d_pad // 64
+        self.x = H.dev(W.initial_x(w) if x0 is None else x0)
+        self.e = torch.zeros((self.K, d_pad), **f32)
+        self.m = torch.zeros((self.K, d_pad), **f32) if mu is not None else None
+        self.e_srv = torch.zeros(d_pad, **f32)
+        self.xh = torch.zeros((self.K, d_pad), **f32)
+        self.g = torch.zeros((self.K, d_pad), **f32)
+        self.sel = torch.zeros((self.K, Wd), dtype=torch.int64, device="cuda")
+        self.rank = torch.zeros((self.K, Wd), dtype=torch.int32, device="cuda")
+        self.vals = torch.zeros((self.K, total), **f32)
+        self.srv_sel = torch.zeros(Wd, dtype=torch.int64, device="cuda")
+        self.srv_rank = torch.zeros(Wd, dtype=torch.int32, device="cuda")
+        self.srv_vals = torch.zeros(total, **f32)
+
+    def round(self, t, g, period=None, mode=None):
+        w = self.w
+        self.g.copy_(torch.from_numpy(g) if isinstance(g, np.ndarray) else g)
+        self.saef.saef_topk_round(self.plan, t, w.period if period is None else period, self.K,
+                                  w.lr, 0.0 if self.mu is None else self.mu,
+                                  w.mode if mode is None else mode, self.g, self.m, self.e,
+                                  self.e_srv, self.x, self.xh, self.sel, self.rank, self.vals,
+                                  self.srv_sel, self.srv_rank, self.srv_vals)
+
+    def status(self):
+        return self.saef.saef_status(self.layout)
+
+
+def _u32(t):
+    return t.cpu().numpy().view(np.uint32)
+
+
+def compare_topk(gpu: TopkGpu, orc: TopkOracle, t, what, mode=1):
+    w = orc.w
+    off, n, d_pad = w.layout()
+    m = W.tensor_mask(w)
+    wm = H.tensor_word_mask(off, n, d_pad)
+    tag = f"{what} t={t}"
+    torch.cuda.synchronize()
+    H.assert_words_equal(H.host(gpu.sel, np.uint64), orc.sel, wm, f"{tag} worker selection")
+    got_rank = _u32(gpu.rank)
+    assert np.array_equal(got_rank[:, wm], orc.rank[:, wm]), f"{tag} worker rank words"
+    H.assert_f32_equal(H.host(gpu.vals), orc.vals, np.ones(orc.vals.shape[-1], bool),
+                       f"{tag} worker values")
+    H.assert_f32_equal(H.host(gpu.e), orc.e, m, f"{tag} worker errors")
+    H.assert_f32_equal(H.host(gpu.xh), orc.xh, m, f"{tag} step-ahead weights")
+    H.assert_f32_equal(H.host(gpu.x), orc.x, m, f"{tag} weights")
+    if orc.m is not None:
+        H.assert_f32_equal(H.host(gpu.m), orc.m, m, f"{tag} momentum buffers")
+    if mode == 1:
+        H.assert_words_equal(H.host(gpu.srv_sel, np.uint64), orc.srv_sel, wm,
+                             f"{tag} server selection")
+        assert np.array_equal(_u32(gpu.srv_rank)[wm], orc.srv_rank[wm]), f"{tag} server ranks"
+        H.assert_f32_equal(H.host(gpu.srv_vals), orc.srv_vals,
+                           np.ones(orc.srv_vals.shape[-1], bool), f"{tag} server values")
+        H.assert_f32_equal(H.host(gpu.e_srv), orc.e_srv, m, f"{tag} server error")
+
+
+COMPRESS_CASES = {
+    # name: (K, sizes, keep rule, value source)
+    "adversarial_1pct": (3, ADVERSARIAL, 1, "grad"),
+    "adversarial_keep_all": (2, ADVERSARIAL, 100, "grad"),
+    "ties_10pct": (4, [300_000, 77, 64, 4097], 10, "ties"),
+    "ties_keep_one": (2, [5000, 1, 130], "one", "ties"),
+    "many_chunks": (2, [64 * 65536 + 4097, 33], 5, "grad"),   # > 64 chunks: second reduce level
+    "big_ties": (2, [70 * 65536 + 5], 1, "ties"),              # tie cut in a later chunk
+}
+
+
+def _keep(w, rule):
+    if rule == "one":
+        return np.ones(w.L, np.int64)
+    return W.topk_keep(w, rule)
+
+
+COMPRESS_RUNS = [(name, False) for name in COMPRESS_CASES] + [
+    ("adversarial_1pct", True), ("ties_10pct", True)]
+
+
+@pytest.mark.parametrize("name,momentum", COMPRESS_RUNS,
+                         ids=[f"{n}-{'momentum' if m else 'plain'}" for n, m in COMPRESS_RUNS])
+def test_topk_compress_parity(name, momentum):
+    K, sizes, rule, src = COMPRESS_CASES[name]
+    _case(f"topk compress {name} K={K} momentum={momentum}")
+    seed = zlib.crc32(name.encode())
+    w = W.custom(sizes, K=K, scale_range=(1e-3, 1.0), seed=seed % 1000 + 11)
+    keep = _keep(w, rule)
+    off, n, d_pad = w.layout()
+    msk = W.tensor_mask(w)
+    rng = np.random.default_rng(seed)
+    if src == "ties":
+        g = _tie_values(rng, (K, d_pad))
+        e = _tie_values(rng, (K, d_pad))
+    else:
+        g = W.gradients(w, 0)
+        e = (rng.standard_normal((K, d_pad)) * 0.01).astype(np.float32)
+    g[:, ~msk] = np.nan
+    e[:, ~msk] = np.nan   # padding must stay untouched
+    mu = 0.9 if momentum else None
+    m0 = _tie_values(rng, (K, d_pad)) if momentum else None
+    orc = TopkOracle(w, keep, mu=mu)
+    orc.e[:] = e
+    if momentum:
+        orc.m[:] = m0
+    rc = orc.orc.topk_compress(K, LR, np.float32(mu or 0.0), keep, g, orc.m, orc.e, orc.sel,
+                               orc.rank, orc.vals)
+    assert rc == 0
+    gs = TopkGpu(w, keep, mu=mu)
+    gs.e.copy_(torch.from_numpy(e))
+    if momentum:
+        gs.m.copy_(torch.from_numpy(m0))
+    gs.saef.saef_topk_compress(gs.plan, K, float(LR), float(mu or 0.0), H.dev(g), gs.m, gs.e,
+                               gs.sel, gs.rank, gs.vals)
+    torch.cuda.synchronize()
+    wm = H.tensor_word_mask(off, n, d_pad)
+    H.assert_words_equal(H.host(gs.sel, np.uint64), orc.sel, wm, "selection")
+    assert np.array_equal(_u32(gs.rank)[:, wm], orc.rank[:, wm]), "rank words"
+    H.assert_f32_equal(H.host(gs.vals), orc.vals, np.ones(orc.vals.shape[-1], bool), "values")
+    got_e = H.host(gs.e)
+    H.assert_f32_equal(got_e, orc.e, msk, "errors")
+    assert np.isnan(got_e[:, ~msk]).all(), "padding written"
+    if momentum:
+        H.assert_f32_equal(H.host(gs.m), orc.m, msk, "momentum buffers")
+    assert gs.status() == 0
+
+
+@pytest.mark.parametrize("mode", [1, 0], ids=["dc", "sc"])
+def test_topk_aggregate_parity(mode):
+    """Server step on oracle-made messages (K = 5: the /K is not a power of two)."""
+    K = 5
+    w = W.custom(ADVERSARIAL + [200_000], K=K, scale_range=(1e-3, 1.0), seed=321, mode=mode)
+    keep = W.topk_keep(w, 5)
+    _case(f"topk aggregate mode={mode}")
+    off, n, d_pad = w.layout()
+    msk = W.tensor_mask(w)
+    orc = TopkOracle(w, keep)
+    g = W.gradients(w, 0)
+    assert orc.orc.topk_compress(K, LR, 0.0, keep, g, None, orc.e, orc.sel, orc.rank,
+                                 orc.vals) == 0
+    rng = np.random.default_rng(9)
+    es0 = (rng.standard_normal(d_pad) * 0.01).astype(np.float32)
+    orc.e_srv[:] = es0
+    avg = np.zeros(d_pad, np.float32)
+    x0 = orc.x.copy()
+    assert orc.orc.topk_aggregate(K, mode, keep, orc.sel, orc.vals, orc.x, orc.e_srv,
+                                  orc.srv_sel, orc.srv_rank, orc.srv_vals, avg) == 0
+    gs = TopkGpu(w, keep)
+    sel = H.dev(orc.sel)
+    rank = torch.from_numpy(orc.rank.view(np.int32)).cuda()
+    vals = H.dev(orc.vals)
+    gs.e_srv.copy_(torch.from_numpy(es0))
+    gs.x.copy_(torch.from_numpy(x0))
+    avg_d = torch.zeros(d_pad, dtype=torch.float32, device="cuda")
+    gs.saef.saef_topk_aggregate(gs.plan, K, mode, sel, rank, vals, gs.x, gs.e_srv if mode else None,
+                                gs.srv_sel if mode else None, gs.srv_rank if mode else None,
+                                gs.srv_vals if mode else None, avg=avg_d)
+    torch.cuda.synchronize()
+    H.assert_f32_equal(H.host(avg_d), avg, msk, "mean")
+    H.assert_f32_equal(H.host(gs.x), orc.x, msk, "weights")
+    if mode == 1:
+        wm = H.tensor_word_mask(off, n, d_pad)
+        H.assert_words_equal(H.host(gs.srv_sel, np.uint64), orc.srv_sel, wm, "server selection")
+        assert np.array_equal(_u32(gs.srv_rank)[wm], orc.srv_rank[wm])
+        H.assert_f32_equal(H.host(gs.srv_vals), orc.srv_vals,
+                           np.ones(orc.srv_vals.shape[-1], bool), "server values")
+        H.assert_f32_equal(H.host(gs.e_srv), orc.e_srv, msk, "server error")
+    assert gs.status() == 0
+
+
+ROUND_CASES = {
+    "resnet56_1pct_dc": (W.get("resnet56").with_(rounds=12, period=0), 1, None),
+    "resnet56_10pct_avg": (W.get("resnet56").with_(rounds=12, period=4), 10, None),
+    "resnet56_5pct_momentum": (W.get("resnet56").with_(rounds=8, period=0), 5, 0.9),
+    "ragged_sc_avg": (W.custom(ADVERSARIAL + [70001], K=3, period=3, rounds=7, mode=0,
+                               scale_range=(1e-4, 1e-1), dist="laplace_zeros", seed=998), 5, None),
+    "flat64k_1pct": (W.get("flat64k"), 1, None),
+}
+
+
+@pytest.mark.parametrize("name", list(ROUND_CASES))
+def test_topk_round_parity(name):
+    """saef_topk_round over every iteration against the oracle."""
+    w, pct, mu = ROUND_CASES[name]
+    keep = W.topk_keep(w, pct)
+    _case(f"topk round {name} K={w.K} L={w.L} rounds={w.rounds} pct={pct} mu={mu}")
+    orc = TopkOracle(w, keep, mu=mu)
+    gs = TopkGpu(w, keep, mu=mu)
+    for t in range(w.rounds):
+        g = W.gradients(w, t)
+        orc.round(t, g)
+        gs.round(t, g)
+        compare_topk(gs, orc, t, name, mode=w.mode)
+    assert gs.status() == 0
+
+
+def test_topk_invalid_and_range():
+    w = W.custom([100, 7], K=2)
+    from paper_2008_05823_amd import saef
+    lay = saef.Layout(*w.layout(), 2)
+    with pytest.raises(saef.SaefError):
+        saef.TopK(lay, [0, 1])           # keep must be >= 1
+    with pytest.raises(saef.SaefError):
+        saef.TopK(lay, [101, 1])         # and <= n
+    gs = TopkGpu(w, [3, 1])
+    with pytest.raises(saef.SaefError):  # mu without a momentum buffer
+        saef.saef_topk_compress(gs.plan, 2, 0.1, 0.9, gs.g, None, gs.e, gs.sel, gs.rank, gs.vals)
+    g = torch.zeros_like(gs.g)
+    g[1, 5] = float("inf")
+    saef.saef_topk_compress(gs.plan, 2, 0.1, 0.0, g, None, gs.e, gs.sel, gs.rank, gs.vals)
+    assert gs.status() == saef.ERANGE
+    assert gs.status() == saef.OK        # the flag clears
