@@ -59,9 +59,9 @@ def traffic_from_profile(workload: str):
         return None
 
 
-def cpu_baseline(w, grads_host, x0, rounds: int) -> dict:
+def cpu_baseline(w, grads_host, x0, rounds: int, keep=None) -> dict:
     """The CPU oracle (single thread) on the first `rounds` iterations of the
-    same workload and inputs."""
+    same workload and inputs (Top-K with kept counts `keep` when given)."""
     import numpy as np
     from oracle import oracle as O
     off, n, d_pad = w.layout()
@@ -75,19 +75,31 @@ def cpu_baseline(w, grads_host, x0, rounds: int) -> dict:
     scales = np.zeros((K, L), np.float32)
     ss = np.zeros(d_pad // 64, np.uint64)
     sscales = np.zeros(L, np.float32)
+    if keep is not None:
+        total_keep = int(np.sum(keep))
+        rank = np.zeros((K, d_pad // 64), np.uint32)
+        vals = np.zeros((K, total_keep), np.float32)
+        srank = np.zeros(d_pad // 64, np.uint32)
+        svals = np.zeros(total_keep, np.float32)
     total = 0.0
     for t in range(rounds):
         g = grads_host[t % len(grads_host)]
         t0 = time.perf_counter()
-        rc = orc.round(t, w.period, K, np.float32(w.lr), w.mode, g, e, e_srv, x, xh, signs,
-                       scales, ss, sscales)
+        if keep is not None:
+            rc = orc.topk_round(t, w.period, K, np.float32(w.lr), 0.0, w.mode, keep, g, None, e,
+                                e_srv, x, xh, signs, rank, vals, ss, srank, svals)
+        else:
+            rc = orc.round(t, w.period, K, np.float32(w.lr), w.mode, g, e, e_srv, x, xh, signs,
+                           scales, ss, sscales)
         total += time.perf_counter() - t0
         if rc != 0:
             raise RuntimeError(f"oracle returned {rc}")
     per_round = total / rounds
     return {"value": w.d / per_round, "unit": "params/s", "cores": 1, "kind": "oracle",
             "sample": f"{rounds} full iterations (t=0..{rounds - 1}) of the {w.name} workload, "
-                      f"K={K}, single-threaded C oracle, {per_round:.2f} s per iteration"}
+                      f"K={K}, single-threaded C oracle"
+                      + (" (Top-K)" if keep is not None else "")
+                      + f", {per_round:.2f} s per iteration"}
 
 
 def copy_probe_gbps(nbytes: int = 2 << 30) -> float:
@@ -125,6 +137,9 @@ def main() -> int:
     ap.add_argument("--variant", choices=("saef", "ef"), default="saef",
                     help="saef: step ahead (default); ef: local error feedback, the gradient "
                          "is taken at x_t (saef_round_begin / saef_round_end)")
+    ap.add_argument("--topk", type=float, default=None,
+                    help="layer-wise Top-K compressor keeping this percent of every tensor "
+                         "(saef_topk_round) instead of the scaled sign")
     ap.add_argument("--mismatch", action="store_true",
                     help="compute the gradient-mismatch bounds in every iteration")
     ap.add_argument("--kernel-events", choices=("on", "off"), default="on",
@@ -168,9 +183,26 @@ def main() -> int:
     variant = saef.VARIANT_EF if args.variant == "ef" else saef.VARIANT_SAEF
     mism = torch.zeros(2 * L, dtype=torch.float64, device="cuda") if args.mismatch else None
     xh_arg = xh if variant == saef.VARIANT_SAEF else xh[0]
+    topk = None
+    if args.topk is not None:
+        if split:
+            print("bench.py: --topk runs the SAEF iteration only", file=sys.stderr)
+            return 2
+        keep = W.topk_keep(w, args.topk)
+        topk = saef.TopK(layout, keep)
+        density = float(keep.sum()) / d
+        W_ = d_pad // 64
+        tk_rank = torch.zeros((K, W_), dtype=torch.int32, device="cuda")
+        tk_vals = torch.zeros((K, topk.total), **f32)
+        tk_srank = torch.zeros(W_, dtype=torch.int32, device="cuda")
+        tk_svals = torch.zeros(topk.total, **f32)
 
     def step(t):
-        if split:
+        if topk is not None:
+            saef.saef_topk_round(topk, t, w.period, K, w.lr, 0.0 if mu is None else mu, w.mode,
+                                 g_dev[t % n_grad], m, e, e_srv, x, xh, signs, tk_rank, tk_vals,
+                                 srv_signs, tk_srank, tk_svals)
+        elif split:
             saef.saef_round_begin(layout, t, w.period, K, w.mode, variant, e, e_srv, x, xh_arg,
                                   signs, scales, srv_signs, srv_scales, mism)
             saef.saef_round_end(layout, t, w.period, K, w.lr, 0.0 if mu is None else mu, w.mode,
@@ -207,17 +239,27 @@ def main() -> int:
 
     timed_ts = range(args.warmup, args.warmup + args.steps)
     n_avg = sum(1 for t in timed_ts if w.period and (t + 1) % w.period == 0)
-    bytes_round = np.mean([W.algorithmic_bytes_per_param(
-        K, w.mode, averaging=bool(w.period and (t + 1) % w.period == 0),
-        momentum=mu is not None, step_ahead=variant == saef.VARIANT_SAEF,
-        mismatch=args.mismatch) for t in timed_ts]) * d
+    if topk is not None:
+        bytes_round = np.mean([W.topk_algorithmic_bytes_per_param(
+            K, density, w.mode, averaging=bool(w.period and (t + 1) % w.period == 0))["round"]
+            + (8 * K if mu is not None else 0) for t in timed_ts]) * d
+    else:
+        bytes_round = np.mean([W.algorithmic_bytes_per_param(
+            K, w.mode, averaging=bool(w.period and (t + 1) % w.period == 0),
+            momentum=mu is not None, step_ahead=variant == saef.VARIANT_SAEF,
+            mismatch=args.mismatch) for t in timed_ts]) * d
 
     # dominant kernel: worker compression (12 K + K/8 bytes per parameter,
     # 20 K + K/8 with momentum)
     c_count, c_ms = prof["compress"]
-    c_bytes = ((20 if mu is not None else 12) * K + K / 8) * d
+    if topk is not None:
+        c_bytes = (W.topk_algorithmic_bytes_per_param(K, density, w.mode)["worker"]
+                   + (8 * K if mu is not None else 0)) * d
+    else:
+        c_bytes = ((20 if mu is not None else 12) * K + K / 8) * d
     c_gbps = c_bytes / (c_ms / c_count * 1e-3) / 1e9 if c_count else None
-    traffic = traffic_from_profile(args.workload) if (mu is None and not split) else None
+    traffic = (traffic_from_profile(args.workload)
+               if (mu is None and not split and topk is None) else None)
 
     # breakdown of every kernel, from a separate pass of the same length (each
     # timed dispatch costs a few microseconds, so it is kept out of the value)
@@ -250,12 +292,15 @@ def main() -> int:
                                f"double-way, lr={w.lr}, error averaging period {w.period}"
                                + (f", momentum {mu}" if mu is not None else "")
                                + (", local error feedback" if args.variant == "ef" else "")
-                               + (", mismatch bounds" if args.mismatch else ""),
+                               + (", mismatch bounds" if args.mismatch else "")
+                               + (f", layer-wise Top-{args.topk}%" if topk is not None
+                                  else ", scaled sign"),
                    "K": K, "d": d, "L": L, "period": w.period,
                    "mode": "DC" if w.mode == 1 else "SC",
                    **({"momentum": mu} if mu is not None else {}),
                    **({"variant": "ef"} if args.variant == "ef" else {}),
-                   **({"mismatch": True} if args.mismatch else {})},
+                   **({"mismatch": True} if args.mismatch else {}),
+                   **({"topk_percent": args.topk} if topk is not None else {})},
         "worker_params_per_s": K * d / (ms_per_step * 1e-3),
         "round_hbm_gbps": bytes_round / (ms_per_step * 1e-3) / 1e9,
         "round_frac_of_peak": bytes_round / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
@@ -263,13 +308,20 @@ def main() -> int:
         "kernels": kernels,
         "kernels_note": "per-kernel averages from a second pass with every dispatch timed",
         "copy_probe_gbps": probe,
-        "roofline": {"bound": "hbm", "kernel": "compress", "achieved": c_gbps,
+        "roofline": {"bound": "hbm",
+                     "kernel": "compress" if topk is None else "topk_compress (all passes)",
+                     "achieved": c_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": c_gbps / HBM_PEAK_GBPS if c_gbps else None,
                      "traffic": traffic, "algorithmic_bytes_per_launch": c_bytes},
     }
     if args.cpu_rounds > 0:
-        out["cpu_baseline"] = cpu_baseline(w, grads_host, x0, args.cpu_rounds)
+        if mu is not None or split:
+            out["cpu_baseline"] = None  # the oracle baseline covers the default iteration
+        else:
+            out["cpu_baseline"] = cpu_baseline(w, grads_host, x0, args.cpu_rounds,
+                                               keep=None if topk is None else W.topk_keep(
+                                                   w, args.topk))
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)

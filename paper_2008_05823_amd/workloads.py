@@ -272,6 +272,28 @@ def topk_keep(w: Workload, percent: float) -> np.ndarray:
     return np.maximum(k, 1).astype(np.int64)
 
 
+def topk_algorithmic_bytes_per_param(K: int, density: float, mode: int = 1,
+                                     averaging: bool = False) -> dict:
+    """Bytes the Top-K iteration itself moves per parameter (density = kept
+    fraction).  A message is the selection bit (1/8), the rank word share
+    (4 B per 64 elements: 1/16) and the kept values (4 density).
+
+    step ahead: read x and e[k], write xh[k]               4 + 8K
+    worker: read g[k], e[k]; write e[k]; write the message  (12 + 3/16 + 4 density) K
+    server, double-way: read the K messages, read/write e_srv, write the
+      server message, update x at the kept elements       K (3/16 + 4 density) + 8 + 3/16
+                                                           + 4 density + 8 density
+    server, single-way: read the K messages, read/write x  K (3/16 + 4 density) + 8
+    an error-averaging round also writes e[k] once more     + 4K
+    """
+    msg = 3 / 16 + 4 * density
+    step = 4 + 8 * K
+    worker = (12 + msg) * K
+    server = K * msg + (8 + msg + 8 * density if mode == 1 else 8)
+    return {"step": step, "worker": worker, "server": server,
+            "round": step + worker + server + (4 * K if averaging else 0)}
+
+
 def algorithmic_bytes_per_param(K: int, mode: int = 1, averaging: bool = False,
                                 momentum: bool = False, step_ahead: bool = True,
                                 mismatch: bool = False) -> float:
