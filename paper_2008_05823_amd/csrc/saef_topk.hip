@@ -28,8 +28,32 @@ namespace saef {
 namespace {
 
 constexpr uint32_t kFiniteLimit = 0x7F800000u;  // keys >= this are Inf or NaN
-constexpr int kTkU = 4;                         // words per wave per pass (streaming kernels)
-constexpr int kTieW = 4;                        // words per wave per step of the tie scan
+constexpr int kTkU = 4;                         // words per wave per pass (first pass, server)
+constexpr int kTkH = 8;                         // words per wave per pass (later passes)
+constexpr int kTkE = 16;                        // words per wave per pass (emit)
+constexpr int kBig = 1024;                      // threads of the single-row (server) kernels
+#ifndef SAEF_TK_HIST_THREADS
+#define SAEF_TK_HIST_THREADS 256
+#endif
+#ifndef SAEF_TK_NT
+#define SAEF_TK_NT 1
+#endif
+// Guarded loads without a branch: the load of p[ok ? j : 0] is always
+// issued (p[0] must exist) and its value replaced by 0 when !ok.  A branch
+// around each load makes the compiler wait for it before the next one.
+__device__ __forceinline__ float ld_nt_or0(const float* p, int64_t j, bool ok) {
+  const float v = __builtin_nontemporal_load(p + (ok ? j : 0));
+  return ok ? v : 0.0f;
+}
+__device__ __forceinline__ float ld_or0(const float* p, int64_t j, bool ok) {
+  const float v = p[ok ? j : 0];
+  return ok ? v : 0.0f;
+}
+// loads of the later passes (the error was just written by the first pass)
+__device__ __forceinline__ float ld_pass_or0(const float* p, int64_t j, bool ok) {
+  return SAEF_TK_NT ? ld_nt_or0(p, j, ok) : ld_or0(p, j, ok);
+}
+constexpr int kAggK = 4;                        // workers whose messages are read together
 
 __device__ __forceinline__ uint32_t key_of(float v) { return __float_as_uint(v) & 0x7FFFFFFFu; }
 
@@ -70,7 +94,7 @@ struct Digit<3> {
 
 template <int kBins>
 __device__ __forceinline__ void hist_clear(uint32_t* h) {
-  for (int i = threadIdx.x; i < kBins; i += kBlock) h[i] = 0;
+  for (int i = threadIdx.x; i < kBins; i += blockDim.x) h[i] = 0;
   __syncthreads();
 }
 
@@ -78,7 +102,7 @@ __device__ __forceinline__ void hist_clear(uint32_t* h) {
 template <int kBins>
 __device__ __forceinline__ void hist_store(const uint32_t* h, uint32_t* out) {
   __syncthreads();
-  for (int i = threadIdx.x; i < kBins; i += kBlock) out[i] = h[i];
+  for (int i = threadIdx.x; i < kBins; i += blockDim.x) out[i] = h[i];
 }
 
 __device__ __forceinline__ uint32_t* chunk_hist(const TkDev& tk, int row, int64_t ci) {
@@ -98,9 +122,9 @@ __device__ __forceinline__ void delta_words(int w0, int nw, int count, float lr,
   for (int u = 0; u < kTkU; ++u) {
     const int j = (w0 + u) * 64 + lane;
     const bool ok = kFull || ((w0 + u < nw) && j < count);
-    gv[u] = ok ? ld_nt(gk + j) : 0.0f;
-    ev[u] = ok ? ld_nt(ek + j) : 0.0f;
-    mv[u] = (kMom && ok) ? ld_nt(mk + j) : 0.0f;
+    gv[u] = ld_nt_or0(gk, j, ok);
+    ev[u] = ld_nt_or0(ek, j, ok);
+    mv[u] = kMom ? ld_nt_or0(mk, j, ok) : 0.0f;
   }
 #pragma unroll
   for (int u = 0; u < kTkU; ++u) {
@@ -148,11 +172,13 @@ __global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, in
 }
 
 // ------------------------------------------------------------------ passes 2 and 3
-// Grid: n_chunks * R workgroups (R rows from row0; data row r at data + r d_pad).
-template <int kPass>
-__global__ __launch_bounds__(kBlock) void k_tk_hist(DevLayout lay, TkDev tk, int R, int row0,
-                                                    const float* __restrict__ data) {
+// Grid: n_chunks * R workgroups of kThreads (R rows from row0; data row r at
+// data + r d_pad).
+template <int kPass, int kThreads>
+__global__ __launch_bounds__(kThreads) void k_tk_hist(DevLayout lay, TkDev tk, int R, int row0,
+                                                      const float* __restrict__ data) {
   constexpr int B = Digit<kPass>::kBins;
+  constexpr int kW = kThreads / kWave;
   __shared__ uint32_t h[B];
   const int r = (int)(blockIdx.x % (unsigned)R);
   const int64_t ci = blockIdx.x / (unsigned)R;
@@ -162,15 +188,15 @@ __global__ __launch_bounds__(kBlock) void k_tk_hist(DevLayout lay, TkDev tk, int
   const float* dr = data + (int64_t)r * lay.d_pad + c.start;
   const int lane = lane_id();
   const int nw = (c.count + 63) >> 6;
-  for (int w0 = wave_id() * kTkU; w0 < nw; w0 += kWaves * kTkU) {
-    float v[kTkU];
+  for (int w0 = wave_id() * kTkH; w0 < nw; w0 += kW * kTkH) {
+    float v[kTkH];
 #pragma unroll
-    for (int u = 0; u < kTkU; ++u) {
+    for (int u = 0; u < kTkH; ++u) {
       const int j = (w0 + u) * 64 + lane;
-      v[u] = (w0 + u < nw && j < c.count) ? ld_nt(dr + j) : 0.0f;
+      v[u] = ld_pass_or0(dr, j, w0 + u < nw && j < c.count);
     }
 #pragma unroll
-    for (int u = 0; u < kTkU; ++u) {
+    for (int u = 0; u < kTkH; ++u) {
       const int j = (w0 + u) * 64 + lane;
       const uint32_t key = key_of(v[u]);
       if (w0 + u < nw && j < c.count && Digit<kPass>::match(key, prefix))
@@ -289,13 +315,16 @@ __global__ __launch_bounds__(kBlock) void k_tk_pick(DevLayout lay, TkDev tk, int
 }
 
 // ------------------------------------------------------------------ ties
-// Grid: R * L workgroups.  When only part of the elements equal to tau are
-// kept, scans the chunk of the cut in index order for the cut_rank-th of
-// them; its index (absolute element index) becomes iota.
-__global__ __launch_bounds__(kBlock) void k_tk_ties(DevLayout lay, TkDev tk, int row0,
-                                                    const float* __restrict__ data) {
-  __shared__ uint32_t s_cnt[kWaves];
-  __shared__ int s_done;
+// Grid: R * L workgroups of kBig threads.  When only part of the elements
+// equal to tau are kept, finds the cut_rank-th of them in index order in the
+// chunk of the cut; its absolute element index becomes iota.  Each wave
+// counts the ties of its own contiguous slice of the chunk, a prefix over
+// the waves names the slice of the cut, and that wave scans its slice again
+// (from the caches) to place it.
+__global__ __launch_bounds__(kBig) void k_tk_ties(DevLayout lay, TkDev tk, int row0,
+                                                  const float* __restrict__ data) {
+  constexpr int kW = kBig / kWave;
+  __shared__ uint32_t s_cnt[kW];
   const int l = (int)(blockIdx.x % lay.L);
   const int r = (int)(blockIdx.x / lay.L);
   TkSel* st = tk.sel + (int64_t)(row0 + r) * lay.L + l;
@@ -308,46 +337,46 @@ __global__ __launch_bounds__(kBlock) void k_tk_ties(DevLayout lay, TkDev tk, int
   const int lane = lane_id();
   const int wave = wave_id();
   const int nw = (c.count + 63) >> 6;
-  if (threadIdx.x == 0) s_done = 0;
-  int64_t seen = 0;  // ties before the current step
-  for (int base = 0; base < nw; base += kWaves * kTieW) {
-    u64 m[kTieW];
-    uint32_t mine = 0;
+  const int per = (nw + kW - 1) / kW;  // words of each wave's slice
+  const int w_lo = min(nw, wave * per), w_hi = min(nw, w_lo + per);
+  uint32_t mine = 0;
+  for (int w0 = w_lo; w0 < w_hi; w0 += kTkE) {
+    float v[kTkE];
 #pragma unroll
-    for (int u = 0; u < kTieW; ++u) {
-      const int w = base + wave * kTieW + u;
-      const int j = w * 64 + lane;
-      const bool ok = w < nw && j < c.count;
-      const float v = ok ? ld_nt(dr + j) : 0.0f;
-      m[u] = __ballot(ok && key_of(v) == tau);
-      mine += (uint32_t)__popcll(m[u]);
+    for (int u = 0; u < kTkE; ++u) {
+      const int j = (w0 + u) * 64 + lane;
+      v[u] = ld_nt_or0(dr, j, w0 + u < w_hi && j < c.count);
     }
-    if (lane == 0) s_cnt[wave] = mine;
-    __syncthreads();
-    int64_t before = seen;
-    int64_t step = 0;
-    for (int i = 0; i < kWaves; ++i) {
-      if (i < wave) before += s_cnt[i];
-      step += s_cnt[i];
-    }
-    if (before < target && target <= before + mine) {
 #pragma unroll
-      for (int u = 0; u < kTieW; ++u) {
-        const int n = (int)__popcll(m[u]);
-        if (before < target && target <= before + n) {
-          const int b = nth_set_bit(m[u], (int)(target - before));
-          if (lane == 0) {
-            st->iota = c.start + (int64_t)(base + wave * kTieW + u) * 64 + b;
-            s_done = 1;
-          }
-        }
-        before += n;
+    for (int u = 0; u < kTkE; ++u) {
+      const int j = (w0 + u) * 64 + lane;
+      mine += (uint32_t)__popcll(__ballot(w0 + u < w_hi && j < c.count && key_of(v[u]) == tau));
+    }
+  }
+  if (lane == 0) s_cnt[wave] = mine;
+  __syncthreads();
+  int64_t before = 0;
+  for (int i = 0; i < wave; ++i) before += s_cnt[i];
+  if (!(before < target && target <= before + mine)) return;
+  // this wave's slice holds the cut
+  for (int w0 = w_lo; w0 < w_hi; w0 += kTkE) {
+    float v[kTkE];
+#pragma unroll
+    for (int u = 0; u < kTkE; ++u) {
+      const int j = (w0 + u) * 64 + lane;
+      v[u] = ld_or0(dr, j, w0 + u < w_hi && j < c.count);
+    }
+#pragma unroll
+    for (int u = 0; u < kTkE; ++u) {
+      const int j = (w0 + u) * 64 + lane;
+      const u64 m = __ballot(w0 + u < w_hi && j < c.count && key_of(v[u]) == tau);
+      const int n = (int)__popcll(m);
+      if (before < target && target <= before + n) {
+        const int b = nth_set_bit(m, (int)(target - before));
+        if (lane == 0) st->iota = c.start + (int64_t)(w0 + u) * 64 + b;
       }
+      before += n;
     }
-    seen += step;
-    __syncthreads();
-    if (s_done) return;
-    __syncthreads();
   }
 }
 
@@ -370,15 +399,15 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit1(DevLayout lay, TkDev tk, in
   const float* dr = data + (int64_t)r * lay.d_pad + tile.start;
   uint64_t* sr = sel + (int64_t)r * (lay.d_pad >> 6) + (tile.start >> 6);
   uint32_t cnt = 0;
-  for (int w0 = 0; w0 < nw; w0 += 2 * kTkU) {
-    float v[2 * kTkU];
+  for (int w0 = 0; w0 < nw; w0 += kTkE) {
+    float v[kTkE];
 #pragma unroll
-    for (int u = 0; u < 2 * kTkU; ++u) {
+    for (int u = 0; u < kTkE; ++u) {
       const int j = (w0 + u) * 64 + lane;
-      v[u] = (w0 + u < nw && j < tile.count) ? ld_nt(dr + j) : 0.0f;
+      v[u] = ld_pass_or0(dr, j, w0 + u < nw && j < tile.count);
     }
 #pragma unroll
-    for (int u = 0; u < 2 * kTkU; ++u) {
+    for (int u = 0; u < kTkE; ++u) {
       const int w = w0 + u;
       if (w >= nw) continue;
       const int j = w * 64 + lane;
@@ -447,24 +476,38 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit2(DevLayout lay, TkDev tk, in
   float* xt = kX ? x + tile.start : nullptr;
   uint32_t run = tk.tile_cnt[(int64_t)(row0 + r) * lay.n_tiles + ti];
   const u64 lt = lanemask_lt(lane);
-  for (int w0 = 0; w0 < nw; w0 += 2 * kTkU) {
-    u64 m[2 * kTkU];
+  for (int w0 = 0; w0 < nw; w0 += kTkE) {
+    u64 m[kTkE];
 #pragma unroll
-    for (int u = 0; u < 2 * kTkU; ++u) m[u] = (w0 + u < nw) ? sr[w0 + u] : 0ull;
+    for (int u = 0; u < kTkE; ++u) {
+      const u64 word = sr[min(w0 + u, nw - 1)];  // always in the tile; masked below
+      m[u] = (w0 + u < nw) ? word : 0ull;
+    }
+    // all loads of the kept elements first, then the stores
+    float v[kTkE];
+    uint32_t pos[kTkE];
+    bool kept[kTkE];
 #pragma unroll
-    for (int u = 0; u < 2 * kTkU; ++u) {
+    for (int u = 0; u < kTkE; ++u) {
+      pos[u] = run + (uint32_t)__popcll(m[u] & lt);
+      kept[u] = ((m[u] >> lane) & 1ull) && pos[u] < (uint32_t)t.keep;  // pos < keep always holds
+      v[u] = ld_or0(dr, (w0 + u) * 64 + lane, kept[u]);
+      run += (uint32_t)__popcll(m[u]);
+    }
+    float xv[kTkE];
+#pragma unroll
+    for (int u = 0; u < kTkE; ++u) xv[u] = kX ? ld_or0(xt, (w0 + u) * 64 + lane, kept[u]) : 0.0f;
+#pragma unroll
+    for (int u = 0; u < kTkE; ++u) {
       const int w = w0 + u;
       if (w >= nw) continue;
-      if (lane == 0) rr[w] = run;
-      const uint32_t pos = run + (uint32_t)__popcll(m[u] & lt);
-      if (((m[u] >> lane) & 1ull) && pos < (uint32_t)t.keep) {  // pos < keep always holds
+      if (lane == 0) rr[w] = pos[u];  // lane 0: the kept count before this word
+      if (kept[u]) {
         const int j = w * 64 + lane;
-        const float v = dr[j];
-        vr[pos] = v;
+        vr[pos[u]] = v[u];
         dr[j] = 0.0f;  // e = Delta - C(Delta) = 0 at a kept element
-        if (kX) xt[j] = xt[j] - v;
+        if (kX) xt[j] = xv[u] - v[u];
       }
-      run += (uint32_t)__popcll(m[u]);
     }
   }
 }
@@ -489,31 +532,45 @@ __device__ __forceinline__ void tk_aggregate_words(
   for (int u = 0; u < kTkU; ++u) {
     const int j = (w0 + u) * 64 + lane;
     const bool ok = kFull || ((w0 + u < nw) && j < count);
-    dv[u] = ok ? ld_nt((kMode == 1 ? es : x) + start + j) : 0.0f;
+    dv[u] = ld_nt_or0((kMode == 1 ? es : x) + start, j, ok);
   }
   double acc[kTkU];
 #pragma unroll
   for (int u = 0; u < kTkU; ++u) acc[u] = 0.0;
-  for (int k = 0; k < K; ++k) {
-    const uint64_t* sk = sel + (int64_t)k * W + gw0;
-    const uint32_t* rk = rank + (int64_t)k * W + gw0;
-    const float* vk = vals + (int64_t)k * tk.total_keep + voff;
-    u64 m[kTkU];
-    uint32_t rb[kTkU];
+  for (int k0 = 0; k0 < K; k0 += kAggK) {
+    // the words and ranks of kAggK workers, then all their value gathers
+    u64 m[kAggK][kTkU];
+    uint32_t rb[kAggK][kTkU];
 #pragma unroll
-    for (int u = 0; u < kTkU; ++u) {
-      const bool w_ok = kFull || w0 + u < nw;
-      m[u] = w_ok ? sk[u] : 0ull;
-      rb[u] = w_ok ? rk[u] : 0u;
+    for (int c = 0; c < kAggK; ++c) {
+      const bool kin = k0 + c < K;
+      const int64_t row = kin ? (int64_t)(k0 + c) * W : 0;  // absent workers read worker 0
+#pragma unroll
+      for (int u = 0; u < kTkU; ++u) {
+        const bool w_ok = kin && (kFull || w0 + u < nw);
+        // always issued at a word of the chunk that exists, masked after
+        const int64_t at = gw0 + row + ((kFull || w0 + u < nw) ? u : 0);
+        const u64 mw = sel[at];
+        const uint32_t rw = rank[at];
+        m[c][u] = w_ok ? mw : 0ull;
+        rb[c][u] = w_ok ? rw : 0u;
+      }
     }
-    float c[kTkU];
+    float cv[kAggK][kTkU];
 #pragma unroll
-    for (int u = 0; u < kTkU; ++u) {
-      const uint32_t pos = rb[u] + (uint32_t)__popcll(m[u] & lt);
-      c[u] = (((m[u] >> lane) & 1ull) && pos < keep) ? vk[pos] : 0.0f;
+    for (int c = 0; c < kAggK; ++c) {
+      const int kk = (k0 + c < K) ? k0 + c : 0;
+      const float* vk = vals + (int64_t)kk * tk.total_keep + voff;
+#pragma unroll
+      for (int u = 0; u < kTkU; ++u) {
+        const uint32_t pos = rb[c][u] + (uint32_t)__popcll(m[c][u] & lt);
+        cv[c][u] = ld_or0(vk, pos, ((m[c][u] >> lane) & 1ull) && pos < keep);
+      }
     }
 #pragma unroll
-    for (int u = 0; u < kTkU; ++u) acc[u] += (double)c[u];
+    for (int c = 0; c < kAggK; ++c)
+#pragma unroll
+      for (int u = 0; u < kTkU; ++u) acc[u] += (double)cv[c][u];  // worker order; absent: +0
   }
 #pragma unroll
   for (int u = 0; u < kTkU; ++u) {
@@ -536,7 +593,7 @@ __device__ __forceinline__ void tk_aggregate_words(
 
 // Grid: n_chunks workgroups.
 template <int kMode, bool kAvg>
-__global__ __launch_bounds__(kBlock) void k_tk_aggregate(DevLayout lay, TkDev tk, int K,
+__global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, int K,
                                                          double inv_k,
                                                          const uint64_t* __restrict__ sel,
                                                          const uint32_t* __restrict__ rank,
@@ -552,7 +609,7 @@ __global__ __launch_bounds__(kBlock) void k_tk_aggregate(DevLayout lay, TkDev tk
   if (kMode == 1) hist_clear<kTkBins>(h);
   const int nw = (c.count + 63) >> 6;
   bool bad = false;
-  for (int w0 = wave_id() * kTkU; w0 < nw; w0 += kWaves * kTkU) {
+  for (int w0 = wave_id() * kTkU; w0 < nw; w0 += (kBig / kWave) * kTkU) {
     if ((w0 + kTkU) * 64 <= c.count)
       tk_aggregate_words<kMode, kAvg, true>(lay, tk, K, inv_k, voff, keep, c.start, w0, nw, c.count,
                                             sel, rank, vals, avg, es, x, h, bad);
@@ -586,21 +643,31 @@ struct Launcher {
     return hipGetLastError();
   }
 
+  // one histogram pass over R rows: 256-thread workgroups when there are
+  // several rows, 1024-thread ones for a single row (the server)
+  template <int kPass>
+  hipError_t hist(int R, int row0, const float* data) const {
+    const LaunchEvents ev;
+    const dim3 grid((unsigned)(tk.n_chunks * R));
+    if (R > 1)
+      SAEF_LAUNCH((k_tk_hist<kPass, SAEF_TK_HIST_THREADS>), grid, dim3(SAEF_TK_HIST_THREADS), 0, s,
+                  lay, tk, R, row0, data);
+    else
+      SAEF_LAUNCH((k_tk_hist<kPass, kBig>), grid, dim3(kBig), 0, s, lay, tk, R, row0, data);
+    return hipGetLastError();
+  }
+
   // passes 2 and 3, ties, emit of R rows of `data` (pass 1 already done)
   hipError_t select_and_emit(int R, int row0, float* data, uint64_t* sel, uint32_t* rank,
                              float* vals, float* x, const LaunchEvents& last) const {
     const LaunchEvents ev;
     hipError_t err = reduce_pick<1>(R, row0);
     if (err != hipSuccess) return err;
-    SAEF_LAUNCH((k_tk_hist<2>), dim3((unsigned)(tk.n_chunks * R)), dim3(kBlock), 0, s, lay, tk, R,
-                row0, data);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
+    if ((err = hist<2>(R, row0, data)) != hipSuccess) return err;
     if ((err = reduce_pick<2>(R, row0)) != hipSuccess) return err;
-    SAEF_LAUNCH((k_tk_hist<3>), dim3((unsigned)(tk.n_chunks * R)), dim3(kBlock), 0, s, lay, tk, R,
-                row0, data);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
+    if ((err = hist<3>(R, row0, data)) != hipSuccess) return err;
     if ((err = reduce_pick<3>(R, row0)) != hipSuccess) return err;
-    SAEF_LAUNCH(k_tk_ties, dim3((unsigned)(R * lay.L)), dim3(kBlock), 0, s, lay, tk, row0, data);
+    SAEF_LAUNCH(k_tk_ties, dim3((unsigned)(R * lay.L)), dim3(kBig), 0, s, lay, tk, row0, data);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     const dim3 tiles((unsigned)(per_wave_grid(lay) * R));
     SAEF_LAUNCH(k_tk_emit1, tiles, dim3(kBlock), 0, s, lay, tk, R, row0, data, sel);
@@ -646,7 +713,7 @@ hipError_t launch_topk_aggregate(const DevLayout& lay, const TkDev& tk, int K, i
   const double ik = inv_pow2(K);
   hipEvent_t stop0 = mode == 1 ? nullptr : ev.stop;
 #define SAEF_TKA(M, A)                                                                          \
-  hipExtLaunchKernelGGL((k_tk_aggregate<M, A>), grid, dim3(kBlock), 0, s, ev.start, stop0, 0, \
+  hipExtLaunchKernelGGL((k_tk_aggregate<M, A>), grid, dim3(kBig), 0, s, ev.start, stop0, 0, \
                         lay, tk, K, ik, sel, rank, vals, avg, e_srv, x)
   if (mode == 1) {
     if (avg != nullptr) SAEF_TKA(1, true); else SAEF_TKA(1, false);
