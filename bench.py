@@ -28,7 +28,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0      # MI355X HBM3E
 METRIC = "params/s per K-worker SAEF round + achieved HBM GB/s vs MI355X peak"
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2008_05823_amd", "csrc", f)
-                  for f in ("saef_kernels.hip", "saef_internal.h")]
+                  for f in ("saef_kernels.hip", "saef_internal.h", "saef_device.h")]
 
 
 def kernel_hash() -> str:
