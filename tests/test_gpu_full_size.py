@@ -179,3 +179,64 @@ def test_full_size_flat256m():
             del p, pf, bits
         _log(f"iteration {t} satisfies the size-independent checks")
     assert gs.status() == 0
+
+
+def test_full_size_topk_resnet50():
+    """Layer-wise Top-1% at the full ResNet-50 shape, K = 8, in the launch
+    configuration bench.py --topk 1 times: saef_topk_round over the whole
+    tensor list; the oracle runs the sampled tensors (the largest included)
+    with the same gradient slices, bit for bit, for 4 iterations (averaging
+    period 2 so that an averaging iteration is covered)."""
+    from tests.test_gpu_topk import TopkGpu, TopkOracle, _u32
+    w = W.get("resnet50").with_(period=2)
+    names = [t for t, _ in w.tensors]
+    idx = [names.index(s) for s in SAMPLES["resnet50"][2]]
+    off, n, d_pad = w.layout()
+    sw = _sub_workload(w, idx)
+    s_off, s_n, s_dpad = sw.layout()
+    keep = W.topk_keep(w, 1)
+    rounds = 4
+    _log(f"topk resnet50: K={w.K} L={w.L} d={w.d}, {rounds} iterations, oracle on {len(idx)} "
+         f"tensors ({int(s_n.sum())} elements)")
+    grads = [W.gradients(w, s) for s in range(2)]
+    x0 = W.initial_x(w)
+    orc = TopkOracle(sw, keep[idx], x0=_gather(x0, off, n, idx, s_off, s_dpad))
+    gs = TopkGpu(w, keep, x0=x0)
+    g_dev = [torch.from_numpy(g).cuda() for g in grads]
+    voff = np.concatenate([[0], np.cumsum(keep)[:-1]])
+    for t in range(rounds):
+        orc.round(t, _gather(grads[t % 2], off, n, idx, s_off, s_dpad))
+        gs.round(t, g_dev[t % 2])
+        torch.cuda.synchronize()
+
+        def pack(dev_t):
+            parts = _device_slices(dev_t, off, n, idx)
+            out = np.zeros(dev_t.shape[:-1] + (s_dpad,), np.float32)
+            for j, p in enumerate(parts):
+                out[..., s_off[j]:s_off[j] + s_n[j]] = p
+            return out
+        m = W.tensor_mask(sw)
+        wm = H.tensor_word_mask(s_off, s_n, s_dpad)
+        tag = f"topk resnet50 t={t}"
+        for key in ("e", "xh"):
+            H.assert_f32_equal(pack(getattr(gs, key)), getattr(orc, key), m, f"{tag} {key}")
+        H.assert_f32_equal(pack(gs.x), orc.x, m, f"{tag} weights")
+        H.assert_f32_equal(pack(gs.e_srv), orc.e_srv, m, f"{tag} server error")
+        sel = _gather_words(H.host(gs.sel, np.uint64), off, n, idx, s_off, s_dpad // 64)
+        H.assert_words_equal(sel, orc.sel, wm, f"{tag} worker selection")
+        rank = _gather_words(_u32(gs.rank), off, n, idx, s_off, s_dpad // 64)
+        assert np.array_equal(rank[:, wm], orc.rank[:, wm]), f"{tag} worker rank words"
+        ssel = _gather_words(H.host(gs.srv_sel, np.uint64), off, n, idx, s_off, s_dpad // 64)
+        H.assert_words_equal(ssel, orc.srv_sel, wm, f"{tag} server selection")
+        vals = H.host(gs.vals)
+        svals = H.host(gs.srv_vals)
+        o_voff = np.concatenate([[0], np.cumsum(keep[idx])[:-1]])
+        for j, i in enumerate(idx):
+            kl = int(keep[i])
+            got = vals[:, voff[i]:voff[i] + kl]
+            H.assert_f32_equal(got, orc.vals[:, o_voff[j]:o_voff[j] + kl], np.ones(kl, bool),
+                               f"{tag} worker values of {names[i]}")
+            H.assert_f32_equal(svals[voff[i]:voff[i] + kl], orc.srv_vals[o_voff[j]:o_voff[j] + kl],
+                               np.ones(kl, bool), f"{tag} server values of {names[i]}")
+        _log(f"topk resnet50: iteration {t} matches the oracle on the sampled tensors")
+    assert gs.status() == 0
