@@ -185,9 +185,6 @@ def main() -> int:
     xh_arg = xh if variant == saef.VARIANT_SAEF else xh[0]
     topk = None
     if args.topk is not None:
-        if split:
-            print("bench.py: --topk runs the SAEF iteration only", file=sys.stderr)
-            return 2
         keep = W.topk_keep(w, args.topk)
         topk = saef.TopK(layout, keep)
         density = float(keep.sum()) / d
@@ -198,7 +195,13 @@ def main() -> int:
         tk_svals = torch.zeros(topk.total, **f32)
 
     def step(t):
-        if topk is not None:
+        if topk is not None and split:
+            saef.saef_topk_round_begin(topk, t, w.period, K, w.mode, variant, e, e_srv, x, xh_arg,
+                                       mism)
+            saef.saef_topk_round_end(topk, K, w.lr, 0.0 if mu is None else mu, w.mode,
+                                     g_dev[t % n_grad], m, e, e_srv, x, signs, tk_rank, tk_vals,
+                                     srv_signs, tk_srank, tk_svals)
+        elif topk is not None:
             saef.saef_topk_round(topk, t, w.period, K, w.lr, 0.0 if mu is None else mu, w.mode,
                                  g_dev[t % n_grad], m, e, e_srv, x, xh, signs, tk_rank, tk_vals,
                                  srv_signs, tk_srank, tk_svals)
@@ -240,9 +243,13 @@ def main() -> int:
     timed_ts = range(args.warmup, args.warmup + args.steps)
     n_avg = sum(1 for t in timed_ts if w.period and (t + 1) % w.period == 0)
     if topk is not None:
+        step_ahead = variant == saef.VARIANT_SAEF
         bytes_round = np.mean([W.topk_algorithmic_bytes_per_param(
             K, density, w.mode, averaging=bool(w.period and (t + 1) % w.period == 0))["round"]
-            + (8 * K if mu is not None else 0) for t in timed_ts]) * d
+            + (8 * K if mu is not None else 0)
+            - (0 if step_ahead else (4 + 8 * K) - 8)
+            + ((4 * K + (4 if w.mode == 1 else 0)) if args.mismatch else 0)
+            for t in timed_ts]) * d
     else:
         bytes_round = np.mean([W.algorithmic_bytes_per_param(
             K, w.mode, averaging=bool(w.period and (t + 1) % w.period == 0),

@@ -246,10 +246,22 @@ int saef_topk_aggregate(const saef_topk* plan, int32_t K, int32_t mode, const ui
                         uint64_t* srv_sel, uint32_t* srv_rank, float* srv_vals, float* x,
                         hipStream_t stream);
 
-/* One iteration t of Algorithm 1 (SAEF branch) with Top-K: error averaging
- * when (t+1) mod period == 0 (period 0 = never), step ahead xh[k] = x -
- * e[k], [gradient g computed at xh by the caller], saef_topk_compress (m
- * may be NULL, then mu must be 0), saef_topk_aggregate. */
+/* One iteration t of Algorithm 1 with Top-K, in two halves around the
+ * gradient (the state is plain, so t only decides the averaging):
+ * saef_topk_round_begin: error averaging when (t+1) mod period == 0 (period
+ * 0 = never), then the evaluation point: SAEF_VARIANT_SAEF xh[k] = x - e[k]
+ * ((K, d_pad)), SAEF_VARIANT_EF xh = x ((d_pad)); mismatch (may be NULL):
+ * the 2 L bounds of saef_round_begin from the state after averaging.
+ * saef_topk_round_end: saef_topk_compress (m may be NULL, then mu must be
+ * 0) and saef_topk_aggregate with the gradient g the caller computed at xh.
+ * saef_topk_round is begin (SAEF) + end. */
+int saef_topk_round_begin(const saef_topk* plan, int64_t t, int64_t period, int32_t K,
+                          int32_t mode, int32_t variant, float* e, const float* e_srv,
+                          const float* x, float* xh, double* mismatch, hipStream_t stream);
+int saef_topk_round_end(const saef_topk* plan, int32_t K, float lr, float mu, int32_t mode,
+                        const float* g, float* m, float* e, float* e_srv, float* x, uint64_t* sel,
+                        uint32_t* rank, float* vals, uint64_t* srv_sel, uint32_t* srv_rank,
+                        float* srv_vals, hipStream_t stream);
 int saef_topk_round(const saef_topk* plan, int64_t t, int64_t period, int32_t K, float lr,
                     float mu, int32_t mode, const float* g, float* m, float* e, float* e_srv,
                     float* x, float* xh, uint64_t* sel, uint32_t* rank, float* vals,

@@ -710,6 +710,72 @@ int saef_topk_aggregate(const saef_topk* plan, int32_t K, int32_t mode, const ui
   }));
 }
 
+int saef_topk_round_begin(const saef_topk* plan, int64_t t, int64_t period, int32_t K,
+                          int32_t mode, int32_t variant, float* e, const float* e_srv,
+                          const float* x, float* xh, double* mismatch, hipStream_t stream) {
+  if (plan == nullptr) return SAEF_EINVAL;
+  const saef_layout* layout = plan->layout;
+  int rc = check_common(layout, K);
+  if (rc != SAEF_OK) return rc;
+  if (t < 0 || period < 0) return SAEF_EINVAL;
+  if (mode != SAEF_MODE_SC && mode != SAEF_MODE_DC) return SAEF_EINVAL;
+  if (variant != SAEF_VARIANT_EF && variant != SAEF_VARIANT_SAEF) return SAEF_EINVAL;
+  if (!f32_ok(e) || !f32_ok(x) || !f32_ok(xh)) return SAEF_EINVAL;
+  if (mismatch != nullptr && (!aligned(mismatch, 8) || (mode == SAEF_MODE_DC && !f32_ok(e_srv))))
+    return SAEF_EINVAL;
+  const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
+  const size_t xb = layout->d_pad * sizeof(float);
+  const size_t hb = variant == SAEF_VARIANT_SAEF ? vb : xb;
+  if (overlap(xh, hb, x, xb) || overlap(xh, hb, e, vb) || overlap(e, vb, x, xb) ||
+      (e_srv != nullptr && overlap(xh, hb, e_srv, xb)))
+    return SAEF_EINVAL;
+  if (mismatch != nullptr) {
+    const size_t mb = 2 * (size_t)layout->L * sizeof(double);
+    if (overlap(mismatch, mb, e, vb) || overlap(mismatch, mb, xh, hb) ||
+        overlap(mismatch, mb, x, xb) || (e_srv != nullptr && overlap(mismatch, mb, e_srv, xb)))
+      return SAEF_EINVAL;
+  }
+  // the Top-K state is always plain: nothing to decode
+  const bool averaging = period > 0 && (t + 1) % period == 0;
+  const DevLayout& d = layout->dev;
+  if (variant == SAEF_VARIANT_SAEF || averaging) {
+    float* h = variant == SAEF_VARIANT_SAEF ? xh : nullptr;
+    rc = hip_rc(timed(layout, averaging ? 5 : 0, [&](const saef::LaunchEvents& ev) {
+      return saef::launch_step_ahead(d, K, x, nullptr, nullptr, false, e, nullptr, nullptr, false,
+                                     averaging, h, stream, ev);
+    }));
+    if (rc != SAEF_OK) return rc;
+  }
+  if (mismatch != nullptr) {
+    rc = hip_rc(timed(layout, 6, [&](const saef::LaunchEvents& ev) {
+      return saef::launch_mismatch(d, K, mode, e, nullptr, nullptr, false, e_srv, nullptr,
+                                   nullptr, false, mismatch, stream, ev);
+    }));
+    if (rc != SAEF_OK) return rc;
+  }
+  if (variant == SAEF_VARIANT_SAEF) return SAEF_OK;
+  return hip_rc(timed(layout, 0, [&](const saef::LaunchEvents& ev) {
+    return saef::launch_weights(d, x, nullptr, nullptr, false, xh, stream, ev);
+  }));
+}
+
+int saef_topk_round_end(const saef_topk* plan, int32_t K, float lr, float mu, int32_t mode,
+                        const float* g, float* m, float* e, float* e_srv, float* x, uint64_t* sel,
+                        uint32_t* rank, float* vals, uint64_t* srv_sel, uint32_t* srv_rank,
+                        float* srv_vals, hipStream_t stream) {
+  if (plan == nullptr) return SAEF_EINVAL;
+  const saef_layout* layout = plan->layout;
+  const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
+  const size_t xb = layout->d_pad * sizeof(float);
+  if (g != nullptr && x != nullptr && e != nullptr &&
+      (overlap(g, vb, x, xb) || overlap(e, vb, x, xb)))
+    return SAEF_EINVAL;
+  int rc = saef_topk_compress(plan, K, lr, mu, g, m, e, sel, rank, vals, stream);
+  if (rc != SAEF_OK) return rc;
+  return saef_topk_aggregate(plan, K, mode, sel, rank, vals, nullptr, e_srv, srv_sel, srv_rank,
+                             srv_vals, x, stream);
+}
+
 int saef_topk_round(const saef_topk* plan, int64_t t, int64_t period, int32_t K, float lr,
                     float mu, int32_t mode, const float* g, float* m, float* e, float* e_srv,
                     float* x, float* xh, uint64_t* sel, uint32_t* rank, float* vals,
@@ -718,25 +784,15 @@ int saef_topk_round(const saef_topk* plan, int64_t t, int64_t period, int32_t K,
   const saef_layout* layout = plan->layout;
   int rc = check_common(layout, K);
   if (rc != SAEF_OK) return rc;
-  if (t < 0 || period < 0) return SAEF_EINVAL;
-  if (!f32_ok(x) || !f32_ok(xh) || !f32_ok(e)) return SAEF_EINVAL;
+  if (!f32_ok(xh) || !f32_ok(g)) return SAEF_EINVAL;
   const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
-  const size_t xb = layout->d_pad * sizeof(float);
-  if (overlap(xh, vb, x, xb) || overlap(xh, vb, e, vb) || overlap(e, vb, x, xb) ||
-      (g != nullptr && overlap(xh, vb, g, vb)))
-    return SAEF_EINVAL;
-  // the Top-K state is always plain: step ahead (after averaging when due)
-  const bool averaging = period > 0 && (t + 1) % period == 0;
-  rc = hip_rc(timed(layout, averaging ? 5 : 0, [&](const saef::LaunchEvents& ev) {
-    return saef::launch_step_ahead(layout->dev, K, x, nullptr, nullptr, false, e, nullptr,
-                                   nullptr, false, averaging, xh, stream, ev);
-  }));
+  if (overlap(xh, vb, g, vb)) return SAEF_EINVAL;
+  rc = saef_topk_round_begin(plan, t, period, K, mode, SAEF_VARIANT_SAEF, e, e_srv, x, xh,
+                             nullptr, stream);
   if (rc != SAEF_OK) return rc;
   // [gradient slot: g was computed by the caller at xh]
-  rc = saef_topk_compress(plan, K, lr, mu, g, m, e, sel, rank, vals, stream);
-  if (rc != SAEF_OK) return rc;
-  return saef_topk_aggregate(plan, K, mode, sel, rank, vals, nullptr, e_srv, srv_sel, srv_rank,
-                             srv_vals, x, stream);
+  return saef_topk_round_end(plan, K, lr, mu, mode, g, m, e, e_srv, x, sel, rank, vals, srv_sel,
+                             srv_rank, srv_vals, stream);
 }
 
 int saef_status(const saef_layout* layout, hipStream_t stream) {

@@ -67,6 +67,24 @@ class TopkOracle:
                                  self.srv_vals)
         assert rc == self.O.OK, rc
 
+    def begin(self, t, variant, mismatch=True):
+        w = self.w
+        mism = np.full(2 * w.L, np.nan) if mismatch else None
+        rc = self.orc.round_begin(t, w.period, self.K, w.mode, variant, self.e, self.e_srv, self.x,
+                                  self.xh, mism)
+        assert rc == self.O.OK, rc
+        return mism
+
+    def end(self, g):
+        w = self.w
+        mu = np.float32(0.0 if self.mu is None else self.mu)
+        rc = self.orc.topk_compress(self.K, np.float32(w.lr), mu, self.keep, g, self.m, self.e,
+                                    self.sel, self.rank, self.vals)
+        assert rc == self.O.OK, rc
+        rc = self.orc.topk_aggregate(self.K, w.mode, self.keep, self.sel, self.vals, self.x,
+                                     self.e_srv, self.srv_sel, self.srv_rank, self.srv_vals)
+        assert rc == self.O.OK, rc
+
 
 class TopkGpu:
     def __init__(self, w, keep, K=None, x0=None, mu=None):
@@ -100,6 +118,23 @@ class TopkGpu:
                                   w.mode if mode is None else mode, self.g, self.m, self.e,
                                   self.e_srv, self.x, self.xh, self.sel, self.rank, self.vals,
                                   self.srv_sel, self.srv_rank, self.srv_vals)
+
+    def begin(self, t, variant, mismatch=True):
+        w = self.w
+        mism = torch.full((2 * w.L,), float("nan"), dtype=torch.float64,
+                          device="cuda") if mismatch else None
+        xh = self.xh if variant == self.saef.VARIANT_SAEF else self.xh[0]
+        self.saef.saef_topk_round_begin(self.plan, t, w.period, self.K, w.mode, variant, self.e,
+                                        self.e_srv, self.x, xh, mism)
+        return None if mism is None else mism.cpu().numpy()
+
+    def end(self, g):
+        w = self.w
+        self.g.copy_(torch.from_numpy(g) if isinstance(g, np.ndarray) else g)
+        self.saef.saef_topk_round_end(self.plan, self.K, w.lr, 0.0 if self.mu is None else self.mu,
+                                      w.mode, self.g, self.m, self.e, self.e_srv, self.x, self.sel,
+                                      self.rank, self.vals, self.srv_sel, self.srv_rank,
+                                      self.srv_vals)
 
     def status(self):
         return self.saef.saef_status(self.layout)
@@ -270,6 +305,64 @@ def test_topk_round_parity(name):
         gs.round(t, g)
         compare_topk(gs, orc, t, name, mode=w.mode)
     assert gs.status() == 0
+
+
+HALVES_CASES = {
+    "resnet56_5pct_avg_dc": (W.get("resnet56").with_(rounds=8, period=3), 5),
+    "ragged_1pct_sc": (W.custom(ADVERSARIAL + [70001], K=3, period=0, rounds=6, mode=0,
+                                scale_range=(1e-4, 1e-1), seed=991), 1),
+}
+
+
+@pytest.mark.parametrize("variant", [0, 1], ids=["ef", "saef"])
+@pytest.mark.parametrize("name", list(HALVES_CASES))
+def test_topk_round_halves_parity(name, variant):
+    """Top-K in two halves (the EF branch of the paper's Table 1 comparison,
+    and SAEF) with the mismatch bounds at every iteration."""
+    w, pct = HALVES_CASES[name]
+    keep = W.topk_keep(w, pct)
+    _case(f"topk halves {name} variant={variant}")
+    orc = TopkOracle(w, keep)
+    gs = TopkGpu(w, keep)
+    for t in range(w.rounds):
+        g = W.gradients(w, t)
+        want = orc.begin(t, variant)
+        got = gs.begin(t, variant)
+        H.assert_mismatch_close(got, want, w, w.K, f"{name} t={t}")
+        orc.end(g)
+        gs.end(g)
+        compare_topk(gs, orc, t, f"{name} v{variant}", mode=w.mode)
+    assert gs.status() == 0
+
+
+def test_topk_closed_loop_quadratic_ef_vs_saef():
+    """Gradients taken at the evaluation point (noisy quadratic, fp32
+    elementwise on both sides): with Top-K the EF and SAEF trajectories
+    differ, and each matches the oracle bit for bit."""
+    w = W.get("resnet56").with_(period=0, rounds=6)
+    keep = W.topk_keep(w, 5)
+    off, n, d_pad = w.layout()
+    finals = []
+    for variant in (0, 1):
+        _case(f"topk closed loop variant={variant}")
+        rng = np.random.default_rng(77)
+        xstar = (rng.standard_normal(d_pad) * 0.05).astype(np.float32)
+        xstar_d = torch.from_numpy(xstar).cuda()
+        orc = TopkOracle(w, keep)
+        gs = TopkGpu(w, keep)
+        for t in range(w.rounds):
+            noise = (rng.standard_normal((w.K, d_pad)) * 0.01).astype(np.float32)
+            orc.begin(t, variant, mismatch=False)
+            gs.begin(t, variant, mismatch=False)
+            rows = orc.xh if variant == 1 else np.repeat(orc.xh[:1], w.K, axis=0)
+            g_host = (np.float32(0.5) * (rows - xstar)).astype(np.float32) + noise
+            xh_d = gs.xh if variant == 1 else gs.xh[:1].expand(w.K, d_pad)
+            g_dev = (0.5 * (xh_d - xstar_d)) + torch.from_numpy(noise).cuda()
+            orc.end(g_host)
+            gs.end(g_dev.contiguous())
+            compare_topk(gs, orc, t, f"closed loop v{variant}")
+        finals.append(orc.x.copy())
+    assert not np.array_equal(finals[0], finals[1])
 
 
 def test_topk_invalid_and_range():
