@@ -45,6 +45,8 @@ struct saef_topk {
   void* mem_hist2 = nullptr;
   void* mem_sel = nullptr;
   void* mem_tile_cnt = nullptr;
+  void* mem_cand = nullptr;
+  void* mem_cand_off = nullptr;
 };
 
 namespace {
@@ -133,6 +135,8 @@ void free_topk(saef_topk* p) {
   (void)hipFree(p->mem_hist2);
   (void)hipFree(p->mem_sel);
   (void)hipFree(p->mem_tile_cnt);
+  (void)hipFree(p->mem_cand);
+  (void)hipFree(p->mem_cand_off);
   delete p;
 }
 
@@ -604,12 +608,17 @@ int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk**
       red_split > 1 ? rows * L * red_split * saef::kTkBins * sizeof(uint32_t) : 0;
   const size_t sel_bytes = rows * L * sizeof(saef::TkSel);
   const size_t cnt_bytes = rows * layout->dev.n_tiles * sizeof(uint32_t);
+  // candidate slots: at most every element of a tensor (8 B each) per row
+  const size_t cand_bytes = rows * (size_t)layout->d_pad * sizeof(unsigned long long);
+  const size_t cand_off_bytes = rows * chunks.size() * sizeof(uint32_t);
   hipError_t err = hipMalloc(&p->mem_chunks, chunks.size() * sizeof(saef::TkChunk));
   if (err == hipSuccess) err = hipMalloc(&p->mem_tens, tens.size() * sizeof(saef::TkTensor));
   if (err == hipSuccess) err = hipMalloc(&p->mem_hist, hist_bytes);
   if (err == hipSuccess && hist2_bytes) err = hipMalloc(&p->mem_hist2, hist2_bytes);
   if (err == hipSuccess) err = hipMalloc(&p->mem_sel, sel_bytes);
   if (err == hipSuccess) err = hipMalloc(&p->mem_tile_cnt, cnt_bytes);
+  if (err == hipSuccess) err = hipMalloc(&p->mem_cand, cand_bytes);
+  if (err == hipSuccess) err = hipMalloc(&p->mem_cand_off, cand_off_bytes);
   if (err == hipSuccess)
     err = hipMemcpy(p->mem_chunks, chunks.data(), chunks.size() * sizeof(saef::TkChunk),
                     hipMemcpyHostToDevice);
@@ -629,6 +638,8 @@ int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk**
   d.hist2 = static_cast<uint32_t*>(p->mem_hist2);
   d.sel = static_cast<saef::TkSel*>(p->mem_sel);
   d.tile_cnt = static_cast<uint32_t*>(p->mem_tile_cnt);
+  d.cand = static_cast<unsigned long long*>(p->mem_cand);
+  d.cand_off = static_cast<uint32_t*>(p->mem_cand_off);
   d.n_chunks = (int64_t)chunks.size();
   d.total_keep = p->total_keep;
   d.red_split = red_split;

@@ -133,6 +133,9 @@ constexpr int kTkChunk = 65536;    // elements per histogram chunk (multiple of 
 constexpr int kTkBins = 2048;      // bins of the first two radix passes (11 bits)
 constexpr int kTkBins3 = 512;      // bins of the last pass (9 bits)
 constexpr int kTkRedChunks = 64;   // chunk histograms one reduce workgroup adds
+static_assert(kTkChunk % kTileElems == 0, "a Top-K chunk holds whole tiles");
+static_assert((int64_t)kTileElems * kMaxTilesPerTensor >= kMaxTensor,
+              "every tensor is cut into tiles of kTileElems elements");
 
 struct TkChunk {
   int64_t start;  // absolute element index (multiple of 64)
@@ -147,16 +150,17 @@ struct TkTensor {
   int32_t nchunks;
 };
 
-// Selection state of one (row, tensor): the key prefix found so far, how
-// many elements still to take at or below it, and after the last pass the
-// threshold key tau, the tie cut and the largest kept tie index.
+// Selection state of one (row, tensor): after the pick, the bin b1 of key
+// bits 30..20 that holds the k-th largest key, how many elements to take
+// from it and how many it holds (the candidates); after the select, the
+// threshold key tau and the last kept index iota (in the tensor) of the
+// elements equal to tau.
 struct TkSel {
-  uint32_t prefix;
+  uint32_t prefix;  // b1, then tau
   uint32_t pad;
   int64_t need;
-  int64_t cut_chunk;  // chunk (index in the tensor) holding the last kept tie, or -1
-  int64_t cut_rank;   // 1-based rank of that tie inside the chunk
-  int64_t iota;       // elements equal to tau with index <= iota are kept
+  int64_t cand;
+  int64_t iota;     // elements equal to tau with index <= iota are kept
 };
 
 struct TkDev {
@@ -166,6 +170,8 @@ struct TkDev {
   uint32_t* hist2;   // [rows][L][red_split][kTkBins] second-level sums (red_split > 1)
   TkSel* sel;        // [rows][L]
   uint32_t* tile_cnt;  // [rows][n_tiles] kept per tile, then the exclusive prefix
+  unsigned long long* cand;  // [rows][d_pad] candidate slots: (row, tensor) at the tensor's offset
+  uint32_t* cand_off;  // [rows][n_chunks] first slot of each chunk's candidates
   int64_t n_chunks;
   int64_t total_keep;
   int32_t red_split;   // reduce workgroups per (row, tensor)

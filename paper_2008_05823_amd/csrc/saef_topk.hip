@@ -1,25 +1,30 @@
 // HIP kernels of the layer-wise Top-K compressor on gfx950 (CDNA4, wave64).
 //
 // C(v) keeps the k_l elements of largest |v| of each tensor (equal
-// magnitudes: the lower index first) and zeroes the others.  The kept set is
-// found by a radix select on the 31-bit key |v| (the bit pattern of a
-// non-negative float orders like its value), per (row, tensor):
-//   pass 1  histogram of key bits 30..20 (2048 bins) per 64Ki-element chunk,
-//           built with LDS atomics and stored with plain stores; a pick
-//           kernel adds the chunk histograms of the tensor and finds the
-//           bucket that holds the k-th largest key;
-//   pass 2  bits 19..9 of the elements of that bucket;
-//   pass 3  bits 8..0: the threshold key tau and how many of the elements
-//           equal to tau are kept; if not all, the chunk that holds the cut
-//           is scanned in index order for the last kept index iota.
-// Emit: kept = key > tau, or key == tau and index <= iota; the selection
-// words (one ballot per 64 elements) and the kept count of each tile; an
-// exclusive scan of the counts over the tensor's tiles; then the rank words
+// magnitudes: the lower index first) and zeroes the others.  The kept set of
+// each (row, tensor) is found on the 31-bit key |v| (the bit pattern of a
+// non-negative float orders like its value):
+//   histogram  the pass that forms Delta also counts key bits 30..20 (2048
+//              bins) per 64Ki-element chunk, with LDS atomics and plain stores
+//              of the chunk histogram (no global atomics);
+//   pick       a workgroup per (row, tensor) adds the chunk histograms, finds
+//              the bin b1 that holds the k-th largest key and lays out, per
+//              chunk, slots for the elements of b1 (the candidates);
+//   gather     one read of Delta: elements above b1 are kept for sure and
+//              written to the selection words; the candidates go to their
+//              chunk's slots as (key, index in the tensor);
+//   select     a workgroup per (row, tensor) finds, among the candidates only,
+//              the threshold key tau and the last kept index iota of the
+//              elements equal to tau (radix passes on the key's low 20 bits,
+//              then on the index);
+//   apply      the kept candidates' bits are added to the selection words
+//              of their chunk, and the kept count of each tile is taken.
+// Emit: an exclusive scan of the tile counts per tensor; then the rank words
 // and the kept values in index order, and the kept elements of the error set
 // to 0 (e = Delta - C(Delta) is Delta elsewhere).  All of it is integer
 // counting, so the kept set does not depend on the launch geometry.
 //
-// The server runs the same passes on its one row (row k_max of the scratch)
+// The server runs the same steps on its one row (row k_max of the scratch)
 // after k_tk_aggregate has formed Delta = e_srv + mean of the K messages.
 #include "saef_device.h"
 #include "saef_internal.h"
@@ -29,12 +34,8 @@ namespace {
 
 constexpr uint32_t kFiniteLimit = 0x7F800000u;  // keys >= this are Inf or NaN
 constexpr int kTkU = 4;                         // words per wave per pass (first pass, server)
-constexpr int kTkH = 8;                         // words per wave per pass (later passes)
-constexpr int kTkE = 16;                        // words per wave per pass (emit)
+constexpr int kTkH = 16;                        // words per wave per pass (gather)
 constexpr int kBig = 1024;                      // threads of the single-row (server) kernels
-#ifndef SAEF_TK_HIST_THREADS
-#define SAEF_TK_HIST_THREADS 256
-#endif
 #ifndef SAEF_TK_NT
 #define SAEF_TK_NT 1
 #endif
@@ -61,36 +62,8 @@ __device__ __forceinline__ u64 lanemask_lt(int lane) {
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
-// Lane of the n-th (1-based) set bit of m; m has at least n set bits.
-__device__ __forceinline__ int nth_set_bit(u64 m, int n) {
-  for (int i = 1; i < n; ++i) m &= m - 1;
-  return __builtin_ctzll(m);
-}
-
-// The digit of each radix pass and the prefix an element must match.
-template <int kPass>
-struct Digit;
-template <>
-struct Digit<1> {
-  static constexpr int kBins = kTkBins;
-  static constexpr int kBits = 11;
-  __device__ static uint32_t get(uint32_t key) { return key >> 20; }
-  __device__ static bool match(uint32_t, uint32_t) { return true; }
-};
-template <>
-struct Digit<2> {
-  static constexpr int kBins = kTkBins;
-  static constexpr int kBits = 11;
-  __device__ static uint32_t get(uint32_t key) { return (key >> 9) & (kTkBins - 1); }
-  __device__ static bool match(uint32_t key, uint32_t prefix) { return (key >> 20) == prefix; }
-};
-template <>
-struct Digit<3> {
-  static constexpr int kBins = kTkBins3;
-  static constexpr int kBits = 9;
-  __device__ static uint32_t get(uint32_t key) { return key & (kTkBins3 - 1); }
-  __device__ static bool match(uint32_t key, uint32_t prefix) { return (key >> 9) == prefix; }
-};
+// Pass-1 digit: key bits 30..20.
+__device__ __forceinline__ uint32_t digit1(uint32_t key) { return key >> 20; }
 
 template <int kBins>
 __device__ __forceinline__ void hist_clear(uint32_t* h) {
@@ -140,7 +113,7 @@ __device__ __forceinline__ void delta_words(int w0, int nw, int count, float lr,
     st_nt(ek + j, p);
     const uint32_t key = key_of(p);
     bad |= key >= kFiniteLimit;
-    atomicAdd(&h[Digit<1>::get(key)], 1u);
+    atomicAdd(&h[digit1(key)], 1u);
   }
 }
 
@@ -171,48 +144,11 @@ __global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, in
   hist_store<kTkBins>(h, chunk_hist(tk, k, ci));
 }
 
-// ------------------------------------------------------------------ passes 2 and 3
-// Grid: n_chunks * R workgroups of kThreads (R rows from row0; data row r at
-// data + r d_pad).
-template <int kPass, int kThreads>
-__global__ __launch_bounds__(kThreads) void k_tk_hist(DevLayout lay, TkDev tk, int R, int row0,
-                                                      const float* __restrict__ data) {
-  constexpr int B = Digit<kPass>::kBins;
-  constexpr int kW = kThreads / kWave;
-  __shared__ uint32_t h[B];
-  const int r = (int)(blockIdx.x % (unsigned)R);
-  const int64_t ci = blockIdx.x / (unsigned)R;
-  const TkChunk c = tk.chunks[ci];
-  const uint32_t prefix = tk.sel[(int64_t)(row0 + r) * lay.L + c.l].prefix;
-  hist_clear<B>(h);
-  const float* dr = data + (int64_t)r * lay.d_pad + c.start;
-  const int lane = lane_id();
-  const int nw = (c.count + 63) >> 6;
-  for (int w0 = wave_id() * kTkH; w0 < nw; w0 += kW * kTkH) {
-    float v[kTkH];
-#pragma unroll
-    for (int u = 0; u < kTkH; ++u) {
-      const int j = (w0 + u) * 64 + lane;
-      v[u] = ld_pass_or0(dr, j, w0 + u < nw && j < c.count);
-    }
-#pragma unroll
-    for (int u = 0; u < kTkH; ++u) {
-      const int j = (w0 + u) * 64 + lane;
-      const uint32_t key = key_of(v[u]);
-      if (w0 + u < nw && j < c.count && Digit<kPass>::match(key, prefix))
-        atomicAdd(&h[Digit<kPass>::get(key)], 1u);
-    }
-  }
-  hist_store<B>(h, chunk_hist(tk, row0 + r, ci));
-}
-
-// ------------------------------------------------------------------ reduce and pick
+// ------------------------------------------------------------------ reduce
 // Grid: R * L * red_split workgroups: group s adds the chunk histograms
 // [s kTkRedChunks, (s+1) kTkRedChunks) of the tensor (those that exist).
-template <int kPass>
 __global__ __launch_bounds__(kBlock) void k_tk_sum(DevLayout lay, TkDev tk, int row0) {
-  constexpr int B = Digit<kPass>::kBins;
-  constexpr int kPer = B / kBlock;
+  constexpr int kPer = kTkBins / kBlock;
   const int S = tk.red_split;
   const int s = (int)(blockIdx.x % S);
   const int l = (int)((blockIdx.x / S) % lay.L);
@@ -233,23 +169,90 @@ __global__ __launch_bounds__(kBlock) void k_tk_sum(DevLayout lay, TkDev tk, int 
   for (int j = 0; j < kPer; ++j) dst[j] = acc[j];
 }
 
-// Grid: R * L workgroups.  Adds the tensor's histograms (the chunk
-// histograms, or the red_split partial sums), finds the bin that holds the
-// need-th largest key counted from the top, and updates the selection state.
-// After pass 3 the prefix is the threshold key tau; when only some of the
-// elements equal to tau are kept, the chunk of the cut and the rank in it
-// are located from the chunk histograms.
-template <int kPass>
+// ------------------------------------------------------------------ block helpers
+// Exclusive prefix sum of v over the workgroup (threads in order); *total
+// receives the sum.  s must hold blockDim.x / 64 entries.
+__device__ uint32_t block_excl_scan(uint32_t v, uint32_t* s, uint32_t* total) {
+  const int lane = lane_id();
+  const int wave = threadIdx.x / kWave;
+  const int nwaves = blockDim.x / kWave;
+  uint32_t x = v;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint32_t y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  if (lane == kWave - 1) s[wave] = x;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+  for (int i = 0; i < nwaves; ++i) {
+    if (i < wave) before += s[i];
+    all += s[i];
+  }
+  __syncthreads();
+  *total = all;
+  return before + x - v;
+}
+
+// Over the LDS histogram h[0..nb), the bin that holds the need-th element
+// counted from the top (kTop) or from the bottom (1 <= need <= total).
+// Returns to every thread the bin, how many to take inside it and its count.
+template <bool kTop>
+__device__ void find_bin(const uint32_t* h, int nb, int64_t need, uint32_t* s_scan,
+                         uint32_t* s_res, uint32_t& bin, int64_t& left, uint32_t& count) {
+  const int per = (nb + (int)blockDim.x - 1) / (int)blockDim.x;
+  if (threadIdx.x == 0) {  // defined result even if need exceeded the total
+    s_res[0] = 0;
+    s_res[1] = 1;
+    s_res[2] = 0;
+  }
+  // thread t owns positions [t per, (t+1) per) counted in the search direction
+  uint32_t tot = 0;
+  for (int j = 0; j < per; ++j) {
+    const int q = threadIdx.x * per + j;
+    if (q < nb) tot += h[kTop ? nb - 1 - q : q];
+  }
+  uint32_t all;
+  const uint32_t before = block_excl_scan(tot, s_scan, &all);
+  if ((int64_t)before < need && need <= (int64_t)before + tot) {
+    int64_t run = before;
+    for (int j = 0; j < per; ++j) {
+      const int q = threadIdx.x * per + j;
+      if (q >= nb) break;
+      const int b = kTop ? nb - 1 - q : q;
+      if (run + h[b] >= need) {
+        s_res[0] = (uint32_t)b;
+        s_res[1] = (uint32_t)(need - run);
+        s_res[2] = h[b];
+        break;
+      }
+      run += h[b];
+    }
+  }
+  __syncthreads();
+  bin = s_res[0];
+  left = s_res[1];
+  count = s_res[2];
+  __syncthreads();
+}
+
+// ------------------------------------------------------------------ pick
+// Grid: R * L workgroups.  Adds the tensor's pass-1 histograms (the chunk
+// histograms, or the red_split partial sums), finds the bin b1 that holds
+// the k-th largest key and how many to take from it, and lays out the
+// candidate slots: chunk c's elements of b1 go to slots [off_c, off_c +
+// count_c) of the (row, tensor)'s candidate area (one slot per element of
+// the tensor at most), off_c the exclusive prefix of the counts in chunk
+// order.
 __global__ __launch_bounds__(kBlock) void k_tk_pick(DevLayout lay, TkDev tk, int row0) {
-  constexpr int B = Digit<kPass>::kBins;
-  constexpr int kPer = B / kBlock;
-  __shared__ uint32_t s_tot[kBlock];
-  __shared__ uint32_t s_above[kBlock];
+  constexpr int kPer = kTkBins / kBlock;
+  __shared__ uint32_t s_scan[kWaves];
+  __shared__ uint32_t s_res[3];
+  __shared__ uint32_t h[kTkBins];
   const int l = (int)(blockIdx.x % lay.L);
   const int r = (int)(blockIdx.x / lay.L);
   const int row = row0 + r;
   const TkTensor t = tk.tens[l];
-  TkSel* st = tk.sel + (int64_t)row * lay.L + l;
   const int S = tk.red_split;
   uint32_t cnt[kPer];
 #pragma unroll
@@ -266,162 +269,219 @@ __global__ __launch_bounds__(kBlock) void k_tk_pick(DevLayout lay, TkDev tk, int
       for (int j = 0; j < kPer; ++j) cnt[j] += src[j];
     }
   }
-  uint32_t tot = 0;
 #pragma unroll
-  for (int j = 0; j < kPer; ++j) tot += cnt[j];
-  s_tot[threadIdx.x] = tot;
-  const int64_t need = (kPass == 1) ? t.keep : st->need;
-  const uint32_t prefix = (kPass == 1) ? 0u : st->prefix;
+  for (int j = 0; j < kPer; ++j) h[threadIdx.x * kPer + j] = cnt[j];
   __syncthreads();
-  if (threadIdx.x == 0) {
-    // elements in the bins above each thread's range (a tensor has < 2^32)
-    uint32_t run = 0;
-    for (int i = kBlock - 1; i >= 0; --i) {
-      s_above[i] = run;
-      run += s_tot[i];
-    }
+  uint32_t b1, n1;
+  int64_t left;
+  find_bin<true>(h, kTkBins, t.keep, s_scan, s_res, b1, left, n1);
+  // candidate slots per chunk
+  uint32_t carry = 0;
+  for (int c0 = 0; c0 < t.nchunks; c0 += kBlock) {
+    const int c = c0 + threadIdx.x;
+    const uint32_t v = c < t.nchunks ? chunk_hist(tk, row, t.first_chunk + c)[b1] : 0u;
+    uint32_t all;
+    const uint32_t before = block_excl_scan(v, s_scan, &all);
+    if (c < t.nchunks) tk.cand_off[(int64_t)row * tk.n_chunks + t.first_chunk + c] = carry + before;
+    carry += all;
   }
-  __syncthreads();
-  int64_t run = s_above[threadIdx.x];
-  if (run >= need || run + tot < need) return;  // the need-th key is not in this range
-  for (int j = kPer - 1; j >= 0; --j) {
-    if (run + cnt[j] >= need) {
-      const uint32_t bin = (uint32_t)(threadIdx.x * kPer + j);
-      const uint32_t np = (prefix << Digit<kPass>::kBits) | bin;
-      const int64_t left = need - run;  // to take from this bin
-      st->prefix = np;
-      st->need = left;
-      if (kPass == 3) {
-        if (left == (int64_t)cnt[j]) {
-          st->cut_chunk = -1;
-          st->iota = INT64_MAX;  // every element equal to tau is kept
-        } else {
-          int64_t before = 0;
-          for (int c = 0; c < t.nchunks; ++c) {
-            const int64_t in_c = chunk_hist(tk, row, t.first_chunk + c)[bin];
-            if (before + in_c >= left) {
-              st->cut_chunk = c;
-              st->cut_rank = left - before;
-              break;
-            }
-            before += in_c;
-          }
-        }
-      }
-      return;
-    }
-    run += cnt[j];
+  if (threadIdx.x == 0) {
+    TkSel* st = tk.sel + (int64_t)row * lay.L + l;
+    st->prefix = b1;
+    st->need = left;
+    st->cand = n1;  // the elements of b1 (the sum of the chunk counts)
   }
 }
 
-// ------------------------------------------------------------------ ties
-// Grid: R * L workgroups of kBig threads.  When only part of the elements
-// equal to tau are kept, finds the cut_rank-th of them in index order in the
-// chunk of the cut; its absolute element index becomes iota.  Each wave
-// counts the ties of its own contiguous slice of the chunk, a prefix over
-// the waves names the slice of the cut, and that wave scans its slice again
-// (from the caches) to place it.
-__global__ __launch_bounds__(kBig) void k_tk_ties(DevLayout lay, TkDev tk, int row0,
-                                                  const float* __restrict__ data) {
-  constexpr int kW = kBig / kWave;
-  __shared__ uint32_t s_cnt[kW];
-  const int l = (int)(blockIdx.x % lay.L);
-  const int r = (int)(blockIdx.x / lay.L);
-  TkSel* st = tk.sel + (int64_t)(row0 + r) * lay.L + l;
-  if (st->cut_chunk < 0) return;  // uniform over the workgroup
-  const TkTensor t = tk.tens[l];
-  const TkChunk c = tk.chunks[t.first_chunk + st->cut_chunk];
-  const uint32_t tau = st->prefix;
-  const int64_t target = st->cut_rank;
+// ------------------------------------------------------------------ gather
+// Grid: n_chunks * R workgroups of kThreads.  One read of Delta: the
+// selection words with the elements above b1 (kept for sure), and the
+// elements of b1 appended to the chunk's candidate slots as
+// key | (index in the tensor) << 32.  Their order inside the chunk's slots
+// is that of the LDS reservations; nothing downstream depends on it.
+template <int kThreads>
+__global__ __launch_bounds__(kThreads) void k_tk_gather(DevLayout lay, TkDev tk, int R, int row0,
+                                                        const float* __restrict__ data,
+                                                        uint64_t* __restrict__ sel) {
+  constexpr int kW = kThreads / kWave;
+  __shared__ uint32_t s_next;
+  const int r = (int)(blockIdx.x % (unsigned)R);
+  const int64_t ci = blockIdx.x / (unsigned)R;
+  const int row = row0 + r;
+  const TkChunk c = tk.chunks[ci];
+  const uint32_t b1 = tk.sel[(int64_t)row * lay.L + c.l].prefix;
+  const TkTensor t = tk.tens[c.l];
+  const int64_t t_off = tk.chunks[t.first_chunk].start;
+  const int64_t rel0 = c.start - t_off;  // the chunk's first element, index in the tensor
+  u64* slots = tk.cand + (int64_t)row * lay.d_pad + t_off +
+               tk.cand_off[(int64_t)row * tk.n_chunks + ci];
+  const uint32_t nslots = chunk_hist(tk, row, ci)[b1];  // elements of b1 in the chunk
+  if (threadIdx.x == 0) s_next = 0;
+  __syncthreads();
   const float* dr = data + (int64_t)r * lay.d_pad + c.start;
+  uint64_t* sr = sel + (int64_t)r * (lay.d_pad >> 6) + (c.start >> 6);
   const int lane = lane_id();
-  const int wave = wave_id();
+  const u64 lt = lanemask_lt(lane);
   const int nw = (c.count + 63) >> 6;
-  const int per = (nw + kW - 1) / kW;  // words of each wave's slice
-  const int w_lo = min(nw, wave * per), w_hi = min(nw, w_lo + per);
-  uint32_t mine = 0;
-  for (int w0 = w_lo; w0 < w_hi; w0 += kTkE) {
-    float v[kTkE];
+  for (int w0 = wave_id() * kTkH; w0 < nw; w0 += kW * kTkH) {
+    float v[kTkH];
 #pragma unroll
-    for (int u = 0; u < kTkE; ++u) {
+    for (int u = 0; u < kTkH; ++u) {
       const int j = (w0 + u) * 64 + lane;
-      v[u] = ld_nt_or0(dr, j, w0 + u < w_hi && j < c.count);
+      v[u] = ld_pass_or0(dr, j, w0 + u < nw && j < c.count);
     }
+    u64 cm[kTkH];
+    uint32_t ncand = 0;
 #pragma unroll
-    for (int u = 0; u < kTkE; ++u) {
+    for (int u = 0; u < kTkH; ++u) {
       const int j = (w0 + u) * 64 + lane;
-      mine += (uint32_t)__popcll(__ballot(w0 + u < w_hi && j < c.count && key_of(v[u]) == tau));
+      const bool ok = w0 + u < nw && j < c.count;
+      const uint32_t hi = digit1(key_of(v[u]));
+      const u64 word = __ballot(ok && hi > b1);
+      if (lane == 0 && w0 + u < nw) sr[w0 + u] = word;
+      cm[u] = __ballot(ok && hi == b1);
+      ncand += (uint32_t)__popcll(cm[u]);
+    }
+    if (ncand != 0) {  // uniform over the wave
+      uint32_t base = 0;
+      if (lane == 0) base = atomicAdd(&s_next, ncand);
+      base = __shfl(base, 0);
+#pragma unroll
+      for (int u = 0; u < kTkH; ++u) {
+        const uint32_t pos = base + (uint32_t)__popcll(cm[u] & lt);
+        if (((cm[u] >> lane) & 1ull) && pos < nslots) {  // pos < nslots always holds
+          const int64_t idx = rel0 + (int64_t)(w0 + u) * 64 + lane;
+          slots[pos] = (u64)key_of(v[u]) | ((u64)idx << 32);
+        }
+        base += (uint32_t)__popcll(cm[u]);
+      }
     }
   }
-  if (lane == 0) s_cnt[wave] = mine;
+}
+
+// ------------------------------------------------------------------ select
+// One radix pass over the candidates: histogram (LDS) of digit(e) of those
+// with match(e).
+template <typename Match, typename Dig>
+__device__ void cand_hist(uint32_t* h, int nb, const u64* __restrict__ cand, int64_t C,
+                          Match match, Dig digit) {
+  for (int i = threadIdx.x; i < nb; i += blockDim.x) h[i] = 0;
   __syncthreads();
-  int64_t before = 0;
-  for (int i = 0; i < wave; ++i) before += s_cnt[i];
-  if (!(before < target && target <= before + mine)) return;
-  // this wave's slice holds the cut
-  for (int w0 = w_lo; w0 < w_hi; w0 += kTkE) {
-    float v[kTkE];
-#pragma unroll
-    for (int u = 0; u < kTkE; ++u) {
-      const int j = (w0 + u) * 64 + lane;
-      v[u] = ld_or0(dr, j, w0 + u < w_hi && j < c.count);
-    }
-#pragma unroll
-    for (int u = 0; u < kTkE; ++u) {
-      const int j = (w0 + u) * 64 + lane;
-      const u64 m = __ballot(w0 + u < w_hi && j < c.count && key_of(v[u]) == tau);
-      const int n = (int)__popcll(m);
-      if (before < target && target <= before + n) {
-        const int b = nth_set_bit(m, (int)(target - before));
-        if (lane == 0) st->iota = c.start + (int64_t)(w0 + u) * 64 + b;
-      }
-      before += n;
-    }
+  for (int64_t i = threadIdx.x; i < C; i += blockDim.x) {
+    const u64 e = cand[i];
+    if (match(e)) atomicAdd(&h[digit(e)], 1u);
+  }
+  __syncthreads();
+}
+
+// Grid: R * L workgroups of kBig threads.  Among the candidates of (row,
+// tensor) (the elements of bin b1), takes the `need` largest keys, equal
+// keys by lower index: radix passes on key bits 19..9 and 8..0 give the
+// threshold key tau and how many of the elements equal to tau are kept; if
+// not all, passes on the index in the tensor (bits 27..17, 16..6, 5..0)
+// give the last kept index iota.
+__global__ __launch_bounds__(kBig) void k_tk_select(DevLayout lay, TkDev tk, int row0) {
+  __shared__ uint32_t h[kTkBins];
+  __shared__ uint32_t s_scan[kBig / kWave];
+  __shared__ uint32_t s_res[3];
+  const int l = (int)(blockIdx.x % lay.L);
+  const int r = (int)(blockIdx.x / lay.L);
+  const int row = row0 + r;
+  TkSel* st = tk.sel + (int64_t)row * lay.L + l;
+  const TkTensor t = tk.tens[l];
+  const int64_t t_off = tk.chunks[t.first_chunk].start;
+  const u64* cand = tk.cand + (int64_t)row * lay.d_pad + t_off;
+  const int64_t C = st->cand;
+  const uint32_t b1 = st->prefix;
+  int64_t need = st->need;
+  uint32_t bin, cnt;
+  int64_t left;
+  // key bits 19..9
+  cand_hist(h, kTkBins, cand, C, [](u64) { return true; },
+            [](u64 e) { return ((uint32_t)e >> 9) & 2047u; });
+  find_bin<true>(h, kTkBins, need, s_scan, s_res, bin, left, cnt);
+  const uint32_t p2 = (b1 << 11) | bin;
+  need = left;
+  // key bits 8..0
+  cand_hist(h, kTkBins3, cand, C, [p2](u64 e) { return ((uint32_t)e >> 9) == p2; },
+            [](u64 e) { return (uint32_t)e & 511u; });
+  find_bin<true>(h, kTkBins3, need, s_scan, s_res, bin, left, cnt);
+  const uint32_t tau = (p2 << 9) | bin;
+  int64_t iota = INT64_MAX;  // every element equal to tau is kept
+  if (left < (int64_t)cnt) {
+    // the left-th smallest index among the elements equal to tau
+    need = left;
+    cand_hist(h, kTkBins, cand, C, [tau](u64 e) { return (uint32_t)e == tau; },
+              [](u64 e) { return (uint32_t)(e >> 49) & 2047u; });
+    find_bin<false>(h, kTkBins, need, s_scan, s_res, bin, left, cnt);
+    const uint32_t q1 = bin;
+    need = left;
+    cand_hist(h, kTkBins, cand, C,
+              [tau, q1](u64 e) { return (uint32_t)e == tau && (uint32_t)(e >> 49) == q1; },
+              [](u64 e) { return (uint32_t)(e >> 38) & 2047u; });
+    find_bin<false>(h, kTkBins, need, s_scan, s_res, bin, left, cnt);
+    const uint32_t q2 = (q1 << 11) | bin;
+    need = left;
+    cand_hist(h, 64, cand, C,
+              [tau, q2](u64 e) { return (uint32_t)e == tau && (uint32_t)(e >> 38) == q2; },
+              [](u64 e) { return (uint32_t)(e >> 32) & 63u; });
+    find_bin<false>(h, 64, need, s_scan, s_res, bin, left, cnt);
+    iota = ((int64_t)q2 << 6) | bin;
+  }
+  if (threadIdx.x == 0) {
+    st->prefix = tau;
+    st->iota = iota;
+  }
+}
+
+// ------------------------------------------------------------------ apply
+// Grid: n_chunks * R workgroups.  Adds the bits of the kept candidates to the
+// chunk's selection words (in LDS, then written back) and stores the kept
+// count of each tile of the chunk.
+__global__ __launch_bounds__(kBlock) void k_tk_apply(DevLayout lay, TkDev tk, int R, int row0,
+                                                     uint64_t* __restrict__ sel) {
+  constexpr int kWords = kTkChunk / 64;
+  constexpr int kTileWords = kTileElems / 64;
+  __shared__ u64 words[kWords];
+  const int r = (int)(blockIdx.x % (unsigned)R);
+  const int64_t ci = blockIdx.x / (unsigned)R;
+  const int row = row0 + r;
+  const TkChunk c = tk.chunks[ci];
+  const TkSel st = tk.sel[(int64_t)row * lay.L + c.l];
+  const uint32_t tau = st.prefix;
+  const int64_t iota = st.iota;
+  const TkTensor t = tk.tens[c.l];
+  const int64_t t_off = tk.chunks[t.first_chunk].start;
+  const int64_t rel0 = c.start - t_off;
+  const int nw = (c.count + 63) >> 6;
+  uint64_t* sr = sel + (int64_t)r * (lay.d_pad >> 6) + (c.start >> 6);
+  for (int i = threadIdx.x; i < nw; i += kBlock) words[i] = sr[i];
+  __syncthreads();
+  const uint32_t ncand = chunk_hist(tk, row, ci)[digit1(tau)];
+  const u64* slots = tk.cand + (int64_t)row * lay.d_pad + t_off +
+                     tk.cand_off[(int64_t)row * tk.n_chunks + ci];
+  for (uint32_t i = threadIdx.x; i < ncand; i += kBlock) {
+    const u64 e = slots[i];
+    const uint32_t key = (uint32_t)e;
+    const int64_t idx = (int64_t)(e >> 32);
+    const int64_t q = idx - rel0;  // element of the chunk
+    if ((key > tau || (key == tau && idx <= iota)) && q >= 0 && q < c.count)
+      atomicOr(&words[q >> 6], 1ull << (q & 63));
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < nw; i += kBlock) sr[i] = words[i];
+  // tiles of the chunk (a chunk starts on a tile boundary)
+  const int ntile = (nw + kTileWords - 1) / kTileWords;
+  const int64_t tile0 = lay.tensors[c.l].first_tile + rel0 / kTileElems;
+  for (int i = threadIdx.x; i < ntile; i += kBlock) {
+    uint32_t n = 0;
+    for (int w = i * kTileWords; w < min(nw, (i + 1) * kTileWords); ++w)
+      n += (uint32_t)__popcll(words[w]);
+    tk.tile_cnt[(int64_t)row * lay.n_tiles + tile0 + i] = n;
   }
 }
 
 // ------------------------------------------------------------------ emit
-// Grid: per_wave_grid(lay) * R workgroups; wave w of workgroup b owns tile
-// 4 (b / R) + w of row b % R.  Writes the selection words of the tile and
-// its kept count.
-__global__ __launch_bounds__(kBlock) void k_tk_emit1(DevLayout lay, TkDev tk, int R, int row0,
-                                                     const float* __restrict__ data,
-                                                     uint64_t* __restrict__ sel) {
-  const int r = (int)(blockIdx.x % (unsigned)R);
-  const int64_t ti = (int64_t)(blockIdx.x / (unsigned)R) * kWaves + wave_id();
-  if (ti >= lay.n_tiles) return;
-  const Tile tile = lay.tiles[ti];
-  const TkSel st = tk.sel[(int64_t)(row0 + r) * lay.L + tile.l];
-  const uint32_t tau = st.prefix;
-  const int64_t iota = st.iota;
-  const int lane = lane_id();
-  const int nw = (tile.count + 63) >> 6;
-  const float* dr = data + (int64_t)r * lay.d_pad + tile.start;
-  uint64_t* sr = sel + (int64_t)r * (lay.d_pad >> 6) + (tile.start >> 6);
-  uint32_t cnt = 0;
-  for (int w0 = 0; w0 < nw; w0 += kTkE) {
-    float v[kTkE];
-#pragma unroll
-    for (int u = 0; u < kTkE; ++u) {
-      const int j = (w0 + u) * 64 + lane;
-      v[u] = ld_pass_or0(dr, j, w0 + u < nw && j < tile.count);
-    }
-#pragma unroll
-    for (int u = 0; u < kTkE; ++u) {
-      const int w = w0 + u;
-      if (w >= nw) continue;
-      const int j = w * 64 + lane;
-      const uint32_t key = key_of(v[u]);
-      const bool kept = j < tile.count &&
-                        (key > tau || (key == tau && tile.start + j <= iota));
-      const u64 word = __ballot(kept);
-      if (lane == 0) sr[w] = word;
-      cnt += (uint32_t)__popcll(word);
-    }
-  }
-  if (lane == 0) tk.tile_cnt[(int64_t)(row0 + r) * lay.n_tiles + ti] = cnt;
-}
-
 // Grid: R * L workgroups: exclusive prefix of the kept counts over the
 // tensor's tiles, in tile order, in place.
 __global__ __launch_bounds__(kBlock) void k_tk_scan(DevLayout lay, TkDev tk, int row0) {
@@ -450,10 +510,12 @@ __global__ __launch_bounds__(kBlock) void k_tk_scan(DevLayout lay, TkDev tk, int
   }
 }
 
-// Grid: per_wave_grid(lay) * R workgroups, tiles as in k_tk_emit1.  Rank
-// words, the kept values in index order, the kept elements of data set to
-// 0; kX (server): x <- x - Delta at the kept elements (C(Delta) is zero
-// elsewhere).
+// Grid: per_wave_grid(lay) * R workgroups; wave w of workgroup b owns tile
+// 4 (b / R) + w of row b % R.  Rank words, the kept values in index order,
+// the kept elements of data set to 0; kX (server): x <- x - Delta at the
+// kept elements (C(Delta) is zero elsewhere).  One pass per tile: lane j
+// loads selection word j of the tile, a wave scan of the word counts gives
+// every rank word, then the loads of all kept elements go out together.
 template <bool kX>
 __global__ __launch_bounds__(kBlock) void k_tk_emit2(DevLayout lay, TkDev tk, int R, int row0,
                                                      float* __restrict__ data,
@@ -461,6 +523,8 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit2(DevLayout lay, TkDev tk, in
                                                      uint32_t* __restrict__ rank,
                                                      float* __restrict__ vals,
                                                      float* __restrict__ x) {
+  constexpr int kTileWords = kTileElems / 64;
+  static_assert(kTileWords <= kWave, "one selection word per lane");
   const int r = (int)(blockIdx.x % (unsigned)R);
   const int64_t ti = (int64_t)(blockIdx.x / (unsigned)R) * kWaves + wave_id();
   if (ti >= lay.n_tiles) return;
@@ -474,39 +538,44 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit2(DevLayout lay, TkDev tk, in
   uint32_t* rr = rank + (int64_t)r * W + (tile.start >> 6);
   float* vr = vals + (int64_t)r * tk.total_keep + t.voff;
   float* xt = kX ? x + tile.start : nullptr;
-  uint32_t run = tk.tile_cnt[(int64_t)(row0 + r) * lay.n_tiles + ti];
+  const uint32_t base = tk.tile_cnt[(int64_t)(row0 + r) * lay.n_tiles + ti];
+  // lane j: word j of the tile, its kept count and the exclusive prefix
+  const u64 my = sr[lane < nw ? lane : 0];
+  const u64 mine = lane < nw ? my : 0ull;
+  const uint32_t c = (uint32_t)__popcll(mine);
+  uint32_t incl = c;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint32_t y = __shfl_up(incl, off);
+    if (lane >= off) incl += y;
+  }
+  const uint32_t my_rank = base + incl - c;
+  if (lane < nw) rr[lane] = my_rank;
   const u64 lt = lanemask_lt(lane);
-  for (int w0 = 0; w0 < nw; w0 += kTkE) {
-    u64 m[kTkE];
+  const uint32_t lo = (uint32_t)mine, hi = (uint32_t)(mine >> 32);
+  // words per pass: the server also loads x, so it takes two passes
+  constexpr int kP = kX ? kTileWords / 2 : kTileWords;
 #pragma unroll
-    for (int u = 0; u < kTkE; ++u) {
-      const u64 word = sr[min(w0 + u, nw - 1)];  // always in the tile; masked below
-      m[u] = (w0 + u < nw) ? word : 0ull;
+  for (int u0 = 0; u0 < kTileWords; u0 += kP) {
+    float v[kP], xv[kP];
+    uint32_t pos[kP];
+    bool kept[kP];
+#pragma unroll
+    for (int i = 0; i < kP; ++i) {
+      const int u = u0 + i;
+      const u64 m = ((u64)(uint32_t)__shfl(hi, u) << 32) | (uint32_t)__shfl(lo, u);
+      pos[i] = (uint32_t)__shfl(my_rank, u) + (uint32_t)__popcll(m & lt);
+      kept[i] = u < nw && ((m >> lane) & 1ull) && pos[i] < (uint32_t)t.keep;  // always < keep
+      v[i] = ld_or0(dr, u * 64 + lane, kept[i]);
+      xv[i] = kX ? ld_or0(xt, u * 64 + lane, kept[i]) : 0.0f;
     }
-    // all loads of the kept elements first, then the stores
-    float v[kTkE];
-    uint32_t pos[kTkE];
-    bool kept[kTkE];
 #pragma unroll
-    for (int u = 0; u < kTkE; ++u) {
-      pos[u] = run + (uint32_t)__popcll(m[u] & lt);
-      kept[u] = ((m[u] >> lane) & 1ull) && pos[u] < (uint32_t)t.keep;  // pos < keep always holds
-      v[u] = ld_or0(dr, (w0 + u) * 64 + lane, kept[u]);
-      run += (uint32_t)__popcll(m[u]);
-    }
-    float xv[kTkE];
-#pragma unroll
-    for (int u = 0; u < kTkE; ++u) xv[u] = kX ? ld_or0(xt, (w0 + u) * 64 + lane, kept[u]) : 0.0f;
-#pragma unroll
-    for (int u = 0; u < kTkE; ++u) {
-      const int w = w0 + u;
-      if (w >= nw) continue;
-      if (lane == 0) rr[w] = pos[u];  // lane 0: the kept count before this word
-      if (kept[u]) {
-        const int j = w * 64 + lane;
-        vr[pos[u]] = v[u];
+    for (int i = 0; i < kP; ++i) {
+      if (kept[i]) {
+        const int j = (u0 + i) * 64 + lane;
+        vr[pos[i]] = v[i];
         dr[j] = 0.0f;  // e = Delta - C(Delta) = 0 at a kept element
-        if (kX) xt[j] = xv[u] - v[u];
+        if (kX) xt[j] = xv[i] - v[i];
       }
     }
   }
@@ -584,7 +653,7 @@ __device__ __forceinline__ void tk_aggregate_words(
       st_nt(es + start + j, D);
       const uint32_t key = key_of(D);
       bad |= key >= kFiniteLimit;
-      atomicAdd(&h[Digit<1>::get(key)], 1u);
+      atomicAdd(&h[digit1(key)], 1u);
     } else {
       st_nt(x + start + j, dv[u] - mean);  // single-way: the mean itself comes back
     }
@@ -629,52 +698,34 @@ struct Launcher {
   const TkDev& tk;
   hipStream_t s;
 
-  template <int kPass>
-  hipError_t reduce_pick(int R, int row0) const {
-    const LaunchEvents ev;
-    if (tk.red_split > 1) {
-      SAEF_LAUNCH((k_tk_sum<kPass>), dim3((unsigned)(R * lay.L * tk.red_split)), dim3(kBlock), 0,
-                  s, lay, tk, row0);
-      const hipError_t err = hipGetLastError();
-      if (err != hipSuccess) return err;
-    }
-    SAEF_LAUNCH((k_tk_pick<kPass>), dim3((unsigned)(R * lay.L)), dim3(kBlock), 0, s, lay, tk,
-                row0);
-    return hipGetLastError();
-  }
-
-  // one histogram pass over R rows: 256-thread workgroups when there are
-  // several rows, 1024-thread ones for a single row (the server)
-  template <int kPass>
-  hipError_t hist(int R, int row0, const float* data) const {
-    const LaunchEvents ev;
-    const dim3 grid((unsigned)(tk.n_chunks * R));
-    if (R > 1)
-      SAEF_LAUNCH((k_tk_hist<kPass, SAEF_TK_HIST_THREADS>), grid, dim3(SAEF_TK_HIST_THREADS), 0, s,
-                  lay, tk, R, row0, data);
-    else
-      SAEF_LAUNCH((k_tk_hist<kPass, kBig>), grid, dim3(kBig), 0, s, lay, tk, R, row0, data);
-    return hipGetLastError();
-  }
-
-  // passes 2 and 3, ties, emit of R rows of `data` (pass 1 already done)
+  // everything after the first pass for R rows of `data` (rows row0..):
+  // pick, gather, select, apply, scan, emit.  The last kernel stamps the
+  // caller's stop event.
   hipError_t select_and_emit(int R, int row0, float* data, uint64_t* sel, uint32_t* rank,
                              float* vals, float* x, const LaunchEvents& last) const {
     const LaunchEvents ev;
-    hipError_t err = reduce_pick<1>(R, row0);
-    if (err != hipSuccess) return err;
-    if ((err = hist<2>(R, row0, data)) != hipSuccess) return err;
-    if ((err = reduce_pick<2>(R, row0)) != hipSuccess) return err;
-    if ((err = hist<3>(R, row0, data)) != hipSuccess) return err;
-    if ((err = reduce_pick<3>(R, row0)) != hipSuccess) return err;
-    SAEF_LAUNCH(k_tk_ties, dim3((unsigned)(R * lay.L)), dim3(kBig), 0, s, lay, tk, row0, data);
+    hipError_t err;
+    if (tk.red_split > 1) {
+      SAEF_LAUNCH(k_tk_sum, dim3((unsigned)(R * lay.L * tk.red_split)), dim3(kBlock), 0, s, lay,
+                  tk, row0);
+      if ((err = hipGetLastError()) != hipSuccess) return err;
+    }
+    const dim3 pairs((unsigned)(R * lay.L));
+    const dim3 chunks((unsigned)(tk.n_chunks * R));
+    SAEF_LAUNCH(k_tk_pick, pairs, dim3(kBlock), 0, s, lay, tk, row0);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    if (R > 1)
+      SAEF_LAUNCH((k_tk_gather<kBlock>), chunks, dim3(kBlock), 0, s, lay, tk, R, row0, data, sel);
+    else
+      SAEF_LAUNCH((k_tk_gather<kBig>), chunks, dim3(kBig), 0, s, lay, tk, R, row0, data, sel);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    SAEF_LAUNCH(k_tk_select, pairs, dim3(kBig), 0, s, lay, tk, row0);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    SAEF_LAUNCH(k_tk_apply, chunks, dim3(kBlock), 0, s, lay, tk, R, row0, sel);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    SAEF_LAUNCH(k_tk_scan, pairs, dim3(kBlock), 0, s, lay, tk, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     const dim3 tiles((unsigned)(per_wave_grid(lay) * R));
-    SAEF_LAUNCH(k_tk_emit1, tiles, dim3(kBlock), 0, s, lay, tk, R, row0, data, sel);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
-    SAEF_LAUNCH(k_tk_scan, dim3((unsigned)(R * lay.L)), dim3(kBlock), 0, s, lay, tk, row0);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
-    // the last kernel stamps the caller's stop event
     if (x != nullptr)
       hipExtLaunchKernelGGL((k_tk_emit2<true>), tiles, dim3(kBlock), 0, s, nullptr, last.stop, 0,
                             lay, tk, R, row0, data, sel, rank, vals, x);
