@@ -9,6 +9,7 @@
 
 #include "saef.h"
 #include "saef_internal.h"
+#include "saef_topk.h"
 
 using saef::DevLayout;
 using saef::TensorInfo;

@@ -27,7 +27,7 @@
 // The server runs the same steps on its one row (row k_max of the scratch)
 // after k_tk_aggregate has formed Delta = e_srv + mean of the K messages.
 #include "saef_device.h"
-#include "saef_internal.h"
+#include "saef_topk.h"
 
 namespace saef {
 namespace {
