@@ -240,3 +240,78 @@ def test_full_size_topk_resnet50():
                                np.ones(kl, bool), f"{tag} server values of {names[i]}")
         _log(f"topk resnet50: iteration {t} matches the oracle on the sampled tensors")
     assert gs.status() == 0
+
+
+def _check_topk_row(delta, sel_words, vals, kept_count, tag):
+    """Properties that define the Top-K of one vector, at any size: exactly
+    kept_count kept, every kept magnitude >= every dropped one, equal
+    magnitudes at the cut kept by lower index, the values in index order."""
+    n = delta.size
+    bits = np.unpackbits(sel_words.view(np.uint8), bitorder="little")[:n].astype(bool)
+    assert int(bits.sum()) == kept_count, (tag, int(bits.sum()), kept_count)
+    mag = np.abs(delta)
+    lo_kept = mag[bits].min()
+    if kept_count < n:
+        hi_drop = mag[~bits].max()
+        assert lo_kept >= hi_drop, (tag, lo_kept, hi_drop)
+        if lo_kept == hi_drop:
+            tie = mag == lo_kept
+            assert np.flatnonzero(tie & bits).max() < np.flatnonzero(tie & ~bits).min(), tag
+    assert np.array_equal(vals[:kept_count].view(np.uint32), delta[bits].view(np.uint32)), tag
+    return bits
+
+
+def test_full_size_topk_flat256m():
+    """Top-1% of one 2^28-element tensor (4096 histogram chunks: the
+    second reduction level), K = 8, iteration 0 of saef_topk_round, checked
+    against the defining properties of Top-K on every worker and on the
+    server, and the error / weight updates bit for bit."""
+    from tests.test_gpu_topk import TopkGpu
+    w = W.get("flat256m")
+    K = w.K
+    keep = W.topk_keep(w, 1)
+    k1 = int(keep[0])
+    _log(f"topk flat256m: K={K} d={w.d} keep={k1}")
+    g = W.gradients(w, 0)
+    x0 = W.initial_x(w)
+    gs = TopkGpu(w, keep, x0=x0)
+    gs.round(0, torch.from_numpy(g).cuda())
+    torch.cuda.synchronize()
+    assert gs.status() == 0
+    n = w.d
+    lr = np.float32(w.lr)
+    acc = np.zeros(n, np.float64)
+    for k in range(K):
+        # Delta = fma(lr, g, e) with e = +0: the exact product rounded once, and
+        # a zero product becomes +0 (+0 + -0 = +0)
+        delta = (np.float64(lr) * g[k, :n].astype(np.float64) + 0.0).astype(np.float32)
+        sel = gs.sel[k].cpu().numpy().view(np.uint64)
+        vals = gs.vals[k].cpu().numpy()
+        bits = _check_topk_row(delta, sel, vals, k1, f"worker {k}")
+        e = gs.e[k, :n].cpu().numpy()
+        want = np.where(bits, np.float32(0.0), delta)
+        bad = np.flatnonzero(e.view(np.uint32) != want.view(np.uint32))
+        assert bad.size == 0, (f"worker {k} error: {bad.size} differ, first {bad[:5].tolist()}, "
+                               f"got {e[bad[:5]].tolist()} want {want[bad[:5]].tolist()} "
+                               f"kept {bits[bad[:5]].tolist()}")
+        dense = np.zeros(n, np.float32)
+        dense[bits] = delta[bits]
+        acc += dense
+        del delta, sel, vals, bits, e, want, dense
+        _log(f"topk flat256m: worker {k} satisfies the Top-K properties")
+    mean = (acc / K).astype(np.float32)
+    del acc
+    D = (np.float32(0.0) + mean).astype(np.float32)  # e_srv = 0 at t = 0
+    bits = _check_topk_row(D, gs.srv_sel.cpu().numpy().view(np.uint64), gs.srv_vals.cpu().numpy(),
+                           k1, "server")
+    es = gs.e_srv[:n].cpu().numpy()
+    want_es = np.where(bits, np.float32(0.0), D)
+    bad = np.flatnonzero(es.view(np.uint32) != want_es.view(np.uint32))
+    assert bad.size == 0, (f"server error: {bad.size} differ, first {bad[:5].tolist()}, "
+                           f"got {es[bad[:5]].tolist()} want {want_es[bad[:5]].tolist()}")
+    x = gs.x[:n].cpu().numpy()
+    want_x = np.where(bits, (x0[:n] - D).astype(np.float32), x0[:n])
+    bad = np.flatnonzero(x.view(np.uint32) != want_x.view(np.uint32))
+    assert bad.size == 0, (f"weights: {bad.size} differ, first {bad[:5].tolist()}, "
+                           f"got {x[bad[:5]].tolist()} want {want_x[bad[:5]].tolist()}")
+    _log("topk flat256m: server and weights satisfy the Top-K properties")
