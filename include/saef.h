@@ -1,20 +1,23 @@
 /*
  * saef.h -- C ABI of the MI355X (gfx950) library for the per-iteration hot
- * path of Step-Ahead Error Feedback (SAEF) with the scaled sign compressor.
+ * path of Step-Ahead Error Feedback (SAEF).
  *
  * The method (Xu, Huo, Huang, "Step-Ahead Error Feedback for Distributed
- * Training with Compressed Gradient", AAAI 2021):
- *   C(v) = (||v||_1 / d) sign(v)                                   Eq. (2)
- * applied layer-wise (one scale per parameter tensor, d = tensor size n_l),
- * inside Algorithm 1 (SAEF branch) with momentum constant 0:
+ * Training with Compressed Gradient", AAAI 2021), Algorithm 1:
  *   if (t+1) mod p == 0:  e^(k) <- (1/K) sum_k e^(k)          error averaging
  *   x^(k)_{t+1/2} = x_t - e^(k)                                step ahead
+ *     (local error feedback, the EF branch: the gradient is taken at x_t)
  *   [gradient g^(k) computed at x^(k)_{t+1/2} by the caller]
- *   Delta^(k) = e^(k) + lr g^(k);  e^(k) <- Delta^(k) - C(Delta^(k))   worker
+ *   m^(k) <- mu m^(k) + g^(k)                                  (mu = 0: m = g)
+ *   Delta^(k) = e^(k) + lr m^(k);  e^(k) <- Delta^(k) - C(Delta^(k))   worker
  *   Delta = e + (1/K) sum_k C(Delta^(k));  e <- Delta - C(Delta)       server
  *   x <- x - C(Delta)                                          re-update
- * The K workers are simulated on one GPU: worker k's vectors are rows of
- * (K, d_pad) device arrays and "send"/"broadcast" are device buffers.
+ * with the scaled sign compressor
+ *   C(v) = (||v||_1 / d) sign(v)                                   Eq. (2)
+ * or layer-wise Top-K (the saef_topk_* calls), both applied per parameter
+ * tensor (d = tensor size n_l).  The K workers are simulated on one GPU:
+ * worker k's vectors are rows of (K, d_pad) device arrays and
+ * "send"/"broadcast" are device buffers.
  *
  * ---------------------------------------------------------------- numbers
  * Every fp32 result is defined exactly, so results do not depend on the

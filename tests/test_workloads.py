@@ -1,4 +1,6 @@
 """The synthetic workloads have the shapes of the models they stand for."""
+import os
+
 import numpy as np
 import pytest
 
@@ -52,3 +54,29 @@ def test_byte_model():
     assert W.algorithmic_bytes_per_param(4) == 101.125
     assert W.algorithmic_bytes_per_param(16) == 344.125
     assert W.algorithmic_bytes_per_param(8, mode=0) == 12 + 20.25 * 8
+
+
+def test_bench_refuses_several_gpus():
+    """bench.py measures one GPU: --gpus N > 1 exits with a message (no GPU
+    is touched before the check)."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    res = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                         capture_output=True, text=True, timeout=120)
+    assert res.returncode == 2
+    assert "one GPU" in res.stderr
+
+
+def test_topk_keep_and_byte_models():
+    from paper_2008_05823_amd import workloads as W
+    w = W.custom([1, 99, 100, 101, 12345], K=2)
+    assert W.topk_keep(w, 1).tolist() == [1, 1, 1, 2, 124]
+    assert W.topk_keep(w, 100).tolist() == [1, 99, 100, 101, 12345]
+    assert W.topk_keep(w, 5).tolist() == [1, 5, 5, 6, 618]
+    # sign path, K = 8, double-way: 20.125 + 20.25 K
+    assert W.algorithmic_bytes_per_param(8) == 20.125 + 20.25 * 8
+    assert W.algorithmic_bytes_per_param(8, averaging=True) == 20.125 + 20.25 * 8 + 32
+    assert W.algorithmic_bytes_per_param(8, momentum=True) == 20.125 + 28.25 * 8
+    tk = W.topk_algorithmic_bytes_per_param(8, 0.01)
+    assert abs(tk["worker"] - 8 * (12 + 3 / 16 + 0.04)) < 1e-12
