@@ -129,7 +129,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="resnet50",
                     help="flat64k | resnet56 | resnet50 | bert_base | flat256m")
-    ap.add_argument("--cpu-rounds", type=int, default=1,
+    ap.add_argument("--cpu-rounds", type=int, default=2,
                     help="iterations of the CPU oracle baseline (0 = skip)")
     ap.add_argument("--no-probe", action="store_true", help="skip the copy-bandwidth probe")
     ap.add_argument("--momentum", type=float, default=None,
