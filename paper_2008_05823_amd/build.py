@@ -50,5 +50,26 @@ def build(out: str = LIB, verbose: bool = False, defines=()) -> str:
     return out
 
 
+CLIENT_SRC = os.path.join(ROOT, "tests", "c", "abi_client.cpp")
+CLIENT = os.path.join(ROOT, "tests", "c", "abi_client")
+
+
+def build_client(out: str = CLIENT, lib: str = LIB) -> str:
+    """Compile the C/C++ client of the C ABI (tests/c/abi_client.cpp) against
+    the built library; it finds the library through a relative run path."""
+    libdir = os.path.dirname(lib)
+    rel = os.path.relpath(libdir, os.path.dirname(out))
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O2", "-std=c++17", "-Wall", "-Werror",
+           "-I", os.path.join(ROOT, "include"), CLIENT_SRC, "-L", libdir,
+           f"-l:{os.path.basename(lib)}", f"-Wl,-rpath,$ORIGIN/{rel}", "-o", out + ".tmp"]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stderr)
+        raise RuntimeError(f"hipcc failed ({res.returncode})")
+    os.replace(out + ".tmp", out)
+    return out
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_client())
