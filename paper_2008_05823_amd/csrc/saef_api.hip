@@ -74,9 +74,14 @@ bool overlap(const void* p, size_t bytes, const void* q, size_t qbytes) {
   return a < b + qbytes && b < a + bytes;
 }
 
+// Largest grid (workgroups in x) a launch may use.
+constexpr int64_t kMaxGrid = 2147483647;
+
 int check_common(const saef_layout* lay, int32_t K) {
   if (lay == nullptr) return SAEF_EINVAL;
   if (K < 1 || K > lay->k_max) return SAEF_EINVAL;
+  // the per-(tile, worker) grids must fit the launch limit
+  if ((lay->dev.n_tiles + 8) * (int64_t)K > kMaxGrid) return SAEF_EINVAL;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess) return SAEF_EHIP;
   if (dev != lay->device) return SAEF_EINVAL;
@@ -599,6 +604,10 @@ int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk**
       chunks.push_back(saef::TkChunk{layout->off[l] + c * saef::kTkChunk, l,
                                      (int32_t)std::min<int64_t>(saef::kTkChunk,
                                                                 n - c * saef::kTkChunk)});
+  }
+  if ((int64_t)chunks.size() * (layout->k_max + 1) > kMaxGrid) {
+    free_topk(p);
+    return SAEF_EINVAL;
   }
   const int32_t red_split = max_chunks > saef::kTkRedChunks
                                 ? (max_chunks + saef::kTkRedChunks - 1) / saef::kTkRedChunks
