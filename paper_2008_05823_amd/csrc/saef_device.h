@@ -22,6 +22,23 @@ __device__ __forceinline__ int wave_id() {
 __device__ __forceinline__ float ld_nt(const float* p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ void st_nt(float* p, float v) { __builtin_nontemporal_store(v, p); }
 
+// Per lane: bit `lane` of the 64-bit mask ? if1 : if0, in one VALU op
+// (v_cndmask with the mask as its lane condition).  The mask must be the
+// same in every lane (a sign word read at a wave-uniform address); it is
+// moved to scalar registers explicitly, which costs nothing when it already
+// is in one.
+__device__ __forceinline__ uint32_t sel_by_bit(u64 mask, uint32_t if1, uint32_t if0) {
+  const uint32_t mlo = __builtin_amdgcn_readfirstlane((uint32_t)mask);
+  const uint32_t mhi = __builtin_amdgcn_readfirstlane((uint32_t)(mask >> 32));
+  const u64 m = ((u64)mhi << 32) | mlo;
+  uint32_t r;
+  asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(if0), "v"(if1), "s"(m));
+  return r;
+}
+__device__ __forceinline__ float sel_by_bit(u64 mask, float if1, float if0) {
+  return __uint_as_float(sel_by_bit(mask, __float_as_uint(if1), __float_as_uint(if0)));
+}
+
 // (1/K) * acc, binary64; inv_k is 1/K when K is a power of two (exact), else 0.
 __device__ __forceinline__ double mean_of(double acc, double inv_k, int K) {
   return (inv_k != 0.0) ? acc * inv_k : acc / (double)K;

@@ -36,22 +36,6 @@ constexpr uint32_t kAbsLimitBits = 0x49000000u;  // bit pattern of 2^19
 constexpr int kU = 4;     // words per wave per pass in the per-(tile, worker) kernels
 constexpr int kWPW = 16;  // words per wave per pass in the one-wave-per-tile kernels
 
-// Per lane: bit `lane` of the 64-bit mask ? if1 : if0, in one VALU op
-// (v_cndmask with the mask as its lane condition).  The mask must be the
-// same in every lane (a sign word read at a wave-uniform address); it is
-// moved to scalar registers explicitly, which costs nothing when it already
-// is in one.
-__device__ __forceinline__ uint32_t sel_by_bit(u64 mask, uint32_t if1, uint32_t if0) {
-  const uint32_t mlo = __builtin_amdgcn_readfirstlane((uint32_t)mask);
-  const uint32_t mhi = __builtin_amdgcn_readfirstlane((uint32_t)(mask >> 32));
-  const u64 m = ((u64)mhi << 32) | mlo;
-  uint32_t r;
-  asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(if0), "v"(if1), "s"(m));
-  return r;
-}
-__device__ __forceinline__ float sel_by_bit(u64 mask, float if1, float if0) {
-  return __uint_as_float(sel_by_bit(mask, __float_as_uint(if1), __float_as_uint(if0)));
-}
 // The compression correction C(v)_i = bit ? scale : -scale.
 __device__ __forceinline__ float corr(u64 word, float s) { return sel_by_bit(word, s, -s); }
 

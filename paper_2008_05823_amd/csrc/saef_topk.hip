@@ -54,7 +54,10 @@ __device__ __forceinline__ float ld_or0(const float* p, int64_t j, bool ok) {
 __device__ __forceinline__ float ld_pass_or0(const float* p, int64_t j, bool ok) {
   return SAEF_TK_NT ? ld_nt_or0(p, j, ok) : ld_or0(p, j, ok);
 }
-constexpr int kAggK = 4;                        // workers whose messages are read together
+// Word 3 of a raw buffer descriptor on gfx9 parts (32-bit data format, no
+// swizzle, no index stride).  A load through a raw buffer resource of n
+// bytes returns 0 for a byte offset at or past n, without touching memory.
+constexpr int kBufWord3 = 0x00020000;
 
 __device__ __forceinline__ uint32_t key_of(float v) { return __float_as_uint(v) & 0x7FFFFFFFu; }
 
@@ -582,109 +585,125 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit2(DevLayout lay, TkDev tk, in
 }
 
 // ------------------------------------------------------------------ server aggregation
-// kTkU words of a chunk: mean of the K decoded messages (binary64, worker
-// order, /K, fp32); mode 1: Delta = e_srv + mean stored into e_srv and its
-// pass-1 histogram; mode 0: x <- x - mean.
-template <int kMode, bool kAvg, bool kFull>
-__device__ __forceinline__ void tk_aggregate_words(
-    const DevLayout& lay, const TkDev& tk, int K, double inv_k, int64_t voff, uint32_t keep,
-    int64_t start,
-    int w0, int nw, int count, const uint64_t* __restrict__ sel,
-    const uint32_t* __restrict__ rank, const float* __restrict__ vals, float* __restrict__ avg,
-    float* __restrict__ es, float* __restrict__ x, uint32_t* h, bool& bad) {
-  const int lane = lane_id();
-  const int64_t W = lay.d_pad >> 6;
-  const int64_t gw0 = (start >> 6) + w0;
-  const u64 lt = lanemask_lt(lane);
-  float dv[kTkU];
-#pragma unroll
-  for (int u = 0; u < kTkU; ++u) {
-    const int j = (w0 + u) * 64 + lane;
-    const bool ok = kFull || ((w0 + u < nw) && j < count);
-    dv[u] = ld_nt_or0((kMode == 1 ? es : x) + start, j, ok);
-  }
-  double acc[kTkU];
-#pragma unroll
-  for (int u = 0; u < kTkU; ++u) acc[u] = 0.0;
-  for (int k0 = 0; k0 < K; k0 += kAggK) {
-    // the words and ranks of kAggK workers, then all their value gathers
-    u64 m[kAggK][kTkU];
-    uint32_t rb[kAggK][kTkU];
-#pragma unroll
-    for (int c = 0; c < kAggK; ++c) {
-      const bool kin = k0 + c < K;
-      const int64_t row = kin ? (int64_t)(k0 + c) * W : 0;  // absent workers read worker 0
-#pragma unroll
-      for (int u = 0; u < kTkU; ++u) {
-        const bool w_ok = kin && (kFull || w0 + u < nw);
-        // always issued at a word of the chunk that exists, masked after
-        const int64_t at = gw0 + row + ((kFull || w0 + u < nw) ? u : 0);
-        const u64 mw = sel[at];
-        const uint32_t rw = rank[at];
-        m[c][u] = w_ok ? mw : 0ull;
-        rb[c][u] = w_ok ? rw : 0u;
-      }
-    }
-    float cv[kAggK][kTkU];
-#pragma unroll
-    for (int c = 0; c < kAggK; ++c) {
-      const int kk = (k0 + c < K) ? k0 + c : 0;
-      const float* vk = vals + (int64_t)kk * tk.total_keep + voff;
-#pragma unroll
-      for (int u = 0; u < kTkU; ++u) {
-        const uint32_t pos = rb[c][u] + (uint32_t)__popcll(m[c][u] & lt);
-        cv[c][u] = ld_or0(vk, pos, ((m[c][u] >> lane) & 1ull) && pos < keep);
-      }
-    }
-#pragma unroll
-    for (int c = 0; c < kAggK; ++c)
-#pragma unroll
-      for (int u = 0; u < kTkU; ++u) acc[u] += (double)cv[c][u];  // worker order; absent: +0
-  }
-#pragma unroll
-  for (int u = 0; u < kTkU; ++u) {
-    const int j = (w0 + u) * 64 + lane;
-    const bool ok = kFull || ((w0 + u < nw) && j < count);
-    if (!ok) continue;
-    const float mean = (float)mean_of(acc[u], inv_k, K);
-    if (kAvg) avg[start + j] = mean;
-    if (kMode == 1) {
-      const float D = dv[u] + mean;  // Delta_{t+1} = e_t + (1/K) sum_k C(Delta^(k))
-      st_nt(es + start + j, D);
-      const uint32_t key = key_of(D);
-      bad |= key >= kFiniteLimit;
-      atomicAdd(&h[digit1(key)], 1u);
-    } else {
-      st_nt(x + start + j, dv[u] - mean);  // single-way: the mean itself comes back
-    }
-  }
+// A wave takes U selection words (U x 64 elements) of a chunk per pass and
+// the workers in batches of kWave / U: in a batch, lane q loads selection word
+// q % U of worker q / U together with its rank word (one vector load each),
+// and the value gathers of the whole batch are issued at once, their masks and
+// ranks read out of those lanes (v_readlane).  The words of the next step are
+// loaded before the values of the current one are waited for, so one step
+// costs one memory round trip.  The K values of an element are added in
+// binary64 in worker order (/K, fp32); mode 1: Delta = e_srv + mean stored into
+// e_srv and its pass-1 histogram; mode 0: x <- x - mean.
+template <int U>
+struct AggStep {
+  uint32_t lo, hi, rk4;  // this lane's (worker, word) pair: selection word, 4 x rank word
+};
+
+template <int U>
+__device__ __forceinline__ AggStep<U> agg_words(const uint64_t* __restrict__ sel,
+                                                const uint32_t* __restrict__ rank, int64_t W,
+                                                int64_t gw, int K, int nw, int w0, int k0,
+                                                int lane) {
+  const int kq = k0 + lane / U, uq = lane % U;
+  const bool ok = kq < K && w0 + uq < nw;
+  // always issued at a word that exists (the chunk's first word of worker 0)
+  const int64_t at = ok ? (int64_t)kq * W + gw + w0 + uq : gw;
+  const u64 s = sel[at];
+  const uint32_t r = rank[at];
+  AggStep<U> a;
+  a.lo = ok ? (uint32_t)s : 0u;
+  a.hi = ok ? (uint32_t)(s >> 32) : 0u;
+  a.rk4 = ok ? r * 4u : 0u;
+  return a;
 }
 
-// Grid: n_chunks workgroups.
-template <int kMode, bool kAvg>
+template <int kMode, bool kAvg, int U>
 __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, int K,
-                                                         double inv_k,
-                                                         const uint64_t* __restrict__ sel,
-                                                         const uint32_t* __restrict__ rank,
-                                                         const float* __restrict__ vals,
-                                                         float* __restrict__ avg,
-                                                         float* __restrict__ es,
-                                                         float* __restrict__ x) {
+                                                       double inv_k,
+                                                       const uint64_t* __restrict__ sel,
+                                                       const uint32_t* __restrict__ rank,
+                                                       const float* __restrict__ vals,
+                                                       float* __restrict__ avg,
+                                                       float* __restrict__ es,
+                                                       float* __restrict__ x) {
+  constexpr int kB = kWave / U;  // workers per batch
+  static_assert(kB * U == kWave, "one (worker, word) pair per lane");
   __shared__ uint32_t h[kTkBins];
   const int64_t ci = blockIdx.x;
   const TkChunk c = tk.chunks[ci];
   const int64_t voff = tk.tens[c.l].voff;
   const uint32_t keep = (uint32_t)tk.tens[c.l].keep;
   if (kMode == 1) hist_clear<kTkBins>(h);
+  const int lane = lane_id();
   const int nw = (c.count + 63) >> 6;
+  const int64_t W = lay.d_pad >> 6;
+  const int64_t gw = c.start >> 6;
+  float* dr = (kMode == 1 ? es : x) + c.start;
+  const int stride = (kBig / kWave) * U;
   bool bad = false;
-  for (int w0 = wave_id() * kTkU; w0 < nw; w0 += (kBig / kWave) * kTkU) {
-    if ((w0 + kTkU) * 64 <= c.count)
-      tk_aggregate_words<kMode, kAvg, true>(lay, tk, K, inv_k, voff, keep, c.start, w0, nw, c.count,
-                                            sel, rank, vals, avg, es, x, h, bad);
-    else
-      tk_aggregate_words<kMode, kAvg, false>(lay, tk, K, inv_k, voff, keep, c.start, w0, nw, c.count,
-                                             sel, rank, vals, avg, es, x, h, bad);
+  // (past the chunk's last word, agg_words issues a load at a word that
+  // exists and returns empty words: no branch, so no early wait)
+  AggStep<U> cur = agg_words<U>(sel, rank, W, gw, K, nw, wave_id() * U, 0, lane);
+  for (int w0 = wave_id() * U; w0 < nw; w0 += stride) {
+    // e_srv (mode 1) or x (mode 0) of the pass; elements past the chunk are
+    // loaded at its first element and never stored
+    float dv[U];
+    double acc[U];
+#pragma unroll
+    for (int i = 0; i < U; ++i) {
+      const int j = (w0 + i) * 64 + lane;
+      dv[i] = __builtin_nontemporal_load(dr + ((w0 + i < nw && j < c.count) ? j : 0));
+      acc[i] = 0.0;
+    }
+    for (int k0 = 0; k0 < K; k0 += kB) {
+      // the next step's words go out before this step's values are waited for
+      const bool last_b = k0 + kB >= K;
+      const int nw0 = last_b ? w0 + stride : w0;
+      const AggStep<U> nxt = agg_words<U>(sel, rank, W, gw, K, nw, nw0, last_b ? 0 : k0 + kB, lane);
+      // This step's values, read through a buffer resource over the worker's
+      // k_l values (a lane whose bit is clear reads past the end and gets 0);
+      // the loads of all pairs go out before the first one is used.
+      float cv[kB][U];
+#pragma unroll
+      for (int kk = 0; kk < kB; ++kk) {
+        const int kidx = min(k0 + kk, K - 1);  // absent workers have empty words
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(vals + (int64_t)kidx * tk.total_keep + voff), 0, (int)(keep * 4u),
+            kBufWord3);
+#pragma unroll
+        for (int i = 0; i < U; ++i) {
+          const int q = kk * U + i;
+          const uint32_t mlo = __builtin_amdgcn_readlane(cur.lo, q);
+          const uint32_t mhi = __builtin_amdgcn_readlane(cur.hi, q);
+          const uint32_t r4 = __builtin_amdgcn_readlane(cur.rk4, q);
+          // rank of the lane's element among the word's kept ones, in bytes
+          const uint32_t below = __builtin_amdgcn_mbcnt_hi(mhi, __builtin_amdgcn_mbcnt_lo(mlo, 0u));
+          const uint32_t off = sel_by_bit(((u64)mhi << 32) | mlo, below * 4u + r4, 0x80000000u);
+          cv[kk][i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0));
+        }
+      }
+#pragma unroll
+      for (int kk = 0; kk < kB; ++kk)
+#pragma unroll
+        for (int i = 0; i < U; ++i) acc[i] += (double)cv[kk][i];  // worker order; absent: +0
+      cur = nxt;
+    }
+#pragma unroll
+    for (int i = 0; i < U; ++i) {
+      const int j = (w0 + i) * 64 + lane;
+      if (!(w0 + i < nw && j < c.count)) continue;
+      const float mean = (float)mean_of(acc[i], inv_k, K);
+      if (kAvg) avg[c.start + j] = mean;
+      if (kMode == 1) {
+        const float D = dv[i] + mean;  // Delta_{t+1} = e_t + (1/K) sum_k C(Delta^(k))
+        st_nt(dr + j, D);
+        const uint32_t key = key_of(D);
+        bad |= key >= kFiniteLimit;
+        atomicAdd(&h[digit1(key)], 1u);
+      } else {
+        st_nt(dr + j, dv[i] - mean);  // single-way: the mean itself comes back
+      }
+    }
   }
   if (kMode == 1) {
     if (__ballot(bad) != 0 && lane_id() == 0) atomicOr(lay.status, kStatusRange);
@@ -763,14 +782,20 @@ hipError_t launch_topk_aggregate(const DevLayout& lay, const TkDev& tk, int K, i
   const dim3 grid((unsigned)tk.n_chunks);
   const double ik = inv_pow2(K);
   hipEvent_t stop0 = mode == 1 ? nullptr : ev.stop;
-#define SAEF_TKA(M, A)                                                                          \
-  hipExtLaunchKernelGGL((k_tk_aggregate<M, A>), grid, dim3(kBig), 0, s, ev.start, stop0, 0, \
+#define SAEF_TKA(M, A, U)                                                                       \
+  hipExtLaunchKernelGGL((k_tk_aggregate<M, A, U>), grid, dim3(kBig), 0, s, ev.start, stop0, 0, \
                         lay, tk, K, ik, sel, rank, vals, avg, e_srv, x)
+#define SAEF_TKA_U(M, A)                                 \
+  do {                                                   \
+    if (K <= 8) SAEF_TKA(M, A, 8);                       \
+    else SAEF_TKA(M, A, 4);                              \
+  } while (0)
   if (mode == 1) {
-    if (avg != nullptr) SAEF_TKA(1, true); else SAEF_TKA(1, false);
+    if (avg != nullptr) SAEF_TKA_U(1, true); else SAEF_TKA_U(1, false);
   } else {
-    if (avg != nullptr) SAEF_TKA(0, true); else SAEF_TKA(0, false);
+    if (avg != nullptr) SAEF_TKA_U(0, true); else SAEF_TKA_U(0, false);
   }
+#undef SAEF_TKA_U
 #undef SAEF_TKA
   const hipError_t err = hipGetLastError();
   if (err != hipSuccess || mode != 1) return err;

@@ -238,13 +238,15 @@ def test_topk_compress_parity(name, momentum):
     assert gs.status() == 0
 
 
+@pytest.mark.parametrize("K", [3, 5, 12, 17])
 @pytest.mark.parametrize("mode", [1, 0], ids=["dc", "sc"])
-def test_topk_aggregate_parity(mode):
-    """Server step on oracle-made messages (K = 5: the /K is not a power of two)."""
-    K = 5
+def test_topk_aggregate_parity(mode, K):
+    """Server step on oracle-made messages.  The server kernel reads the
+    workers in batches of 8 (K <= 8) or 16: K = 3 and 12 leave part of a batch
+    empty, K = 17 takes two batches; /K is not a power of two for 3, 5, 12, 17."""
     w = W.custom(ADVERSARIAL + [200_000], K=K, scale_range=(1e-3, 1.0), seed=321, mode=mode)
     keep = W.topk_keep(w, 5)
-    _case(f"topk aggregate mode={mode}")
+    _case(f"topk aggregate mode={mode} K={K}")
     off, n, d_pad = w.layout()
     msk = W.tensor_mask(w)
     orc = TopkOracle(w, keep)
