@@ -35,6 +35,7 @@ namespace {
 constexpr uint32_t kFiniteLimit = 0x7F800000u;  // keys >= this are Inf or NaN
 constexpr int kTkU = 4;                         // words per wave per pass (first pass, server)
 constexpr int kTkH = 16;                        // words per wave per pass (gather)
+static_assert(kTkH <= kWave, "one selection word per lane in a gather pass");
 constexpr int kBig = 1024;                      // threads of the single-row (server) kernels
 #ifndef SAEF_TK_NT
 #define SAEF_TK_NT 1
@@ -334,6 +335,7 @@ __global__ __launch_bounds__(kThreads) void k_tk_gather(DevLayout lay, TkDev tk,
       v[u] = ld_pass_or0(dr, j, w0 + u < nw && j < c.count);
     }
     u64 cm[kTkH];
+    u64 myw = 0;  // lane u < kTkH: selection word u of the pass
     uint32_t ncand = 0;
 #pragma unroll
     for (int u = 0; u < kTkH; ++u) {
@@ -341,10 +343,12 @@ __global__ __launch_bounds__(kThreads) void k_tk_gather(DevLayout lay, TkDev tk,
       const bool ok = w0 + u < nw && j < c.count;
       const uint32_t hi = digit1(key_of(v[u]));
       const u64 word = __ballot(ok && hi > b1);
-      if (lane == 0 && w0 + u < nw) sr[w0 + u] = word;
+      if (lane == u) myw = word;
       cm[u] = __ballot(ok && hi == b1);
       ncand += (uint32_t)__popcll(cm[u]);
     }
+    // the pass's words in one store (a single-lane store per word costs more)
+    if (lane < kTkH && w0 + lane < nw) sr[w0 + lane] = myw;
     if (ncand != 0) {  // uniform over the wave
       uint32_t base = 0;
       if (lane == 0) base = atomicAdd(&s_next, ncand);
@@ -513,21 +517,46 @@ __global__ __launch_bounds__(kBlock) void k_tk_scan(DevLayout lay, TkDev tk, int
   }
 }
 
+// The position of the r-th set bit of w (r counted from 0, r < popcount(w)):
+// the 32-bit half that holds it, then five halving steps.
+__device__ __forceinline__ int nth_set_bit(u64 w, uint32_t r) {
+  uint32_t x = (uint32_t)w;
+  int pos = 0;
+  const uint32_t c_lo = (uint32_t)__popc(x);
+  if (r >= c_lo) {
+    r -= c_lo;
+    x = (uint32_t)(w >> 32);
+    pos = 32;
+  }
+#pragma unroll
+  for (int s = 16; s >= 1; s >>= 1) {
+    const uint32_t c = (uint32_t)__popc(x & ((1u << s) - 1u));
+    if (r >= c) {
+      r -= c;
+      x >>= s;
+      pos += s;
+    }
+  }
+  return pos;
+}
+
 // Grid: per_wave_grid(lay) * R workgroups; wave w of workgroup b owns tile
 // 4 (b / R) + w of row b % R.  Rank words, the kept values in index order,
 // the kept elements of data set to 0; kX (server): x <- x - Delta at the
-// kept elements (C(Delta) is zero elsewhere).  One pass per tile: lane j
-// loads selection word j of the tile, a wave scan of the word counts gives
-// every rank word, then the loads of all kept elements go out together.
+// kept elements (C(Delta) is zero elsewhere).  Lane j loads selection word j
+// of the tile and a wave scan of the word counts gives every rank word; then
+// lane i takes the tile's kept elements i, i + 64, ...: its word by a binary
+// search over the scan, its bit by nth_set_bit, so the work follows the kept
+// count, not the tile size.
 template <bool kX>
-__global__ __launch_bounds__(kBlock) void k_tk_emit2(DevLayout lay, TkDev tk, int R, int row0,
-                                                     float* __restrict__ data,
-                                                     const uint64_t* __restrict__ sel,
-                                                     uint32_t* __restrict__ rank,
-                                                     float* __restrict__ vals,
-                                                     float* __restrict__ x) {
+__global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, int R, int row0,
+                                                    float* __restrict__ data,
+                                                    const uint64_t* __restrict__ sel,
+                                                    uint32_t* __restrict__ rank,
+                                                    float* __restrict__ vals,
+                                                    float* __restrict__ x) {
   constexpr int kTileWords = kTileElems / 64;
-  static_assert(kTileWords <= kWave, "one selection word per lane");
+  static_assert(kTileWords == 32, "five halving steps find a word of the tile");
   const int r = (int)(blockIdx.x % (unsigned)R);
   const int64_t ti = (int64_t)(blockIdx.x / (unsigned)R) * kWaves + wave_id();
   if (ti >= lay.n_tiles) return;
@@ -542,7 +571,7 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit2(DevLayout lay, TkDev tk, in
   float* vr = vals + (int64_t)r * tk.total_keep + t.voff;
   float* xt = kX ? x + tile.start : nullptr;
   const uint32_t base = tk.tile_cnt[(int64_t)(row0 + r) * lay.n_tiles + ti];
-  // lane j: word j of the tile, its kept count and the exclusive prefix
+  // lane j: word j of the tile, its kept count and the inclusive prefix
   const u64 my = sr[lane < nw ? lane : 0];
   const u64 mine = lane < nw ? my : 0ull;
   const uint32_t c = (uint32_t)__popcll(mine);
@@ -552,34 +581,27 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit2(DevLayout lay, TkDev tk, in
     const uint32_t y = __shfl_up(incl, off);
     if (lane >= off) incl += y;
   }
-  const uint32_t my_rank = base + incl - c;
-  if (lane < nw) rr[lane] = my_rank;
-  const u64 lt = lanemask_lt(lane);
+  const uint32_t excl = incl - c;
+  if (lane < nw) rr[lane] = base + excl;
+  const uint32_t total = (uint32_t)__shfl(incl, kWave - 1);  // kept in the tile
   const uint32_t lo = (uint32_t)mine, hi = (uint32_t)(mine >> 32);
-  // words per pass: the server also loads x, so it takes two passes
-  constexpr int kP = kX ? kTileWords / 2 : kTileWords;
+  for (uint32_t i0 = 0; i0 < total; i0 += kWave) {
+    const uint32_t i = i0 + (uint32_t)lane;  // the i-th kept element of the tile
+    // its word: the number of words whose inclusive count is <= i (words past
+    // nw count all of the tile, so the search stays below kTileWords)
+    int u = 0;
 #pragma unroll
-  for (int u0 = 0; u0 < kTileWords; u0 += kP) {
-    float v[kP], xv[kP];
-    uint32_t pos[kP];
-    bool kept[kP];
-#pragma unroll
-    for (int i = 0; i < kP; ++i) {
-      const int u = u0 + i;
-      const u64 m = ((u64)(uint32_t)__shfl(hi, u) << 32) | (uint32_t)__shfl(lo, u);
-      pos[i] = (uint32_t)__shfl(my_rank, u) + (uint32_t)__popcll(m & lt);
-      kept[i] = u < nw && ((m >> lane) & 1ull) && pos[i] < (uint32_t)t.keep;  // always < keep
-      v[i] = ld_or0(dr, u * 64 + lane, kept[i]);
-      xv[i] = kX ? ld_or0(xt, u * 64 + lane, kept[i]) : 0.0f;
-    }
-#pragma unroll
-    for (int i = 0; i < kP; ++i) {
-      if (kept[i]) {
-        const int j = (u0 + i) * 64 + lane;
-        vr[pos[i]] = v[i];
-        dr[j] = 0.0f;  // e = Delta - C(Delta) = 0 at a kept element
-        if (kX) xt[j] = xv[i] - v[i];
-      }
+    for (int step = kTileWords / 2; step >= 1; step >>= 1)
+      if ((uint32_t)__shfl(incl, u + step - 1) <= i) u += step;
+    const uint32_t wlo = (uint32_t)__shfl(lo, u), whi = (uint32_t)__shfl(hi, u);
+    const uint32_t wex = (uint32_t)__shfl(excl, u);
+    const int j = u * 64 + nth_set_bit(((u64)whi << 32) | wlo, i - wex);
+    const uint32_t pos = base + i;
+    if (i < total && j < tile.count && pos < (uint32_t)t.keep) {  // the last two always hold
+      const float v = dr[j];
+      vr[pos] = v;
+      dr[j] = 0.0f;  // e = Delta - C(Delta) = 0 at a kept element
+      if (kX) xt[j] -= v;
     }
   }
 }
@@ -746,10 +768,10 @@ struct Launcher {
     if ((err = hipGetLastError()) != hipSuccess) return err;
     const dim3 tiles((unsigned)(per_wave_grid(lay) * R));
     if (x != nullptr)
-      hipExtLaunchKernelGGL((k_tk_emit2<true>), tiles, dim3(kBlock), 0, s, nullptr, last.stop, 0,
+      hipExtLaunchKernelGGL((k_tk_emit<true>), tiles, dim3(kBlock), 0, s, nullptr, last.stop, 0,
                             lay, tk, R, row0, data, sel, rank, vals, x);
     else
-      hipExtLaunchKernelGGL((k_tk_emit2<false>), tiles, dim3(kBlock), 0, s, nullptr, last.stop, 0,
+      hipExtLaunchKernelGGL((k_tk_emit<false>), tiles, dim3(kBlock), 0, s, nullptr, last.stop, 0,
                             lay, tk, R, row0, data, sel, rank, vals, x);
     return hipGetLastError();
   }
