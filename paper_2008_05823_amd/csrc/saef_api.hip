@@ -21,6 +21,7 @@ struct saef_layout {
   int32_t k_max = 0;
   int64_t d_pad = 0;
   std::vector<int64_t> off, n;
+  std::vector<TensorInfo> tensors;  // host copy of the tensor table (tiles per tensor)
   DevLayout dev{};
   void* mem_tiles = nullptr;
   void* mem_tensors = nullptr;
@@ -42,8 +43,12 @@ struct saef_topk {
   saef::TkDev dev{};
   void* mem_chunks = nullptr;
   void* mem_tens = nullptr;
-  void* mem_hist = nullptr;
-  void* mem_hist2 = nullptr;
+  void* mem_groups = nullptr;
+  void* mem_sgroups = nullptr;
+  void* mem_thist = nullptr;
+  void* mem_ghist = nullptr;
+  void* mem_sghist = nullptr;
+  void* mem_goff = nullptr;
   void* mem_sel = nullptr;
   void* mem_tile_cnt = nullptr;
   void* mem_cand = nullptr;
@@ -135,14 +140,10 @@ void free_layout(saef_layout* l) {
 
 void free_topk(saef_topk* p) {
   if (p == nullptr) return;
-  (void)hipFree(p->mem_chunks);
-  (void)hipFree(p->mem_tens);
-  (void)hipFree(p->mem_hist);
-  (void)hipFree(p->mem_hist2);
-  (void)hipFree(p->mem_sel);
-  (void)hipFree(p->mem_tile_cnt);
-  (void)hipFree(p->mem_cand);
-  (void)hipFree(p->mem_cand_off);
+  for (void* q : {p->mem_chunks, p->mem_tens, p->mem_groups, p->mem_sgroups, p->mem_thist,
+                  p->mem_ghist, p->mem_sghist, p->mem_goff, p->mem_sel, p->mem_tile_cnt,
+                  p->mem_cand, p->mem_cand_off})
+    (void)hipFree(q);
   delete p;
 }
 
@@ -217,6 +218,7 @@ int saef_layout_create(const int64_t* off, const int64_t* n, int32_t L, int64_t 
     return SAEF_EHIP;
   }
   DevLayout& d = lay->dev;
+  lay->tensors = tensors;
   d.tiles = static_cast<const Tile*>(lay->mem_tiles);
   d.tensors = static_cast<const TensorInfo*>(lay->mem_tensors);
   d.part = static_cast<unsigned long long*>(lay->mem_part);
@@ -591,40 +593,57 @@ int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk**
   if (p == nullptr) return SAEF_EHIP;
   p->layout = layout;
   p->keep.assign(keep, keep + L);
+  // server chunks (kTkChunk elements), tile groups (kTkGroup tiles) and, for
+  // tensors with more than kTkGroup groups, super-groups (kTkGroup groups)
   std::vector<saef::TkChunk> chunks;
   std::vector<saef::TkTensor> tens(L);
-  int32_t max_chunks = 1;
+  std::vector<saef::TkGroup> groups, sgroups;
   for (int32_t l = 0; l < L; ++l) {
     const int64_t n = layout->n[l];
     const int64_t nc = (n + saef::kTkChunk - 1) / saef::kTkChunk;
-    tens[l] = saef::TkTensor{p->total_keep, keep[l], (int32_t)chunks.size(), (int32_t)nc};
+    const int32_t first_tile = layout->tensors[l].first_tile, ntiles = layout->tensors[l].ntiles;
+    const int32_t ng = (ntiles + saef::kTkGroup - 1) / saef::kTkGroup;
+    const int32_t nsg = ng > saef::kTkGroup ? (ng + saef::kTkGroup - 1) / saef::kTkGroup : 0;
+    tens[l] = saef::TkTensor{p->total_keep,          keep[l],
+                             (int32_t)chunks.size(), (int32_t)nc,
+                             (int32_t)groups.size(), ng,
+                             (int32_t)sgroups.size(), nsg};
     p->total_keep += keep[l];
-    max_chunks = std::max(max_chunks, (int32_t)nc);
     for (int64_t c = 0; c < nc; ++c)
       chunks.push_back(saef::TkChunk{layout->off[l] + c * saef::kTkChunk, l,
                                      (int32_t)std::min<int64_t>(saef::kTkChunk,
                                                                 n - c * saef::kTkChunk)});
+    for (int32_t s = 0; s < nsg; ++s)
+      sgroups.push_back(saef::TkGroup{l, (int32_t)groups.size() + s * saef::kTkGroup,
+                                      std::min(saef::kTkGroup, ng - s * saef::kTkGroup), 0});
+    for (int32_t g = 0; g < ng; ++g)
+      groups.push_back(saef::TkGroup{l, first_tile + g * saef::kTkGroup,
+                                     std::min(saef::kTkGroup, ntiles - g * saef::kTkGroup), 0});
   }
-  if ((int64_t)chunks.size() * (layout->k_max + 1) > kMaxGrid) {
+  const size_t rows = (size_t)layout->k_max + 1;
+  if ((int64_t)std::max(chunks.size(), groups.size()) * (int64_t)rows > kMaxGrid) {
     free_topk(p);
     return SAEF_EINVAL;
   }
-  const int32_t red_split = max_chunks > saef::kTkRedChunks
-                                ? (max_chunks + saef::kTkRedChunks - 1) / saef::kTkRedChunks
-                                : 1;
-  const size_t rows = (size_t)layout->k_max + 1;
-  const size_t hist_bytes = rows * chunks.size() * saef::kTkBins * sizeof(uint32_t);
-  const size_t hist2_bytes =
-      red_split > 1 ? rows * L * red_split * saef::kTkBins * sizeof(uint32_t) : 0;
+  const size_t n_tiles = (size_t)layout->dev.n_tiles;
+  const size_t thist_bytes = rows * n_tiles * saef::kTkHistPad * sizeof(uint16_t);
+  const size_t ghist_bytes = rows * groups.size() * saef::kTkHistPad * sizeof(uint32_t);
+  const size_t sghist_bytes = rows * sgroups.size() * saef::kTkHistPad * sizeof(uint32_t);
+  const size_t goff_bytes = rows * groups.size() * sizeof(uint32_t);
   const size_t sel_bytes = rows * L * sizeof(saef::TkSel);
-  const size_t cnt_bytes = rows * layout->dev.n_tiles * sizeof(uint32_t);
+  const size_t cnt_bytes = rows * n_tiles * sizeof(uint32_t);
   // candidate slots: at most every element of a tensor (8 B each) per row
   const size_t cand_bytes = rows * (size_t)layout->d_pad * sizeof(unsigned long long);
-  const size_t cand_off_bytes = rows * chunks.size() * sizeof(uint32_t);
+  const size_t cand_off_bytes = rows * n_tiles * sizeof(uint32_t);
   hipError_t err = hipMalloc(&p->mem_chunks, chunks.size() * sizeof(saef::TkChunk));
   if (err == hipSuccess) err = hipMalloc(&p->mem_tens, tens.size() * sizeof(saef::TkTensor));
-  if (err == hipSuccess) err = hipMalloc(&p->mem_hist, hist_bytes);
-  if (err == hipSuccess && hist2_bytes) err = hipMalloc(&p->mem_hist2, hist2_bytes);
+  if (err == hipSuccess) err = hipMalloc(&p->mem_groups, groups.size() * sizeof(saef::TkGroup));
+  if (err == hipSuccess && !sgroups.empty())
+    err = hipMalloc(&p->mem_sgroups, sgroups.size() * sizeof(saef::TkGroup));
+  if (err == hipSuccess) err = hipMalloc(&p->mem_thist, thist_bytes);
+  if (err == hipSuccess) err = hipMalloc(&p->mem_ghist, ghist_bytes);
+  if (err == hipSuccess && sghist_bytes) err = hipMalloc(&p->mem_sghist, sghist_bytes);
+  if (err == hipSuccess) err = hipMalloc(&p->mem_goff, goff_bytes);
   if (err == hipSuccess) err = hipMalloc(&p->mem_sel, sel_bytes);
   if (err == hipSuccess) err = hipMalloc(&p->mem_tile_cnt, cnt_bytes);
   if (err == hipSuccess) err = hipMalloc(&p->mem_cand, cand_bytes);
@@ -635,6 +654,12 @@ int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk**
   if (err == hipSuccess)
     err = hipMemcpy(p->mem_tens, tens.data(), tens.size() * sizeof(saef::TkTensor),
                     hipMemcpyHostToDevice);
+  if (err == hipSuccess)
+    err = hipMemcpy(p->mem_groups, groups.data(), groups.size() * sizeof(saef::TkGroup),
+                    hipMemcpyHostToDevice);
+  if (err == hipSuccess && !sgroups.empty())
+    err = hipMemcpy(p->mem_sgroups, sgroups.data(), sgroups.size() * sizeof(saef::TkGroup),
+                    hipMemcpyHostToDevice);
   if (err == hipSuccess) err = hipMemset(p->mem_sel, 0, sel_bytes);
   if (err == hipSuccess) err = hipDeviceSynchronize();
   if (err != hipSuccess) {
@@ -644,15 +669,20 @@ int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk**
   saef::TkDev& d = p->dev;
   d.chunks = static_cast<const saef::TkChunk*>(p->mem_chunks);
   d.tens = static_cast<const saef::TkTensor*>(p->mem_tens);
-  d.hist = static_cast<uint32_t*>(p->mem_hist);
-  d.hist2 = static_cast<uint32_t*>(p->mem_hist2);
+  d.groups = static_cast<const saef::TkGroup*>(p->mem_groups);
+  d.sgroups = static_cast<const saef::TkGroup*>(p->mem_sgroups);
+  d.thist = static_cast<uint16_t*>(p->mem_thist);
+  d.ghist = static_cast<uint32_t*>(p->mem_ghist);
+  d.sghist = static_cast<uint32_t*>(p->mem_sghist);
+  d.goff = static_cast<uint32_t*>(p->mem_goff);
   d.sel = static_cast<saef::TkSel*>(p->mem_sel);
   d.tile_cnt = static_cast<uint32_t*>(p->mem_tile_cnt);
   d.cand = static_cast<unsigned long long*>(p->mem_cand);
   d.cand_off = static_cast<uint32_t*>(p->mem_cand_off);
   d.n_chunks = (int64_t)chunks.size();
+  d.n_groups = (int64_t)groups.size();
+  d.n_sgroups = (int64_t)sgroups.size();
   d.total_keep = p->total_keep;
-  d.red_split = red_split;
   *out = p;
   return SAEF_OK;
 }

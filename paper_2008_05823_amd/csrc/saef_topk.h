@@ -6,34 +6,61 @@
 
 namespace saef {
 
-constexpr int kTkChunk = 65536;    // elements per histogram chunk (multiple of the tile)
-constexpr int kTkBins = 2048;      // bins of an 11-bit radix digit
-constexpr int kTkBins3 = 512;      // bins of the 9-bit key digit
-constexpr int kTkRedChunks = 64;   // chunk histograms one reduce workgroup adds
-static_assert(kTkChunk % kTileElems == 0, "a Top-K chunk holds whole tiles");
+// Pass-1 histogram of the key |v| over a window of four binades (exponents)
+// of a (row, tensor), placed around the previous call's threshold: 64 bins
+// per binade (key bits 22..17) inside the window, one bin below it and one
+// above it.  The window only decides how many elements become candidates;
+// the kept set is exact wherever the threshold falls.
+constexpr int kTkSubShift = 17;                // in-window bin width: 2^17 keys
+constexpr int kTkWin = 256;                    // in-window bins (4 binades)
+constexpr int kTkHist = kTkWin + 2;            // + below, + above
+constexpr int kTkHistPad = 260;                // 16-bit counts per tile (even, 8-byte rows)
+constexpr int kTkGroup = 64;      // tile histograms (or group sums) one sum workgroup adds
+constexpr int kTkBins = 2048;     // bins of an 11-bit radix digit
+constexpr int kTkChunk = 65536;   // elements per server-aggregation workgroup
+static_assert(kTkHistPad >= kTkHist && kTkHistPad % 4 == 0, "padded tile histogram");
+static_assert(kTileElems == 2048, "the Top-K kernels take a tile as 32 words, one per lane");
+static_assert(kTileElems < 65536, "a tile's bin counts fit 16 bits");
+static_assert(kTkChunk % kTileElems == 0, "a server chunk holds whole tiles");
 static_assert((int64_t)kTileElems * kMaxTilesPerTensor >= kMaxTensor,
               "every tensor is cut into tiles of kTileElems elements");
 
+// Up to kTkChunk elements of one tensor (whole tiles): the server's workgroups.
 struct TkChunk {
   int64_t start;  // absolute element index (multiple of 64)
   int32_t l;
   int32_t count;
 };
 
-struct TkTensor {
-  int64_t voff;        // first value of the tensor in a message
-  int64_t keep;        // k_l
-  int32_t first_chunk;
-  int32_t nchunks;
+// kTkGroup consecutive tiles of one tensor (a group), or kTkGroup consecutive
+// groups of one tensor (a super-group).
+struct TkGroup {
+  int32_t l;
+  int32_t first;  // first tile (group) index, global
+  int32_t n;      // tiles (groups) in it
+  int32_t pad;
 };
 
-// Selection state of one (row, tensor): after the pick, the bin b1 of key
-// bits 30..20 that holds the k-th largest key, how many elements to take
-// from it and how many it holds (the candidates); after the select, the
-// threshold key tau and the last kept index iota (in the tensor) of the
-// elements equal to tau.
+struct TkTensor {
+  int64_t voff;         // first value of the tensor in a message
+  int64_t keep;         // k_l
+  int32_t first_chunk;  // server chunks
+  int32_t nchunks;
+  int32_t first_group;  // tile groups
+  int32_t ngroups;
+  int32_t first_sgroup;  // super-groups, when ngroups > kTkGroup
+  int32_t nsgroups;      // 0 otherwise
+};
+
+// Selection state of one (row, tensor): the histogram window (kept from one
+// call to the next); after the pick, the bin b1 that holds the k-th largest
+// key, how many elements to take from it and how many it holds (the
+// candidates); after the select, the threshold key tau and the last kept
+// index iota (in the tensor) of the elements equal to tau.
 struct TkSel {
-  uint32_t prefix;  // b1, then tau
+  uint32_t tau;
+  uint32_t win;     // window base key (a multiple of 2^23)
+  uint32_t bin;     // b1
   uint32_t pad;
   int64_t need;
   int64_t cand;
@@ -43,20 +70,25 @@ struct TkSel {
 struct TkDev {
   const TkChunk* chunks;
   const TkTensor* tens;
-  uint32_t* hist;    // [rows][n_chunks][kTkBins] chunk histograms
-  uint32_t* hist2;   // [rows][L][red_split][kTkBins] second-level sums (red_split > 1)
-  TkSel* sel;        // [rows][L]
+  const TkGroup* groups;
+  const TkGroup* sgroups;
+  uint16_t* thist;     // [rows][n_tiles][kTkHistPad] tile histograms
+  uint32_t* ghist;     // [rows][n_groups][kTkHistPad] group sums
+  uint32_t* sghist;    // [rows][n_sgroups][kTkHistPad] super-group sums
+  uint32_t* goff;      // [rows][n_groups] first candidate slot of the group in its tensor
+  TkSel* sel;          // [rows][L]
   uint32_t* tile_cnt;  // [rows][n_tiles] kept per tile, then the exclusive prefix
+  uint32_t* cand_off;  // [rows][n_tiles] first candidate slot of the tile in its tensor
   unsigned long long* cand;  // [rows][d_pad] candidate slots: (row, tensor) at the tensor's offset
-  uint32_t* cand_off;  // [rows][n_chunks] first slot of each chunk's candidates
   int64_t n_chunks;
+  int64_t n_groups;
+  int64_t n_sgroups;
   int64_t total_keep;
-  int32_t red_split;   // reduce workgroups per (row, tensor)
 };
 
-// Worker Top-K compression of K rows (row k of e, hist row k).  m non-null:
-// momentum.  Writes Delta into e (then the kept elements are zeroed), the
-// selection words, rank words and values of each row.
+// Worker Top-K compression of K rows (row k of e, histogram row k).  m
+// non-null: momentum.  Writes Delta into e (then the kept elements are
+// zeroed), the selection words, rank words and values of each row.
 hipError_t launch_topk_compress(const DevLayout& lay, const TkDev& tk, int K, float lr, float mu,
                                 const float* g, float* m, float* e, uint64_t* sel,
                                 uint32_t* rank, float* vals, hipStream_t s,

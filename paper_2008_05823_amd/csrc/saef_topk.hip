@@ -4,25 +4,36 @@
 // magnitudes: the lower index first) and zeroes the others.  The kept set of
 // each (row, tensor) is found on the 31-bit key |v| (the bit pattern of a
 // non-negative float orders like its value):
-//   histogram  the pass that forms Delta also counts key bits 30..20 (2048
-//              bins) per 64Ki-element chunk, with LDS atomics and plain stores
-//              of the chunk histogram (no global atomics);
-//   pick       a workgroup per (row, tensor) adds the chunk histograms, finds
-//              the bin b1 that holds the k-th largest key and lays out, per
-//              chunk, slots for the elements of b1 (the candidates);
-//   gather     one read of Delta: elements above b1 are kept for sure and
-//              written to the selection words; the candidates go to their
-//              chunk's slots as (key, index in the tensor);
+//   histogram  the pass that forms Delta (one workgroup per tile and row)
+//              also counts the keys into a tile histogram (LDS atomics,
+//              16-bit counts stored): 64 bins per binade over a window of
+//              four binades placed around the (row, tensor)'s previous
+//              threshold, one bin below the window and one above it;
+//   sum        tile histograms are added per group of 64 tiles (and groups
+//              per super-group for very large tensors);
+//   pick       a workgroup per (row, tensor) finds the bin b1 that holds the
+//              k-th largest key and each group's first candidate slot;
+//   offsets    each tile's first candidate slot (a scan inside its group);
+//   gather     one wave per tile reads Delta once more: elements above b1
+//              are kept for sure and go to the selection words; the elements
+//              of b1 (the candidates) go to the tile's slots as
+//              (key, index in the tensor), in index order;
 //   select     a workgroup per (row, tensor) finds, among the candidates only,
 //              the threshold key tau and the last kept index iota of the
-//              elements equal to tau (radix passes on the key's low 20 bits,
-//              then on the index);
-//   apply      the kept candidates' bits are added to the selection words
-//              of their chunk, and the kept count of each tile is taken.
+//              elements equal to tau (radix passes on the key bits below
+//              b1's prefix, then on the index), and places the next call's
+//              window around tau;
+//   apply      one wave per tile adds its kept candidates to the tile's
+//              selection words and counts the tile's kept elements.
 // Emit: an exclusive scan of the tile counts per tensor; then the rank words
 // and the kept values in index order, and the kept elements of the error set
 // to 0 (e = Delta - C(Delta) is Delta elsewhere).  All of it is integer
 // counting, so the kept set does not depend on the launch geometry.
+//
+// The streaming passes (Delta, gather) run one short-lived workgroup or wave
+// per 2048-element tile: on MI355X a 2-read/1-write stream reaches about
+// 6.1 TB/s that way and about 5.1 TB/s when each workgroup walks 64Ki
+// elements.
 //
 // The server runs the same steps on its one row (row k_max of the scratch)
 // after k_tk_aggregate has formed Delta = e_srv + mean of the K messages.
@@ -33,27 +44,16 @@ namespace saef {
 namespace {
 
 constexpr uint32_t kFiniteLimit = 0x7F800000u;  // keys >= this are Inf or NaN
-constexpr int kTkU = 4;                         // words per wave per pass (first pass, server)
-constexpr int kTkH = 16;                        // words per wave per pass (gather)
-static_assert(kTkH <= kWave, "one selection word per lane in a gather pass");
-constexpr int kBig = 1024;                      // threads of the single-row (server) kernels
-#ifndef SAEF_TK_NT
-#define SAEF_TK_NT 1
-#endif
+constexpr int kTkU = 4;                         // words per wave per pass (Delta pass)
+constexpr int kTileWords = kTileElems / 64;     // 32
+constexpr int kBig = 1024;                      // threads of the per-(row, tensor) kernels
+static_assert(kTileWords <= kWave, "one selection word of a tile per lane");
 // Guarded loads without a branch: the load of p[ok ? j : 0] is always
 // issued (p[0] must exist) and its value replaced by 0 when !ok.  A branch
 // around each load makes the compiler wait for it before the next one.
 __device__ __forceinline__ float ld_nt_or0(const float* p, int64_t j, bool ok) {
   const float v = __builtin_nontemporal_load(p + (ok ? j : 0));
   return ok ? v : 0.0f;
-}
-__device__ __forceinline__ float ld_or0(const float* p, int64_t j, bool ok) {
-  const float v = p[ok ? j : 0];
-  return ok ? v : 0.0f;
-}
-// loads of the later passes (the error was just written by the first pass)
-__device__ __forceinline__ float ld_pass_or0(const float* p, int64_t j, bool ok) {
-  return SAEF_TK_NT ? ld_nt_or0(p, j, ok) : ld_or0(p, j, ok);
 }
 // Word 3 of a raw buffer descriptor on gfx9 parts (32-bit data format, no
 // swizzle, no index stride).  A load through a raw buffer resource of n
@@ -62,37 +62,40 @@ constexpr int kBufWord3 = 0x00020000;
 
 __device__ __forceinline__ uint32_t key_of(float v) { return __float_as_uint(v) & 0x7FFFFFFFu; }
 
-__device__ __forceinline__ u64 lanemask_lt(int lane) {
-  return lane == 0 ? 0ull : (~0ull >> (64 - lane));
+// Pass-1 bin of a key for the window [win, win + 4 binades): 0 below it,
+// 1 .. kTkWin inside it (key bits 22..17 within each binade), kTkWin + 1
+// above it.  Bins order like the keys.
+__device__ __forceinline__ uint32_t hist_bin(uint32_t key, uint32_t win) {
+  if (key < win) return 0u;
+  const uint32_t d = (key - win) >> kTkSubShift;
+  return d < (uint32_t)kTkWin ? d + 1u : (uint32_t)kTkWin + 1u;
 }
 
-// Pass-1 digit: key bits 30..20.
-__device__ __forceinline__ uint32_t digit1(uint32_t key) { return key >> 20; }
-
-template <int kBins>
-__device__ __forceinline__ void hist_clear(uint32_t* h) {
-  for (int i = threadIdx.x; i < kBins; i += blockDim.x) h[i] = 0;
-  __syncthreads();
+// The window for the next call: the binade of tau is the third of four.
+__device__ __forceinline__ uint32_t window_for(uint32_t tau) {
+  const uint32_t b = tau >> 23;
+  return (b >= 2u ? b - 2u : 0u) << 23;
 }
 
-// Stores the workgroup's LDS histogram (plain stores).
-template <int kBins>
-__device__ __forceinline__ void hist_store(const uint32_t* h, uint32_t* out) {
-  __syncthreads();
-  for (int i = threadIdx.x; i < kBins; i += blockDim.x) out[i] = h[i];
+__device__ __forceinline__ uint16_t* tile_hist(const TkDev& tk, const DevLayout& lay, int row,
+                                               int64_t ti) {
+  return tk.thist + ((int64_t)row * lay.n_tiles + ti) * kTkHistPad;
 }
 
-__device__ __forceinline__ uint32_t* chunk_hist(const TkDev& tk, int row, int64_t ci) {
-  return tk.hist + ((int64_t)row * tk.n_chunks + ci) * kTkBins;
+// Stores an LDS histogram of kTkHistPad bins as 16-bit counts, two per store.
+__device__ __forceinline__ void store_hist16(const uint32_t* h, uint16_t* out) {
+  for (int i = threadIdx.x; i < kTkHistPad / 2; i += blockDim.x)
+    reinterpret_cast<uint32_t*>(out)[i] = (h[2 * i] & 0xFFFFu) | (h[2 * i + 1] << 16);
 }
 
 // ------------------------------------------------------------------ pass 1 (workers)
-// kTkU words of one worker's chunk: m <- fma(mu, m, g) with kMom, Delta =
-// fma(lr, m or g, e), Delta stored into e, pass-1 histogram of its key.
+// kTkU words of one worker's tile: m <- fma(mu, m, g) with kMom, Delta =
+// fma(lr, m or g, e), Delta stored into e, its key counted.
 template <bool kMom, bool kFull>
 __device__ __forceinline__ void delta_words(int w0, int nw, int count, float lr, float mu,
                                             const float* __restrict__ gk, float* __restrict__ mk,
-                                            float* __restrict__ ek, uint32_t* h, bool& bad) {
+                                            float* __restrict__ ek, uint32_t win, uint32_t* h,
+                                            bool& bad) {
   const int lane = lane_id();
   float gv[kTkU], ev[kTkU], mv[kTkU];
 #pragma unroll
@@ -117,60 +120,65 @@ __device__ __forceinline__ void delta_words(int w0, int nw, int count, float lr,
     st_nt(ek + j, p);
     const uint32_t key = key_of(p);
     bad |= key >= kFiniteLimit;
-    atomicAdd(&h[digit1(key)], 1u);
+    atomicAdd(&h[hist_bin(key, win)], 1u);
   }
 }
 
-// Grid: n_chunks * K workgroups; workgroup b handles worker b % K of chunk b / K.
+// Grid: n_tiles * K workgroups; workgroup b handles worker b % K of tile b / K.
 template <bool kMom>
 __global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, int K, float lr,
                                                      float mu, const float* __restrict__ g,
                                                      float* __restrict__ m,
                                                      float* __restrict__ e) {
-  __shared__ uint32_t h[kTkBins];
+  __shared__ uint32_t h[kTkHistPad];
   const int k = (int)(blockIdx.x % (unsigned)K);
-  const int64_t ci = blockIdx.x / (unsigned)K;
-  const TkChunk c = tk.chunks[ci];
-  hist_clear<kTkBins>(h);
-  const int64_t row = (int64_t)k * lay.d_pad + c.start;
+  const int64_t ti = blockIdx.x / (unsigned)K;
+  const Tile tile = lay.tiles[ti];
+  const uint32_t win = tk.sel[(int64_t)k * lay.L + tile.l].win;
+  for (int i = threadIdx.x; i < kTkHistPad; i += kBlock) h[i] = 0;
+  __syncthreads();
+  const int64_t row = (int64_t)k * lay.d_pad + tile.start;
   const float* gk = g + row;
   float* mk = kMom ? m + row : nullptr;
   float* ek = e + row;
-  const int nw = (c.count + 63) >> 6;
+  const int nw = (tile.count + 63) >> 6;
   bool bad = false;
   for (int w0 = wave_id() * kTkU; w0 < nw; w0 += kWaves * kTkU) {
-    if ((w0 + kTkU) * 64 <= c.count)
-      delta_words<kMom, true>(w0, nw, c.count, lr, mu, gk, mk, ek, h, bad);
+    if ((w0 + kTkU) * 64 <= tile.count)
+      delta_words<kMom, true>(w0, nw, tile.count, lr, mu, gk, mk, ek, win, h, bad);
     else
-      delta_words<kMom, false>(w0, nw, c.count, lr, mu, gk, mk, ek, h, bad);
+      delta_words<kMom, false>(w0, nw, tile.count, lr, mu, gk, mk, ek, win, h, bad);
   }
   if (__ballot(bad) != 0 && lane_id() == 0) atomicOr(lay.status, kStatusRange);
-  hist_store<kTkBins>(h, chunk_hist(tk, k, ci));
+  __syncthreads();
+  store_hist16(h, tile_hist(tk, lay, k, ti));
 }
 
-// ------------------------------------------------------------------ reduce
-// Grid: R * L * red_split workgroups: group s adds the chunk histograms
-// [s kTkRedChunks, (s+1) kTkRedChunks) of the tensor (those that exist).
+// ------------------------------------------------------------------ sums
+// Grid: R * n_groups workgroups (kSuper: R * n_sgroups).  Workgroup b adds
+// the tile histograms of group b % n_groups (or the group sums of
+// super-group b % n_sgroups) of row row0 + b / n.
+template <bool kSuper>
 __global__ __launch_bounds__(kBlock) void k_tk_sum(DevLayout lay, TkDev tk, int row0) {
-  constexpr int kPer = kTkBins / kBlock;
-  const int S = tk.red_split;
-  const int s = (int)(blockIdx.x % S);
-  const int l = (int)((blockIdx.x / S) % lay.L);
-  const int r = (int)(blockIdx.x / ((unsigned)S * lay.L));
-  const int row = row0 + r;
-  const TkTensor t = tk.tens[l];
-  const int c0 = min(t.nchunks, s * kTkRedChunks), c1 = min(t.nchunks, c0 + kTkRedChunks);
-  uint32_t acc[kPer];
-#pragma unroll
-  for (int j = 0; j < kPer; ++j) acc[j] = 0;
-  for (int c = c0; c < c1; ++c) {
-    const uint32_t* src = chunk_hist(tk, row, t.first_chunk + c) + threadIdx.x * kPer;
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) acc[j] += src[j];
+  const int64_t n = kSuper ? tk.n_sgroups : tk.n_groups;
+  const int64_t gi = blockIdx.x % n;
+  const int row = row0 + (int)(blockIdx.x / n);
+  const TkGroup gr = (kSuper ? tk.sgroups : tk.groups)[gi];
+  uint32_t* dst = (kSuper ? tk.sghist + ((int64_t)row * tk.n_sgroups + gi) * kTkHistPad
+                          : tk.ghist + ((int64_t)row * tk.n_groups + gi) * kTkHistPad);
+  for (int b = threadIdx.x; b < kTkHistPad; b += kBlock) {
+    uint32_t acc = 0;
+    if (kSuper) {
+      const uint32_t* src = tk.ghist + ((int64_t)row * tk.n_groups + gr.first) * kTkHistPad + b;
+#pragma unroll 8
+      for (int i = 0; i < gr.n; ++i) acc += src[(int64_t)i * kTkHistPad];
+    } else {
+      const uint16_t* src = tile_hist(tk, lay, row, gr.first) + b;
+#pragma unroll 8
+      for (int i = 0; i < gr.n; ++i) acc += src[(int64_t)i * kTkHistPad];
+    }
+    dst[b] = acc;
   }
-  uint32_t* dst = tk.hist2 + (((int64_t)row * lay.L + l) * S + s) * kTkBins + threadIdx.x * kPer;
-#pragma unroll
-  for (int j = 0; j < kPer; ++j) dst[j] = acc[j];
 }
 
 // ------------------------------------------------------------------ block helpers
@@ -241,152 +249,156 @@ __device__ void find_bin(const uint32_t* h, int nb, int64_t need, uint32_t* s_sc
 }
 
 // ------------------------------------------------------------------ pick
-// Grid: R * L workgroups.  Adds the tensor's pass-1 histograms (the chunk
-// histograms, or the red_split partial sums), finds the bin b1 that holds
-// the k-th largest key and how many to take from it, and lays out the
-// candidate slots: chunk c's elements of b1 go to slots [off_c, off_c +
-// count_c) of the (row, tensor)'s candidate area (one slot per element of
-// the tensor at most), off_c the exclusive prefix of the counts in chunk
-// order.
+// Grid: R * L workgroups.  Adds the tensor's group sums (or super-group
+// sums), finds the bin b1 that holds the k-th largest key and how many to
+// take from it, and gives each group of the tensor its first candidate slot:
+// the elements of b1 go to the (row, tensor)'s candidate area (one slot per
+// element of the tensor at most) in tile order.
 __global__ __launch_bounds__(kBlock) void k_tk_pick(DevLayout lay, TkDev tk, int row0) {
-  constexpr int kPer = kTkBins / kBlock;
   __shared__ uint32_t s_scan[kWaves];
   __shared__ uint32_t s_res[3];
-  __shared__ uint32_t h[kTkBins];
+  __shared__ uint32_t h[kTkHistPad];
   const int l = (int)(blockIdx.x % lay.L);
   const int r = (int)(blockIdx.x / lay.L);
   const int row = row0 + r;
   const TkTensor t = tk.tens[l];
-  const int S = tk.red_split;
-  uint32_t cnt[kPer];
-#pragma unroll
-  for (int j = 0; j < kPer; ++j) cnt[j] = 0;
-  if (S > 1) {
-    const uint32_t* src = tk.hist2 + ((int64_t)row * lay.L + l) * S * kTkBins + threadIdx.x * kPer;
-    for (int s = 0; s < S; ++s)
-#pragma unroll
-      for (int j = 0; j < kPer; ++j) cnt[j] += src[(int64_t)s * kTkBins + j];
-  } else {
-    for (int c = 0; c < t.nchunks; ++c) {
-      const uint32_t* src = chunk_hist(tk, row, t.first_chunk + c) + threadIdx.x * kPer;
-#pragma unroll
-      for (int j = 0; j < kPer; ++j) cnt[j] += src[j];
-    }
+  const bool super = t.nsgroups > 0;
+  const uint32_t* src = super
+      ? tk.sghist + ((int64_t)row * tk.n_sgroups + t.first_sgroup) * kTkHistPad
+      : tk.ghist + ((int64_t)row * tk.n_groups + t.first_group) * kTkHistPad;
+  const int ns = super ? t.nsgroups : t.ngroups;
+  for (int b = threadIdx.x; b < kTkHistPad; b += kBlock) {
+    uint32_t cnt = 0;
+    for (int i = 0; i < ns; ++i) cnt += src[(int64_t)i * kTkHistPad + b];
+    h[b] = cnt;
   }
-#pragma unroll
-  for (int j = 0; j < kPer; ++j) h[threadIdx.x * kPer + j] = cnt[j];
   __syncthreads();
   uint32_t b1, n1;
   int64_t left;
-  find_bin<true>(h, kTkBins, t.keep, s_scan, s_res, b1, left, n1);
-  // candidate slots per chunk
+  find_bin<true>(h, kTkHist, t.keep, s_scan, s_res, b1, left, n1);
+  // first candidate slot of each group, in group order
   uint32_t carry = 0;
-  for (int c0 = 0; c0 < t.nchunks; c0 += kBlock) {
-    const int c = c0 + threadIdx.x;
-    const uint32_t v = c < t.nchunks ? chunk_hist(tk, row, t.first_chunk + c)[b1] : 0u;
+  const uint32_t* gh = tk.ghist + ((int64_t)row * tk.n_groups + t.first_group) * kTkHistPad + b1;
+  for (int g0 = 0; g0 < t.ngroups; g0 += kBlock) {
+    const int gi = g0 + threadIdx.x;
+    const uint32_t v = gi < t.ngroups ? gh[(int64_t)gi * kTkHistPad] : 0u;
     uint32_t all;
     const uint32_t before = block_excl_scan(v, s_scan, &all);
-    if (c < t.nchunks) tk.cand_off[(int64_t)row * tk.n_chunks + t.first_chunk + c] = carry + before;
+    if (gi < t.ngroups) tk.goff[(int64_t)row * tk.n_groups + t.first_group + gi] = carry + before;
     carry += all;
   }
   if (threadIdx.x == 0) {
     TkSel* st = tk.sel + (int64_t)row * lay.L + l;
-    st->prefix = b1;
+    st->bin = b1;
     st->need = left;
-    st->cand = n1;  // the elements of b1 (the sum of the chunk counts)
+    st->cand = n1;  // the elements of b1 (the sum of the tile counts)
   }
 }
 
-// ------------------------------------------------------------------ gather
-// Grid: n_chunks * R workgroups of kThreads.  One read of Delta: the
-// selection words with the elements above b1 (kept for sure), and the
-// elements of b1 appended to the chunk's candidate slots as
-// key | (index in the tensor) << 32.  Their order inside the chunk's slots
-// is that of the LDS reservations; nothing downstream depends on it.
-template <int kThreads>
-__global__ __launch_bounds__(kThreads) void k_tk_gather(DevLayout lay, TkDev tk, int R, int row0,
-                                                        const float* __restrict__ data,
-                                                        uint64_t* __restrict__ sel) {
-  constexpr int kW = kThreads / kWave;
-  __shared__ uint32_t s_next;
-  const int r = (int)(blockIdx.x % (unsigned)R);
-  const int64_t ci = blockIdx.x / (unsigned)R;
-  const int row = row0 + r;
-  const TkChunk c = tk.chunks[ci];
-  const uint32_t b1 = tk.sel[(int64_t)row * lay.L + c.l].prefix;
-  const TkTensor t = tk.tens[c.l];
-  const int64_t t_off = tk.chunks[t.first_chunk].start;
-  const int64_t rel0 = c.start - t_off;  // the chunk's first element, index in the tensor
-  u64* slots = tk.cand + (int64_t)row * lay.d_pad + t_off +
-               tk.cand_off[(int64_t)row * tk.n_chunks + ci];
-  const uint32_t nslots = chunk_hist(tk, row, ci)[b1];  // elements of b1 in the chunk
-  if (threadIdx.x == 0) s_next = 0;
-  __syncthreads();
-  const float* dr = data + (int64_t)r * lay.d_pad + c.start;
-  uint64_t* sr = sel + (int64_t)r * (lay.d_pad >> 6) + (c.start >> 6);
+// Grid: R * n_groups workgroups of one wave: the first candidate slot of
+// each tile of group b % n_groups in row row0 + b / n_groups (the group's
+// slot plus the b1 counts of the group's earlier tiles).
+__global__ __launch_bounds__(kWave) void k_tk_offsets(DevLayout lay, TkDev tk, int row0) {
+  static_assert(kTkGroup == kWave, "one tile of a group per lane");
+  const int64_t gi = blockIdx.x % tk.n_groups;
+  const int row = row0 + (int)(blockIdx.x / tk.n_groups);
+  const TkGroup gr = tk.groups[gi];
+  const uint32_t b1 = tk.sel[(int64_t)row * lay.L + gr.l].bin;
   const int lane = lane_id();
-  const u64 lt = lanemask_lt(lane);
-  const int nw = (c.count + 63) >> 6;
-  for (int w0 = wave_id() * kTkH; w0 < nw; w0 += kW * kTkH) {
-    float v[kTkH];
+  const uint32_t c = lane < gr.n ? tile_hist(tk, lay, row, gr.first + lane)[b1] : 0u;
+  uint32_t x = c;
 #pragma unroll
-    for (int u = 0; u < kTkH; ++u) {
-      const int j = (w0 + u) * 64 + lane;
-      v[u] = ld_pass_or0(dr, j, w0 + u < nw && j < c.count);
-    }
-    u64 cm[kTkH];
-    u64 myw = 0;  // lane u < kTkH: selection word u of the pass
-    uint32_t ncand = 0;
-#pragma unroll
-    for (int u = 0; u < kTkH; ++u) {
-      const int j = (w0 + u) * 64 + lane;
-      const bool ok = w0 + u < nw && j < c.count;
-      const uint32_t hi = digit1(key_of(v[u]));
-      const u64 word = __ballot(ok && hi > b1);
-      if (lane == u) myw = word;
-      cm[u] = __ballot(ok && hi == b1);
-      ncand += (uint32_t)__popcll(cm[u]);
-    }
-    // the pass's words in one store (a single-lane store per word costs more)
-    if (lane < kTkH && w0 + lane < nw) sr[w0 + lane] = myw;
-    if (ncand != 0) {  // uniform over the wave
-      uint32_t base = 0;
-      if (lane == 0) base = atomicAdd(&s_next, ncand);
-      base = __shfl(base, 0);
-#pragma unroll
-      for (int u = 0; u < kTkH; ++u) {
-        const uint32_t pos = base + (uint32_t)__popcll(cm[u] & lt);
-        if (((cm[u] >> lane) & 1ull) && pos < nslots) {  // pos < nslots always holds
-          const int64_t idx = rel0 + (int64_t)(w0 + u) * 64 + lane;
-          slots[pos] = (u64)key_of(v[u]) | ((u64)idx << 32);
-        }
-        base += (uint32_t)__popcll(cm[u]);
-      }
-    }
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint32_t y = __shfl_up(x, off);
+    if (lane >= off) x += y;
   }
+  if (lane < gr.n)
+    tk.cand_off[(int64_t)row * lay.n_tiles + gr.first + lane] =
+        tk.goff[(int64_t)row * tk.n_groups + gi] + x - c;
+}
+
+// ------------------------------------------------------------------ gather
+// Grid: per_wave_grid(lay) * R workgroups; wave w of workgroup b owns tile
+// 4 (b / R) + w of row b % R.  One read of the tile's Delta (all 32 words at
+// once): the selection words with the elements above b1 (kept for sure), and
+// the elements of b1 to the tile's candidate slots as key | (index in the
+// tensor) << 32, in index order.
+__global__ __launch_bounds__(kBlock) void k_tk_gather(DevLayout lay, TkDev tk, int R, int row0,
+                                                      const float* __restrict__ data,
+                                                      uint64_t* __restrict__ sel) {
+  const int r = (int)(blockIdx.x % (unsigned)R);
+  const int64_t ti = (int64_t)(blockIdx.x / (unsigned)R) * kWaves + wave_id();
+  if (ti >= lay.n_tiles) return;
+  const int row = row0 + r;
+  const Tile tile = lay.tiles[ti];
+  const TkSel* st = tk.sel + (int64_t)row * lay.L + tile.l;
+  const uint32_t b1 = st->bin, win = st->win;
+  const TensorInfo ten = lay.tensors[tile.l];
+  const int64_t rel0 = tile.start - ten.off;  // the tile's first element, index in the tensor
+  u64* slots = tk.cand + (int64_t)row * lay.d_pad + ten.off +
+               tk.cand_off[(int64_t)row * lay.n_tiles + ti];
+  const uint32_t nslots = tile_hist(tk, lay, row, ti)[b1];  // elements of b1 in the tile
+  const float* dr = data + (int64_t)r * lay.d_pad + tile.start;
+  uint64_t* sr = sel + (int64_t)r * (lay.d_pad >> 6) + (tile.start >> 6);
+  const int lane = lane_id();
+  const int nw = (tile.count + 63) >> 6;
+  float v[kTileWords];
+#pragma unroll
+  for (int u = 0; u < kTileWords; ++u) {
+    const int j = u * 64 + lane;
+    v[u] = ld_nt_or0(dr, j, j < tile.count);
+  }
+  u64 myw = 0;        // lane u < nw: selection word u
+  uint32_t base = 0;  // candidates in the earlier words
+#pragma unroll
+  for (int u = 0; u < kTileWords; ++u) {
+    const int j = u * 64 + lane;
+    const bool ok = j < tile.count;
+    const uint32_t hi = hist_bin(key_of(v[u]), win);
+    const u64 word = __ballot(ok && hi > b1);
+    if (lane == u) myw = word;
+    const u64 cm = __ballot(ok && hi == b1);
+    const uint32_t pos = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(cm >> 32),
+                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)cm, 0u));
+    if (((cm >> lane) & 1ull) && pos < nslots)  // pos < nslots always holds
+      slots[pos] = (u64)key_of(v[u]) | ((u64)(rel0 + j) << 32);
+    base += (uint32_t)__popcll(cm);
+  }
+  if (lane < nw) sr[lane] = myw;
 }
 
 // ------------------------------------------------------------------ select
 // One radix pass over the candidates: histogram (LDS) of digit(e) of those
-// with match(e).
+// with match(e).  Each thread has kIlp candidate loads in flight.
 template <typename Match, typename Dig>
 __device__ void cand_hist(uint32_t* h, int nb, const u64* __restrict__ cand, int64_t C,
                           Match match, Dig digit) {
+  constexpr int kIlp = 8;
   for (int i = threadIdx.x; i < nb; i += blockDim.x) h[i] = 0;
   __syncthreads();
-  for (int64_t i = threadIdx.x; i < C; i += blockDim.x) {
-    const u64 e = cand[i];
-    if (match(e)) atomicAdd(&h[digit(e)], 1u);
+  const int64_t nt = blockDim.x;
+  for (int64_t i0 = threadIdx.x; i0 < C; i0 += nt * kIlp) {
+    u64 e[kIlp];
+#pragma unroll
+    for (int u = 0; u < kIlp; ++u) {
+      const int64_t i = i0 + u * nt;
+      e[u] = cand[i < C ? i : 0];  // C > 0 here
+    }
+#pragma unroll
+    for (int u = 0; u < kIlp; ++u)
+      if (i0 + u * nt < C && match(e[u])) atomicAdd(&h[digit(e[u])], 1u);
   }
   __syncthreads();
 }
 
 // Grid: R * L workgroups of kBig threads.  Among the candidates of (row,
 // tensor) (the elements of bin b1), takes the `need` largest keys, equal
-// keys by lower index: radix passes on key bits 19..9 and 8..0 give the
-// threshold key tau and how many of the elements equal to tau are kept; if
-// not all, passes on the index in the tensor (bits 27..17, 16..6, 5..0)
-// give the last kept index iota.
+// keys by lower index: radix passes of up to 11 bits over the key bits that
+// b1 leaves open (bits 16..0 inside the window; all 31 for the bins below
+// and above it) give the threshold key tau and how many of the elements
+// equal to tau are kept; if not all, passes on the index in the tensor
+// (bits 27..17, 16..6, 5..0) give the last kept index iota.  The next
+// call's window is placed around tau.
 __global__ __launch_bounds__(kBig) void k_tk_select(DevLayout lay, TkDev tk, int row0) {
   __shared__ uint32_t h[kTkBins];
   __shared__ uint32_t s_scan[kBig / kWave];
@@ -395,25 +407,27 @@ __global__ __launch_bounds__(kBig) void k_tk_select(DevLayout lay, TkDev tk, int
   const int r = (int)(blockIdx.x / lay.L);
   const int row = row0 + r;
   TkSel* st = tk.sel + (int64_t)row * lay.L + l;
-  const TkTensor t = tk.tens[l];
-  const int64_t t_off = tk.chunks[t.first_chunk].start;
-  const u64* cand = tk.cand + (int64_t)row * lay.d_pad + t_off;
+  const u64* cand = tk.cand + (int64_t)row * lay.d_pad + lay.tensors[l].off;
   const int64_t C = st->cand;
-  const uint32_t b1 = st->prefix;
+  const uint32_t b1 = st->bin, win = st->win;
   int64_t need = st->need;
-  uint32_t bin, cnt;
-  int64_t left;
-  // key bits 19..9
-  cand_hist(h, kTkBins, cand, C, [](u64) { return true; },
-            [](u64 e) { return ((uint32_t)e >> 9) & 2047u; });
-  find_bin<true>(h, kTkBins, need, s_scan, s_res, bin, left, cnt);
-  const uint32_t p2 = (b1 << 11) | bin;
-  need = left;
-  // key bits 8..0
-  cand_hist(h, kTkBins3, cand, C, [p2](u64 e) { return ((uint32_t)e >> 9) == p2; },
-            [](u64 e) { return (uint32_t)e & 511u; });
-  find_bin<true>(h, kTkBins3, need, s_scan, s_res, bin, left, cnt);
-  const uint32_t tau = (p2 << 9) | bin;
+  const bool inside = b1 >= 1u && b1 <= (uint32_t)kTkWin;
+  uint32_t prefix = inside ? (win >> kTkSubShift) + (b1 - 1u) : 0u;  // key >> open
+  int open = inside ? kTkSubShift : 31;
+  uint32_t bin = 0, cnt = 0;
+  int64_t left = need;
+  while (open > 0) {
+    const int d = open > 11 ? 11 : open;
+    const int sh = open - d;
+    const uint32_t mask = (1u << d) - 1u;
+    cand_hist(h, 1 << d, cand, C, [prefix, open](u64 e) { return ((uint32_t)e >> open) == prefix; },
+              [sh, mask](u64 e) { return ((uint32_t)e >> sh) & mask; });
+    find_bin<true>(h, 1 << d, need, s_scan, s_res, bin, left, cnt);
+    prefix = (prefix << d) | bin;
+    open = sh;
+    need = left;
+  }
+  const uint32_t tau = prefix;
   int64_t iota = INT64_MAX;  // every element equal to tau is kept
   if (left < (int64_t)cnt) {
     // the left-th smallest index among the elements equal to tau
@@ -436,56 +450,60 @@ __global__ __launch_bounds__(kBig) void k_tk_select(DevLayout lay, TkDev tk, int
     iota = ((int64_t)q2 << 6) | bin;
   }
   if (threadIdx.x == 0) {
-    st->prefix = tau;
+    st->tau = tau;
     st->iota = iota;
+    st->win = window_for(tau);
   }
 }
 
 // ------------------------------------------------------------------ apply
-// Grid: n_chunks * R workgroups.  Adds the bits of the kept candidates to the
-// chunk's selection words (in LDS, then written back) and stores the kept
-// count of each tile of the chunk.
+// Grid: per_wave_grid(lay) * R workgroups, one wave per tile (as the gather).
+// Adds the bits of the tile's kept candidates to its selection words (in
+// LDS, then written back) and stores the tile's kept count.
 __global__ __launch_bounds__(kBlock) void k_tk_apply(DevLayout lay, TkDev tk, int R, int row0,
                                                      uint64_t* __restrict__ sel) {
-  constexpr int kWords = kTkChunk / 64;
-  constexpr int kTileWords = kTileElems / 64;
-  __shared__ u64 words[kWords];
+  __shared__ u64 words[kWaves][kTileWords];
   const int r = (int)(blockIdx.x % (unsigned)R);
-  const int64_t ci = blockIdx.x / (unsigned)R;
+  const int64_t ti = (int64_t)(blockIdx.x / (unsigned)R) * kWaves + wave_id();
+  const int wave = threadIdx.x / kWave;
+  const int lane = lane_id();
+  const bool live = ti < lay.n_tiles;  // every wave reaches the barriers
   const int row = row0 + r;
-  const TkChunk c = tk.chunks[ci];
-  const TkSel st = tk.sel[(int64_t)row * lay.L + c.l];
-  const uint32_t tau = st.prefix;
-  const int64_t iota = st.iota;
-  const TkTensor t = tk.tens[c.l];
-  const int64_t t_off = tk.chunks[t.first_chunk].start;
-  const int64_t rel0 = c.start - t_off;
-  const int nw = (c.count + 63) >> 6;
-  uint64_t* sr = sel + (int64_t)r * (lay.d_pad >> 6) + (c.start >> 6);
-  for (int i = threadIdx.x; i < nw; i += kBlock) words[i] = sr[i];
+  Tile tile{};
+  int nw = 0;
+  uint64_t* sr = nullptr;
+  if (live) {
+    tile = lay.tiles[ti];
+    nw = (tile.count + 63) >> 6;
+    sr = sel + (int64_t)r * (lay.d_pad >> 6) + (tile.start >> 6);
+  }
+  if (lane < kTileWords) words[wave][lane] = lane < nw ? sr[lane] : 0ull;
   __syncthreads();
-  const uint32_t ncand = chunk_hist(tk, row, ci)[digit1(tau)];
-  const u64* slots = tk.cand + (int64_t)row * lay.d_pad + t_off +
-                     tk.cand_off[(int64_t)row * tk.n_chunks + ci];
-  for (uint32_t i = threadIdx.x; i < ncand; i += kBlock) {
-    const u64 e = slots[i];
-    const uint32_t key = (uint32_t)e;
-    const int64_t idx = (int64_t)(e >> 32);
-    const int64_t q = idx - rel0;  // element of the chunk
-    if ((key > tau || (key == tau && idx <= iota)) && q >= 0 && q < c.count)
-      atomicOr(&words[q >> 6], 1ull << (q & 63));
+  if (live) {
+    const TkSel st = tk.sel[(int64_t)row * lay.L + tile.l];
+    const TensorInfo ten = lay.tensors[tile.l];
+    const int64_t rel0 = tile.start - ten.off;
+    const u64* slots = tk.cand + (int64_t)row * lay.d_pad + ten.off +
+                       tk.cand_off[(int64_t)row * lay.n_tiles + ti];
+    // the tile's candidates: the b1 count of its histogram
+    const uint32_t ncand = tile_hist(tk, lay, row, ti)[st.bin];
+    for (uint32_t i = lane; i < ncand; i += kWave) {
+      const u64 e = slots[i];
+      const uint32_t key = (uint32_t)e;
+      const int64_t idx = (int64_t)(e >> 32);
+      const int64_t q = idx - rel0;  // element of the tile
+      if ((key > st.tau || (key == st.tau && idx <= st.iota)) && q >= 0 && q < tile.count)
+        atomicOr(&words[wave][q >> 6], 1ull << (q & 63));
+    }
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < nw; i += kBlock) sr[i] = words[i];
-  // tiles of the chunk (a chunk starts on a tile boundary)
-  const int ntile = (nw + kTileWords - 1) / kTileWords;
-  const int64_t tile0 = lay.tensors[c.l].first_tile + rel0 / kTileElems;
-  for (int i = threadIdx.x; i < ntile; i += kBlock) {
-    uint32_t n = 0;
-    for (int w = i * kTileWords; w < min(nw, (i + 1) * kTileWords); ++w)
-      n += (uint32_t)__popcll(words[w]);
-    tk.tile_cnt[(int64_t)row * lay.n_tiles + tile0 + i] = n;
-  }
+  if (!live) return;
+  const u64 w = lane < nw ? words[wave][lane] : 0ull;
+  if (lane < nw) sr[lane] = w;
+  uint32_t n = (uint32_t)__popcll(w);
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) n += __shfl_xor(n, off);
+  if (lane == 0) tk.tile_cnt[(int64_t)row * lay.n_tiles + ti] = n;
 }
 
 // ------------------------------------------------------------------ emit
@@ -555,7 +573,6 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, int
                                                     uint32_t* __restrict__ rank,
                                                     float* __restrict__ vals,
                                                     float* __restrict__ x) {
-  constexpr int kTileWords = kTileElems / 64;
   static_assert(kTileWords == 32, "five halving steps find a word of the tile");
   const int r = (int)(blockIdx.x % (unsigned)R);
   const int64_t ti = (int64_t)(blockIdx.x / (unsigned)R) * kWaves + wave_id();
@@ -650,12 +667,18 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
                                                        float* __restrict__ x) {
   constexpr int kB = kWave / U;  // workers per batch
   static_assert(kB * U == kWave, "one (worker, word) pair per lane");
-  __shared__ uint32_t h[kTkBins];
+  static_assert(kTileWords % U == 0, "a pass of U words stays in one tile");
+  constexpr int kChunkTiles = kTkChunk / kTileElems;
+  __shared__ uint32_t h[kMode == 1 ? kChunkTiles * kTkHistPad : 1];  // per tile of the chunk
   const int64_t ci = blockIdx.x;
   const TkChunk c = tk.chunks[ci];
   const int64_t voff = tk.tens[c.l].voff;
   const uint32_t keep = (uint32_t)tk.tens[c.l].keep;
-  if (kMode == 1) hist_clear<kTkBins>(h);
+  const uint32_t win = kMode == 1 ? tk.sel[(int64_t)lay.k_max * lay.L + c.l].win : 0u;
+  if (kMode == 1) {
+    for (int i = threadIdx.x; i < kChunkTiles * kTkHistPad; i += kBig) h[i] = 0;
+    __syncthreads();
+  }
   const int lane = lane_id();
   const int nw = (c.count + 63) >> 6;
   const int64_t W = lay.d_pad >> 6;
@@ -721,7 +744,8 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
         st_nt(dr + j, D);
         const uint32_t key = key_of(D);
         bad |= key >= kFiniteLimit;
-        atomicAdd(&h[digit1(key)], 1u);
+        // a pass stays in one tile
+        atomicAdd(&h[(w0 / kTileWords) * kTkHistPad + hist_bin(key, win)], 1u);
       } else {
         st_nt(dr + j, dv[i] - mean);  // single-way: the mean itself comes back
       }
@@ -729,7 +753,14 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
   }
   if (kMode == 1) {
     if (__ballot(bad) != 0 && lane_id() == 0) atomicOr(lay.status, kStatusRange);
-    hist_store<kTkBins>(h, chunk_hist(tk, lay.k_max, ci));
+    __syncthreads();
+    // the tile histograms of the chunk, 16-bit counts, two bins per store
+    const TensorInfo ten = lay.tensors[c.l];
+    const int64_t tile0 = ten.first_tile + (c.start - ten.off) / kTileElems;
+    const int ntile = (c.count + kTileElems - 1) / kTileElems;
+    uint32_t* out = reinterpret_cast<uint32_t*>(tile_hist(tk, lay, lay.k_max, tile0));
+    for (int i = threadIdx.x; i < ntile * (kTkHistPad / 2); i += kBig)
+      out[i] = (h[2 * i] & 0xFFFFu) | (h[2 * i + 1] << 16);
   }
 }
 
@@ -740,33 +771,34 @@ struct Launcher {
   hipStream_t s;
 
   // everything after the first pass for R rows of `data` (rows row0..):
-  // pick, gather, select, apply, scan, emit.  The last kernel stamps the
-  // caller's stop event.
+  // sums, pick, offsets, gather, select, apply, scan, emit.  The last kernel
+  // stamps the caller's stop event.
   hipError_t select_and_emit(int R, int row0, float* data, uint64_t* sel, uint32_t* rank,
                              float* vals, float* x, const LaunchEvents& last) const {
     const LaunchEvents ev;
     hipError_t err;
-    if (tk.red_split > 1) {
-      SAEF_LAUNCH(k_tk_sum, dim3((unsigned)(R * lay.L * tk.red_split)), dim3(kBlock), 0, s, lay,
+    SAEF_LAUNCH(k_tk_sum<false>, dim3((unsigned)(R * tk.n_groups)), dim3(kBlock), 0, s, lay, tk,
+                row0);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    if (tk.n_sgroups > 0) {
+      SAEF_LAUNCH(k_tk_sum<true>, dim3((unsigned)(R * tk.n_sgroups)), dim3(kBlock), 0, s, lay,
                   tk, row0);
       if ((err = hipGetLastError()) != hipSuccess) return err;
     }
     const dim3 pairs((unsigned)(R * lay.L));
-    const dim3 chunks((unsigned)(tk.n_chunks * R));
+    const dim3 tiles((unsigned)(per_wave_grid(lay) * R));
     SAEF_LAUNCH(k_tk_pick, pairs, dim3(kBlock), 0, s, lay, tk, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    if (R > 1)
-      SAEF_LAUNCH((k_tk_gather<kBlock>), chunks, dim3(kBlock), 0, s, lay, tk, R, row0, data, sel);
-    else
-      SAEF_LAUNCH((k_tk_gather<kBig>), chunks, dim3(kBig), 0, s, lay, tk, R, row0, data, sel);
+    SAEF_LAUNCH(k_tk_offsets, dim3((unsigned)(R * tk.n_groups)), dim3(kWave), 0, s, lay, tk, row0);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    SAEF_LAUNCH(k_tk_gather, tiles, dim3(kBlock), 0, s, lay, tk, R, row0, data, sel);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     SAEF_LAUNCH(k_tk_select, pairs, dim3(kBig), 0, s, lay, tk, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    SAEF_LAUNCH(k_tk_apply, chunks, dim3(kBlock), 0, s, lay, tk, R, row0, sel);
+    SAEF_LAUNCH(k_tk_apply, tiles, dim3(kBlock), 0, s, lay, tk, R, row0, sel);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     SAEF_LAUNCH(k_tk_scan, pairs, dim3(kBlock), 0, s, lay, tk, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    const dim3 tiles((unsigned)(per_wave_grid(lay) * R));
     if (x != nullptr)
       hipExtLaunchKernelGGL((k_tk_emit<true>), tiles, dim3(kBlock), 0, s, nullptr, last.stop, 0,
                             lay, tk, R, row0, data, sel, rank, vals, x);
@@ -783,7 +815,7 @@ hipError_t launch_topk_compress(const DevLayout& lay, const TkDev& tk, int K, fl
                                 const float* g, float* m, float* e, uint64_t* sel,
                                 uint32_t* rank, float* vals, hipStream_t s,
                                 const LaunchEvents& ev) {
-  const dim3 grid((unsigned)(tk.n_chunks * K));
+  const dim3 grid((unsigned)(lay.n_tiles * K));
   // the first kernel stamps the start event, the last one the stop event
   if (m != nullptr)
     hipExtLaunchKernelGGL((k_tk_delta<true>), grid, dim3(kBlock), 0, s, ev.start, nullptr, 0, lay,
