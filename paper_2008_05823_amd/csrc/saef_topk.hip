@@ -15,20 +15,24 @@
 //              k-th largest key and each group's first candidate slot;
 //   offsets    each tile's first candidate slot (a scan inside its group);
 //   gather     one wave per tile reads Delta once more: elements above b1
-//              are kept for sure and go to the selection words; the elements
-//              of b1 (the candidates) go to the tile's slots as
-//              (key, index in the tensor), in index order;
+//              are kept for sure and go to the selection words (their count
+//              to the tile's kept count); the elements of b1 (the
+//              candidates) go to the tile's slots as (key, index in the
+//              tensor), in index order;
 //   select     a workgroup per (row, tensor) finds, among the candidates only,
 //              the threshold key tau and the last kept index iota of the
 //              elements equal to tau (radix passes on the key bits below
 //              b1's prefix, then on the index), and places the next call's
 //              window around tau;
-//   apply      one wave per tile adds its kept candidates to the tile's
-//              selection words and counts the tile's kept elements.
-// Emit: an exclusive scan of the tile counts per tensor; then the rank words
-// and the kept values in index order, and the kept elements of the error set
-// to 0 (e = Delta - C(Delta) is Delta elsewhere).  All of it is integer
-// counting, so the kept set does not depend on the launch geometry.
+//   scan       a workgroup per (row, tensor) counts each tile's kept elements
+//              (its definite ones, from the gather, and its kept candidates)
+//              and turns the counts into each tile's first rank;
+//   emit       one wave per tile adds its kept candidates to its selection
+//              words, then writes the rank words and the kept values in
+//              index order, and sets the kept elements of the error to 0
+//              (e = Delta - C(Delta) is Delta elsewhere).
+// All of it is integer counting, so the kept set does not depend on the
+// launch geometry.
 //
 // The streaming passes (Delta, gather) run one short-lived workgroup or wave
 // per 2048-element tile: on MI355X a 2-read/1-write stream reaches about
@@ -320,9 +324,9 @@ __global__ __launch_bounds__(kWave) void k_tk_offsets(DevLayout lay, TkDev tk, i
 // ------------------------------------------------------------------ gather
 // Grid: per_wave_grid(lay) * R workgroups; wave w of workgroup b owns tile
 // 4 (b / R) + w of row b % R.  One read of the tile's Delta (all 32 words at
-// once): the selection words with the elements above b1 (kept for sure), and
-// the elements of b1 to the tile's candidate slots as key | (index in the
-// tensor) << 32, in index order.
+// once): the selection words with the elements above b1 (kept for sure) and
+// their count, and the elements of b1 to the tile's candidate slots as
+// key | (index in the tensor) << 32, in index order.
 __global__ __launch_bounds__(kBlock) void k_tk_gather(DevLayout lay, TkDev tk, int R, int row0,
                                                       const float* __restrict__ data,
                                                       uint64_t* __restrict__ sel) {
@@ -365,6 +369,10 @@ __global__ __launch_bounds__(kBlock) void k_tk_gather(DevLayout lay, TkDev tk, i
     base += (uint32_t)__popcll(cm);
   }
   if (lane < nw) sr[lane] = myw;
+  uint32_t ndef = (uint32_t)__popcll(myw);
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) ndef += __shfl_xor(ndef, off);
+  if (lane == 0) tk.tile_cnt[(int64_t)row * lay.n_tiles + ti] = ndef;  // kept for sure
 }
 
 // ------------------------------------------------------------------ select
@@ -456,82 +464,71 @@ __global__ __launch_bounds__(kBig) void k_tk_select(DevLayout lay, TkDev tk, int
   }
 }
 
-// ------------------------------------------------------------------ apply
-// Grid: per_wave_grid(lay) * R workgroups, one wave per tile (as the gather).
-// Adds the bits of the tile's kept candidates to its selection words (in
-// LDS, then written back) and stores the tile's kept count.
-__global__ __launch_bounds__(kBlock) void k_tk_apply(DevLayout lay, TkDev tk, int R, int row0,
-                                                     uint64_t* __restrict__ sel) {
-  __shared__ u64 words[kWaves][kTileWords];
-  const int r = (int)(blockIdx.x % (unsigned)R);
-  const int64_t ti = (int64_t)(blockIdx.x / (unsigned)R) * kWaves + wave_id();
-  const int wave = threadIdx.x / kWave;
-  const int lane = lane_id();
-  const bool live = ti < lay.n_tiles;  // every wave reaches the barriers
-  const int row = row0 + r;
-  Tile tile{};
-  int nw = 0;
-  uint64_t* sr = nullptr;
-  if (live) {
-    tile = lay.tiles[ti];
-    nw = (tile.count + 63) >> 6;
-    sr = sel + (int64_t)r * (lay.d_pad >> 6) + (tile.start >> 6);
-  }
-  if (lane < kTileWords) words[wave][lane] = lane < nw ? sr[lane] : 0ull;
-  __syncthreads();
-  if (live) {
-    const TkSel st = tk.sel[(int64_t)row * lay.L + tile.l];
-    const TensorInfo ten = lay.tensors[tile.l];
-    const int64_t rel0 = tile.start - ten.off;
-    const u64* slots = tk.cand + (int64_t)row * lay.d_pad + ten.off +
-                       tk.cand_off[(int64_t)row * lay.n_tiles + ti];
-    // the tile's candidates: the b1 count of its histogram
-    const uint32_t ncand = tile_hist(tk, lay, row, ti)[st.bin];
-    for (uint32_t i = lane; i < ncand; i += kWave) {
-      const u64 e = slots[i];
-      const uint32_t key = (uint32_t)e;
-      const int64_t idx = (int64_t)(e >> 32);
-      const int64_t q = idx - rel0;  // element of the tile
-      if ((key > st.tau || (key == st.tau && idx <= st.iota)) && q >= 0 && q < tile.count)
-        atomicOr(&words[wave][q >> 6], 1ull << (q & 63));
-    }
-  }
-  __syncthreads();
-  if (!live) return;
-  const u64 w = lane < nw ? words[wave][lane] : 0ull;
-  if (lane < nw) sr[lane] = w;
-  uint32_t n = (uint32_t)__popcll(w);
-#pragma unroll
-  for (int off = kWave / 2; off > 0; off >>= 1) n += __shfl_xor(n, off);
-  if (lane == 0) tk.tile_cnt[(int64_t)row * lay.n_tiles + ti] = n;
+// ------------------------------------------------------------------ emit
+// A tile's candidates: slots [first, first + n) of its (row, tensor)'s
+// candidate area (the next tile's first slot, or the candidate total after
+// the tensor's last tile).
+struct TileCands {
+  uint32_t first, n;
+};
+__device__ __forceinline__ TileCands tile_cands(const DevLayout& lay, const TkDev& tk, int row,
+                                                int64_t ti, const TensorInfo& ten, int64_t C) {
+  const uint32_t* co = tk.cand_off + (int64_t)row * lay.n_tiles;
+  const uint32_t first = co[ti];
+  const uint32_t end = ti + 1 < ten.first_tile + ten.ntiles ? co[ti + 1] : (uint32_t)C;
+  return TileCands{first, end - first};
 }
 
-// ------------------------------------------------------------------ emit
-// Grid: R * L workgroups: exclusive prefix of the kept counts over the
-// tensor's tiles, in tile order, in place.
+__device__ __forceinline__ bool cand_kept(u64 e, const TkSel& st) {
+  const uint32_t key = (uint32_t)e;
+  const int64_t idx = (int64_t)(e >> 32);
+  return key > st.tau || (key == st.tau && idx <= st.iota);
+}
+
+// Grid: R * L workgroups.  Each tile's kept count (the gather's count of
+// definite elements plus its kept candidates), then the exclusive prefix
+// over the tensor's tiles in tile order, in place.  The candidates of a
+// block of kBlock tiles are contiguous: the whole workgroup reads them and
+// counts the kept ones per tile in LDS.
 __global__ __launch_bounds__(kBlock) void k_tk_scan(DevLayout lay, TkDev tk, int row0) {
-  __shared__ uint32_t s[kBlock];
+  constexpr int kIlp = 4;
+  __shared__ uint32_t s_scan[kWaves];
+  __shared__ uint32_t s_cnt[kBlock];
   const int l = (int)(blockIdx.x % lay.L);
   const int r = (int)(blockIdx.x / lay.L);
-  const TensorInfo t = lay.tensors[l];
-  uint32_t* cnt = tk.tile_cnt + (int64_t)(row0 + r) * lay.n_tiles + t.first_tile;
+  const int row = row0 + r;
+  const TensorInfo ten = lay.tensors[l];
+  const TkSel st = tk.sel[(int64_t)row * lay.L + l];
+  const u64* cand = tk.cand + (int64_t)row * lay.d_pad + ten.off;
+  const uint32_t* co = tk.cand_off + (int64_t)row * lay.n_tiles + ten.first_tile;
+  uint32_t* cnt = tk.tile_cnt + (int64_t)row * lay.n_tiles + ten.first_tile;
   uint32_t carry = 0;
-  for (int b = 0; b < t.ntiles; b += kBlock) {
-    const int i = b + threadIdx.x;
-    const uint32_t v = i < t.ntiles ? cnt[i] : 0u;
-    s[threadIdx.x] = v;
+  for (int b = 0; b < ten.ntiles; b += kBlock) {
+    s_cnt[threadIdx.x] = 0;
     __syncthreads();
-    // inclusive scan (Hillis-Steele) in LDS
-    for (int off = 1; off < kBlock; off <<= 1) {
-      const uint32_t add = (int)threadIdx.x >= off ? s[threadIdx.x - off] : 0u;
-      __syncthreads();
-      s[threadIdx.x] += add;
-      __syncthreads();
+    const uint32_t lo = co[b];
+    const uint32_t hi = b + kBlock < ten.ntiles ? co[b + kBlock] : (uint32_t)st.cand;
+    for (uint32_t c0 = lo + threadIdx.x; c0 < hi; c0 += kBlock * kIlp) {
+      u64 e[kIlp];
+#pragma unroll
+      for (int u = 0; u < kIlp; ++u) {
+        const uint32_t c = c0 + u * kBlock;
+        e[u] = cand[c < hi ? c : lo];  // lo < hi here
+      }
+#pragma unroll
+      for (int u = 0; u < kIlp; ++u) {
+        const int64_t t = (int64_t)(e[u] >> 32) / kTileElems - b;  // tile of the block
+        if (c0 + u * kBlock < hi && cand_kept(e[u], st) && t >= 0 && t < kBlock)
+          atomicAdd(&s_cnt[t], 1u);
+      }
     }
-    if (i < t.ntiles) cnt[i] = carry + s[threadIdx.x] - v;
-    const uint32_t total = s[kBlock - 1];
     __syncthreads();
-    carry += total;
+    const int i = b + threadIdx.x;
+    const uint32_t v = i < ten.ntiles ? cnt[i] + s_cnt[threadIdx.x] : 0u;
+    uint32_t all;
+    const uint32_t before = block_excl_scan(v, s_scan, &all);  // ends with a barrier
+    if (i < ten.ntiles) cnt[i] = carry + before;
+    carry += all;
   }
 }
 
@@ -559,9 +556,10 @@ __device__ __forceinline__ int nth_set_bit(u64 w, uint32_t r) {
 }
 
 // Grid: per_wave_grid(lay) * R workgroups; wave w of workgroup b owns tile
-// 4 (b / R) + w of row b % R.  Rank words, the kept values in index order,
-// the kept elements of data set to 0; kX (server): x <- x - Delta at the
-// kept elements (C(Delta) is zero elsewhere).  Lane j loads selection word j
+// 4 (b / R) + w of row b % R.  The tile's kept candidates are added to its
+// selection words (LDS), then the rank words, the kept values in index order
+// and the kept elements of data set to 0; kX (server): x <- x - Delta at the
+// kept elements (C(Delta) is zero elsewhere).  Lane j holds selection word j
 // of the tile and a wave scan of the word counts gives every rank word; then
 // lane i takes the tile's kept elements i, i + 64, ...: its word by a binary
 // search over the scan, its bit by nth_set_bit, so the work follows the kept
@@ -569,28 +567,54 @@ __device__ __forceinline__ int nth_set_bit(u64 w, uint32_t r) {
 template <bool kX>
 __global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, int R, int row0,
                                                     float* __restrict__ data,
-                                                    const uint64_t* __restrict__ sel,
+                                                    uint64_t* __restrict__ sel,
                                                     uint32_t* __restrict__ rank,
                                                     float* __restrict__ vals,
                                                     float* __restrict__ x) {
   static_assert(kTileWords == 32, "five halving steps find a word of the tile");
+  __shared__ u64 words[kWaves][kTileWords];
   const int r = (int)(blockIdx.x % (unsigned)R);
   const int64_t ti = (int64_t)(blockIdx.x / (unsigned)R) * kWaves + wave_id();
-  if (ti >= lay.n_tiles) return;
-  const Tile tile = lay.tiles[ti];
-  const TkTensor t = tk.tens[tile.l];
+  const int wave = threadIdx.x / kWave;
   const int lane = lane_id();
-  const int nw = (tile.count + 63) >> 6;
+  const bool live = ti < lay.n_tiles;  // every wave reaches the barriers
+  const int row = row0 + r;
   const int64_t W = lay.d_pad >> 6;
+  Tile tile{};
+  int nw = 0;
+  uint64_t* sr = nullptr;
+  if (live) {
+    tile = lay.tiles[ti];
+    nw = (tile.count + 63) >> 6;
+    sr = sel + (int64_t)r * W + (tile.start >> 6);
+  }
+  if (lane < kTileWords) words[wave][lane] = lane < nw ? sr[lane] : 0ull;  // kept for sure
+  __syncthreads();
+  TensorInfo ten{};
+  if (live) {
+    ten = lay.tensors[tile.l];
+    const TkSel st = tk.sel[(int64_t)row * lay.L + tile.l];
+    const TileCands tc = tile_cands(lay, tk, row, ti, ten, st.cand);
+    const u64* slots = tk.cand + (int64_t)row * lay.d_pad + ten.off + tc.first;
+    const int64_t rel0 = tile.start - ten.off;
+    for (uint32_t i = lane; i < tc.n; i += kWave) {
+      const u64 e = slots[i];
+      const int64_t q = (int64_t)(e >> 32) - rel0;  // element of the tile
+      if (cand_kept(e, st) && q >= 0 && q < tile.count)
+        atomicOr(&words[wave][q >> 6], 1ull << (q & 63));
+    }
+  }
+  __syncthreads();
+  if (!live) return;
+  const TkTensor t = tk.tens[tile.l];
   float* dr = data + (int64_t)r * lay.d_pad + tile.start;
-  const uint64_t* sr = sel + (int64_t)r * W + (tile.start >> 6);
   uint32_t* rr = rank + (int64_t)r * W + (tile.start >> 6);
   float* vr = vals + (int64_t)r * tk.total_keep + t.voff;
   float* xt = kX ? x + tile.start : nullptr;
-  const uint32_t base = tk.tile_cnt[(int64_t)(row0 + r) * lay.n_tiles + ti];
+  const uint32_t base = tk.tile_cnt[(int64_t)row * lay.n_tiles + ti];
   // lane j: word j of the tile, its kept count and the inclusive prefix
-  const u64 my = sr[lane < nw ? lane : 0];
-  const u64 mine = lane < nw ? my : 0ull;
+  const u64 mine = lane < nw ? words[wave][lane] : 0ull;
+  if (lane < nw) sr[lane] = mine;
   const uint32_t c = (uint32_t)__popcll(mine);
   uint32_t incl = c;
 #pragma unroll
@@ -771,7 +795,7 @@ struct Launcher {
   hipStream_t s;
 
   // everything after the first pass for R rows of `data` (rows row0..):
-  // sums, pick, offsets, gather, select, apply, scan, emit.  The last kernel
+  // sums, pick, offsets, gather, select, scan, emit.  The last kernel
   // stamps the caller's stop event.
   hipError_t select_and_emit(int R, int row0, float* data, uint64_t* sel, uint32_t* rank,
                              float* vals, float* x, const LaunchEvents& last) const {
@@ -794,8 +818,6 @@ struct Launcher {
     SAEF_LAUNCH(k_tk_gather, tiles, dim3(kBlock), 0, s, lay, tk, R, row0, data, sel);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     SAEF_LAUNCH(k_tk_select, pairs, dim3(kBig), 0, s, lay, tk, row0);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
-    SAEF_LAUNCH(k_tk_apply, tiles, dim3(kBlock), 0, s, lay, tk, R, row0, sel);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     SAEF_LAUNCH(k_tk_scan, pairs, dim3(kBlock), 0, s, lay, tk, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;

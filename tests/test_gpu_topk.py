@@ -283,6 +283,58 @@ def test_topk_aggregate_parity(mode, K):
     assert gs.status() == 0
 
 
+# data scale of successive calls on one plan: the threshold falls far below
+# the histogram window placed by the previous call (the bin below it), far
+# above it (the bin above it), then back inside it
+SCALES = [1.0, 2.0 ** -20, 2.0 ** 30, 2.0 ** 30 * 1.5, 1.0]
+
+
+def test_topk_threshold_moves():
+    """Successive compress and server calls on one plan whose data scale jumps
+    by many binades: the kept set must not depend on where the previous
+    call's threshold placed the histogram window."""
+    K = 3
+    w = W.custom([5000, 70001, 300_000], K=K, scale_range=(1e-2, 1.0), seed=77)
+    keep = W.topk_keep(w, 1)
+    off, n, d_pad = w.layout()
+    msk = W.tensor_mask(w)
+    wm = H.tensor_word_mask(off, n, d_pad)
+    orc = TopkOracle(w, keep)
+    gs = TopkGpu(w, keep)
+    rng = np.random.default_rng(5)
+    for c, scale in enumerate(SCALES):
+        _case(f"topk threshold moves: call {c} scale {scale}")
+        sc = np.float32(scale)
+        g = (W.gradients(w, c) * sc).astype(np.float32)
+        e = (rng.standard_normal((K, d_pad)) * np.float32(0.01) * sc).astype(np.float32)
+        es = (rng.standard_normal(d_pad) * np.float32(0.01) * sc).astype(np.float32)
+        orc.e[:] = e
+        orc.e_srv[:] = es
+        assert orc.orc.topk_compress(K, LR, 0.0, keep, g, None, orc.e, orc.sel, orc.rank,
+                                     orc.vals) == 0
+        assert orc.orc.topk_aggregate(K, 1, keep, orc.sel, orc.vals, orc.x, orc.e_srv,
+                                      orc.srv_sel, orc.srv_rank, orc.srv_vals, None) == 0
+        gs.e.copy_(torch.from_numpy(e))
+        gs.e_srv.copy_(torch.from_numpy(es))
+        gs.saef.saef_topk_compress(gs.plan, K, float(LR), 0.0, H.dev(g), None, gs.e, gs.sel,
+                                   gs.rank, gs.vals)
+        gs.saef.saef_topk_aggregate(gs.plan, K, 1, gs.sel, gs.rank, gs.vals, gs.x, gs.e_srv,
+                                    gs.srv_sel, gs.srv_rank, gs.srv_vals)
+        torch.cuda.synchronize()
+        H.assert_words_equal(H.host(gs.sel, np.uint64), orc.sel, wm, f"selection, call {c}")
+        assert np.array_equal(_u32(gs.rank)[:, wm], orc.rank[:, wm]), f"rank words, call {c}"
+        H.assert_f32_equal(H.host(gs.vals), orc.vals, np.ones(orc.vals.shape[-1], bool),
+                           f"values, call {c}")
+        H.assert_f32_equal(H.host(gs.e), orc.e, msk, f"errors, call {c}")
+        H.assert_words_equal(H.host(gs.srv_sel, np.uint64), orc.srv_sel, wm,
+                             f"server selection, call {c}")
+        H.assert_f32_equal(H.host(gs.srv_vals), orc.srv_vals,
+                           np.ones(orc.srv_vals.shape[-1], bool), f"server values, call {c}")
+        H.assert_f32_equal(H.host(gs.e_srv), orc.e_srv, msk, f"server error, call {c}")
+        H.assert_f32_equal(H.host(gs.x), orc.x, msk, f"weights, call {c}")
+    assert gs.status() == 0
+
+
 ROUND_CASES = {
     "resnet56_1pct_dc": (W.get("resnet56").with_(rounds=12, period=0), 1, None),
     "resnet56_10pct_avg": (W.get("resnet56").with_(rounds=12, period=4), 10, None),
