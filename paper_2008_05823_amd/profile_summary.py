@@ -7,12 +7,16 @@ prints a short text summary:
 * per kernel: calls and average duration (kernel trace statistics);
 * per kernel: HBM bytes per dispatch from FETCH_SIZE and WRITE_SIZE, each
   scaled by the factor that makes the same counter read exactly the size of
-  a plain device-to-device copy of known size found in the same run.
+  a plain device-to-device copy of known size found in the same run;
+* or, from a kernel trace alone (``--trace``), per (kernel, workgroup count):
+  the dispatches after the first ``--skip`` ones, their average duration,
+  and the duration of the first one.
 
 Usage:
   python -m paper_2008_05823_amd.profile_summary --stats DIR/x_kernel_stats.csv
       --fetch DIR/y_counter_collection.csv --write DIR/z_counter_collection.csv
       --copy-bytes 2147483648 [--source-hash HASH]
+  python -m paper_2008_05823_amd.profile_summary --trace DIR/x_kernel_trace.csv [--skip N]
 """
 from __future__ import annotations
 
@@ -51,15 +55,41 @@ def copy_factor(per_kernel, copy_bytes: int, expect_kib: float) -> float:
     return (copy_bytes / 1024.0) / (sum(vals) / len(vals)) if expect_kib else 1.0
 
 
+def trace_table(path: str, skip: int) -> None:
+    """Per (kernel, workgroup count): dispatches after the first `skip`, their
+    average duration and the first dispatch's duration."""
+    runs = collections.defaultdict(list)
+    for r in csv.DictReader(open(path)):
+        wg = int(r["Grid_Size_X"]) // max(1, int(r["Workgroup_Size_X"]))
+        us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        runs[(short_name(r["Kernel_Name"]), wg)].append(us)
+    rows = []
+    for (name, wg), v in runs.items():
+        tail = v[skip:] or v
+        rows.append((sum(tail) / len(tail), name, wg, len(tail), v[0]))
+    print(f"  {'kernel':40s} {'workgroups':>10s} {'calls':>6s} {'avg_us':>10s} {'first_us':>10s}")
+    for avg, name, wg, n, first in sorted(rows, reverse=True):
+        if name.startswith("__amd") or name.startswith("void at::") or name.startswith("at::"):
+            continue
+        print(f"  {name:40s} {wg:10d} {n:6d} {avg:10.1f} {first:10.1f}")
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
-    ap.add_argument("--stats", required=True)
-    ap.add_argument("--fetch", required=True)
-    ap.add_argument("--write", required=True)
-    ap.add_argument("--copy-bytes", type=int, required=True,
+    ap.add_argument("--trace", default=None, help="kernel trace CSV (per launch shape table)")
+    ap.add_argument("--skip", type=int, default=0, help="first dispatches of each shape left out")
+    ap.add_argument("--stats")
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--copy-bytes", type=int,
                     help="bytes read (and written) by the reference device copy")
     ap.add_argument("--source-hash", default=None)
     args = ap.parse_args()
+    if args.trace:
+        trace_table(args.trace, args.skip)
+        return 0
+    if not (args.stats and args.fetch and args.write and args.copy_bytes):
+        ap.error("--stats, --fetch, --write and --copy-bytes are required without --trace")
 
     print("kernel durations (rocprofv3 --kernel-trace --stats)")
     print(f"  {'kernel':44s} {'calls':>6s} {'avg_us':>10s} {'pct':>7s}")

@@ -262,8 +262,8 @@ def _check_topk_row(delta, sel_words, vals, kept_count, tag):
 
 
 def test_full_size_topk_flat256m():
-    """Top-1% of one 2^28-element tensor (4096 histogram chunks: the
-    second reduction level), K = 8, iteration 0 of saef_topk_round, checked
+    """Top-1% of one 2^28-element tensor (131072 tiles: 2048 tile groups in
+    32 super-groups), K = 8, iteration 0 of saef_topk_round, checked
     against the defining properties of Top-K on every worker and on the
     server, and the error / weight updates bit for bit."""
     from tests.test_gpu_topk import TopkGpu

@@ -4,8 +4,9 @@
 The kept set is a discrete decision taken on exact keys on both sides, so
 everything is compared bit for bit: selection words, rank words, kept
 values, errors, weights.  Inputs include heavy ties (few distinct
-magnitudes), exact zeros of both signs, tensors spanning many histogram
-chunks (a second reduction level above 64 chunks) and ragged sizes.
+magnitudes), exact zeros of both signs, tensors spanning many tile groups
+(and super-groups above 4096 tiles), ragged sizes, and a data scale that
+jumps across the histogram window between calls.
 """
 import zlib
 
@@ -176,8 +177,9 @@ COMPRESS_CASES = {
     "adversarial_keep_all": (2, ADVERSARIAL, 100, "grad"),
     "ties_10pct": (4, [300_000, 77, 64, 4097], 10, "ties"),
     "ties_keep_one": (2, [5000, 1, 130], "one", "ties"),
-    "many_chunks": (2, [64 * 65536 + 4097, 33], 5, "grad"),   # > 64 chunks: second reduce level
-    "big_ties": (2, [70 * 65536 + 5], 1, "ties"),              # tie cut in a later chunk
+    "many_chunks": (2, [64 * 65536 + 4097, 33], 5, "grad"),   # 2050 tiles: 33 tile groups
+    "big_ties": (2, [70 * 65536 + 5], 1, "ties"),              # tie cut in a later group
+    "super_groups": (1, [4097 * 2048 + 77, 100], 1, "grad"),   # > 4096 tiles: super-groups
 }
 
 
@@ -220,21 +222,26 @@ def test_topk_compress_parity(name, momentum):
                                orc.rank, orc.vals)
     assert rc == 0
     gs = TopkGpu(w, keep, mu=mu)
-    gs.e.copy_(torch.from_numpy(e))
-    if momentum:
-        gs.m.copy_(torch.from_numpy(m0))
-    gs.saef.saef_topk_compress(gs.plan, K, float(LR), float(mu or 0.0), H.dev(g), gs.m, gs.e,
-                               gs.sel, gs.rank, gs.vals)
-    torch.cuda.synchronize()
     wm = H.tensor_word_mask(off, n, d_pad)
-    H.assert_words_equal(H.host(gs.sel, np.uint64), orc.sel, wm, "selection")
-    assert np.array_equal(_u32(gs.rank)[:, wm], orc.rank[:, wm]), "rank words"
-    H.assert_f32_equal(H.host(gs.vals), orc.vals, np.ones(orc.vals.shape[-1], bool), "values")
-    got_e = H.host(gs.e)
-    H.assert_f32_equal(got_e, orc.e, msk, "errors")
-    assert np.isnan(got_e[:, ~msk]).all(), "padding written"
-    if momentum:
-        H.assert_f32_equal(H.host(gs.m), orc.m, msk, "momentum buffers")
+    # the same inputs twice on one plan: the first call finds the threshold
+    # outside the histogram window (it starts at the bottom of the key range),
+    # the second one inside the window the first call placed
+    for call in range(2):
+        gs.e.copy_(torch.from_numpy(e))
+        if momentum:
+            gs.m.copy_(torch.from_numpy(m0))
+        gs.saef.saef_topk_compress(gs.plan, K, float(LR), float(mu or 0.0), H.dev(g), gs.m, gs.e,
+                                   gs.sel, gs.rank, gs.vals)
+        torch.cuda.synchronize()
+        H.assert_words_equal(H.host(gs.sel, np.uint64), orc.sel, wm, f"selection, call {call}")
+        assert np.array_equal(_u32(gs.rank)[:, wm], orc.rank[:, wm]), f"rank words, call {call}"
+        H.assert_f32_equal(H.host(gs.vals), orc.vals, np.ones(orc.vals.shape[-1], bool),
+                           f"values, call {call}")
+        got_e = H.host(gs.e)
+        H.assert_f32_equal(got_e, orc.e, msk, f"errors, call {call}")
+        assert np.isnan(got_e[:, ~msk]).all(), "padding written"
+        if momentum:
+            H.assert_f32_equal(H.host(gs.m), orc.m, msk, f"momentum buffers, call {call}")
     assert gs.status() == 0
 
 
