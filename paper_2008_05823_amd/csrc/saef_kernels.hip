@@ -719,73 +719,56 @@ __device__ __forceinline__ void mismatch_pass(const DevLayout& lay, int K, doubl
     if (kFull || u * 64 < lim) b += bs[u];
 }
 
-// One-read path (K <= kMisRegK): the decoded errors stay in registers; the
-// loads of kAvgChunk workers are issued together, sign words are read per
-// lane as the 32-bit half that holds the lane's bit.  Same arithmetic as
-// mismatch_pass.
-template <bool kDC, bool kDecE, bool kDecS, bool kFull, int kN>
+// One-read path (K <= kRK <= kMisRegK): the decoded errors stay in
+// registers.  All loads of the pass (the kRK workers' errors and sign-word
+// halves, e_srv and its word) are issued before the first one is used: rows
+// past K and lanes past the tile's end load an element that exists and are
+// masked afterwards.  Same arithmetic as mismatch_pass.
+template <bool kDC, bool kDecE, bool kDecS, bool kFull, int kN, int kRK>
 __device__ __forceinline__ void mismatch_pass_reg(const DevLayout& lay, int K, double inv_k,
-                                                  int l, int64_t base, int64_t gw, int lim,
+                                                  int64_t base, int64_t gw, int lim,
                                                   const float* __restrict__ e,
                                                   const uint64_t* __restrict__ signs,
-                                                  const float* __restrict__ scales,
+                                                  const float (&sc)[kRK],
                                                   const float* __restrict__ es,
                                                   const uint64_t* __restrict__ ss, float s_srv,
                                                   double& a, double& b) {
   const int lane = lane_id();
   const int64_t W = lay.d_pad >> 6;
   const int64_t d_pad = lay.d_pad;
-  float v[kMisRegK][kN];
-  double acc[kN];
-#pragma unroll
-  for (int u = 0; u < kN; ++u) acc[u] = 0.0;
+  float v[kRK][kN];
+  uint32_t hw[kRK][kN];
   float esv[kN];
   uint32_t hs[kN];
 #pragma unroll
   for (int u = 0; u < kN; ++u) {
     const bool ok = kFull || u * 64 < lim;
-    esv[u] = (kDC && ok) ? ld_nt(es + base + u * 64) : 0.0f;
+    const int64_t j = base + (ok ? u * 64 : -lane);  // the word's first element exists
+    esv[u] = kDC ? ld_nt(es + j) : 0.0f;
     hs[u] = kDecS ? half_word(ss + gw + u, lane) : 0u;
-  }
 #pragma unroll
-  for (int k0 = 0; k0 < kMisRegK; k0 += kAvgChunk) {
-    if (k0 >= K) break;
-    uint32_t hw[kAvgChunk][kN];
-#pragma unroll
-    for (int c = 0; c < kAvgChunk; ++c) {
-      const int k = k0 + c;
-      const bool kin = k < K;
-      const float* ek = e + (int64_t)k * d_pad + base;
-      const uint64_t* sk = signs + (int64_t)k * W + gw;
-#pragma unroll
-      for (int u = 0; u < kN; ++u) {
-        const bool ok = kFull || u * 64 < lim;
-        v[k][u] = (kin && ok) ? ld_nt(ek + u * 64) : 0.0f;
-        hw[c][u] = (kDecE && kin) ? half_word(sk + u, lane) : 0u;
-      }
-    }
-#pragma unroll
-    for (int c = 0; c < kAvgChunk; ++c) {
-      const int k = k0 + c;
-      if (k >= K) continue;
-      const float s = kDecE ? scales[(int64_t)k * lay.L + l] : 0.0f;
-#pragma unroll
-      for (int u = 0; u < kN; ++u) {
-        if (kDecE) v[k][u] = v[k][u] - (half_bit(hw[c][u], lane) ? s : -s);
-        acc[u] += (double)v[k][u];
-      }
+    for (int k = 0; k < kRK; ++k) {
+      const int64_t row = k < K ? k : 0;
+      v[k][u] = ld_nt(e + row * d_pad + j);
+      hw[k][u] = kDecE ? half_word(signs + row * W + gw + u, lane) : 0u;
     }
   }
 #pragma unroll
   for (int u = 0; u < kN; ++u) {
     const bool ok = kFull || u * 64 < lim;
-    const double ebar = mean_of(acc[u], inv_k, K);
+    double acc = 0.0;
+#pragma unroll
+    for (int k = 0; k < kRK; ++k) {
+      if (kDecE) v[k][u] = v[k][u] - (half_bit(hw[k][u], lane) ? sc[k] : -sc[k]);
+      if (k < K) acc += (double)v[k][u];  // worker order
+    }
+    const double ebar = mean_of(acc, inv_k, K);
     float ev = esv[u];
     if (kDecS) ev = ev - (half_bit(hs[u], lane) ? s_srv : -s_srv);
     const double uu = (double)ev + ebar;
     double bs = 0.0;
 #pragma unroll
-    for (int k = 0; k < kMisRegK; ++k) {
+    for (int k = 0; k < kRK; ++k) {
       if (k < K) {
         const double dk = uu - (double)v[k][u];
         bs += dk * dk;
@@ -804,8 +787,11 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
   return v;
 }
 
-// Grid: ceil(n_tiles / 4) workgroups; wave w of workgroup b owns tile 4b + w.
-template <bool kDC, bool kDecE, bool kDecS, bool kReg>
+// Grid: n_tiles workgroups; wave w of workgroup b takes words
+// [w kMisWaveWords, (w + 1) kMisWaveWords) of tile b, and the four waves'
+// sums are added in wave order.
+constexpr int kMisWaveWords = kTileElems / 64 / kWaves;  // 8
+template <bool kDC, bool kDecE, bool kDecS, int kRK>
 __global__ __launch_bounds__(kBlock) void k_mismatch(DevLayout lay, int K, double inv_k,
                                                      const float* __restrict__ e,
                                                      const uint64_t* __restrict__ signs,
@@ -813,31 +799,42 @@ __global__ __launch_bounds__(kBlock) void k_mismatch(DevLayout lay, int K, doubl
                                                      const float* __restrict__ es,
                                                      const uint64_t* __restrict__ ss,
                                                      const float* __restrict__ sscales) {
-  const int64_t ti = (int64_t)blockIdx.x * kWaves + wave_id();
-  if (ti >= lay.n_tiles) return;
+  static_assert(kMisWaveWords % kMisWords == 0 && kMisWaveWords % kMisRegWords == 0,
+                "a wave's words split into whole passes");
+  constexpr bool kReg = kRK > 0;
+  constexpr int kR = kReg ? kRK : 1;
+  __shared__ double s_a[kWaves];
+  __shared__ double s_b[kWaves];
+  const int64_t ti = blockIdx.x;
   const Tile tile = lay.tiles[ti];
   const int lane = lane_id();
+  const int wave = wave_id();
   const int nw = (tile.count + 63) >> 6;
   const float s_srv = kDecS ? sscales[tile.l] : 0.0f;
+  float sc[kR];  // the workers' scales of the tile's tensor (register path)
+#pragma unroll
+  for (int k = 0; k < kR; ++k)
+    sc[k] = (kReg && kDecE) ? scales[(int64_t)(k < K ? k : 0) * lay.L + tile.l] : 0.0f;
   constexpr int kW = kReg ? kMisRegWords : kMisWords;
   double a = 0.0, b = 0.0;
-  for (int wb = 0; wb < nw; wb += kW) {
+  const int wend = min(nw, (wave + 1) * kMisWaveWords);
+  for (int wb = wave * kMisWaveWords; wb < wend; wb += kW) {
     const int64_t base = tile.start + wb * 64 + lane;
     const int64_t gw = (tile.start >> 6) + wb;
     if ((wb + kW) * 64 <= tile.count) {
-      if (kReg)
-        mismatch_pass_reg<kDC, kDecE, kDecS, true, kW>(lay, K, inv_k, tile.l, base, gw, 0, e,
-                                                       signs, scales, es, ss, s_srv, a, b);
+      if constexpr (kReg)
+        mismatch_pass_reg<kDC, kDecE, kDecS, true, kW, kR>(lay, K, inv_k, base, gw, 0, e, signs,
+                                                           sc, es, ss, s_srv, a, b);
       else
         mismatch_pass<kDC, kDecE, kDecS, true, kW>(lay, K, inv_k, tile.l, base, gw, 0, e, signs,
                                                    scales, es, ss, s_srv, a, b);
     } else {
       for (int u = 0; u < min(kW, nw - wb); ++u) {
         const int lim = tile.count - (wb + u) * 64 - lane;
-        if (kReg)
-          mismatch_pass_reg<kDC, kDecE, kDecS, false, 1>(lay, K, inv_k, tile.l, base + u * 64,
-                                                         gw + u, lim, e, signs, scales, es, ss,
-                                                         s_srv, a, b);
+        if constexpr (kReg)
+          mismatch_pass_reg<kDC, kDecE, kDecS, false, 1, kR>(lay, K, inv_k, base + u * 64, gw + u,
+                                                             lim, e, signs, sc, es, ss, s_srv, a,
+                                                             b);
         else
           mismatch_pass<kDC, kDecE, kDecS, false, 1>(lay, K, inv_k, tile.l, base + u * 64,
                                                      gw + u, lim, e, signs, scales, es, ss,
@@ -848,9 +845,19 @@ __global__ __launch_bounds__(kBlock) void k_mismatch(DevLayout lay, int K, doubl
   a = wave_sum_f64(a);
   b = wave_sum_f64(b);
   if (lane == 0) {
+    s_a[wave] = a;
+    s_b[wave] = b;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double ta = 0.0, tb = 0.0;
+    for (int w = 0; w < kWaves; ++w) {
+      ta += s_a[w];
+      tb += s_b[w];
+    }
     u64* p = lay.part + ti * 2;
-    p[0] = (u64)__double_as_longlong(a);
-    p[1] = (u64)__double_as_longlong(b);
+    p[0] = (u64)__double_as_longlong(ta);
+    p[1] = (u64)__double_as_longlong(tb);
   }
 }
 
@@ -1047,15 +1054,17 @@ hipError_t launch_mismatch(const DevLayout& lay, int K, int mode, const float* e
                            const float* e_srv, const uint64_t* srv_signs,
                            const float* srv_scales, bool decode_s, double* out, hipStream_t s,
                            const LaunchEvents& ev) {
-  const dim3 grid(per_wave_grid(lay));
+  const dim3 grid((unsigned)lay.n_tiles);
   const double ik = inv_pow2(K);
 #define SAEF_MIS2(DC, DE, DS, R)                                                               \
   hipExtLaunchKernelGGL((k_mismatch<DC, DE, DS, R>), grid, dim3(kBlock), 0, s, ev.start,        \
                         nullptr, 0, lay, K, ik, e, signs, scales, e_srv, srv_signs, srv_scales)
 #define SAEF_MIS(DC, DE, DS)                                  \
   do {                                                        \
-    if (K <= kMisRegK) SAEF_MIS2(DC, DE, DS, true);           \
-    else SAEF_MIS2(DC, DE, DS, false);                        \
+    if (K <= 4) SAEF_MIS2(DC, DE, DS, 4);                     \
+    else if (K <= 8) SAEF_MIS2(DC, DE, DS, 8);                \
+    else if (K <= kMisRegK) SAEF_MIS2(DC, DE, DS, kMisRegK);  \
+    else SAEF_MIS2(DC, DE, DS, 0);                            \
   } while (0)
   if (mode == 1) {
     if (decode_e) {

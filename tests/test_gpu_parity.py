@@ -301,6 +301,10 @@ SPLIT_CASES = {
     "ragged_sc": W.custom(ADVERSARIAL + [70001], K=3, period=3, rounds=7, mode=0,
                           scale_range=(1e-4, 1e-1), dist="laplace_zeros", seed=998),
     "flat64k_no_avg": W.get("flat64k").with_(period=0, rounds=6),
+    # the mismatch kernel keeps up to 4, 8 or 16 workers in registers, and
+    # reads the errors twice above 16
+    "k12_avg": W.custom(ADVERSARIAL + [9000], K=12, period=3, rounds=4, seed=41),
+    "k20_dc": W.custom([4097, 65, 30000], K=20, period=2, rounds=4, seed=42),
 }
 
 
