@@ -322,6 +322,41 @@ __global__ __launch_bounds__(kWave) void k_tk_offsets(DevLayout lay, TkDev tk, i
 }
 
 // ------------------------------------------------------------------ gather
+// The smallest key of bin b for the window at win; kTkHist (one past the
+// last bin) gives 2^31, above every key.
+__device__ __forceinline__ uint32_t bin_floor(uint32_t b, uint32_t win) {
+  if (b == 0u) return 0u;
+  if (b >= (uint32_t)kTkHist) return 0x80000000u;
+  const u64 f = (u64)win + ((u64)(b - 1u) << kTkSubShift);
+  return f < 0x80000000ull ? (uint32_t)f : 0x80000000u;
+}
+
+// The gather's classification of a tile's 32 words (kFull: all 2048
+// elements exist): selection words (lane u gets word u) and candidates to
+// their slots in index order.
+template <bool kFull>
+__device__ __forceinline__ void gather_words(const float (&v)[kTileWords], int count, uint32_t lo,
+                                             uint32_t up, int64_t rel0, uint32_t nslots,
+                                             u64* __restrict__ slots, u64& myw, uint32_t& base) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int u = 0; u < kTileWords; ++u) {
+    const int j = u * 64 + lane;
+    const bool ok = kFull || j < count;
+    const uint32_t key = key_of(v[u]);
+    const u64 word = __ballot(ok && key >= up);
+    if (lane == u) myw = word;
+    const u64 cm = __ballot(ok && key - lo < up - lo);  // lo <= key < up
+    if (cm != 0ull) {  // wave-uniform: most words have no candidate
+      const uint32_t pos = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(cm >> 32),
+                                                            __builtin_amdgcn_mbcnt_lo((uint32_t)cm, 0u));
+      if (((cm >> lane) & 1ull) && pos < nslots)  // pos < nslots always holds
+        slots[pos] = (u64)key | ((u64)(rel0 + j) << 32);
+      base += (uint32_t)__popcll(cm);
+    }
+  }
+}
+
 // Grid: per_wave_grid(lay) * R workgroups; wave w of workgroup b owns tile
 // 4 (b / R) + w of row b % R.  One read of the tile's Delta (all 32 words at
 // once): the selection words with the elements above b1 (kept for sure) and
@@ -352,22 +387,14 @@ __global__ __launch_bounds__(kBlock) void k_tk_gather(DevLayout lay, TkDev tk, i
     const int j = u * 64 + lane;
     v[u] = ld_nt_or0(dr, j, j < tile.count);
   }
+  // bin b1 holds the keys [lo, up): above it kept for sure, inside it candidates
+  const uint32_t lo = bin_floor(b1, win), up = bin_floor(b1 + 1u, win);
   u64 myw = 0;        // lane u < nw: selection word u
   uint32_t base = 0;  // candidates in the earlier words
-#pragma unroll
-  for (int u = 0; u < kTileWords; ++u) {
-    const int j = u * 64 + lane;
-    const bool ok = j < tile.count;
-    const uint32_t hi = hist_bin(key_of(v[u]), win);
-    const u64 word = __ballot(ok && hi > b1);
-    if (lane == u) myw = word;
-    const u64 cm = __ballot(ok && hi == b1);
-    const uint32_t pos = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(cm >> 32),
-                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)cm, 0u));
-    if (((cm >> lane) & 1ull) && pos < nslots)  // pos < nslots always holds
-      slots[pos] = (u64)key_of(v[u]) | ((u64)(rel0 + j) << 32);
-    base += (uint32_t)__popcll(cm);
-  }
+  if (tile.count == kTileElems)
+    gather_words<true>(v, tile.count, lo, up, rel0, nslots, slots, myw, base);
+  else
+    gather_words<false>(v, tile.count, lo, up, rel0, nslots, slots, myw, base);
   if (lane < nw) sr[lane] = myw;
   uint32_t ndef = (uint32_t)__popcll(myw);
 #pragma unroll
