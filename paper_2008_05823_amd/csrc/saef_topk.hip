@@ -599,29 +599,27 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, int
                                                     float* __restrict__ vals,
                                                     float* __restrict__ x) {
   static_assert(kTileWords == 32, "five halving steps find a word of the tile");
-  __shared__ u64 words[kWaves][kTileWords];
+  __shared__ u64 words[kWaves][kTileWords];  // one row per wave, used by that wave only
   const int r = (int)(blockIdx.x % (unsigned)R);
   const int64_t ti = (int64_t)(blockIdx.x / (unsigned)R) * kWaves + wave_id();
+  if (ti >= lay.n_tiles) return;
   const int wave = threadIdx.x / kWave;
   const int lane = lane_id();
-  const bool live = ti < lay.n_tiles;  // every wave reaches the barriers
   const int row = row0 + r;
   const int64_t W = lay.d_pad >> 6;
-  Tile tile{};
-  int nw = 0;
-  uint64_t* sr = nullptr;
-  if (live) {
-    tile = lay.tiles[ti];
-    nw = (tile.count + 63) >> 6;
-    sr = sel + (int64_t)r * W + (tile.start >> 6);
-  }
-  if (lane < kTileWords) words[wave][lane] = lane < nw ? sr[lane] : 0ull;  // kept for sure
-  __syncthreads();
-  TensorInfo ten{};
-  if (live) {
-    ten = lay.tensors[tile.l];
-    const TkSel st = tk.sel[(int64_t)row * lay.L + tile.l];
-    const TileCands tc = tile_cands(lay, tk, row, ti, ten, st.cand);
+  const Tile tile = lay.tiles[ti];
+  const int nw = (tile.count + 63) >> 6;
+  uint64_t* sr = sel + (int64_t)r * W + (tile.start >> 6);
+  const TensorInfo ten = lay.tensors[tile.l];
+  const TkSel st = tk.sel[(int64_t)row * lay.L + tile.l];
+  const TkTensor t = tk.tens[tile.l];
+  const TileCands tc = tile_cands(lay, tk, row, ti, ten, st.cand);
+  const uint32_t base = tk.tile_cnt[(int64_t)row * lay.n_tiles + ti];
+  // lane j: word j of the tile (the gather's elements kept for sure)
+  u64 mine = lane < nw ? sr[lane] : 0ull;
+  if (tc.n > 0) {  // wave-uniform: add the kept candidates' bits
+    if (lane < kTileWords) words[wave][lane] = mine;
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     const u64* slots = tk.cand + (int64_t)row * lay.d_pad + ten.off + tc.first;
     const int64_t rel0 = tile.start - ten.off;
     for (uint32_t i = lane; i < tc.n; i += kWave) {
@@ -630,18 +628,14 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, int
       if (cand_kept(e, st) && q >= 0 && q < tile.count)
         atomicOr(&words[wave][q >> 6], 1ull << (q & 63));
     }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    mine = lane < nw ? words[wave][lane] : 0ull;
+    if (lane < nw) sr[lane] = mine;
   }
-  __syncthreads();
-  if (!live) return;
-  const TkTensor t = tk.tens[tile.l];
   float* dr = data + (int64_t)r * lay.d_pad + tile.start;
   uint32_t* rr = rank + (int64_t)r * W + (tile.start >> 6);
   float* vr = vals + (int64_t)r * tk.total_keep + t.voff;
   float* xt = kX ? x + tile.start : nullptr;
-  const uint32_t base = tk.tile_cnt[(int64_t)row * lay.n_tiles + ti];
-  // lane j: word j of the tile, its kept count and the inclusive prefix
-  const u64 mine = lane < nw ? words[wave][lane] : 0ull;
-  if (lane < nw) sr[lane] = mine;
   const uint32_t c = (uint32_t)__popcll(mine);
   uint32_t incl = c;
 #pragma unroll
