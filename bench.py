@@ -145,7 +145,13 @@ def main() -> int:
     ap.add_argument("--kernel-events", choices=("on", "off"), default="on",
                     help="HIP events around each kernel in the timed region (roofline); "
                          "'off' times the iterations alone")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay each iteration from a HIP graph (one captured per kind of "
+                         "iteration: gradient buffer, error averaging or not); implies "
+                         "--kernel-events off")
     args = ap.parse_args()
+    if args.graph:
+        args.kernel_events = "off"
 
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (got --gpus {args.gpus}); the "
@@ -221,6 +227,29 @@ def main() -> int:
     for t in range(args.warmup):
         step(t)
     torch.cuda.synchronize()
+    run = step
+    if args.graph:
+        # one graph per kind of iteration in the timed range; capturing
+        # records the launches without running them
+        if args.warmup < 1:
+            print("bench.py: --graph needs --warmup >= 1 (t = 0 is the plain-state iteration)",
+                  file=sys.stderr)
+            return 2
+        graphs = {}
+
+        def kind(t):
+            return (t % n_grad, bool(w.period and (t + 1) % w.period == 0))
+
+        for t in range(args.warmup, args.warmup + args.steps):
+            if kind(t) not in graphs:
+                graph = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(graph):
+                    step(t)
+                graphs[kind(t)] = graph
+        torch.cuda.synchronize()
+
+        def run(t):
+            graphs[kind(t)].replay()
     # timed region: K iterations; the dispatches of the dominant kernel
     # (worker compression) stamp HIP events on the launch stream
     if args.kernel_events == "on":
@@ -229,7 +258,7 @@ def main() -> int:
     torch.cuda.synchronize()
     start.record()
     for i in range(args.steps):
-        step(args.warmup + i)
+        run(args.warmup + i)
     stop.record()
     torch.cuda.synchronize()
     ms_total = start.elapsed_time(stop)
@@ -307,7 +336,8 @@ def main() -> int:
                    **({"momentum": mu} if mu is not None else {}),
                    **({"variant": "ef"} if args.variant == "ef" else {}),
                    **({"mismatch": True} if args.mismatch else {}),
-                   **({"topk_percent": args.topk} if topk is not None else {})},
+                   **({"topk_percent": args.topk} if topk is not None else {}),
+                   **({"graph": True} if args.graph else {})},
         "worker_params_per_s": K * d / (ms_per_step * 1e-3),
         "round_hbm_gbps": bytes_round / (ms_per_step * 1e-3) / 1e9,
         "round_frac_of_peak": bytes_round / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,

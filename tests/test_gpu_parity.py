@@ -393,3 +393,35 @@ def test_round_halves_invalid():
                            torch.zeros(2, dtype=torch.float64, device="cuda"))
     torch.cuda.synchronize()
     assert gs.status() == 0
+
+
+# ---------------------------------------------------------------- HIP graphs
+
+def test_graph_replay_parity():
+    """saef_round captured in HIP graphs (torch.cuda.CUDAGraph, the library
+    launching on the capture stream): one graph per kind of iteration (t = 0
+    with plain state, pending state, pending state with error averaging),
+    replayed over the iterations with the gradients copied in eagerly between
+    replays and the state checked against the oracle after every replay."""
+    w = W.get("resnet56").with_(period=4, rounds=10)
+    _case(f"graph replay resnet56 K={w.K} rounds={w.rounds}")
+    orc = H.OracleState(w)
+    gs = H.GpuState(w)
+    S = gs.saef
+    graphs = {}
+    for t in range(w.rounds):
+        kind = (t > 0, (t + 1) % w.period == 0)
+        if kind not in graphs:
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                S.saef_round(gs.layout, t, w.period, gs.K, w.lr, w.mode, gs.g, gs.e, gs.e_srv,
+                             gs.x, gs.xh, gs.signs, gs.scales, gs.srv_signs, gs.srv_scales)
+            graphs[kind] = graph
+        grad = W.gradients(w, t)
+        gs.g.copy_(torch.from_numpy(grad))
+        graphs[kind].replay()
+        torch.cuda.synchronize()
+        orc.round(t, grad)
+        H.compare_state(gs.plain(), orc, t, "graph replay")
+    assert len(graphs) == 3
+    assert gs.status() == 0

@@ -442,3 +442,32 @@ def test_topk_invalid_and_range():
     saef.saef_topk_compress(gs.plan, 2, 0.1, 0.0, g, None, gs.e, gs.sel, gs.rank, gs.vals)
     assert gs.status() == saef.ERANGE
     assert gs.status() == saef.OK        # the flag clears
+
+
+def test_topk_graph_replay_parity():
+    """saef_topk_round captured in HIP graphs (one per kind of iteration:
+    plain averaging or not), replayed with the gradients copied in between
+    replays and checked against the oracle after every replay."""
+    w = W.get("resnet56").with_(rounds=8, period=4)
+    keep = W.topk_keep(w, 5)
+    _case(f"topk graph replay resnet56 K={w.K} rounds={w.rounds}")
+    orc = TopkOracle(w, keep)
+    gs = TopkGpu(w, keep)
+    S = gs.saef
+    graphs = {}
+    for t in range(w.rounds):
+        kind = (t + 1) % w.period == 0
+        if kind not in graphs:
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                S.saef_topk_round(gs.plan, t, w.period, gs.K, w.lr, 0.0, w.mode, gs.g, None, gs.e,
+                                  gs.e_srv, gs.x, gs.xh, gs.sel, gs.rank, gs.vals, gs.srv_sel,
+                                  gs.srv_rank, gs.srv_vals)
+            graphs[kind] = graph
+        grad = W.gradients(w, t)
+        gs.g.copy_(torch.from_numpy(grad))
+        graphs[kind].replay()
+        torch.cuda.synchronize()
+        orc.round(t, grad)
+        compare_topk(gs, orc, t, "graph replay", mode=w.mode)
+    assert gs.status() == 0
