@@ -223,9 +223,14 @@ int saef_materialize(const saef_layout* layout, int32_t K, int32_t mode, const f
 typedef struct saef_topk saef_topk;
 
 /* Top-K plan on a layout: keep[L] (host, 1 <= keep[l] <= n[l]) is copied;
- * the plan owns the selection scratch (per-chunk histograms, selection
- * state, tile counts).  Calls using one plan must not run concurrently.
- * Synchronises the device; the layout must outlive the plan. */
+ * the plan owns the selection scratch (tile histograms and their sums,
+ * selection state, candidate slots, tile counts: about 8.3 bytes per
+ * element of d_pad for each of the k_max + 1 rows).  The selection state
+ * keeps, per worker row and tensor, where the last call found its threshold:
+ * the next call's histogram is placed there, so the first call on a plan (or
+ * one after the data scale jumped by more than about two binades) takes
+ * longer; the results never depend on it.  Calls using one plan must not run
+ * concurrently.  Synchronises the device; the layout must outlive the plan. */
 int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk** out);
 int saef_topk_destroy(saef_topk* plan);
 /* total = sum keep, the length of one message's value array. */
