@@ -11,8 +11,6 @@ namespace saef {
 
 typedef unsigned long long u64;
 
-constexpr int kXcds = 8;  // MI355X: 8 XCDs, workgroups dealt round-robin
-
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 __device__ __forceinline__ int wave_id() {
   return __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -46,6 +44,18 @@ __device__ __forceinline__ double mean_of(double acc, double inv_k, int K) {
 
 // Host: 1/K when K is a power of two (then acc * inv_k == acc / K exactly), else 0.
 inline double inv_pow2(int K) { return (K & (K - 1)) == 0 ? 1.0 / (double)K : 0.0; }
+
+// The (row, tile) of workgroup b when each tile has `rows` workgroups: along
+// a run, tile by tile, then the next row on the same run.  ti may be past the
+// last tile (the grid is rounded up to whole groups).
+__device__ __forceinline__ void run_tile_of(unsigned b, int rows, int s, int& row, int64_t& ti) {
+  const unsigned xcd = b % kXcds, r = b / kXcds;
+  const unsigned j = r & ((1u << s) - 1u);
+  const unsigned u = r >> s;
+  row = (int)(u % (unsigned)rows);
+  const int64_t grp = u / (unsigned)rows;
+  ti = ((grp * kXcds + xcd) << s) + j;
+}
 
 // Workgroups of 4 waves, one wave per tile.
 inline unsigned per_wave_grid(const DevLayout& lay) {

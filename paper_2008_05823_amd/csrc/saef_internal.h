@@ -17,6 +17,22 @@ constexpr int kTileElems = SAEF_TILE_ELEMS;  // default work tile (elements, mul
 constexpr int kMaxTilesPerTensor = 1 << 17;  // 2048-element tiles up to 2^28 elements
 constexpr int kFinChunk = 4096;              // tile partials per finalize workgroup
 constexpr int64_t kMaxTensor = int64_t(1) << 28;
+constexpr int kXcds = 8;  // MI355X: 8 XCDs, workgroups dealt round-robin
+
+// XCD-aware tile order.  Workgroups are dealt to the 8 XCDs round-robin
+// (XCD b mod 8); XCD x takes run x of every group of 8 runs of 2^s
+// consecutive tiles, so each XCD streams contiguous memory and sees every
+// row (worker) of its tiles, which shares x through its L2.  Long runs
+// (s = 6, 512 KB of a row) stream best on large layouts (measured: -15% for
+// the step ahead at 2^28 parameters); layouts of fewer than 2048 tiles keep
+// s = 0, where long runs would leave XCDs idle.
+__host__ __device__ inline int tile_run_shift(int64_t n_tiles) { return n_tiles >= 2048 ? 6 : 0; }
+
+// Tiles rounded up to whole groups of 8 runs.
+inline int64_t run_padded_tiles(int64_t n_tiles) {
+  const int64_t g = (int64_t)kXcds << tile_run_shift(n_tiles);
+  return (n_tiles + g - 1) / g * g;
+}
 
 // One unit of work: `count` consecutive elements of tensor `l` starting at
 // absolute element index `start` (a multiple of 64).

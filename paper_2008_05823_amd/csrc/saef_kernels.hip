@@ -342,12 +342,12 @@ __device__ __forceinline__ void step_words(int w0, int nw, int count,
   }
 }
 
-// Grid: ceil(n_tiles / 8) * 8 * K workgroups, one per (tile, worker).  The K
-// workgroups of a tile are consecutive in dispatch order on one XCD
-// (workgroups go to the XCDs round-robin), so x is fetched from HBM once and
-// re-read from that XCD's L2.  x itself is not written: the pending
-// re-update of x is applied here on the fly and materialized by the
-// aggregate kernel.  kHasE false (K = 1, e unused): xh = x_t.
+// Grid: run_padded_tiles(n_tiles) * K workgroups, one per (tile, worker), in
+// the XCD-aware tile order of run_tile_of: the K workers of a run of tiles
+// follow one another on one XCD, so x is fetched from HBM once and re-read
+// from that XCD's L2.  x itself is not written: the pending re-update of x
+// is applied here on the fly and materialized by the aggregate kernel.
+// kHasE false (K = 1, e unused): xh = x_t.
 template <bool kDecX, bool kDecE, bool kHasE>
 __global__ __launch_bounds__(kBlock) void k_step(DevLayout lay, int K, const float* __restrict__ x,
                                                  const uint64_t* __restrict__ ss,
@@ -356,10 +356,9 @@ __global__ __launch_bounds__(kBlock) void k_step(DevLayout lay, int K, const flo
                                                  const uint64_t* __restrict__ signs,
                                                  const float* __restrict__ scales,
                                                  float* __restrict__ xh) {
-  const unsigned b = blockIdx.x;
-  const unsigned r = b / kXcds;
-  const int k = (int)(r % (unsigned)K);
-  const int64_t ti = (int64_t)(r / (unsigned)K) * kXcds + (b % kXcds);
+  int k;
+  int64_t ti;
+  run_tile_of(blockIdx.x, K, tile_run_shift(lay.n_tiles), k, ti);
   if (ti >= lay.n_tiles) return;
   const Tile tile = lay.tiles[ti];
   const int wave = wave_id();
@@ -460,8 +459,9 @@ __device__ __forceinline__ void average_words(const DevLayout& lay, int K, doubl
   }
 }
 
-// Grid: n_tiles workgroups; wave w takes words w*kU .. w*kU+kU-1 of the tile,
-// then strides by 4*kU words.
+// Grid: run_padded_tiles(n_tiles) workgroups, one per tile in the XCD-aware
+// tile order of run_tile_of; wave w takes words w*kU .. w*kU+kU-1 of the
+// tile, then strides by 4*kU words.
 template <bool kDecX, bool kDecE, bool kXh>
 __global__ __launch_bounds__(kBlock) void k_step_average(DevLayout lay, int K, double inv_k,
                                                          const float* __restrict__ x,
@@ -471,7 +471,11 @@ __global__ __launch_bounds__(kBlock) void k_step_average(DevLayout lay, int K, d
                                                          const uint64_t* __restrict__ signs,
                                                          const float* __restrict__ scales,
                                                          float* __restrict__ xh) {
-  const Tile tile = lay.tiles[blockIdx.x];
+  int row0;
+  int64_t ti;
+  run_tile_of(blockIdx.x, 1, tile_run_shift(lay.n_tiles), row0, ti);
+  if (ti >= lay.n_tiles) return;
+  const Tile tile = lay.tiles[ti];
   const int wave = wave_id();
   const int nw = (tile.count + 63) >> 6;
   const float s_x = kDecX ? sscales[tile.l] : 0.0f;
@@ -987,7 +991,7 @@ hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
                              bool average, float* xh, hipStream_t s, const LaunchEvents& ev) {
   if (decode_x && !decode_e) return hipErrorInvalidValue;  // never requested
   if (average) {
-    const dim3 grid((unsigned)lay.n_tiles);
+    const dim3 grid((unsigned)run_padded_tiles(lay.n_tiles));
     const double ik = inv_pow2(K);
 #define SAEF_AV(DX, DE, XH)                                                                  \
   SAEF_LAUNCH((k_step_average<DX, DE, XH>), grid, dim3(kBlock), 0, s, lay, K, ik, x, \
@@ -1005,7 +1009,7 @@ hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
 #undef SAEF_AV
   } else {
     if (xh == nullptr) return hipErrorInvalidValue;
-    const dim3 grid((unsigned)((lay.n_tiles + kXcds - 1) / kXcds * kXcds * K));
+    const dim3 grid((unsigned)(run_padded_tiles(lay.n_tiles) * K));
 #define SAEF_ST(DX, DE)                                                                \
   SAEF_LAUNCH((k_step<DX, DE, true>), grid, dim3(kBlock), 0, s, lay, K, x, srv_signs, \
                      srv_scales, e, signs, scales, xh)
@@ -1024,7 +1028,7 @@ hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
 hipError_t launch_weights(const DevLayout& lay, const float* x, const uint64_t* srv_signs,
                           const float* srv_scales, bool decode_x, float* xh, hipStream_t s,
                           const LaunchEvents& ev) {
-  const dim3 grid((unsigned)((lay.n_tiles + kXcds - 1) / kXcds * kXcds));
+  const dim3 grid((unsigned)run_padded_tiles(lay.n_tiles));
   if (decode_x) {
     SAEF_LAUNCH((k_step<true, false, false>), grid, dim3(kBlock), 0, s, lay, 1, x, srv_signs,
                 srv_scales, nullptr, nullptr, nullptr, xh);
