@@ -99,7 +99,20 @@ def cpu_baseline(w, grads_host, x0, rounds: int, keep=None) -> dict:
             "sample": f"{rounds} full iterations (t=0..{rounds - 1}) of the {w.name} workload, "
                       f"K={K}, single-threaded C oracle"
                       + (" (Top-K)" if keep is not None else "")
-                      + f", {per_round:.2f} s per iteration"}
+                      + f", {per_round:.2f} s per iteration",
+            "host_cpu": host_cpu_model(), "host_threads": os.cpu_count()}
+
+
+def host_cpu_model() -> str:
+    """The host CPU's model name (Linux /proc/cpuinfo), or "unknown"."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def copy_probe_gbps(nbytes: int = 2 << 30) -> float:
