@@ -48,7 +48,7 @@ namespace saef {
 namespace {
 
 constexpr uint32_t kFiniteLimit = 0x7F800000u;  // keys >= this are Inf or NaN
-constexpr int kTkU = 4;                         // words per wave per pass (Delta pass)
+constexpr int kTkU = 8;                         // words per wave per pass (Delta pass: one pass)
 constexpr int kTileWords = kTileElems / 64;     // 32
 constexpr int kBig = 1024;                      // threads of the per-(row, tensor) kernels
 static_assert(kTileWords <= kWave, "one selection word of a tile per lane");
