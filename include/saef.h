@@ -288,13 +288,16 @@ int saef_status(const saef_layout* layout, hipStream_t stream);
  * copy of x_t for local error feedback, 1 = worker compression, 2 = worker
  * scales from the tile sums, 3 = server aggregation, 4 = server scales, 5 =
  * error averaging (with step ahead in the SAEF variant), 6 = mismatch
- * bounds), until the pairs run out.  saef_profile_read waits for the
+ * bounds), until the pairs run out; with every > 1 only the 1st, (every+1)-th,
+ * ... dispatch of each timed kind since the call is stamped (a sample spread
+ * over the run; every < 1 is SAEF_EINVAL).  saef_profile_read waits for the
  * recorded events and returns, per kind, the number of launches timed
  * (counts[7]) and their summed durations in milliseconds (total_ms[7]), then
  * starts over with all pairs free.  capacity 0 releases
  * the events and stops recording.  Timed dispatches cost a few microseconds
  * each, so time only the kernels of interest. */
-int saef_profile_enable(saef_layout* layout, int32_t capacity, uint32_t kind_mask);
+int saef_profile_enable(saef_layout* layout, int32_t capacity, uint32_t kind_mask,
+                        int32_t every);
 int saef_profile_read(saef_layout* layout, int32_t* counts, double* total_ms);
 
 /* Host-side query of a layout: tensor count, padded length, worker limit and

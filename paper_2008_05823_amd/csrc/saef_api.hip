@@ -15,6 +15,10 @@ using saef::DevLayout;
 using saef::TensorInfo;
 using saef::Tile;
 
+// Kernel kinds timed by saef_profile_enable (step ahead, compression, worker
+// scales, aggregation, server scales, averaging, mismatch).
+constexpr int kProfileKinds = 7;
+
 struct saef_layout {
   int device = 0;
   int32_t L = 0;
@@ -33,6 +37,8 @@ struct saef_layout {
   std::vector<int> ev_kind;
   size_t ev_used = 0;
   uint32_t ev_mask = 0;  // kinds being timed
+  int32_t ev_every = 1;  // every ev_every-th dispatch of a timed kind is stamped
+  int64_t ev_seen[kProfileKinds] = {};  // dispatches of each kind since enable
 };
 
 // A Top-K plan: the kept count of every tensor and the selection scratch.
@@ -53,6 +59,7 @@ struct saef_topk {
   void* mem_tile_cnt = nullptr;
   void* mem_cand = nullptr;
   void* mem_cand_off = nullptr;
+  void* mem_spec = nullptr;
 };
 
 namespace {
@@ -68,8 +75,6 @@ int64_t tile_elems(int64_t n) {
   }
   return t;
 }
-
-constexpr int kProfileKinds = 7;
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -114,13 +119,15 @@ template <typename F>
 hipError_t timed(const saef_layout* cl, int kind, F&& launch) {
   saef_layout* l = const_cast<saef_layout*>(cl);
   saef::LaunchEvents ev;
-  const bool rec = l->ev_used < l->ev_start.size() && ((l->ev_mask >> kind) & 1u) != 0;
+  const bool sel = ((l->ev_mask >> kind) & 1u) != 0;
+  const bool rec = sel && l->ev_used < l->ev_start.size() && l->ev_seen[kind] % l->ev_every == 0;
   if (rec) {
     ev.start = l->ev_start[l->ev_used];
     ev.stop = l->ev_stop[l->ev_used];
   }
   hipError_t err = launch(ev);
   if (err != hipSuccess) return err;
+  if (sel) ++l->ev_seen[kind];
   if (rec) {
     l->ev_kind[l->ev_used] = kind;
     ++l->ev_used;
@@ -143,7 +150,7 @@ void free_topk(saef_topk* p) {
   if (p == nullptr) return;
   for (void* q : {p->mem_chunks, p->mem_tens, p->mem_groups, p->mem_sgroups, p->mem_thist,
                   p->mem_ghist, p->mem_sghist, p->mem_goff, p->mem_sel, p->mem_tile_cnt,
-                  p->mem_cand, p->mem_cand_off})
+                  p->mem_cand, p->mem_cand_off, p->mem_spec})
     (void)hipFree(q);
   delete p;
 }
@@ -540,10 +547,13 @@ int saef_materialize(const saef_layout* layout, int32_t K, int32_t mode, const f
                                          x_out, stream));
 }
 
-int saef_profile_enable(saef_layout* layout, int32_t capacity, uint32_t kind_mask) {
-  if (layout == nullptr || capacity < 0 || capacity > (1 << 20)) return SAEF_EINVAL;
+int saef_profile_enable(saef_layout* layout, int32_t capacity, uint32_t kind_mask,
+                        int32_t every) {
+  if (layout == nullptr || capacity < 0 || capacity > (1 << 20) || every < 1) return SAEF_EINVAL;
   release_events(layout);
   layout->ev_mask = kind_mask;
+  layout->ev_every = every;
+  for (int i = 0; i < kProfileKinds; ++i) layout->ev_seen[i] = 0;
   for (int32_t i = 0; i < capacity; ++i) {
     hipEvent_t a = nullptr, b = nullptr;
     if (hipEventCreate(&a) != hipSuccess) return SAEF_EHIP;
@@ -636,6 +646,9 @@ int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk**
   // candidate slots: at most every element of a tensor (8 B each) per row
   const size_t cand_bytes = rows * (size_t)layout->d_pad * sizeof(unsigned long long);
   const size_t cand_off_bytes = rows * n_tiles * sizeof(uint32_t);
+  // speculative candidate lists of the worker rows
+  const size_t spec_bytes =
+      (size_t)layout->k_max * n_tiles * saef::kTkSpecCap * sizeof(unsigned long long);
   hipError_t err = hipMalloc(&p->mem_chunks, chunks.size() * sizeof(saef::TkChunk));
   if (err == hipSuccess) err = hipMalloc(&p->mem_tens, tens.size() * sizeof(saef::TkTensor));
   if (err == hipSuccess) err = hipMalloc(&p->mem_groups, groups.size() * sizeof(saef::TkGroup));
@@ -649,6 +662,7 @@ int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk**
   if (err == hipSuccess) err = hipMalloc(&p->mem_tile_cnt, cnt_bytes);
   if (err == hipSuccess) err = hipMalloc(&p->mem_cand, cand_bytes);
   if (err == hipSuccess) err = hipMalloc(&p->mem_cand_off, cand_off_bytes);
+  if (err == hipSuccess) err = hipMalloc(&p->mem_spec, spec_bytes);
   if (err == hipSuccess)
     err = hipMemcpy(p->mem_chunks, chunks.data(), chunks.size() * sizeof(saef::TkChunk),
                     hipMemcpyHostToDevice);
@@ -661,7 +675,18 @@ int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk**
   if (err == hipSuccess && !sgroups.empty())
     err = hipMemcpy(p->mem_sgroups, sgroups.data(), sgroups.size() * sizeof(saef::TkGroup),
                     hipMemcpyHostToDevice);
-  if (err == hipSuccess) err = hipMemset(p->mem_sel, 0, sel_bytes);
+  if (err == hipSuccess) {
+    // zero state (the first call's window starts at the bottom of the key
+    // range), and the per-tensor speculative-list switch
+    std::vector<saef::TkSel> sel0(rows * L);
+    for (size_t r = 0; r < rows; ++r)
+      for (int32_t l = 0; l < L; ++l) {
+        saef::TkSel z{};
+        z.lists = p->keep[l] * saef::kTkSpecMaxShare <= layout->n[l] ? 1u : 0u;
+        sel0[r * L + l] = z;
+      }
+    err = hipMemcpy(p->mem_sel, sel0.data(), sel_bytes, hipMemcpyHostToDevice);
+  }
   if (err == hipSuccess) err = hipDeviceSynchronize();
   if (err != hipSuccess) {
     free_topk(p);
@@ -680,6 +705,7 @@ int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk**
   d.tile_cnt = static_cast<uint32_t*>(p->mem_tile_cnt);
   d.cand = static_cast<unsigned long long*>(p->mem_cand);
   d.cand_off = static_cast<uint32_t*>(p->mem_cand_off);
+  d.spec = static_cast<unsigned long long*>(p->mem_spec);
   d.n_chunks = (int64_t)chunks.size();
   d.n_groups = (int64_t)groups.size();
   d.n_sgroups = (int64_t)sgroups.size();

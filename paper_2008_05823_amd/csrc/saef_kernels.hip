@@ -40,7 +40,6 @@ constexpr int kU = 8;
 // Words per wave per pass in the averaging kernel (it keeps kAvgChunk * kUA
 // errors and sign words live; 8 was 2% slower).
 constexpr int kUA = 4;
-constexpr int kWPW = 16;  // words per wave per pass in the one-wave-per-tile kernels
 
 // The compression correction C(v)_i = bit ? scale : -scale.
 __device__ __forceinline__ float corr(u64 word, float s) { return sel_by_bit(word, s, -s); }
@@ -131,19 +130,6 @@ __device__ float scale_from_sum(u64 hi, u64 lo, int64_t n) {
   return (float)(mean * 0x1p-80);
 }
 
-
-// Stores the exact partial of (row, tile) summed over one wave.
-__device__ __forceinline__ void wave_partial(const DevLayout& lay, int row, int64_t tile, u64 lo,
-                                             u64 hi, bool bad) {
-  wave_sum128(lo, hi);
-  const bool any_bad = __ballot(bad) != 0;
-  if (lane_id() == 0) {
-    u64* p = lay.part + ((int64_t)row * lay.n_tiles + tile) * 2;
-    p[0] = lo;
-    p[1] = hi;
-    if (any_bad) atomicOr(lay.status, kStatusRange);
-  }
-}
 
 // Stores the exact partial of (row, tile) summed over the workgroup.
 __device__ void block_partial(const DevLayout& lay, int row, int64_t tile, u64 lo, u64 hi,
@@ -570,7 +556,9 @@ __device__ __forceinline__ void aggregate_pass(const DevLayout& lay, int K, doub
   }
 }
 
-// Grid: ceil(n_tiles / 4) workgroups; wave w of workgroup b owns tile 4b + w.
+// Grid: n_tiles workgroups; workgroup b handles tile b.  Wave w takes words
+// w*kU .. w*kU+kU-1 of the tile (one pass over a whole tile), then strides by
+// 4*kU words.
 template <int kMode, bool kDecode, bool kAvg>
 __global__ __launch_bounds__(kBlock) void k_aggregate(DevLayout lay, int K, double inv_k,
                                                       const uint64_t* __restrict__ signs,
@@ -580,31 +568,29 @@ __global__ __launch_bounds__(kBlock) void k_aggregate(DevLayout lay, int K, doub
                                                       uint64_t* __restrict__ ss,
                                                       const float* __restrict__ sscales,
                                                       float* __restrict__ x) {
-  const int64_t ti = (int64_t)blockIdx.x * kWaves + wave_id();
-  if (ti >= lay.n_tiles) return;
+  const int64_t ti = blockIdx.x;
   const Tile tile = lay.tiles[ti];
   const int lane = lane_id();
   const int nw = (tile.count + 63) >> 6;
   const float s_old = (kMode == 1 && kDecode) ? sscales[tile.l] : 0.0f;
   u64 lo = 0, hi = 0;
   bool bad = false;
-  for (int wb = 0; wb < nw; wb += kWPW) {
-    const int64_t base = tile.start + wb * 64 + lane;
-    const int64_t gw = (tile.start >> 6) + wb;
-    if ((wb + kWPW) * 64 <= tile.count) {
-      aggregate_pass<kMode, kDecode, kAvg, true, kWPW>(lay, K, inv_k, tile.l, base, gw, 0, signs,
-                                                       scales, avg, es, ss, s_old, x, lo, hi,
-                                                       bad);
+  for (int w0 = wave_id() * kU; w0 < nw; w0 += kWaves * kU) {
+    const int64_t base = tile.start + w0 * 64 + lane;
+    const int64_t gw = (tile.start >> 6) + w0;
+    if ((w0 + kU) * 64 <= tile.count) {
+      aggregate_pass<kMode, kDecode, kAvg, true, kU>(lay, K, inv_k, tile.l, base, gw, 0, signs,
+                                                     scales, avg, es, ss, s_old, x, lo, hi, bad);
     } else {
       // tail of the tile: one word at a time, guarded per lane
-      for (int u = 0; u < min(kWPW, nw - wb); ++u) {
+      for (int u = 0; u < min(kU, nw - w0); ++u) {
         aggregate_pass<kMode, kDecode, kAvg, false, 1>(
-            lay, K, inv_k, tile.l, base + u * 64, gw + u, tile.count - (wb + u) * 64 - lane,
+            lay, K, inv_k, tile.l, base + u * 64, gw + u, tile.count - (w0 + u) * 64 - lane,
             signs, scales, avg, es, ss, s_old, x, lo, hi, bad);
       }
     }
   }
-  if (kMode == 1) wave_partial(lay, lay.k_max, ti, lo, hi, bad);
+  if (kMode == 1) block_partial(lay, lay.k_max, ti, lo, hi, bad);
 }
 
 // ------------------------------------------------------------------ materialize
@@ -972,7 +958,7 @@ hipError_t launch_finalize(const DevLayout& lay, int K, bool server, float* scal
 hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_t* signs,
                             const float* scales, float* avg, float* e_srv, uint64_t* srv_signs,
                             const float* srv_scales, float* x, bool decode, hipStream_t s, const LaunchEvents& ev) {
-  const dim3 grid(per_wave_grid(lay));
+  const dim3 grid((unsigned)lay.n_tiles);
   const double ik = inv_pow2(K);
 #define SAEF_AGG(M, D, A)                                                                  \
   SAEF_LAUNCH((k_aggregate<M, D, A>), grid, dim3(kBlock), 0, s, lay, K, ik, signs, \

@@ -18,10 +18,27 @@ constexpr int kTkHistPad = 260;                // 16-bit counts per tile (even, 
 constexpr int kTkGroup = 64;      // tile histograms (or group sums) one sum workgroup adds
 constexpr int kTkBins = 2048;     // bins of an 11-bit radix digit
 constexpr int kTkChunk = 65536;   // elements per server-aggregation workgroup
+// Speculative candidate lists: for a tensor that keeps at most 1/16 of its
+// elements, the worker Delta pass also writes, per (row, tile), the elements
+// whose key is at least the previous call's threshold key minus
+// kTkSpecMargin (1/32 binade), in index order, up to kTkSpecCap of them; their
+// count goes to slot kTkSpecSlot of the tile histogram (kTkSpecNone when the
+// tile had more, or for the server row).  When the bin b1 that this call's
+// histogram picks lies at or above that bound, the list holds every element
+// the gather needs and the tile's Delta is not read again.  (Under error
+// feedback the threshold mostly rises from call to call, and the elements
+// just below it pile up: at 1% kept the lists hold about 3% of the elements.)
+constexpr int kTkSpecCap = 512;
+constexpr int kTkSpecSlot = kTkHist;
+constexpr uint32_t kTkSpecNone = 0xFFFFu;
+constexpr uint32_t kTkSpecMargin = 1u << 18;
+constexpr int kTkSpecMaxShare = 16;  // lists when k_l * 16 <= n_l
 static_assert(kTkHistPad >= kTkHist && kTkHistPad % 4 == 0, "padded tile histogram");
 static_assert(kTileElems == 2048, "the Top-K kernels take a tile as 32 words, one per lane");
 static_assert(kTileElems < 65536, "a tile's bin counts fit 16 bits");
 static_assert(kTkChunk % kTileElems == 0, "a server chunk holds whole tiles");
+static_assert(kTkSpecSlot < kTkHistPad && kTkSpecSlot % 2 == 0, "a spare, even histogram slot");
+static_assert(kTkSpecCap < (int)kTkSpecNone, "list counts fit the slot below the marker");
 static_assert((int64_t)kTileElems * kMaxTilesPerTensor >= kMaxTensor,
               "every tensor is cut into tiles of kTileElems elements");
 
@@ -61,7 +78,7 @@ struct TkSel {
   uint32_t tau;
   uint32_t win;     // window base key (a multiple of 2^23)
   uint32_t bin;     // b1
-  uint32_t pad;
+  uint32_t lists;   // 1: worker rows of this tensor keep speculative lists (set at creation)
   int64_t need;
   int64_t cand;
   int64_t iota;     // elements equal to tau with index <= iota are kept
@@ -80,6 +97,7 @@ struct TkDev {
   uint32_t* tile_cnt;  // [rows][n_tiles] kept per tile, then the exclusive prefix
   uint32_t* cand_off;  // [rows][n_tiles] first candidate slot of the tile in its tensor
   unsigned long long* cand;  // [rows][d_pad] candidate slots: (row, tensor) at the tensor's offset
+  unsigned long long* spec;  // [k_max][n_tiles][kTkSpecCap] key | (index in the tile) << 32
   int64_t n_chunks;
   int64_t n_groups;
   int64_t n_sgroups;

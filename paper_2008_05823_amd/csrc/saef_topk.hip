@@ -86,10 +86,20 @@ __device__ __forceinline__ uint16_t* tile_hist(const TkDev& tk, const DevLayout&
   return tk.thist + ((int64_t)row * lay.n_tiles + ti) * kTkHistPad;
 }
 
-// Stores an LDS histogram of kTkHistPad bins as 16-bit counts, two per store.
-__device__ __forceinline__ void store_hist16(const uint32_t* h, uint16_t* out) {
+// Stores an LDS histogram of kTkHistPad bins as 16-bit counts, two per store,
+// with `spec` (the tile's speculative list count) in slot kTkSpecSlot.
+__device__ __forceinline__ void store_hist16(const uint32_t* h, uint16_t* out, uint32_t spec) {
   for (int i = threadIdx.x; i < kTkHistPad / 2; i += blockDim.x)
-    reinterpret_cast<uint32_t*>(out)[i] = (h[2 * i] & 0xFFFFu) | (h[2 * i + 1] << 16);
+    reinterpret_cast<uint32_t*>(out)[i] =
+        2 * i == kTkSpecSlot ? spec : (h[2 * i] & 0xFFFFu) | (h[2 * i + 1] << 16);
+}
+
+// Lower key bound of the speculative lists of a (row, tensor): the previous
+// threshold key minus the margin; 2^31 (no element) before the first
+// threshold or when the tensor keeps no lists.
+__device__ __forceinline__ uint32_t spec_floor(const TkSel& st) {
+  if (st.tau == 0u || st.lists == 0u) return 0x80000000u;
+  return st.tau > kTkSpecMargin ? st.tau - kTkSpecMargin : 0u;
 }
 
 // ------------------------------------------------------------------ pass 1 (workers)
@@ -98,8 +108,9 @@ __device__ __forceinline__ void store_hist16(const uint32_t* h, uint16_t* out) {
 template <bool kMom, bool kFull>
 __device__ __forceinline__ void delta_words(int w0, int nw, int count, float lr, float mu,
                                             const float* __restrict__ gk, float* __restrict__ mk,
-                                            float* __restrict__ ek, uint32_t win, uint32_t* h,
-                                            bool& bad) {
+                                            float* __restrict__ ek, uint32_t win, uint32_t lo,
+                                            uint32_t* h, uint32_t (&keys)[kTkU],
+                                            u64 (&lm)[kTkU], bool& bad) {
   const int lane = lane_id();
   float gv[kTkU], ev[kTkU], mv[kTkU];
 #pragma unroll
@@ -114,31 +125,39 @@ __device__ __forceinline__ void delta_words(int w0, int nw, int count, float lr,
   for (int u = 0; u < kTkU; ++u) {
     const int j = (w0 + u) * 64 + lane;
     const bool ok = kFull || ((w0 + u < nw) && j < count);
-    if (!ok) continue;
     float step = gv[u];
     if (kMom) {
       step = __builtin_fmaf(mu, mv[u], gv[u]);  // m^(k)_{t+1} = mu m^(k)_t + grad
-      st_nt(mk + j, step);
+      if (ok) st_nt(mk + j, step);
     }
     const float p = __builtin_fmaf(lr, step, ev[u]);  // Delta^(k) = e^(k) + lr m^(k)_{t+1}
-    st_nt(ek + j, p);
     const uint32_t key = key_of(p);
+    keys[u] = key;
+    lm[u] = __ballot(ok && key >= lo);
+    if (!ok) continue;
+    st_nt(ek + j, p);
     bad |= key >= kFiniteLimit;
     atomicAdd(&h[hist_bin(key, win)], 1u);
   }
 }
 
 // Grid: n_tiles * K workgroups; workgroup b handles worker b % K of tile b / K.
+// Each wave takes kTkU words of the tile (one pass); the tile's speculative
+// list is written in index order (wave by wave) when it fits.
 template <bool kMom>
 __global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, int K, float lr,
                                                      float mu, const float* __restrict__ g,
                                                      float* __restrict__ m,
                                                      float* __restrict__ e) {
+  static_assert(kWaves * kTkU == kTileWords, "one pass of the four waves covers a tile");
   __shared__ uint32_t h[kTkHistPad];
+  __shared__ uint32_t s_cnt[kWaves];
   const int k = (int)(blockIdx.x % (unsigned)K);
   const int64_t ti = blockIdx.x / (unsigned)K;
   const Tile tile = lay.tiles[ti];
-  const uint32_t win = tk.sel[(int64_t)k * lay.L + tile.l].win;
+  const TkSel* st = tk.sel + (int64_t)k * lay.L + tile.l;
+  const uint32_t win = st->win;
+  const uint32_t lo = spec_floor(*st);
   for (int i = threadIdx.x; i < kTkHistPad; i += kBlock) h[i] = 0;
   __syncthreads();
   const int64_t row = (int64_t)k * lay.d_pad + tile.start;
@@ -146,16 +165,47 @@ __global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, in
   float* mk = kMom ? m + row : nullptr;
   float* ek = e + row;
   const int nw = (tile.count + 63) >> 6;
+  const int wave = wave_id();
+  const int w0 = wave * kTkU;
   bool bad = false;
-  for (int w0 = wave_id() * kTkU; w0 < nw; w0 += kWaves * kTkU) {
+  uint32_t keys[kTkU];
+  u64 lm[kTkU];
+#pragma unroll
+  for (int u = 0; u < kTkU; ++u) lm[u] = 0ull;
+  if (w0 < nw) {
     if ((w0 + kTkU) * 64 <= tile.count)
-      delta_words<kMom, true>(w0, nw, tile.count, lr, mu, gk, mk, ek, win, h, bad);
+      delta_words<kMom, true>(w0, nw, tile.count, lr, mu, gk, mk, ek, win, lo, h, keys, lm, bad);
     else
-      delta_words<kMom, false>(w0, nw, tile.count, lr, mu, gk, mk, ek, win, h, bad);
+      delta_words<kMom, false>(w0, nw, tile.count, lr, mu, gk, mk, ek, win, lo, h, keys, lm,
+                               bad);
   }
   if (__ballot(bad) != 0 && lane_id() == 0) atomicOr(lay.status, kStatusRange);
+  uint32_t mine = 0;
+#pragma unroll
+  for (int u = 0; u < kTkU; ++u) mine += (uint32_t)__popcll(lm[u]);
+  if (lane_id() == 0) s_cnt[wave] = mine;
   __syncthreads();
-  store_hist16(h, tile_hist(tk, lay, k, ti));
+  uint32_t before = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    before += w < wave ? s_cnt[w] : 0u;
+    total += s_cnt[w];
+  }
+  const bool fits = total <= (uint32_t)kTkSpecCap;
+  store_hist16(h, tile_hist(tk, lay, k, ti), fits ? total : kTkSpecNone);
+  if (fits && mine != 0u) {
+    u64* out = tk.spec + ((int64_t)k * lay.n_tiles + ti) * kTkSpecCap;
+    const int lane = lane_id();
+#pragma unroll
+    for (int u = 0; u < kTkU; ++u) {
+      const uint32_t pos =
+          before + __builtin_amdgcn_mbcnt_hi((uint32_t)(lm[u] >> 32),
+                                             __builtin_amdgcn_mbcnt_lo((uint32_t)lm[u], 0u));
+      if ((lm[u] >> lane) & 1ull)  // pos < total <= kTkSpecCap
+        out[pos] = (u64)keys[u] | ((u64)((w0 + u) * 64 + lane) << 32);
+      before += (uint32_t)__popcll(lm[u]);
+    }
+  }
 }
 
 // ------------------------------------------------------------------ sums
@@ -357,14 +407,55 @@ __device__ __forceinline__ void gather_words(const float (&v)[kTileWords], int c
   }
 }
 
+// The gather's classification of a tile's speculative list (1 <= n <= 64 kNC
+// entries, index order; every element with a key >= lo is in it): the same
+// selection words (lane u gets word u, assembled in LDS) and candidate slots
+// as gather_words.  The kNC loads of a lane are issued together.
+template <int kNC>
+__device__ __forceinline__ void gather_list(const u64* __restrict__ ent, uint32_t n, uint32_t lo,
+                                            uint32_t up, int64_t rel0, uint32_t nslots,
+                                            u64* __restrict__ slots, u64* s_w, u64& myw,
+                                            uint32_t& base) {
+  const int lane = lane_id();
+  u64 e[kNC];
+#pragma unroll
+  for (int c = 0; c < kNC; ++c) {
+    const uint32_t i = (uint32_t)(c * kWave + lane);
+    e[c] = ent[i < n ? i : 0u];
+  }
+  if (lane < kTileWords) s_w[lane] = 0ull;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int c = 0; c < kNC; ++c) {
+    const bool ok = (uint32_t)(c * kWave + lane) < n;
+    const uint32_t key = (uint32_t)e[c], idx = (uint32_t)(e[c] >> 32);  // idx < kTileElems
+    if (ok && key >= up) atomicOr(&s_w[idx >> 6], 1ull << (idx & 63u));
+    const u64 cm = __ballot(ok && key - lo < up - lo);  // lo <= key < up
+    if (cm != 0ull) {
+      const uint32_t pos = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(cm >> 32),
+                                                            __builtin_amdgcn_mbcnt_lo((uint32_t)cm, 0u));
+      if (((cm >> lane) & 1ull) && pos < nslots)  // pos < nslots always holds
+        slots[pos] = (u64)key | ((u64)(rel0 + idx) << 32);
+      base += (uint32_t)__popcll(cm);
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  myw = lane < kTileWords ? s_w[lane] : 0ull;
+}
+
 // Grid: per_wave_grid(lay) * R workgroups; wave w of workgroup b owns tile
-// 4 (b / R) + w of row b % R.  One read of the tile's Delta (all 32 words at
-// once): the selection words with the elements above b1 (kept for sure) and
-// their count, and the elements of b1 to the tile's candidate slots as
-// key | (index in the tensor) << 32, in index order.
+// 4 (b / R) + w of row b % R.  The selection words with the elements above
+// b1 (kept for sure) and their count, and the elements of b1 to the tile's
+// candidate slots as key | (index in the tensor) << 32, in index order:
+// from the tile's speculative list when `spec` is set, the list fits and its
+// bound lies at or below b1 (then every element at or above b1 is in it),
+// otherwise from one read of the tile's Delta (all 32 words at once).
 __global__ __launch_bounds__(kBlock) void k_tk_gather(DevLayout lay, TkDev tk, int R, int row0,
-                                                      const float* __restrict__ data,
+                                                      int spec, const float* __restrict__ data,
                                                       uint64_t* __restrict__ sel) {
+  __shared__ u64 s_w[kWaves][kTileWords];
   const int r = (int)(blockIdx.x % (unsigned)R);
   const int64_t ti = (int64_t)(blockIdx.x / (unsigned)R) * kWaves + wave_id();
   if (ti >= lay.n_tiles) return;
@@ -376,25 +467,44 @@ __global__ __launch_bounds__(kBlock) void k_tk_gather(DevLayout lay, TkDev tk, i
   const int64_t rel0 = tile.start - ten.off;  // the tile's first element, index in the tensor
   u64* slots = tk.cand + (int64_t)row * lay.d_pad + ten.off +
                tk.cand_off[(int64_t)row * lay.n_tiles + ti];
-  const uint32_t nslots = tile_hist(tk, lay, row, ti)[b1];  // elements of b1 in the tile
-  const float* dr = data + (int64_t)r * lay.d_pad + tile.start;
+  const uint16_t* th = tile_hist(tk, lay, row, ti);
+  const uint32_t nslots = th[b1];  // elements of b1 in the tile
   uint64_t* sr = sel + (int64_t)r * (lay.d_pad >> 6) + (tile.start >> 6);
   const int lane = lane_id();
   const int nw = (tile.count + 63) >> 6;
-  float v[kTileWords];
-#pragma unroll
-  for (int u = 0; u < kTileWords; ++u) {
-    const int j = u * 64 + lane;
-    v[u] = ld_nt_or0(dr, j, j < tile.count);
-  }
   // bin b1 holds the keys [lo, up): above it kept for sure, inside it candidates
   const uint32_t lo = bin_floor(b1, win), up = bin_floor(b1 + 1u, win);
   u64 myw = 0;        // lane u < nw: selection word u
   uint32_t base = 0;  // candidates in the earlier words
-  if (tile.count == kTileElems)
-    gather_words<true>(v, tile.count, lo, up, rel0, nslots, slots, myw, base);
-  else
-    gather_words<false>(v, tile.count, lo, up, rel0, nslots, slots, myw, base);
+  const uint32_t n_spec = spec ? (uint32_t)th[kTkSpecSlot] : kTkSpecNone;
+  if (n_spec != kTkSpecNone && spec_floor(*st) <= lo) {
+    static_assert(kTkSpecCap == 8 * kWave, "lists of up to 8 loads per lane");
+    const u64* ent = tk.spec + ((int64_t)row * lay.n_tiles + ti) * kTkSpecCap;
+    u64* sw = s_w[wave_id()];
+    switch ((n_spec + kWave - 1) / kWave) {
+      case 0: break;  // no element at or above the bound: nothing kept in the tile
+      case 1: gather_list<1>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
+      case 2: gather_list<2>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
+      case 3: gather_list<3>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
+      case 4: gather_list<4>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
+      case 5: gather_list<5>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
+      case 6: gather_list<6>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
+      case 7: gather_list<7>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
+      default: gather_list<8>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
+    }
+  } else {
+    const float* dr = data + (int64_t)r * lay.d_pad + tile.start;
+    float v[kTileWords];
+#pragma unroll
+    for (int u = 0; u < kTileWords; ++u) {
+      const int j = u * 64 + lane;
+      v[u] = ld_nt_or0(dr, j, j < tile.count);
+    }
+    if (tile.count == kTileElems)
+      gather_words<true>(v, tile.count, lo, up, rel0, nslots, slots, myw, base);
+    else
+      gather_words<false>(v, tile.count, lo, up, rel0, nslots, slots, myw, base);
+  }
   if (lane < nw) sr[lane] = myw;
   uint32_t ndef = (uint32_t)__popcll(myw);
 #pragma unroll
@@ -836,7 +946,10 @@ struct Launcher {
     if ((err = hipGetLastError()) != hipSuccess) return err;
     SAEF_LAUNCH(k_tk_offsets, dim3((unsigned)(R * tk.n_groups)), dim3(kWave), 0, s, lay, tk, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    SAEF_LAUNCH(k_tk_gather, tiles, dim3(kBlock), 0, s, lay, tk, R, row0, data, sel);
+    // speculative lists exist for the worker rows only (the server's Delta
+    // comes from the aggregation kernel)
+    const int spec = row0 + R <= lay.k_max ? 1 : 0;
+    SAEF_LAUNCH(k_tk_gather, tiles, dim3(kBlock), 0, s, lay, tk, R, row0, spec, data, sel);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     SAEF_LAUNCH(k_tk_select, pairs, dim3(kBig), 0, s, lay, tk, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;

@@ -60,7 +60,7 @@ _SIGS = {
                             _P, _P],
     "saef_materialize": [_P, _i32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P],
     "saef_status": [_P, _P],
-    "saef_profile_enable": [_P, _i32, ctypes.c_uint32],
+    "saef_profile_enable": [_P, _i32, ctypes.c_uint32, _i32],
     "saef_profile_read": [_P, _P, _P],
 }
 for _name, _args in _SIGS.items():
@@ -330,13 +330,16 @@ def saef_status(layout: Layout, stream=None) -> int:
     return rc
 
 
-def saef_profile_enable(layout: Layout, capacity: int, kinds=PROFILE_KINDS) -> None:
+def saef_profile_enable(layout: Layout, capacity: int, kinds=PROFILE_KINDS,
+                        every: int = 1) -> None:
     """Time the kernels of the given kinds (names from PROFILE_KINDS) in the
-    next saef_round calls, up to `capacity` launches."""
+    next saef_round calls, up to `capacity` launches; every > 1 times only
+    every `every`-th dispatch of each kind."""
     mask = 0
     for k in kinds:
         mask |= 1 << PROFILE_KINDS.index(k)
-    _check("saef_profile_enable", _lib.saef_profile_enable(layout.handle, int(capacity), mask))
+    _check("saef_profile_enable",
+           _lib.saef_profile_enable(layout.handle, int(capacity), mask, int(every)))
 
 
 def saef_profile_read(layout: Layout) -> dict:

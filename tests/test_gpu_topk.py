@@ -342,6 +342,70 @@ def test_topk_threshold_moves():
     assert gs.status() == 0
 
 
+# successive calls on one plan for the Delta pass's speculative lists (the
+# elements just below the previous threshold and above): (data scale, hot
+# tile).  A small drop of the threshold stays within the lists' bound, a
+# larger one falls below it (Delta read again), a hot tile (its values x 8)
+# overflows its list while the other tiles use theirs, and values of few
+# distinct magnitudes overflow every list.
+SPEC_CALLS = [(1.0, False), (1.0, False), (0.97, False), (1.0, False), (0.75, False),
+              (1.0, True), (1.0, False), (1.0, "ties"), (1.0, False)]
+
+
+def test_topk_speculative_lists():
+    """Compress and server calls on one plan where the gather takes each
+    tile from its speculative list or from Delta: bit-equal either way."""
+    K = 3
+    w = W.custom([5000, 70001, 300_000, 33], K=K, scale_range=(1e-2, 1.0), seed=91)
+    keep = W.topk_keep(w, 1)
+    off, n, d_pad = w.layout()
+    msk = W.tensor_mask(w)
+    wm = H.tensor_word_mask(off, n, d_pad)
+    orc = TopkOracle(w, keep)
+    gs = TopkGpu(w, keep)
+    rng = np.random.default_rng(6)
+    for c, (scale, hot) in enumerate(SPEC_CALLS):
+        _case(f"topk speculative lists: call {c} scale {scale} hot {hot}")
+        sc = np.float32(scale)
+        g = (W.gradients(w, c % 2) * sc).astype(np.float32)
+        e = (rng.standard_normal((K, d_pad)) * np.float32(0.01) * sc).astype(np.float32)
+        if hot is True:
+            a = int(off[1]) + 4096
+            g[:, a:a + 2048] *= np.float32(8.0)
+            e[:, a:a + 2048] *= np.float32(8.0)
+        elif hot == "ties":
+            g = _tie_values(rng, g.shape)
+            e = np.zeros_like(e)
+        e = np.where(msk, e, np.float32(0.0)).astype(np.float32)
+        es = (rng.standard_normal(d_pad) * np.float32(0.01) * sc).astype(np.float32)
+        es = np.where(msk, es, np.float32(0.0)).astype(np.float32)
+        orc.e[:] = e
+        orc.e_srv[:] = es
+        assert orc.orc.topk_compress(K, LR, 0.0, keep, g, None, orc.e, orc.sel, orc.rank,
+                                     orc.vals) == 0
+        assert orc.orc.topk_aggregate(K, 1, keep, orc.sel, orc.vals, orc.x, orc.e_srv,
+                                      orc.srv_sel, orc.srv_rank, orc.srv_vals, None) == 0
+        gs.e.copy_(torch.from_numpy(e))
+        gs.e_srv.copy_(torch.from_numpy(es))
+        gs.saef.saef_topk_compress(gs.plan, K, float(LR), 0.0, H.dev(g), None, gs.e, gs.sel,
+                                   gs.rank, gs.vals)
+        gs.saef.saef_topk_aggregate(gs.plan, K, 1, gs.sel, gs.rank, gs.vals, gs.x, gs.e_srv,
+                                    gs.srv_sel, gs.srv_rank, gs.srv_vals)
+        torch.cuda.synchronize()
+        H.assert_words_equal(H.host(gs.sel, np.uint64), orc.sel, wm, f"selection, call {c}")
+        assert np.array_equal(_u32(gs.rank)[:, wm], orc.rank[:, wm]), f"rank words, call {c}"
+        H.assert_f32_equal(H.host(gs.vals), orc.vals, np.ones(orc.vals.shape[-1], bool),
+                           f"values, call {c}")
+        H.assert_f32_equal(H.host(gs.e), orc.e, msk, f"errors, call {c}")
+        H.assert_words_equal(H.host(gs.srv_sel, np.uint64), orc.srv_sel, wm,
+                             f"server selection, call {c}")
+        H.assert_f32_equal(H.host(gs.srv_vals), orc.srv_vals,
+                           np.ones(orc.srv_vals.shape[-1], bool), f"server values, call {c}")
+        H.assert_f32_equal(H.host(gs.e_srv), orc.e_srv, msk, f"server error, call {c}")
+        H.assert_f32_equal(H.host(gs.x), orc.x, msk, f"weights, call {c}")
+    assert gs.status() == 0
+
+
 ROUND_CASES = {
     "resnet56_1pct_dc": (W.get("resnet56").with_(rounds=12, period=0), 1, None),
     "resnet56_10pct_avg": (W.get("resnet56").with_(rounds=12, period=4), 10, None),
