@@ -710,6 +710,9 @@ int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk**
   d.n_groups = (int64_t)groups.size();
   d.n_sgroups = (int64_t)sgroups.size();
   d.total_keep = p->total_keep;
+  d.lists = 0;
+  for (int32_t l = 0; l < L; ++l)
+    if (p->keep[l] * saef::kTkSpecMaxShare <= layout->n[l]) d.lists = 1;
   *out = p;
   return SAEF_OK;
 }

@@ -102,6 +102,8 @@ struct TkDev {
   int64_t n_groups;
   int64_t n_sgroups;
   int64_t total_keep;
+  int32_t lists;  // 1: some tensor keeps speculative lists
+  int32_t pad;
 };
 
 // Worker Top-K compression of K rows (row k of e, histogram row k).  m

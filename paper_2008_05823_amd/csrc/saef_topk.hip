@@ -109,7 +109,7 @@ template <bool kMom, bool kFull>
 __device__ __forceinline__ void delta_words(int w0, int nw, int count, float lr, float mu,
                                             const float* __restrict__ gk, float* __restrict__ mk,
                                             float* __restrict__ ek, uint32_t win, uint32_t lo,
-                                            uint32_t* h, uint32_t (&keys)[kTkU],
+                                            uint32_t* h, uint32_t (&bits)[kTkU],
                                             u64 (&lm)[kTkU], bool& bad) {
   const int lane = lane_id();
   float gv[kTkU], ev[kTkU], mv[kTkU];
@@ -132,7 +132,7 @@ __device__ __forceinline__ void delta_words(int w0, int nw, int count, float lr,
     }
     const float p = __builtin_fmaf(lr, step, ev[u]);  // Delta^(k) = e^(k) + lr m^(k)_{t+1}
     const uint32_t key = key_of(p);
-    keys[u] = key;
+    bits[u] = __float_as_uint(p);
     lm[u] = __ballot(ok && key >= lo);
     if (!ok) continue;
     st_nt(ek + j, p);
@@ -168,15 +168,15 @@ __global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, in
   const int wave = wave_id();
   const int w0 = wave * kTkU;
   bool bad = false;
-  uint32_t keys[kTkU];
+  uint32_t bits[kTkU];  // Delta's bit patterns
   u64 lm[kTkU];
 #pragma unroll
   for (int u = 0; u < kTkU; ++u) lm[u] = 0ull;
   if (w0 < nw) {
     if ((w0 + kTkU) * 64 <= tile.count)
-      delta_words<kMom, true>(w0, nw, tile.count, lr, mu, gk, mk, ek, win, lo, h, keys, lm, bad);
+      delta_words<kMom, true>(w0, nw, tile.count, lr, mu, gk, mk, ek, win, lo, h, bits, lm, bad);
     else
-      delta_words<kMom, false>(w0, nw, tile.count, lr, mu, gk, mk, ek, win, lo, h, keys, lm,
+      delta_words<kMom, false>(w0, nw, tile.count, lr, mu, gk, mk, ek, win, lo, h, bits, lm,
                                bad);
   }
   if (__ballot(bad) != 0 && lane_id() == 0) atomicOr(lay.status, kStatusRange);
@@ -191,7 +191,9 @@ __global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, in
     before += w < wave ? s_cnt[w] : 0u;
     total += s_cnt[w];
   }
-  const bool fits = total <= (uint32_t)kTkSpecCap;
+  // no list (kTkSpecNone) before the first threshold, for a tensor without
+  // lists, or when the tile has more than kTkSpecCap such elements
+  const bool fits = lo != 0x80000000u && total <= (uint32_t)kTkSpecCap;
   store_hist16(h, tile_hist(tk, lay, k, ti), fits ? total : kTkSpecNone);
   if (fits && mine != 0u) {
     u64* out = tk.spec + ((int64_t)k * lay.n_tiles + ti) * kTkSpecCap;
@@ -202,7 +204,7 @@ __global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, in
           before + __builtin_amdgcn_mbcnt_hi((uint32_t)(lm[u] >> 32),
                                              __builtin_amdgcn_mbcnt_lo((uint32_t)lm[u], 0u));
       if ((lm[u] >> lane) & 1ull)  // pos < total <= kTkSpecCap
-        out[pos] = (u64)keys[u] | ((u64)((w0 + u) * 64 + lane) << 32);
+        out[pos] = (u64)bits[u] | ((u64)((w0 + u) * 64 + lane) << 32);
       before += (uint32_t)__popcll(lm[u]);
     }
   }
@@ -407,92 +409,111 @@ __device__ __forceinline__ void gather_words(const float (&v)[kTileWords], int c
   }
 }
 
-// The gather's classification of a tile's speculative list (1 <= n <= 64 kNC
-// entries, index order; every element with a key >= lo is in it): the same
-// selection words (lane u gets word u, assembled in LDS) and candidate slots
-// as gather_words.  The kNC loads of a lane are issued together.
+// The gather from a tile's speculative list (n <= 64 kNC entries: Delta's
+// bits | index in the tile << 32, index order), if the list's bound lies at
+// or below b1 (then every element with a key >= lo is in it): the count of
+// the elements above b1 (per lane, to be added) and the elements of b1 to the
+// candidate slots in index order; returns false, having written nothing,
+// otherwise.  The list loads are issued before the selection state is waited
+// for.  The selection words are left to the emit, which reads the list too.
 template <int kNC>
-__device__ __forceinline__ void gather_list(const u64* __restrict__ ent, uint32_t n, uint32_t lo,
-                                            uint32_t up, int64_t rel0, uint32_t nslots,
-                                            u64* __restrict__ slots, u64* s_w, u64& myw,
-                                            uint32_t& base) {
+__device__ __forceinline__ bool gather_list(const u64* __restrict__ ent, uint32_t n,
+                                            const TkSel* st, const TensorInfo* ten,
+                                            const uint32_t* co, int64_t row_cand, int64_t start,
+                                            int count, const TkDev& tk, uint32_t& ndef) {
   const int lane = lane_id();
-  u64 e[kNC];
+  u64 e[kNC > 0 ? kNC : 1];
 #pragma unroll
   for (int c = 0; c < kNC; ++c) {
     const uint32_t i = (uint32_t)(c * kWave + lane);
     e[c] = ent[i < n ? i : 0u];
   }
-  if (lane < kTileWords) s_w[lane] = 0ull;
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
+  const uint32_t b1 = st->bin, win = st->win;
+  // bin b1 holds the keys [lo, up): above it kept for sure, inside it candidates
+  const uint32_t lo = bin_floor(b1, win), up = bin_floor(b1 + 1u, win);
+  if (spec_floor(*st) > lo) return false;
+  const int64_t off = ten->off;
+  const int64_t rel0 = start - off;  // the tile's first element, index in the tensor
+  u64* slots = tk.cand + row_cand + off + *co;
+  uint32_t base = 0;  // candidates in the earlier entries
 #pragma unroll
   for (int c = 0; c < kNC; ++c) {
     const bool ok = (uint32_t)(c * kWave + lane) < n;
-    const uint32_t key = (uint32_t)e[c], idx = (uint32_t)(e[c] >> 32);  // idx < kTileElems
-    if (ok && key >= up) atomicOr(&s_w[idx >> 6], 1ull << (idx & 63u));
+    const uint32_t key = (uint32_t)e[c] & 0x7FFFFFFFu, idx = (uint32_t)(e[c] >> 32);
+    const u64 sure = __ballot(ok && key >= up);
+    ndef += lane == 0 ? (uint32_t)__popcll(sure) : 0u;
     const u64 cm = __ballot(ok && key - lo < up - lo);  // lo <= key < up
     if (cm != 0ull) {
       const uint32_t pos = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(cm >> 32),
                                                             __builtin_amdgcn_mbcnt_lo((uint32_t)cm, 0u));
-      if (((cm >> lane) & 1ull) && pos < nslots)  // pos < nslots always holds
+      // the tile's slots follow the b1 elements of the earlier tiles of the
+      // tensor, so pos < count keeps the store inside the tensor's area
+      if (((cm >> lane) & 1ull) && pos < (uint32_t)count)
         slots[pos] = (u64)key | ((u64)(rel0 + idx) << 32);
       base += (uint32_t)__popcll(cm);
     }
   }
-  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  myw = lane < kTileWords ? s_w[lane] : 0ull;
+  return true;
 }
 
 // Grid: per_wave_grid(lay) * R workgroups; wave w of workgroup b owns tile
-// 4 (b / R) + w of row b % R.  The selection words with the elements above
-// b1 (kept for sure) and their count, and the elements of b1 to the tile's
-// candidate slots as key | (index in the tensor) << 32, in index order:
-// from the tile's speculative list when `spec` is set, the list fits and its
-// bound lies at or below b1 (then every element at or above b1 is in it),
-// otherwise from one read of the tile's Delta (all 32 words at once).
-__global__ __launch_bounds__(kBlock) void k_tk_gather(DevLayout lay, TkDev tk, int R, int row0,
-                                                      int spec, const float* __restrict__ data,
-                                                      uint64_t* __restrict__ sel) {
-  __shared__ u64 s_w[kWaves][kTileWords];
+// 4 (b / R) + w of row b % R.  The count of the elements above b1 (kept for
+// sure) and the elements of b1 to the tile's candidate slots as key | (index
+// in the tensor) << 32, in index order: from the tile's speculative list when
+// `spec` is set, the list fits and its bound lies at or below b1 (slot
+// kTkSpecSlot + 1 of the tile histogram then says so to the emit), otherwise
+// from one read of the tile's Delta (all 32 words at once), which also gives
+// the selection words of the elements kept for sure.  At most 64 VGPRs: 8
+// waves per SIMD (the kernel is bound by the latency of its dependent loads).
+// Without lists (kSpec false) every tile takes the Delta read, with its 32
+// loads in flight at once (85 VGPRs: k_tk_gather_full).
+template <bool kSpec>
+__device__ __forceinline__ void gather_tile(const DevLayout& lay, const TkDev& tk, int R,
+                                            int row0, const float* __restrict__ data,
+                                            uint64_t* __restrict__ sel) {
+  constexpr int spec = kSpec ? 1 : 0;
   const int r = (int)(blockIdx.x % (unsigned)R);
   const int64_t ti = (int64_t)(blockIdx.x / (unsigned)R) * kWaves + wave_id();
   if (ti >= lay.n_tiles) return;
   const int row = row0 + r;
+  uint16_t* th = tile_hist(tk, lay, row, ti);
+  // the list count and the flag slot in one 32-bit word: a scalar load issued
+  // together with the tile's (a 16-bit load would be a vector one, waited for
+  // before anything else)
+  const uint32_t sp = spec ? *reinterpret_cast<const uint32_t*>(th + kTkSpecSlot) : kTkSpecNone;
   const Tile tile = lay.tiles[ti];
+  const uint32_t n_spec = sp & 0xFFFFu;
   const TkSel* st = tk.sel + (int64_t)row * lay.L + tile.l;
-  const uint32_t b1 = st->bin, win = st->win;
-  const TensorInfo ten = lay.tensors[tile.l];
-  const int64_t rel0 = tile.start - ten.off;  // the tile's first element, index in the tensor
-  u64* slots = tk.cand + (int64_t)row * lay.d_pad + ten.off +
-               tk.cand_off[(int64_t)row * lay.n_tiles + ti];
-  const uint16_t* th = tile_hist(tk, lay, row, ti);
-  const uint32_t nslots = th[b1];  // elements of b1 in the tile
-  uint64_t* sr = sel + (int64_t)r * (lay.d_pad >> 6) + (tile.start >> 6);
+  const TensorInfo* ten = lay.tensors + tile.l;
+  const uint32_t* co = tk.cand_off + (int64_t)row * lay.n_tiles + ti;
+  const int64_t row_cand = (int64_t)row * lay.d_pad;
   const int lane = lane_id();
-  const int nw = (tile.count + 63) >> 6;
-  // bin b1 holds the keys [lo, up): above it kept for sure, inside it candidates
-  const uint32_t lo = bin_floor(b1, win), up = bin_floor(b1 + 1u, win);
-  u64 myw = 0;        // lane u < nw: selection word u
-  uint32_t base = 0;  // candidates in the earlier words
-  const uint32_t n_spec = spec ? (uint32_t)th[kTkSpecSlot] : kTkSpecNone;
-  if (n_spec != kTkSpecNone && spec_floor(*st) <= lo) {
+  uint32_t ndef = 0;  // kept for sure (lane 0 holds the list path's count)
+  bool listed = false;
+  if (n_spec != kTkSpecNone) {
     static_assert(kTkSpecCap == 8 * kWave, "lists of up to 8 loads per lane");
     const u64* ent = tk.spec + ((int64_t)row * lay.n_tiles + ti) * kTkSpecCap;
-    u64* sw = s_w[wave_id()];
+#define SAEF_GL(NC) \
+  listed = gather_list<NC>(ent, n_spec, st, ten, co, row_cand, tile.start, tile.count, tk, ndef)
     switch ((n_spec + kWave - 1) / kWave) {
-      case 0: break;  // no element at or above the bound: nothing kept in the tile
-      case 1: gather_list<1>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
-      case 2: gather_list<2>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
-      case 3: gather_list<3>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
-      case 4: gather_list<4>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
-      case 5: gather_list<5>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
-      case 6: gather_list<6>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
-      case 7: gather_list<7>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
-      default: gather_list<8>(ent, n_spec, lo, up, rel0, nslots, slots, sw, myw, base); break;
+      case 0: SAEF_GL(0); break;
+      case 1: SAEF_GL(1); break;
+      case 2: SAEF_GL(2); break;
+      case 3: SAEF_GL(3); break;
+      case 4: SAEF_GL(4); break;
+      case 5: SAEF_GL(5); break;
+      case 6: SAEF_GL(6); break;
+      case 7: SAEF_GL(7); break;
+      default: SAEF_GL(8); break;
     }
-  } else {
+#undef SAEF_GL
+  }
+  if (!listed) {
+    const uint32_t b1 = st->bin, win = st->win;
+    const uint32_t lo = bin_floor(b1, win), up = bin_floor(b1 + 1u, win);
+    const int64_t rel0 = tile.start - ten->off;
+    u64* slots = tk.cand + row_cand + ten->off + *co;
+    const uint32_t nslots = th[b1];  // elements of b1 in the tile
     const float* dr = data + (int64_t)r * lay.d_pad + tile.start;
     float v[kTileWords];
 #pragma unroll
@@ -500,16 +521,35 @@ __global__ __launch_bounds__(kBlock) void k_tk_gather(DevLayout lay, TkDev tk, i
       const int j = u * 64 + lane;
       v[u] = ld_nt_or0(dr, j, j < tile.count);
     }
+    u64 myw = 0;        // lane u < nw: selection word u
+    uint32_t base = 0;  // candidates in the earlier words
     if (tile.count == kTileElems)
       gather_words<true>(v, tile.count, lo, up, rel0, nslots, slots, myw, base);
     else
       gather_words<false>(v, tile.count, lo, up, rel0, nslots, slots, myw, base);
+    const int nw = (tile.count + 63) >> 6;
+    uint64_t* sr = sel + (int64_t)r * (lay.d_pad >> 6) + (tile.start >> 6);
+    if (lane < nw) sr[lane] = myw;
+    ndef = (uint32_t)__popcll(myw);
   }
-  if (lane < nw) sr[lane] = myw;
-  uint32_t ndef = (uint32_t)__popcll(myw);
 #pragma unroll
   for (int off = kWave / 2; off > 0; off >>= 1) ndef += __shfl_xor(ndef, off);
-  if (lane == 0) tk.tile_cnt[(int64_t)row * lay.n_tiles + ti] = ndef;  // kept for sure
+  if (lane == 0) {
+    tk.tile_cnt[(int64_t)row * lay.n_tiles + ti] = ndef;  // kept for sure
+    if (spec) th[kTkSpecSlot + 1] = listed ? 1 : 0;
+  }
+}
+
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8)))
+void k_tk_gather_spec(DevLayout lay, TkDev tk, int R, int row0, const float* __restrict__ data,
+                      uint64_t* __restrict__ sel) {
+  gather_tile<true>(lay, tk, R, row0, data, sel);
+}
+
+__global__ __launch_bounds__(kBlock)
+void k_tk_gather_full(DevLayout lay, TkDev tk, int R, int row0, const float* __restrict__ data,
+                      uint64_t* __restrict__ sel) {
+  gather_tile<false>(lay, tk, R, row0, data, sel);
 }
 
 // ------------------------------------------------------------------ select
@@ -692,6 +732,64 @@ __device__ __forceinline__ int nth_set_bit(u64 w, uint32_t r) {
   return pos;
 }
 
+// The emit of a tile that the gather took from its speculative list (n <=
+// 64 kNC entries, index order, every kept element among them): an entry is
+// kept iff its key is above tau, or equal to it with an index up to iota;
+// its value (from the entry) goes to the message at the tile's first rank
+// plus the kept entries before it, the error there is set to 0, and the
+// selection words (assembled in LDS) and rank words are written.
+template <int kNC>
+__device__ __forceinline__ void emit_list(const u64* __restrict__ ent, uint32_t n,
+                                          const TkSel* stp, int64_t rel0, uint32_t base,
+                                          uint32_t keep, int count, int nw,
+                                          uint64_t* __restrict__ sr, uint32_t* __restrict__ rr,
+                                          float* __restrict__ vr, float* __restrict__ dr,
+                                          u64* s_w) {
+  const int lane = lane_id();
+  u64 e[kNC > 0 ? kNC : 1];
+#pragma unroll
+  for (int c = 0; c < kNC; ++c) {
+    const uint32_t i = (uint32_t)(c * kWave + lane);
+    e[c] = ent[i < n ? i : 0u];
+  }
+  const uint32_t tau = stp->tau;
+  const int64_t iota = stp->iota;
+  if (lane < kTileWords) s_w[lane] = 0ull;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  uint32_t run = 0;  // kept entries in the earlier chunks
+#pragma unroll
+  for (int c = 0; c < kNC; ++c) {
+    const bool ok = (uint32_t)(c * kWave + lane) < n;
+    const uint32_t raw = (uint32_t)e[c], key = raw & 0x7FFFFFFFu;
+    const uint32_t idx = (uint32_t)(e[c] >> 32);  // index in the tile
+    const bool kept = ok && (key > tau || (key == tau && rel0 + (int64_t)idx <= iota));
+    const u64 km = __ballot(kept);
+    if (kept) {
+      atomicOr(&s_w[idx >> 6], 1ull << (idx & 63u));
+      const uint32_t pos = base + run + __builtin_amdgcn_mbcnt_hi((uint32_t)(km >> 32),
+                                                                  __builtin_amdgcn_mbcnt_lo((uint32_t)km, 0u));
+      if (pos < keep && idx < (uint32_t)count) {  // both always hold
+        vr[pos] = __uint_as_float(raw);
+        st_nt(dr + idx, 0.0f);  // e = Delta - C(Delta) = 0 at a kept element
+      }
+    }
+    run += (uint32_t)__popcll(km);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  const u64 mine = lane < nw ? s_w[lane] : 0ull;
+  if (lane < nw) sr[lane] = mine;
+  const uint32_t cnt = (uint32_t)__popcll(mine);
+  uint32_t incl = cnt;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint32_t y = __shfl_up(incl, off);
+    if (lane >= off) incl += y;
+  }
+  if (lane < nw) rr[lane] = base + incl - cnt;
+}
+
 // Grid: per_wave_grid(lay) * R workgroups; wave w of workgroup b owns tile
 // 4 (b / R) + w of row b % R.  The tile's kept candidates are added to its
 // selection words (LDS), then the rank words, the kept values in index order
@@ -703,7 +801,7 @@ __device__ __forceinline__ int nth_set_bit(u64 w, uint32_t r) {
 // count, not the tile size.
 template <bool kX>
 __global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, int R, int row0,
-                                                    float* __restrict__ data,
+                                                    int spec, float* __restrict__ data,
                                                     uint64_t* __restrict__ sel,
                                                     uint32_t* __restrict__ rank,
                                                     float* __restrict__ vals,
@@ -717,9 +815,45 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, int
   const int lane = lane_id();
   const int row = row0 + r;
   const int64_t W = lay.d_pad >> 6;
+  // count and flag of the tile's speculative list (read before the tile so
+  // that the two loads overlap)
+  const uint32_t sp =
+      !kX && spec ? *reinterpret_cast<const uint32_t*>(tile_hist(tk, lay, row, ti) + kTkSpecSlot)
+                  : 0u;
   const Tile tile = lay.tiles[ti];
   const int nw = (tile.count + 63) >> 6;
   uint64_t* sr = sel + (int64_t)r * W + (tile.start >> 6);
+  if (!kX) {
+    // a tile the gather took from its speculative list: emit it from the list
+    if ((sp >> 16) != 0u) {
+      static_assert(kTkSpecSlot % 2 == 0, "count and flag in one 32-bit word");
+      const uint32_t n = sp & 0xFFFFu;
+      const u64* ent = tk.spec + ((int64_t)row * lay.n_tiles + ti) * kTkSpecCap;
+      const uint32_t base = tk.tile_cnt[(int64_t)row * lay.n_tiles + ti];
+      const TkSel* stp = tk.sel + (int64_t)row * lay.L + tile.l;
+      const int64_t rel0 = tile.start - lay.tensors[tile.l].off;
+      const TkTensor* tp = tk.tens + tile.l;
+      uint32_t* rr = rank + (int64_t)r * W + (tile.start >> 6);
+      float* vr = vals + (int64_t)r * tk.total_keep + tp->voff;
+      float* dr = data + (int64_t)r * lay.d_pad + tile.start;
+      const uint32_t keep = (uint32_t)tp->keep;
+#define SAEF_EL(NC)                                                                       \
+  emit_list<NC>(ent, n, stp, rel0, base, keep, tile.count, nw, sr, rr, vr, dr, words[wave])
+      switch ((n + kWave - 1) / kWave) {
+        case 0: SAEF_EL(0); break;
+        case 1: SAEF_EL(1); break;
+        case 2: SAEF_EL(2); break;
+        case 3: SAEF_EL(3); break;
+        case 4: SAEF_EL(4); break;
+        case 5: SAEF_EL(5); break;
+        case 6: SAEF_EL(6); break;
+        case 7: SAEF_EL(7); break;
+        default: SAEF_EL(8); break;
+      }
+#undef SAEF_EL
+      return;
+    }
+  }
   const TensorInfo ten = lay.tensors[tile.l];
   const TkSel st = tk.sel[(int64_t)row * lay.L + tile.l];
   const TkTensor t = tk.tens[tile.l];
@@ -947,9 +1081,12 @@ struct Launcher {
     SAEF_LAUNCH(k_tk_offsets, dim3((unsigned)(R * tk.n_groups)), dim3(kWave), 0, s, lay, tk, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     // speculative lists exist for the worker rows only (the server's Delta
-    // comes from the aggregation kernel)
-    const int spec = row0 + R <= lay.k_max ? 1 : 0;
-    SAEF_LAUNCH(k_tk_gather, tiles, dim3(kBlock), 0, s, lay, tk, R, row0, spec, data, sel);
+    // comes from the aggregation kernel), and only if some tensor keeps them
+    const int spec = row0 + R <= lay.k_max && tk.lists != 0 ? 1 : 0;
+    if (spec)
+      SAEF_LAUNCH(k_tk_gather_spec, tiles, dim3(kBlock), 0, s, lay, tk, R, row0, data, sel);
+    else
+      SAEF_LAUNCH(k_tk_gather_full, tiles, dim3(kBlock), 0, s, lay, tk, R, row0, data, sel);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     SAEF_LAUNCH(k_tk_select, pairs, dim3(kBig), 0, s, lay, tk, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;
@@ -957,10 +1094,10 @@ struct Launcher {
     if ((err = hipGetLastError()) != hipSuccess) return err;
     if (x != nullptr)
       hipExtLaunchKernelGGL((k_tk_emit<true>), tiles, dim3(kBlock), 0, s, nullptr, last.stop, 0,
-                            lay, tk, R, row0, data, sel, rank, vals, x);
+                            lay, tk, R, row0, 0, data, sel, rank, vals, x);
     else
       hipExtLaunchKernelGGL((k_tk_emit<false>), tiles, dim3(kBlock), 0, s, nullptr, last.stop, 0,
-                            lay, tk, R, row0, data, sel, rank, vals, x);
+                            lay, tk, R, row0, spec, data, sel, rank, vals, x);
     return hipGetLastError();
   }
 };
