@@ -225,7 +225,9 @@ typedef struct saef_topk saef_topk;
 /* Top-K plan on a layout: keep[L] (host, 1 <= keep[l] <= n[l]) is copied;
  * the plan owns the selection scratch (tile histograms and their sums,
  * selection state, candidate slots, tile counts: about 8.3 bytes per
- * element of d_pad for each of the k_max + 1 rows).  The selection state
+ * element of d_pad for each of the k_max + 1 rows; lists of candidate
+ * elements for the worker Delta pass: 2 bytes per element of d_pad for each
+ * of the k_max worker rows).  The selection state
  * keeps, per worker row and tensor, where the last call found its threshold:
  * the next call's histogram is placed there, so the first call on a plan (or
  * one after the data scale jumped by more than about two binades) takes

@@ -14,11 +14,14 @@
 //   pick       a workgroup per (row, tensor) finds the bin b1 that holds the
 //              k-th largest key and each group's first candidate slot;
 //   offsets    each tile's first candidate slot (a scan inside its group);
-//   gather     one wave per tile reads Delta once more: elements above b1
-//              are kept for sure and go to the selection words (their count
-//              to the tile's kept count); the elements of b1 (the
-//              candidates) go to the tile's slots as (key, index in the
-//              tensor), in index order;
+//   gather     one wave per tile: elements above b1 are kept for sure
+//              (their count to the tile's kept count); the elements of b1
+//              (the candidates) go to the tile's slots as (key, index in the
+//              tensor), in index order.  Taken from the tile's speculative
+//              list (written by the Delta pass: the elements at or above a
+//              bound just below the previous threshold) when its bound lies
+//              at or below b1, else from one more read of Delta, which also
+//              gives the selection words of the sure elements;
 //   select     a workgroup per (row, tensor) finds, among the candidates only,
 //              the threshold key tau and the last kept index iota of the
 //              elements equal to tau (radix passes on the key bits below
@@ -30,7 +33,8 @@
 //   emit       one wave per tile adds its kept candidates to its selection
 //              words, then writes the rank words and the kept values in
 //              index order, and sets the kept elements of the error to 0
-//              (e = Delta - C(Delta) is Delta elsewhere).
+//              (e = Delta - C(Delta) is Delta elsewhere); a tile the gather
+//              took from its list is emitted from the list alone.
 // All of it is integer counting, so the kept set does not depend on the
 // launch geometry.
 //
