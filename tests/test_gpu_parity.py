@@ -294,6 +294,31 @@ def test_invalid_arguments_are_rejected():
         S.saef_compress(gs.layout, 2, 0.1, gs.e, gs.e, gs.signs, gs.scales)
 
 
+def test_profile_sampling():
+    """saef_profile_enable with every = 3 stamps dispatches 0, 3, 6 of each
+    timed kind and nothing else; every < 1 is rejected; the iterations give
+    the same bits as unprofiled ones."""
+    w = W.custom([5000, 70, 4097], K=2, period=0, seed=6)
+    _case("profile sampling")
+    gs, ref = H.GpuState(w), H.GpuState(w)
+    S = gs.saef
+    with pytest.raises(S.SaefError) as ex:
+        S.saef_profile_enable(gs.layout, 4, kinds=("compress",), every=0)
+    assert ex.value.rc == S.EINVAL
+    S.saef_profile_enable(gs.layout, 10, kinds=("compress", "aggregate"), every=3)
+    for t in range(7):
+        g = W.gradients(w, t)
+        gs.round(t, g)
+        ref.round(t, g)
+    prof = S.saef_profile_read(gs.layout)
+    S.saef_profile_enable(gs.layout, 0)
+    assert prof["compress"][0] == 3 and prof["aggregate"][0] == 3, prof
+    assert prof["compress"][1] > 0.0 and prof["aggregate"][1] > 0.0, prof
+    assert all(c == 0 for k, (c, _) in prof.items() if k not in ("compress", "aggregate")), prof
+    for name in ("x", "e", "e_srv", "signs", "scales"):
+        assert torch.equal(getattr(gs, name), getattr(ref, name)), name
+
+
 # ---------------------------------------------------------------- two halves, EF, mismatch
 
 SPLIT_CASES = {
