@@ -140,7 +140,7 @@ def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="resnet50",
                     help="flat64k | resnet56 | resnet50 | bert_base | flat256m")
     ap.add_argument("--cpu-rounds", type=int, default=2,

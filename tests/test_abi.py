@@ -61,3 +61,11 @@ def test_null_layout_is_rejected(saef):
     assert lib.saef_compress(None, 1, ctypes.c_float(0.1), None, None, None, None,
                              None) == saef.EINVAL
     assert lib.saef_round(None, 0, 0, 1, ctypes.c_float(0.1), 1, *([None] * 10)) == saef.EINVAL
+
+
+def test_profile_calls_reject_bad_arguments_on_host(saef):
+    lib = saef.raw_library()
+    counts = (ctypes.c_int32 * 7)()
+    ms = (ctypes.c_double * 7)()
+    assert lib.saef_profile_enable(None, 4, 1, 1) == saef.EINVAL   # no layout
+    assert lib.saef_profile_read(None, counts, ms) == saef.EINVAL
