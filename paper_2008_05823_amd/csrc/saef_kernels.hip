@@ -487,6 +487,7 @@ __global__ __launch_bounds__(kBlock) void k_step_average(DevLayout lay, int K, d
 }
 
 // ------------------------------------------------------------------ aggregate
+constexpr int kAggChunk = 4;  // workers whose sign words are loaded together
 // One pass of a wave over kN words of a tile: the K worker messages are
 // decoded in order, mean = (sum_k +-scale_k in binary64, k order) / K.
 // kFull: all kN words lie inside the tile; otherwise element base + 64 u
@@ -515,19 +516,31 @@ __device__ __forceinline__ void aggregate_pass(const DevLayout& lay, int K, doub
   double acc[kN];
 #pragma unroll
   for (int u = 0; u < kN; ++u) acc[u] = 0.0;
-  for (int k = 0; k < K; ++k) {
-    // +-scale_k in binary64: the two values differ only in the sign bit
-    const double sd = (double)scales[(int64_t)k * lay.L + l];
-    const uint32_t pos_hi = (uint32_t)__double2hiint(sd);
-    const uint32_t lo_bits = (uint32_t)__double2loint(sd);
-    const uint32_t neg_hi = pos_hi ^ 0x80000000u;
-    const uint64_t* sk = signs + (int64_t)k * W + gw;
-    u64 m[kN];
+  // workers in chunks of kAggChunk: the chunk's scales and sign words are all
+  // loaded (a worker past K reloads worker K - 1) before the first is used
+  for (int k0 = 0; k0 < K; k0 += kAggChunk) {
+    float sc[kAggChunk];
+    u64 m[kAggChunk][kN];
 #pragma unroll
-    for (int u = 0; u < kN; ++u) m[u] = sk[u];
+    for (int c = 0; c < kAggChunk; ++c) {
+      const int k = min(k0 + c, K - 1);
+      sc[c] = scales[(int64_t)k * lay.L + l];
+      const uint64_t* sk = signs + (int64_t)k * W + gw;
 #pragma unroll
-    for (int u = 0; u < kN; ++u)
-      acc[u] += __hiloint2double((int)sel_by_bit(m[u], pos_hi, neg_hi), (int)lo_bits);
+      for (int u = 0; u < kN; ++u) m[c][u] = sk[u];
+    }
+#pragma unroll
+    for (int c = 0; c < kAggChunk; ++c) {
+      if (k0 + c >= K) break;  // wave-uniform
+      // +-scale_k in binary64: the two values differ only in the sign bit
+      const double sd = (double)sc[c];
+      const uint32_t pos_hi = (uint32_t)__double2hiint(sd);
+      const uint32_t lo_bits = (uint32_t)__double2loint(sd);
+      const uint32_t neg_hi = pos_hi ^ 0x80000000u;
+#pragma unroll
+      for (int u = 0; u < kN; ++u)
+        acc[u] += __hiloint2double((int)sel_by_bit(m[c][u], pos_hi, neg_hi), (int)lo_bits);
+    }
   }
 #pragma unroll
   for (int u = 0; u < kN; ++u) {
