@@ -18,7 +18,7 @@ constexpr int kTkHistPad = 260;                // 16-bit counts per tile (even, 
 constexpr int kTkGroup = 64;      // tile histograms (or group sums) one sum workgroup adds
 constexpr int kTkBins = 2048;     // bins of an 11-bit radix digit
 constexpr int kTkChunk = 65536;   // elements per server-aggregation workgroup
-// Speculative candidate lists: for a tensor that keeps at most 1/16 of its
+// Speculative candidate lists: for a tensor that keeps at most 1/8 of its
 // elements, the worker Delta pass also writes, per (row, tile), the elements
 // whose key is at least the previous call's threshold key minus
 // kTkSpecMargin (1/32 binade), in index order, up to kTkSpecCap of them; their
@@ -32,7 +32,7 @@ constexpr int kTkSpecCap = 512;
 constexpr int kTkSpecSlot = kTkHist;
 constexpr uint32_t kTkSpecNone = 0xFFFFu;
 constexpr uint32_t kTkSpecMargin = 1u << 18;
-constexpr int kTkSpecMaxShare = 16;  // lists when k_l * 16 <= n_l
+constexpr int kTkSpecMaxShare = 8;  // lists when k_l * 8 <= n_l
 static_assert(kTkHistPad >= kTkHist && kTkHistPad % 4 == 0, "padded tile histogram");
 static_assert(kTileElems == 2048, "the Top-K kernels take a tile as 32 words, one per lane");
 static_assert(kTileElems < 65536, "a tile's bin counts fit 16 bits");
