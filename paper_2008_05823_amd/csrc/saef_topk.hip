@@ -949,7 +949,7 @@ __device__ __forceinline__ AggStep<U> agg_words(const uint64_t* __restrict__ sel
   return a;
 }
 
-template <int kMode, bool kAvg, int U>
+template <int kMode, bool kAvg, int U, bool kCo>
 __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, int K,
                                                        double inv_k,
                                                        const uint64_t* __restrict__ sel,
@@ -998,32 +998,87 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
       const bool last_b = k0 + kB >= K;
       const int nw0 = last_b ? w0 + stride : w0;
       const AggStep<U> nxt = agg_words<U>(sel, rank, W, gw, K, nw, nw0, last_b ? 0 : k0 + kB, lane);
-      // This step's values, read through a buffer resource over the worker's
-      // k_l values (a lane whose bit is clear reads past the end and gets 0);
-      // the loads of all pairs go out before the first one is used.
-      float cv[kB][U];
+      // This step's values, read through a buffer resource over each worker's
+      // k_l values (a read past the end gets 0 from the range check, with no
+      // memory access).
+      bool done = false;
+      if (kCo) {
+        // Dense messages: the kept values of a worker's U words are contiguous
+        // in its message; when no worker of the step has more than 64 of them,
+        // one load per worker brings them all (lane j: the group's j-th
+        // value) and each element takes its own with ds_bpermute.
+        uint32_t gcnt = (uint32_t)(__popc(cur.lo) + __popc(cur.hi));
 #pragma unroll
-      for (int kk = 0; kk < kB; ++kk) {
-        const int kidx = min(k0 + kk, K - 1);  // absent workers have empty words
-        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-            (void*)(vals + (int64_t)kidx * tk.total_keep + voff), 0, (int)(keep * 4u),
-            kBufWord3);
+        for (int off = 1; off < U; off <<= 1) gcnt += (uint32_t)__shfl_xor((int)gcnt, off);
+        if (__ballot(gcnt > (uint32_t)kWave) == 0ull) {  // wave-uniform
+          float gv[kB];
 #pragma unroll
-        for (int i = 0; i < U; ++i) {
-          const int q = kk * U + i;
-          const uint32_t mlo = __builtin_amdgcn_readlane(cur.lo, q);
-          const uint32_t mhi = __builtin_amdgcn_readlane(cur.hi, q);
-          const uint32_t r4 = __builtin_amdgcn_readlane(cur.rk4, q);
-          // rank of the lane's element among the word's kept ones, in bytes
-          const uint32_t below = __builtin_amdgcn_mbcnt_hi(mhi, __builtin_amdgcn_mbcnt_lo(mlo, 0u));
-          const uint32_t off = sel_by_bit(((u64)mhi << 32) | mlo, below * 4u + r4, 0x80000000u);
-          cv[kk][i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0));
+          for (int kk = 0; kk < kB; ++kk) {
+            const int kidx = min(k0 + kk, K - 1);  // absent workers have empty words
+            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                (void*)(vals + (int64_t)kidx * tk.total_keep + voff), 0, (int)(keep * 4u),
+                kBufWord3);
+            const uint32_t g4 = __builtin_amdgcn_readlane(cur.rk4, kk * U);  // group's first rank
+            gv[kk] = __uint_as_float(
+                __builtin_amdgcn_raw_buffer_load_b32(rs, g4 + 4u * (uint32_t)lane, 0, 0));
+          }
+#pragma unroll
+          for (int kk = 0; kk < kB; ++kk) {
+            const uint32_t g4 = __builtin_amdgcn_readlane(cur.rk4, kk * U);
+#pragma unroll
+            for (int i = 0; i < U; ++i) {
+              const int q = kk * U + i;
+              const uint32_t mlo = __builtin_amdgcn_readlane(cur.lo, q);
+              const uint32_t mhi = __builtin_amdgcn_readlane(cur.hi, q);
+              const uint32_t r4 = __builtin_amdgcn_readlane(cur.rk4, q);
+              // the lane's element: its position among the group's kept values
+              const uint32_t below =
+                  __builtin_amdgcn_mbcnt_hi(mhi, __builtin_amdgcn_mbcnt_lo(mlo, 0u));
+              const int src = (int)((r4 - g4) + 4u * below);  // < 4 * 64 for a kept element
+              const float v = __int_as_float(
+                  __builtin_amdgcn_ds_bpermute(src, __float_as_int(gv[kk])));
+              acc[i] += (double)sel_by_bit(((u64)mhi << 32) | mlo, v, 0.0f);  // worker order
+            }
+          }
+          done = true;
         }
       }
+      if (!done) {
+        // Sparse messages (or a worker with more than 64 kept values in the
+        // step's words): every (worker, word) pair gathers its values, a lane
+        // whose bit is clear reading past the end; the loads go out before the
+        // first one is used (with kCo, one worker at a time, which needs fewer
+        // registers next to the dense path).
+        constexpr int kW = kCo ? 1 : kB;  // workers whose loads go out together
+        for (int kw = 0; kw < kB; kw += kW) {
+          float cv[kW][U];
 #pragma unroll
-      for (int kk = 0; kk < kB; ++kk)
+          for (int kx = 0; kx < kW; ++kx) {
+            const int kk = kw + kx;
+            const int kidx = min(k0 + kk, K - 1);  // absent workers have empty words
+            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                (void*)(vals + (int64_t)kidx * tk.total_keep + voff), 0, (int)(keep * 4u),
+                kBufWord3);
 #pragma unroll
-        for (int i = 0; i < U; ++i) acc[i] += (double)cv[kk][i];  // worker order; absent: +0
+            for (int i = 0; i < U; ++i) {
+              const int q = kk * U + i;
+              const uint32_t mlo = __builtin_amdgcn_readlane(cur.lo, q);
+              const uint32_t mhi = __builtin_amdgcn_readlane(cur.hi, q);
+              const uint32_t r4 = __builtin_amdgcn_readlane(cur.rk4, q);
+              // rank of the lane's element among the word's kept ones, in bytes
+              const uint32_t below =
+                  __builtin_amdgcn_mbcnt_hi(mhi, __builtin_amdgcn_mbcnt_lo(mlo, 0u));
+              const uint32_t off =
+                  sel_by_bit(((u64)mhi << 32) | mlo, below * 4u + r4, 0x80000000u);
+              cv[kx][i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0));
+            }
+          }
+#pragma unroll
+          for (int kx = 0; kx < kW; ++kx)
+#pragma unroll
+            for (int i = 0; i < U; ++i) acc[i] += (double)cv[kx][i];  // worker order; absent: +0
+        }
+      }
       cur = nxt;
     }
 #pragma unroll
@@ -1133,13 +1188,23 @@ hipError_t launch_topk_aggregate(const DevLayout& lay, const TkDev& tk, int K, i
   const dim3 grid((unsigned)tk.n_chunks);
   const double ik = inv_pow2(K);
   hipEvent_t stop0 = mode == 1 ? nullptr : ev.stop;
-#define SAEF_TKA(M, A, U)                                                                       \
-  hipExtLaunchKernelGGL((k_tk_aggregate<M, A, U>), grid, dim3(kBig), 0, s, ev.start, stop0, 0, \
+  // dense messages (at least 1/32 of the elements kept): one load per worker
+  // and step, values handed out with ds_bpermute; sparser ones: per-pair
+  // gathers (faster there: at 1% kept 117 against 153 us at resnet50, K = 8;
+  // at 5% and 10%, 281 and 316 us against 265 and 290 us for the server step)
+  const bool co = tk.total_keep * 32 >= lay.d_pad;
+#define SAEF_TKA(M, A, U, C)                                                                       \
+  hipExtLaunchKernelGGL((k_tk_aggregate<M, A, U, C>), grid, dim3(kBig), 0, s, ev.start, stop0, 0, \
                         lay, tk, K, ik, sel, rank, vals, avg, e_srv, x)
 #define SAEF_TKA_U(M, A)                                 \
   do {                                                   \
-    if (K <= 8) SAEF_TKA(M, A, 8);                       \
-    else SAEF_TKA(M, A, 4);                              \
+    if (K <= 8) {                                        \
+      if (co) SAEF_TKA(M, A, 8, true);                   \
+      else SAEF_TKA(M, A, 8, false);                     \
+    } else {                                             \
+      if (co) SAEF_TKA(M, A, 4, true);                   \
+      else SAEF_TKA(M, A, 4, false);                     \
+    }                                                    \
   } while (0)
   if (mode == 1) {
     if (avg != nullptr) SAEF_TKA_U(1, true); else SAEF_TKA_U(1, false);
