@@ -216,9 +216,9 @@ def main() -> int:
 
     def step(t):
         if topk is not None and split:
-            saef.saef_topk_round_begin(topk, t, w.period, K, w.mode, variant, e, e_srv, x, xh_arg,
-                                       mism)
-            saef.saef_topk_round_end(topk, K, w.lr, 0.0 if mu is None else mu, w.mode,
+            saef.saef_topk_round_begin(topk, t, w.period, K, w.mode, variant, e, signs, e_srv, x,
+                                       xh_arg, mism)
+            saef.saef_topk_round_end(topk, t, w.period, K, w.lr, 0.0 if mu is None else mu, w.mode,
                                      g_dev[t % n_grad], m, e, e_srv, x, signs, tk_rank, tk_vals,
                                      srv_signs, tk_srank, tk_svals)
         elif topk is not None:

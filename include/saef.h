@@ -257,25 +257,42 @@ int saef_topk_aggregate(const saef_topk* plan, int32_t K, int32_t mode, const ui
                         hipStream_t stream);
 
 /* One iteration t of Algorithm 1 with Top-K, in two halves around the
- * gradient (the state is plain, so t only decides the averaging):
+ * gradient.  Worker state between iterations (build-defined, like the
+ * pending correction of saef_round): after saef_topk_round_end the worker
+ * errors e hold Delta with the kept elements not yet set to 0; the
+ * selection words sel written by the same call mark them.  The next
+ * iteration (t > 0) reads those elements as 0, and saef_topk_materialize
+ * gives the plain errors.  sel must not be changed in between.
  * saef_topk_round_begin: error averaging when (t+1) mod period == 0 (period
- * 0 = never), then the evaluation point: SAEF_VARIANT_SAEF xh[k] = x - e[k]
- * ((K, d_pad)), SAEF_VARIANT_EF xh = x ((d_pad)); mismatch (may be NULL):
- * the 2 L bounds of saef_round_begin from the state after averaging.
- * saef_topk_round_end: saef_topk_compress (m may be NULL, then mu must be
- * 0) and saef_topk_aggregate with the gradient g the caller computed at xh.
+ * 0 = never; the errors are then plain), then the evaluation point:
+ * SAEF_VARIANT_SAEF xh[k] = x - e[k] ((K, d_pad)), SAEF_VARIANT_EF xh = x
+ * ((d_pad)); mismatch (may be NULL): the 2 L bounds of saef_round_begin from
+ * the state after averaging (they first set the pending elements to 0 in
+ * place).  sel may be NULL at t = 0.
+ * saef_topk_round_end: the worker compression of saef_topk_compress (m may be
+ * NULL, then mu must be 0), leaving the kept elements pending, and
+ * saef_topk_aggregate with the gradient g the caller computed at xh; t and
+ * period must be those of the begin call (they tell whether e is pending).
  * saef_topk_round is begin (SAEF) + end. */
 int saef_topk_round_begin(const saef_topk* plan, int64_t t, int64_t period, int32_t K,
-                          int32_t mode, int32_t variant, float* e, const float* e_srv,
-                          const float* x, float* xh, double* mismatch, hipStream_t stream);
-int saef_topk_round_end(const saef_topk* plan, int32_t K, float lr, float mu, int32_t mode,
-                        const float* g, float* m, float* e, float* e_srv, float* x, uint64_t* sel,
-                        uint32_t* rank, float* vals, uint64_t* srv_sel, uint32_t* srv_rank,
-                        float* srv_vals, hipStream_t stream);
+                          int32_t mode, int32_t variant, float* e, const uint64_t* sel,
+                          const float* e_srv, const float* x, float* xh, double* mismatch,
+                          hipStream_t stream);
+int saef_topk_round_end(const saef_topk* plan, int64_t t, int64_t period, int32_t K, float lr,
+                        float mu, int32_t mode, const float* g, float* m, float* e, float* e_srv,
+                        float* x, uint64_t* sel, uint32_t* rank, float* vals, uint64_t* srv_sel,
+                        uint32_t* srv_rank, float* srv_vals, hipStream_t stream);
 int saef_topk_round(const saef_topk* plan, int64_t t, int64_t period, int32_t K, float lr,
                     float mu, int32_t mode, const float* g, float* m, float* e, float* e_srv,
                     float* x, float* xh, uint64_t* sel, uint32_t* rank, float* vals,
                     uint64_t* srv_sel, uint32_t* srv_rank, float* srv_vals, hipStream_t stream);
+
+/* The plain worker errors after saef_topk_round / saef_topk_round_end: sets
+ * to 0, in place, the elements of the K rows of e whose bit in sel (the
+ * selection words of the last compression) is set.  Doing it again, or on
+ * errors that are already plain, changes nothing. */
+int saef_topk_materialize(const saef_topk* plan, int32_t K, float* e, const uint64_t* sel,
+                          hipStream_t stream);
 
 /* Synchronises `stream`, then returns and clears the layout's sticky device
  * flag: SAEF_ERANGE if any call since the last saef_status met a value with

@@ -729,9 +729,12 @@ int saef_topk_info(const saef_topk* plan, int64_t* total_keep) {
   return SAEF_OK;
 }
 
-int saef_topk_compress(const saef_topk* plan, int32_t K, float lr, float mu, const float* g,
-                       float* m, float* e, uint64_t* sel, uint32_t* rank, float* vals,
-                       hipStream_t stream) {
+namespace {
+
+// saef_topk_compress with the pending flags of launch_topk_compress.
+int topk_compress(const saef_topk* plan, int32_t K, float lr, float mu, const float* g,
+                  float* m, float* e, uint64_t* sel, uint32_t* rank, float* vals, bool pend_in,
+                  bool pend_out, hipStream_t stream) {
   if (plan == nullptr) return SAEF_EINVAL;
   const saef_layout* layout = plan->layout;
   int rc = check_common(layout, K);
@@ -753,8 +756,29 @@ int saef_topk_compress(const saef_topk* plan, int32_t K, float lr, float mu, con
     return SAEF_EINVAL;
   return hip_rc(timed(layout, 1, [&](const saef::LaunchEvents& ev) {
     return saef::launch_topk_compress(layout->dev, plan->dev, K, lr, mu, g, m, e, sel, rank,
-                                      vals, stream, ev);
+                                      vals, pend_in, pend_out, stream, ev);
   }));
+}
+
+}  // namespace
+
+int saef_topk_compress(const saef_topk* plan, int32_t K, float lr, float mu, const float* g,
+                       float* m, float* e, uint64_t* sel, uint32_t* rank, float* vals,
+                       hipStream_t stream) {
+  return topk_compress(plan, K, lr, mu, g, m, e, sel, rank, vals, false, false, stream);
+}
+
+int saef_topk_materialize(const saef_topk* plan, int32_t K, float* e, const uint64_t* sel,
+                          hipStream_t stream) {
+  if (plan == nullptr) return SAEF_EINVAL;
+  const saef_layout* layout = plan->layout;
+  int rc = check_common(layout, K);
+  if (rc != SAEF_OK) return rc;
+  if (!f32_ok(e) || !u64_ok(sel)) return SAEF_EINVAL;
+  const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
+  const size_t wb = (size_t)K * (layout->d_pad / 64) * sizeof(uint64_t);
+  if (overlap(sel, wb, e, vb)) return SAEF_EINVAL;
+  return hip_rc(saef::launch_topk_materialize(layout->dev, K, e, sel, stream));
 }
 
 int saef_topk_aggregate(const saef_topk* plan, int32_t K, int32_t mode, const uint64_t* sel,
@@ -792,8 +816,9 @@ int saef_topk_aggregate(const saef_topk* plan, int32_t K, int32_t mode, const ui
 }
 
 int saef_topk_round_begin(const saef_topk* plan, int64_t t, int64_t period, int32_t K,
-                          int32_t mode, int32_t variant, float* e, const float* e_srv,
-                          const float* x, float* xh, double* mismatch, hipStream_t stream) {
+                          int32_t mode, int32_t variant, float* e, const uint64_t* sel,
+                          const float* e_srv, const float* x, float* xh, double* mismatch,
+                          hipStream_t stream) {
   if (plan == nullptr) return SAEF_EINVAL;
   const saef_layout* layout = plan->layout;
   int rc = check_common(layout, K);
@@ -802,6 +827,10 @@ int saef_topk_round_begin(const saef_topk* plan, int64_t t, int64_t period, int3
   if (mode != SAEF_MODE_SC && mode != SAEF_MODE_DC) return SAEF_EINVAL;
   if (variant != SAEF_VARIANT_EF && variant != SAEF_VARIANT_SAEF) return SAEF_EINVAL;
   if (!f32_ok(e) || !f32_ok(x) || !f32_ok(xh)) return SAEF_EINVAL;
+  // after t = 0, e holds the previous iteration's Delta with its kept
+  // elements (the selection words sel) pending
+  const bool pending = t > 0;
+  if (pending && !u64_ok(sel)) return SAEF_EINVAL;
   if (mismatch != nullptr && (!aligned(mismatch, 8) || (mode == SAEF_MODE_DC && !f32_ok(e_srv))))
     return SAEF_EINVAL;
   const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
@@ -816,15 +845,26 @@ int saef_topk_round_begin(const saef_topk* plan, int64_t t, int64_t period, int3
         overlap(mismatch, mb, x, xb) || (e_srv != nullptr && overlap(mismatch, mb, e_srv, xb)))
       return SAEF_EINVAL;
   }
-  // the Top-K state is always plain: nothing to decode
+  if (pending) {
+    const size_t wb = (size_t)K * (layout->d_pad / 64) * sizeof(uint64_t);
+    if (overlap(sel, wb, e, vb) || overlap(sel, wb, xh, hb) || overlap(sel, wb, x, xb))
+      return SAEF_EINVAL;
+  }
   const bool averaging = period > 0 && (t + 1) % period == 0;
   const DevLayout& d = layout->dev;
+  const int dec = pending ? saef::kDecZero : saef::kDecPlain;
   if (variant == SAEF_VARIANT_SAEF || averaging) {
     float* h = variant == SAEF_VARIANT_SAEF ? xh : nullptr;
     rc = hip_rc(timed(layout, averaging ? 5 : 0, [&](const saef::LaunchEvents& ev) {
-      return saef::launch_step_ahead(d, K, x, nullptr, nullptr, false, e, nullptr, nullptr, false,
+      return saef::launch_step_ahead(d, K, x, nullptr, nullptr, false, e, sel, nullptr, dec,
                                      averaging, h, stream, ev);
     }));
+    if (rc != SAEF_OK) return rc;
+  }
+  if (mismatch != nullptr && pending && !averaging) {
+    // the bounds read the plain errors: set the pending elements to 0 in place
+    // (the next reader's zeroing of them is then a no-op)
+    rc = hip_rc(saef::launch_topk_materialize(d, K, e, sel, stream));
     if (rc != SAEF_OK) return rc;
   }
   if (mismatch != nullptr) {
@@ -840,18 +880,24 @@ int saef_topk_round_begin(const saef_topk* plan, int64_t t, int64_t period, int3
   }));
 }
 
-int saef_topk_round_end(const saef_topk* plan, int32_t K, float lr, float mu, int32_t mode,
-                        const float* g, float* m, float* e, float* e_srv, float* x, uint64_t* sel,
-                        uint32_t* rank, float* vals, uint64_t* srv_sel, uint32_t* srv_rank,
-                        float* srv_vals, hipStream_t stream) {
+int saef_topk_round_end(const saef_topk* plan, int64_t t, int64_t period, int32_t K, float lr,
+                        float mu, int32_t mode, const float* g, float* m, float* e, float* e_srv,
+                        float* x, uint64_t* sel, uint32_t* rank, float* vals, uint64_t* srv_sel,
+                        uint32_t* srv_rank, float* srv_vals, hipStream_t stream) {
   if (plan == nullptr) return SAEF_EINVAL;
+  if (t < 0 || period < 0) return SAEF_EINVAL;
   const saef_layout* layout = plan->layout;
+  if (layout == nullptr || K < 1 || K > layout->k_max) return SAEF_EINVAL;
   const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
   const size_t xb = layout->d_pad * sizeof(float);
   if (g != nullptr && x != nullptr && e != nullptr &&
       (overlap(g, vb, x, xb) || overlap(e, vb, x, xb)))
     return SAEF_EINVAL;
-  int rc = saef_topk_compress(plan, K, lr, mu, g, m, e, sel, rank, vals, stream);
+  // e is pending unless t = 0 or this iteration's averaging wrote it plain;
+  // the compression leaves its own kept elements pending
+  const bool averaging = period > 0 && (t + 1) % period == 0;
+  int rc = topk_compress(plan, K, lr, mu, g, m, e, sel, rank, vals, t > 0 && !averaging, true,
+                         stream);
   if (rc != SAEF_OK) return rc;
   return saef_topk_aggregate(plan, K, mode, sel, rank, vals, nullptr, e_srv, srv_sel, srv_rank,
                              srv_vals, x, stream);
@@ -868,12 +914,12 @@ int saef_topk_round(const saef_topk* plan, int64_t t, int64_t period, int32_t K,
   if (!f32_ok(xh) || !f32_ok(g)) return SAEF_EINVAL;
   const size_t vb = (size_t)K * layout->d_pad * sizeof(float);
   if (overlap(xh, vb, g, vb)) return SAEF_EINVAL;
-  rc = saef_topk_round_begin(plan, t, period, K, mode, SAEF_VARIANT_SAEF, e, e_srv, x, xh,
+  rc = saef_topk_round_begin(plan, t, period, K, mode, SAEF_VARIANT_SAEF, e, sel, e_srv, x, xh,
                              nullptr, stream);
   if (rc != SAEF_OK) return rc;
   // [gradient slot: g was computed by the caller at xh]
-  return saef_topk_round_end(plan, K, lr, mu, mode, g, m, e, e_srv, x, sel, rank, vals, srv_sel,
-                             srv_rank, srv_vals, stream);
+  return saef_topk_round_end(plan, t, period, K, lr, mu, mode, g, m, e, e_srv, x, sel, rank,
+                             vals, srv_sel, srv_rank, srv_vals, stream);
 }
 
 int saef_status(const saef_layout* layout, hipStream_t stream) {

@@ -105,15 +105,23 @@ hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_
                             const float* srv_scales, float* x, bool decode, hipStream_t s,
                            const LaunchEvents& ev = LaunchEvents());
 
+// How the worker errors are read: as stored; with the pending scaled-sign
+// correction (e - (bit ? s : -s), sign words and scales); or with the
+// pending Top-K zeroing (0 where the selection bit is set).
+constexpr int kDecPlain = 0;
+constexpr int kDecSign = 1;
+constexpr int kDecZero = 2;
+
 // Step ahead / error averaging.  decode_x: apply the pending server
 // correction to x on read (x is never written here; the aggregate kernel
-// materializes it).  decode_e: apply the pending worker corrections to e on
-// read.  average: replace every e[k] by the mean and write it back (plain).
-// xh written when non-null (required unless average; without xh, x is not
-// read and decode_x must be false).
+// materializes it; requires decode_e == kDecSign).  decode_e: how e is read
+// (kDecPlain / kDecSign / kDecZero; `signs` holds the sign or selection
+// words).  average: replace every e[k] by the mean and write it back
+// (plain).  xh written when non-null (required unless average; without xh,
+// x is not read and decode_x must be false).
 hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
                              const uint64_t* srv_signs, const float* srv_scales, bool decode_x,
-                             float* e, const uint64_t* signs, const float* scales, bool decode_e,
+                             float* e, const uint64_t* signs, const float* scales, int decode_e,
                              bool average, float* xh, hipStream_t s,
                            const LaunchEvents& ev = LaunchEvents());
 

@@ -304,7 +304,7 @@ __global__ __launch_bounds__(kBlock) void k_finalize2(DevLayout lay, int server,
 // e^(k)_t with the pending corrections of x and e applied on the fly
 // (kHasE false: x_t itself, the evaluation point of local error feedback).
 // kFull: all kU words are whole words of the tile (no guards).
-template <bool kDecX, bool kDecE, bool kHasE, bool kFull>
+template <bool kDecX, int kDecE, bool kHasE, bool kFull>
 __device__ __forceinline__ void step_words(int w0, int nw, int count,
                                            const float* __restrict__ xt,
                                            const float* __restrict__ ek, float* __restrict__ hk,
@@ -321,7 +321,7 @@ __device__ __forceinline__ void step_words(int w0, int nw, int count,
     xv[u] = ok ? (kHasE ? xt[j] : ld_nt(xt + j)) : 0.0f;
     ev[u] = (kHasE && ok) ? ld_nt(ek + j) : 0.0f;
     mx[u] = (kDecX && (kFull || w0 + u < nw)) ? sx[w0 + u] : 0ull;
-    me[u] = (kDecE && (kFull || w0 + u < nw)) ? sk[w0 + u] : 0ull;
+    me[u] = (kDecE != kDecPlain && (kFull || w0 + u < nw)) ? sk[w0 + u] : 0ull;
   }
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
@@ -329,7 +329,8 @@ __device__ __forceinline__ void step_words(int w0, int nw, int count,
     if (!kFull && w0 + u >= nw) continue;
     float xc = xv[u], ec = ev[u];
     if (kDecX) xc = xc - corr(mx[u], s_x);  // x_t = x_{t-1} - C(Delta_t)
-    if (kDecE) ec = ec - corr(me[u], s_e);  // e_t = Delta - C(Delta)
+    if (kDecE == kDecSign) ec = ec - corr(me[u], s_e);  // e_t = Delta - C(Delta)
+    if (kDecE == kDecZero) ec = sel_by_bit(me[u], 0.0f, ec);  // kept elements: 0
     if (kFull || j < count) st_nt(hk + j, kHasE ? xc - ec : xc);  // x^(k)_{t+1/2} = x_t - e^(k)_t
   }
 }
@@ -340,7 +341,7 @@ __device__ __forceinline__ void step_words(int w0, int nw, int count,
 // from that XCD's L2.  x itself is not written: the pending re-update of x
 // is applied here on the fly and materialized by the aggregate kernel.
 // kHasE false (K = 1, e unused): xh = x_t.
-template <bool kDecX, bool kDecE, bool kHasE>
+template <bool kDecX, int kDecE, bool kHasE>
 __global__ __launch_bounds__(kBlock) void k_step(DevLayout lay, int K, const float* __restrict__ x,
                                                  const uint64_t* __restrict__ ss,
                                                  const float* __restrict__ sscales,
@@ -361,7 +362,7 @@ __global__ __launch_bounds__(kBlock) void k_step(DevLayout lay, int K, const flo
   const float* xt = x + tile.start;
   const uint64_t* sk = signs + (int64_t)k * (d_pad >> 6) + gw0;
   const uint64_t* sx = ss + gw0;
-  const float s_e = kDecE ? scales[(int64_t)k * lay.L + tile.l] : 0.0f;
+  const float s_e = kDecE == kDecSign ? scales[(int64_t)k * lay.L + tile.l] : 0.0f;
   const float s_x = kDecX ? sscales[tile.l] : 0.0f;
   const int nw = (tile.count + 63) >> 6;
   for (int w0 = wave * kU; w0 < nw; w0 += kWaves * kU) {
@@ -382,7 +383,7 @@ constexpr int kAvgChunk = 4;  // workers whose loads are issued together
 // x^(k)_{t+1/2} = x_t - mean for every worker when kXh.  kFull: the kN
 // words are whole words of the tile; otherwise kN is 1 and the lane's
 // element exists iff `valid`.
-template <bool kDecX, bool kDecE, bool kXh, bool kFull, int kN>
+template <bool kDecX, int kDecE, bool kXh, bool kFull, int kN>
 __device__ __forceinline__ void average_words(const DevLayout& lay, int K, double inv_k, int l,
                                               int w0, bool valid, int64_t start,
                                               const float* __restrict__ x,
@@ -413,17 +414,18 @@ __device__ __forceinline__ void average_words(const DevLayout& lay, int K, doubl
 #pragma unroll
       for (int u = 0; u < kN; ++u) {
         ev[c][u] = (kin && ok) ? ld_nt(ek + u * 64) : 0.0f;
-        hw[c][u] = (kDecE && kin) ? half_word(sk + u, lane) : 0u;
+        hw[c][u] = (kDecE != kDecPlain && kin) ? half_word(sk + u, lane) : 0u;
       }
     }
 #pragma unroll
     for (int c = 0; c < kAvgChunk; ++c) {
       if (k0 + c >= K) continue;
-      const float s = kDecE ? scales[(int64_t)(k0 + c) * lay.L + l] : 0.0f;
+      const float s = kDecE == kDecSign ? scales[(int64_t)(k0 + c) * lay.L + l] : 0.0f;
 #pragma unroll
       for (int u = 0; u < kN; ++u) {
         float v = ev[c][u];
-        if (kDecE) v = v - (half_bit(hw[c][u], lane) ? s : -s);
+        if (kDecE == kDecSign) v = v - (half_bit(hw[c][u], lane) ? s : -s);
+        if (kDecE == kDecZero) v = half_bit(hw[c][u], lane) ? 0.0f : v;
         acc[u] += (double)v;
       }
     }
@@ -454,7 +456,7 @@ __device__ __forceinline__ void average_words(const DevLayout& lay, int K, doubl
 // Grid: run_padded_tiles(n_tiles) workgroups, one per tile in the XCD-aware
 // tile order of run_tile_of; wave w takes words w*kUA .. w*kUA+kUA-1 of the
 // tile, then strides by 4*kUA words.
-template <bool kDecX, bool kDecE, bool kXh>
+template <bool kDecX, int kDecE, bool kXh>
 __global__ __launch_bounds__(kBlock) void k_step_average(DevLayout lay, int K, double inv_k,
                                                          const float* __restrict__ x,
                                                          const uint64_t* __restrict__ ss,
@@ -992,9 +994,10 @@ hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_
 
 hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
                              const uint64_t* srv_signs, const float* srv_scales, bool decode_x,
-                             float* e, const uint64_t* signs, const float* scales, bool decode_e,
+                             float* e, const uint64_t* signs, const float* scales, int decode_e,
                              bool average, float* xh, hipStream_t s, const LaunchEvents& ev) {
-  if (decode_x && !decode_e) return hipErrorInvalidValue;  // never requested
+  if (decode_e < kDecPlain || decode_e > kDecZero) return hipErrorInvalidValue;
+  if (decode_x && decode_e != kDecSign) return hipErrorInvalidValue;  // never requested
   if (average) {
     const dim3 grid((unsigned)run_padded_tiles(lay.n_tiles));
     const double ik = inv_pow2(K);
@@ -1003,13 +1006,17 @@ hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
                      srv_signs, srv_scales, e, signs, scales, xh)
     if (xh == nullptr) {
       if (decode_x) return hipErrorInvalidValue;  // x is not read without xh
-      if (decode_e) SAEF_AV(false, true, false); else SAEF_AV(false, false, false);
+      if (decode_e == kDecSign) SAEF_AV(false, kDecSign, false);
+      else if (decode_e == kDecZero) SAEF_AV(false, kDecZero, false);
+      else SAEF_AV(false, kDecPlain, false);
     } else if (decode_x) {
-      SAEF_AV(true, true, true);
-    } else if (decode_e) {
-      SAEF_AV(false, true, true);
+      SAEF_AV(true, kDecSign, true);
+    } else if (decode_e == kDecSign) {
+      SAEF_AV(false, kDecSign, true);
+    } else if (decode_e == kDecZero) {
+      SAEF_AV(false, kDecZero, true);
     } else {
-      SAEF_AV(false, false, true);
+      SAEF_AV(false, kDecPlain, true);
     }
 #undef SAEF_AV
   } else {
@@ -1019,11 +1026,13 @@ hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
   SAEF_LAUNCH((k_step<DX, DE, true>), grid, dim3(kBlock), 0, s, lay, K, x, srv_signs, \
                      srv_scales, e, signs, scales, xh)
     if (decode_x) {
-      SAEF_ST(true, true);
-    } else if (decode_e) {
-      SAEF_ST(false, true);
+      SAEF_ST(true, kDecSign);
+    } else if (decode_e == kDecSign) {
+      SAEF_ST(false, kDecSign);
+    } else if (decode_e == kDecZero) {
+      SAEF_ST(false, kDecZero);
     } else {
-      SAEF_ST(false, false);
+      SAEF_ST(false, kDecPlain);
     }
 #undef SAEF_ST
   }
@@ -1035,10 +1044,10 @@ hipError_t launch_weights(const DevLayout& lay, const float* x, const uint64_t* 
                           const LaunchEvents& ev) {
   const dim3 grid((unsigned)run_padded_tiles(lay.n_tiles));
   if (decode_x) {
-    SAEF_LAUNCH((k_step<true, false, false>), grid, dim3(kBlock), 0, s, lay, 1, x, srv_signs,
+    SAEF_LAUNCH((k_step<true, kDecPlain, false>), grid, dim3(kBlock), 0, s, lay, 1, x, srv_signs,
                 srv_scales, nullptr, nullptr, nullptr, xh);
   } else {
-    SAEF_LAUNCH((k_step<false, false, false>), grid, dim3(kBlock), 0, s, lay, 1, x, srv_signs,
+    SAEF_LAUNCH((k_step<false, kDecPlain, false>), grid, dim3(kBlock), 0, s, lay, 1, x, srv_signs,
                 srv_scales, nullptr, nullptr, nullptr, xh);
   }
   return hipGetLastError();

@@ -107,12 +107,19 @@ struct TkDev {
 };
 
 // Worker Top-K compression of K rows (row k of e, histogram row k).  m
-// non-null: momentum.  Writes Delta into e (then the kept elements are
-// zeroed), the selection words, rank words and values of each row.
+// non-null: momentum.  Writes Delta into e, the selection words, rank words
+// and values of each row.  pend_in: e holds the previous call's Delta whose
+// kept elements (the selection words in sel) are still to be set to 0; they
+// are read as 0.  pend_out: this call's kept elements are left as they are
+// (pending, for the next reader) instead of being set to 0.
 hipError_t launch_topk_compress(const DevLayout& lay, const TkDev& tk, int K, float lr, float mu,
                                 const float* g, float* m, float* e, uint64_t* sel,
-                                uint32_t* rank, float* vals, hipStream_t s,
-                                const LaunchEvents& ev = LaunchEvents());
+                                uint32_t* rank, float* vals, bool pend_in, bool pend_out,
+                                hipStream_t s, const LaunchEvents& ev = LaunchEvents());
+
+// Sets to 0 the elements of the K rows of e whose selection bit is set.
+hipError_t launch_topk_materialize(const DevLayout& lay, int K, float* e, const uint64_t* sel,
+                                   hipStream_t s, const LaunchEvents& ev = LaunchEvents());
 
 // Server Top-K aggregation: mean of the K decoded messages; mode 1: e_srv
 // <- e_srv + mean, its Top-K message, e_srv at kept elements <- 0 and x <- x

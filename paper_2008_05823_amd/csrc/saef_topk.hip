@@ -109,14 +109,16 @@ __device__ __forceinline__ uint32_t spec_floor(const TkSel& st) {
 // ------------------------------------------------------------------ pass 1 (workers)
 // kTkU words of one worker's tile: m <- fma(mu, m, g) with kMom, Delta =
 // fma(lr, m or g, e), Delta stored into e, its key counted.
-template <bool kMom, bool kFull>
+template <bool kMom, bool kPend, bool kFull>
 __device__ __forceinline__ void delta_words(int w0, int nw, int count, float lr, float mu,
                                             const float* __restrict__ gk, float* __restrict__ mk,
-                                            float* __restrict__ ek, uint32_t win, uint32_t lo,
-                                            uint32_t* h, uint32_t (&bits)[kTkU],
+                                            float* __restrict__ ek,
+                                            const uint64_t* __restrict__ pk, uint32_t win,
+                                            uint32_t lo, uint32_t* h, uint32_t (&bits)[kTkU],
                                             u64 (&lm)[kTkU], bool& bad) {
   const int lane = lane_id();
   float gv[kTkU], ev[kTkU], mv[kTkU];
+  u64 pw[kTkU];
 #pragma unroll
   for (int u = 0; u < kTkU; ++u) {
     const int j = (w0 + u) * 64 + lane;
@@ -124,7 +126,12 @@ __device__ __forceinline__ void delta_words(int w0, int nw, int count, float lr,
     gv[u] = ld_nt_or0(gk, j, ok);
     ev[u] = ld_nt_or0(ek, j, ok);
     mv[u] = kMom ? ld_nt_or0(mk, j, ok) : 0.0f;
+    pw[u] = (kPend && (kFull || w0 + u < nw)) ? pk[w0 + u] : 0ull;
   }
+  // the previous call left its kept elements pending: they are 0
+#pragma unroll
+  for (int u = 0; u < kTkU; ++u)
+    if (kPend) ev[u] = sel_by_bit(pw[u], 0.0f, ev[u]);
 #pragma unroll
   for (int u = 0; u < kTkU; ++u) {
     const int j = (w0 + u) * 64 + lane;
@@ -147,12 +154,15 @@ __device__ __forceinline__ void delta_words(int w0, int nw, int count, float lr,
 
 // Grid: n_tiles * K workgroups; workgroup b handles worker b % K of tile b / K.
 // Each wave takes kTkU words of the tile (one pass); the tile's speculative
-// list is written in index order (wave by wave) when it fits.
-template <bool kMom>
+// list is written in index order (wave by wave) when it fits.  kPend: e
+// holds the previous call's Delta with its kept elements (selection words
+// psel) still to be set to 0; they are read as 0.
+template <bool kMom, bool kPend>
 __global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, int K, float lr,
                                                      float mu, const float* __restrict__ g,
                                                      float* __restrict__ m,
-                                                     float* __restrict__ e) {
+                                                     float* __restrict__ e,
+                                                     const uint64_t* __restrict__ psel) {
   static_assert(kWaves * kTkU == kTileWords, "one pass of the four waves covers a tile");
   __shared__ uint32_t h[kTkHistPad];
   __shared__ uint32_t s_cnt[kWaves];
@@ -176,12 +186,14 @@ __global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, in
   u64 lm[kTkU];
 #pragma unroll
   for (int u = 0; u < kTkU; ++u) lm[u] = 0ull;
+  const uint64_t* pk = kPend ? psel + (int64_t)k * (lay.d_pad >> 6) + (tile.start >> 6) : nullptr;
   if (w0 < nw) {
     if ((w0 + kTkU) * 64 <= tile.count)
-      delta_words<kMom, true>(w0, nw, tile.count, lr, mu, gk, mk, ek, win, lo, h, bits, lm, bad);
+      delta_words<kMom, kPend, true>(w0, nw, tile.count, lr, mu, gk, mk, ek, pk, win, lo, h, bits,
+                                     lm, bad);
     else
-      delta_words<kMom, false>(w0, nw, tile.count, lr, mu, gk, mk, ek, win, lo, h, bits, lm,
-                               bad);
+      delta_words<kMom, kPend, false>(w0, nw, tile.count, lr, mu, gk, mk, ek, pk, win, lo, h,
+                                      bits, lm, bad);
   }
   if (__ballot(bad) != 0 && lane_id() == 0) atomicOr(lay.status, kStatusRange);
   uint32_t mine = 0;
@@ -742,7 +754,7 @@ __device__ __forceinline__ int nth_set_bit(u64 w, uint32_t r) {
 // its value (from the entry) goes to the message at the tile's first rank
 // plus the kept entries before it, the error there is set to 0, and the
 // selection words (assembled in LDS) and rank words are written.
-template <int kNC>
+template <int kNC, bool kPend>
 __device__ __forceinline__ void emit_list(const u64* __restrict__ ent, uint32_t n,
                                           const TkSel* stp, int64_t rel0, uint32_t base,
                                           uint32_t keep, int count, int nw,
@@ -775,7 +787,7 @@ __device__ __forceinline__ void emit_list(const u64* __restrict__ ent, uint32_t 
                                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)km, 0u));
       if (pos < keep && idx < (uint32_t)count) {  // both always hold
         vr[pos] = __uint_as_float(raw);
-        st_nt(dr + idx, 0.0f);  // e = Delta - C(Delta) = 0 at a kept element
+        if (!kPend) st_nt(dr + idx, 0.0f);  // e = Delta - C(Delta) = 0 at a kept element
       }
     }
     run += (uint32_t)__popcll(km);
@@ -803,7 +815,7 @@ __device__ __forceinline__ void emit_list(const u64* __restrict__ ent, uint32_t 
 // lane i takes the tile's kept elements i, i + 64, ...: its word by a binary
 // search over the scan, its bit by nth_set_bit, so the work follows the kept
 // count, not the tile size.
-template <bool kX>
+template <bool kX, bool kPend>
 __global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, int R, int row0,
                                                     int spec, float* __restrict__ data,
                                                     uint64_t* __restrict__ sel,
@@ -842,7 +854,7 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, int
       float* dr = data + (int64_t)r * lay.d_pad + tile.start;
       const uint32_t keep = (uint32_t)tp->keep;
 #define SAEF_EL(NC)                                                                       \
-  emit_list<NC>(ent, n, stp, rel0, base, keep, tile.count, nw, sr, rr, vr, dr, words[wave])
+  emit_list<NC, kPend>(ent, n, stp, rel0, base, keep, tile.count, nw, sr, rr, vr, dr, words[wave])
       switch ((n + kWave - 1) / kWave) {
         case 0: SAEF_EL(0); break;
         case 1: SAEF_EL(1); break;
@@ -910,7 +922,7 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, int
     if (i < total && j < tile.count && pos < (uint32_t)t.keep) {  // the last two always hold
       const float v = dr[j];
       vr[pos] = v;
-      dr[j] = 0.0f;  // e = Delta - C(Delta) = 0 at a kept element
+      if (!kPend) dr[j] = 0.0f;  // e = Delta - C(Delta) = 0 at a kept element
       if (kX) xt[j] -= v;
     }
   }
@@ -1122,7 +1134,8 @@ struct Launcher {
   // sums, pick, offsets, gather, select, scan, emit.  The last kernel
   // stamps the caller's stop event.
   hipError_t select_and_emit(int R, int row0, float* data, uint64_t* sel, uint32_t* rank,
-                             float* vals, float* x, const LaunchEvents& last) const {
+                             float* vals, float* x, bool pend_out,
+                             const LaunchEvents& last) const {
     const LaunchEvents ev;
     hipError_t err;
     SAEF_LAUNCH(k_tk_sum<false>, dim3((unsigned)(R * tk.n_groups)), dim3(kBlock), 0, s, lay, tk,
@@ -1152,11 +1165,14 @@ struct Launcher {
     SAEF_LAUNCH(k_tk_scan, pairs, dim3(kBlock), 0, s, lay, tk, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     if (x != nullptr)
-      hipExtLaunchKernelGGL((k_tk_emit<true>), tiles, dim3(kBlock), 0, s, nullptr, last.stop, 0,
-                            lay, tk, R, row0, 0, data, sel, rank, vals, x);
+      hipExtLaunchKernelGGL((k_tk_emit<true, false>), tiles, dim3(kBlock), 0, s, nullptr,
+                            last.stop, 0, lay, tk, R, row0, 0, data, sel, rank, vals, x);
+    else if (pend_out)
+      hipExtLaunchKernelGGL((k_tk_emit<false, true>), tiles, dim3(kBlock), 0, s, nullptr,
+                            last.stop, 0, lay, tk, R, row0, spec, data, sel, rank, vals, x);
     else
-      hipExtLaunchKernelGGL((k_tk_emit<false>), tiles, dim3(kBlock), 0, s, nullptr, last.stop, 0,
-                            lay, tk, R, row0, spec, data, sel, rank, vals, x);
+      hipExtLaunchKernelGGL((k_tk_emit<false, false>), tiles, dim3(kBlock), 0, s, nullptr,
+                            last.stop, 0, lay, tk, R, row0, spec, data, sel, rank, vals, x);
     return hipGetLastError();
   }
 };
@@ -1165,19 +1181,47 @@ struct Launcher {
 
 hipError_t launch_topk_compress(const DevLayout& lay, const TkDev& tk, int K, float lr, float mu,
                                 const float* g, float* m, float* e, uint64_t* sel,
-                                uint32_t* rank, float* vals, hipStream_t s,
-                                const LaunchEvents& ev) {
+                                uint32_t* rank, float* vals, bool pend_in, bool pend_out,
+                                hipStream_t s, const LaunchEvents& ev) {
   const dim3 grid((unsigned)(lay.n_tiles * K));
   // the first kernel stamps the start event, the last one the stop event
-  if (m != nullptr)
-    hipExtLaunchKernelGGL((k_tk_delta<true>), grid, dim3(kBlock), 0, s, ev.start, nullptr, 0, lay,
-                          tk, K, lr, mu, g, m, e);
-  else
-    hipExtLaunchKernelGGL((k_tk_delta<false>), grid, dim3(kBlock), 0, s, ev.start, nullptr, 0,
-                          lay, tk, K, lr, mu, g, m, e);
+#define SAEF_TKD(MOM, PEND)                                                                     \
+  hipExtLaunchKernelGGL((k_tk_delta<MOM, PEND>), grid, dim3(kBlock), 0, s, ev.start, nullptr, 0, \
+                        lay, tk, K, lr, mu, g, m, e, sel)
+  if (m != nullptr) {
+    if (pend_in) SAEF_TKD(true, true); else SAEF_TKD(true, false);
+  } else {
+    if (pend_in) SAEF_TKD(false, true); else SAEF_TKD(false, false);
+  }
+#undef SAEF_TKD
   const hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  return Launcher{lay, tk, s}.select_and_emit(K, 0, e, sel, rank, vals, nullptr, ev);
+  return Launcher{lay, tk, s}.select_and_emit(K, 0, e, sel, rank, vals, nullptr, pend_out, ev);
+}
+
+// Grid: n_tiles * K workgroups; workgroup b sets to 0 the elements of worker
+// b % K's tile b / K whose selection bit is set (wave w: words w*kTkU ..).
+__global__ __launch_bounds__(kBlock) void k_tk_zero(DevLayout lay, int K, float* __restrict__ e,
+                                                    const uint64_t* __restrict__ sel) {
+  const int k = (int)(blockIdx.x % (unsigned)K);
+  const int64_t ti = blockIdx.x / (unsigned)K;
+  const Tile tile = lay.tiles[ti];
+  const int nw = (tile.count + 63) >> 6;
+  const int lane = lane_id();
+  const uint64_t* sk = sel + (int64_t)k * (lay.d_pad >> 6) + (tile.start >> 6);
+  float* ek = e + (int64_t)k * lay.d_pad + tile.start;
+  for (int w = wave_id() * kTkU; w < min(nw, wave_id() * kTkU + kTkU); ++w) {
+    const u64 word = sk[w];
+    const int j = w * 64 + lane;
+    if (((word >> lane) & 1ull) && j < tile.count) ek[j] = 0.0f;
+  }
+}
+
+hipError_t launch_topk_materialize(const DevLayout& lay, int K, float* e, const uint64_t* sel,
+                                   hipStream_t s, const LaunchEvents& ev) {
+  const dim3 grid((unsigned)(lay.n_tiles * K));
+  SAEF_LAUNCH(k_tk_zero, grid, dim3(kBlock), 0, s, lay, K, e, sel);
+  return hipGetLastError();
 }
 
 hipError_t launch_topk_aggregate(const DevLayout& lay, const TkDev& tk, int K, int mode,
@@ -1216,7 +1260,7 @@ hipError_t launch_topk_aggregate(const DevLayout& lay, const TkDev& tk, int K, i
   const hipError_t err = hipGetLastError();
   if (err != hipSuccess || mode != 1) return err;
   return Launcher{lay, tk, s}.select_and_emit(1, lay.k_max, e_srv, srv_sel, srv_rank, srv_vals,
-                                              x, ev);
+                                              x, false, ev);
 }
 
 }  // namespace saef

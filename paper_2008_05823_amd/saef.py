@@ -55,9 +55,10 @@ _SIGS = {
     "saef_topk_aggregate": [_P, _i32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P],
     "saef_topk_round": [_P, _i64, _i64, _i32, _f32, _f32, _i32, _P, _P, _P, _P, _P, _P, _P, _P,
                         _P, _P, _P, _P, _P],
-    "saef_topk_round_begin": [_P, _i64, _i64, _i32, _i32, _i32, _P, _P, _P, _P, _P, _P],
-    "saef_topk_round_end": [_P, _i32, _f32, _f32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
-                            _P, _P],
+    "saef_topk_round_begin": [_P, _i64, _i64, _i32, _i32, _i32, _P, _P, _P, _P, _P, _P, _P],
+    "saef_topk_round_end": [_P, _i64, _i64, _i32, _f32, _f32, _i32, _P, _P, _P, _P, _P, _P, _P,
+                            _P, _P, _P, _P, _P],
+    "saef_topk_materialize": [_P, _i32, _P, _P, _P],
     "saef_materialize": [_P, _i32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P],
     "saef_status": [_P, _P],
     "saef_profile_enable": [_P, _i32, ctypes.c_uint32, _i32],
@@ -277,19 +278,30 @@ def saef_topk_round(plan: TopK, t: int, period: int, K: int, lr: float, mu: floa
 
 
 def saef_topk_round_begin(plan: TopK, t: int, period: int, K: int, mode: int, variant: int, e,
-                          e_srv, x, xh, mismatch=None, stream=None):
+                          sel, e_srv, x, xh, mismatch=None, stream=None):
+    """First half of iteration t; sel: the selection words of the previous
+    iteration (None only at t = 0)."""
     _check("saef_topk_round_begin",
-           _lib.saef_topk_round_begin(plan.handle, t, period, K, mode, variant, _f(e), _f(e_srv),
-                                      _f(x), _f(xh), _dev(mismatch, torch.float64),
+           _lib.saef_topk_round_begin(plan.handle, t, period, K, mode, variant, _f(e), _w(sel),
+                                      _f(e_srv), _f(x), _f(xh), _dev(mismatch, torch.float64),
                                       _stream(stream)))
 
 
-def saef_topk_round_end(plan: TopK, K: int, lr: float, mu: float, mode: int, g, m, e, e_srv, x,
-                        sel, rank, vals, srv_sel=None, srv_rank=None, srv_vals=None, stream=None):
+def saef_topk_round_end(plan: TopK, t: int, period: int, K: int, lr: float, mu: float, mode: int,
+                        g, m, e, e_srv, x, sel, rank, vals, srv_sel=None, srv_rank=None,
+                        srv_vals=None, stream=None):
+    """Second half of iteration t (the same t and period as the first)."""
     _check("saef_topk_round_end",
-           _lib.saef_topk_round_end(plan.handle, K, lr, mu, mode, _f(g), _f(m), _f(e), _f(e_srv),
-                                    _f(x), _w(sel), _u32(rank), _f(vals), _w(srv_sel),
+           _lib.saef_topk_round_end(plan.handle, t, period, K, lr, mu, mode, _f(g), _f(m), _f(e),
+                                    _f(e_srv), _f(x), _w(sel), _u32(rank), _f(vals), _w(srv_sel),
                                     _u32(srv_rank), _f(srv_vals), _stream(stream)))
+
+
+def saef_topk_materialize(plan: TopK, K: int, e, sel, stream=None):
+    """The plain worker errors: e (K, d_pad) with the elements whose bit in
+    sel is set put to 0, in place."""
+    _check("saef_topk_materialize",
+           _lib.saef_topk_materialize(plan.handle, K, _f(e), _w(sel), _stream(stream)))
 
 
 def saef_round_begin(layout: Layout, t: int, period: int, K: int, mode: int, variant: int, e,

@@ -126,16 +126,23 @@ class TopkGpu:
                           device="cuda") if mismatch else None
         xh = self.xh if variant == self.saef.VARIANT_SAEF else self.xh[0]
         self.saef.saef_topk_round_begin(self.plan, t, w.period, self.K, w.mode, variant, self.e,
-                                        self.e_srv, self.x, xh, mism)
+                                        self.sel, self.e_srv, self.x, xh, mism)
         return None if mism is None else mism.cpu().numpy()
 
-    def end(self, g):
+    def end(self, t, g):
         w = self.w
         self.g.copy_(torch.from_numpy(g) if isinstance(g, np.ndarray) else g)
-        self.saef.saef_topk_round_end(self.plan, self.K, w.lr, 0.0 if self.mu is None else self.mu,
-                                      w.mode, self.g, self.m, self.e, self.e_srv, self.x, self.sel,
-                                      self.rank, self.vals, self.srv_sel, self.srv_rank,
-                                      self.srv_vals)
+        self.saef.saef_topk_round_end(self.plan, t, w.period, self.K, w.lr,
+                                      0.0 if self.mu is None else self.mu, w.mode, self.g, self.m,
+                                      self.e, self.e_srv, self.x, self.sel, self.rank, self.vals,
+                                      self.srv_sel, self.srv_rank, self.srv_vals)
+
+    def plain_e(self):
+        """The plain worker errors (a materialized copy; the state itself
+        stays pending)."""
+        e = self.e.clone()
+        self.saef.saef_topk_materialize(self.plan, self.K, e, self.sel)
+        return e
 
     def status(self):
         return self.saef.saef_status(self.layout)
@@ -157,7 +164,7 @@ def compare_topk(gpu: TopkGpu, orc: TopkOracle, t, what, mode=1):
     assert np.array_equal(got_rank[:, wm], orc.rank[:, wm]), f"{tag} worker rank words"
     H.assert_f32_equal(H.host(gpu.vals), orc.vals, np.ones(orc.vals.shape[-1], bool),
                        f"{tag} worker values")
-    H.assert_f32_equal(H.host(gpu.e), orc.e, m, f"{tag} worker errors")
+    H.assert_f32_equal(H.host(gpu.plain_e()), orc.e, m, f"{tag} worker errors")
     H.assert_f32_equal(H.host(gpu.xh), orc.xh, m, f"{tag} step-ahead weights")
     H.assert_f32_equal(H.host(gpu.x), orc.x, m, f"{tag} weights")
     if orc.m is not None:
@@ -455,7 +462,7 @@ def test_topk_round_halves_parity(name, variant):
         got = gs.begin(t, variant)
         H.assert_mismatch_close(got, want, w, w.K, f"{name} t={t}")
         orc.end(g)
-        gs.end(g)
+        gs.end(t, g)
         compare_topk(gs, orc, t, f"{name} v{variant}", mode=w.mode)
     assert gs.status() == 0
 
@@ -484,7 +491,7 @@ def test_topk_closed_loop_quadratic_ef_vs_saef():
             xh_d = gs.xh if variant == 1 else gs.xh[:1].expand(w.K, d_pad)
             g_dev = (0.5 * (xh_d - xstar_d)) + torch.from_numpy(noise).cuda()
             orc.end(g_host)
-            gs.end(g_dev.contiguous())
+            gs.end(t, g_dev.contiguous())
             compare_topk(gs, orc, t, f"closed loop v{variant}")
         finals.append(orc.x.copy())
     assert not np.array_equal(finals[0], finals[1])
@@ -510,8 +517,9 @@ def test_topk_invalid_and_range():
 
 def test_topk_graph_replay_parity():
     """saef_topk_round captured in HIP graphs (one per kind of iteration:
-    plain averaging or not), replayed with the gradients copied in between
-    replays and checked against the oracle after every replay."""
+    t = 0 with plain errors, pending errors, pending errors with averaging),
+    replayed with the gradients copied in between replays and checked
+    against the oracle after every replay."""
     w = W.get("resnet56").with_(rounds=8, period=4)
     keep = W.topk_keep(w, 5)
     _case(f"topk graph replay resnet56 K={w.K} rounds={w.rounds}")
@@ -520,7 +528,7 @@ def test_topk_graph_replay_parity():
     S = gs.saef
     graphs = {}
     for t in range(w.rounds):
-        kind = (t + 1) % w.period == 0
+        kind = (t > 0, (t + 1) % w.period == 0)
         if kind not in graphs:
             graph = torch.cuda.CUDAGraph()
             with torch.cuda.graph(graph):
@@ -534,4 +542,5 @@ def test_topk_graph_replay_parity():
         torch.cuda.synchronize()
         orc.round(t, grad)
         compare_topk(gs, orc, t, "graph replay", mode=w.mode)
+    assert len(graphs) == 3
     assert gs.status() == 0
