@@ -69,3 +69,11 @@ def test_profile_calls_reject_bad_arguments_on_host(saef):
     ms = (ctypes.c_double * 7)()
     assert lib.saef_profile_enable(None, 4, 1, 1) == saef.EINVAL   # no layout
     assert lib.saef_profile_read(None, counts, ms) == saef.EINVAL
+
+
+def test_topk_calls_reject_null_plans_on_host(saef):
+    lib = saef.raw_library()
+    assert lib.saef_topk_materialize(None, 1, None, None, None) == saef.EINVAL
+    assert lib.saef_topk_round_begin(None, 0, 0, 1, 1, 1, *([None] * 7)) == saef.EINVAL
+    assert lib.saef_topk_round_end(None, 0, 0, 1, ctypes.c_float(0.1), ctypes.c_float(0.0), 1,
+                                   *([None] * 12)) == saef.EINVAL
