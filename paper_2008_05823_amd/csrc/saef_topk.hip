@@ -1037,6 +1037,9 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
 #pragma unroll
           for (int kk = 0; kk < kB; ++kk) {
             const uint32_t g4 = __builtin_amdgcn_readlane(cur.rk4, kk * U);
+            // the U shuffles of the worker go out together (distinct
+            // registers), then their values are added
+            int pv[U];
 #pragma unroll
             for (int i = 0; i < U; ++i) {
               const int q = kk * U + i;
@@ -1047,9 +1050,15 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
               const uint32_t below =
                   __builtin_amdgcn_mbcnt_hi(mhi, __builtin_amdgcn_mbcnt_lo(mlo, 0u));
               const int src = (int)((r4 - g4) + 4u * below);  // < 4 * 64 for a kept element
-              const float v = __int_as_float(
-                  __builtin_amdgcn_ds_bpermute(src, __float_as_int(gv[kk])));
-              acc[i] += (double)sel_by_bit(((u64)mhi << 32) | mlo, v, 0.0f);  // worker order
+              pv[i] = __builtin_amdgcn_ds_bpermute(src, __float_as_int(gv[kk]));
+            }
+#pragma unroll
+            for (int i = 0; i < U; ++i) {
+              const int q = kk * U + i;
+              const uint32_t mlo = __builtin_amdgcn_readlane(cur.lo, q);
+              const uint32_t mhi = __builtin_amdgcn_readlane(cur.hi, q);
+              acc[i] += (double)sel_by_bit(((u64)mhi << 32) | mlo, __int_as_float(pv[i]),
+                                           0.0f);  // worker order
             }
           }
           done = true;
