@@ -216,10 +216,11 @@ int saef_materialize(const saef_layout* layout, int32_t K, int32_t mode, const f
  *                    words before this one;
  *   vals[total]      the kept values of tensor l, in index order, at
  *                    voff_l = keep[0] + ... + keep[l-1]; total = sum keep.
- * The Top-K state is always plain (no pending corrections): e = Delta -
- * C(Delta) is Delta with the kept elements set to 0, and x is updated in
- * place.  The tie rule, encoding and plain state are the library's own
- * choices; the paper gives none. */
+ * After saef_topk_compress and saef_topk_aggregate the state is plain: e =
+ * Delta - C(Delta) is Delta with the kept elements set to 0, and x is
+ * updated in place; the fused iteration (saef_topk_round, _round_end) leaves
+ * the kept worker errors pending instead (below).  The tie rule, encoding and
+ * state are the library's own choices; the paper gives none. */
 typedef struct saef_topk saef_topk;
 
 /* Top-K plan on a layout: keep[L] (host, 1 <= keep[l] <= n[l]) is copied;
