@@ -32,7 +32,6 @@
 namespace saef {
 namespace {
 
-constexpr uint32_t kAbsLimitBits = 0x49000000u;  // bit pattern of 2^19
 // Words per wave per pass in the per-(tile, worker) kernels: 8, so that the
 // four waves cover a 2048-element tile in one pass (momentum compression
 // 727 -> 677 us at resnet50 K = 8 against 4 words; the sign kernels gain 1%).
@@ -44,6 +43,13 @@ constexpr int kUA = 4;
 // The compression correction C(v)_i = bit ? scale : -scale.
 __device__ __forceinline__ float corr(u64 word, float s) { return sel_by_bit(word, s, -s); }
 
+// The same with +-scale already held in vector registers (in_vgpr).
+struct Corr {
+  float pos, neg;
+  __device__ __forceinline__ explicit Corr(float s) : pos(in_vgpr(s)), neg(in_vgpr(-s)) {}
+  __device__ __forceinline__ float operator()(u64 word) const { return sel_by_bit(word, pos, neg); }
+};
+
 // The 32-bit half of the sign word at p that holds bit `lane`, read per lane
 // (a vector register instead of a scalar pair, for kernels that keep many
 // words live), and the lane's bit in it.
@@ -52,41 +58,6 @@ __device__ __forceinline__ uint32_t half_word(const uint64_t* p, int lane) {
 }
 __device__ __forceinline__ bool half_bit(uint32_t h, int lane) {
   return ((h >> (lane & 31)) & 1u) != 0;
-}
-
-// Adds floor(|v| * 2^80) to the 128-bit integer (hi, lo); `a` is the bit
-// pattern of |v| and must be below that of 2^19.
-__device__ __forceinline__ void add_fixed(uint32_t a, u64& lo, u64& hi) {
-  uint32_t ex = a >> 23;
-  uint32_t m = a & 0x7FFFFFu;
-  m |= (ex != 0) ? 0x800000u : 0u;
-  ex = (ex != 0) ? ex : 1u;  // subnormal: m * 2^-149
-  // |v| = m * 2^(ex - 150), so |v| * 2^80 = m * 2^(ex - 70), ex - 70 in [-69, 75]
-  const int sh = (int)ex - 70;
-  // split as t * 2^(32 q) with t = m * 2^(sh mod 32) < 2^55, q in {0, 1, 2}
-  u64 t;
-  int q;
-  if (sh >= 0) {
-    q = sh >> 5;
-    t = (u64)m << (sh & 31);
-  } else {
-    q = 0;
-    t = (sh > -32) ? (u64)(m >> (-sh)) : 0ull;
-  }
-  const u64 vlo = (q == 0) ? t : ((q == 1) ? (t << 32) : 0ull);
-  const u64 vhi = (q == 0) ? 0ull : ((q == 1) ? (t >> 32) : t);
-  lo += vlo;
-  hi += vhi + (lo < vlo ? 1ull : 0ull);
-}
-
-// Exact-sum term of one value: adds it when |v| < 2^19, else flags it.
-__device__ __forceinline__ void sum_abs(float v, u64& lo, u64& hi, bool& bad) {
-  const uint32_t a = __float_as_uint(v) & 0x7FFFFFFFu;
-  if (a < kAbsLimitBits) {
-    add_fixed(a, lo, hi);
-  } else {
-    bad = true;  // |v| >= 2^19, Inf or NaN
-  }
 }
 
 __device__ __forceinline__ void add128(u64& lo, u64& hi, u64 olo, u64 ohi) {
@@ -153,50 +124,45 @@ __device__ void block_partial(const DevLayout& lay, int row, int64_t tile, u64 l
 }
 
 // ------------------------------------------------------------------ compress
-// kU words of one worker's tile starting at word w0: with kMom, the momentum
-// buffer m <- fma(mu, m, g) first (one rounding); Delta = fma(lr, m or g, e)
-// (e decoded when kDecode), sign words by ballot, exact-sum terms, Delta
-// stored.  kFull: all kU words are whole words of the tile (no guards).
+// kU words of one worker's tile starting at word w0 (element offsets
+// relative to the tile; the buffer resources cover the tile's elements and
+// sign words, so out-of-range loads read 0 and stores are dropped): with
+// kMom, the momentum buffer m <- fma(mu, m, g) first (one rounding); Delta =
+// fma(lr, m or g, e) (e decoded when kDecode), sign words by ballot,
+// exact-sum terms, Delta stored.  kFull: all kU words are whole words of the
+// tile (no lane masks).
 template <bool kDecode, bool kMom, bool kFull>
-__device__ __forceinline__ void compress_words(int w0, int nw, int count, float lr, float mu,
-                                               const float* __restrict__ gk,
-                                               float* __restrict__ mk,
-                                               float* __restrict__ ek,
-                                               uint64_t* __restrict__ sk, float s_old, u64& lo,
-                                               u64& hi, bool& bad) {
+__device__ __forceinline__ void compress_words(int w0, int count, float lr, float mu, Buf rg,
+                                               Buf rm, Buf re, Buf rs, const Corr& c_old,
+                                               ExactSum& acc) {
   const int lane = lane_id();
+  const uint32_t off0 = (uint32_t)(w0 * 64 + lane) * 4u;
   float gv[kU], ev[kU], mv[kU];
-  u64 ow[kU];
+  const u64 ow = kDecode ? buf_ld_words(rs, w0, kU) : 0ull;  // the old words
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
-    const int j = (w0 + u) * 64 + lane;
-    const bool ok = kFull || ((w0 + u < nw) && j < count);
-    gv[u] = ok ? ld_nt(gk + j) : 0.0f;
-    ev[u] = ok ? ld_nt(ek + j) : 0.0f;
-    mv[u] = (kMom && ok) ? ld_nt(mk + j) : 0.0f;
-    ow[u] = (kDecode && (kFull || w0 + u < nw)) ? sk[w0 + u] : 0ull;
+    gv[u] = buf_ld(rg, off0 + 256u * u);
+    ev[u] = buf_ld(re, off0 + 256u * u);
+    mv[u] = kMom ? buf_ld(rm, off0 + 256u * u) : 0.0f;
   }
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
-    const int w = w0 + u;
-    if (!kFull && w >= nw) continue;
-    const int j = w * 64 + lane;
-    const bool ok = kFull || j < count;
+    const uint32_t off = off0 + 256u * u;
+    const bool ok = kFull || (w0 + u) * 64 + lane < count;
     float ev2 = ev[u];
-    if (kDecode) ev2 = ev2 - corr(ow[u], s_old);
+    if (kDecode) ev2 = ev2 - c_old(word_of(ow, u));
     float step = gv[u];
     if (kMom) {
       step = __builtin_fmaf(mu, mv[u], gv[u]);  // m^(k)_{t+1} = mu m^(k)_t + grad
-      if (ok) st_nt(mk + j, step);
+      buf_st(rm, off, step);
     }
     // Delta^(k) = e^(k) + lr * m^(k)_{t+1}, one rounding (m = grad when mu = 0)
-    const float p = __builtin_fmaf(lr, step, ev2);
+    float p = __builtin_fmaf(lr, step, ev2);
+    if (!kFull) p = ok ? p : 0.0f;
     const u64 word = __ballot(ok && p >= 0.0f);
-    if (lane == 0) sk[w] = word;
-    if (ok) {
-      sum_abs(p, lo, hi, bad);
-      st_nt(ek + j, p);
-    }
+    if (lane == 0) buf_st_word(rs, (uint32_t)(w0 + u) * 8u, word);
+    acc.add(p);
+    buf_st(re, off, p);
   }
 }
 
@@ -216,24 +182,27 @@ __global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float
   const Tile tile = lay.tiles[ti];
   const int wave = wave_id();
   const int64_t row = (int64_t)k * lay.d_pad + tile.start;
-  const float* gk = g + row;
-  float* mk = kMom ? m + row : nullptr;
-  float* ek = e + row;
-  uint64_t* sk = signs + (int64_t)k * (lay.d_pad >> 6) + (tile.start >> 6);
-  const float s_old = kDecode ? scales[(int64_t)k * lay.L + tile.l] : 0.0f;
+  const uint32_t nbytes = (uint32_t)tile.count * 4u;
   const int nw = (tile.count + 63) >> 6;
+  const Buf rg = buf_of(g + row, nbytes);
+  const Buf rm = buf_of(kMom ? m + row : g + row, nbytes);
+  const Buf re = buf_of(e + row, nbytes);
+  const Buf rs = buf_of(signs + (int64_t)k * (lay.d_pad >> 6) + (tile.start >> 6),
+                        (uint32_t)nw * 8u);
+  const Corr c_old(kDecode ? scales[(int64_t)k * lay.L + tile.l] : 0.0f);
 
+  ExactSum acc;
   u64 lo = 0, hi = 0;
   bool bad = false;
   for (int w0 = wave * kU; w0 < nw; w0 += kWaves * kU) {
     if ((w0 + kU) * 64 <= tile.count) {
-      compress_words<kDecode, kMom, true>(w0, nw, tile.count, lr, mu, gk, mk, ek, sk, s_old,
-                                          lo, hi, bad);
+      compress_words<kDecode, kMom, true>(w0, tile.count, lr, mu, rg, rm, re, rs, c_old, acc);
     } else {
-      compress_words<kDecode, kMom, false>(w0, nw, tile.count, lr, mu, gk, mk, ek, sk, s_old,
-                                           lo, hi, bad);
+      compress_words<kDecode, kMom, false>(w0, tile.count, lr, mu, rg, rm, re, rs, c_old, acc);
     }
+    acc.added(kU, lo, hi, bad);
   }
+  acc.finish(lo, hi, bad);
   block_partial(lay, k, ti, lo, hi, bad);
 }
 
@@ -300,38 +269,35 @@ __global__ __launch_bounds__(kBlock) void k_finalize2(DevLayout lay, int server,
 }
 
 // ------------------------------------------------------------------ step ahead
-// kU words of one worker's tile starting at word w0: x^(k)_{t+1/2} = x_t -
-// e^(k)_t with the pending corrections of x and e applied on the fly
-// (kHasE false: x_t itself, the evaluation point of local error feedback).
-// kFull: all kU words are whole words of the tile (no guards).
-template <bool kDecX, int kDecE, bool kHasE, bool kFull>
-__device__ __forceinline__ void step_words(int w0, int nw, int count,
-                                           const float* __restrict__ xt,
-                                           const float* __restrict__ ek, float* __restrict__ hk,
+// kU words of one worker's tile starting at word w0 (offsets relative to the
+// tile; buffer resources over the tile's elements and sign words, so the
+// ragged tail needs no guards): x^(k)_{t+1/2} = x_t - e^(k)_t with the
+// pending corrections of x and e applied on the fly (kHasE false: x_t
+// itself, the evaluation point of local error feedback).
+template <bool kDecX, int kDecE, bool kHasE>
+__device__ __forceinline__ void step_words(int w0, int nw, Buf rx, Buf re, Buf rh,
                                            const uint64_t* __restrict__ sx,
-                                           const uint64_t* __restrict__ sk, float s_x,
-                                           float s_e) {
-  const int lane = lane_id();
+                                           const uint64_t* __restrict__ se, const Corr& c_x,
+                                           const Corr& c_e) {
+  const uint32_t off0 = (uint32_t)(w0 * 64 + lane_id()) * 4u;
   float xv[kU], ev[kU];
   u64 mx[kU], me[kU];
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
-    const int j = (w0 + u) * 64 + lane;
-    const bool ok = kFull || ((w0 + u < nw) && j < count);
-    xv[u] = ok ? (kHasE ? xt[j] : ld_nt(xt + j)) : 0.0f;
-    ev[u] = (kHasE && ok) ? ld_nt(ek + j) : 0.0f;
-    mx[u] = (kDecX && (kFull || w0 + u < nw)) ? sx[w0 + u] : 0ull;
-    me[u] = (kDecE != kDecPlain && (kFull || w0 + u < nw)) ? sk[w0 + u] : 0ull;
+    const uint32_t off = off0 + 256u * u;
+    const bool wok = w0 + u < nw;  // wave-uniform: the tile's words only
+    xv[u] = kHasE ? buf_ld_cached(rx, off) : buf_ld(rx, off);
+    ev[u] = kHasE ? buf_ld(re, off) : 0.0f;
+    mx[u] = (kDecX && wok) ? ld_word_ro(sx + w0 + u) : 0ull;
+    me[u] = (kDecE != kDecPlain && wok) ? ld_word_ro(se + w0 + u) : 0ull;
   }
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
-    const int j = (w0 + u) * 64 + lane;
-    if (!kFull && w0 + u >= nw) continue;
     float xc = xv[u], ec = ev[u];
-    if (kDecX) xc = xc - corr(mx[u], s_x);  // x_t = x_{t-1} - C(Delta_t)
-    if (kDecE == kDecSign) ec = ec - corr(me[u], s_e);  // e_t = Delta - C(Delta)
+    if (kDecX) xc = xc - c_x(mx[u]);  // x_t = x_{t-1} - C(Delta_t)
+    if (kDecE == kDecSign) ec = ec - c_e(me[u]);  // e_t = Delta - C(Delta)
     if (kDecE == kDecZero) ec = sel_by_bit(me[u], 0.0f, ec);  // kept elements: 0
-    if (kFull || j < count) st_nt(hk + j, kHasE ? xc - ec : xc);  // x^(k)_{t+1/2} = x_t - e^(k)_t
+    buf_st(rh, off0 + 256u * u, kHasE ? xc - ec : xc);  // x^(k)_{t+1/2} = x_t - e^(k)_t
   }
 }
 
@@ -357,72 +323,68 @@ __global__ __launch_bounds__(kBlock) void k_step(DevLayout lay, int K, const flo
   const int wave = wave_id();
   const int64_t d_pad = lay.d_pad;
   const int64_t gw0 = tile.start >> 6;
-  const float* ek = kHasE ? e + (int64_t)k * d_pad + tile.start : nullptr;
-  float* hk = xh + (int64_t)k * d_pad + tile.start;
-  const float* xt = x + tile.start;
-  const uint64_t* sk = signs + (int64_t)k * (d_pad >> 6) + gw0;
-  const uint64_t* sx = ss + gw0;
-  const float s_e = kDecE == kDecSign ? scales[(int64_t)k * lay.L + tile.l] : 0.0f;
-  const float s_x = kDecX ? sscales[tile.l] : 0.0f;
   const int nw = (tile.count + 63) >> 6;
-  for (int w0 = wave * kU; w0 < nw; w0 += kWaves * kU) {
-    if ((w0 + kU) * 64 <= tile.count) {
-      step_words<kDecX, kDecE, kHasE, true>(w0, nw, tile.count, xt, ek, hk, sx, sk, s_x, s_e);
-    } else {
-      step_words<kDecX, kDecE, kHasE, false>(w0, nw, tile.count, xt, ek, hk, sx, sk, s_x, s_e);
-    }
-  }
+  const uint32_t nbytes = (uint32_t)tile.count * 4u;
+  const Buf rx = buf_of(x + tile.start, nbytes);
+  const Buf re = buf_of(kHasE ? e + (int64_t)k * d_pad + tile.start : x + tile.start, nbytes);
+  const Buf rh = buf_of(xh + (int64_t)k * d_pad + tile.start, nbytes);
+  const uint64_t* sx = kDecX ? ss + gw0 : nullptr;
+  const uint64_t* se = kDecE != kDecPlain ? signs + (int64_t)k * (d_pad >> 6) + gw0 : nullptr;
+  const Corr c_e(kDecE == kDecSign ? scales[(int64_t)k * lay.L + tile.l] : 0.0f);
+  const Corr c_x(kDecX ? sscales[tile.l] : 0.0f);
+  for (int w0 = wave * kU; w0 < nw; w0 += kWaves * kU)
+    step_words<kDecX, kDecE, kHasE>(w0, nw, rx, re, rh, sx, se, c_x, c_e);
 }
 
 // ------------------------------------------------------------------ step ahead with averaging
 constexpr int kAvgChunk = 4;  // workers whose loads are issued together
 
-// kN words of one tile starting at word w0, all K workers: the local errors
-// are read in worker order (pending corrections applied when kDecE) and
-// replaced by their mean (binary64 sum in worker order, /K, fp32); then
-// x^(k)_{t+1/2} = x_t - mean for every worker when kXh.  kFull: the kN
-// words are whole words of the tile; otherwise kN is 1 and the lane's
-// element exists iff `valid`.
-template <bool kDecX, int kDecE, bool kXh, bool kFull, int kN>
-__device__ __forceinline__ void average_words(const DevLayout& lay, int K, double inv_k, int l,
-                                              int w0, bool valid, int64_t start,
-                                              const float* __restrict__ x,
-                                              const uint64_t* __restrict__ ss, float s_x,
+// kUA words of one tile starting at word w0 (offsets relative to the tile;
+// lanes past the tile's end compute on zeros and their stores are dropped by
+// the buffer range check), all K workers: the local errors are read in
+// worker order (pending corrections applied when kDecE) and replaced by their
+// mean (binary64 sum in worker order, /K, fp32); then x^(k)_{t+1/2} = x_t -
+// mean for every worker when kXh.
+template <bool kDecX, int kDecE, bool kXh>
+__device__ __forceinline__ void average_words(int K, double inv_k, int L, int l, int64_t d_pad,
+                                              int w0, int64_t start, uint32_t nbytes,
+                                              uint32_t wbytes, Buf rx, Buf rsx, float s_x,
                                               float* __restrict__ e,
                                               const uint64_t* __restrict__ signs,
                                               const float* __restrict__ scales,
                                               float* __restrict__ xh) {
   const int lane = lane_id();
-  const int64_t d_pad = lay.d_pad;
   const int64_t W = d_pad >> 6;
-  const int64_t gw0 = (start >> 6) + w0;
-  const int64_t base = start + w0 * 64 + lane;
-  const bool ok = kFull || valid;
-  double acc[kN];
+  const int64_t gw0 = start >> 6;
+  const uint32_t off0 = (uint32_t)(w0 * 64 + lane) * 4u;
+  // a lane reads the 32-bit half of a sign word that holds its bit (vector
+  // registers: this kernel keeps kAvgChunk * kUA words live)
+  const uint32_t hoff0 = (uint32_t)w0 * 8u + (uint32_t)(lane >> 5) * 4u;
+  double acc[kUA];
 #pragma unroll
-  for (int u = 0; u < kN; ++u) acc[u] = 0.0;
+  for (int u = 0; u < kUA; ++u) acc[u] = 0.0;
   for (int k0 = 0; k0 < K; k0 += kAvgChunk) {
-    // sign words are fetched per lane as the 32-bit half holding the lane's
-    // bit (vector registers: this kernel keeps kAvgChunk * kN words live)
-    float ev[kAvgChunk][kN];
-    uint32_t hw[kAvgChunk][kN];
+    float ev[kAvgChunk][kUA];
+    uint32_t hw[kAvgChunk][kUA];
 #pragma unroll
     for (int c = 0; c < kAvgChunk; ++c) {
-      const bool kin = k0 + c < K;
-      const float* ek = e + (int64_t)(k0 + c) * d_pad + base;
-      const uint64_t* sk = signs + (int64_t)(k0 + c) * W + gw0;
+      const int k = min(k0 + c, K - 1);
+      const Buf re = buf_of(e + (int64_t)k * d_pad + start, nbytes);
+      const Buf rs = buf_of(signs + (int64_t)k * W + gw0, kDecE != kDecPlain ? wbytes : 0u);
 #pragma unroll
-      for (int u = 0; u < kN; ++u) {
-        ev[c][u] = (kin && ok) ? ld_nt(ek + u * 64) : 0.0f;
-        hw[c][u] = (kDecE != kDecPlain && kin) ? half_word(sk + u, lane) : 0u;
+      for (int u = 0; u < kUA; ++u) {
+        ev[c][u] = buf_ld(re, off0 + 256u * u);
+        hw[c][u] = kDecE != kDecPlain
+                       ? __builtin_amdgcn_raw_buffer_load_b32(rs, hoff0 + 8u * u, 0, 0)
+                       : 0u;
       }
     }
 #pragma unroll
     for (int c = 0; c < kAvgChunk; ++c) {
       if (k0 + c >= K) continue;
-      const float s = kDecE == kDecSign ? scales[(int64_t)(k0 + c) * lay.L + l] : 0.0f;
+      const float s = kDecE == kDecSign ? scales[(int64_t)(k0 + c) * L + l] : 0.0f;
 #pragma unroll
-      for (int u = 0; u < kN; ++u) {
+      for (int u = 0; u < kUA; ++u) {
         float v = ev[c][u];
         if (kDecE == kDecSign) v = v - (half_bit(hw[c][u], lane) ? s : -s);
         if (kDecE == kDecZero) v = half_bit(hw[c][u], lane) ? 0.0f : v;
@@ -430,25 +392,25 @@ __device__ __forceinline__ void average_words(const DevLayout& lay, int K, doubl
       }
     }
   }
-  float mean[kN], xv[kN];
+  float mean[kUA], xv[kUA];
 #pragma unroll
-  for (int u = 0; u < kN; ++u) {
+  for (int u = 0; u < kUA; ++u) {
     mean[u] = (float)mean_of(acc[u], inv_k, K);
     xv[u] = 0.0f;
     if (kXh) {
-      const uint32_t hx = kDecX ? half_word(ss + gw0 + u, lane) : 0u;
-      if (ok) xv[u] = x[base + u * 64];
+      const uint32_t hx =
+          kDecX ? __builtin_amdgcn_raw_buffer_load_b32(rsx, hoff0 + 8u * u, 0, 0) : 0u;
+      xv[u] = buf_ld_cached(rx, off0 + 256u * u);
       if (kDecX) xv[u] = xv[u] - (half_bit(hx, lane) ? s_x : -s_x);
     }
   }
-  if (!ok) return;
   for (int k = 0; k < K; ++k) {
-    float* ek = e + (int64_t)k * d_pad + base;
-    float* hk = xh + (int64_t)k * d_pad + base;
+    const Buf re = buf_of(e + (int64_t)k * d_pad + start, nbytes);
+    const Buf rh = buf_of(kXh ? xh + (int64_t)k * d_pad + start : e, kXh ? nbytes : 0u);
 #pragma unroll
-    for (int u = 0; u < kN; ++u) {
-      st_nt(ek + u * 64, mean[u]);
-      if (kXh) st_nt(hk + u * 64, xv[u] - mean[u]);
+    for (int u = 0; u < kUA; ++u) {
+      buf_st(re, off0 + 256u * u, mean[u]);
+      if (kXh) buf_st(rh, off0 + 256u * u, xv[u] - mean[u]);
     }
   }
 }
@@ -472,64 +434,57 @@ __global__ __launch_bounds__(kBlock) void k_step_average(DevLayout lay, int K, d
   const Tile tile = lay.tiles[ti];
   const int wave = wave_id();
   const int nw = (tile.count + 63) >> 6;
+  const uint32_t nbytes = (uint32_t)tile.count * 4u;
+  const uint32_t wbytes = (uint32_t)nw * 8u;
+  const Buf rx = buf_of(kXh ? x + tile.start : e, kXh ? nbytes : 0u);
+  const Buf rsx = buf_of(kDecX ? (const void*)(ss + (tile.start >> 6)) : e, kDecX ? wbytes : 0u);
   const float s_x = kDecX ? sscales[tile.l] : 0.0f;
-  for (int w0 = wave * kUA; w0 < nw; w0 += kWaves * kUA) {
-    if ((w0 + kUA) * 64 <= tile.count) {
-      average_words<kDecX, kDecE, kXh, true, kUA>(lay, K, inv_k, tile.l, w0, true, tile.start, x,
-                                                 ss, s_x, e, signs, scales, xh);
-    } else {
-      // tail of the tile: one word at a time, guarded per lane
-      for (int w = w0; w < min(w0 + kUA, nw); ++w) {
-        average_words<kDecX, kDecE, kXh, false, 1>(lay, K, inv_k, tile.l, w,
-                                                   w * 64 + lane_id() < tile.count, tile.start, x,
-                                                   ss, s_x, e, signs, scales, xh);
-      }
-    }
-  }
+  for (int w0 = wave * kUA; w0 < nw; w0 += kWaves * kUA)
+    average_words<kDecX, kDecE, kXh>(K, inv_k, lay.L, tile.l, lay.d_pad, w0, tile.start, nbytes,
+                                     wbytes, rx, rsx, s_x, e, signs, scales, xh);
 }
 
 // ------------------------------------------------------------------ aggregate
-constexpr int kAggChunk = 4;  // workers whose sign words are loaded together
-// One pass of a wave over kN words of a tile: the K worker messages are
-// decoded in order, mean = (sum_k +-scale_k in binary64, k order) / K.
-// kFull: all kN words lie inside the tile; otherwise element base + 64 u
-// exists iff 64 u < lim (kN is then 1).
-template <int kMode, bool kDecode, bool kAvg, bool kFull, int kN>
-__device__ __forceinline__ void aggregate_pass(const DevLayout& lay, int K, double inv_k, int l,
-                                               int64_t base, int64_t gw, int lim,
-                                               const uint64_t* __restrict__ signs,
-                                               const float* __restrict__ scales,
-                                               float* __restrict__ avg, float* __restrict__ es,
-                                               uint64_t* __restrict__ ss, float s_old,
-                                               float* __restrict__ x, u64& lo, u64& hi,
-                                               bool& bad) {
+constexpr int kAggChunk = 2;  // workers whose sign words are loaded together
+// One pass of a wave over the kU words starting at word w0 of a tile (offsets
+// relative to the tile; buffer resources over the tile's elements and server
+// words): the K worker messages are decoded in order, mean = (sum_k +-scale_k
+// in binary64, k order) / K.  Worker words come from sw (the tile's first
+// word of worker 0; worker k at sw + k W).  kFull: all kU words lie inside
+// the tile (no lane masks).
+template <int kMode, bool kDecode, bool kAvg, bool kFull>
+__device__ __forceinline__ void aggregate_pass(int K, double inv_k, int L, int l, int64_t W,
+                                               int w0, int count,
+                                               const uint64_t* __restrict__ sw,
+                                               const float* __restrict__ scales, Buf ravg,
+                                               Buf res, Buf rss, const Corr& c_old, Buf rx,
+                                               ExactSum& acc) {
   const int lane = lane_id();
-  const int64_t W = lay.d_pad >> 6;
+  const uint32_t off0 = (uint32_t)(w0 * 64 + lane) * 4u;
   constexpr bool kUpdX = kMode == 0 || kDecode;  // x is read and written
-  float ev[kN], xv[kN];
-  u64 mo[kN];
+  float ev[kU], xv[kU];
+  const u64 mo = (kMode == 1 && kDecode) ? buf_ld_words(rss, w0, kU) : 0ull;  // old words
 #pragma unroll
-  for (int u = 0; u < kN; ++u) {
-    const bool ok = kFull || u * 64 < lim;
-    ev[u] = (kMode == 1 && ok) ? ld_nt(es + base + u * 64) : 0.0f;
-    xv[u] = (kUpdX && ok) ? ld_nt(x + base + u * 64) : 0.0f;
-    mo[u] = (kMode == 1 && kDecode) ? ss[gw + u] : 0ull;
+  for (int u = 0; u < kU; ++u) {
+    ev[u] = kMode == 1 ? buf_ld(res, off0 + 256u * u) : 0.0f;
+    xv[u] = kUpdX ? buf_ld(rx, off0 + 256u * u) : 0.0f;
   }
-  double acc[kN];
+  double acc_m[kU];
 #pragma unroll
-  for (int u = 0; u < kN; ++u) acc[u] = 0.0;
+  for (int u = 0; u < kU; ++u) acc_m[u] = 0.0;
   // workers in chunks of kAggChunk: the chunk's scales and sign words are all
-  // loaded (a worker past K reloads worker K - 1) before the first is used
+  // loaded (a worker past K reloads worker K - 1) before the first is used;
+  // the tail pass reads only the tile's words (wave-uniform conditions)
   for (int k0 = 0; k0 < K; k0 += kAggChunk) {
     float sc[kAggChunk];
-    u64 m[kAggChunk][kN];
+    u64 m[kAggChunk][kU];
 #pragma unroll
     for (int c = 0; c < kAggChunk; ++c) {
       const int k = min(k0 + c, K - 1);
-      sc[c] = scales[(int64_t)k * lay.L + l];
-      const uint64_t* sk = signs + (int64_t)k * W + gw;
+      sc[c] = scales[(int64_t)k * L + l];
+      const uint64_t* sk = sw + (int64_t)k * W + w0;
 #pragma unroll
-      for (int u = 0; u < kN; ++u) m[c][u] = sk[u];
+      for (int u = 0; u < kU; ++u) m[c][u] = (kFull || (w0 + u) * 64 < count) ? sk[u] : 0ull;
     }
 #pragma unroll
     for (int c = 0; c < kAggChunk; ++c) {
@@ -540,33 +495,32 @@ __device__ __forceinline__ void aggregate_pass(const DevLayout& lay, int K, doub
       const uint32_t lo_bits = (uint32_t)__double2loint(sd);
       const uint32_t neg_hi = pos_hi ^ 0x80000000u;
 #pragma unroll
-      for (int u = 0; u < kN; ++u)
-        acc[u] += __hiloint2double((int)sel_by_bit(m[c][u], pos_hi, neg_hi), (int)lo_bits);
+      for (int u = 0; u < kU; ++u)
+        acc_m[u] += __hiloint2double((int)sel_by_bit(m[c][u], pos_hi, neg_hi), (int)lo_bits);
     }
   }
 #pragma unroll
-  for (int u = 0; u < kN; ++u) {
-    const bool ok = kFull || u * 64 < lim;
-    const float mean = (float)mean_of(acc[u], inv_k, K);
-    const int64_t i = base + u * 64;
-    if (kAvg && ok) avg[i] = mean;
+  for (int u = 0; u < kU; ++u) {
+    const uint32_t off = off0 + 256u * u;
+    const bool ok = kFull || (w0 + u) * 64 + lane < count;
+    const float mean = (float)mean_of(acc_m[u], inv_k, K);
+    if (kAvg) buf_st(ravg, off, mean);
     if (kMode == 1) {
       float evc = ev[u];
       if (kDecode) {
-        const float c = corr(mo[u], s_old);
-        evc = evc - c;                    // e_t = Delta_t - C(Delta_t)
-        if (ok) st_nt(x + i, xv[u] - c);  // re-update x_t = x_{t-1} - C(Delta_t)
+        const float c = c_old(word_of(mo, u));
+        evc = evc - c;                   // e_t = Delta_t - C(Delta_t)
+        buf_st(rx, off, xv[u] - c);      // re-update x_t = x_{t-1} - C(Delta_t)
       }
       // Delta_{t+1} = e_t + (1/K) sum_k C(Delta^(k))
-      const float D = evc + mean;
+      float D = evc + mean;
+      if (!kFull) D = ok ? D : 0.0f;
       const u64 word = __ballot(ok && D >= 0.0f);
-      if (lane == 0) ss[gw + u] = word;
-      if (ok) {
-        sum_abs(D, lo, hi, bad);
-        st_nt(es + i, D);
-      }
-    } else if (ok) {
-      st_nt(x + i, xv[u] - mean);  // single-way: the mean itself comes back
+      if (lane == 0) buf_st_word(rss, (uint32_t)(w0 + u) * 8u, word);
+      acc.add(D);
+      buf_st(res, off, D);
+    } else {
+      buf_st(rx, off, xv[u] - mean);  // single-way: the mean itself comes back
     }
   }
 }
@@ -585,27 +539,34 @@ __global__ __launch_bounds__(kBlock) void k_aggregate(DevLayout lay, int K, doub
                                                       float* __restrict__ x) {
   const int64_t ti = blockIdx.x;
   const Tile tile = lay.tiles[ti];
-  const int lane = lane_id();
   const int nw = (tile.count + 63) >> 6;
-  const float s_old = (kMode == 1 && kDecode) ? sscales[tile.l] : 0.0f;
+  const uint32_t nbytes = (uint32_t)tile.count * 4u;
+  const int64_t gw0 = tile.start >> 6;
+  const Buf ravg = buf_of(kAvg ? avg + tile.start : x + tile.start, nbytes);
+  const Buf res = buf_of(kMode == 1 ? es + tile.start : x + tile.start, nbytes);
+  const Buf rss = buf_of(kMode == 1 ? ss + gw0 : signs, (uint32_t)nw * 8u);
+  const Buf rx = buf_of(x + tile.start, nbytes);
+  const Corr c_old((kMode == 1 && kDecode) ? sscales[tile.l] : 0.0f);
+  const int64_t W = lay.d_pad >> 6;
+  ExactSum acc;
   u64 lo = 0, hi = 0;
   bool bad = false;
   for (int w0 = wave_id() * kU; w0 < nw; w0 += kWaves * kU) {
-    const int64_t base = tile.start + w0 * 64 + lane;
-    const int64_t gw = (tile.start >> 6) + w0;
     if ((w0 + kU) * 64 <= tile.count) {
-      aggregate_pass<kMode, kDecode, kAvg, true, kU>(lay, K, inv_k, tile.l, base, gw, 0, signs,
-                                                     scales, avg, es, ss, s_old, x, lo, hi, bad);
+      aggregate_pass<kMode, kDecode, kAvg, true>(K, inv_k, lay.L, tile.l, W, w0, tile.count,
+                                                 signs + gw0, scales, ravg, res, rss, c_old, rx,
+                                                 acc);
     } else {
-      // tail of the tile: one word at a time, guarded per lane
-      for (int u = 0; u < min(kU, nw - w0); ++u) {
-        aggregate_pass<kMode, kDecode, kAvg, false, 1>(
-            lay, K, inv_k, tile.l, base + u * 64, gw + u, tile.count - (w0 + u) * 64 - lane,
-            signs, scales, avg, es, ss, s_old, x, lo, hi, bad);
-      }
+      aggregate_pass<kMode, kDecode, kAvg, false>(K, inv_k, lay.L, tile.l, W, w0, tile.count,
+                                                  signs + gw0, scales, ravg, res, rss, c_old, rx,
+                                                  acc);
     }
+    if (kMode == 1) acc.added(kU, lo, hi, bad);
   }
-  if (kMode == 1) block_partial(lay, lay.k_max, ti, lo, hi, bad);
+  if (kMode == 1) {
+    acc.finish(lo, hi, bad);
+    block_partial(lay, lay.k_max, ti, lo, hi, bad);
+  }
 }
 
 // ------------------------------------------------------------------ materialize
