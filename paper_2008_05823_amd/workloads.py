@@ -255,11 +255,25 @@ def gradient(w: Workload, t: int, k: int, scales_elem: np.ndarray | None = None)
     return g
 
 
-def gradients(w: Workload, t: int, K: int | None = None) -> np.ndarray:
-    """All K workers' gradients of round t as a (K, d_pad) float32 array."""
+def gradients(w: Workload, t: int, K: int | None = None, threads: int = 1) -> np.ndarray:
+    """All K workers' gradients of round t as a (K, d_pad) float32 array;
+    threads > 1 draws the workers' streams in parallel (same values: every
+    (t, k) has its own stream)."""
     K = w.K if K is None else K
     se = _per_element(w, tensor_scales(w).astype(np.float32))
-    return np.stack([gradient(w, t, k, se) for k in range(K)])
+    out = np.empty((K, se.size), dtype=np.float32)
+
+    def fill(k):
+        out[k] = gradient(w, t, k, se)
+
+    if threads > 1 and K > 1:
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(min(threads, K)) as ex:
+            list(ex.map(fill, range(K)))
+    else:
+        for k in range(K):
+            fill(k)
+    return out
 
 
 def topk_keep(w: Workload, percent: float) -> np.ndarray:

@@ -1,15 +1,20 @@
 """Parity at the full workload sizes, in the launch configuration bench.py
 times (saef_round over the whole tensor list, same tiles and kernels).
 
-The oracle cannot redo a whole ResNet-50 or BERT-base iteration for K workers
-in test time, but it does not need to: every tensor evolves independently of
-the others (one scale per tensor, everything else elementwise), so the oracle
-runs the full iteration sequence on a sample of tensors -- the largest ones
-included -- fed with the same gradient slices, and the GPU state of those
-tensors must match it bit for bit after every iteration.
+The scaled-sign workloads are compared with the oracle in full: every tensor,
+every element, every iteration of the workload (ResNet-50: 161 tensors, 20
+iterations; BERT-base: 199 tensors, K = 16, 10 iterations; one tensor of
+2^28 elements, K = 8, 5 iterations), including the server error, the
+weights and the server message.  The oracle runs piecewise on a thread pool
+(tests.split_oracle; its equality with the whole-layout oracle is a CPU
+test), which brings a ResNet-50 iteration to about a second of host time.
 
-The 2^28-element single tensor is checked against one full oracle iteration
-and, for later iterations, against properties that hold at any size.
+A mid-size multi-tensor layout of more than 2048 tiles covers the long
+XCD tile runs of the step-ahead and averaging kernels with the pending
+corrections, over several iterations that include error averaging.
+
+The Top-K workloads (the paper's second compressor) are checked on a sample
+of tensors (the largest included) and by the defining properties of Top-K.
 
 Gradient recipe at these sizes: iteration t uses the seeded gradient set of
 t mod 2 (two sets, as in bench.py), so the host generates 2 K vectors.
@@ -20,6 +25,7 @@ import torch
 
 from paper_2008_05823_amd import workloads as W
 from tests import gpu_harness as H
+from tests.split_oracle import SplitOracle, default_threads, rows_equal
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -56,131 +62,91 @@ def _device_slices(t, off, n, idx):
     return parts
 
 
-SAMPLES = {
-    # conv1, bn1.bias, layer1.0.conv2, layer3.5.conv3, layer4.0.conv2 (the largest,
-    # 3x3x512x512), layer4.2.bn3.weight, fc.weight (2048x1000), fc.bias
-    "resnet50": ("resnet50", None, ["conv1.weight", "bn1.bias", "layer1.0.conv2.weight",
-                                    "layer3.5.conv3.weight", "layer4.0.conv2.weight",
-                                    "layer4.2.bn3.weight", "fc.weight", "fc.bias"]),
-    # word embedding (largest, 30522x768), token type, a LayerNorm bias, a query
-    # weight, an FFN input bias, the pooler bias; 5 iterations cover the
-    # pending-correction path and the averaging iteration t = 4
-    "bert_base": ("bert_base", 5, ["embeddings.word", "embeddings.token_type",
-                                   "layer0.attn.ln.bias", "layer5.attn.query.weight",
-                                   "layer11.ffn.in.bias", "pooler.bias"]),
-}
+def compare_full(gpu: dict, so: SplitOracle, t: int, tag: str):
+    """Every element, word and scale of the state against the oracle, bit for
+    bit (padding included: neither side ever writes it, both start at 0)."""
+    names = ["signs", "e", "xh", "x"] + (["srv_signs", "e_srv"] if so.w.mode == 1 else [])
+    for name in names:
+        if not rows_equal(gpu[name], getattr(so, name)):
+            so.m = None
+            H.compare_state(gpu, so, t, tag)  # names the first difference
+            raise AssertionError(f"{tag} t={t}: {name} differs from the oracle")
+    if not np.array_equal(gpu["scales"].view(np.uint32), so.scales.view(np.uint32)):
+        so.m = None
+        H.compare_state(gpu, so, t, tag)
+        raise AssertionError(f"{tag} t={t}: worker scales differ")
+    if so.w.mode == 1 and not np.array_equal(gpu["srv_scales"].view(np.uint32),
+                                             so.srv_scales.view(np.uint32)):
+        raise AssertionError(f"{tag} t={t}: server scales differ")
 
 
-@pytest.mark.parametrize("case", list(SAMPLES))
-def test_full_size_sampled_tensors(case):
-    name, rounds, sample_names = SAMPLES[case]
-    w = W.get(name)
-    rounds = rounds or w.rounds
-    names = [t for t, _ in w.tensors]
-    idx = [names.index(s) for s in sample_names]
-    off, n, d_pad = w.layout()
-    sw = _sub_workload(w, idx)
-    s_off, s_n, s_dpad = sw.layout()
-    _log(f"{case}: K={w.K} L={w.L} d={w.d}, {rounds} iterations, oracle on {len(idx)} tensors "
-         f"({int(s_n.sum())} elements)")
-
-    grads = [W.gradients(w, s) for s in range(2)]
-    _log("gradients generated")
-    x0 = W.initial_x(w)
-    orc = H.OracleState(sw, x0=_gather(x0, off, n, idx, s_off, s_dpad))
-    gs = H.GpuState(w, x0=x0)
+def run_full(w: W.Workload, rounds: int, tag: str):
+    """rounds iterations of w through saef_round, each compared in full."""
+    threads = default_threads()
+    _log(f"{tag}: K={w.K} L={w.L} d={w.d} d_pad={w.d_pad}, {rounds} iterations, period "
+         f"{w.period}, oracle on {threads} threads")
+    grads = [W.gradients(w, s, threads=threads) for s in range(min(2, rounds))]
+    _log(f"{tag}: gradients generated")
+    so = SplitOracle(w, threads=threads)
+    gs = H.GpuState(w)
     g_dev = [torch.from_numpy(g).cuda() for g in grads]
-    f32 = dict(dtype=torch.float32, device="cuda")
-    e_out = torch.empty((w.K, d_pad), **f32)
-    es_out = torch.empty(d_pad, **f32)
-    x_out = torch.empty(d_pad, **f32)
     for t in range(rounds):
-        orc.round(t, _gather(grads[t % 2], off, n, idx, s_off, s_dpad))
         gs.round(t, g_dev[t % 2])
-        gs.saef.saef_materialize(gs.layout, w.K, w.mode, gs.e, gs.e_srv, gs.x, gs.signs,
-                                 gs.scales, gs.srv_signs, gs.srv_scales, e_out, es_out, x_out)
-        torch.cuda.synchronize()
-        # pack each state array tensor by tensor into the sample layout
-        def pack(dev_t):
-            parts = _device_slices(dev_t, off, n, idx)
-            out = np.zeros(dev_t.shape[:-1] + (s_dpad,), np.float32)
-            for j, p in enumerate(parts):
-                out[..., s_off[j]:s_off[j] + s_n[j]] = p
-            return out
-        got = {"e": pack(e_out), "e_srv": pack(es_out), "x": pack(x_out), "xh": pack(gs.xh)}
-        signs = H.host(gs.signs, np.uint64)
-        got["signs"] = _gather_words(signs, off, n, idx, s_off, s_dpad // 64)
-        got["srv_signs"] = _gather_words(H.host(gs.srv_signs, np.uint64), off, n, idx, s_off,
-                                         s_dpad // 64)
-        got["scales"] = H.host(gs.scales)[:, idx]
-        got["srv_scales"] = H.host(gs.srv_scales)[idx]
-        H.compare_state(got, orc, t, case)
-        _log(f"{case}: iteration {t} matches the oracle on the sampled tensors")
+        so.round(t, grads[t % 2])
+        compare_full(gs.plain(), so, t, tag)
+        _log(f"{tag}: iteration {t} matches the oracle on every element"
+             + (" (error averaging)" if w.period and (t + 1) % w.period == 0 else ""))
     assert gs.status() == 0
 
 
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["resnet50", "bert_base"])
+def test_full_size_every_tensor(name):
+    """ResNet-50 (K = 8, 20 iterations, averaging at t = 19) and BERT-base
+    (K = 16, 10 iterations, averaging at t = 4 and 9): the whole state after
+    every iteration."""
+    w = W.get(name)
+    run_full(w, w.rounds, name)
+
+
+@pytest.mark.timeout(900)
 def test_full_size_flat256m():
-    """One tensor of 2^28 elements, K = 8: iteration 0 against the full oracle,
-    later iterations against size-independent properties of Eq. (2)."""
+    """One tensor of 2^28 elements, K = 8, 5 iterations (averaging at t = 4):
+    the whole state after every iteration, server error, weights and server
+    message included."""
     w = W.get("flat256m")
-    off, n, d_pad = w.layout()
-    K = w.K
-    _log(f"flat256m: K={K} d={w.d}")
-    grads = [W.gradients(w, s) for s in range(2)]
-    x0 = W.initial_x(w)
-    _log("gradients generated")
-    gs = H.GpuState(w, x0=x0)
-    g_dev = [torch.from_numpy(g).cuda() for g in grads]
-
-    # iteration 0: full oracle, bit for bit
-    orc = H.OracleState(w, x0=x0)
-    orc.round(0, grads[0])
-    _log("oracle iteration 0 done")
-    gs.round(0, g_dev[0])
-    H.compare_state(gs.plain(), orc, 0, "flat256m")
-    _log("iteration 0 matches the oracle")
-    del orc
-
-    lr = np.float64(np.float32(w.lr))
-    rng = np.random.default_rng(5)
-    probe = rng.integers(0, w.d, 1 << 20)
-    for t in range(1, w.rounds):
-        check = t in (1, w.period - 1)  # first pending-correction iteration, averaging iteration
-        prev = gs.plain() if check else None
-        gs.round(t, g_dev[t % 2])
-        if not check:
-            continue
-        cur = gs.plain()
-        g = grads[t % 2]
-        if (t + 1) % w.period == 0:
-            # every worker starts from the binary64 mean of the errors (worker order), in fp32
-            acc = np.zeros(w.d, np.float64)
-            for k in range(K):
-                acc += prev["e"][k]
-            e_avg = (acc / K).astype(np.float32)
-        for k in range(K):
-            e_in = e_avg if (t + 1) % w.period == 0 else prev["e"][k]
-            p = lr * g[k].astype(np.float64) + e_in.astype(np.float64)  # Delta, before rounding
-            # sign words: bit i is [Delta_i >= 0] (rounding to fp32 keeps the sign)
-            bits = np.packbits((p >= 0).astype(np.uint8), bitorder="little").view(np.uint64)
-            assert np.array_equal(bits, cur["signs"][k]), (t, k)
-            # ||C(Delta)||_1 = ||Delta||_1: n * scale is the L1 norm of Delta
-            pf = p.astype(np.float32)
-            l1 = np.abs(pf.astype(np.float64)).sum()
-            assert abs(float(cur["scales"][k, 0]) * w.d - l1) <= 1e-6 * l1, (t, k)
-            # e = Delta - C(Delta), on a probe of elements
-            pp = pf[probe]
-            s = cur["scales"][k, 0]
-            want = (pp - np.where(pp >= 0, s, -s)).astype(np.float32)
-            np.testing.assert_allclose(cur["e"][k][probe], want, rtol=1e-6, atol=1e-7)
-            # step-ahead weights x_t - e_t
-            xe = (prev["x"][probe] - e_in[probe]).astype(np.float32)
-            np.testing.assert_allclose(cur["xh"][k][probe], xe, rtol=1e-6, atol=1e-7)
-            del p, pf, bits
-        _log(f"iteration {t} satisfies the size-independent checks")
-    assert gs.status() == 0
+    run_full(w, w.rounds, "flat256m")
 
 
+def _mid_size_workload():
+    """48 tensors of seeded sizes (1 .. 300000, ragged), more than 2048 tiles."""
+    rng = np.random.default_rng(2048)
+    sizes = np.concatenate([rng.integers(1, 300001, 40), rng.integers(1, 200, 6), [1, 64]])
+    return W.custom(sizes.tolist(), K=8, period=3, rounds=7, dist="laplace_zeros",
+                    scale_range=(1e-5, 1e-2), seed=W.SEED_BASE + 2048, name="mid")
+
+
+@pytest.mark.timeout(600)
+def test_mid_size_long_tile_runs():
+    """A multi-tensor layout past 2048 tiles (the step-ahead and averaging
+    kernels then deal runs of 64 tiles to each XCD) with the pending
+    corrections, 7 iterations with averaging at t = 2 and 5, in full."""
+    from paper_2008_05823_amd import saef
+    w = _mid_size_workload()
+    lay = saef.Layout(*w.layout(), w.K)
+    n_tiles = lay.info()["n_tiles"]
+    lay.close()
+    assert n_tiles >= 2048, n_tiles
+    run_full(w, w.rounds, f"mid ({n_tiles} tiles)")
+
+
+# conv1, bn1.bias, layer1.0.conv2, layer3.5.conv3, layer4.0.conv2 (the largest,
+# 3x3x512x512), layer4.2.bn3.weight, fc.weight (2048x1000), fc.bias
+TOPK_SAMPLE = ["conv1.weight", "bn1.bias", "layer1.0.conv2.weight", "layer3.5.conv3.weight",
+               "layer4.0.conv2.weight", "layer4.2.bn3.weight", "fc.weight", "fc.bias"]
+
+
+@pytest.mark.timeout(600)
 def test_full_size_topk_resnet50():
     """Layer-wise Top-1% at the full ResNet-50 shape, K = 8, in the launch
     configuration bench.py --topk 1 times: saef_topk_round over the whole
@@ -190,7 +156,7 @@ def test_full_size_topk_resnet50():
     from tests.test_gpu_topk import TopkGpu, TopkOracle, _u32
     w = W.get("resnet50").with_(period=2)
     names = [t for t, _ in w.tensors]
-    idx = [names.index(s) for s in SAMPLES["resnet50"][2]]
+    idx = [names.index(s) for s in TOPK_SAMPLE]
     off, n, d_pad = w.layout()
     sw = _sub_workload(w, idx)
     s_off, s_n, s_dpad = sw.layout()
@@ -198,7 +164,7 @@ def test_full_size_topk_resnet50():
     rounds = 4
     _log(f"topk resnet50: K={w.K} L={w.L} d={w.d}, {rounds} iterations, oracle on {len(idx)} "
          f"tensors ({int(s_n.sum())} elements)")
-    grads = [W.gradients(w, s) for s in range(2)]
+    grads = [W.gradients(w, s, threads=default_threads()) for s in range(2)]
     x0 = W.initial_x(w)
     orc = TopkOracle(sw, keep[idx], x0=_gather(x0, off, n, idx, s_off, s_dpad))
     gs = TopkGpu(w, keep, x0=x0)
@@ -261,6 +227,7 @@ def _check_topk_row(delta, sel_words, vals, kept_count, tag):
     return bits
 
 
+@pytest.mark.timeout(600)
 def test_full_size_topk_flat256m():
     """Top-1% of one 2^28-element tensor (131072 tiles: 2048 tile groups in
     32 super-groups), K = 8, iteration 0 of saef_topk_round, checked
@@ -272,7 +239,7 @@ def test_full_size_topk_flat256m():
     keep = W.topk_keep(w, 1)
     k1 = int(keep[0])
     _log(f"topk flat256m: K={K} d={w.d} keep={k1}")
-    g = W.gradients(w, 0)
+    g = W.gradients(w, 0, threads=default_threads())
     x0 = W.initial_x(w)
     gs = TopkGpu(w, keep, x0=x0)
     gs.round(0, torch.from_numpy(g).cuda())
