@@ -16,7 +16,6 @@ iteration, roofline of the dominant kernel, CPU oracle baseline).
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -28,17 +27,12 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0      # MI355X HBM3E
 METRIC = "params/s per K-worker SAEF round + achieved HBM GB/s vs MI355X peak"
 EVENT_EVERY = 4             # timed region: HIP events on every 4th dominant-kernel dispatch
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2008_05823_amd", "csrc", f)
-                  for f in ("saef_kernels.hip", "saef_internal.h", "saef_device.h")]
 
 
 def kernel_hash() -> str:
     """Hash of the kernel sources (the counters in profiles/ apply to it only)."""
-    h = hashlib.sha256()
-    for path in KERNEL_SOURCES:
-        with open(path, "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
+    from paper_2008_05823_amd.profile_summary import kernel_source_hash
+    return kernel_source_hash()
 
 
 def traffic_from_profile(workload: str):
@@ -116,24 +110,28 @@ def host_cpu_model() -> str:
     return "unknown"
 
 
-def copy_probe_gbps(nbytes: int = 2 << 30) -> float:
-    """Read+write GB/s of a plain device-to-device copy (context for the roofline)."""
+def stream_probe_gbps(n: int, reps: int = 10) -> float:
+    """GB/s of the library's stream probe (c = a + b over n fp32 elements: 2
+    reads + 1 write, the worker compression's access pattern) -- the HBM
+    ceiling the roofline fraction is also given against."""
     import torch
-    a = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda")
+    from paper_2008_05823_amd import saef
+    a = torch.empty(n, dtype=torch.float32, device="cuda")
     b = torch.empty_like(a)
+    c = torch.empty_like(a)
     a.fill_(1.0)
+    b.fill_(2.0)
     for _ in range(2):
-        b.copy_(a)
+        saef.saef_stream_probe(a, b, c)
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    reps = 10
     s.record()
     for _ in range(reps):
-        b.copy_(a)
+        saef.saef_stream_probe(a, b, c)
     e.record()
     torch.cuda.synchronize()
     ms = s.elapsed_time(e) / reps
-    del a, b
-    return 2 * nbytes / (ms * 1e-3) / 1e9
+    del a, b, c
+    return 12 * n / (ms * 1e-3) / 1e9
 
 
 def main() -> int:
@@ -145,7 +143,8 @@ def main() -> int:
                     help="flat64k | resnet56 | resnet50 | bert_base | flat256m")
     ap.add_argument("--cpu-rounds", type=int, default=2,
                     help="iterations of the CPU oracle baseline (0 = skip)")
-    ap.add_argument("--no-probe", action="store_true", help="skip the copy-bandwidth probe")
+    ap.add_argument("--no-probe", action="store_true",
+                    help="skip the stream probe (the HBM ceiling of the compression's pattern)")
     ap.add_argument("--momentum", type=float, default=None,
                     help="momentum constant mu in [0, 1): time saef_round_momentum")
     ap.add_argument("--variant", choices=("saef", "ef"), default="saef",
@@ -324,7 +323,9 @@ def main() -> int:
         kernels = {k: {"launches": c, "avg_us": (ms / c * 1e3) if c else None}
                    for k, (c, ms) in saef.saef_profile_read(layout).items()}
         saef.saef_profile_enable(layout, 0)
-    probe = None if args.no_probe else round(copy_probe_gbps(), 1)
+    # the HBM ceiling of the dominant kernel's pattern: as many elements as
+    # the compression streams per launch (K rows of d_pad)
+    probe = None if args.no_probe else round(stream_probe_gbps(K * d_pad), 1)
 
     out = {
         "metric": METRIC,
@@ -359,14 +360,21 @@ def main() -> int:
         "averaging_steps_timed": n_avg,
         "kernels": kernels,
         "kernels_note": "per-kernel averages from a second pass with every dispatch timed",
-        "copy_probe_gbps": probe,
+        "stream_probe_gbps": probe,
         "roofline": {"bound": "hbm",
                      "kernel": "compress" if topk is None else "topk_compress (all passes)",
                      "achieved": c_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": c_gbps / HBM_PEAK_GBPS if c_gbps else None,
                      "traffic": traffic, "algorithmic_bytes_per_launch": c_bytes,
-                     "launches_timed": c_count},
+                     "launches_timed": c_count,
+                     "achieved_source": f"HIP events on every {EVENT_EVERY}th compression "
+                                        "dispatch of the timed region",
+                     "traffic_source": (f"profiles/compress_{args.workload}_counters.txt "
+                                        f"(rocprofv3 FETCH_SIZE + WRITE_SIZE, kernel source "
+                                        f"sha256[:16] {kernel_hash()})") if traffic else None,
+                     "stream_ceiling_gbps": probe,
+                     "frac_of_stream": (c_gbps / probe) if (c_gbps and probe) else None},
     }
     if args.cpu_rounds > 0:
         if mu is not None or split:

@@ -45,7 +45,9 @@
  *
  * ---------------------------------------------------------------- conventions
  * All pointers other than the layout arrays are DEVICE pointers owned by the
- * caller (16-byte aligned; PyTorch gives 256).  Every call is asynchronous
+ * caller, aligned to their element type (4 bytes for fp32 and uint32 arrays,
+ * 8 for uint64 and binary64 ones; a misaligned or NULL required pointer is
+ * SAEF_EINVAL; PyTorch allocations are 256-byte aligned).  Every call is asynchronous
  * and ordered on `stream`; nothing allocates or frees device memory except
  * saef_layout_create / saef_layout_destroy.  Calls that use the same layout
  * must not run concurrently (the layout holds the reduction scratch).
@@ -319,6 +321,13 @@ int saef_status(const saef_layout* layout, hipStream_t stream);
 int saef_profile_enable(saef_layout* layout, int32_t capacity, uint32_t kind_mask,
                         int32_t every);
 int saef_profile_read(saef_layout* layout, int32_t* counts, double* total_ms);
+
+/* Measurement aid (no paper operation): the HBM ceiling of the streaming
+ * pattern the worker compression uses.  c[i] = a[i] + b[i] for i < n (two
+ * fp32 reads and one fp32 write per element, 12 bytes), one 256-thread
+ * workgroup per 2048-element tile, non-temporal accesses.  a, b, c: device
+ * arrays of n floats, c must not overlap a or b (SAEF_EINVAL); n >= 1. */
+int saef_stream_probe(const float* a, const float* b, float* c, int64_t n, hipStream_t stream);
 
 /* Host-side query of a layout: tensor count, padded length, worker limit and
  * the number of work tiles the kernels split the tensors into.  Any output

@@ -14,6 +14,10 @@ ROOT = os.path.dirname(HERE)
 SOURCES = [os.path.join(HERE, "csrc", f) for f in ("saef_kernels.hip", "saef_topk.hip",
                                                           "saef_api.hip")]
 LIB = os.path.join(HERE, "libsaef.so")
+# the same library with 4096-element work tiles: the tile-size determinism
+# test runs the sign path with both builds and compares the bytes
+TILE_VARIANT_ELEMS = 4096
+LIB_TILE_VARIANT = os.path.join(HERE, f"libsaef_tile{TILE_VARIANT_ELEMS}.so")
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -70,6 +74,14 @@ def build_client(out: str = CLIENT, lib: str = LIB) -> str:
     return out
 
 
+def build_tile_variant(verbose: bool = False) -> str:
+    """The library with SAEF_TILE_ELEMS = TILE_VARIANT_ELEMS (Top-K plans are
+    refused by that build; the sign path is complete)."""
+    return build(out=LIB_TILE_VARIANT, verbose=verbose,
+                 defines=(f"SAEF_TILE_ELEMS={TILE_VARIANT_ELEMS}",))
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_tile_variant())
     print(build_client())

@@ -569,6 +569,15 @@ int saef_profile_enable(saef_layout* layout, int32_t capacity, uint32_t kind_mas
   return SAEF_OK;
 }
 
+int saef_stream_probe(const float* a, const float* b, float* c, int64_t n,
+                      hipStream_t stream) {
+  if (n < 1 || n > (int64_t)saef::kTileElems * 2147483647) return SAEF_EINVAL;
+  if (!f32_ok(a) || !f32_ok(b) || !f32_ok(c)) return SAEF_EINVAL;
+  const size_t vb = (size_t)n * sizeof(float);
+  if (overlap(c, vb, a, vb) || overlap(c, vb, b, vb)) return SAEF_EINVAL;
+  return hip_rc(saef::launch_stream_probe(a, b, c, n, stream));
+}
+
 int saef_profile_read(saef_layout* layout, int32_t* counts, double* total_ms) {
   if (layout == nullptr || counts == nullptr || total_ms == nullptr) return SAEF_EINVAL;
   for (int i = 0; i < kProfileKinds; ++i) {
@@ -594,6 +603,7 @@ int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk**
   if (out == nullptr) return SAEF_EINVAL;
   *out = nullptr;
   if (layout == nullptr || keep == nullptr) return SAEF_EINVAL;
+  if (!saef::kTkUsable) return SAEF_EINVAL;  // a build with other than 2048-element tiles
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess) return SAEF_EHIP;
   if (dev != layout->device) return SAEF_EINVAL;

@@ -152,4 +152,9 @@ hipError_t launch_mismatch(const DevLayout& lay, int K, int mode, const float* e
                            const float* srv_scales, bool decode_s, double* out, hipStream_t s,
                            const LaunchEvents& ev = LaunchEvents());
 
+// The HBM ceiling of the compression's access pattern: c = a + b over n
+// elements (measurement aid; no layout).
+hipError_t launch_stream_probe(const float* a, const float* b, float* c, int64_t n,
+                               hipStream_t s);
+
 }  // namespace saef

@@ -572,12 +572,13 @@ __global__ __launch_bounds__(kBlock) void k_aggregate(DevLayout lay, int K, doub
 // ------------------------------------------------------------------ materialize
 // Grid: n_tiles * rows, rows = K (+1 when the server row is requested); row K
 // is the server error and the weights.
+// e_out may be e, es_out es and x_out x (in place): every element is read and
+// then written by the same lane, so those pairs are not restrict-qualified.
 __global__ __launch_bounds__(kBlock) void k_materialize(
-    DevLayout lay, int K, int rows, int mode, const float* __restrict__ e,
-    const uint64_t* __restrict__ signs, const float* __restrict__ scales,
-    float* __restrict__ e_out, const float* __restrict__ es, const float* __restrict__ x,
-    const uint64_t* __restrict__ ss, const float* __restrict__ sscales,
-    float* __restrict__ es_out, float* __restrict__ x_out) {
+    DevLayout lay, int K, int rows, int mode, const float* e,
+    const uint64_t* __restrict__ signs, const float* __restrict__ scales, float* e_out,
+    const float* es, const float* x, const uint64_t* __restrict__ ss,
+    const float* __restrict__ sscales, float* es_out, float* x_out) {
   const int64_t b = blockIdx.x;
   const int row = (int)(b % rows);
   const Tile tile = lay.tiles[b / rows];
@@ -763,6 +764,10 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
 // [w kMisWaveWords, (w + 1) kMisWaveWords) of tile b, and the four waves'
 // sums are added in wave order.
 constexpr int kMisWaveWords = kTileElems / 64 / kWaves;  // 8
+// Every tile holds at most kTileElems elements (a tensor of at most 2^28
+// elements never needs larger tiles), so the waves' word ranges cover it.
+static_assert((int64_t)kTileElems * kMaxTilesPerTensor >= kMaxTensor,
+              "tiles of a maximal tensor hold kTileElems elements");
 template <bool kDC, bool kDecE, bool kDecS, int kRK>
 __global__ __launch_bounds__(kBlock) void k_mismatch(DevLayout lay, int K, double inv_k,
                                                      const float* __restrict__ e,
@@ -896,7 +901,40 @@ __global__ __launch_bounds__(kBlock) void k_mfinalize2(DevLayout lay, int K,
 }
 
 
+// ------------------------------------------------------------------ stream probe
+// The HBM ceiling of the worker compression's access pattern: c = a + b over
+// n elements (2 reads + 1 write of fp32), one 256-thread workgroup per
+// 2048-element tile, kU words per wave, non-temporal buffer accesses.
+__global__ __launch_bounds__(kBlock) void k_stream_probe(const float* __restrict__ a,
+                                                         const float* __restrict__ b,
+                                                         float* __restrict__ c, int64_t n) {
+  const int64_t start = (int64_t)blockIdx.x * kTileElems;
+  const uint32_t nbytes = (uint32_t)min((int64_t)kTileElems, n - start) * 4u;
+  const Buf ra = buf_of(a + start, nbytes);
+  const Buf rb = buf_of(b + start, nbytes);
+  const Buf rc = buf_of(c + start, nbytes);
+  for (int w0 = wave_id() * kU; w0 * 256u < nbytes; w0 += kWaves * kU) {
+    const uint32_t off0 = (uint32_t)(w0 * 64 + lane_id()) * 4u;
+    float av[kU], bv[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      av[u] = buf_ld(ra, off0 + 256u * u);
+      bv[u] = buf_ld(rb, off0 + 256u * u);
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) buf_st(rc, off0 + 256u * u, av[u] + bv[u]);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_stream_probe(const float* a, const float* b, float* c, int64_t n,
+                               hipStream_t s) {
+  const LaunchEvents ev;
+  const dim3 grid((unsigned)((n + kTileElems - 1) / kTileElems));
+  SAEF_LAUNCH(k_stream_probe, grid, dim3(kBlock), 0, s, a, b, c, n);
+  return hipGetLastError();
+}
 
 hipError_t launch_compress(const DevLayout& lay, int K, float lr, float mu, const float* g,
                            float* m, float* e, uint64_t* signs, const float* scales, bool decode,

@@ -33,10 +33,15 @@ constexpr int kTkSpecSlot = kTkHist;
 constexpr uint32_t kTkSpecNone = 0xFFFFu;
 constexpr uint32_t kTkSpecMargin = 1u << 18;
 constexpr int kTkSpecMaxShare = 8;  // lists when k_l * 8 <= n_l
+// The Top-K kernels take a tile as 32 sign words (one per lane of a gather
+// wave): they need the layout's tiles to hold 2048 elements.  A library built
+// with another SAEF_TILE_ELEMS (the sign path works with any) refuses Top-K
+// plans (saef_topk_create returns SAEF_EINVAL).
+constexpr int kTkTileElems = 2048;
+constexpr bool kTkUsable = kTileElems == kTkTileElems;
 static_assert(kTkHistPad >= kTkHist && kTkHistPad % 4 == 0, "padded tile histogram");
-static_assert(kTileElems == 2048, "the Top-K kernels take a tile as 32 words, one per lane");
-static_assert(kTileElems < 65536, "a tile's bin counts fit 16 bits");
-static_assert(kTkChunk % kTileElems == 0, "a server chunk holds whole tiles");
+static_assert(kTkTileElems < 65536, "a tile's bin counts fit 16 bits");
+static_assert(kTkChunk % kTkTileElems == 0, "a server chunk holds whole tiles");
 static_assert(kTkSpecSlot < kTkHistPad && kTkSpecSlot % 2 == 0, "a spare, even histogram slot");
 static_assert(kTkSpecCap < (int)kTkSpecNone, "list counts fit the slot below the marker");
 static_assert((int64_t)kTileElems * kMaxTilesPerTensor >= kMaxTensor,

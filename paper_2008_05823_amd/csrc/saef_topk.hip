@@ -53,7 +53,7 @@ namespace {
 
 constexpr uint32_t kFiniteLimit = 0x7F800000u;  // keys >= this are Inf or NaN
 constexpr int kTkU = 8;                         // words per wave per pass (Delta pass: one pass)
-constexpr int kTileWords = kTileElems / 64;     // 32
+constexpr int kTileWords = kTkTileElems / 64;     // 32
 constexpr int kBig = 1024;                      // threads of the per-(row, tensor) kernels
 static_assert(kTileWords <= kWave, "one selection word of a tile per lane");
 // Guarded loads without a branch: the load of p[ok ? j : 0] is always
@@ -539,7 +539,7 @@ __device__ __forceinline__ void gather_tile(const DevLayout& lay, const TkDev& t
     }
     u64 myw = 0;        // lane u < nw: selection word u
     uint32_t base = 0;  // candidates in the earlier words
-    if (tile.count == kTileElems)
+    if (tile.count == kTkTileElems)
       gather_words<true>(v, tile.count, lo, up, rel0, nslots, slots, myw, base);
     else
       gather_words<false>(v, tile.count, lo, up, rel0, nslots, slots, myw, base);
@@ -710,7 +710,7 @@ __global__ __launch_bounds__(kBlock) void k_tk_scan(DevLayout lay, TkDev tk, int
       }
 #pragma unroll
       for (int u = 0; u < kIlp; ++u) {
-        const int64_t t = (int64_t)(e[u] >> 32) / kTileElems - b;  // tile of the block
+        const int64_t t = (int64_t)(e[u] >> 32) / kTkTileElems - b;  // tile of the block
         if (c0 + u * kBlock < hi && cand_kept(e[u], st) && t >= 0 && t < kBlock)
           atomicAdd(&s_cnt[t], 1u);
       }
@@ -973,7 +973,7 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
   constexpr int kB = kWave / U;  // workers per batch
   static_assert(kB * U == kWave, "one (worker, word) pair per lane");
   static_assert(kTileWords % U == 0, "a pass of U words stays in one tile");
-  constexpr int kChunkTiles = kTkChunk / kTileElems;
+  constexpr int kChunkTiles = kTkChunk / kTkTileElems;
   __shared__ uint32_t h[kMode == 1 ? kChunkTiles * kTkHistPad : 1];  // per tile of the chunk
   const int64_t ci = blockIdx.x;
   const TkChunk c = tk.chunks[ci];
@@ -1125,8 +1125,8 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
     __syncthreads();
     // the tile histograms of the chunk, 16-bit counts, two bins per store
     const TensorInfo ten = lay.tensors[c.l];
-    const int64_t tile0 = ten.first_tile + (c.start - ten.off) / kTileElems;
-    const int ntile = (c.count + kTileElems - 1) / kTileElems;
+    const int64_t tile0 = ten.first_tile + (c.start - ten.off) / kTkTileElems;
+    const int ntile = (c.count + kTkTileElems - 1) / kTkTileElems;
     uint32_t* out = reinterpret_cast<uint32_t*>(tile_hist(tk, lay, lay.k_max, tile0));
     for (int i = threadIdx.x; i < ntile * (kTkHistPad / 2); i += kBig)
       out[i] = (h[2 * i] & 0xFFFFu) | (h[2 * i + 1] << 16);

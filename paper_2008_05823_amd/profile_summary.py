@@ -6,8 +6,9 @@ prints a short text summary:
 
 * per kernel: calls and average duration (kernel trace statistics);
 * per kernel: HBM bytes per dispatch from FETCH_SIZE and WRITE_SIZE, each
-  scaled by the factor that makes the same counter read exactly the size of
-  a plain device-to-device copy of known size found in the same run;
+  scaled by the factor that makes the same counter read exactly the bytes of
+  the library's stream probe found in the same run (k_stream_probe: reads
+  8 N and writes 4 N bytes for N elements per launch);
 * or, from a kernel trace alone (``--trace``), per (kernel, workgroup count):
   the dispatches after the first ``--skip`` ones, their average duration,
   and the duration of the first one.
@@ -15,7 +16,7 @@ prints a short text summary:
 Usage:
   python -m paper_2008_05823_amd.profile_summary --stats DIR/x_kernel_stats.csv
       --fetch DIR/y_counter_collection.csv --write DIR/z_counter_collection.csv
-      --copy-bytes 2147483648 [--source-hash HASH]
+      --probe-elems N [--kernel NAME --algorithmic BYTES --counters-out FILE]
   python -m paper_2008_05823_amd.profile_summary --trace DIR/x_kernel_trace.csv [--skip N]
 """
 from __future__ import annotations
@@ -23,7 +24,23 @@ from __future__ import annotations
 import argparse
 import collections
 import csv
+import hashlib
+import os
 import re
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+# the sources the sign-path kernels are built from (the counters in a
+# summary apply to this hash only)
+KERNEL_SOURCES = [os.path.join(HERE, "csrc", f)
+                  for f in ("saef_kernels.hip", "saef_internal.h", "saef_device.h")]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def short_name(name: str) -> str:
@@ -47,12 +64,12 @@ def counter_per_kernel(path: str):
     return out
 
 
-def copy_factor(per_kernel, copy_bytes: int, expect_kib: float) -> float:
-    """Scale that turns the counter of the known-size copy into its true size."""
-    vals = [v for g, v in per_kernel.get("__amd_rocclr_copyBuffer", []) if v > 0.25 * expect_kib]
+def probe_factor(per_kernel, true_kib: float) -> float:
+    """Scale that turns the counter of the stream probe into its true size."""
+    vals = [v for _, v in per_kernel.get("k_stream_probe", []) if v > 0]
     if not vals:
-        raise SystemExit("no copy dispatch of the expected size in the counter file")
-    return (copy_bytes / 1024.0) / (sum(vals) / len(vals)) if expect_kib else 1.0
+        raise SystemExit("no stream-probe dispatch in the counter file")
+    return true_kib / (sum(vals) / len(vals))
 
 
 def trace_table(path: str, skip: int) -> None:
@@ -81,30 +98,39 @@ def main() -> int:
     ap.add_argument("--stats")
     ap.add_argument("--fetch")
     ap.add_argument("--write")
-    ap.add_argument("--copy-bytes", type=int,
-                    help="bytes read (and written) by the reference device copy")
-    ap.add_argument("--source-hash", default=None)
+    ap.add_argument("--probe-elems", type=int,
+                    help="elements per stream-probe launch (reads 8 N, writes 4 N bytes)")
+    ap.add_argument("--kernel", default=None, help="kernel whose bytes go to --counters-out")
+    ap.add_argument("--algorithmic", type=float, default=None,
+                    help="algorithmic bytes per launch of --kernel")
+    ap.add_argument("--counters-out", default=None,
+                    help="write the kernel's HBM bytes per launch and the source hash here")
+    ap.add_argument("--header", default=None,
+                    help="comment lines (a file) put at the top of --counters-out")
     args = ap.parse_args()
     if args.trace:
         trace_table(args.trace, args.skip)
         return 0
-    if not (args.stats and args.fetch and args.write and args.copy_bytes):
-        ap.error("--stats, --fetch, --write and --copy-bytes are required without --trace")
+    if not (args.stats and args.fetch and args.write and args.probe_elems):
+        ap.error("--stats, --fetch, --write and --probe-elems are required without --trace")
 
+    stats = kernel_stats(args.stats)
     print("kernel durations (rocprofv3 --kernel-trace --stats)")
     print(f"  {'kernel':44s} {'calls':>6s} {'avg_us':>10s} {'pct':>7s}")
-    for name, calls, avg_us, pct in kernel_stats(args.stats):
+    for name, calls, avg_us, pct in stats:
         print(f"  {name:44s} {calls:6d} {avg_us:10.1f} {pct:7.2f}")
 
     fetch = counter_per_kernel(args.fetch)
     write = counter_per_kernel(args.write)
-    ff = copy_factor(fetch, args.copy_bytes, args.copy_bytes / 1024.0)
-    wf = copy_factor(write, args.copy_bytes, args.copy_bytes / 1024.0)
+    n = args.probe_elems
+    ff = probe_factor(fetch, 8 * n / 1024.0)
+    wf = probe_factor(write, 4 * n / 1024.0)
     print()
-    print(f"HBM bytes per dispatch (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE; KiB scaled by the "
-          f"copy calibration: fetch x{ff:.4f}, write x{wf:.4f}, from a {args.copy_bytes}-byte "
-          f"device-to-device copy in the same run)")
+    print(f"HBM bytes per dispatch (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE; KiB scaled so that "
+          f"the stream probe of the same run reads {8 * n} and writes {4 * n} bytes: fetch "
+          f"x{ff:.4f}, write x{wf:.4f})")
     print(f"  {'kernel':44s} {'n':>4s} {'read_MB':>10s} {'write_MB':>10s} {'total_MB':>10s}")
+    per = {}
     for name in fetch:
         if name.startswith("__amd") or name.startswith("void at::") or name.startswith("at::"):
             continue
@@ -112,10 +138,30 @@ def main() -> int:
         wv = [v for _, v in write.get(name, [])]
         r = sum(fv) / len(fv) * 1024 * ff / 1e6
         w = (sum(wv) / len(wv) * 1024 * wf / 1e6) if wv else float("nan")
+        per[name] = (r, w, len(fv))
         print(f"  {name:44s} {len(fv):4d} {r:10.1f} {w:10.1f} {r + w:10.1f}")
-    if args.source_hash:
-        print()
-        print(f"kernel_source_sha256_16: {args.source_hash}")
+    src = kernel_source_hash()
+    print()
+    print(f"kernel_source_sha256_16: {src}")
+    if args.counters_out:
+        if args.kernel not in per:
+            raise SystemExit(f"kernel {args.kernel!r} not in the counter files")
+        r, w, cnt = per[args.kernel]
+        avg = {name: us for name, _, us, _ in stats}.get(args.kernel)
+        with open(args.counters_out, "w") as f:
+            if args.header:
+                f.write(open(args.header).read())
+            f.write(f"# {args.kernel}: FETCH_SIZE x {ff:.4f} + WRITE_SIZE x {wf:.4f} (stream-probe "
+                    f"calibration), average of {cnt} dispatches: read {r:.1f} MB, write "
+                    f"{w:.1f} MB\n")
+            if args.algorithmic:
+                f.write(f"# algorithmic bytes per launch {args.algorithmic:.0f}: traffic / "
+                        f"algorithmic = {(r + w) * 1e6 / args.algorithmic:.4f}\n")
+            if avg is not None:
+                f.write(f"# rocprofv3 average duration: {avg:.1f} us\n")
+            f.write(f"kernel: {args.kernel}\n")
+            f.write(f"hbm_bytes_per_launch: {(r + w) * 1e6:.0f}\n")
+            f.write(f"kernel_source_sha256_16: {src}\n")
     return 0
 
 

@@ -63,6 +63,7 @@ _SIGS = {
     "saef_status": [_P, _P],
     "saef_profile_enable": [_P, _i32, ctypes.c_uint32, _i32],
     "saef_profile_read": [_P, _P, _P],
+    "saef_stream_probe": [_P, _P, _P, _i64, _P],
 }
 for _name, _args in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -360,6 +361,15 @@ def saef_profile_read(layout: Layout) -> dict:
     ms = (ctypes.c_double * len(PROFILE_KINDS))()
     _check("saef_profile_read", _lib.saef_profile_read(layout.handle, counts, ms))
     return {k: (counts[i], ms[i]) for i, k in enumerate(PROFILE_KINDS)}
+
+
+def saef_stream_probe(a, b, c, stream=None) -> None:
+    """c = a + b over equal-size contiguous fp32 device tensors (the HBM
+    ceiling of the compression's streaming pattern; measurement aid)."""
+    n = a.numel()
+    if b.numel() != n or c.numel() != n:
+        raise ValueError("saef_stream_probe: a, b and c must have the same size")
+    _check("saef_stream_probe", _lib.saef_stream_probe(_f(a), _f(b), _f(c), n, _stream(stream)))
 
 
 def raw_library() -> ctypes.CDLL:

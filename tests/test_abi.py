@@ -77,3 +77,36 @@ def test_topk_calls_reject_null_plans_on_host(saef):
     assert lib.saef_topk_round_begin(None, 0, 0, 1, 1, 1, *([None] * 7)) == saef.EINVAL
     assert lib.saef_topk_round_end(None, 0, 0, 1, ctypes.c_float(0.1), ctypes.c_float(0.0), 1,
                                    *([None] * 12)) == saef.EINVAL
+
+
+@pytest.mark.gpu
+def test_alignment_rule_on_device(saef):
+    """Buffers must be aligned to their element type, no more: a float buffer
+    4 bytes past a 256-byte boundary is accepted, one 2 bytes past is
+    SAEF_EINVAL (nothing enqueued); sign words need 8 bytes."""
+    import torch
+    from paper_2008_05823_amd import workloads as W
+    w = W.custom([100, 70], K=2)
+    off, n, d_pad = w.layout()
+    lay = saef.Layout(off, n, d_pad, 2)
+    lib = saef.raw_library()
+    f32 = dict(dtype=torch.float32, device="cuda")
+    g = torch.zeros(2 * d_pad + 8, **f32)
+    e = torch.zeros(2 * d_pad + 8, **f32)
+    words = torch.zeros(2 * (d_pad // 64) + 2, dtype=torch.int64, device="cuda")
+    scales = torch.zeros(2 * w.L + 4, **f32)
+    s = torch.cuda.current_stream().cuda_stream
+
+    def compress(g_ptr, e_ptr, w_ptr):
+        return lib.saef_compress(lay.handle, 2, ctypes.c_float(0.1), g_ptr, e_ptr, w_ptr,
+                                 scales.data_ptr(), s)
+
+    base_w = words.data_ptr()
+    assert compress(g.data_ptr() + 4, e.data_ptr() + 4, base_w) == saef.OK
+    assert compress(g.data_ptr() + 2, e.data_ptr(), base_w) == saef.EINVAL
+    assert compress(g.data_ptr(), e.data_ptr() + 2, base_w) == saef.EINVAL
+    assert compress(g.data_ptr(), e.data_ptr(), base_w + 4) == saef.EINVAL
+    assert compress(g.data_ptr(), e.data_ptr(), base_w + 8) == saef.OK
+    torch.cuda.synchronize()
+    assert saef.saef_status(lay) == saef.OK
+    lay.close()
