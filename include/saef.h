@@ -322,6 +322,23 @@ int saef_profile_enable(saef_layout* layout, int32_t capacity, uint32_t kind_mas
                         int32_t every);
 int saef_profile_read(saef_layout* layout, int32_t* counts, double* total_ms);
 
+/* For callers that cannot allocate device memory during the iteration
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): saef_round with the same arguments and the same results, whose
+ * kernels keep their tile partial sums in a static device array of the
+ * library (32 MiB per GPU, held until the process ends) instead of the
+ * layout's scratch.  The call allocates nothing.  It needs (K + 1) * n_tiles
+ * * 16 bytes (rounded up to 256) plus (K + 1) * L * ceil(max tiles per tensor
+ * / 4096) * 16 bytes of that array; a layout and K needing more are
+ * SAEF_EINVAL.  Every call on one GPU shares the array, whatever the layout:
+ * calls that overlap on one GPU (other streams, other threads) race.  The
+ * array's device address is looked up by saef_layout_create (SAEF_EHIP here
+ * if that failed). */
+int saef_round_noalloc(const saef_layout* layout, int64_t t, int64_t period, int32_t K, float lr,
+                       int32_t mode, const float* g, float* e, float* e_srv, float* x, float* xh,
+                       uint64_t* signs, float* scales, uint64_t* srv_signs, float* srv_scales,
+                       hipStream_t stream);
+
 /* Measurement aid (no paper operation): the HBM ceiling of the streaming
  * pattern the worker compression uses.  c[i] = a[i] + b[i] for i < n (two
  * fp32 reads and one fp32 write per element, 12 bytes), one 256-thread

@@ -4,6 +4,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -63,6 +64,35 @@ struct saef_topk {
 };
 
 namespace {
+
+// ---- scratch of the allocation-free iteration (saef_round_noalloc) --------
+// The tile partial sums and their second level live in this file-scope
+// device array instead of the layout's buffers.  Host code never uses the
+// array's name as an address: saef_layout_create looks up its device
+// address once per device (hipGetSymbolAddress, with that device current)
+// and saef_round_noalloc passes that address to the kernels.
+constexpr size_t kScratchBytes = size_t(32) << 20;
+constexpr int kMaxDevices = 64;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+bool g_scratch_tried[kMaxDevices] = {};
+
+// Looks up `scratch` on the current device (device `dev`) once.
+void scratch_init(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_tried[dev]) return;
+  g_scratch_tried[dev] = true;
+  void* p = nullptr;
+  if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) == hipSuccess) g_scratch_ptr[dev] = p;
+}
+
+void* scratch_of(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  return g_scratch_ptr[dev];
+}
 
 // Elements per work tile of a tensor of n elements: kTileElems, or more for
 // very large tensors so that no tensor has more than kMaxTilesPerTensor tiles
@@ -183,6 +213,7 @@ int saef_layout_create(const int64_t* off, const int64_t* n, int32_t L, int64_t 
     delete lay;
     return SAEF_EHIP;
   }
+  scratch_init(lay->device);  // the allocation-free iteration's scratch on this device
   lay->L = L;
   lay->k_max = k_max;
   lay->d_pad = d_pad;
@@ -355,7 +386,7 @@ int round_begin_impl(const saef_layout* layout, int64_t t, int64_t period, int32
                      int32_t mode, int32_t variant, float* e, const float* e_srv, const float* x,
                      float* xh, const uint64_t* signs, const float* scales,
                      const uint64_t* srv_signs, const float* srv_scales, double* mismatch,
-                     hipStream_t stream) {
+                     hipStream_t stream, const DevLayout* dev = nullptr) {
   int rc = check_common(layout, K);
   if (rc != SAEF_OK) return rc;
   if (t < 0 || period < 0) return SAEF_EINVAL;
@@ -381,7 +412,7 @@ int round_begin_impl(const saef_layout* layout, int64_t t, int64_t period, int32
         overlap(mismatch, mb, x, xb) || (e_srv != nullptr && overlap(mismatch, mb, e_srv, xb)))
       return SAEF_EINVAL;
   }
-  const DevLayout& d = layout->dev;
+  const DevLayout& d = dev != nullptr ? *dev : layout->dev;
   if (variant == SAEF_VARIANT_SAEF) {
     // error averaging (when due) and step ahead, applying last iteration's
     // pending corrections to e and (double-way) x
@@ -419,7 +450,7 @@ int round_begin_impl(const saef_layout* layout, int64_t t, int64_t period, int32
 int round_end_impl(const saef_layout* layout, int64_t t, int64_t period, int32_t K, float lr,
                    float mu, int32_t mode, const float* g, float* m, float* e, float* e_srv,
                    float* x, uint64_t* signs, float* scales, uint64_t* srv_signs,
-                   float* srv_scales, hipStream_t stream) {
+                   float* srv_scales, hipStream_t stream, const DevLayout* dev = nullptr) {
   int rc = check_common(layout, K);
   if (rc != SAEF_OK) return rc;
   if (t < 0 || period < 0 || !std::isfinite(lr)) return SAEF_EINVAL;
@@ -438,7 +469,7 @@ int round_end_impl(const saef_layout* layout, int64_t t, int64_t period, int32_t
   const bool pending = t > 0;
   const bool averaging = period > 0 && (t + 1) % period == 0;
   const bool dc = mode == SAEF_MODE_DC;
-  const DevLayout& d = layout->dev;
+  const DevLayout& d = dev != nullptr ? *dev : layout->dev;
   // [gradient slot: g was computed by the caller at the first half's xh]
   rc = hip_rc(timed(layout, 1, [&](const saef::LaunchEvents& ev) {
     return saef::launch_compress(d, K, lr, mu, g, m, e, signs, scales, pending && !averaging,
@@ -463,7 +494,7 @@ int round_end_impl(const saef_layout* layout, int64_t t, int64_t period, int32_t
 int round_impl(const saef_layout* layout, int64_t t, int64_t period, int32_t K, float lr,
                float mu, int32_t mode, const float* g, float* m, float* e, float* e_srv,
                float* x, float* xh, uint64_t* signs, float* scales, uint64_t* srv_signs,
-               float* srv_scales, hipStream_t stream) {
+               float* srv_scales, hipStream_t stream, const DevLayout* dev = nullptr) {
   // check both halves' arguments before anything is enqueued
   int rc = check_common(layout, K);
   if (rc != SAEF_OK) return rc;
@@ -482,10 +513,10 @@ int round_impl(const saef_layout* layout, int64_t t, int64_t period, int32_t K, 
                        overlap(m, vb, xh, vb) || overlap(m, vb, x, xb)))
     return SAEF_EINVAL;
   rc = round_begin_impl(layout, t, period, K, mode, SAEF_VARIANT_SAEF, e, e_srv, x, xh, signs,
-                        scales, srv_signs, srv_scales, nullptr, stream);
+                        scales, srv_signs, srv_scales, nullptr, stream, dev);
   if (rc != SAEF_OK) return rc;
   return round_end_impl(layout, t, period, K, lr, mu, mode, g, m, e, e_srv, x, signs, scales,
-                        srv_signs, srv_scales, stream);
+                        srv_signs, srv_scales, stream, dev);
 }
 
 }  // namespace
@@ -498,6 +529,31 @@ int saef_round(const saef_layout* layout, int64_t t, int64_t period, int32_t K, 
                hipStream_t stream) {
   return round_impl(layout, t, period, K, lr, 0.0f, mode, g, nullptr, e, e_srv, x, xh, signs,
                     scales, srv_signs, srv_scales, stream);
+}
+
+int saef_round_noalloc(const saef_layout* layout, int64_t t, int64_t period, int32_t K, float lr,
+                       int32_t mode, const float* g, float* e, float* e_srv, float* x, float* xh,
+                       uint64_t* signs, float* scales, uint64_t* srv_signs, float* srv_scales,
+                       hipStream_t stream) {
+  int rc = check_common(layout, K);
+  if (rc != SAEF_OK) return rc;
+  // the tile partial sums of K worker rows and the server row, and their
+  // second level, must fit the static scratch
+  const DevLayout& ld = layout->dev;
+  const size_t rows = (size_t)K + 1;
+  const size_t part_bytes = rows * (size_t)ld.n_tiles * 2 * sizeof(unsigned long long);
+  const size_t part2_bytes = rows * (size_t)ld.L * (size_t)ld.fin_split * 2 *
+                             sizeof(unsigned long long);
+  const size_t part_pad = (part_bytes + 255) / 256 * 256;
+  if (part_pad + part2_bytes > kScratchBytes) return SAEF_EINVAL;
+  unsigned char* base = static_cast<unsigned char*>(scratch_of(layout->device));
+  if (base == nullptr) return SAEF_EHIP;
+  DevLayout d = ld;
+  d.part = reinterpret_cast<unsigned long long*>(base);
+  d.part2 = reinterpret_cast<unsigned long long*>(base + part_pad);
+  d.k_max = K;  // the server's partial sums go to row K of the scratch
+  return round_impl(layout, t, period, K, lr, 0.0f, mode, g, nullptr, e, e_srv, x, xh, signs,
+                    scales, srv_signs, srv_scales, stream, &d);
 }
 
 int saef_round_momentum(const saef_layout* layout, int64_t t, int64_t period, int32_t K,

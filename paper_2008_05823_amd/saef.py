@@ -42,6 +42,8 @@ _SIGS = {
     "saef_step_ahead": [_P, _i32, _P, _P, _P, _P],
     "saef_error_average": [_P, _i32, _P, _P],
     "saef_round": [_P, _i64, _i64, _i32, _f32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P],
+    "saef_round_noalloc": [_P, _i64, _i64, _i32, _f32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                           _P],
     "saef_round_momentum": [_P, _i64, _i64, _i32, _f32, _f32, _i32, _P, _P, _P, _P, _P, _P, _P,
                             _P, _P, _P, _P],
     "saef_round_begin": [_P, _i64, _i64, _i32, _i32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _P,
@@ -201,6 +203,15 @@ def saef_round(layout: Layout, t: int, period: int, K: int, lr: float, mode: int
     _check("saef_round", _lib.saef_round(layout.handle, t, period, K, lr, mode, _f(g), _f(e),
                                          _f(e_srv), _f(x), _f(xh), _w(signs), _f(scales),
                                          _w(srv_signs), _f(srv_scales), _stream(stream)))
+
+
+def saef_round_noalloc(layout: Layout, t: int, period: int, K: int, lr: float, mode: int, g, e,
+                       e_srv, x, xh, signs, scales, srv_signs=None, srv_scales=None,
+                       stream=None):
+    _check("saef_round_noalloc",
+           _lib.saef_round_noalloc(layout.handle, t, period, K, lr, mode, _f(g), _f(e), _f(e_srv),
+                                   _f(x), _f(xh), _w(signs), _f(scales), _w(srv_signs),
+                                   _f(srv_scales), _stream(stream)))
 
 
 def saef_round_momentum(layout: Layout, t: int, period: int, K: int, lr: float, mu: float,
