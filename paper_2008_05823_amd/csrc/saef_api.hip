@@ -61,6 +61,9 @@ struct saef_topk {
   void* mem_cand = nullptr;
   void* mem_cand_off = nullptr;
   void* mem_spec = nullptr;
+  // the side stream (default priority) and fork/join events of the worker
+  // compression's two row groups
+  saef::TkStreams side{};
 };
 
 namespace {
@@ -178,6 +181,12 @@ void free_layout(saef_layout* l) {
 
 void free_topk(saef_topk* p) {
   if (p == nullptr) return;
+  if (p->side.stream != nullptr) {
+    (void)hipStreamSynchronize(p->side.stream);
+    (void)hipStreamDestroy(p->side.stream);
+  }
+  if (p->side.fork != nullptr) (void)hipEventDestroy(p->side.fork);
+  if (p->side.join != nullptr) (void)hipEventDestroy(p->side.join);
   for (void* q : {p->mem_chunks, p->mem_tens, p->mem_groups, p->mem_sgroups, p->mem_thist,
                   p->mem_ghist, p->mem_sghist, p->mem_goff, p->mem_sel, p->mem_tile_cnt,
                   p->mem_cand, p->mem_cand_off, p->mem_spec})
@@ -753,6 +762,9 @@ int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk**
       }
     err = hipMemcpy(p->mem_sel, sel0.data(), sel_bytes, hipMemcpyHostToDevice);
   }
+  if (err == hipSuccess) err = hipStreamCreateWithFlags(&p->side.stream, hipStreamNonBlocking);
+  if (err == hipSuccess) err = hipEventCreateWithFlags(&p->side.fork, hipEventDisableTiming);
+  if (err == hipSuccess) err = hipEventCreateWithFlags(&p->side.join, hipEventDisableTiming);
   if (err == hipSuccess) err = hipDeviceSynchronize();
   if (err != hipSuccess) {
     free_topk(p);
@@ -822,7 +834,7 @@ int topk_compress(const saef_topk* plan, int32_t K, float lr, float mu, const fl
     return SAEF_EINVAL;
   return hip_rc(timed(layout, 1, [&](const saef::LaunchEvents& ev) {
     return saef::launch_topk_compress(layout->dev, plan->dev, K, lr, mu, g, m, e, sel, rank,
-                                      vals, pend_in, pend_out, stream, ev);
+                                      vals, pend_in, pend_out, stream, plan->side, ev);
   }));
 }
 

@@ -117,10 +117,22 @@ struct TkDev {
 // kept elements (the selection words in sel) are still to be set to 0; they
 // are read as 0.  pend_out: this call's kept elements are left as they are
 // (pending, for the next reader) instead of being set to 0.
+//
+// side: a second stream of the plan and two events (fork, join).  When
+// given and K >= 2, the rows are compressed in two groups and the first
+// group's selection runs on the side stream, overlapping the second group's
+// Delta pass; s waits for the side stream before the call returns (an event
+// fork and join, so the launches stay capturable in a HIP graph).
+struct TkStreams {
+  hipStream_t stream = nullptr;
+  hipEvent_t fork = nullptr;
+  hipEvent_t join = nullptr;
+};
 hipError_t launch_topk_compress(const DevLayout& lay, const TkDev& tk, int K, float lr, float mu,
                                 const float* g, float* m, float* e, uint64_t* sel,
                                 uint32_t* rank, float* vals, bool pend_in, bool pend_out,
-                                hipStream_t s, const LaunchEvents& ev = LaunchEvents());
+                                hipStream_t s, const TkStreams& side,
+                                const LaunchEvents& ev = LaunchEvents());
 
 // Sets to 0 the elements of the K rows of e whose selection bit is set.
 hipError_t launch_topk_materialize(const DevLayout& lay, int K, float* e, const uint64_t* sel,

@@ -158,16 +158,17 @@ __device__ __forceinline__ void delta_words(int w0, int nw, int count, float lr,
 // holds the previous call's Delta with its kept elements (selection words
 // psel) still to be set to 0; they are read as 0.
 template <bool kMom, bool kPend>
-__global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, int K, float lr,
-                                                     float mu, const float* __restrict__ g,
+__global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, int R, int row0,
+                                                     float lr, float mu,
+                                                     const float* __restrict__ g,
                                                      float* __restrict__ m,
                                                      float* __restrict__ e,
                                                      const uint64_t* __restrict__ psel) {
   static_assert(kWaves * kTkU == kTileWords, "one pass of the four waves covers a tile");
   __shared__ uint32_t h[kTkHistPad];
   __shared__ uint32_t s_cnt[kWaves];
-  const int k = (int)(blockIdx.x % (unsigned)K);
-  const int64_t ti = blockIdx.x / (unsigned)K;
+  const int k = row0 + (int)(blockIdx.x % (unsigned)R);
+  const int64_t ti = blockIdx.x / (unsigned)R;
   const Tile tile = lay.tiles[ti];
   const TkSel* st = tk.sel + (int64_t)k * lay.L + tile.l;
   const uint32_t win = st->win;
@@ -1191,21 +1192,48 @@ struct Launcher {
 hipError_t launch_topk_compress(const DevLayout& lay, const TkDev& tk, int K, float lr, float mu,
                                 const float* g, float* m, float* e, uint64_t* sel,
                                 uint32_t* rank, float* vals, bool pend_in, bool pend_out,
-                                hipStream_t s, const LaunchEvents& ev) {
-  const dim3 grid((unsigned)(lay.n_tiles * K));
-  // the first kernel stamps the start event, the last one the stop event
-#define SAEF_TKD(MOM, PEND)                                                                     \
-  hipExtLaunchKernelGGL((k_tk_delta<MOM, PEND>), grid, dim3(kBlock), 0, s, ev.start, nullptr, 0, \
-                        lay, tk, K, lr, mu, g, m, e, sel)
-  if (m != nullptr) {
-    if (pend_in) SAEF_TKD(true, true); else SAEF_TKD(true, false);
-  } else {
-    if (pend_in) SAEF_TKD(false, true); else SAEF_TKD(false, false);
-  }
+                                hipStream_t s, const TkStreams& side, const LaunchEvents& ev) {
+  // The Delta pass of a group of rows is HBM-bound; the selection chain that
+  // follows it (sums, pick, offsets, gather, select, scan, emit) is mostly
+  // launch- and latency-bound.  With a side stream the workers are taken in
+  // two groups: the first group's chain runs on the side stream while the
+  // second group's Delta pass streams on s; s waits for the side stream at
+  // the end.  The groups' scratch rows are disjoint.
+  const bool split = side.stream != nullptr && K >= 2;
+  const int R0 = split ? (K + 1) / 2 : K;
+  const Launcher main{lay, tk, s};
+  const int64_t W = lay.d_pad >> 6;
+  // the first Delta pass stamps the start event, the last kernel on s the stop event
+  auto delta = [&](int R, int row0, hipEvent_t start) -> hipError_t {
+    const dim3 grid((unsigned)(lay.n_tiles * R));
+#define SAEF_TKD(MOM, PEND)                                                                  \
+  hipExtLaunchKernelGGL((k_tk_delta<MOM, PEND>), grid, dim3(kBlock), 0, s, start, nullptr, 0, \
+                        lay, tk, R, row0, lr, mu, g, m, e, sel)
+    if (m != nullptr) {
+      if (pend_in) SAEF_TKD(true, true); else SAEF_TKD(true, false);
+    } else {
+      if (pend_in) SAEF_TKD(false, true); else SAEF_TKD(false, false);
+    }
 #undef SAEF_TKD
-  const hipError_t err = hipGetLastError();
+    return hipGetLastError();
+  };
+  hipError_t err = delta(R0, 0, ev.start);
   if (err != hipSuccess) return err;
-  return Launcher{lay, tk, s}.select_and_emit(K, 0, e, sel, rank, vals, nullptr, pend_out, ev);
+  if (!split) return main.select_and_emit(K, 0, e, sel, rank, vals, nullptr, pend_out, ev);
+  const int R1 = K - R0;
+  if ((err = hipEventRecord(side.fork, s)) != hipSuccess) return err;
+  if ((err = hipStreamWaitEvent(side.stream, side.fork, 0)) != hipSuccess) return err;
+  const Launcher aside{lay, tk, side.stream};
+  if ((err = aside.select_and_emit(R0, 0, e, sel, rank, vals, nullptr, pend_out,
+                                   LaunchEvents())) != hipSuccess)
+    return err;
+  if ((err = hipEventRecord(side.join, side.stream)) != hipSuccess) return err;
+  if ((err = delta(R1, R0, nullptr)) != hipSuccess) return err;
+  if ((err = main.select_and_emit(R1, R0, e + (int64_t)R0 * lay.d_pad, sel + (int64_t)R0 * W,
+                                  rank + (int64_t)R0 * W, vals + (int64_t)R0 * tk.total_keep,
+                                  nullptr, pend_out, ev)) != hipSuccess)
+    return err;
+  return hipStreamWaitEvent(s, side.join, 0);
 }
 
 // Grid: n_tiles * K workgroups; workgroup b sets to 0 the elements of worker
