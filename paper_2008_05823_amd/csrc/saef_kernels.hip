@@ -138,12 +138,15 @@ __device__ __forceinline__ void compress_words(int w0, int count, float lr, floa
   const int lane = lane_id();
   const uint32_t off0 = (uint32_t)(w0 * 64 + lane) * 4u;
   float gv[kU], ev[kU], mv[kU];
-  const u64 ow = kDecode ? buf_ld_words(rs, w0, kU) : 0ull;  // the old words
+  // the old words first (every element waits for them; the scheduling
+  // barrier keeps the compiler from moving the load behind the others)
+  const u64 ow = kDecode ? buf_ld_words(rs, w0, kU) : 0ull;
+  if (kDecode) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
+    mv[u] = kMom ? buf_ld(rm, off0 + 256u * u) : 0.0f;
     gv[u] = buf_ld(rg, off0 + 256u * u);
     ev[u] = buf_ld(re, off0 + 256u * u);
-    mv[u] = kMom ? buf_ld(rm, off0 + 256u * u) : 0.0f;
   }
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
@@ -170,12 +173,11 @@ __device__ __forceinline__ void compress_words(int w0, int count, float lr, floa
 // b / K.  Wave w takes words w*kU .. w*kU+kU-1 of the tile, then strides by
 // 4*kU words.
 template <bool kDecode, bool kMom>
-__global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float lr, float mu,
-                                                     const float* __restrict__ g,
-                                                     float* __restrict__ m,
-                                                     float* __restrict__ e,
-                                                     uint64_t* __restrict__ signs,
-                                                     const float* __restrict__ scales) {
+__device__ __forceinline__ void compress_tile(const DevLayout& lay, int K, float lr, float mu,
+                                              const float* __restrict__ g,
+                                              float* __restrict__ m, float* __restrict__ e,
+                                              uint64_t* __restrict__ signs,
+                                              const float* __restrict__ scales) {
   const unsigned b = blockIdx.x;
   const int k = (int)(b % (unsigned)K);
   const int64_t ti = b / (unsigned)K;
@@ -204,6 +206,27 @@ __global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float
   }
   acc.finish(lo, hi, bad);
   block_partial(lay, k, ti, lo, hi, bad);
+}
+
+template <bool kDecode>
+__global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float lr, float mu,
+                                                     const float* __restrict__ g,
+                                                     float* __restrict__ m,
+                                                     float* __restrict__ e,
+                                                     uint64_t* __restrict__ signs,
+                                                     const float* __restrict__ scales) {
+  compress_tile<kDecode, false>(lay, K, lr, mu, g, m, e, signs, scales);
+}
+
+// With momentum (three streams in, two out) at most 5 waves per SIMD: 672
+// against 696 us at 8 waves (resnet50, K = 8); the sign kernel prefers 8
+// (400 against 406 us).
+template <bool kDecode>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(1, 5))) void
+k_compress_mom(DevLayout lay, int K, float lr, float mu, const float* __restrict__ g,
+               float* __restrict__ m, float* __restrict__ e, uint64_t* __restrict__ signs,
+               const float* __restrict__ scales) {
+  compress_tile<kDecode, true>(lay, K, lr, mu, g, m, e, signs, scales);
 }
 
 // ------------------------------------------------------------------ finalize
@@ -274,7 +297,10 @@ __global__ __launch_bounds__(kBlock) void k_finalize2(DevLayout lay, int server,
 // ragged tail needs no guards): x^(k)_{t+1/2} = x_t - e^(k)_t with the
 // pending corrections of x and e applied on the fly (kHasE false: x_t
 // itself, the evaluation point of local error feedback).
-template <bool kDecX, int kDecE, bool kHasE>
+// kFull: all kU words lie inside the tile (their sign words are read
+// unconditionally, in one scalar load per buffer; a guarded load per word
+// costs a branch and a wait each).
+template <bool kDecX, int kDecE, bool kHasE, bool kFull>
 __device__ __forceinline__ void step_words(int w0, int nw, Buf rx, Buf re, Buf rh,
                                            const uint64_t* __restrict__ sx,
                                            const uint64_t* __restrict__ se, const Corr& c_x,
@@ -285,7 +311,7 @@ __device__ __forceinline__ void step_words(int w0, int nw, Buf rx, Buf re, Buf r
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
     const uint32_t off = off0 + 256u * u;
-    const bool wok = w0 + u < nw;  // wave-uniform: the tile's words only
+    const bool wok = kFull || w0 + u < nw;  // wave-uniform: the tile's words only
     xv[u] = kHasE ? buf_ld_cached(rx, off) : buf_ld(rx, off);
     ev[u] = kHasE ? buf_ld(re, off) : 0.0f;
     mx[u] = (kDecX && wok) ? ld_word_ro(sx + w0 + u) : 0ull;
@@ -332,8 +358,12 @@ __global__ __launch_bounds__(kBlock) void k_step(DevLayout lay, int K, const flo
   const uint64_t* se = kDecE != kDecPlain ? signs + (int64_t)k * (d_pad >> 6) + gw0 : nullptr;
   const Corr c_e(kDecE == kDecSign ? scales[(int64_t)k * lay.L + tile.l] : 0.0f);
   const Corr c_x(kDecX ? sscales[tile.l] : 0.0f);
-  for (int w0 = wave * kU; w0 < nw; w0 += kWaves * kU)
-    step_words<kDecX, kDecE, kHasE>(w0, nw, rx, re, rh, sx, se, c_x, c_e);
+  for (int w0 = wave * kU; w0 < nw; w0 += kWaves * kU) {
+    if (w0 + kU <= nw)
+      step_words<kDecX, kDecE, kHasE, true>(w0, nw, rx, re, rh, sx, se, c_x, c_e);
+    else
+      step_words<kDecX, kDecE, kHasE, false>(w0, nw, rx, re, rh, sx, se, c_x, c_e);
+  }
 }
 
 // ------------------------------------------------------------------ step ahead with averaging
@@ -940,12 +970,12 @@ hipError_t launch_compress(const DevLayout& lay, int K, float lr, float mu, cons
                            float* m, float* e, uint64_t* signs, const float* scales, bool decode,
                            hipStream_t s, const LaunchEvents& ev) {
   const dim3 grid((unsigned)(lay.n_tiles * K));
-#define SAEF_CMP(D, M) \
-  SAEF_LAUNCH((k_compress<D, M>), grid, dim3(kBlock), 0, s, lay, K, lr, mu, g, m, e, signs, scales)
+#define SAEF_CMP(KERNEL, D) \
+  SAEF_LAUNCH((KERNEL<D>), grid, dim3(kBlock), 0, s, lay, K, lr, mu, g, m, e, signs, scales)
   if (m != nullptr) {
-    if (decode) SAEF_CMP(true, true); else SAEF_CMP(false, true);
+    if (decode) SAEF_CMP(k_compress_mom, true); else SAEF_CMP(k_compress_mom, false);
   } else {
-    if (decode) SAEF_CMP(true, false); else SAEF_CMP(false, false);
+    if (decode) SAEF_CMP(k_compress, true); else SAEF_CMP(k_compress, false);
   }
 #undef SAEF_CMP
   return hipGetLastError();
