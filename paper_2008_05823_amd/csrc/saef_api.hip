@@ -125,7 +125,8 @@ int check_common(const saef_layout* lay, int32_t K) {
   if (K < 1 || K > lay->k_max) return SAEF_EINVAL;
   // the per-(tile, worker) grids (tiles rounded up to whole groups of runs)
   // must fit the launch limit
-  if (saef::run_padded_tiles(lay->dev.n_tiles) * (int64_t)K > kMaxGrid) return SAEF_EINVAL;
+  if (saef::run_padded_tiles(lay->dev.n_tiles * saef::kStepSplit) * (int64_t)K > kMaxGrid)
+    return SAEF_EINVAL;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess) return SAEF_EHIP;
   if (dev != lay->device) return SAEF_EINVAL;

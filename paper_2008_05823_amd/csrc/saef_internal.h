@@ -14,9 +14,16 @@ constexpr int kWaves = kBlock / kWave;
 #define SAEF_TILE_ELEMS 2048
 #endif
 constexpr int kTileElems = SAEF_TILE_ELEMS;  // default work tile (elements, multiple of 64)
-constexpr int kMaxTilesPerTensor = 1 << 17;  // 2048-element tiles up to 2^28 elements
-constexpr int kFinChunk = 4096;              // tile partials per finalize workgroup
+static_assert((SAEF_TILE_ELEMS & (SAEF_TILE_ELEMS - 1)) == 0 && SAEF_TILE_ELEMS >= 64,
+              "the tile size is a power of two of at least one sign word");
 constexpr int64_t kMaxTensor = int64_t(1) << 28;
+constexpr int kMaxTilesPerTensor = (int)(kMaxTensor / kTileElems);  // tiles of a maximal tensor
+constexpr int kFinChunk = 4096;              // tile partials per finalize workgroup
+// The step ahead keeps no per-tile sums, so it takes a tile in work units of
+// kStepElems elements, one workgroup each (1024-element units stream faster
+// than whole 2048-element tiles).
+constexpr int kStepElems = kTileElems < 1024 ? kTileElems : 1024;
+constexpr int kStepSplit = kTileElems / kStepElems;  // units per tile
 constexpr int kXcds = 8;  // MI355X: 8 XCDs, workgroups dealt round-robin
 
 // XCD-aware tile order.  Workgroups are dealt to the 8 XCDs round-robin

@@ -32,10 +32,35 @@
 namespace saef {
 namespace {
 
-// Words per wave per pass in the per-(tile, worker) kernels: 8, so that the
-// four waves cover a 2048-element tile in one pass (momentum compression
-// 727 -> 677 us at resnet50 K = 8 against 4 words; the sign kernels gain 1%).
-constexpr int kU = 8;
+// Workgroup shapes.  The compression and the server (and the stream probe,
+// which measures the compression's pattern) take a 2048-element tile with
+// kSWaves waves of kU words per pass; the step ahead with kTWaves waves of
+// kTU words.  Each wave of the compression and the server ends with a
+// 128-bit wave reduction of its exact sum, so fewer, longer waves suit them.
+#ifndef SAEF_STREAM_WAVES
+#define SAEF_STREAM_WAVES 4
+#endif
+#ifndef SAEF_STREAM_WORDS
+#define SAEF_STREAM_WORDS 8
+#endif
+#ifndef SAEF_STEP_WAVES
+#define SAEF_STEP_WAVES 4
+#endif
+#ifndef SAEF_STEP_WORDS
+#define SAEF_STEP_WORDS 4
+#endif
+constexpr int kSWaves = SAEF_STREAM_WAVES;
+constexpr int kSBlock = kSWaves * kWave;
+constexpr int kU = SAEF_STREAM_WORDS;
+constexpr int kTWaves = SAEF_STEP_WAVES;
+constexpr int kTBlock = kTWaves * kWave;
+constexpr int kTU = SAEF_STEP_WORDS;
+// The step ahead's work unit (kStepElems elements of a tile) is one pass of
+// its workgroup: 1024-element units of 4 waves x 4 words against whole
+// 2048-element tiles of 4 x 8: 276-286 against 288-292 us at resnet50
+// K = 8, 2951 against 3016-3026 us at 2^28 parameters.
+static_assert(kTWaves * kTU * 64 <= kStepElems && kStepElems % (kTWaves * kTU * 64) == 0,
+              "a step unit is whole passes of the workgroup");
 // Words per wave per pass in the averaging kernel (it keeps kAvgChunk * kUA
 // errors and sign words live; 8 was 2% slower).
 constexpr int kUA = 4;
@@ -103,10 +128,11 @@ __device__ float scale_from_sum(u64 hi, u64 lo, int64_t n) {
 
 
 // Stores the exact partial of (row, tile) summed over the workgroup.
+template <int kNW>
 __device__ void block_partial(const DevLayout& lay, int row, int64_t tile, u64 lo, u64 hi,
                               bool bad) {
-  __shared__ u64 s_lo[kWaves];
-  __shared__ u64 s_hi[kWaves];
+  __shared__ u64 s_lo[kNW];
+  __shared__ u64 s_hi[kNW];
   wave_sum128(lo, hi);
   const int w = threadIdx.x / kWave;
   if (lane_id() == 0) {
@@ -116,7 +142,7 @@ __device__ void block_partial(const DevLayout& lay, int row, int64_t tile, u64 l
   const int any_bad = __syncthreads_or(bad ? 1 : 0);
   if (threadIdx.x != 0) return;
   u64 tlo = 0, thi = 0;
-  for (int i = 0; i < kWaves; ++i) add128(tlo, thi, s_lo[i], s_hi[i]);
+  for (int i = 0; i < kNW; ++i) add128(tlo, thi, s_lo[i], s_hi[i]);
   u64* p = lay.part + ((int64_t)row * lay.n_tiles + tile) * 2;
   p[0] = tlo;
   p[1] = thi;
@@ -196,7 +222,7 @@ __device__ __forceinline__ void compress_tile(const DevLayout& lay, int K, float
   ExactSum acc;
   u64 lo = 0, hi = 0;
   bool bad = false;
-  for (int w0 = wave * kU; w0 < nw; w0 += kWaves * kU) {
+  for (int w0 = wave * kU; w0 < nw; w0 += kSWaves * kU) {
     if ((w0 + kU) * 64 <= tile.count) {
       compress_words<kDecode, kMom, true>(w0, tile.count, lr, mu, rg, rm, re, rs, c_old, acc);
     } else {
@@ -205,11 +231,11 @@ __device__ __forceinline__ void compress_tile(const DevLayout& lay, int K, float
     acc.added(kU, lo, hi, bad);
   }
   acc.finish(lo, hi, bad);
-  block_partial(lay, k, ti, lo, hi, bad);
+  block_partial<kSWaves>(lay, k, ti, lo, hi, bad);
 }
 
 template <bool kDecode>
-__global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float lr, float mu,
+__global__ __launch_bounds__(kSBlock) void k_compress(DevLayout lay, int K, float lr, float mu,
                                                      const float* __restrict__ g,
                                                      float* __restrict__ m,
                                                      float* __restrict__ e,
@@ -222,7 +248,7 @@ __global__ __launch_bounds__(kBlock) void k_compress(DevLayout lay, int K, float
 // against 696 us at 8 waves (resnet50, K = 8); the sign kernel prefers 8
 // (400 against 406 us).
 template <bool kDecode>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(1, 5))) void
+__global__ __launch_bounds__(kSBlock) __attribute__((amdgpu_waves_per_eu(1, 5))) void
 k_compress_mom(DevLayout lay, int K, float lr, float mu, const float* __restrict__ g,
                float* __restrict__ m, float* __restrict__ e, uint64_t* __restrict__ signs,
                const float* __restrict__ scales) {
@@ -292,12 +318,12 @@ __global__ __launch_bounds__(kBlock) void k_finalize2(DevLayout lay, int server,
 }
 
 // ------------------------------------------------------------------ step ahead
-// kU words of one worker's tile starting at word w0 (offsets relative to the
+// kTU words of one worker's tile starting at word w0 (offsets relative to the
 // tile; buffer resources over the tile's elements and sign words, so the
 // ragged tail needs no guards): x^(k)_{t+1/2} = x_t - e^(k)_t with the
 // pending corrections of x and e applied on the fly (kHasE false: x_t
 // itself, the evaluation point of local error feedback).
-// kFull: all kU words lie inside the tile (their sign words are read
+// kFull: all kTU words lie inside the tile (their sign words are read
 // unconditionally, in one scalar load per buffer; a guarded load per word
 // costs a branch and a wait each).
 template <bool kDecX, int kDecE, bool kHasE, bool kFull>
@@ -306,10 +332,10 @@ __device__ __forceinline__ void step_words(int w0, int nw, Buf rx, Buf re, Buf r
                                            const uint64_t* __restrict__ se, const Corr& c_x,
                                            const Corr& c_e) {
   const uint32_t off0 = (uint32_t)(w0 * 64 + lane_id()) * 4u;
-  float xv[kU], ev[kU];
-  u64 mx[kU], me[kU];
+  float xv[kTU], ev[kTU];
+  u64 mx[kTU], me[kTU];
 #pragma unroll
-  for (int u = 0; u < kU; ++u) {
+  for (int u = 0; u < kTU; ++u) {
     const uint32_t off = off0 + 256u * u;
     const bool wok = kFull || w0 + u < nw;  // wave-uniform: the tile's words only
     xv[u] = kHasE ? buf_ld_cached(rx, off) : buf_ld(rx, off);
@@ -318,7 +344,7 @@ __device__ __forceinline__ void step_words(int w0, int nw, Buf rx, Buf re, Buf r
     me[u] = (kDecE != kDecPlain && wok) ? ld_word_ro(se + w0 + u) : 0ull;
   }
 #pragma unroll
-  for (int u = 0; u < kU; ++u) {
+  for (int u = 0; u < kTU; ++u) {
     float xc = xv[u], ec = ev[u];
     if (kDecX) xc = xc - c_x(mx[u]);  // x_t = x_{t-1} - C(Delta_t)
     if (kDecE == kDecSign) ec = ec - c_e(me[u]);  // e_t = Delta - C(Delta)
@@ -327,39 +353,47 @@ __device__ __forceinline__ void step_words(int w0, int nw, Buf rx, Buf re, Buf r
   }
 }
 
-// Grid: run_padded_tiles(n_tiles) * K workgroups, one per (tile, worker), in
-// the XCD-aware tile order of run_tile_of: the K workers of a run of tiles
-// follow one another on one XCD, so x is fetched from HBM once and re-read
-// from that XCD's L2.  x itself is not written: the pending re-update of x
-// is applied here on the fly and materialized by the aggregate kernel.
+// Grid: run_padded_tiles(n_tiles kStepSplit) * K workgroups, one per (work
+// unit, worker), in the XCD-aware order of run_tile_of over the units: the K
+// workers of a run of units follow one another on one XCD, so x is fetched
+// from HBM once and re-read from that XCD's L2.  x itself is not written:
+// the pending re-update of x is applied here on the fly and materialized by
+// the aggregate kernel.
 // kHasE false (K = 1, e unused): xh = x_t.
 template <bool kDecX, int kDecE, bool kHasE>
-__global__ __launch_bounds__(kBlock) void k_step(DevLayout lay, int K, const float* __restrict__ x,
+__global__ __launch_bounds__(kTBlock) void k_step(DevLayout lay, int K, const float* __restrict__ x,
                                                  const uint64_t* __restrict__ ss,
                                                  const float* __restrict__ sscales,
                                                  const float* __restrict__ e,
                                                  const uint64_t* __restrict__ signs,
                                                  const float* __restrict__ scales,
                                                  float* __restrict__ xh) {
+  // work unit: kStepElems elements of a tile (the step ahead keeps no
+  // per-tile sums, so its units need not be whole tiles)
   int k;
-  int64_t ti;
-  run_tile_of(blockIdx.x, K, tile_run_shift(lay.n_tiles), k, ti);
-  if (ti >= lay.n_tiles) return;
-  const Tile tile = lay.tiles[ti];
+  int64_t unit;
+  const int64_t n_units = lay.n_tiles * kStepSplit;
+  run_tile_of(blockIdx.x, K, tile_run_shift(n_units), k, unit);
+  if (unit >= n_units) return;
+  const Tile tile = lay.tiles[unit / kStepSplit];
+  const int part = (int)(unit % kStepSplit);
+  const int count = min(tile.count - part * kStepElems, kStepElems);
+  if (count <= 0) return;  // a short tile's empty part
+  const int64_t start = tile.start + (int64_t)part * kStepElems;
   const int wave = wave_id();
   const int64_t d_pad = lay.d_pad;
-  const int64_t gw0 = tile.start >> 6;
-  const int nw = (tile.count + 63) >> 6;
-  const uint32_t nbytes = (uint32_t)tile.count * 4u;
-  const Buf rx = buf_of(x + tile.start, nbytes);
-  const Buf re = buf_of(kHasE ? e + (int64_t)k * d_pad + tile.start : x + tile.start, nbytes);
-  const Buf rh = buf_of(xh + (int64_t)k * d_pad + tile.start, nbytes);
+  const int64_t gw0 = start >> 6;
+  const int nw = (count + 63) >> 6;
+  const uint32_t nbytes = (uint32_t)count * 4u;
+  const Buf rx = buf_of(x + start, nbytes);
+  const Buf re = buf_of(kHasE ? e + (int64_t)k * d_pad + start : x + start, nbytes);
+  const Buf rh = buf_of(xh + (int64_t)k * d_pad + start, nbytes);
   const uint64_t* sx = kDecX ? ss + gw0 : nullptr;
   const uint64_t* se = kDecE != kDecPlain ? signs + (int64_t)k * (d_pad >> 6) + gw0 : nullptr;
   const Corr c_e(kDecE == kDecSign ? scales[(int64_t)k * lay.L + tile.l] : 0.0f);
   const Corr c_x(kDecX ? sscales[tile.l] : 0.0f);
-  for (int w0 = wave * kU; w0 < nw; w0 += kWaves * kU) {
-    if (w0 + kU <= nw)
+  for (int w0 = wave * kTU; w0 < nw; w0 += kTWaves * kTU) {
+    if (w0 + kTU <= nw)
       step_words<kDecX, kDecE, kHasE, true>(w0, nw, rx, re, rh, sx, se, c_x, c_e);
     else
       step_words<kDecX, kDecE, kHasE, false>(w0, nw, rx, re, rh, sx, se, c_x, c_e);
@@ -559,7 +593,7 @@ __device__ __forceinline__ void aggregate_pass(int K, double inv_k, int L, int l
 // w*kU .. w*kU+kU-1 of the tile (one pass over a whole tile), then strides by
 // 4*kU words.
 template <int kMode, bool kDecode, bool kAvg>
-__global__ __launch_bounds__(kBlock) void k_aggregate(DevLayout lay, int K, double inv_k,
+__global__ __launch_bounds__(kSBlock) void k_aggregate(DevLayout lay, int K, double inv_k,
                                                       const uint64_t* __restrict__ signs,
                                                       const float* __restrict__ scales,
                                                       float* __restrict__ avg,
@@ -581,7 +615,7 @@ __global__ __launch_bounds__(kBlock) void k_aggregate(DevLayout lay, int K, doub
   ExactSum acc;
   u64 lo = 0, hi = 0;
   bool bad = false;
-  for (int w0 = wave_id() * kU; w0 < nw; w0 += kWaves * kU) {
+  for (int w0 = wave_id() * kU; w0 < nw; w0 += kSWaves * kU) {
     if ((w0 + kU) * 64 <= tile.count) {
       aggregate_pass<kMode, kDecode, kAvg, true>(K, inv_k, lay.L, tile.l, W, w0, tile.count,
                                                  signs + gw0, scales, ravg, res, rss, c_old, rx,
@@ -595,7 +629,7 @@ __global__ __launch_bounds__(kBlock) void k_aggregate(DevLayout lay, int K, doub
   }
   if (kMode == 1) {
     acc.finish(lo, hi, bad);
-    block_partial(lay, lay.k_max, ti, lo, hi, bad);
+    block_partial<kSWaves>(lay, lay.k_max, ti, lo, hi, bad);
   }
 }
 
@@ -935,7 +969,7 @@ __global__ __launch_bounds__(kBlock) void k_mfinalize2(DevLayout lay, int K,
 // The HBM ceiling of the worker compression's access pattern: c = a + b over
 // n elements (2 reads + 1 write of fp32), one 256-thread workgroup per
 // 2048-element tile, kU words per wave, non-temporal buffer accesses.
-__global__ __launch_bounds__(kBlock) void k_stream_probe(const float* __restrict__ a,
+__global__ __launch_bounds__(kSBlock) void k_stream_probe(const float* __restrict__ a,
                                                          const float* __restrict__ b,
                                                          float* __restrict__ c, int64_t n) {
   const int64_t start = (int64_t)blockIdx.x * kTileElems;
@@ -943,7 +977,7 @@ __global__ __launch_bounds__(kBlock) void k_stream_probe(const float* __restrict
   const Buf ra = buf_of(a + start, nbytes);
   const Buf rb = buf_of(b + start, nbytes);
   const Buf rc = buf_of(c + start, nbytes);
-  for (int w0 = wave_id() * kU; w0 * 256u < nbytes; w0 += kWaves * kU) {
+  for (int w0 = wave_id() * kU; w0 * 256u < nbytes; w0 += kSWaves * kU) {
     const uint32_t off0 = (uint32_t)(w0 * 64 + lane_id()) * 4u;
     float av[kU], bv[kU];
 #pragma unroll
@@ -962,7 +996,7 @@ hipError_t launch_stream_probe(const float* a, const float* b, float* c, int64_t
                                hipStream_t s) {
   const LaunchEvents ev;
   const dim3 grid((unsigned)((n + kTileElems - 1) / kTileElems));
-  SAEF_LAUNCH(k_stream_probe, grid, dim3(kBlock), 0, s, a, b, c, n);
+  SAEF_LAUNCH(k_stream_probe, grid, dim3(kSBlock), 0, s, a, b, c, n);
   return hipGetLastError();
 }
 
@@ -971,7 +1005,7 @@ hipError_t launch_compress(const DevLayout& lay, int K, float lr, float mu, cons
                            hipStream_t s, const LaunchEvents& ev) {
   const dim3 grid((unsigned)(lay.n_tiles * K));
 #define SAEF_CMP(KERNEL, D) \
-  SAEF_LAUNCH((KERNEL<D>), grid, dim3(kBlock), 0, s, lay, K, lr, mu, g, m, e, signs, scales)
+  SAEF_LAUNCH((KERNEL<D>), grid, dim3(kSBlock), 0, s, lay, K, lr, mu, g, m, e, signs, scales)
   if (m != nullptr) {
     if (decode) SAEF_CMP(k_compress_mom, true); else SAEF_CMP(k_compress_mom, false);
   } else {
@@ -1005,7 +1039,7 @@ hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_
   const dim3 grid((unsigned)lay.n_tiles);
   const double ik = inv_pow2(K);
 #define SAEF_AGG(M, D, A)                                                                  \
-  SAEF_LAUNCH((k_aggregate<M, D, A>), grid, dim3(kBlock), 0, s, lay, K, ik, signs, \
+  SAEF_LAUNCH((k_aggregate<M, D, A>), grid, dim3(kSBlock), 0, s, lay, K, ik, signs, \
                      scales, avg, e_srv, srv_signs, srv_scales, x)
   const bool a = avg != nullptr;
   if (mode == 1) {
@@ -1050,9 +1084,9 @@ hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
 #undef SAEF_AV
   } else {
     if (xh == nullptr) return hipErrorInvalidValue;
-    const dim3 grid((unsigned)(run_padded_tiles(lay.n_tiles) * K));
+    const dim3 grid((unsigned)(run_padded_tiles(lay.n_tiles * kStepSplit) * K));
 #define SAEF_ST(DX, DE)                                                                \
-  SAEF_LAUNCH((k_step<DX, DE, true>), grid, dim3(kBlock), 0, s, lay, K, x, srv_signs, \
+  SAEF_LAUNCH((k_step<DX, DE, true>), grid, dim3(kTBlock), 0, s, lay, K, x, srv_signs, \
                      srv_scales, e, signs, scales, xh)
     if (decode_x) {
       SAEF_ST(true, kDecSign);
@@ -1071,12 +1105,12 @@ hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
 hipError_t launch_weights(const DevLayout& lay, const float* x, const uint64_t* srv_signs,
                           const float* srv_scales, bool decode_x, float* xh, hipStream_t s,
                           const LaunchEvents& ev) {
-  const dim3 grid((unsigned)run_padded_tiles(lay.n_tiles));
+  const dim3 grid((unsigned)run_padded_tiles(lay.n_tiles * kStepSplit));
   if (decode_x) {
-    SAEF_LAUNCH((k_step<true, kDecPlain, false>), grid, dim3(kBlock), 0, s, lay, 1, x, srv_signs,
+    SAEF_LAUNCH((k_step<true, kDecPlain, false>), grid, dim3(kTBlock), 0, s, lay, 1, x, srv_signs,
                 srv_scales, nullptr, nullptr, nullptr, xh);
   } else {
-    SAEF_LAUNCH((k_step<false, kDecPlain, false>), grid, dim3(kBlock), 0, s, lay, 1, x, srv_signs,
+    SAEF_LAUNCH((k_step<false, kDecPlain, false>), grid, dim3(kTBlock), 0, s, lay, 1, x, srv_signs,
                 srv_scales, nullptr, nullptr, nullptr, xh);
   }
   return hipGetLastError();

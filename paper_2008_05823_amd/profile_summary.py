@@ -34,12 +34,22 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = [os.path.join(HERE, "csrc", f)
                   for f in ("saef_kernels.hip", "saef_internal.h", "saef_device.h")]
 
+_COMMENT = re.compile(r"//[^\n]*|/\*.*?\*/", re.S)
+
+
+def code_tokens(text: str) -> str:
+    """The source without its comments, whitespace runs collapsed: what the
+    compiler sees, so that editing a comment keeps the hash.  (No string
+    literal in these sources holds a comment opener.)"""
+    return " ".join(_COMMENT.sub(" ", text).split())
+
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
     for path in KERNEL_SOURCES:
-        with open(path, "rb") as fh:
-            h.update(fh.read())
+        with open(path, encoding="utf-8") as fh:
+            h.update(code_tokens(fh.read()).encode())
+            h.update(b"\0")
     return h.hexdigest()[:16]
 
 
