@@ -110,17 +110,20 @@ def host_cpu_model() -> str:
     return "unknown"
 
 
-def stream_probe_gbps(n: int, reps: int = 10) -> float:
-    """GB/s of the library's stream probe (c = a + b over n fp32 elements: 2
-    reads + 1 write, the worker compression's access pattern) -- the HBM
-    ceiling the roofline fraction is also given against."""
+def stream_probe_gbps(n: int, reps: int = 10, in_place_copy: bool = False) -> float:
+    """GB/s of the library's stream probe: c = a + b over n fp32 elements (2
+    reads + 1 write, the worker compression's access pattern: the HBM ceiling
+    the roofline fraction is also given against), or with in_place_copy
+    a = a (1 read + 1 write in place, the server step's streams)."""
     import torch
     from paper_2008_05823_amd import saef
     a = torch.empty(n, dtype=torch.float32, device="cuda")
-    b = torch.empty_like(a)
-    c = torch.empty_like(a)
     a.fill_(1.0)
-    b.fill_(2.0)
+    if in_place_copy:
+        b, c, nbytes = None, a, 8 * n
+    else:
+        b, c, nbytes = torch.empty_like(a), torch.empty_like(a), 12 * n
+        b.fill_(2.0)
     for _ in range(2):
         saef.saef_stream_probe(a, b, c)
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -131,7 +134,7 @@ def stream_probe_gbps(n: int, reps: int = 10) -> float:
     torch.cuda.synchronize()
     ms = s.elapsed_time(e) / reps
     del a, b, c
-    return 12 * n / (ms * 1e-3) / 1e9
+    return nbytes / (ms * 1e-3) / 1e9
 
 
 def main() -> int:
@@ -326,6 +329,9 @@ def main() -> int:
     # the HBM ceiling of the dominant kernel's pattern: as many elements as
     # the compression streams per launch (K rows of d_pad)
     probe = None if args.no_probe else round(stream_probe_gbps(K * d_pad), 1)
+    # and of the server step's: its error and weight rows, read and written in place
+    probe_1r1w = None if args.no_probe else round(stream_probe_gbps(2 * d_pad,
+                                                                    in_place_copy=True), 1)
 
     out = {
         "metric": METRIC,
@@ -361,6 +367,7 @@ def main() -> int:
         "kernels": kernels,
         "kernels_note": "per-kernel averages from a second pass with every dispatch timed",
         "stream_probe_gbps": probe,
+        "stream_probe_1r1w_gbps": probe_1r1w,
         "roofline": {"bound": "hbm",
                      "kernel": "compress" if topk is None else "topk_compress (all passes)",
                      "achieved": c_gbps,

@@ -343,7 +343,10 @@ int saef_round_noalloc(const saef_layout* layout, int64_t t, int64_t period, int
  * pattern the worker compression uses.  c[i] = a[i] + b[i] for i < n (two
  * fp32 reads and one fp32 write per element, 12 bytes), one 256-thread
  * workgroup per 2048-element tile, non-temporal accesses.  a, b, c: device
- * arrays of n floats, c must not overlap a or b (SAEF_EINVAL); n >= 1. */
+ * arrays of n floats, c must not overlap a or b (SAEF_EINVAL); n >= 1.
+ * b may be NULL: then c[i] = a[i] (one read and one write, 8 bytes), and c
+ * may also be a itself (in place: the pattern of the server step's error
+ * and weight streams); a partial overlap of c and a is SAEF_EINVAL. */
 int saef_stream_probe(const float* a, const float* b, float* c, int64_t n, hipStream_t stream);
 
 /* Host-side query of a layout: tensor count, padded length, worker limit and

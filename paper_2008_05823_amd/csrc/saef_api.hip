@@ -638,9 +638,10 @@ int saef_profile_enable(saef_layout* layout, int32_t capacity, uint32_t kind_mas
 int saef_stream_probe(const float* a, const float* b, float* c, int64_t n,
                       hipStream_t stream) {
   if (n < 1 || n > (int64_t)saef::kTileElems * 2147483647) return SAEF_EINVAL;
-  if (!f32_ok(a) || !f32_ok(b) || !f32_ok(c)) return SAEF_EINVAL;
+  if (!f32_ok(a) || (b != nullptr && !f32_ok(b)) || !f32_ok(c)) return SAEF_EINVAL;
   const size_t vb = (size_t)n * sizeof(float);
-  if (overlap(c, vb, a, vb) || overlap(c, vb, b, vb)) return SAEF_EINVAL;
+  if (b != nullptr && (overlap(c, vb, a, vb) || overlap(c, vb, b, vb))) return SAEF_EINVAL;
+  if (b == nullptr && c != a && overlap(c, vb, a, vb)) return SAEF_EINVAL;
   return hip_rc(saef::launch_stream_probe(a, b, c, n, stream));
 }
 

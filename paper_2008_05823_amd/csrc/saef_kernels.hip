@@ -509,7 +509,30 @@ __global__ __launch_bounds__(kBlock) void k_step_average(DevLayout lay, int K, d
 }
 
 // ------------------------------------------------------------------ aggregate
-constexpr int kAggChunk = 2;  // workers whose sign words are loaded together
+constexpr int kAggGroup = 64 / kU;  // workers whose sign words one vector load brings
+
+// The sign words of workers k0 .. k0 + kAggGroup - 1 for a pass of a wave
+// over the kU words starting at w0 (lane i: word w0 + i mod kU of worker
+// k0 + i / kU; 0 past K or past the tile), and their scales (lane c: the
+// scale of worker k0 + c): one vector load each, read out with v_readlane.
+struct AggGroup {
+  u64 words;
+  float sc;
+};
+template <bool kFull>
+__device__ __forceinline__ AggGroup agg_group_load(int k0, int K, int L, int l, int64_t W,
+                                                   int w0, int count,
+                                                   const uint64_t* __restrict__ sw,
+                                                   const float* __restrict__ scales) {
+  const int lane = lane_id();
+  const int kl = k0 + lane / kU, ul = lane % kU;
+  AggGroup g;
+  g.words = 0ull;
+  if (kl < K && (kFull || (w0 + ul) * 64 < count)) g.words = sw[(int64_t)kl * W + w0 + ul];
+  g.sc = 0.0f;
+  if (lane < kAggGroup && k0 + lane < K) g.sc = scales[(int64_t)(k0 + lane) * L + l];
+  return g;
+}
 // One pass of a wave over the kU words starting at word w0 of a tile (offsets
 // relative to the tile; buffer resources over the tile's elements and server
 // words): the K worker messages are decoded in order, mean = (sum_k +-scale_k
@@ -526,6 +549,11 @@ __device__ __forceinline__ void aggregate_pass(int K, double inv_k, int L, int l
   const int lane = lane_id();
   const uint32_t off0 = (uint32_t)(w0 * 64 + lane) * 4u;
   constexpr bool kUpdX = kMode == 0 || kDecode;  // x is read and written
+  // the first group's words and scales go out before the element loads, so
+  // that waiting for them (vector loads complete in order) does not wait for
+  // the elements
+  AggGroup grp = agg_group_load<kFull>(0, K, L, l, W, w0, count, sw, scales);
+  __builtin_amdgcn_sched_barrier(0);
   float ev[kU], xv[kU];
   const u64 mo = (kMode == 1 && kDecode) ? buf_ld_words(rss, w0, kU) : 0ull;  // old words
 #pragma unroll
@@ -536,31 +564,21 @@ __device__ __forceinline__ void aggregate_pass(int K, double inv_k, int L, int l
   double acc_m[kU];
 #pragma unroll
   for (int u = 0; u < kU; ++u) acc_m[u] = 0.0;
-  // workers in chunks of kAggChunk: the chunk's scales and sign words are all
-  // loaded (a worker past K reloads worker K - 1) before the first is used;
-  // the tail pass reads only the tile's words (wave-uniform conditions)
-  for (int k0 = 0; k0 < K; k0 += kAggChunk) {
-    float sc[kAggChunk];
-    u64 m[kAggChunk][kU];
+  for (int k0 = 0; k0 < K; k0 += kAggGroup) {
+    if (k0 > 0) grp = agg_group_load<kFull>(k0, K, L, l, W, w0, count, sw, scales);
 #pragma unroll
-    for (int c = 0; c < kAggChunk; ++c) {
-      const int k = min(k0 + c, K - 1);
-      sc[c] = scales[(int64_t)k * L + l];
-      const uint64_t* sk = sw + (int64_t)k * W + w0;
-#pragma unroll
-      for (int u = 0; u < kU; ++u) m[c][u] = (kFull || (w0 + u) * 64 < count) ? sk[u] : 0ull;
-    }
-#pragma unroll
-    for (int c = 0; c < kAggChunk; ++c) {
+    for (int c = 0; c < kAggGroup; ++c) {
       if (k0 + c >= K) break;  // wave-uniform
       // +-scale_k in binary64: the two values differ only in the sign bit
-      const double sd = (double)sc[c];
+      const double sd =
+          (double)__uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(grp.sc), c));
       const uint32_t pos_hi = (uint32_t)__double2hiint(sd);
       const uint32_t lo_bits = (uint32_t)__double2loint(sd);
       const uint32_t neg_hi = pos_hi ^ 0x80000000u;
 #pragma unroll
       for (int u = 0; u < kU; ++u)
-        acc_m[u] += __hiloint2double((int)sel_by_bit(m[c][u], pos_hi, neg_hi), (int)lo_bits);
+        acc_m[u] += __hiloint2double(
+            (int)sel_by_bit(word_of(grp.words, c * kU + u), pos_hi, neg_hi), (int)lo_bits);
     }
   }
 #pragma unroll
@@ -969,13 +987,16 @@ __global__ __launch_bounds__(kBlock) void k_mfinalize2(DevLayout lay, int K,
 // The HBM ceiling of the worker compression's access pattern: c = a + b over
 // n elements (2 reads + 1 write of fp32), one 256-thread workgroup per
 // 2048-element tile, kU words per wave, non-temporal buffer accesses.
-__global__ __launch_bounds__(kSBlock) void k_stream_probe(const float* __restrict__ a,
+// kTwo: c = a + b; else c = a (c may be a: every element is read and then
+// written by the same lane, so a and c are not restrict-qualified).
+template <bool kTwo>
+__global__ __launch_bounds__(kSBlock) void k_stream_probe(const float* a,
                                                          const float* __restrict__ b,
-                                                         float* __restrict__ c, int64_t n) {
+                                                         float* c, int64_t n) {
   const int64_t start = (int64_t)blockIdx.x * kTileElems;
   const uint32_t nbytes = (uint32_t)min((int64_t)kTileElems, n - start) * 4u;
   const Buf ra = buf_of(a + start, nbytes);
-  const Buf rb = buf_of(b + start, nbytes);
+  const Buf rb = buf_of(kTwo ? b + start : a + start, nbytes);
   const Buf rc = buf_of(c + start, nbytes);
   for (int w0 = wave_id() * kU; w0 * 256u < nbytes; w0 += kSWaves * kU) {
     const uint32_t off0 = (uint32_t)(w0 * 64 + lane_id()) * 4u;
@@ -983,10 +1004,10 @@ __global__ __launch_bounds__(kSBlock) void k_stream_probe(const float* __restric
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
       av[u] = buf_ld(ra, off0 + 256u * u);
-      bv[u] = buf_ld(rb, off0 + 256u * u);
+      bv[u] = kTwo ? buf_ld(rb, off0 + 256u * u) : 0.0f;
     }
 #pragma unroll
-    for (int u = 0; u < kU; ++u) buf_st(rc, off0 + 256u * u, av[u] + bv[u]);
+    for (int u = 0; u < kU; ++u) buf_st(rc, off0 + 256u * u, kTwo ? av[u] + bv[u] : av[u]);
   }
 }
 
@@ -996,7 +1017,10 @@ hipError_t launch_stream_probe(const float* a, const float* b, float* c, int64_t
                                hipStream_t s) {
   const LaunchEvents ev;
   const dim3 grid((unsigned)((n + kTileElems - 1) / kTileElems));
-  SAEF_LAUNCH(k_stream_probe, grid, dim3(kSBlock), 0, s, a, b, c, n);
+  if (b != nullptr)
+    SAEF_LAUNCH(k_stream_probe<true>, grid, dim3(kSBlock), 0, s, a, b, c, n);
+  else
+    SAEF_LAUNCH(k_stream_probe<false>, grid, dim3(kSBlock), 0, s, a, b, c, n);
   return hipGetLastError();
 }
 

@@ -7,7 +7,7 @@ prints a short text summary:
 * per kernel: calls and average duration (kernel trace statistics);
 * per kernel: HBM bytes per dispatch from FETCH_SIZE and WRITE_SIZE, each
   scaled by the factor that makes the same counter read exactly the bytes of
-  the library's stream probe found in the same run (k_stream_probe: reads
+  the library's stream probe found in the same run (k_stream_probe<true>: reads
   8 N and writes 4 N bytes for N elements per launch);
 * or, from a kernel trace alone (``--trace``), per (kernel, workgroup count):
   the dispatches after the first ``--skip`` ones, their average duration,
@@ -74,9 +74,43 @@ def counter_per_kernel(path: str):
     return out
 
 
+def counters_by_name(path: str):
+    """{kernel: {counter: average over the kernel's dispatches}} of a
+    counter-collection CSV that may hold several counters per dispatch."""
+    vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    for r in csv.DictReader(open(path)):
+        vals[short_name(r["Kernel_Name"])][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    return {k: {c: (sum(v) / len(v), len(v)) for c, v in cs.items()} for k, cs in vals.items()}
+
+
+# Bytes of an L2-to-memory request by its counted size (gfx950 TCC counters).
+READ_REQS = (("TCC_EA0_RDREQ_128B_sum", 128), ("TCC_EA0_RDREQ_64B_sum", 64),
+             ("TCC_EA0_RDREQ_32B_sum", 32))
+
+
+def request_bytes(reads, writes, name: str):
+    """(read bytes, write bytes, dispatches) per dispatch of `name` from the
+    request counts: reads 128/64/32-byte requests, writes 64-byte requests
+    and the remaining (32-byte) ones.  No calibration is involved."""
+    rc = reads.get(name, {})
+    if not all(c in rc for c, _ in READ_REQS):
+        return None
+    rb = sum(rc[c][0] * size for c, size in READ_REQS)
+    wc = writes.get(name, {})
+    wb = float("nan")
+    if "TCC_EA0_WRREQ_sum" in wc and "TCC_EA0_WRREQ_64B_sum" in wc:
+        w64 = wc["TCC_EA0_WRREQ_64B_sum"][0]
+        wb = w64 * 64 + (wc["TCC_EA0_WRREQ_sum"][0] - w64) * 32
+    return rb, wb, rc[READ_REQS[0][0]][1]
+
+
+# the 2-read/1-write stream probe (c = a + b) the counters are calibrated on
+PROBE_KERNEL = "k_stream_probe<true>"
+
+
 def probe_factor(per_kernel, true_kib: float) -> float:
     """Scale that turns the counter of the stream probe into its true size."""
-    vals = [v for _, v in per_kernel.get("k_stream_probe", []) if v > 0]
+    vals = [v for _, v in per_kernel.get(PROBE_KERNEL, []) if v > 0]
     if not vals:
         raise SystemExit("no stream-probe dispatch in the counter file")
     return true_kib / (sum(vals) / len(vals))
@@ -117,6 +151,12 @@ def main() -> int:
                     help="write the kernel's HBM bytes per launch and the source hash here")
     ap.add_argument("--header", default=None,
                     help="comment lines (a file) put at the top of --counters-out")
+    ap.add_argument("--read-reqs", default=None,
+                    help="counter CSV of TCC_EA0_RDREQ_128B_sum, _64B_sum and _32B_sum")
+    ap.add_argument("--write-reqs", default=None,
+                    help="counter CSV of TCC_EA0_WRREQ_sum and TCC_EA0_WRREQ_64B_sum")
+    ap.add_argument("--algo", action="append", default=[], metavar="KERNEL=BYTES",
+                    help="algorithmic bytes per launch of a kernel, for the ratio column")
     args = ap.parse_args()
     if args.trace:
         trace_table(args.trace, args.skip)
@@ -150,6 +190,30 @@ def main() -> int:
         w = (sum(wv) / len(wv) * 1024 * wf / 1e6) if wv else float("nan")
         per[name] = (r, w, len(fv))
         print(f"  {name:44s} {len(fv):4d} {r:10.1f} {w:10.1f} {r + w:10.1f}")
+    algo = {}
+    for item in args.algo:
+        name, _, val = item.rpartition("=")
+        algo[name] = float(val)
+    if args.read_reqs:
+        reads = counters_by_name(args.read_reqs)
+        writes = counters_by_name(args.write_reqs) if args.write_reqs else {}
+        print()
+        print("HBM bytes per dispatch from request counts (rocprofv3 --pmc TCC_EA0_RDREQ_128B_sum "
+              "TCC_EA0_RDREQ_64B_sum TCC_EA0_RDREQ_32B_sum, then TCC_EA0_WRREQ_sum "
+              "TCC_EA0_WRREQ_64B_sum; each request at its counted size, no calibration)")
+        print(f"  {'kernel':44s} {'n':>4s} {'read_MB':>10s} {'write_MB':>10s} {'total_MB':>10s} "
+              f"{'algo_MB':>10s} {'ratio':>7s}")
+        for name in reads:
+            if name.startswith("__amd") or name.startswith("void at::") or name.startswith("at::"):
+                continue
+            got = request_bytes(reads, writes, name)
+            if got is None:
+                continue
+            rb, wb, cnt = got
+            a_mb = algo.get(name, float("nan")) / 1e6
+            ratio = (rb + wb) / 1e6 / a_mb if name in algo else float("nan")
+            print(f"  {name:44s} {cnt:4d} {rb / 1e6:10.1f} {wb / 1e6:10.1f} "
+                  f"{(rb + wb) / 1e6:10.1f} {a_mb:10.1f} {ratio:7.4f}")
     src = kernel_source_hash()
     print()
     print(f"kernel_source_sha256_16: {src}")

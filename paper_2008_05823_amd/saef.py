@@ -376,11 +376,13 @@ def saef_profile_read(layout: Layout) -> dict:
 
 def saef_stream_probe(a, b, c, stream=None) -> None:
     """c = a + b over equal-size contiguous fp32 device tensors (the HBM
-    ceiling of the compression's streaming pattern; measurement aid)."""
+    ceiling of the compression's streaming pattern; measurement aid); with
+    b None, c = a (c may be a itself: one read and one write in place)."""
     n = a.numel()
-    if b.numel() != n or c.numel() != n:
+    if (b is not None and b.numel() != n) or c.numel() != n:
         raise ValueError("saef_stream_probe: a, b and c must have the same size")
-    _check("saef_stream_probe", _lib.saef_stream_probe(_f(a), _f(b), _f(c), n, _stream(stream)))
+    _check("saef_stream_probe", _lib.saef_stream_probe(_f(a), None if b is None else _f(b),
+                                                       _f(c), n, _stream(stream)))
 
 
 def raw_library() -> ctypes.CDLL:
