@@ -607,9 +607,10 @@ __device__ __forceinline__ void aggregate_pass(int K, double inv_k, int L, int l
   }
 }
 
-// Grid: n_tiles workgroups; workgroup b handles tile b.  Wave w takes words
-// w*kU .. w*kU+kU-1 of the tile (one pass over a whole tile), then strides by
-// 4*kU words.
+// Grid: run_padded_tiles(n_tiles) workgroups, one per tile in the XCD-aware
+// tile order of run_tile_of (neighbouring tiles, whose sign words share cache
+// lines, run on one XCD).  Wave w takes words w*kU .. w*kU+kU-1 of the tile
+// (one pass over a whole tile), then strides by 4*kU words.
 template <int kMode, bool kDecode, bool kAvg>
 __global__ __launch_bounds__(kSBlock) void k_aggregate(DevLayout lay, int K, double inv_k,
                                                       const uint64_t* __restrict__ signs,
@@ -619,7 +620,10 @@ __global__ __launch_bounds__(kSBlock) void k_aggregate(DevLayout lay, int K, dou
                                                       uint64_t* __restrict__ ss,
                                                       const float* __restrict__ sscales,
                                                       float* __restrict__ x) {
-  const int64_t ti = blockIdx.x;
+  int row0;
+  int64_t ti;
+  run_tile_of(blockIdx.x, 1, tile_run_shift(lay.n_tiles), row0, ti);
+  if (ti >= lay.n_tiles) return;
   const Tile tile = lay.tiles[ti];
   const int nw = (tile.count + 63) >> 6;
   const uint32_t nbytes = (uint32_t)tile.count * 4u;
@@ -1060,7 +1064,7 @@ hipError_t launch_finalize(const DevLayout& lay, int K, bool server, float* scal
 hipError_t launch_aggregate(const DevLayout& lay, int K, int mode, const uint64_t* signs,
                             const float* scales, float* avg, float* e_srv, uint64_t* srv_signs,
                             const float* srv_scales, float* x, bool decode, hipStream_t s, const LaunchEvents& ev) {
-  const dim3 grid((unsigned)lay.n_tiles);
+  const dim3 grid((unsigned)run_padded_tiles(lay.n_tiles));
   const double ik = inv_pow2(K);
 #define SAEF_AGG(M, D, A)                                                                  \
   SAEF_LAUNCH((k_aggregate<M, D, A>), grid, dim3(kSBlock), 0, s, lay, K, ik, signs, \
