@@ -305,9 +305,13 @@ def main() -> int:
     # dominant kernel: worker compression (12 K + K/8 bytes per parameter,
     # 20 K + K/8 with momentum)
     c_count, c_ms = prof["compress"]
+    # Top-K: the iteration end (compression and server step) runs pipelined
+    # over tensor groups as one timed span when the plan pipelines it
+    tk_pipelined = topk is not None and c_count > 0 and prof["aggregate"][0] == 0
     if topk is not None:
-        c_bytes = (W.topk_algorithmic_bytes_per_param(K, density, w.mode)["worker"]
-                   + (8 * K if mu is not None else 0)) * d
+        tb = W.topk_algorithmic_bytes_per_param(K, density, w.mode)
+        c_bytes = (tb["worker"] + (8 * K if mu is not None else 0)
+                   + (tb["server"] if tk_pipelined else 0)) * d
     else:
         c_bytes = ((20 if mu is not None else 12) * K + K / 8) * d
     c_gbps = c_bytes / (c_ms / c_count * 1e-3) / 1e9 if c_count else None
@@ -369,7 +373,10 @@ def main() -> int:
         "stream_probe_gbps": probe,
         "stream_probe_1r1w_gbps": probe_1r1w,
         "roofline": {"bound": "hbm",
-                     "kernel": "compress" if topk is None else "topk_compress (all passes)",
+                     "kernel": ("compress" if topk is None else
+                                "topk_round_end (worker compression and server step, pipelined "
+                                "over two tensor groups)" if tk_pipelined else
+                                "topk_compress (all passes)"),
                      "achieved": c_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": c_gbps / HBM_PEAK_GBPS if c_gbps else None,

@@ -62,8 +62,10 @@ struct saef_topk {
   void* mem_cand_off = nullptr;
   void* mem_spec = nullptr;
   // the side stream (default priority) and fork/join events of the worker
-  // compression's two row groups
+  // compression's two row groups and of the pipelined iteration end
   saef::TkStreams side{};
+  saef::TkPart all{};               // every tensor
+  std::vector<saef::TkPart> pipe;   // the iteration end's parts (empty: not pipelined)
 };
 
 namespace {
@@ -100,6 +102,52 @@ void* scratch_of(int dev) {
 // Elements per work tile of a tensor of n elements: kTileElems, or more for
 // very large tensors so that no tensor has more than kMaxTilesPerTensor tiles
 // (bounds the number of partial sums the finalize kernel adds per tensor).
+// The parts of the pipelined Top-K iteration end: runs of whole tensors in
+// order (SAEF_TK_PARTS of them, fewer when there are fewer tensors; one part
+// means no pipeline), cut where the running element count passes the first
+// part's share of d (SAEF_TK_FIRST_PCT percent), then equal shares of the
+// rest.
+#ifndef SAEF_TK_PARTS
+#define SAEF_TK_PARTS 2
+#endif
+#ifndef SAEF_TK_FIRST_PCT
+#define SAEF_TK_FIRST_PCT 50
+#endif
+std::vector<saef::TkPart> pipeline_parts(const saef_layout* layout,
+                                         const std::vector<saef::TkTensor>& tens) {
+  const int32_t L = layout->L;
+  const int parts = std::min<int>(SAEF_TK_PARTS, L);
+  std::vector<saef::TkPart> out;
+  if (parts < 2) return out;
+  int64_t d = 0;
+  for (int32_t l = 0; l < L; ++l) d += layout->n[l];
+  int32_t l0 = 0;
+  int64_t cum = 0;
+  for (int i = 0; i < parts; ++i) {
+    int32_t l1 = l0;
+    if (i == parts - 1) {
+      l1 = L;
+    } else {
+      // the running count's target after part i (in parts of 100 * (parts - 1))
+      const int64_t first = SAEF_TK_FIRST_PCT * (parts - 1);
+      const int64_t target = first + (100 - SAEF_TK_FIRST_PCT) * i;
+      // at least one tensor, and one left for each later part
+      while (l1 < L - (parts - 1 - i) && (l1 == l0 || cum * 100 * (parts - 1) < d * target))
+        cum += layout->n[l1++];
+    }
+    const saef::TkTensor& a = tens[l0];
+    const saef::TkTensor& b = tens[l1 - 1];
+    const saef::TensorInfo& ta = layout->tensors[l0];
+    const saef::TensorInfo& tb = layout->tensors[l1 - 1];
+    out.push_back(saef::TkPart{l0, l1, ta.first_tile, tb.first_tile + tb.ntiles, a.first_group,
+                               b.first_group + b.ngroups, a.first_sgroup,
+                               b.first_sgroup + b.nsgroups, a.first_chunk,
+                               b.first_chunk + b.nchunks});
+    l0 = l1;
+  }
+  return out;
+}
+
 int64_t tile_elems(int64_t n) {
   int64_t t = saef::kTileElems;
   if (n > t * saef::kMaxTilesPerTensor) {
@@ -708,6 +756,9 @@ int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk**
       groups.push_back(saef::TkGroup{l, first_tile + g * saef::kTkGroup,
                                      std::min(saef::kTkGroup, ntiles - g * saef::kTkGroup), 0});
   }
+  p->all = saef::TkPart{0, L, 0, (int32_t)layout->dev.n_tiles, 0, (int32_t)groups.size(),
+                        0, (int32_t)sgroups.size(), 0, (int32_t)chunks.size()};
+  p->pipe = pipeline_parts(layout, tens);
   const size_t rows = (size_t)layout->k_max + 1;
   if ((int64_t)std::max(chunks.size(), groups.size()) * (int64_t)rows > kMaxGrid) {
     free_topk(p);
@@ -811,10 +862,10 @@ int saef_topk_info(const saef_topk* plan, int64_t* total_keep) {
 
 namespace {
 
-// saef_topk_compress with the pending flags of launch_topk_compress.
-int topk_compress(const saef_topk* plan, int32_t K, float lr, float mu, const float* g,
-                  float* m, float* e, uint64_t* sel, uint32_t* rank, float* vals, bool pend_in,
-                  bool pend_out, hipStream_t stream) {
+// The argument checks of saef_topk_compress.
+int topk_compress_check(const saef_topk* plan, int32_t K, float lr, float mu, const float* g,
+                        const float* m, const float* e, const uint64_t* sel,
+                        const uint32_t* rank, const float* vals) {
   if (plan == nullptr) return SAEF_EINVAL;
   const saef_layout* layout = plan->layout;
   int rc = check_common(layout, K);
@@ -834,10 +885,52 @@ int topk_compress(const saef_topk* plan, int32_t K, float lr, float mu, const fl
   if (m != nullptr && (!f32_ok(m) || overlap(m, vb, g, vb) || overlap(m, vb, e, vb) ||
                        overlap(m, vb, vals, mb)))
     return SAEF_EINVAL;
+  return SAEF_OK;
+}
+
+// saef_topk_compress with the pending flags of launch_topk_compress.
+int topk_compress(const saef_topk* plan, int32_t K, float lr, float mu, const float* g,
+                  float* m, float* e, uint64_t* sel, uint32_t* rank, float* vals, bool pend_in,
+                  bool pend_out, hipStream_t stream) {
+  const int rc = topk_compress_check(plan, K, lr, mu, g, m, e, sel, rank, vals);
+  if (rc != SAEF_OK) return rc;
+  const saef_layout* layout = plan->layout;
   return hip_rc(timed(layout, 1, [&](const saef::LaunchEvents& ev) {
-    return saef::launch_topk_compress(layout->dev, plan->dev, K, lr, mu, g, m, e, sel, rank,
-                                      vals, pend_in, pend_out, stream, plan->side, ev);
+    return saef::launch_topk_compress(layout->dev, plan->dev, plan->all, K, lr, mu, g, m, e, sel,
+                                      rank, vals, pend_in, pend_out, stream, plan->side, ev);
   }));
+}
+
+// The argument checks of saef_topk_aggregate.
+int topk_aggregate_check(const saef_topk* plan, int32_t K, int32_t mode, const uint64_t* sel,
+                         const uint32_t* rank, const float* vals, const float* avg,
+                         const float* e_srv, const uint64_t* srv_sel, const uint32_t* srv_rank,
+                         const float* srv_vals, const float* x) {
+  if (plan == nullptr) return SAEF_EINVAL;
+  const saef_layout* layout = plan->layout;
+  int rc = check_common(layout, K);
+  if (rc != SAEF_OK) return rc;
+  if (mode != SAEF_MODE_SC && mode != SAEF_MODE_DC) return SAEF_EINVAL;
+  if (!u64_ok(sel) || rank == nullptr || !aligned(rank, 4) || !f32_ok(vals) || !f32_ok(x))
+    return SAEF_EINVAL;
+  if (avg != nullptr && !f32_ok(avg)) return SAEF_EINVAL;
+  const size_t xb = layout->d_pad * sizeof(float);
+  const size_t wb1 = (layout->d_pad / 64) * sizeof(uint64_t);
+  const size_t rb1 = (layout->d_pad / 64) * sizeof(uint32_t);
+  const size_t mb1 = plan->total_keep * sizeof(float);
+  if (mode == SAEF_MODE_DC) {
+    if (!f32_ok(e_srv) || !u64_ok(srv_sel) || srv_rank == nullptr || !aligned(srv_rank, 4) ||
+        !f32_ok(srv_vals))
+      return SAEF_EINVAL;
+    if (overlap(e_srv, xb, x, xb) || overlap(srv_vals, mb1, x, xb) ||
+        overlap(srv_vals, mb1, e_srv, xb) || overlap(srv_sel, wb1, x, xb) ||
+        overlap(srv_sel, wb1, e_srv, xb) || overlap(srv_rank, rb1, x, xb) ||
+        overlap(srv_rank, rb1, e_srv, xb) || overlap(srv_rank, rb1, srv_vals, mb1))
+      return SAEF_EINVAL;
+  }
+  if (avg != nullptr && (overlap(avg, xb, x, xb) || (e_srv && overlap(avg, xb, e_srv, xb))))
+    return SAEF_EINVAL;
+  return SAEF_OK;
 }
 
 }  // namespace
@@ -865,33 +958,14 @@ int saef_topk_aggregate(const saef_topk* plan, int32_t K, int32_t mode, const ui
                         const uint32_t* rank, const float* vals, float* avg, float* e_srv,
                         uint64_t* srv_sel, uint32_t* srv_rank, float* srv_vals, float* x,
                         hipStream_t stream) {
-  if (plan == nullptr) return SAEF_EINVAL;
-  const saef_layout* layout = plan->layout;
-  int rc = check_common(layout, K);
+  const int rc = topk_aggregate_check(plan, K, mode, sel, rank, vals, avg, e_srv, srv_sel,
+                                     srv_rank, srv_vals, x);
   if (rc != SAEF_OK) return rc;
-  if (mode != SAEF_MODE_SC && mode != SAEF_MODE_DC) return SAEF_EINVAL;
-  if (!u64_ok(sel) || rank == nullptr || !aligned(rank, 4) || !f32_ok(vals) || !f32_ok(x))
-    return SAEF_EINVAL;
-  if (avg != nullptr && !f32_ok(avg)) return SAEF_EINVAL;
-  const size_t xb = layout->d_pad * sizeof(float);
-  const size_t wb1 = (layout->d_pad / 64) * sizeof(uint64_t);
-  const size_t rb1 = (layout->d_pad / 64) * sizeof(uint32_t);
-  const size_t mb1 = plan->total_keep * sizeof(float);
-  if (mode == SAEF_MODE_DC) {
-    if (!f32_ok(e_srv) || !u64_ok(srv_sel) || srv_rank == nullptr || !aligned(srv_rank, 4) ||
-        !f32_ok(srv_vals))
-      return SAEF_EINVAL;
-    if (overlap(e_srv, xb, x, xb) || overlap(srv_vals, mb1, x, xb) ||
-        overlap(srv_vals, mb1, e_srv, xb) || overlap(srv_sel, wb1, x, xb) ||
-        overlap(srv_sel, wb1, e_srv, xb) || overlap(srv_rank, rb1, x, xb) ||
-        overlap(srv_rank, rb1, e_srv, xb) || overlap(srv_rank, rb1, srv_vals, mb1))
-      return SAEF_EINVAL;
-  }
-  if (avg != nullptr && (overlap(avg, xb, x, xb) || (e_srv && overlap(avg, xb, e_srv, xb))))
-    return SAEF_EINVAL;
+  const saef_layout* layout = plan->layout;
   return hip_rc(timed(layout, 3, [&](const saef::LaunchEvents& ev) {
-    return saef::launch_topk_aggregate(layout->dev, plan->dev, K, mode, sel, rank, vals, avg,
-                                       e_srv, srv_sel, srv_rank, srv_vals, x, stream, ev);
+    return saef::launch_topk_aggregate(layout->dev, plan->dev, plan->all, K, mode, sel, rank,
+                                       vals, avg, e_srv, srv_sel, srv_rank, srv_vals, x, stream,
+                                       ev);
   }));
 }
 
@@ -976,8 +1050,23 @@ int saef_topk_round_end(const saef_topk* plan, int64_t t, int64_t period, int32_
   // e is pending unless t = 0 or this iteration's averaging wrote it plain;
   // the compression leaves its own kept elements pending
   const bool averaging = period > 0 && (t + 1) % period == 0;
-  int rc = topk_compress(plan, K, lr, mu, g, m, e, sel, rank, vals, t > 0 && !averaging, true,
-                         stream);
+  const bool pend_in = t > 0 && !averaging;
+  if (plan->pipe.size() >= 2 && plan->side.stream != nullptr) {
+    // pipelined over the plan's parts: one timed span (kind 1) from the
+    // first Delta pass to the last kernel on the caller's stream
+    int rc = topk_compress_check(plan, K, lr, mu, g, m, e, sel, rank, vals);
+    if (rc == SAEF_OK)
+      rc = topk_aggregate_check(plan, K, mode, sel, rank, vals, nullptr, e_srv, srv_sel,
+                                srv_rank, srv_vals, x);
+    if (rc != SAEF_OK) return rc;
+    return hip_rc(timed(layout, 1, [&](const saef::LaunchEvents& ev) {
+      return saef::launch_topk_round_end(layout->dev, plan->dev, plan->pipe.data(),
+                                         (int)plan->pipe.size(), K, lr, mu, mode, g, m, e, sel,
+                                         rank, vals, pend_in, e_srv, srv_sel, srv_rank, srv_vals,
+                                         x, stream, plan->side, ev);
+    }));
+  }
+  int rc = topk_compress(plan, K, lr, mu, g, m, e, sel, rank, vals, pend_in, true, stream);
   if (rc != SAEF_OK) return rc;
   return saef_topk_aggregate(plan, K, mode, sel, rank, vals, nullptr, e_srv, srv_sel, srv_rank,
                              srv_vals, x, stream);

@@ -89,6 +89,18 @@ struct TkSel {
   int64_t iota;     // elements equal to tau with index <= iota are kept
 };
 
+// A run of whole tensors [l0, l1) with the tiles, tile groups, super-groups
+// and server chunks that belong to them: each a contiguous index range, since
+// all four are numbered tensor by tensor.  The Top-K kernels work on one
+// part; the whole layout is one part.
+struct TkPart {
+  int32_t l0, l1;  // tensors
+  int32_t t0, t1;  // tiles
+  int32_t g0, g1;  // tile groups
+  int32_t s0, s1;  // super-groups
+  int32_t c0, c1;  // server chunks
+};
+
 struct TkDev {
   const TkChunk* chunks;
   const TkTensor* tens;
@@ -128,10 +140,11 @@ struct TkStreams {
   hipEvent_t fork = nullptr;
   hipEvent_t join = nullptr;
 };
-hipError_t launch_topk_compress(const DevLayout& lay, const TkDev& tk, int K, float lr, float mu,
-                                const float* g, float* m, float* e, uint64_t* sel,
-                                uint32_t* rank, float* vals, bool pend_in, bool pend_out,
-                                hipStream_t s, const TkStreams& side,
+// `all`: the part of every tensor.
+hipError_t launch_topk_compress(const DevLayout& lay, const TkDev& tk, const TkPart& all, int K,
+                                float lr, float mu, const float* g, float* m, float* e,
+                                uint64_t* sel, uint32_t* rank, float* vals, bool pend_in,
+                                bool pend_out, hipStream_t s, const TkStreams& side,
                                 const LaunchEvents& ev = LaunchEvents());
 
 // Sets to 0 the elements of the K rows of e whose selection bit is set.
@@ -141,10 +154,27 @@ hipError_t launch_topk_materialize(const DevLayout& lay, int K, float* e, const 
 // Server Top-K aggregation: mean of the K decoded messages; mode 1: e_srv
 // <- e_srv + mean, its Top-K message, e_srv at kept elements <- 0 and x <- x
 // - C(Delta); mode 0: x <- x - mean.  avg written when non-null.
-hipError_t launch_topk_aggregate(const DevLayout& lay, const TkDev& tk, int K, int mode,
-                                 const uint64_t* sel, const uint32_t* rank, const float* vals,
-                                 float* avg, float* e_srv, uint64_t* srv_sel, uint32_t* srv_rank,
-                                 float* srv_vals, float* x, hipStream_t s,
+hipError_t launch_topk_aggregate(const DevLayout& lay, const TkDev& tk, const TkPart& all,
+                                 int K, int mode, const uint64_t* sel, const uint32_t* rank,
+                                 const float* vals, float* avg, float* e_srv, uint64_t* srv_sel,
+                                 uint32_t* srv_rank, float* srv_vals, float* x, hipStream_t s,
+                                 const LaunchEvents& ev = LaunchEvents());
+
+// The worker compression (pend_out: its kept elements left pending) and the
+// server step of one iteration, pipelined over n_parts >= 2 parts that
+// cover the tensors in order: the parts' Delta passes run one after another
+// on s, and each part but the last then takes its selection, messages and
+// server step on the side stream while the later parts' Delta passes
+// stream; s waits for the side stream at the end (an event fork and join).
+// The same results as launch_topk_compress then launch_topk_aggregate (avg
+// null).  ev: start stamped by the first Delta pass, stop by the last kernel
+// on s.
+hipError_t launch_topk_round_end(const DevLayout& lay, const TkDev& tk, const TkPart* parts,
+                                 int n_parts, int K, float lr, float mu, int mode,
+                                 const float* g, float* m, float* e, uint64_t* sel,
+                                 uint32_t* rank, float* vals, bool pend_in, float* e_srv,
+                                 uint64_t* srv_sel, uint32_t* srv_rank, float* srv_vals,
+                                 float* x, hipStream_t s, const TkStreams& side,
                                  const LaunchEvents& ev = LaunchEvents());
 
 }  // namespace saef

@@ -152,13 +152,15 @@ __device__ __forceinline__ void delta_words(int w0, int nw, int count, float lr,
   }
 }
 
-// Grid: n_tiles * K workgroups; workgroup b handles worker b % K of tile b / K.
+// Grid: (p.t1 - p.t0) * R workgroups; workgroup b handles row row0 + b % R of
+// tile p.t0 + b / R.
 // Each wave takes kTkU words of the tile (one pass); the tile's speculative
 // list is written in index order (wave by wave) when it fits.  kPend: e
 // holds the previous call's Delta with its kept elements (selection words
 // psel) still to be set to 0; they are read as 0.
 template <bool kMom, bool kPend>
-__global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, int R, int row0,
+__global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, TkPart p, int R,
+                                                     int row0,
                                                      float lr, float mu,
                                                      const float* __restrict__ g,
                                                      float* __restrict__ m,
@@ -168,7 +170,7 @@ __global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, in
   __shared__ uint32_t h[kTkHistPad];
   __shared__ uint32_t s_cnt[kWaves];
   const int k = row0 + (int)(blockIdx.x % (unsigned)R);
-  const int64_t ti = blockIdx.x / (unsigned)R;
+  const int64_t ti = p.t0 + (int64_t)(blockIdx.x / (unsigned)R);
   const Tile tile = lay.tiles[ti];
   const TkSel* st = tk.sel + (int64_t)k * lay.L + tile.l;
   const uint32_t win = st->win;
@@ -228,13 +230,13 @@ __global__ __launch_bounds__(kBlock) void k_tk_delta(DevLayout lay, TkDev tk, in
 }
 
 // ------------------------------------------------------------------ sums
-// Grid: R * n_groups workgroups (kSuper: R * n_sgroups).  Workgroup b adds
-// the tile histograms of group b % n_groups (or the group sums of
-// super-group b % n_sgroups) of row row0 + b / n.
+// Grid: R * n workgroups, n the part's groups (kSuper: super-groups).
+// Workgroup b adds the tile histograms of the part's group b % n (or the
+// group sums of its super-group b % n) of row row0 + b / n.
 template <bool kSuper>
-__global__ __launch_bounds__(kBlock) void k_tk_sum(DevLayout lay, TkDev tk, int row0) {
-  const int64_t n = kSuper ? tk.n_sgroups : tk.n_groups;
-  const int64_t gi = blockIdx.x % n;
+__global__ __launch_bounds__(kBlock) void k_tk_sum(DevLayout lay, TkDev tk, TkPart p, int row0) {
+  const int64_t n = kSuper ? p.s1 - p.s0 : p.g1 - p.g0;
+  const int64_t gi = (kSuper ? p.s0 : p.g0) + (int64_t)(blockIdx.x % n);
   const int row = row0 + (int)(blockIdx.x / n);
   const TkGroup gr = (kSuper ? tk.sgroups : tk.groups)[gi];
   uint32_t* dst = (kSuper ? tk.sghist + ((int64_t)row * tk.n_sgroups + gi) * kTkHistPad
@@ -322,17 +324,19 @@ __device__ void find_bin(const uint32_t* h, int nb, int64_t need, uint32_t* s_sc
 }
 
 // ------------------------------------------------------------------ pick
-// Grid: R * L workgroups.  Adds the tensor's group sums (or super-group
+// Grid: R * nl workgroups, nl the part's tensors (workgroup b: tensor
+// p.l0 + b % nl of row row0 + b / nl).  Adds the tensor's group sums (or super-group
 // sums), finds the bin b1 that holds the k-th largest key and how many to
 // take from it, and gives each group of the tensor its first candidate slot:
 // the elements of b1 go to the (row, tensor)'s candidate area (one slot per
 // element of the tensor at most) in tile order.
-__global__ __launch_bounds__(kBlock) void k_tk_pick(DevLayout lay, TkDev tk, int row0) {
+__global__ __launch_bounds__(kBlock) void k_tk_pick(DevLayout lay, TkDev tk, TkPart p, int row0) {
   __shared__ uint32_t s_scan[kWaves];
   __shared__ uint32_t s_res[3];
   __shared__ uint32_t h[kTkHistPad];
-  const int l = (int)(blockIdx.x % lay.L);
-  const int r = (int)(blockIdx.x / lay.L);
+  const int nl = p.l1 - p.l0;
+  const int l = p.l0 + (int)(blockIdx.x % (unsigned)nl);
+  const int r = (int)(blockIdx.x / (unsigned)nl);
   const int row = row0 + r;
   const TkTensor t = tk.tens[l];
   const bool super = t.nsgroups > 0;
@@ -368,13 +372,15 @@ __global__ __launch_bounds__(kBlock) void k_tk_pick(DevLayout lay, TkDev tk, int
   }
 }
 
-// Grid: R * n_groups workgroups of one wave: the first candidate slot of
-// each tile of group b % n_groups in row row0 + b / n_groups (the group's
-// slot plus the b1 counts of the group's earlier tiles).
-__global__ __launch_bounds__(kWave) void k_tk_offsets(DevLayout lay, TkDev tk, int row0) {
+// Grid: R * n workgroups of one wave, n the part's groups: the first
+// candidate slot of each tile of the part's group b % n in row row0 + b / n
+// (the group's slot plus the b1 counts of the group's earlier tiles).
+__global__ __launch_bounds__(kWave) void k_tk_offsets(DevLayout lay, TkDev tk, TkPart p,
+                                                      int row0) {
   static_assert(kTkGroup == kWave, "one tile of a group per lane");
-  const int64_t gi = blockIdx.x % tk.n_groups;
-  const int row = row0 + (int)(blockIdx.x / tk.n_groups);
+  const int64_t n = p.g1 - p.g0;
+  const int64_t gi = p.g0 + (int64_t)(blockIdx.x % n);
+  const int row = row0 + (int)(blockIdx.x / n);
   const TkGroup gr = tk.groups[gi];
   const uint32_t b1 = tk.sel[(int64_t)row * lay.L + gr.l].bin;
   const int lane = lane_id();
@@ -473,8 +479,8 @@ __device__ __forceinline__ bool gather_list(const u64* __restrict__ ent, uint32_
   return true;
 }
 
-// Grid: per_wave_grid(lay) * R workgroups; wave w of workgroup b owns tile
-// 4 (b / R) + w of row b % R.  The count of the elements above b1 (kept for
+// Grid: ceil((p.t1 - p.t0) / 4) * R workgroups; wave w of workgroup b owns
+// tile p.t0 + 4 (b / R) + w of row b % R.  The count of the elements above b1 (kept for
 // sure) and the elements of b1 to the tile's candidate slots as key | (index
 // in the tensor) << 32, in index order: from the tile's speculative list when
 // `spec` is set, the list fits and its bound lies at or below b1 (slot
@@ -485,13 +491,14 @@ __device__ __forceinline__ bool gather_list(const u64* __restrict__ ent, uint32_
 // Without lists (kSpec false) every tile takes the Delta read, with its 32
 // loads in flight at once (85 VGPRs: k_tk_gather_full).
 template <bool kSpec>
-__device__ __forceinline__ void gather_tile(const DevLayout& lay, const TkDev& tk, int R,
-                                            int row0, const float* __restrict__ data,
+__device__ __forceinline__ void gather_tile(const DevLayout& lay, const TkDev& tk,
+                                            const TkPart& p, int R, int row0,
+                                            const float* __restrict__ data,
                                             uint64_t* __restrict__ sel) {
   constexpr int spec = kSpec ? 1 : 0;
   const int r = (int)(blockIdx.x % (unsigned)R);
-  const int64_t ti = (int64_t)(blockIdx.x / (unsigned)R) * kWaves + wave_id();
-  if (ti >= lay.n_tiles) return;
+  const int64_t ti = p.t0 + (int64_t)(blockIdx.x / (unsigned)R) * kWaves + wave_id();
+  if (ti >= p.t1) return;
   const int row = row0 + r;
   uint16_t* th = tile_hist(tk, lay, row, ti);
   // the list count and the flag slot in one 32-bit word: a scalar load issued
@@ -558,15 +565,15 @@ __device__ __forceinline__ void gather_tile(const DevLayout& lay, const TkDev& t
 }
 
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8, 8)))
-void k_tk_gather_spec(DevLayout lay, TkDev tk, int R, int row0, const float* __restrict__ data,
-                      uint64_t* __restrict__ sel) {
-  gather_tile<true>(lay, tk, R, row0, data, sel);
+void k_tk_gather_spec(DevLayout lay, TkDev tk, TkPart p, int R, int row0,
+                      const float* __restrict__ data, uint64_t* __restrict__ sel) {
+  gather_tile<true>(lay, tk, p, R, row0, data, sel);
 }
 
 __global__ __launch_bounds__(kBlock)
-void k_tk_gather_full(DevLayout lay, TkDev tk, int R, int row0, const float* __restrict__ data,
-                      uint64_t* __restrict__ sel) {
-  gather_tile<false>(lay, tk, R, row0, data, sel);
+void k_tk_gather_full(DevLayout lay, TkDev tk, TkPart p, int R, int row0,
+                      const float* __restrict__ data, uint64_t* __restrict__ sel) {
+  gather_tile<false>(lay, tk, p, R, row0, data, sel);
 }
 
 // ------------------------------------------------------------------ select
@@ -593,7 +600,7 @@ __device__ void cand_hist(uint32_t* h, int nb, const u64* __restrict__ cand, int
   __syncthreads();
 }
 
-// Grid: R * L workgroups of kBig threads.  Among the candidates of (row,
+// Grid: R * nl workgroups of kBig threads (as k_tk_pick).  Among the candidates of (row,
 // tensor) (the elements of bin b1), takes the `need` largest keys, equal
 // keys by lower index: radix passes of up to 11 bits over the key bits that
 // b1 leaves open (bits 16..0 inside the window; all 31 for the bins below
@@ -601,12 +608,14 @@ __device__ void cand_hist(uint32_t* h, int nb, const u64* __restrict__ cand, int
 // equal to tau are kept; if not all, passes on the index in the tensor
 // (bits 27..17, 16..6, 5..0) give the last kept index iota.  The next
 // call's window is placed around tau.
-__global__ __launch_bounds__(kBig) void k_tk_select(DevLayout lay, TkDev tk, int row0) {
+__global__ __launch_bounds__(kBig) void k_tk_select(DevLayout lay, TkDev tk, TkPart p,
+                                                     int row0) {
   __shared__ uint32_t h[kTkBins];
   __shared__ uint32_t s_scan[kBig / kWave];
   __shared__ uint32_t s_res[3];
-  const int l = (int)(blockIdx.x % lay.L);
-  const int r = (int)(blockIdx.x / lay.L);
+  const int nl = p.l1 - p.l0;
+  const int l = p.l0 + (int)(blockIdx.x % (unsigned)nl);
+  const int r = (int)(blockIdx.x / (unsigned)nl);
   const int row = row0 + r;
   TkSel* st = tk.sel + (int64_t)row * lay.L + l;
   const u64* cand = tk.cand + (int64_t)row * lay.d_pad + lay.tensors[l].off;
@@ -679,17 +688,18 @@ __device__ __forceinline__ bool cand_kept(u64 e, const TkSel& st) {
   return key > st.tau || (key == st.tau && idx <= st.iota);
 }
 
-// Grid: R * L workgroups.  Each tile's kept count (the gather's count of
+// Grid: R * nl workgroups (as k_tk_pick).  Each tile's kept count (the gather's count of
 // definite elements plus its kept candidates), then the exclusive prefix
 // over the tensor's tiles in tile order, in place.  The candidates of a
 // block of kBlock tiles are contiguous: the whole workgroup reads them and
 // counts the kept ones per tile in LDS.
-__global__ __launch_bounds__(kBlock) void k_tk_scan(DevLayout lay, TkDev tk, int row0) {
+__global__ __launch_bounds__(kBlock) void k_tk_scan(DevLayout lay, TkDev tk, TkPart p, int row0) {
   constexpr int kIlp = 4;
   __shared__ uint32_t s_scan[kWaves];
   __shared__ uint32_t s_cnt[kBlock];
-  const int l = (int)(blockIdx.x % lay.L);
-  const int r = (int)(blockIdx.x / lay.L);
+  const int nl = p.l1 - p.l0;
+  const int l = p.l0 + (int)(blockIdx.x % (unsigned)nl);
+  const int r = (int)(blockIdx.x / (unsigned)nl);
   const int row = row0 + r;
   const TensorInfo ten = lay.tensors[l];
   const TkSel st = tk.sel[(int64_t)row * lay.L + l];
@@ -807,8 +817,8 @@ __device__ __forceinline__ void emit_list(const u64* __restrict__ ent, uint32_t 
   if (lane < nw) rr[lane] = base + incl - cnt;
 }
 
-// Grid: per_wave_grid(lay) * R workgroups; wave w of workgroup b owns tile
-// 4 (b / R) + w of row b % R.  The tile's kept candidates are added to its
+// Grid: ceil((p.t1 - p.t0) / 4) * R workgroups; wave w of workgroup b owns
+// tile p.t0 + 4 (b / R) + w of row b % R.  The tile's kept candidates are added to its
 // selection words (LDS), then the rank words, the kept values in index order
 // and the kept elements of data set to 0; kX (server): x <- x - Delta at the
 // kept elements (C(Delta) is zero elsewhere).  Lane j holds selection word j
@@ -817,8 +827,9 @@ __device__ __forceinline__ void emit_list(const u64* __restrict__ ent, uint32_t 
 // search over the scan, its bit by nth_set_bit, so the work follows the kept
 // count, not the tile size.
 template <bool kX, bool kPend>
-__global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, int R, int row0,
-                                                    int spec, float* __restrict__ data,
+__global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, TkPart p, int R,
+                                                    int row0, int spec,
+                                                    float* __restrict__ data,
                                                     uint64_t* __restrict__ sel,
                                                     uint32_t* __restrict__ rank,
                                                     float* __restrict__ vals,
@@ -826,8 +837,8 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, int
   static_assert(kTileWords == 32, "five halving steps find a word of the tile");
   __shared__ u64 words[kWaves][kTileWords];  // one row per wave, used by that wave only
   const int r = (int)(blockIdx.x % (unsigned)R);
-  const int64_t ti = (int64_t)(blockIdx.x / (unsigned)R) * kWaves + wave_id();
-  if (ti >= lay.n_tiles) return;
+  const int64_t ti = p.t0 + (int64_t)(blockIdx.x / (unsigned)R) * kWaves + wave_id();
+  if (ti >= p.t1) return;
   const int wave = threadIdx.x / kWave;
   const int lane = lane_id();
   const int row = row0 + r;
@@ -963,8 +974,8 @@ __device__ __forceinline__ AggStep<U> agg_words(const uint64_t* __restrict__ sel
 }
 
 template <int kMode, bool kAvg, int U, bool kCo>
-__global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, int K,
-                                                       double inv_k,
+__global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, TkPart p,
+                                                       int K, double inv_k,
                                                        const uint64_t* __restrict__ sel,
                                                        const uint32_t* __restrict__ rank,
                                                        const float* __restrict__ vals,
@@ -976,7 +987,7 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
   static_assert(kTileWords % U == 0, "a pass of U words stays in one tile");
   constexpr int kChunkTiles = kTkChunk / kTkTileElems;
   __shared__ uint32_t h[kMode == 1 ? kChunkTiles * kTkHistPad : 1];  // per tile of the chunk
-  const int64_t ci = blockIdx.x;
+  const int64_t ci = p.c0 + (int64_t)blockIdx.x;
   const TkChunk c = tk.chunks[ci];
   const int64_t voff = tk.tens[c.l].voff;
   const uint32_t keep = (uint32_t)tk.tens[c.l].keep;
@@ -1140,59 +1151,118 @@ struct Launcher {
   const TkDev& tk;
   hipStream_t s;
 
-  // everything after the first pass for R rows of `data` (rows row0..):
-  // sums, pick, offsets, gather, select, scan, emit.  The last kernel
-  // stamps the caller's stop event.
-  hipError_t select_and_emit(int R, int row0, float* data, uint64_t* sel, uint32_t* rank,
-                             float* vals, float* x, bool pend_out,
+  // The Delta pass of R rows (row0..) over the part's tiles; `start` stamps
+  // the dispatch's start when non-null.
+  hipError_t delta(const TkPart& p, int R, int row0, float lr, float mu, const float* g,
+                   float* m, float* e, const uint64_t* psel, bool pend_in,
+                   hipEvent_t start) const {
+    const dim3 grid((unsigned)((int64_t)(p.t1 - p.t0) * R));
+#define SAEF_TKD(MOM, PEND)                                                                  \
+  hipExtLaunchKernelGGL((k_tk_delta<MOM, PEND>), grid, dim3(kBlock), 0, s, start, nullptr, 0, \
+                        lay, tk, p, R, row0, lr, mu, g, m, e, psel)
+    if (m != nullptr) {
+      if (pend_in) SAEF_TKD(true, true); else SAEF_TKD(true, false);
+    } else {
+      if (pend_in) SAEF_TKD(false, true); else SAEF_TKD(false, false);
+    }
+#undef SAEF_TKD
+    return hipGetLastError();
+  }
+
+  // everything after the first pass for R rows of `data` (rows row0..) over
+  // the part's tensors: sums, pick, offsets, gather, select, scan, emit.
+  // The last kernel stamps the caller's stop event.
+  hipError_t select_and_emit(const TkPart& p, int R, int row0, float* data, uint64_t* sel,
+                             uint32_t* rank, float* vals, float* x, bool pend_out,
                              const LaunchEvents& last) const {
     const LaunchEvents ev;
     hipError_t err;
-    SAEF_LAUNCH(k_tk_sum<false>, dim3((unsigned)(R * tk.n_groups)), dim3(kBlock), 0, s, lay, tk,
-                row0);
+    const dim3 groups((unsigned)((int64_t)R * (p.g1 - p.g0)));
+    SAEF_LAUNCH(k_tk_sum<false>, groups, dim3(kBlock), 0, s, lay, tk, p, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    if (tk.n_sgroups > 0) {
-      SAEF_LAUNCH(k_tk_sum<true>, dim3((unsigned)(R * tk.n_sgroups)), dim3(kBlock), 0, s, lay,
-                  tk, row0);
+    if (p.s1 > p.s0) {
+      SAEF_LAUNCH(k_tk_sum<true>, dim3((unsigned)((int64_t)R * (p.s1 - p.s0))), dim3(kBlock), 0,
+                  s, lay, tk, p, row0);
       if ((err = hipGetLastError()) != hipSuccess) return err;
     }
-    const dim3 pairs((unsigned)(R * lay.L));
-    const dim3 tiles((unsigned)(per_wave_grid(lay) * R));
-    SAEF_LAUNCH(k_tk_pick, pairs, dim3(kBlock), 0, s, lay, tk, row0);
+    const dim3 pairs((unsigned)((int64_t)R * (p.l1 - p.l0)));
+    const dim3 tiles((unsigned)((int64_t)(p.t1 - p.t0 + kWaves - 1) / kWaves * R));
+    SAEF_LAUNCH(k_tk_pick, pairs, dim3(kBlock), 0, s, lay, tk, p, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    SAEF_LAUNCH(k_tk_offsets, dim3((unsigned)(R * tk.n_groups)), dim3(kWave), 0, s, lay, tk, row0);
+    SAEF_LAUNCH(k_tk_offsets, groups, dim3(kWave), 0, s, lay, tk, p, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     // speculative lists exist for the worker rows only (the server's Delta
     // comes from the aggregation kernel), and only if some tensor keeps them
     const int spec = row0 + R <= lay.k_max && tk.lists != 0 ? 1 : 0;
     if (spec)
-      SAEF_LAUNCH(k_tk_gather_spec, tiles, dim3(kBlock), 0, s, lay, tk, R, row0, data, sel);
+      SAEF_LAUNCH(k_tk_gather_spec, tiles, dim3(kBlock), 0, s, lay, tk, p, R, row0, data, sel);
     else
-      SAEF_LAUNCH(k_tk_gather_full, tiles, dim3(kBlock), 0, s, lay, tk, R, row0, data, sel);
+      SAEF_LAUNCH(k_tk_gather_full, tiles, dim3(kBlock), 0, s, lay, tk, p, R, row0, data, sel);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    SAEF_LAUNCH(k_tk_select, pairs, dim3(kBig), 0, s, lay, tk, row0);
+    SAEF_LAUNCH(k_tk_select, pairs, dim3(kBig), 0, s, lay, tk, p, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    SAEF_LAUNCH(k_tk_scan, pairs, dim3(kBlock), 0, s, lay, tk, row0);
+    SAEF_LAUNCH(k_tk_scan, pairs, dim3(kBlock), 0, s, lay, tk, p, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     if (x != nullptr)
       hipExtLaunchKernelGGL((k_tk_emit<true, false>), tiles, dim3(kBlock), 0, s, nullptr,
-                            last.stop, 0, lay, tk, R, row0, 0, data, sel, rank, vals, x);
+                            last.stop, 0, lay, tk, p, R, row0, 0, data, sel, rank, vals, x);
     else if (pend_out)
       hipExtLaunchKernelGGL((k_tk_emit<false, true>), tiles, dim3(kBlock), 0, s, nullptr,
-                            last.stop, 0, lay, tk, R, row0, spec, data, sel, rank, vals, x);
+                            last.stop, 0, lay, tk, p, R, row0, spec, data, sel, rank, vals, x);
     else
       hipExtLaunchKernelGGL((k_tk_emit<false, false>), tiles, dim3(kBlock), 0, s, nullptr,
-                            last.stop, 0, lay, tk, R, row0, spec, data, sel, rank, vals, x);
+                            last.stop, 0, lay, tk, p, R, row0, spec, data, sel, rank, vals, x);
     return hipGetLastError();
+  }
+
+  // The server step over the part's tensors: the aggregation of the K
+  // messages, then (mode 1) the server row's selection and message.  The
+  // aggregation stamps ev.start; the last kernel ev.stop.
+  hipError_t server(const TkPart& p, int K, int mode, const uint64_t* sel, const uint32_t* rank,
+                    const float* vals, float* avg, float* e_srv, uint64_t* srv_sel,
+                    uint32_t* srv_rank, float* srv_vals, float* x,
+                    const LaunchEvents& ev) const {
+    const dim3 grid((unsigned)(p.c1 - p.c0));
+    const double ik = inv_pow2(K);
+    hipEvent_t stop0 = mode == 1 ? nullptr : ev.stop;
+    // dense messages (at least 1/32 of the elements kept): one load per worker
+    // and step, values handed out with ds_bpermute; sparser ones: per-pair
+    // gathers (faster there: at 1% kept 117 against 153 us at resnet50, K = 8;
+    // at 5% and 10%, 281 and 316 us against 265 and 290 us for the server step)
+    const bool co = tk.total_keep * 32 >= lay.d_pad;
+#define SAEF_TKA(M, A, U, C)                                                                 \
+  hipExtLaunchKernelGGL((k_tk_aggregate<M, A, U, C>), grid, dim3(kBig), 0, s, ev.start, stop0, \
+                        0, lay, tk, p, K, ik, sel, rank, vals, avg, e_srv, x)
+#define SAEF_TKA_U(M, A)                                 \
+  do {                                                   \
+    if (K <= 8) {                                        \
+      if (co) SAEF_TKA(M, A, 8, true);                   \
+      else SAEF_TKA(M, A, 8, false);                     \
+    } else {                                             \
+      if (co) SAEF_TKA(M, A, 4, true);                   \
+      else SAEF_TKA(M, A, 4, false);                     \
+    }                                                    \
+  } while (0)
+    if (mode == 1) {
+      if (avg != nullptr) SAEF_TKA_U(1, true); else SAEF_TKA_U(1, false);
+    } else {
+      if (avg != nullptr) SAEF_TKA_U(0, true); else SAEF_TKA_U(0, false);
+    }
+#undef SAEF_TKA_U
+#undef SAEF_TKA
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess || mode != 1) return err;
+    return select_and_emit(p, 1, lay.k_max, e_srv, srv_sel, srv_rank, srv_vals, x, false, ev);
   }
 };
 
 }  // namespace
 
-hipError_t launch_topk_compress(const DevLayout& lay, const TkDev& tk, int K, float lr, float mu,
-                                const float* g, float* m, float* e, uint64_t* sel,
-                                uint32_t* rank, float* vals, bool pend_in, bool pend_out,
-                                hipStream_t s, const TkStreams& side, const LaunchEvents& ev) {
+hipError_t launch_topk_compress(const DevLayout& lay, const TkDev& tk, const TkPart& all, int K,
+                                float lr, float mu, const float* g, float* m, float* e,
+                                uint64_t* sel, uint32_t* rank, float* vals, bool pend_in,
+                                bool pend_out, hipStream_t s, const TkStreams& side,
+                                const LaunchEvents& ev) {
   // The Delta pass of a group of rows is HBM-bound; the selection chain that
   // follows it (sums, pick, offsets, gather, select, scan, emit) is mostly
   // launch- and latency-bound.  With a side stream the workers are taken in
@@ -1204,35 +1274,66 @@ hipError_t launch_topk_compress(const DevLayout& lay, const TkDev& tk, int K, fl
   const Launcher main{lay, tk, s};
   const int64_t W = lay.d_pad >> 6;
   // the first Delta pass stamps the start event, the last kernel on s the stop event
-  auto delta = [&](int R, int row0, hipEvent_t start) -> hipError_t {
-    const dim3 grid((unsigned)(lay.n_tiles * R));
-#define SAEF_TKD(MOM, PEND)                                                                  \
-  hipExtLaunchKernelGGL((k_tk_delta<MOM, PEND>), grid, dim3(kBlock), 0, s, start, nullptr, 0, \
-                        lay, tk, R, row0, lr, mu, g, m, e, sel)
-    if (m != nullptr) {
-      if (pend_in) SAEF_TKD(true, true); else SAEF_TKD(true, false);
-    } else {
-      if (pend_in) SAEF_TKD(false, true); else SAEF_TKD(false, false);
-    }
-#undef SAEF_TKD
-    return hipGetLastError();
-  };
-  hipError_t err = delta(R0, 0, ev.start);
+  hipError_t err = main.delta(all, R0, 0, lr, mu, g, m, e, sel, pend_in, ev.start);
   if (err != hipSuccess) return err;
-  if (!split) return main.select_and_emit(K, 0, e, sel, rank, vals, nullptr, pend_out, ev);
+  if (!split) return main.select_and_emit(all, K, 0, e, sel, rank, vals, nullptr, pend_out, ev);
   const int R1 = K - R0;
   if ((err = hipEventRecord(side.fork, s)) != hipSuccess) return err;
   if ((err = hipStreamWaitEvent(side.stream, side.fork, 0)) != hipSuccess) return err;
   const Launcher aside{lay, tk, side.stream};
-  if ((err = aside.select_and_emit(R0, 0, e, sel, rank, vals, nullptr, pend_out,
+  if ((err = aside.select_and_emit(all, R0, 0, e, sel, rank, vals, nullptr, pend_out,
                                    LaunchEvents())) != hipSuccess)
     return err;
   if ((err = hipEventRecord(side.join, side.stream)) != hipSuccess) return err;
-  if ((err = delta(R1, R0, nullptr)) != hipSuccess) return err;
-  if ((err = main.select_and_emit(R1, R0, e + (int64_t)R0 * lay.d_pad, sel + (int64_t)R0 * W,
-                                  rank + (int64_t)R0 * W, vals + (int64_t)R0 * tk.total_keep,
-                                  nullptr, pend_out, ev)) != hipSuccess)
+  if ((err = main.delta(all, R1, R0, lr, mu, g, m, e, sel, pend_in, nullptr)) != hipSuccess)
     return err;
+  if ((err = main.select_and_emit(all, R1, R0, e + (int64_t)R0 * lay.d_pad,
+                                  sel + (int64_t)R0 * W, rank + (int64_t)R0 * W,
+                                  vals + (int64_t)R0 * tk.total_keep, nullptr, pend_out, ev)) !=
+      hipSuccess)
+    return err;
+  return hipStreamWaitEvent(s, side.join, 0);
+}
+
+hipError_t launch_topk_round_end(const DevLayout& lay, const TkDev& tk, const TkPart* parts,
+                                 int n_parts, int K, float lr, float mu, int mode,
+                                 const float* g, float* m, float* e, uint64_t* sel,
+                                 uint32_t* rank, float* vals, bool pend_in, float* e_srv,
+                                 uint64_t* srv_sel, uint32_t* srv_rank, float* srv_vals,
+                                 float* x, hipStream_t s, const TkStreams& side,
+                                 const LaunchEvents& ev) {
+  // Every step after the Delta pass works tensor by tensor, so the parts are
+  // independent once their Delta is formed: the Delta passes of the parts
+  // stream one after another on s, and each part but the last, as soon as
+  // its Delta is stored, runs its worker selection and messages and its
+  // server step on the side stream, under the next parts' Delta passes; the
+  // last part's steps run on s, which then waits for the side stream.  All
+  // data and scratch of two parts are disjoint (tiles, groups, chunks and
+  // (row, tensor) state).
+  const Launcher main{lay, tk, s};
+  const Launcher aside{lay, tk, side.stream};
+  hipError_t err;
+  for (int i = 0; i < n_parts; ++i) {
+    const TkPart& p = parts[i];
+    const bool last = i == n_parts - 1;
+    if ((err = main.delta(p, K, 0, lr, mu, g, m, e, sel, pend_in, i == 0 ? ev.start : nullptr)) !=
+        hipSuccess)
+      return err;
+    const Launcher& on = last ? main : aside;
+    if (!last) {
+      if ((err = hipEventRecord(side.fork, s)) != hipSuccess) return err;
+      if ((err = hipStreamWaitEvent(side.stream, side.fork, 0)) != hipSuccess) return err;
+    }
+    if ((err = on.select_and_emit(p, K, 0, e, sel, rank, vals, nullptr, true, LaunchEvents())) !=
+        hipSuccess)
+      return err;
+    LaunchEvents tail;
+    if (last) tail.stop = ev.stop;
+    if ((err = on.server(p, K, mode, sel, rank, vals, nullptr, e_srv, srv_sel, srv_rank,
+                         srv_vals, x, tail)) != hipSuccess)
+      return err;
+  }
+  if ((err = hipEventRecord(side.join, side.stream)) != hipSuccess) return err;
   return hipStreamWaitEvent(s, side.join, 0);
 }
 
@@ -1261,43 +1362,13 @@ hipError_t launch_topk_materialize(const DevLayout& lay, int K, float* e, const 
   return hipGetLastError();
 }
 
-hipError_t launch_topk_aggregate(const DevLayout& lay, const TkDev& tk, int K, int mode,
-                                 const uint64_t* sel, const uint32_t* rank, const float* vals,
-                                 float* avg, float* e_srv, uint64_t* srv_sel, uint32_t* srv_rank,
-                                 float* srv_vals, float* x, hipStream_t s,
+hipError_t launch_topk_aggregate(const DevLayout& lay, const TkDev& tk, const TkPart& all,
+                                 int K, int mode, const uint64_t* sel, const uint32_t* rank,
+                                 const float* vals, float* avg, float* e_srv, uint64_t* srv_sel,
+                                 uint32_t* srv_rank, float* srv_vals, float* x, hipStream_t s,
                                  const LaunchEvents& ev) {
-  const dim3 grid((unsigned)tk.n_chunks);
-  const double ik = inv_pow2(K);
-  hipEvent_t stop0 = mode == 1 ? nullptr : ev.stop;
-  // dense messages (at least 1/32 of the elements kept): one load per worker
-  // and step, values handed out with ds_bpermute; sparser ones: per-pair
-  // gathers (faster there: at 1% kept 117 against 153 us at resnet50, K = 8;
-  // at 5% and 10%, 281 and 316 us against 265 and 290 us for the server step)
-  const bool co = tk.total_keep * 32 >= lay.d_pad;
-#define SAEF_TKA(M, A, U, C)                                                                       \
-  hipExtLaunchKernelGGL((k_tk_aggregate<M, A, U, C>), grid, dim3(kBig), 0, s, ev.start, stop0, 0, \
-                        lay, tk, K, ik, sel, rank, vals, avg, e_srv, x)
-#define SAEF_TKA_U(M, A)                                 \
-  do {                                                   \
-    if (K <= 8) {                                        \
-      if (co) SAEF_TKA(M, A, 8, true);                   \
-      else SAEF_TKA(M, A, 8, false);                     \
-    } else {                                             \
-      if (co) SAEF_TKA(M, A, 4, true);                   \
-      else SAEF_TKA(M, A, 4, false);                     \
-    }                                                    \
-  } while (0)
-  if (mode == 1) {
-    if (avg != nullptr) SAEF_TKA_U(1, true); else SAEF_TKA_U(1, false);
-  } else {
-    if (avg != nullptr) SAEF_TKA_U(0, true); else SAEF_TKA_U(0, false);
-  }
-#undef SAEF_TKA_U
-#undef SAEF_TKA
-  const hipError_t err = hipGetLastError();
-  if (err != hipSuccess || mode != 1) return err;
-  return Launcher{lay, tk, s}.select_and_emit(1, lay.k_max, e_srv, srv_sel, srv_rank, srv_vals,
-                                              x, false, ev);
+  return Launcher{lay, tk, s}.server(all, K, mode, sel, rank, vals, avg, e_srv, srv_sel,
+                                     srv_rank, srv_vals, x, ev);
 }
 
 }  // namespace saef
