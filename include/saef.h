@@ -276,6 +276,15 @@ int saef_topk_aggregate(const saef_topk* plan, int32_t K, int32_t mode, const ui
  * NULL, then mu must be 0), leaving the kept elements pending, and
  * saef_topk_aggregate with the gradient g the caller computed at xh; t and
  * period must be those of the begin call (they tell whether e is pending).
+ * With two or more tensors the plan's side stream runs part of it: the
+ * tensor list is cut in two runs of whole tensors, and the first run's
+ * selection, messages and server step go to the side stream (after an event
+ * recorded on `stream`) while the second run's worker pass streams on
+ * `stream`, which then waits for the side stream (an event), so the call
+ * stays stream-ordered and capturable in a HIP graph.  The results are those
+ * of saef_topk_compress then saef_topk_aggregate.  Profiled (kind 1), the
+ * whole of it is one timed span, from its first kernel to its last on
+ * `stream`; kind 3 is not used.
  * saef_topk_round is begin (SAEF) + end. */
 int saef_topk_round_begin(const saef_topk* plan, int64_t t, int64_t period, int32_t K,
                           int32_t mode, int32_t variant, float* e, const uint64_t* sel,

@@ -135,10 +135,32 @@ def trace_table(path: str, skip: int) -> None:
         print(f"  {name:40s} {wg:10d} {n:6d} {avg:10.1f} {first:10.1f}")
 
 
+def timeline(path: str, marker: str, index: int) -> None:
+    """The dispatches between the index-th and the next dispatch whose kernel
+    name starts with `marker` (one iteration), in start order: queue (HIP
+    stream), workgroups, start and end in microseconds from the first."""
+    rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Start_Timestamp"]))
+    marks = [i for i, r in enumerate(rows) if short_name(r["Kernel_Name"]).startswith(marker)]
+    if len(marks) < index + 2:
+        raise SystemExit(f"fewer than {index + 2} dispatches of {marker!r}")
+    i0, i1 = marks[index], marks[index + 1]
+    t0 = int(rows[i0]["Start_Timestamp"])
+    print(f"  {'kernel':36s} {'queue':>5s} {'workgroups':>10s} {'start_us':>9s} {'end_us':>9s} "
+          f"{'dur_us':>8s}")
+    for r in rows[i0:i1 + 1]:
+        s, e = int(r["Start_Timestamp"]) - t0, int(r["End_Timestamp"]) - t0
+        wg = int(r["Grid_Size_X"]) // max(1, int(r["Workgroup_Size_X"]))
+        print(f"  {short_name(r['Kernel_Name']):36s} {r['Queue_Id']:>5s} {wg:10d} {s / 1e3:9.1f} "
+              f"{e / 1e3:9.1f} {(e - s) / 1e3:8.1f}")
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--trace", default=None, help="kernel trace CSV (per launch shape table)")
     ap.add_argument("--skip", type=int, default=0, help="first dispatches of each shape left out")
+    ap.add_argument("--timeline", default=None, metavar="MARKER:INDEX",
+                    help="with --trace: the dispatches of one iteration, from the INDEX-th "
+                         "dispatch of a kernel whose name starts with MARKER to the next")
     ap.add_argument("--stats")
     ap.add_argument("--fetch")
     ap.add_argument("--write")
@@ -159,7 +181,11 @@ def main() -> int:
                     help="algorithmic bytes per launch of a kernel, for the ratio column")
     args = ap.parse_args()
     if args.trace:
-        trace_table(args.trace, args.skip)
+        if args.timeline:
+            marker, _, index = args.timeline.rpartition(":")
+            timeline(args.trace, marker, int(index))
+        else:
+            trace_table(args.trace, args.skip)
         return 0
     if not (args.stats and args.fetch and args.write and args.probe_elems):
         ap.error("--stats, --fetch, --write and --probe-elems are required without --trace")
