@@ -62,8 +62,21 @@ constexpr int kTU = SAEF_STEP_WORDS;
 static_assert(kTWaves * kTU * 64 <= kStepElems && kStepElems % (kTWaves * kTU * 64) == 0,
               "a step unit is whole passes of the workgroup");
 // Words per wave per pass in the averaging kernel (it keeps kAvgChunk * kUA
-// errors and sign words live; 8 was 2% slower).
-constexpr int kUA = 4;
+// errors and sign words live), and its work units per tile: 1024-element
+// units of one pass of 4 waves x 4 words, all 8 workers' loads issued
+// together, took 451 us at resnet50 K = 8 against 481 us for whole tiles of
+// two passes with the workers in chunks of 4 (460 us: one pass of 8 words;
+// 479-502 us: 2 words).
+#ifndef SAEF_AVG_WORDS
+#define SAEF_AVG_WORDS 4
+#endif
+#ifndef SAEF_AVG_SPLIT
+#define SAEF_AVG_SPLIT 2
+#endif
+constexpr int kUA = SAEF_AVG_WORDS;
+constexpr int kAvgSplit = SAEF_AVG_SPLIT;
+static_assert(kAvgSplit >= 1 && kAvgSplit <= kStepSplit && kTileElems % (kAvgSplit * 64) == 0,
+              "an averaging unit is whole words of a tile, within the step ahead's grid limit");
 
 // The compression correction C(v)_i = bit ? scale : -scale.
 __device__ __forceinline__ float corr(u64 word, float s) { return sel_by_bit(word, s, -s); }
@@ -401,7 +414,10 @@ __global__ __launch_bounds__(kTBlock) void k_step(DevLayout lay, int K, const fl
 }
 
 // ------------------------------------------------------------------ step ahead with averaging
-constexpr int kAvgChunk = 4;  // workers whose loads are issued together
+#ifndef SAEF_AVG_CHUNK
+#define SAEF_AVG_CHUNK 8
+#endif
+constexpr int kAvgChunk = SAEF_AVG_CHUNK;  // workers whose loads are issued together
 
 // kUA words of one tile starting at word w0 (offsets relative to the tile;
 // lanes past the tile's end compute on zeros and their stores are dropped by
@@ -492,18 +508,24 @@ __global__ __launch_bounds__(kBlock) void k_step_average(DevLayout lay, int K, d
                                                          const float* __restrict__ scales,
                                                          float* __restrict__ xh) {
   int row0;
-  int64_t ti;
-  run_tile_of(blockIdx.x, 1, tile_run_shift(lay.n_tiles), row0, ti);
-  if (ti >= lay.n_tiles) return;
-  const Tile tile = lay.tiles[ti];
+  int64_t unit;
+  const int64_t n_units = lay.n_tiles * kAvgSplit;
+  run_tile_of(blockIdx.x, 1, tile_run_shift(n_units), row0, unit);
+  if (unit >= n_units) return;
+  const Tile tile = lay.tiles[unit / kAvgSplit];
   const int wave = wave_id();
   const int nw = (tile.count + 63) >> 6;
+  // the unit's words of the tile
+  constexpr int kUnitWords = kTileElems / 64 / kAvgSplit;
+  static_assert(kUnitWords % kUA == 0, "a pass stays in its unit");
+  const int uw0 = (int)(unit % kAvgSplit) * kUnitWords;
+  const int uw1 = min(nw, uw0 + kUnitWords);
   const uint32_t nbytes = (uint32_t)tile.count * 4u;
   const uint32_t wbytes = (uint32_t)nw * 8u;
   const Buf rx = buf_of(kXh ? x + tile.start : e, kXh ? nbytes : 0u);
   const Buf rsx = buf_of(kDecX ? (const void*)(ss + (tile.start >> 6)) : e, kDecX ? wbytes : 0u);
   const float s_x = kDecX ? sscales[tile.l] : 0.0f;
-  for (int w0 = wave * kUA; w0 < nw; w0 += kWaves * kUA)
+  for (int w0 = uw0 + wave * kUA; w0 < uw1; w0 += kWaves * kUA)
     average_words<kDecX, kDecE, kXh>(K, inv_k, lay.L, tile.l, lay.d_pad, w0, tile.start, nbytes,
                                      wbytes, rx, rsx, s_x, e, signs, scales, xh);
 }
@@ -1090,7 +1112,7 @@ hipError_t launch_step_ahead(const DevLayout& lay, int K, const float* x,
   if (decode_e < kDecPlain || decode_e > kDecZero) return hipErrorInvalidValue;
   if (decode_x && decode_e != kDecSign) return hipErrorInvalidValue;  // never requested
   if (average) {
-    const dim3 grid((unsigned)run_padded_tiles(lay.n_tiles));
+    const dim3 grid((unsigned)run_padded_tiles(lay.n_tiles * kAvgSplit));
     const double ik = inv_pow2(K);
 #define SAEF_AV(DX, DE, XH)                                                                  \
   SAEF_LAUNCH((k_step_average<DX, DE, XH>), grid, dim3(kBlock), 0, s, lay, K, ik, x, \
