@@ -8,13 +8,18 @@ namespace saef {
 
 // Pass-1 histogram of the key |v| over a window of four binades (exponents)
 // of a (row, tensor), placed around the previous call's threshold: 64 bins
-// per binade (key bits 22..17) inside the window, one bin below it and one
-// above it.  The window only decides how many elements become candidates;
-// the kept set is exact wherever the threshold falls.
+// per binade (key bits 22..17) inside the window; below it one bin per binade
+// for the kTkLo - 1 binades under the window and one bin for all lower keys;
+// one bin above it.  The window only decides how many elements become
+// candidates; the kept set is exact wherever the threshold falls.  (With one
+// bin below, a threshold that fell more than two binades made every element
+// under the window a candidate: at bert_base Top-1% the selection of the word
+// embedding then took 10-23 ms.  Above the window there are few elements.)
 constexpr int kTkSubShift = 17;                // in-window bin width: 2^17 keys
 constexpr int kTkWin = 256;                    // in-window bins (4 binades)
-constexpr int kTkHist = kTkWin + 2;            // + below, + above
-constexpr int kTkHistPad = 260;                // 16-bit counts per tile (even, 8-byte rows)
+constexpr int kTkLo = 8;                       // bins below the window
+constexpr int kTkHist = kTkLo + kTkWin + 1;    // + one above
+constexpr int kTkHistPad = 268;                // 16-bit counts per tile (even, 8-byte rows)
 constexpr int kTkGroup = 64;      // tile histograms (or group sums) one sum workgroup adds
 constexpr int kTkBins = 2048;     // bins of an 11-bit radix digit
 constexpr int kTkChunk = 65536;   // elements per server-aggregation workgroup
@@ -29,7 +34,7 @@ constexpr int kTkChunk = 65536;   // elements per server-aggregation workgroup
 // feedback the threshold mostly rises from call to call, and the elements
 // just below it pile up: at 1% kept the lists hold about 3% of the elements.)
 constexpr int kTkSpecCap = 512;
-constexpr int kTkSpecSlot = kTkHist;
+constexpr int kTkSpecSlot = (kTkHist + 1) & ~1;  // the first even slot past the bins
 constexpr uint32_t kTkSpecNone = 0xFFFFu;
 constexpr uint32_t kTkSpecMargin = 1u << 18;
 constexpr int kTkSpecMaxShare = 8;  // lists when k_l * 8 <= n_l
@@ -39,7 +44,7 @@ constexpr int kTkSpecMaxShare = 8;  // lists when k_l * 8 <= n_l
 // plans (saef_topk_create returns SAEF_EINVAL).
 constexpr int kTkTileElems = 2048;
 constexpr bool kTkUsable = kTileElems == kTkTileElems;
-static_assert(kTkHistPad >= kTkHist && kTkHistPad % 4 == 0, "padded tile histogram");
+static_assert(kTkHistPad >= kTkSpecSlot + 2 && kTkHistPad % 4 == 0, "padded tile histogram");
 static_assert(kTkTileElems < 65536, "a tile's bin counts fit 16 bits");
 static_assert(kTkChunk % kTkTileElems == 0, "a server chunk holds whole tiles");
 static_assert(kTkSpecSlot < kTkHistPad && kTkSpecSlot % 2 == 0, "a spare, even histogram slot");

@@ -8,7 +8,8 @@
 //              also counts the keys into a tile histogram (LDS atomics,
 //              16-bit counts stored): 64 bins per binade over a window of
 //              four binades placed around the (row, tensor)'s previous
-//              threshold, one bin below the window and one above it;
+//              threshold, one bin per binade for seven binades below it,
+//              one for the keys further down and one above the window;
 //   sum        tile histograms are added per group of 64 tiles (and groups
 //              per super-group for very large tensors);
 //   pick       a workgroup per (row, tensor) finds the bin b1 that holds the
@@ -70,13 +71,18 @@ constexpr int kBufWord3 = 0x00020000;
 
 __device__ __forceinline__ uint32_t key_of(float v) { return __float_as_uint(v) & 0x7FFFFFFFu; }
 
-// Pass-1 bin of a key for the window [win, win + 4 binades): 0 below it,
-// 1 .. kTkWin inside it (key bits 22..17 within each binade), kTkWin + 1
-// above it.  Bins order like the keys.
+// Pass-1 bin of a key for the window [win, win + 4 binades) (win a multiple
+// of 2^23, its binade wb): below it, bin kTkLo - j for binade wb - j (j <
+// kTkLo) and bin 0 for all lower keys; kTkLo .. kTkLo + kTkWin - 1 inside it
+// (key bits 22..17 within each binade); kTkLo + kTkWin above it.  Bins order
+// like the keys.
 __device__ __forceinline__ uint32_t hist_bin(uint32_t key, uint32_t win) {
-  if (key < win) return 0u;
-  const uint32_t d = (key - win) >> kTkSubShift;
-  return d < (uint32_t)kTkWin ? d + 1u : (uint32_t)kTkWin + 1u;
+  const int32_t s = (int32_t)(key - win);  // keys and win are below 2^31
+  const uint32_t d = (uint32_t)s >> kTkSubShift;
+  if (d < (uint32_t)kTkWin) return (uint32_t)kTkLo + d;
+  if (s >= 0) return (uint32_t)(kTkLo + kTkWin);
+  const int32_t j = s >> 23;  // -(binades below the window's first): <= -1 (win is 2^23-aligned)
+  return (uint32_t)max(j + kTkLo, 0);
 }
 
 // The window for the next call: the binade of tau is the third of four.
@@ -397,13 +403,40 @@ __global__ __launch_bounds__(kWave) void k_tk_offsets(DevLayout lay, TkDev tk, T
 }
 
 // ------------------------------------------------------------------ gather
-// The smallest key of bin b for the window at win; kTkHist (one past the
-// last bin) gives 2^31, above every key.
+// The smallest key of bin b for the window at win (hist_bin's layout; a
+// below bin for a binade under 0 is empty and starts at 0); kTkHist (one
+// past the last bin) gives 2^31, above every key.
 __device__ __forceinline__ uint32_t bin_floor(uint32_t b, uint32_t win) {
+  const int64_t wb = win >> 23;
   if (b == 0u) return 0u;
   if (b >= (uint32_t)kTkHist) return 0x80000000u;
-  const u64 f = (u64)win + ((u64)(b - 1u) << kTkSubShift);
-  return f < 0x80000000ull ? (uint32_t)f : 0x80000000u;
+  int64_t f;
+  if (b < (uint32_t)kTkLo) {
+    const int64_t kb = wb - (kTkLo - (int64_t)b);  // the bin's binade
+    f = kb > 0 ? kb << 23 : 0;
+  } else if (b < (uint32_t)(kTkLo + kTkWin)) {
+    f = (int64_t)win + ((int64_t)(b - kTkLo) << kTkSubShift);
+  } else {
+    f = (wb + 4) << 23;  // the bin above the window
+  }
+  return f < 0x80000000ll ? (uint32_t)f : 0x80000000u;
+}
+
+// The key bits bin b fixes: keys of the bin are those with key >> open ==
+// prefix (open = 17 inside the window, 23 for a one-binade bin, 31 for the
+// lowest bin and the one above the window).
+__device__ __forceinline__ void bin_prefix(uint32_t b, uint32_t win, uint32_t& prefix, int& open) {
+  const uint32_t wb = win >> 23;
+  if (b >= (uint32_t)kTkLo && b < (uint32_t)(kTkLo + kTkWin)) {
+    prefix = (win >> kTkSubShift) + (b - kTkLo);
+    open = kTkSubShift;
+  } else if (b >= 1u && b < (uint32_t)kTkLo && wb >= (uint32_t)kTkLo - b) {
+    prefix = wb - ((uint32_t)kTkLo - b);
+    open = 23;
+  } else {
+    prefix = 0u;
+    open = 31;
+  }
 }
 
 // The gather's classification of a tile's 32 words (kFull: all 2048
@@ -603,8 +636,8 @@ __device__ void cand_hist(uint32_t* h, int nb, const u64* __restrict__ cand, int
 // Grid: R * nl workgroups of kBig threads (as k_tk_pick).  Among the candidates of (row,
 // tensor) (the elements of bin b1), takes the `need` largest keys, equal
 // keys by lower index: radix passes of up to 11 bits over the key bits that
-// b1 leaves open (bits 16..0 inside the window; all 31 for the bins below
-// and above it) give the threshold key tau and how many of the elements
+// b1 leaves open (bits 16..0 inside the window, 22..0 for a one-binade bin,
+// all 31 for the lowest bin and the one above) give the threshold key tau and how many of the elements
 // equal to tau are kept; if not all, passes on the index in the tensor
 // (bits 27..17, 16..6, 5..0) give the last kept index iota.  The next
 // call's window is placed around tau.
@@ -622,9 +655,9 @@ __global__ __launch_bounds__(kBig) void k_tk_select(DevLayout lay, TkDev tk, TkP
   const int64_t C = st->cand;
   const uint32_t b1 = st->bin, win = st->win;
   int64_t need = st->need;
-  const bool inside = b1 >= 1u && b1 <= (uint32_t)kTkWin;
-  uint32_t prefix = inside ? (win >> kTkSubShift) + (b1 - 1u) : 0u;  // key >> open
-  int open = inside ? kTkSubShift : 31;
+  uint32_t prefix;  // key >> open of every candidate
+  int open;
+  bin_prefix(b1, win, prefix, open);
   uint32_t bin = 0, cnt = 0;
   int64_t left = need;
   while (open > 0) {
