@@ -298,9 +298,12 @@ def test_topk_aggregate_parity(mode, K):
 
 
 # data scale of successive calls on one plan: the threshold falls far below
-# the histogram window placed by the previous call (the bin below it), far
-# above it (the bin above it), then back inside it
-SCALES = [1.0, 2.0 ** -20, 2.0 ** 30, 2.0 ** 30 * 1.5, 1.0]
+# the histogram window placed by the previous call (the lowest bin), far
+# above it (the bin above it), back inside it, then 4, 3, 10 and 5 binades
+# down in turn (the one-binade bins below the window, 2 and 1 binades under
+# it, and the lowest bin again) with jumps back up in between
+SCALES = [1.0, 2.0 ** -20, 2.0 ** 30, 2.0 ** 30 * 1.5, 1.0, 2.0 ** -4, 2.0 ** -7, 1.0,
+          2.0 ** -10, 2.0 ** -5, 1.0]
 
 
 def test_topk_threshold_moves():
