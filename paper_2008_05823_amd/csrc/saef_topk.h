@@ -38,6 +38,13 @@ constexpr int kTkSpecSlot = (kTkHist + 1) & ~1;  // the first even slot past the
 constexpr uint32_t kTkSpecNone = 0xFFFFu;
 constexpr uint32_t kTkSpecMargin = 1u << 18;
 constexpr int kTkSpecMaxShare = 8;  // lists when k_l * 8 <= n_l
+// Dynamic LDS the Delta pass requests and does not use: with its own 1 KB
+// it keeps at most 5 of its workgroups on a CU (160 KB of LDS), so the
+// selection kernels of the other rows or tensors, launched on the side
+// stream while a Delta pass streams, find free slots.  At resnet50 K = 8
+// Top-1% per iteration: 1.014 ms against 1.030 ms uncapped, 1.017 ms with
+// only the overlapped pass capped, 1.022 ms at 4 workgroups per CU.
+constexpr unsigned kTkDeltaLdsPad = 26624;
 // The Top-K kernels take a tile as 32 sign words (one per lane of a gather
 // wave): they need the layout's tiles to hold 2048 elements.  A library built
 // with another SAEF_TILE_ELEMS (the sign path works with any) refuses Top-K

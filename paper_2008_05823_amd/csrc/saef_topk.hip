@@ -1191,8 +1191,8 @@ struct Launcher {
                    hipEvent_t start) const {
     const dim3 grid((unsigned)((int64_t)(p.t1 - p.t0) * R));
 #define SAEF_TKD(MOM, PEND)                                                                  \
-  hipExtLaunchKernelGGL((k_tk_delta<MOM, PEND>), grid, dim3(kBlock), 0, s, start, nullptr, 0, \
-                        lay, tk, p, R, row0, lr, mu, g, m, e, psel)
+  hipExtLaunchKernelGGL((k_tk_delta<MOM, PEND>), grid, dim3(kBlock), kTkDeltaLdsPad, s, start, \
+                        nullptr, 0, lay, tk, p, R, row0, lr, mu, g, m, e, psel)
     if (m != nullptr) {
       if (pend_in) SAEF_TKD(true, true); else SAEF_TKD(true, false);
     } else {
