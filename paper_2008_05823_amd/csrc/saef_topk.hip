@@ -1291,6 +1291,14 @@ struct Launcher {
 
 }  // namespace
 
+// After a fork, an error still joins: s waits for whatever the side stream
+// was given, so no work of this call outlives it on the side stream.
+static hipError_t join_side(hipStream_t s, const TkStreams& side, hipError_t err) {
+  const hipError_t e1 = hipEventRecord(side.join, side.stream);
+  const hipError_t e2 = e1 == hipSuccess ? hipStreamWaitEvent(s, side.join, 0) : e1;
+  return err != hipSuccess ? err : e2;
+}
+
 hipError_t launch_topk_compress(const DevLayout& lay, const TkDev& tk, const TkPart& all, int K,
                                 float lr, float mu, const float* g, float* m, float* e,
                                 uint64_t* sel, uint32_t* rank, float* vals, bool pend_in,
@@ -1314,18 +1322,13 @@ hipError_t launch_topk_compress(const DevLayout& lay, const TkDev& tk, const TkP
   if ((err = hipEventRecord(side.fork, s)) != hipSuccess) return err;
   if ((err = hipStreamWaitEvent(side.stream, side.fork, 0)) != hipSuccess) return err;
   const Launcher aside{lay, tk, side.stream};
-  if ((err = aside.select_and_emit(all, R0, 0, e, sel, rank, vals, nullptr, pend_out,
-                                   LaunchEvents())) != hipSuccess)
-    return err;
-  if ((err = hipEventRecord(side.join, side.stream)) != hipSuccess) return err;
-  if ((err = main.delta(all, R1, R0, lr, mu, g, m, e, sel, pend_in, nullptr)) != hipSuccess)
-    return err;
-  if ((err = main.select_and_emit(all, R1, R0, e + (int64_t)R0 * lay.d_pad,
-                                  sel + (int64_t)R0 * W, rank + (int64_t)R0 * W,
-                                  vals + (int64_t)R0 * tk.total_keep, nullptr, pend_out, ev)) !=
-      hipSuccess)
-    return err;
-  return hipStreamWaitEvent(s, side.join, 0);
+  err = aside.select_and_emit(all, R0, 0, e, sel, rank, vals, nullptr, pend_out, LaunchEvents());
+  if (err == hipSuccess) err = main.delta(all, R1, R0, lr, mu, g, m, e, sel, pend_in, nullptr);
+  if (err == hipSuccess)
+    err = main.select_and_emit(all, R1, R0, e + (int64_t)R0 * lay.d_pad, sel + (int64_t)R0 * W,
+                               rank + (int64_t)R0 * W, vals + (int64_t)R0 * tk.total_keep,
+                               nullptr, pend_out, ev);
+  return join_side(s, side, err);
 }
 
 hipError_t launch_topk_round_end(const DevLayout& lay, const TkDev& tk, const TkPart* parts,
@@ -1345,29 +1348,27 @@ hipError_t launch_topk_round_end(const DevLayout& lay, const TkDev& tk, const Tk
   // (row, tensor) state).
   const Launcher main{lay, tk, s};
   const Launcher aside{lay, tk, side.stream};
-  hipError_t err;
-  for (int i = 0; i < n_parts; ++i) {
+  hipError_t err = hipSuccess;
+  bool forked = false;
+  for (int i = 0; i < n_parts && err == hipSuccess; ++i) {
     const TkPart& p = parts[i];
     const bool last = i == n_parts - 1;
-    if ((err = main.delta(p, K, 0, lr, mu, g, m, e, sel, pend_in, i == 0 ? ev.start : nullptr)) !=
-        hipSuccess)
-      return err;
-    const Launcher& on = last ? main : aside;
-    if (!last) {
-      if ((err = hipEventRecord(side.fork, s)) != hipSuccess) return err;
-      if ((err = hipStreamWaitEvent(side.stream, side.fork, 0)) != hipSuccess) return err;
+    err = main.delta(p, K, 0, lr, mu, g, m, e, sel, pend_in, i == 0 ? ev.start : nullptr);
+    if (err == hipSuccess && !last) {
+      err = hipEventRecord(side.fork, s);
+      if (err == hipSuccess) err = hipStreamWaitEvent(side.stream, side.fork, 0);
+      forked = forked || err == hipSuccess;
     }
-    if ((err = on.select_and_emit(p, K, 0, e, sel, rank, vals, nullptr, true, LaunchEvents())) !=
-        hipSuccess)
-      return err;
+    const Launcher& on = last ? main : aside;
+    if (err == hipSuccess)
+      err = on.select_and_emit(p, K, 0, e, sel, rank, vals, nullptr, true, LaunchEvents());
     LaunchEvents tail;
     if (last) tail.stop = ev.stop;
-    if ((err = on.server(p, K, mode, sel, rank, vals, nullptr, e_srv, srv_sel, srv_rank,
-                         srv_vals, x, tail)) != hipSuccess)
-      return err;
+    if (err == hipSuccess)
+      err = on.server(p, K, mode, sel, rank, vals, nullptr, e_srv, srv_sel, srv_rank, srv_vals,
+                      x, tail);
   }
-  if ((err = hipEventRecord(side.join, side.stream)) != hipSuccess) return err;
-  return hipStreamWaitEvent(s, side.join, 0);
+  return forked ? join_side(s, side, err) : err;
 }
 
 // Grid: n_tiles * K workgroups; workgroup b sets to 0 the elements of worker
