@@ -233,9 +233,13 @@ typedef struct saef_topk saef_topk;
  * of the k_max worker rows).  The selection state
  * keeps, per worker row and tensor, where the last call found its threshold:
  * the next call's histogram is placed there, so the first call on a plan (or
- * one after the data scale jumped by more than about two binades) takes
- * longer; the results never depend on it.  Calls using one plan must not run
- * concurrently.  Synchronises the device; the layout must outlive the plan. */
+ * one after the data scale rose by more than about two binades, or fell by
+ * more than about nine) takes longer; the results never depend on it.  The
+ * plan also owns a second HIP stream (default priority) and two events:
+ * saef_topk_compress and saef_topk_round_end give part of their work to that
+ * stream and make the caller's stream wait for it before they return.
+ * Calls using one plan must not run concurrently.  Synchronises the device;
+ * the layout must outlive the plan. */
 int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk** out);
 int saef_topk_destroy(saef_topk* plan);
 /* total = sum keep, the length of one message's value array. */
