@@ -27,10 +27,10 @@
 //              the threshold key tau and the last kept index iota of the
 //              elements equal to tau (radix passes on the key bits below
 //              b1's prefix, then on the index), and places the next call's
-//              window around tau;
-//   scan       a workgroup per (row, tensor) counts each tile's kept elements
-//              (its definite ones, from the gather, and its kept candidates)
-//              and turns the counts into each tile's first rank;
+//              window around tau; the same workgroup then counts each
+//              tile's kept elements (its definite ones, from the gather, and
+//              its kept candidates) and turns the counts into each tile's
+//              first rank;
 //   emit       one wave per tile adds its kept candidates to its selection
 //              words, then writes the rank words and the kept values in
 //              index order, and sets the kept elements of the error to 0
@@ -640,7 +640,10 @@ __device__ void cand_hist(uint32_t* h, int nb, const u64* __restrict__ cand, int
 // all 31 for the lowest bin and the one above) give the threshold key tau and how many of the elements
 // equal to tau are kept; if not all, passes on the index in the tensor
 // (bits 27..17, 16..6, 5..0) give the last kept index iota.  The next
-// call's window is placed around tau.
+// call's window is placed around tau.  Then each tile's kept count and first
+// rank (tile_ranks).
+__device__ void tile_ranks(const DevLayout& lay, const TkDev& tk, int row, int l, int64_t C,
+                           const TkSel& st, uint32_t* s_cnt, uint32_t* s_scan);
 __global__ __launch_bounds__(kBig) void k_tk_select(DevLayout lay, TkDev tk, TkPart p,
                                                      int row0) {
   __shared__ uint32_t h[kTkBins];
@@ -698,6 +701,14 @@ __global__ __launch_bounds__(kBig) void k_tk_select(DevLayout lay, TkDev tk, TkP
     st->iota = iota;
     st->win = window_for(tau);
   }
+  // every thread holds tau and iota; h (free once the last find_bin is done)
+  // holds the per-tile counts
+  static_assert(kTkBins >= kBig, "a count per thread of the workgroup");
+  __syncthreads();
+  TkSel kept{};
+  kept.tau = tau;
+  kept.iota = iota;
+  tile_ranks(lay, tk, row, l, C, kept, h, s_scan);
 }
 
 // ------------------------------------------------------------------ emit
@@ -721,41 +732,37 @@ __device__ __forceinline__ bool cand_kept(u64 e, const TkSel& st) {
   return key > st.tau || (key == st.tau && idx <= st.iota);
 }
 
-// Grid: R * nl workgroups (as k_tk_pick).  Each tile's kept count (the gather's count of
-// definite elements plus its kept candidates), then the exclusive prefix
-// over the tensor's tiles in tile order, in place.  The candidates of a
-// block of kBlock tiles are contiguous: the whole workgroup reads them and
-// counts the kept ones per tile in LDS.
-__global__ __launch_bounds__(kBlock) void k_tk_scan(DevLayout lay, TkDev tk, TkPart p, int row0) {
+// Each tile's kept count (the gather's count of definite elements plus its
+// kept candidates), then the exclusive prefix over the tensor's tiles in
+// tile order, in place, for (row, tensor l) with threshold st.tau / st.iota
+// and C candidates.  The candidates of a block of blockDim tiles are
+// contiguous: the whole workgroup reads them and counts the kept ones per
+// tile in s_cnt (blockDim entries of LDS).
+__device__ void tile_ranks(const DevLayout& lay, const TkDev& tk, int row, int l, int64_t C,
+                           const TkSel& st, uint32_t* s_cnt, uint32_t* s_scan) {
   constexpr int kIlp = 4;
-  __shared__ uint32_t s_scan[kWaves];
-  __shared__ uint32_t s_cnt[kBlock];
-  const int nl = p.l1 - p.l0;
-  const int l = p.l0 + (int)(blockIdx.x % (unsigned)nl);
-  const int r = (int)(blockIdx.x / (unsigned)nl);
-  const int row = row0 + r;
+  const int nt = (int)blockDim.x;
   const TensorInfo ten = lay.tensors[l];
-  const TkSel st = tk.sel[(int64_t)row * lay.L + l];
   const u64* cand = tk.cand + (int64_t)row * lay.d_pad + ten.off;
   const uint32_t* co = tk.cand_off + (int64_t)row * lay.n_tiles + ten.first_tile;
   uint32_t* cnt = tk.tile_cnt + (int64_t)row * lay.n_tiles + ten.first_tile;
   uint32_t carry = 0;
-  for (int b = 0; b < ten.ntiles; b += kBlock) {
+  for (int b = 0; b < ten.ntiles; b += nt) {
     s_cnt[threadIdx.x] = 0;
     __syncthreads();
     const uint32_t lo = co[b];
-    const uint32_t hi = b + kBlock < ten.ntiles ? co[b + kBlock] : (uint32_t)st.cand;
-    for (uint32_t c0 = lo + threadIdx.x; c0 < hi; c0 += kBlock * kIlp) {
+    const uint32_t hi = b + nt < ten.ntiles ? co[b + nt] : (uint32_t)C;
+    for (uint32_t c0 = lo + threadIdx.x; c0 < hi; c0 += (uint32_t)(nt * kIlp)) {
       u64 e[kIlp];
 #pragma unroll
       for (int u = 0; u < kIlp; ++u) {
-        const uint32_t c = c0 + u * kBlock;
+        const uint32_t c = c0 + (uint32_t)(u * nt);
         e[u] = cand[c < hi ? c : lo];  // lo < hi here
       }
 #pragma unroll
       for (int u = 0; u < kIlp; ++u) {
         const int64_t t = (int64_t)(e[u] >> 32) / kTkTileElems - b;  // tile of the block
-        if (c0 + u * kBlock < hi && cand_kept(e[u], st) && t >= 0 && t < kBlock)
+        if (c0 + (uint32_t)(u * nt) < hi && cand_kept(e[u], st) && t >= 0 && t < nt)
           atomicAdd(&s_cnt[t], 1u);
       }
     }
@@ -1203,7 +1210,8 @@ struct Launcher {
   }
 
   // everything after the first pass for R rows of `data` (rows row0..) over
-  // the part's tensors: sums, pick, offsets, gather, select, scan, emit.
+  // the part's tensors: sums, pick, offsets, gather, select (with the tile
+  // ranks), emit.
   // The last kernel stamps the caller's stop event.
   hipError_t select_and_emit(const TkPart& p, int R, int row0, float* data, uint64_t* sel,
                              uint32_t* rank, float* vals, float* x, bool pend_out,
@@ -1233,8 +1241,6 @@ struct Launcher {
       SAEF_LAUNCH(k_tk_gather_full, tiles, dim3(kBlock), 0, s, lay, tk, p, R, row0, data, sel);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     SAEF_LAUNCH(k_tk_select, pairs, dim3(kBig), 0, s, lay, tk, p, row0);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
-    SAEF_LAUNCH(k_tk_scan, pairs, dim3(kBlock), 0, s, lay, tk, p, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     if (x != nullptr)
       hipExtLaunchKernelGGL((k_tk_emit<true, false>), tiles, dim3(kBlock), 0, s, nullptr,
