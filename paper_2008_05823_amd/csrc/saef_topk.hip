@@ -1013,7 +1013,89 @@ __device__ __forceinline__ AggStep<U> agg_words(const uint64_t* __restrict__ sel
   return a;
 }
 
-template <int kMode, bool kAvg, int U, bool kCo>
+// How a pass gathers the K messages' values: per (worker, word) pair, one
+// load per worker for dense messages, or over the pass's union (below).
+constexpr int kTkAggPairs = 0;
+constexpr int kTkAggDense = 1;
+constexpr int kTkAggUnion = 2;
+
+// The means of a pass of U words when one batch holds every worker (K <= kWave
+// / U; lane q holds the words of worker q / U, word q % U): the elements that
+// some worker kept (the union of the K selection words of each word) are
+// taken 64 at a time, one per lane, and each lane gathers its element's K
+// values (a worker that did not keep it reads past the end of its buffer and
+// gets 0), so a sparse pass costs K loads per 64 union elements instead of
+// one per (worker, word) pair.  The sum runs over all kWave / U workers in
+// order in binary64 (absent ones add +0), as in the per-pair gathers, so the
+// means are the same bits.  mb (U x 64 floats, the wave's own) returns them
+// per element; an element no worker kept has mean +0.
+template <int U>
+__device__ __forceinline__ void union_means(const AggStep<U>& cur, int K, double inv_k,
+                                            const float* __restrict__ vals, int64_t total_keep,
+                                            uint32_t keep, int lane, float* __restrict__ mb,
+                                            float (&mean)[U]) {
+  constexpr int kB = kWave / U;
+#pragma unroll
+  for (int i = 0; i < U; ++i) mb[i * kWave + lane] = 0.0f;
+  // the union of word q % U in every lane q (absent workers hold empty words)
+  uint32_t ulo = cur.lo, uhi = cur.hi;
+#pragma unroll
+  for (int off = U; off < kWave; off <<= 1) {
+    ulo |= (uint32_t)__shfl_xor((int)ulo, off);
+    uhi |= (uint32_t)__shfl_xor((int)uhi, off);
+  }
+  // inclusive scan of the union counts over the U words (every group of U
+  // lanes holds the same counts and scans them alike)
+  const uint32_t cnt = (uint32_t)(__popc(ulo) + __popc(uhi));
+  uint32_t incl = cnt;
+#pragma unroll
+  for (int off = 1; off < U; off <<= 1) {
+    const uint32_t y = (uint32_t)__shfl_up((int)incl, off);
+    if ((lane % U) >= off) incl += y;
+  }
+  const uint32_t excl = incl - cnt;
+  const uint32_t total = (uint32_t)__shfl((int)incl, U - 1);  // union elements of the pass
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  for (uint32_t i0 = 0; i0 < total; i0 += kWave) {
+    const uint32_t i = i0 + (uint32_t)lane;  // the i-th union element of the pass
+    // its word: the number of words whose inclusive count is <= i (capped at
+    // U - 1 for lanes past the end, which load and store nothing)
+    int u = 0;
+#pragma unroll
+    for (int step = U / 2; step >= 1; step >>= 1)
+      if ((uint32_t)__shfl((int)incl, u + step - 1) <= i) u += step;
+    const uint32_t wlo = (uint32_t)__shfl((int)ulo, u), whi = (uint32_t)__shfl((int)uhi, u);
+    const uint32_t wex = (uint32_t)__shfl((int)excl, u);
+    const int b = nth_set_bit(((u64)whi << 32) | wlo, i - wex);
+    const bool live = i < total;
+    const u64 below_mask = (1ull << b) - 1ull;
+    float v[kB];
+#pragma unroll
+    for (int kk = 0; kk < kB; ++kk) {
+      const int kidx = min(kk, K - 1);  // absent workers have empty words
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+          (void*)(vals + (int64_t)kidx * total_keep), 0, (int)(keep * 4u), kBufWord3);
+      const int q = kk * U + u;
+      const uint32_t lo = (uint32_t)__shfl((int)cur.lo, q);
+      const uint32_t hi = (uint32_t)__shfl((int)cur.hi, q);
+      const uint32_t r4 = (uint32_t)__shfl((int)cur.rk4, q);
+      const u64 w = ((u64)hi << 32) | lo;
+      const bool bit = live && ((w >> b) & 1ull) != 0ull;
+      const uint32_t off = bit ? r4 + 4u * (uint32_t)__popcll(w & below_mask) : 0x80000000u;
+      v[kk] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0));
+    }
+    double acc = 0.0;
+#pragma unroll
+    for (int kk = 0; kk < kB; ++kk) acc += (double)v[kk];  // worker order; absent: +0
+    if (live) mb[u * kWave + b] = (float)mean_of(acc, inv_k, K);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+#pragma unroll
+  for (int i = 0; i < U; ++i) mean[i] = mb[i * kWave + lane];
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+}
+
+template <int kMode, bool kAvg, int U, int kPath>
 __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, TkPart p,
                                                        int K, double inv_k,
                                                        const uint64_t* __restrict__ sel,
@@ -1027,6 +1109,9 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
   static_assert(kTileWords % U == 0, "a pass of U words stays in one tile");
   constexpr int kChunkTiles = kTkChunk / kTkTileElems;
   __shared__ uint32_t h[kMode == 1 ? kChunkTiles * kTkHistPad : 1];  // per tile of the chunk
+  __shared__ float mb[kPath == kTkAggUnion ? (kBig / kWave) * U * kWave : 1];  // a pass's means
+  static_assert(kPath != kTkAggUnion || U * kWave <= (int)(sizeof(mb) / sizeof(float)),
+                "a wave's means");
   const int64_t ci = p.c0 + (int64_t)blockIdx.x;
   const TkChunk c = tk.chunks[ci];
   const int64_t voff = tk.tens[c.l].voff;
@@ -1050,125 +1135,137 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
     // e_srv (mode 1) or x (mode 0) of the pass; elements past the chunk are
     // loaded at its first element and never stored
     float dv[U];
-    double acc[U];
 #pragma unroll
     for (int i = 0; i < U; ++i) {
       const int j = (w0 + i) * 64 + lane;
       dv[i] = __builtin_nontemporal_load(dr + ((w0 + i < nw && j < c.count) ? j : 0));
-      acc[i] = 0.0;
     }
-    for (int k0 = 0; k0 < K; k0 += kB) {
-      // the next step's words go out before this step's values are waited for
-      const bool last_b = k0 + kB >= K;
-      const int nw0 = last_b ? w0 + stride : w0;
-      const AggStep<U> nxt = agg_words<U>(sel, rank, W, gw, K, nw, nw0, last_b ? 0 : k0 + kB, lane);
-      // This step's values, read through a buffer resource over each worker's
-      // k_l values (a read past the end gets 0 from the range check, with no
-      // memory access).
-      bool done = false;
-      if (kCo) {
-        // Dense messages: the kept values of a worker's U words are contiguous
-        // in its message; when no worker of the step has more than 64 of them,
-        // one load per worker brings them all (lane j: the group's j-th
-        // value) and each element takes its own with ds_bpermute.
-        uint32_t gcnt = (uint32_t)(__popc(cur.lo) + __popc(cur.hi));
-#pragma unroll
-        for (int off = 1; off < U; off <<= 1) gcnt += (uint32_t)__shfl_xor((int)gcnt, off);
-        if (__ballot(gcnt > (uint32_t)kWave) == 0ull) {  // wave-uniform
-          float gv[kB];
-#pragma unroll
-          for (int kk = 0; kk < kB; ++kk) {
-            const int kidx = min(k0 + kk, K - 1);  // absent workers have empty words
-            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-                (void*)(vals + (int64_t)kidx * tk.total_keep + voff), 0, (int)(keep * 4u),
-                kBufWord3);
-            const uint32_t g4 = __builtin_amdgcn_readlane(cur.rk4, kk * U);  // group's first rank
-            gv[kk] = __uint_as_float(
-                __builtin_amdgcn_raw_buffer_load_b32(rs, g4 + 4u * (uint32_t)lane, 0, 0));
-          }
-#pragma unroll
-          for (int kk = 0; kk < kB; ++kk) {
-            const uint32_t g4 = __builtin_amdgcn_readlane(cur.rk4, kk * U);
-            // the U shuffles of the worker go out together (distinct
-            // registers), then their values are added
-            int pv[U];
-#pragma unroll
-            for (int i = 0; i < U; ++i) {
-              const int q = kk * U + i;
-              const uint32_t mlo = __builtin_amdgcn_readlane(cur.lo, q);
-              const uint32_t mhi = __builtin_amdgcn_readlane(cur.hi, q);
-              const uint32_t r4 = __builtin_amdgcn_readlane(cur.rk4, q);
-              // the lane's element: its position among the group's kept values
-              const uint32_t below =
-                  __builtin_amdgcn_mbcnt_hi(mhi, __builtin_amdgcn_mbcnt_lo(mlo, 0u));
-              const int src = (int)((r4 - g4) + 4u * below);  // < 4 * 64 for a kept element
-              pv[i] = __builtin_amdgcn_ds_bpermute(src, __float_as_int(gv[kk]));
-            }
-#pragma unroll
-            for (int i = 0; i < U; ++i) {
-              const int q = kk * U + i;
-              const uint32_t mlo = __builtin_amdgcn_readlane(cur.lo, q);
-              const uint32_t mhi = __builtin_amdgcn_readlane(cur.hi, q);
-              acc[i] += (double)sel_by_bit(((u64)mhi << 32) | mlo, __int_as_float(pv[i]),
-                                           0.0f);  // worker order
-            }
-          }
-          done = true;
-        }
-      }
-      if (!done) {
-        // Sparse messages (or a worker with more than 64 kept values in the
-        // step's words): every (worker, word) pair gathers its values, a lane
-        // whose bit is clear reading past the end; the loads go out before the
-        // first one is used (with kCo, one worker at a time, which needs fewer
-        // registers next to the dense path).
-        constexpr int kW = kCo ? 1 : kB;  // workers whose loads go out together
-        for (int kw = 0; kw < kB; kw += kW) {
-          float cv[kW][U];
-#pragma unroll
-          for (int kx = 0; kx < kW; ++kx) {
-            const int kk = kw + kx;
-            const int kidx = min(k0 + kk, K - 1);  // absent workers have empty words
-            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-                (void*)(vals + (int64_t)kidx * tk.total_keep + voff), 0, (int)(keep * 4u),
-                kBufWord3);
-#pragma unroll
-            for (int i = 0; i < U; ++i) {
-              const int q = kk * U + i;
-              const uint32_t mlo = __builtin_amdgcn_readlane(cur.lo, q);
-              const uint32_t mhi = __builtin_amdgcn_readlane(cur.hi, q);
-              const uint32_t r4 = __builtin_amdgcn_readlane(cur.rk4, q);
-              // rank of the lane's element among the word's kept ones, in bytes
-              const uint32_t below =
-                  __builtin_amdgcn_mbcnt_hi(mhi, __builtin_amdgcn_mbcnt_lo(mlo, 0u));
-              const uint32_t off =
-                  sel_by_bit(((u64)mhi << 32) | mlo, below * 4u + r4, 0x80000000u);
-              cv[kx][i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0));
-            }
-          }
-#pragma unroll
-          for (int kx = 0; kx < kW; ++kx)
-#pragma unroll
-            for (int i = 0; i < U; ++i) acc[i] += (double)cv[kx][i];  // worker order; absent: +0
-        }
-      }
+    float mean[U];
+    if (kPath == kTkAggUnion) {
+      // one batch holds every worker: the next pass's words go out first
+      const AggStep<U> nxt = agg_words<U>(sel, rank, W, gw, K, nw, w0 + stride, 0, lane);
+      union_means<U>(cur, K, inv_k, vals + voff, tk.total_keep, keep, lane,
+                     mb + wave_id() * (U * kWave), mean);
       cur = nxt;
+    } else {
+      double acc[U];
+#pragma unroll
+      for (int i = 0; i < U; ++i) acc[i] = 0.0;
+      for (int k0 = 0; k0 < K; k0 += kB) {
+        // the next step's words go out before this step's values are waited for
+        const bool last_b = k0 + kB >= K;
+        const int nw0 = last_b ? w0 + stride : w0;
+        const AggStep<U> nxt =
+            agg_words<U>(sel, rank, W, gw, K, nw, nw0, last_b ? 0 : k0 + kB, lane);
+        // This step's values, read through a buffer resource over each worker's
+        // k_l values (a read past the end gets 0 from the range check, with no
+        // memory access).
+        bool done = false;
+        if (kPath == kTkAggDense) {
+          // Dense messages: the kept values of a worker's U words are contiguous
+          // in its message; when no worker of the step has more than 64 of them,
+          // one load per worker brings them all (lane j: the group's j-th
+          // value) and each element takes its own with ds_bpermute.
+          uint32_t gcnt = (uint32_t)(__popc(cur.lo) + __popc(cur.hi));
+#pragma unroll
+          for (int off = 1; off < U; off <<= 1) gcnt += (uint32_t)__shfl_xor((int)gcnt, off);
+          if (__ballot(gcnt > (uint32_t)kWave) == 0ull) {  // wave-uniform
+            float gv[kB];
+#pragma unroll
+            for (int kk = 0; kk < kB; ++kk) {
+              const int kidx = min(k0 + kk, K - 1);  // absent workers have empty words
+              const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                  (void*)(vals + (int64_t)kidx * tk.total_keep + voff), 0, (int)(keep * 4u),
+                  kBufWord3);
+              const uint32_t g4 = __builtin_amdgcn_readlane(cur.rk4, kk * U);  // group's first rank
+              gv[kk] = __uint_as_float(
+                  __builtin_amdgcn_raw_buffer_load_b32(rs, g4 + 4u * (uint32_t)lane, 0, 0));
+            }
+#pragma unroll
+            for (int kk = 0; kk < kB; ++kk) {
+              const uint32_t g4 = __builtin_amdgcn_readlane(cur.rk4, kk * U);
+              // the U shuffles of the worker go out together (distinct
+              // registers), then their values are added
+              int pv[U];
+#pragma unroll
+              for (int i = 0; i < U; ++i) {
+                const int q = kk * U + i;
+                const uint32_t mlo = __builtin_amdgcn_readlane(cur.lo, q);
+                const uint32_t mhi = __builtin_amdgcn_readlane(cur.hi, q);
+                const uint32_t r4 = __builtin_amdgcn_readlane(cur.rk4, q);
+                // the lane's element: its position among the group's kept values
+                const uint32_t below =
+                    __builtin_amdgcn_mbcnt_hi(mhi, __builtin_amdgcn_mbcnt_lo(mlo, 0u));
+                const int src = (int)((r4 - g4) + 4u * below);  // < 4 * 64 for a kept element
+                pv[i] = __builtin_amdgcn_ds_bpermute(src, __float_as_int(gv[kk]));
+              }
+#pragma unroll
+              for (int i = 0; i < U; ++i) {
+                const int q = kk * U + i;
+                const uint32_t mlo = __builtin_amdgcn_readlane(cur.lo, q);
+                const uint32_t mhi = __builtin_amdgcn_readlane(cur.hi, q);
+                acc[i] += (double)sel_by_bit(((u64)mhi << 32) | mlo, __int_as_float(pv[i]),
+                                             0.0f);  // worker order
+              }
+            }
+            done = true;
+          }
+        }
+        if (!done) {
+          // Sparse messages (or a worker with more than 64 kept values in the
+          // step's words): every (worker, word) pair gathers its values, a lane
+          // whose bit is clear reading past the end; the loads go out before the
+          // first one is used (dense kernels: one worker at a time, which needs fewer
+          // registers next to the dense path).
+          constexpr int kW = kPath == kTkAggDense ? 1 : kB;  // workers whose loads go out together
+          for (int kw = 0; kw < kB; kw += kW) {
+            float cv[kW][U];
+#pragma unroll
+            for (int kx = 0; kx < kW; ++kx) {
+              const int kk = kw + kx;
+              const int kidx = min(k0 + kk, K - 1);  // absent workers have empty words
+              const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                  (void*)(vals + (int64_t)kidx * tk.total_keep + voff), 0, (int)(keep * 4u),
+                  kBufWord3);
+#pragma unroll
+              for (int i = 0; i < U; ++i) {
+                const int q = kk * U + i;
+                const uint32_t mlo = __builtin_amdgcn_readlane(cur.lo, q);
+                const uint32_t mhi = __builtin_amdgcn_readlane(cur.hi, q);
+                const uint32_t r4 = __builtin_amdgcn_readlane(cur.rk4, q);
+                // rank of the lane's element among the word's kept ones, in bytes
+                const uint32_t below =
+                    __builtin_amdgcn_mbcnt_hi(mhi, __builtin_amdgcn_mbcnt_lo(mlo, 0u));
+                const uint32_t off =
+                    sel_by_bit(((u64)mhi << 32) | mlo, below * 4u + r4, 0x80000000u);
+                cv[kx][i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0));
+              }
+            }
+#pragma unroll
+            for (int kx = 0; kx < kW; ++kx)
+#pragma unroll
+              for (int i = 0; i < U; ++i) acc[i] += (double)cv[kx][i];  // worker order; absent: +0
+          }
+        }
+        cur = nxt;
+      }
+#pragma unroll
+      for (int i = 0; i < U; ++i) mean[i] = (float)mean_of(acc[i], inv_k, K);
     }
 #pragma unroll
     for (int i = 0; i < U; ++i) {
       const int j = (w0 + i) * 64 + lane;
       if (!(w0 + i < nw && j < c.count)) continue;
-      const float mean = (float)mean_of(acc[i], inv_k, K);
-      if (kAvg) avg[c.start + j] = mean;
+      if (kAvg) avg[c.start + j] = mean[i];
       if (kMode == 1) {
-        const float D = dv[i] + mean;  // Delta_{t+1} = e_t + (1/K) sum_k C(Delta^(k))
+        const float D = dv[i] + mean[i];  // Delta_{t+1} = e_t + (1/K) sum_k C(Delta^(k))
         st_nt(dr + j, D);
         const uint32_t key = key_of(D);
         bad |= key >= kFiniteLimit;
         // a pass stays in one tile
         atomicAdd(&h[(w0 / kTileWords) * kTkHistPad + hist_bin(key, win)], 1u);
       } else {
-        st_nt(dr + j, dv[i] - mean);  // single-way: the mean itself comes back
+        st_nt(dr + j, dv[i] - mean[i]);  // single-way: the mean itself comes back
       }
     }
   }
@@ -1265,22 +1362,28 @@ struct Launcher {
     const double ik = inv_pow2(K);
     hipEvent_t stop0 = mode == 1 ? nullptr : ev.stop;
     // dense messages (at least 1/32 of the elements kept): one load per worker
-    // and step, values handed out with ds_bpermute; sparser ones: per-pair
-    // gathers (faster there: at 1% kept 117 against 153 us at resnet50, K = 8;
-    // at 5% and 10%, 281 and 316 us against 265 and 290 us for the server step)
+    // and step, values handed out with ds_bpermute; sparser ones: gathers over
+    // the union of the workers' kept elements when one batch holds every
+    // worker (K <= 16), else per-pair gathers.  At resnet50 K = 8 the union
+    // took the Top-1% iteration from 1.000 to 0.984 ms (its end, pipelined:
+    // 710 -> 680 us); for dense messages it lost to the one-load-per-worker
+    // path (Top-5% 1.12 against 1.11 ms, Top-10% 1.29 against 1.25 ms).
     const bool co = tk.total_keep * 32 >= lay.d_pad;
 #define SAEF_TKA(M, A, U, C)                                                                 \
   hipExtLaunchKernelGGL((k_tk_aggregate<M, A, U, C>), grid, dim3(kBig), 0, s, ev.start, stop0, \
                         0, lay, tk, p, K, ik, sel, rank, vals, avg, e_srv, x)
-#define SAEF_TKA_U(M, A)                                 \
-  do {                                                   \
-    if (K <= 8) {                                        \
-      if (co) SAEF_TKA(M, A, 8, true);                   \
-      else SAEF_TKA(M, A, 8, false);                     \
-    } else {                                             \
-      if (co) SAEF_TKA(M, A, 4, true);                   \
-      else SAEF_TKA(M, A, 4, false);                     \
-    }                                                    \
+#define SAEF_TKA_U(M, A)                                                    \
+  do {                                                                      \
+    if (K <= 8) {                                                           \
+      if (co) SAEF_TKA(M, A, 8, kTkAggDense);                               \
+      else SAEF_TKA(M, A, 8, kTkAggUnion);                                  \
+    } else if (K <= 16) {                                                   \
+      if (co) SAEF_TKA(M, A, 4, kTkAggDense);                               \
+      else SAEF_TKA(M, A, 4, kTkAggUnion);                                  \
+    } else {                                                                \
+      if (co) SAEF_TKA(M, A, 4, kTkAggDense);                               \
+      else SAEF_TKA(M, A, 4, kTkAggPairs);                                  \
+    }                                                                       \
   } while (0)
     if (mode == 1) {
       if (avg != nullptr) SAEF_TKA_U(1, true); else SAEF_TKA_U(1, false);

@@ -252,16 +252,22 @@ def test_topk_compress_parity(name, momentum):
     assert gs.status() == 0
 
 
+@pytest.mark.parametrize("pct", [1, 3, 5])
 @pytest.mark.parametrize("K", [3, 5, 12, 17])
 @pytest.mark.parametrize("mode", [1, 0], ids=["dc", "sc"])
-def test_topk_aggregate_parity(mode, K):
+def test_topk_aggregate_parity(mode, K, pct):
     """Server step on oracle-made messages.  The server kernel reads the
     workers in batches of 8 (K <= 8) or 16: K = 3 and 12 leave part of a batch
-    empty, K = 17 takes two batches; /K is not a power of two for 3, 5, 12, 17."""
+    empty, K = 17 takes two batches; /K is not a power of two for 3, 5, 12, 17.
+    Below 1/32 kept (1% and 3%) it gathers over the union of the workers' kept
+    elements when one batch holds every worker (K <= 16; at 3%, K = 5 or 12,
+    a pass holds more than 64 union elements) and per (worker, word) pair at
+    K = 17; at 5% it takes one load per worker and batch."""
     w = W.custom(ADVERSARIAL + [200_000], K=K, scale_range=(1e-3, 1.0), seed=321, mode=mode)
-    keep = W.topk_keep(w, 5)
-    _case(f"topk aggregate mode={mode} K={K}")
+    keep = W.topk_keep(w, pct)
+    _case(f"topk aggregate mode={mode} K={K} pct={pct}")
     off, n, d_pad = w.layout()
+    assert (int(keep.sum()) * 32 >= d_pad) == (pct == 5)  # which gather the server takes
     msk = W.tensor_mask(w)
     orc = TopkOracle(w, keep)
     g = W.gradients(w, 0)
