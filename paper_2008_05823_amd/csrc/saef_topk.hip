@@ -990,26 +990,40 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, TkP
 // costs one memory round trip.  The K values of an element are added in
 // binary64 in worker order (/K, fp32); mode 1: Delta = e_srv + mean stored into
 // e_srv and its pass-1 histogram; mode 0: x <- x - mean.
-template <int U>
+// A lane's (worker, word) pair: selection word, 4 x rank word (0 for a pair
+// that does not exist).
+struct AggWords {
+  uint32_t lo, hi, rk4;
+};
+// The pair as loaded, with whether it exists: the words are cleared where
+// they are used, in the next step (selects right after the loads made the
+// compiler branch around them and wait for them, and so for every load
+// issued before them, at once).
 struct AggStep {
-  uint32_t lo, hi, rk4;  // this lane's (worker, word) pair: selection word, 4 x rank word
+  u64 s;
+  uint32_t r;
+  bool ok;
+  __device__ __forceinline__ AggWords words() const {
+    AggWords a;
+    a.lo = ok ? (uint32_t)s : 0u;
+    a.hi = ok ? (uint32_t)(s >> 32) : 0u;
+    a.rk4 = ok ? r * 4u : 0u;
+    return a;
+  }
 };
 
 template <int U>
-__device__ __forceinline__ AggStep<U> agg_words(const uint64_t* __restrict__ sel,
-                                                const uint32_t* __restrict__ rank, int64_t W,
-                                                int64_t gw, int K, int nw, int w0, int k0,
-                                                int lane) {
+__device__ __forceinline__ AggStep agg_words(const uint64_t* __restrict__ sel,
+                                             const uint32_t* __restrict__ rank, int64_t W,
+                                             int64_t gw, int K, int nw, int w0, int k0,
+                                             int lane) {
   const int kq = k0 + lane / U, uq = lane % U;
-  const bool ok = kq < K && w0 + uq < nw;
+  AggStep a;
+  a.ok = kq < K && w0 + uq < nw;
   // always issued at a word that exists (the chunk's first word of worker 0)
-  const int64_t at = ok ? (int64_t)kq * W + gw + w0 + uq : gw;
-  const u64 s = sel[at];
-  const uint32_t r = rank[at];
-  AggStep<U> a;
-  a.lo = ok ? (uint32_t)s : 0u;
-  a.hi = ok ? (uint32_t)(s >> 32) : 0u;
-  a.rk4 = ok ? r * 4u : 0u;
+  const int64_t at = a.ok ? (int64_t)kq * W + gw + w0 + uq : gw;
+  a.s = sel[at];
+  a.r = rank[at];
   return a;
 }
 
@@ -1030,7 +1044,7 @@ constexpr int kTkAggUnion = 2;
 // means are the same bits.  mb (U x 64 floats, the wave's own) returns them
 // per element; an element no worker kept has mean +0.
 template <int U>
-__device__ __forceinline__ void union_means(const AggStep<U>& cur, int K, double inv_k,
+__device__ __forceinline__ void union_means(const AggWords& cur, int K, double inv_k,
                                             const float* __restrict__ vals, int64_t total_keep,
                                             uint32_t keep, int lane, float* __restrict__ mb,
                                             float (&mean)[U]) {
@@ -1125,26 +1139,31 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
   const int nw = (c.count + 63) >> 6;
   const int64_t W = lay.d_pad >> 6;
   const int64_t gw = c.start >> 6;
-  float* dr = (kMode == 1 ? es : x) + c.start;
+  // e_srv (mode 1) or x (mode 0), and the mean, over the chunk's elements:
+  // past the chunk a load returns 0 and a store is dropped, so the pass has
+  // no per-element branch (a store in one would make the loop wait for every
+  // store before the next pass)
+  const uint32_t nbytes = (uint32_t)c.count * 4u;
+  const Buf rd = buf_of((kMode == 1 ? es : x) + c.start, nbytes);
+  const Buf ra = buf_of(kAvg ? avg + c.start : es, kAvg ? nbytes : 0u);
   const int stride = (kBig / kWave) * U;
   bool bad = false;
   // (past the chunk's last word, agg_words issues a load at a word that
   // exists and returns empty words: no branch, so no early wait)
-  AggStep<U> cur = agg_words<U>(sel, rank, W, gw, K, nw, wave_id() * U, 0, lane);
+  AggStep cur = agg_words<U>(sel, rank, W, gw, K, nw, wave_id() * U, 0, lane);
+  // wait for the first words here, once: the loop header then knows them
+  // loaded on both of its entries and does not wait at every pass for the
+  // stores of the one before
+  asm volatile("" ::"v"(cur.s), "v"(cur.r));
   for (int w0 = wave_id() * U; w0 < nw; w0 += stride) {
-    // e_srv (mode 1) or x (mode 0) of the pass; elements past the chunk are
-    // loaded at its first element and never stored
     float dv[U];
 #pragma unroll
-    for (int i = 0; i < U; ++i) {
-      const int j = (w0 + i) * 64 + lane;
-      dv[i] = __builtin_nontemporal_load(dr + ((w0 + i < nw && j < c.count) ? j : 0));
-    }
+    for (int i = 0; i < U; ++i) dv[i] = buf_ld(rd, (uint32_t)((w0 + i) * 64 + lane) * 4u);
     float mean[U];
     if (kPath == kTkAggUnion) {
       // one batch holds every worker: the next pass's words go out first
-      const AggStep<U> nxt = agg_words<U>(sel, rank, W, gw, K, nw, w0 + stride, 0, lane);
-      union_means<U>(cur, K, inv_k, vals + voff, tk.total_keep, keep, lane,
+      const AggStep nxt = agg_words<U>(sel, rank, W, gw, K, nw, w0 + stride, 0, lane);
+      union_means<U>(cur.words(), K, inv_k, vals + voff, tk.total_keep, keep, lane,
                      mb + wave_id() * (U * kWave), mean);
       cur = nxt;
     } else {
@@ -1155,8 +1174,9 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
         // the next step's words go out before this step's values are waited for
         const bool last_b = k0 + kB >= K;
         const int nw0 = last_b ? w0 + stride : w0;
-        const AggStep<U> nxt =
+        const AggStep nxt =
             agg_words<U>(sel, rank, W, gw, K, nw, nw0, last_b ? 0 : k0 + kB, lane);
+        const AggWords cw = cur.words();
         // This step's values, read through a buffer resource over each worker's
         // k_l values (a read past the end gets 0 from the range check, with no
         // memory access).
@@ -1166,7 +1186,7 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
           // in its message; when no worker of the step has more than 64 of them,
           // one load per worker brings them all (lane j: the group's j-th
           // value) and each element takes its own with ds_bpermute.
-          uint32_t gcnt = (uint32_t)(__popc(cur.lo) + __popc(cur.hi));
+          uint32_t gcnt = (uint32_t)(__popc(cw.lo) + __popc(cw.hi));
 #pragma unroll
           for (int off = 1; off < U; off <<= 1) gcnt += (uint32_t)__shfl_xor((int)gcnt, off);
           if (__ballot(gcnt > (uint32_t)kWave) == 0ull) {  // wave-uniform
@@ -1177,22 +1197,22 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
               const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
                   (void*)(vals + (int64_t)kidx * tk.total_keep + voff), 0, (int)(keep * 4u),
                   kBufWord3);
-              const uint32_t g4 = __builtin_amdgcn_readlane(cur.rk4, kk * U);  // group's first rank
+              const uint32_t g4 = __builtin_amdgcn_readlane(cw.rk4, kk * U);  // group's first rank
               gv[kk] = __uint_as_float(
                   __builtin_amdgcn_raw_buffer_load_b32(rs, g4 + 4u * (uint32_t)lane, 0, 0));
             }
 #pragma unroll
             for (int kk = 0; kk < kB; ++kk) {
-              const uint32_t g4 = __builtin_amdgcn_readlane(cur.rk4, kk * U);
+              const uint32_t g4 = __builtin_amdgcn_readlane(cw.rk4, kk * U);
               // the U shuffles of the worker go out together (distinct
               // registers), then their values are added
               int pv[U];
 #pragma unroll
               for (int i = 0; i < U; ++i) {
                 const int q = kk * U + i;
-                const uint32_t mlo = __builtin_amdgcn_readlane(cur.lo, q);
-                const uint32_t mhi = __builtin_amdgcn_readlane(cur.hi, q);
-                const uint32_t r4 = __builtin_amdgcn_readlane(cur.rk4, q);
+                const uint32_t mlo = __builtin_amdgcn_readlane(cw.lo, q);
+                const uint32_t mhi = __builtin_amdgcn_readlane(cw.hi, q);
+                const uint32_t r4 = __builtin_amdgcn_readlane(cw.rk4, q);
                 // the lane's element: its position among the group's kept values
                 const uint32_t below =
                     __builtin_amdgcn_mbcnt_hi(mhi, __builtin_amdgcn_mbcnt_lo(mlo, 0u));
@@ -1202,8 +1222,8 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
 #pragma unroll
               for (int i = 0; i < U; ++i) {
                 const int q = kk * U + i;
-                const uint32_t mlo = __builtin_amdgcn_readlane(cur.lo, q);
-                const uint32_t mhi = __builtin_amdgcn_readlane(cur.hi, q);
+                const uint32_t mlo = __builtin_amdgcn_readlane(cw.lo, q);
+                const uint32_t mhi = __builtin_amdgcn_readlane(cw.hi, q);
                 acc[i] += (double)sel_by_bit(((u64)mhi << 32) | mlo, __int_as_float(pv[i]),
                                              0.0f);  // worker order
               }
@@ -1230,9 +1250,9 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
 #pragma unroll
               for (int i = 0; i < U; ++i) {
                 const int q = kk * U + i;
-                const uint32_t mlo = __builtin_amdgcn_readlane(cur.lo, q);
-                const uint32_t mhi = __builtin_amdgcn_readlane(cur.hi, q);
-                const uint32_t r4 = __builtin_amdgcn_readlane(cur.rk4, q);
+                const uint32_t mlo = __builtin_amdgcn_readlane(cw.lo, q);
+                const uint32_t mhi = __builtin_amdgcn_readlane(cw.hi, q);
+                const uint32_t r4 = __builtin_amdgcn_readlane(cw.rk4, q);
                 // rank of the lane's element among the word's kept ones, in bytes
                 const uint32_t below =
                     __builtin_amdgcn_mbcnt_hi(mhi, __builtin_amdgcn_mbcnt_lo(mlo, 0u));
@@ -1255,17 +1275,18 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
 #pragma unroll
     for (int i = 0; i < U; ++i) {
       const int j = (w0 + i) * 64 + lane;
-      if (!(w0 + i < nw && j < c.count)) continue;
-      if (kAvg) avg[c.start + j] = mean[i];
+      const bool ok = j < c.count;
+      const uint32_t off = (uint32_t)j * 4u;
+      if (kAvg) buf_st(ra, off, mean[i]);
       if (kMode == 1) {
         const float D = dv[i] + mean[i];  // Delta_{t+1} = e_t + (1/K) sum_k C(Delta^(k))
-        st_nt(dr + j, D);
+        buf_st(rd, off, D);
         const uint32_t key = key_of(D);
-        bad |= key >= kFiniteLimit;
-        // a pass stays in one tile
-        atomicAdd(&h[(w0 / kTileWords) * kTkHistPad + hist_bin(key, win)], 1u);
+        bad |= ok && key >= kFiniteLimit;
+        // a pass stays in one tile; a lane past the chunk adds 0
+        atomicAdd(&h[(w0 / kTileWords) * kTkHistPad + hist_bin(key, win)], ok ? 1u : 0u);
       } else {
-        st_nt(dr + j, dv[i] - mean[i]);  // single-way: the mean itself comes back
+        buf_st(rd, off, dv[i] - mean[i]);  // single-way: the mean itself comes back
       }
     }
   }
