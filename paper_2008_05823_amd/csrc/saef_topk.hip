@@ -1042,15 +1042,22 @@ constexpr int kTkAggUnion = 2;
 // one per (worker, word) pair.  The sum runs over all kWave / U workers in
 // order in binary64 (absent ones add +0), as in the per-pair gathers, so the
 // means are the same bits.  mb (U x 64 floats, the wave's own) returns them
-// per element; an element no worker kept has mean +0.
+// per element; an element no worker kept has mean +0.  The wave's pairs go
+// to wt (64 entries of 16 bytes) and its union words to ut (U entries): a
+// lane reads the entry it needs with one LDS load (lanes of one word read
+// one address, and the U entries of a worker are one 16 U-byte span, so the
+// loads have no bank conflicts), which keeps the pass off the LDS issue
+// limit that one ds_bpermute per word and worker ran into.
 template <int U>
 __device__ __forceinline__ void union_means(const AggWords& cur, int K, double inv_k,
                                             const float* __restrict__ vals, int64_t total_keep,
                                             uint32_t keep, int lane, float* __restrict__ mb,
+                                            uint4* __restrict__ wt, uint4* __restrict__ ut,
                                             float (&mean)[U]) {
   constexpr int kB = kWave / U;
 #pragma unroll
   for (int i = 0; i < U; ++i) mb[i * kWave + lane] = 0.0f;
+  wt[lane] = make_uint4(cur.lo, cur.hi, cur.rk4, 0u);
   // the union of word q % U in every lane q (absent workers hold empty words)
   uint32_t ulo = cur.lo, uhi = cur.hi;
 #pragma unroll
@@ -1067,20 +1074,22 @@ __device__ __forceinline__ void union_means(const AggWords& cur, int K, double i
     const uint32_t y = (uint32_t)__shfl_up((int)incl, off);
     if ((lane % U) >= off) incl += y;
   }
-  const uint32_t excl = incl - cnt;
-  const uint32_t total = (uint32_t)__shfl((int)incl, U - 1);  // union elements of the pass
+  if (lane < U) ut[lane] = make_uint4(ulo, uhi, incl - cnt, 0u);
+  // the inclusive counts of words 0 .. U - 2, and the pass's union size
+  uint32_t inc_s[U - 1];
+#pragma unroll
+  for (int w = 0; w < U - 1; ++w) inc_s[w] = (uint32_t)__builtin_amdgcn_readlane((int)incl, w);
+  const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, U - 1);
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   for (uint32_t i0 = 0; i0 < total; i0 += kWave) {
     const uint32_t i = i0 + (uint32_t)lane;  // the i-th union element of the pass
-    // its word: the number of words whose inclusive count is <= i (capped at
-    // U - 1 for lanes past the end, which load and store nothing)
+    // its word: the number of words whose inclusive count is <= i (at most
+    // U - 1, for lanes past the end, which load and store nothing)
     int u = 0;
 #pragma unroll
-    for (int step = U / 2; step >= 1; step >>= 1)
-      if ((uint32_t)__shfl((int)incl, u + step - 1) <= i) u += step;
-    const uint32_t wlo = (uint32_t)__shfl((int)ulo, u), whi = (uint32_t)__shfl((int)uhi, u);
-    const uint32_t wex = (uint32_t)__shfl((int)excl, u);
-    const int b = nth_set_bit(((u64)whi << 32) | wlo, i - wex);
+    for (int w = 0; w < U - 1; ++w) u += inc_s[w] <= i ? 1 : 0;
+    const uint4 uw = ut[u];  // union word, union elements before it
+    const int b = nth_set_bit(((u64)uw.y << 32) | uw.x, i - uw.z);
     const bool live = i < total;
     const u64 below_mask = (1ull << b) - 1ull;
     float v[kB];
@@ -1089,13 +1098,10 @@ __device__ __forceinline__ void union_means(const AggWords& cur, int K, double i
       const int kidx = min(kk, K - 1);  // absent workers have empty words
       const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
           (void*)(vals + (int64_t)kidx * total_keep), 0, (int)(keep * 4u), kBufWord3);
-      const int q = kk * U + u;
-      const uint32_t lo = (uint32_t)__shfl((int)cur.lo, q);
-      const uint32_t hi = (uint32_t)__shfl((int)cur.hi, q);
-      const uint32_t r4 = (uint32_t)__shfl((int)cur.rk4, q);
-      const u64 w = ((u64)hi << 32) | lo;
+      const uint4 pw = wt[kk * U + u];  // worker kk's selection word, 4 x rank word
+      const u64 w = ((u64)pw.y << 32) | pw.x;
       const bool bit = live && ((w >> b) & 1ull) != 0ull;
-      const uint32_t off = bit ? r4 + 4u * (uint32_t)__popcll(w & below_mask) : 0x80000000u;
+      const uint32_t off = bit ? pw.z + 4u * (uint32_t)__popcll(w & below_mask) : 0x80000000u;
       v[kk] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0));
     }
     double acc = 0.0;
@@ -1124,6 +1130,8 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
   constexpr int kChunkTiles = kTkChunk / kTkTileElems;
   __shared__ uint32_t h[kMode == 1 ? kChunkTiles * kTkHistPad : 1];  // per tile of the chunk
   __shared__ float mb[kPath == kTkAggUnion ? (kBig / kWave) * U * kWave : 1];  // a pass's means
+  __shared__ uint4 wt[kPath == kTkAggUnion ? kBig : 1];                 // per wave: its 64 pairs
+  __shared__ uint4 ut[kPath == kTkAggUnion ? (kBig / kWave) * U : 1];   // per wave: union words
   static_assert(kPath != kTkAggUnion || U * kWave <= (int)(sizeof(mb) / sizeof(float)),
                 "a wave's means");
   const int64_t ci = p.c0 + (int64_t)blockIdx.x;
@@ -1163,8 +1171,9 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
     if (kPath == kTkAggUnion) {
       // one batch holds every worker: the next pass's words go out first
       const AggStep nxt = agg_words<U>(sel, rank, W, gw, K, nw, w0 + stride, 0, lane);
+      const int wv = wave_id();
       union_means<U>(cur.words(), K, inv_k, vals + voff, tk.total_keep, keep, lane,
-                     mb + wave_id() * (U * kWave), mean);
+                     mb + wv * (U * kWave), wt + wv * kWave, ut + wv * U, mean);
       cur = nxt;
     } else {
       double acc[U];
