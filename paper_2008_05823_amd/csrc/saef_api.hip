@@ -776,9 +776,9 @@ int saef_topk_create(const saef_layout* layout, const int64_t* keep, saef_topk**
   // candidate slots: at most every element of a tensor (8 B each) per row
   const size_t cand_bytes = rows * (size_t)layout->d_pad * sizeof(unsigned long long);
   const size_t cand_off_bytes = rows * n_tiles * sizeof(uint32_t);
-  // speculative candidate lists of the worker rows
+  // speculative candidate lists of the worker rows and the server row
   const size_t spec_bytes =
-      (size_t)layout->k_max * n_tiles * saef::kTkSpecCap * sizeof(unsigned long long);
+      (size_t)(layout->k_max + 1) * n_tiles * saef::kTkSpecCap * sizeof(unsigned long long);
   hipError_t err = hipMalloc(&p->mem_chunks, chunks.size() * sizeof(saef::TkChunk));
   if (err == hipSuccess) err = hipMalloc(&p->mem_tens, tens.size() * sizeof(saef::TkTensor));
   if (err == hipSuccess) err = hipMalloc(&p->mem_groups, groups.size() * sizeof(saef::TkGroup));

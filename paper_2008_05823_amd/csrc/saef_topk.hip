@@ -805,13 +805,13 @@ __device__ __forceinline__ int nth_set_bit(u64 w, uint32_t r) {
 // its value (from the entry) goes to the message at the tile's first rank
 // plus the kept entries before it, the error there is set to 0, and the
 // selection words (assembled in LDS) and rank words are written.
-template <int kNC, bool kPend>
+template <int kNC, bool kX, bool kPend>
 __device__ __forceinline__ void emit_list(const u64* __restrict__ ent, uint32_t n,
                                           const TkSel* stp, int64_t rel0, uint32_t base,
                                           uint32_t keep, int count, int nw,
                                           uint64_t* __restrict__ sr, uint32_t* __restrict__ rr,
                                           float* __restrict__ vr, float* __restrict__ dr,
-                                          u64* s_w) {
+                                          float* __restrict__ xt, u64* s_w) {
   const int lane = lane_id();
   u64 e[kNC > 0 ? kNC : 1];
 #pragma unroll
@@ -839,6 +839,7 @@ __device__ __forceinline__ void emit_list(const u64* __restrict__ ent, uint32_t 
       if (pos < keep && idx < (uint32_t)count) {  // both always hold
         vr[pos] = __uint_as_float(raw);
         if (!kPend) st_nt(dr + idx, 0.0f);  // e = Delta - C(Delta) = 0 at a kept element
+        if (kX) xt[idx] -= __uint_as_float(raw);
       }
     }
     run += (uint32_t)__popcll(km);
@@ -886,12 +887,11 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, TkP
   // count and flag of the tile's speculative list (read before the tile so
   // that the two loads overlap)
   const uint32_t sp =
-      !kX && spec ? *reinterpret_cast<const uint32_t*>(tile_hist(tk, lay, row, ti) + kTkSpecSlot)
-                  : 0u;
+      spec ? *reinterpret_cast<const uint32_t*>(tile_hist(tk, lay, row, ti) + kTkSpecSlot) : 0u;
   const Tile tile = lay.tiles[ti];
   const int nw = (tile.count + 63) >> 6;
   uint64_t* sr = sel + (int64_t)r * W + (tile.start >> 6);
-  if (!kX) {
+  {
     // a tile the gather took from its speculative list: emit it from the list
     if ((sp >> 16) != 0u) {
       static_assert(kTkSpecSlot % 2 == 0, "count and flag in one 32-bit word");
@@ -905,8 +905,10 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, TkP
       float* vr = vals + (int64_t)r * tk.total_keep + tp->voff;
       float* dr = data + (int64_t)r * lay.d_pad + tile.start;
       const uint32_t keep = (uint32_t)tp->keep;
-#define SAEF_EL(NC)                                                                       \
-  emit_list<NC, kPend>(ent, n, stp, rel0, base, keep, tile.count, nw, sr, rr, vr, dr, words[wave])
+      float* xt = kX ? x + tile.start : nullptr;
+#define SAEF_EL(NC)                                                                   \
+  emit_list<NC, kX, kPend>(ent, n, stp, rel0, base, keep, tile.count, nw, sr, rr, vr, dr, xt, \
+                           words[wave])
       switch ((n + kWave - 1) / kWave) {
         case 0: SAEF_EL(0); break;
         case 1: SAEF_EL(1); break;
@@ -1157,7 +1159,13 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
   const TkChunk c = tk.chunks[ci];
   const int64_t voff = tk.tens[c.l].voff;
   const uint32_t keep = (uint32_t)tk.tens[c.l].keep;
-  const uint32_t win = kMode == 1 ? tk.sel[(int64_t)lay.k_max * lay.L + c.l].win : 0u;
+  const TkSel* sst = tk.sel + (int64_t)lay.k_max * lay.L + c.l;  // the server row's state
+  const uint32_t win = kMode == 1 ? sst->win : 0u;
+  // the server row's speculative lists, as the worker Delta pass writes them:
+  // per tile, the elements whose key is at least spec_floor, in index order
+  const uint32_t lo_spec = kMode == 1 ? spec_floor(*sst) : 0x80000000u;
+  const TensorInfo ten = lay.tensors[c.l];
+  const int64_t tile0 = ten.first_tile + (c.start - ten.off) / kTkTileElems;
   if (kMode == 1) {
     for (int i = threadIdx.x; i < kChunkTiles * kTkHistPad; i += kBig) h[i] = 0;
     __syncthreads();
@@ -1173,23 +1181,30 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
   const uint32_t nbytes = (uint32_t)c.count * 4u;
   const Buf rd = buf_of((kMode == 1 ? es : x) + c.start, nbytes);
   const Buf ra = buf_of(kAvg ? avg + c.start : es, kAvg ? nbytes : 0u);
-  const int stride = (kBig / kWave) * U;
+  // Wave w takes the chunk's tiles w, w + kBW, ... one at a time, U words per
+  // pass in word order, so that a tile's passes, and its list, are one
+  // wave's.
+  constexpr int kBW = kBig / kWave;
+  const auto next_w0 = [](int w) {
+    return (w + U) % kTileWords != 0 ? w + U : w + U + (kBW - 1) * kTileWords;
+  };
   bool bad = false;
+  uint32_t lc = 0;  // list entries of the wave's tile so far
   // (past the chunk's last word, agg_words issues a load at a word that
   // exists and returns empty words: no branch, so no early wait)
-  AggStep cur = agg_words<U>(sel, rank, W, gw, K, nw, wave_id() * U, 0, lane);
+  AggStep cur = agg_words<U>(sel, rank, W, gw, K, nw, wave_id() * kTileWords, 0, lane);
   // wait for the first words here, once: the loop header then knows them
   // loaded on both of its entries and does not wait at every pass for the
   // stores of the one before
   asm volatile("" ::"v"(cur.s), "v"(cur.r));
-  for (int w0 = wave_id() * U; w0 < nw; w0 += stride) {
+  for (int w0 = wave_id() * kTileWords; w0 < nw; w0 = next_w0(w0)) {
     float dv[U];
 #pragma unroll
     for (int i = 0; i < U; ++i) dv[i] = buf_ld(rd, (uint32_t)((w0 + i) * 64 + lane) * 4u);
     float mean[U];
     if (kPath == kTkAggUnion) {
       // one batch holds every worker: the next pass's words go out first
-      const AggStep nxt = agg_words<U>(sel, rank, W, gw, K, nw, w0 + stride, 0, lane);
+      const AggStep nxt = agg_words<U>(sel, rank, W, gw, K, nw, next_w0(w0), 0, lane);
       const int wv = wave_id();
       union_means<U>(cur.words(), K, inv_k, vals + voff, tk.total_keep, keep, lane,
                      mb + wv * (U * kWave), wt + wv * kWave, ut + wv * U, mean);
@@ -1201,7 +1216,7 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
       for (int k0 = 0; k0 < K; k0 += kB) {
         // the next step's words go out before this step's values are waited for
         const bool last_b = k0 + kB >= K;
-        const int nw0 = last_b ? w0 + stride : w0;
+        const int nw0 = last_b ? next_w0(w0) : w0;
         const AggStep nxt =
             agg_words<U>(sel, rank, W, gw, K, nw, nw0, last_b ? 0 : k0 + kB, lane);
         const AggWords cw = cur.words();
@@ -1300,6 +1315,10 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
 #pragma unroll
       for (int i = 0; i < U; ++i) mean[i] = (float)mean_of(acc[i], inv_k, K);
     }
+    // the tile's list (kTkSpecCap entries; a store past it is dropped)
+    const int tl = w0 / kTileWords;  // tile of the chunk
+    const Buf rl = buf_of(tk.spec + ((int64_t)lay.k_max * lay.n_tiles + tile0 + tl) * kTkSpecCap,
+                          kMode == 1 ? (uint32_t)kTkSpecCap * 8u : 0u);
 #pragma unroll
     for (int i = 0; i < U; ++i) {
       const int j = (w0 + i) * 64 + lane;
@@ -1311,6 +1330,17 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
         buf_st(rd, off, D);
         const uint32_t key = key_of(D);
         bad |= ok && key >= kFiniteLimit;
+        // list entry: Delta's bits | index in the tile << 32
+        const u64 lm = __ballot(ok && key >= lo_spec);
+        const uint32_t pos = lc + __builtin_amdgcn_mbcnt_hi((uint32_t)(lm >> 32),
+                                                            __builtin_amdgcn_mbcnt_lo((uint32_t)lm, 0u));
+        u32x2 ev;
+        ev.x = __float_as_uint(D);
+        ev.y = (uint32_t)(j - tl * kTkTileElems);
+        __builtin_amdgcn_raw_buffer_store_b64(
+            ev, rl, ((lm >> lane) & 1ull) && pos < (uint32_t)kTkSpecCap ? pos * 8u : 0x80000000u,
+            0, 0);
+        lc += (uint32_t)__popcll(lm);
         // a pass stays in one tile; a lane past the chunk adds nothing
         const uint32_t hb = (uint32_t)(w0 / kTileWords) * kTkHistPad + hist_bin(key, win);
         // (the dense gathers lost with the leader: Top-5% 1.122-1.125 against
@@ -1323,13 +1353,20 @@ __global__ __launch_bounds__(kBig) void k_tk_aggregate(DevLayout lay, TkDev tk, 
         buf_st(rd, off, dv[i] - mean[i]);  // single-way: the mean itself comes back
       }
     }
+    if (kMode == 1 && ((w0 + U) % kTileWords == 0 || w0 + U >= nw)) {
+      // the tile's last pass: its list count (none before the first
+      // threshold, for a tensor without lists, or past kTkSpecCap entries)
+      if (lane == 0)
+        h[tl * kTkHistPad + kTkSpecSlot] =
+            lo_spec != 0x80000000u && lc <= (uint32_t)kTkSpecCap ? lc : kTkSpecNone;
+      lc = 0;
+    }
   }
   if (kMode == 1) {
     if (__ballot(bad) != 0 && lane_id() == 0) atomicOr(lay.status, kStatusRange);
     __syncthreads();
     // the tile histograms of the chunk, 16-bit counts, two bins per store
-    const TensorInfo ten = lay.tensors[c.l];
-    const int64_t tile0 = ten.first_tile + (c.start - ten.off) / kTkTileElems;
+    // (the list count in slot kTkSpecSlot, 0 in the flag slot after it)
     const int ntile = (c.count + kTkTileElems - 1) / kTkTileElems;
     uint32_t* out = reinterpret_cast<uint32_t*>(tile_hist(tk, lay, lay.k_max, tile0));
     for (int i = threadIdx.x; i < ntile * (kTkHistPad / 2); i += kBig)
@@ -1384,9 +1421,9 @@ struct Launcher {
     if ((err = hipGetLastError()) != hipSuccess) return err;
     SAEF_LAUNCH(k_tk_offsets, groups, dim3(kWave), 0, s, lay, tk, p, row0);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    // speculative lists exist for the worker rows only (the server's Delta
-    // comes from the aggregation kernel), and only if some tensor keeps them
-    const int spec = row0 + R <= lay.k_max && tk.lists != 0 ? 1 : 0;
+    // speculative lists (written by the worker Delta pass, and for the
+    // server row by the aggregation), if some tensor keeps them
+    const int spec = tk.lists != 0 ? 1 : 0;
     if (spec)
       SAEF_LAUNCH(k_tk_gather_spec, tiles, dim3(kBlock), 0, s, lay, tk, p, R, row0, data, sel);
     else
@@ -1396,7 +1433,7 @@ struct Launcher {
     if ((err = hipGetLastError()) != hipSuccess) return err;
     if (x != nullptr)
       hipExtLaunchKernelGGL((k_tk_emit<true, false>), tiles, dim3(kBlock), 0, s, nullptr,
-                            last.stop, 0, lay, tk, p, R, row0, 0, data, sel, rank, vals, x);
+                            last.stop, 0, lay, tk, p, R, row0, spec, data, sel, rank, vals, x);
     else if (pend_out)
       hipExtLaunchKernelGGL((k_tk_emit<false, true>), tiles, dim3(kBlock), 0, s, nullptr,
                             last.stop, 0, lay, tk, p, R, row0, spec, data, sel, rank, vals, x);
