@@ -229,8 +229,8 @@ typedef struct saef_topk saef_topk;
  * the plan owns the selection scratch (tile histograms and their sums,
  * selection state, candidate slots, tile counts: about 8.3 bytes per
  * element of d_pad for each of the k_max + 1 rows; lists of candidate
- * elements for the worker Delta pass: 2 bytes per element of d_pad for each
- * of the k_max worker rows).  The selection state
+ * elements, written by the worker Delta pass and the server aggregation: 2
+ * bytes per element of d_pad for each of the k_max + 1 rows).  The selection state
  * keeps, per worker row and tensor, where the last call found its threshold:
  * the next call's histogram is placed there, so the first call on a plan (or
  * one after the data scale rose by more than about two binades, or fell by
