@@ -983,15 +983,18 @@ __global__ __launch_bounds__(kBlock) void k_tk_emit(DevLayout lay, TkDev tk, TkP
 }
 
 // ------------------------------------------------------------------ server aggregation
-// A wave takes U selection words (U x 64 elements) of a chunk per pass and
-// the workers in batches of kWave / U: in a batch, lane q loads selection word
-// q % U of worker q / U together with its rank word (one vector load each),
-// and the value gathers of the whole batch are issued at once, their masks and
-// ranks read out of those lanes (v_readlane).  The words of the next step are
-// loaded before the values of the current one are waited for, so one step
-// costs one memory round trip.  The K values of an element are added in
-// binary64 in worker order (/K, fp32); mode 1: Delta = e_srv + mean stored into
-// e_srv and its pass-1 histogram; mode 0: x <- x - mean.
+// A wave takes whole tiles of a chunk, U selection words (U x 64 elements)
+// per pass in word order, and the workers in batches of kWave / U: in a
+// batch, lane q loads selection word q % U of worker q / U together with its
+// rank word (one vector load each).  The values are gathered per pair (their
+// masks and ranks read out of those lanes with v_readlane), per worker for
+// dense messages, or over the union of the workers' kept elements (below).
+// The words of the next step are loaded before the values of the current one
+// are waited for, so one step costs one memory round trip.  The K values of
+// an element are added in binary64 in worker order (/K, fp32); mode 1: Delta
+// = e_srv + mean stored into e_srv, its pass-1 histogram and the server row's
+// speculative lists; mode 0: x <- x - mean.
+
 // A lane's (worker, word) pair: selection word, 4 x rank word (0 for a pair
 // that does not exist).
 struct AggWords {
